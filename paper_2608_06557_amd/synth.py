@@ -1,0 +1,302 @@
+"""Seeded synthetic request populations for the scheduling step.
+
+This module only draws inputs: request fields, block tables, free lists,
+parameters and KV payload bit patterns.  It holds none of the scheduling
+method's arithmetic (no latency model, budget, order or admission), so
+both the GPU library and the CPU oracle can be fed from it.
+
+The Aliyun Bailian production traces used by the paper (Section 5,
+"Workloads and Traces") are not available here; these populations stand in
+for them.  Their shapes follow the paper's Table 2 (input/output lengths of
+ChatBot / Tool&Agent / Coder / Reasoning), Table 3 (seconds-scale TTFT
+targets) and Section 5's serving setup (chunk 512, max batch 128).
+
+Five workloads (``make_workload(cfg)``):
+  0  tiny: 256 chat requests, 3 SLO classes, 8B-class KV, 4096-block pool
+  1  mid: 8192 chat requests, 5 classes, 65536-block pool, token cap 16384
+  2  headline: 65536 requests, 80% chat / 20% agentic, 200 GB pool
+  3  reasoning-heavy, prefix-shared, high load, exact budget ties
+  4  scale: 262144 requests, 70B-class KV, 250 GB pool, token cap 32768
+"""
+from __future__ import annotations
+
+import numpy as np
+
+QUEUED, RUNNING_PREFILL, DECODE = 0, 1, 2
+QT_NEW, QT_TIER1, QT_TIER2 = 0, 1, 2
+KV_HBM, KV_DRAM, KV_NVME, KV_NONE = 0, 1, 2, 3
+
+T_NOW_NS = 10 ** 12
+BLOCK_TOKENS = 16
+CHUNK_TOKENS = 512           # Section 5: chunk size of 512 tokens
+MAX_BATCH = 128              # Section 5: maximum batch size of 128
+GAMMA_Q16 = 81920            # guardband 1.25 (the paper gives no value)
+TIER2_RESERVE_Q16 = 4096     # 1/16 of the token cap reserved for Tier-2
+SEC = 10 ** 9
+
+# Synthetic MI355X-class per-iteration cost coefficients (picoseconds).
+COSTS = {
+    "8b": dict(c_iter_ps=2_000_000_000, c_decode_ps=33_000_000,
+               c_token_ps=12_800_000, c_attn_ps=420),
+    "70b": dict(c_iter_ps=17_500_000_000, c_decode_ps=80_000_000,
+                c_token_ps=112_000_000, c_attn_ps=2_100),
+}
+# KV geometry: 8 KV heads x head_dim 128 x bf16 x 16 tokens = 32 KiB per
+# (layer, K or V) chunk of one block.
+GEOMETRY = {"8b": dict(num_layers=32), "70b": dict(num_layers=80)}
+CHUNK_BYTES = 8 * 128 * 2 * BLOCK_TOKENS
+
+# Links on the restore paths (Section 4.3): DRAM<->HBM and NVMe->DRAM,
+# given as bandwidth (bytes/s) and a fixed per-transfer overhead (ns).
+LINKS = {"dram_hbm": (55e9, 10_000), "nvme_dram": (14e9, 100_000)}
+
+
+def block_bytes(model: str) -> int:
+    return 2 * GEOMETRY[model]["num_layers"] * CHUNK_BYTES
+
+
+def link_params(model: str) -> tuple[list[int], list[int]]:
+    """Per-link fixed overhead (ns) and time per KV block (ns, rounded up).
+
+    Unit conversion of the link specification only."""
+    bb = block_bytes(model)
+    delta, blk = [], []
+    for name in ("dram_hbm", "nvme_dram"):
+        bw, d = LINKS[name]
+        blk.append(int(-(-bb * SEC // int(bw))))
+        delta.append(d)
+    return delta, blk
+
+
+CONFIGS = {
+    0: dict(n=256, model="8b", slo_s=[2, 10, 60], mix={"chat": 1.0},
+            tiers=(0.50, 0.30, 0.00, 0.20), load_decodes=64, pool=4096,
+            token_cap=8192, max_move=2 ** 31 - 1, elapsed_frac=1.0),
+    1: dict(n=8192, model="8b", slo_s=[1, 2, 10, 30, 60], mix={"chat": 1.0},
+            tiers=(0.35, 0.40, 0.10, 0.15), load_decodes=64, pool=65536,
+            token_cap=16384, max_move=512, elapsed_frac=1.0),
+    2: dict(n=65536, model="8b", slo_s=[1, 2, 10, 30, 60], mix={"chat": 0.8, "agentic": 0.2},
+            classes={"chat": [0, 1, 2], "agentic": [2, 3, 4]},
+            tiers=(0.35, 0.40, 0.10, 0.15), load_decodes=64, pool=95367,
+            token_cap=16384, max_move=954, elapsed_frac=0.5),
+    3: dict(n=65536, model="8b", slo_s=[1, 2, 10, 30, 60],
+            mix={"reasoning": 0.5, "chat": 0.25, "agentic": 0.25},
+            classes={"chat": [0, 1, 2], "agentic": [2, 3, 4], "reasoning": [3, 4]},
+            tiers=(0.35, 0.40, 0.10, 0.15), load_decodes=MAX_BATCH - 1, pool=95367,
+            token_cap=16384, max_move=954, elapsed_frac=None, shared_prefix=True),
+    # 70B-class targets are looser, as Table 3's grow with model size
+    4: dict(n=262144, model="70b", slo_s=[2, 5, 10, 30, 60], mix={"chat": 0.8, "agentic": 0.2},
+            classes={"chat": [0, 1, 2], "agentic": [4]},
+            tiers=(0.40, 0.35, 0.15, 0.10), load_decodes=64, pool=47683,
+            token_cap=32768, max_move=1526, elapsed_frac=0.5),
+}
+
+# Lognormal length laws (mu, sigma, clip) per request class.
+LENGTHS = {
+    "chat": dict(n_in=(6.0, 1.0, 16, 8192), n_out=(5.0, 1.0, 1, 65536)),
+    "agentic": dict(n_in=(9.0, 0.7, 16, 131072), n_out=(7.0, 1.0, 1, 65536)),
+    # fitted to Table 2's Reasoning row: input p50 3680, p95 16221
+    "reasoning": dict(n_in=(8.21, 0.90, 16, 131072), n_out=(8.0, 1.0, 1, 131072)),
+}
+
+
+def _lognormal(rng, law, size):
+    mu, sigma, lo, hi = law
+    return np.clip(np.rint(rng.lognormal(mu, sigma, size)), lo, hi).astype(np.int64)
+
+
+def make_params(cfg: int | dict, load_decodes=None) -> dict:
+    c = CONFIGS[cfg] if isinstance(cfg, int) else cfg
+    delta, blk = link_params(c["model"])
+    slo = [int(s * SEC) for s in c["slo_s"]]
+    p = dict(t_now_ns=T_NOW_NS, num_classes=len(slo), slo_ns=slo + [0] * (16 - len(slo)),
+             block_tokens=BLOCK_TOKENS, chunk_tokens=CHUNK_TOKENS,
+             load_decodes=c["load_decodes"] if load_decodes is None else load_decodes,
+             max_batch=MAX_BATCH, gamma_q16=GAMMA_Q16, token_cap=c["token_cap"],
+             tier2_reserve_q16=TIER2_RESERVE_Q16, max_move_blocks=c["max_move"],
+             num_blocks=c["pool"], link_delta_ns=delta, link_blk_ns=blk)
+    p.update(COSTS[c["model"]])
+    return p
+
+
+def kv_geometry(model: str, num_blocks: int, layout: str = "layer_major",
+                chunk_bytes: int = CHUNK_BYTES) -> dict:
+    """Strides (bytes) of a paged KV pool.
+
+    layer_major: one K and one V cache per layer, each [num_blocks, chunk]
+    (per-layer paged caches).  block_major: all layers of a block together."""
+    L = GEOMETRY[model]["num_layers"]
+    if layout == "layer_major":
+        g = dict(slot_stride=chunk_bytes, kv_stride=num_blocks * chunk_bytes,
+                 layer_stride=2 * num_blocks * chunk_bytes)
+    elif layout == "block_major":
+        g = dict(slot_stride=2 * L * chunk_bytes, kv_stride=chunk_bytes,
+                 layer_stride=2 * chunk_bytes)
+    else:
+        raise ValueError(layout)
+    g.update(num_layers=L, chunk_bytes=chunk_bytes, num_blocks=num_blocks,
+             pool_bytes=2 * L * num_blocks * chunk_bytes)
+    return g
+
+
+def make_workload(cfg: int, seed: int | None = None, n: int | None = None) -> dict:
+    """Draw one synthetic scheduling-step input.
+
+    Returns a dict of numpy arrays (request SoA, block table, free list) plus
+    ``params`` (integers), ``geometry`` and ``config``."""
+    c = dict(CONFIGS[cfg])
+    if n is not None:
+        c["n"] = n
+    n = c["n"]
+    rng = np.random.Generator(np.random.PCG64(1000 + cfg if seed is None else seed))
+    bt = BLOCK_TOKENS
+    ncls = len(c["slo_s"])
+    slo_ns = np.array([int(s * SEC) for s in c["slo_s"]], np.int64)
+
+    # population class per request
+    names = list(c["mix"])
+    kind = rng.choice(len(names), size=n, p=[c["mix"][k] for k in names])
+    n_in = np.zeros(n, np.int64)
+    n_out = np.zeros(n, np.int64)
+    for j, name in enumerate(names):
+        m = kind == j
+        n_in[m] = _lognormal(rng, LENGTHS[name]["n_in"], int(m.sum()))
+        n_out[m] = _lognormal(rng, LENGTHS[name]["n_out"], int(m.sum()))
+    # SLO targets are bound to the application class (Section 4.1, Table 3):
+    # a class draws uniformly from its own subset of the SLO classes.
+    slo_class = rng.integers(0, ncls, n).astype(np.int64)
+    for j, name in enumerate(names):
+        allowed = c.get("classes", {}).get(name)
+        if allowed is not None:
+            m = kind == j
+            slo_class[m] = rng.choice(np.array(allowed), int(m.sum()))
+
+    # prefix residency: tier drawn per request; the cached prefix is 50..100%
+    # of the prompt (earlier turns of a conversation or agent loop)
+    # A long prompt is long because of context accumulated in earlier turns,
+    # so "no cached prefix" is drawn only for prompts shorter than the median
+    # of their class (twice as often there); the tier marginals are kept.
+    p_hbm, p_dram, p_nvme, p_none = c["tiers"]
+    cached = np.array([p_hbm, p_dram, p_nvme]) / (1.0 - p_none)
+    tier = rng.choice(3, size=n, p=cached)
+    short = np.zeros(n, bool)
+    for j in range(len(names)):
+        m = kind == j
+        if m.any():
+            short[m] = n_in[m] < np.median(n_in[m])
+    tier = np.where(short & (rng.random(n) < 2.0 * p_none), KV_NONE, tier)
+    frac = rng.uniform(0.5, 1.0, n)
+    n_prefix = bt * np.floor(frac * n_in / bt).astype(np.int64)
+    n_prefix = np.minimum(n_prefix, bt * ((n_in - 1) // bt))
+    arrival_jitter = None
+
+    if c.get("shared_prefix"):
+        # 30% of requests extend one of 512 shared prefixes of 1k..32k tokens;
+        # they come in families of 4 parallel samples with the same suffix
+        # length, class and arrival time (exact ties in every field).
+        nfam_req = int(0.3 * n) // 4 * 4
+        fam_ids = rng.permutation(n)[:nfam_req].reshape(-1, 4)
+        pre_len = bt * (rng.integers(1024, 32769, 512) // bt)
+        pre_tier = rng.choice(4, size=512, p=list(c["tiers"]))
+        which = rng.integers(0, 512, fam_ids.shape[0])
+        lead = fam_ids[:, 0]
+        for col in range(4):
+            members = fam_ids[:, col]
+            n_in[members] = pre_len[which] + n_in[lead]
+            n_out[members] = n_out[lead]
+            slo_class[members] = slo_class[lead]
+            kind[members] = kind[lead]
+            tier[members] = pre_tier[which]
+            n_prefix[members] = pre_len[which]
+        n_in = np.minimum(n_in, 131072)
+        n_prefix = np.minimum(n_prefix, bt * ((n_in - 1) // bt))
+        # High load: every request has already waited about its SLO minus the
+        # time its uncached tokens take at a nominal 25k tokens/s, give or take
+        # up to 20 ms (a queueing-delay model, not the scheduler's estimator).
+        uncached = np.where(tier == KV_NONE, n_in, n_in - n_prefix)
+        nominal = (uncached * SEC) // 25_000
+        eps = rng.choice(np.array([-20, -10, 0, 10, 20], np.int64) * 10 ** 6, n)
+        elapsed = slo_ns[slo_class] - nominal - eps
+        fam_lead_elapsed = elapsed[lead]
+        for col in range(4):
+            elapsed[fam_ids[:, col]] = fam_lead_elapsed
+        elapsed = np.clip(elapsed, 0, slo_ns[slo_class])
+        arrival_jitter = elapsed
+    no_prefix = (tier == KV_NONE) | (n_prefix <= 0)
+    tier = np.where(no_prefix, KV_NONE, tier)
+    n_prefix = np.where(no_prefix, 0, n_prefix)
+
+    if arrival_jitter is None:
+        hi = (slo_ns[slo_class] * c["elapsed_frac"]).astype(np.int64)
+        elapsed = (rng.random(n) * (hi + 1)).astype(np.int64)
+    arrival = T_NOW_NS - elapsed
+
+    # state: QUEUED 90%, RUNNING_PREFILL 4%, DECODE 6%, while running rows fit
+    # in 60% of the pool
+    state = rng.choice(3, size=n, p=[0.90, 0.04, 0.06])
+    u1 = rng.random(n)
+    prog = np.zeros(n, np.int64)
+    rp = state == RUNNING_PREFILL
+    prog[rp] = 1 + np.floor(u1[rp] * (n_in[rp] - 1)).astype(np.int64)
+    de = state == DECODE
+    prog[de] = np.floor(u1[de] * n_out[de]).astype(np.int64)
+    rows = np.zeros(n, np.int64)
+    rows[rp] = -(-prog[rp] // bt)
+    rows[de] = -(-(n_in[de] + prog[de]) // bt)
+    budget = int(0.6 * c["pool"])
+    cum = 0
+    for i in np.flatnonzero(state != QUEUED):
+        if cum + rows[i] <= budget:
+            cum += int(rows[i])
+        else:
+            state[i] = QUEUED
+            prog[i] = 0
+            rows[i] = 0
+    queued = state == QUEUED
+    # a running request's cached prefix is already part of its computed tokens
+    queue_tier = rng.choice(3, size=n, p=[0.25, 0.65, 0.10])
+    queue_tier[de] = QT_TIER1
+
+    nnz = int(rows.sum())
+    perm = rng.permutation(c["pool"])
+    slots = perm[:nnz].astype(np.int32)
+    row_offsets = np.zeros(n + 1, np.int64)
+    row_offsets[1:] = np.cumsum(rows)
+    n_free = min(c["token_cap"] // bt, c["pool"] - nnz)
+    free_slots = perm[nnz:nnz + n_free].astype(np.int32)
+
+    ids = np.cumsum(rng.integers(1, 4, n)).astype(np.uint64) + np.uint64(10 ** 6)
+    params = make_params(c)
+    return dict(
+        id=ids, slo_class=slo_class.astype(np.uint8), state=state.astype(np.uint8),
+        queue_tier=queue_tier.astype(np.uint8), prefix_tier=tier.astype(np.uint8),
+        arrival_ns=arrival.astype(np.int64), n_in=n_in.astype(np.int32),
+        n_out_pred=n_out.astype(np.int32), n_prefix=n_prefix.astype(np.int32),
+        n_progress=prog.astype(np.int32), row_offsets=row_offsets.astype(np.int32),
+        slots=slots, free_slots=free_slots, params=params,
+        geometry=kv_geometry(c["model"], c["pool"]), config=cfg, queued=queued,
+    )
+
+
+# ------------------------------------------------------------ KV payload
+
+def hash32_np(word_index: np.ndarray, seed: int) -> np.ndarray:
+    """Counter-based 32-bit pattern of a 4-byte word index (numpy)."""
+    x = (word_index.astype(np.uint64) + np.uint64(seed * 0x9E3779B9 & 0xFFFFFFFF)) & np.uint64(0xFFFFFFFF)
+    x = (x * np.uint64(0x7FEB352D)) & np.uint64(0xFFFFFFFF)
+    x ^= x >> np.uint64(15)
+    x = (x * np.uint64(0x346CA68B)) & np.uint64(0xFFFFFFFF)
+    x ^= x >> np.uint64(16)
+    return x.astype(np.uint32)
+
+
+def hash32_torch(word_index, seed: int):
+    """The same pattern with torch int64 ops (runs on any device)."""
+    import torch
+    m = 0xFFFFFFFF
+    x = (word_index + (seed * 0x9E3779B9 & m)) & m
+    x = (x * 0x7FEB352D) & m
+    x = x ^ (x >> 15)
+    x = (x * 0x346CA68B) & m
+    x = x ^ (x >> 16)
+    return x.to(torch.int64)
