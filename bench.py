@@ -1,0 +1,235 @@
+#!/usr/bin/env python3
+"""Benchmark of the Cascade scheduling step on one MI355X.
+
+One timed step = the whole hot path on one synthetic queue, inputs resident in
+HBM: cascade_step (budgets, actions, least-budget-first order, admission,
+preemption, move lists), then cascade_pack of the spill moves and
+cascade_unpack of the restore moves it emitted, on one stream.
+
+Prints one JSON line: requests/s of the whole step, the step (parts 1-3)
+latency, pack/unpack GB/s, a roofline record for the dominant kernel (the KV
+copy, measured with HIP events on its stream) and the CPU oracle timed on this
+host as a reported baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("scheduling-step latency (µs) & requests/s at N=65536; "
+          "KV pack/unpack GB/s vs HBM peak")
+HBM_PEAK_GBPS = 8000.0
+WORKLOADS = {
+    0: "tiny: 256 chat requests, 3 SLO classes, 8B-class KV (32 layers), 4096-block pool",
+    1: "mid: 8192 chat requests, 5 SLO classes, 65536-block (128 GiB) pool, token cap 16384",
+    2: ("headline: 65536 requests, 80% chat / 20% agentic, 8B-class KV (32 layers x 8 heads x "
+        "128 x bf16, 16-token blocks), 200 GB pool, token cap 16384, ~2 GB packed and unpacked"),
+    3: ("reasoning-heavy: 65536 requests, 30% sharing 512 prefixes of 1k-32k tokens, high load, "
+        "exact budget ties, 200 GB pool"),
+    4: ("scale: 262144 requests, 70B-class KV (80 layers), 250 GB pool, token cap 32768, "
+        "~8 GB packed and unpacked"),
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--layout", default="layer_major", choices=["layer_major", "block_major"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="approximate CPU time spent on the oracle baseline")
+    ap.add_argument("--calib-copy-gb", type=float, default=0.0,
+                    help="also run a plain torch copy of this size (counter calibration)")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, res, geom, block_bytes, budget_s):
+    """The oracle as it stands, single thread, on this host's cores."""
+    from oracle import ref
+    ref.build(force=False)
+    n = len(w["id"])
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        ref.step(w)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el > 0.5 * budget_s or reps >= 200:
+            break
+    t_step = el / reps
+    # KV copies: a sample of the step's own moves through the oracle's
+    # per-chunk memcpy, on a compact host pool holding just those slots
+    pm, um = res["pack_moves"], res["unpack_moves"]
+    k = int(min(64, max(len(pm), 1)))
+    L, cb = geom["num_layers"], geom["chunk_bytes"]
+    g = dict(num_layers=L, chunk_bytes=cb, slot_stride=cb, kv_stride=k * cb,
+             layer_stride=2 * k * cb)
+    pool = np.ones(2 * L * k * cb, np.uint8)
+    st = np.zeros(k * 2 * L * cb, np.uint8)
+    mv = np.zeros(k, ref.MOVE_DTYPE)
+    mv["pool_slot"] = np.random.default_rng(0).permutation(k)
+    mv["staging_slot"] = np.arange(k)
+    t0 = time.perf_counter()
+    creps = 0
+    while True:
+        ref.pack(pool, g, st, mv)
+        ref.unpack(pool, g, st, mv)
+        creps += 1
+        el = time.perf_counter() - t0
+        if el > 0.5 * budget_s or creps >= 50:
+            break
+    t_copy_block = el / (creps * 2 * k)          # seconds per block per direction
+    t_copy = t_copy_block * (len(pm) + len(um))
+    total = t_step + t_copy
+    return {
+        "value": n / total, "unit": "req/s", "cores": 1, "kind": "oracle",
+        "step_ms": t_step * 1e3, "copy_ms_scaled": t_copy * 1e3,
+        "sample": (f"full {n}-request step x{reps}; KV copies: {k} of the step's "
+                   f"{len(pm) + len(um)} block moves x{creps} through the oracle memcpy, "
+                   f"time scaled to all moves"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only; the step is independent per "
+              "serving instance (no cross-GPU exchange), so --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2608_06557_amd.synth as synth
+    from paper_2608_06557_amd import cascade, device
+
+    assert torch.cuda.is_available(), "needs a ROCm GPU"
+    cascade.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = args.config
+    w = synth.make_workload(cfg)
+    c = synth.CONFIGS[cfg]
+    geom = synth.kv_geometry(c["model"], c["pool"], args.layout)
+    n = len(w["id"])
+    nb = geom["num_blocks"]
+    d = device.DeviceStep(w, slot_cap=nb, unpack_cap=max(1, min(nb, c["max_move"])),
+                          pack_cap=nb)
+    stream = torch.cuda.current_stream()
+    sh = device.stream_handle(stream)
+
+    # first step: learn the move counts (deterministic for this input)
+    assert d.run(stream) == 0
+    res = d.fetch()
+    assert res["status"] == 0, cascade.cascade_strerror(res["status"])
+    n_pack, n_unpack = res["n_pack"], res["n_unpack"]
+    block_bytes = 2 * geom["num_layers"] * geom["chunk_bytes"]
+
+    pool = torch.empty(geom["pool_bytes"], dtype=torch.uint8, device=dev)
+    device.fill_pattern_(pool, seed=1)
+    st_out = torch.empty(max(n_pack, 1) * block_bytes, dtype=torch.uint8, device=dev)
+    st_in = torch.empty(max(n_unpack, 1) * block_bytes, dtype=torch.uint8, device=dev)
+    device.fill_pattern_(st_in, seed=2)
+    cstat = torch.zeros(1, dtype=torch.int32, device=dev)
+    pl = device.kv_pool_struct(pool.data_ptr(), geom)
+    torch.cuda.synchronize()
+
+    def one_step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        rc = d.run(stream)
+        if ev is not None:
+            ev[1].record(stream)
+        rc |= cascade.cascade_pack(pl, st_out.data_ptr(), max(n_pack, 1),
+                                   d.pack_moves.data_ptr(), d.n_pack_ptr(), d.caps[2],
+                                   cstat.data_ptr(), sh)
+        if ev is not None:
+            ev[2].record(stream)
+        rc |= cascade.cascade_unpack(pl, st_in.data_ptr(), max(n_unpack, 1),
+                                     d.unpack_moves.data_ptr(), d.n_unpack_ptr(), d.caps[1],
+                                     cstat.data_ptr(), sh)
+        if ev is not None:
+            ev[3].record(stream)
+        return rc
+
+    for _ in range(args.warmup):
+        assert one_step() == 0
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        assert one_step(evs[k]) == 0
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    res2 = d.fetch()
+    assert res2["status"] == 0 and int(cstat.item()) == 0
+    assert res2["n_pack"] == n_pack and res2["n_unpack"] == n_unpack
+
+    t_step = np.array([e[0].elapsed_time(e[1]) for e in evs]) * 1e3      # us
+    t_pack = np.array([e[1].elapsed_time(e[2]) for e in evs]) * 1e3
+    t_unpack = np.array([e[2].elapsed_time(e[3]) for e in evs]) * 1e3
+    t_all = np.array([e[0].elapsed_time(e[3]) for e in evs]) * 1e3
+    ms_per_step = wall * 1e3 / args.steps
+    bytes_pack = 2.0 * n_pack * block_bytes
+    bytes_unpack = 2.0 * n_unpack * block_bytes
+    gbps = lambda b, us: b / (us * 1e-6) / 1e9 if us > 0 else 0.0
+    copy_us = float(np.mean(t_pack) + np.mean(t_unpack))
+    achieved = gbps(bytes_pack + bytes_unpack, copy_us)
+    extra = None
+    if args.calib_copy_gb > 0:
+        nbytes = int(args.calib_copy_gb * 1e9) // 16 * 16
+        a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        b.copy_(a)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        extra = {"bytes": nbytes, "us": e0.elapsed_time(e1) * 1e3,
+                 "GBps": gbps(2.0 * nbytes, e0.elapsed_time(e1) * 1e3)}
+        del a, b
+    out = {
+        "metric": METRIC,
+        "value": n * args.steps / wall,
+        "unit": "req/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {"workload": f"config {cfg}: " + WORKLOADS[cfg], "requests": n,
+                   "kv_layout": args.layout, "pool_blocks": nb,
+                   "block_bytes": block_bytes, "token_cap": c["token_cap"],
+                   "move_cap_blocks": c["max_move"]},
+        "sched_step_us_p50": float(np.median(t_step)),
+        "sched_step_us_p90": float(np.percentile(t_step, 90)),
+        "sched_req_per_s": n / (float(np.median(t_step)) * 1e-6),
+        "pack_blocks": n_pack, "unpack_blocks": n_unpack,
+        "pack_GBps": gbps(bytes_pack, float(np.median(t_pack))),
+        "unpack_GBps": gbps(bytes_unpack, float(np.median(t_unpack))),
+        "step_total_us_p50": float(np.median(t_all)),
+        "roofline": {"bound": "hbm", "kernel": "kvcopy_kernel (pack + unpack launches)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "bytes_per_launch": (bytes_pack + bytes_unpack) / 2.0,
+                     "us_per_launch": copy_us / 2.0},
+    }
+    if extra:
+        out["calib_copy"] = extra
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, res, geom, block_bytes, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

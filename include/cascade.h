@@ -1,0 +1,239 @@
+/*
+ * cascade.h -- C ABI of the MI355X (gfx950) Cascade scheduling step.
+ *
+ * Cascade (arXiv 2608.06557) gives every request a latency budget: its
+ * class TTFT target minus the predicted remaining service time (Section 4.2,
+ * eq:est_latency and eq:budget_eq), reduced by the time it has waited
+ * (eq:rem_budget_eq).  One scheduling iteration (Algorithm 1, Phase 2, and the
+ * memory management of Section 4.4) is computed here in one call:
+ *
+ *   1. budget of every queued / running request, its Tier-1 / Tier-2 queue,
+ *   2. its memory action: retain in HBM, restore or prefetch a prefix from
+ *      DRAM / NVMe (eq:restore_time, eq:max_restorable), recompute, or be
+ *      preempted with a spill to DRAM or a drop (Section 4.4),
+ *   3. least-remaining-budget-first order and admission under the batch token
+ *      cap (chunked prefill) and the HBM KV-block capacity,
+ *   4. the KV block moves, executed by cascade_pack / cascade_unpack between
+ *      the paged HBM pool and contiguous staging buffers.
+ *
+ * Conventions for every entry point:
+ *   - Pointers named *_dev and every array in the structs below are DEVICE
+ *     pointers (hipMalloc / torch CUDA memory) owned by the caller; structs
+ *     themselves are passed by host pointer and read during the call only.
+ *   - Work is enqueued on `stream` (a hipStream_t, NULL = default stream) and
+ *     runs asynchronously; outputs are valid once the stream has completed
+ *     and info[CASCADE_INFO_STATUS] == CASCADE_OK.
+ *   - The library never allocates memory, never synchronises the stream and
+ *     never throws across the ABI.  Errors that the host can see (NULL
+ *     pointers, parameters out of domain, sizes) are returned at once and
+ *     nothing is enqueued.  Errors in device data are written to
+ *     info[CASCADE_INFO_STATUS]; all outputs are unspecified then.
+ *   - Calls that share a workspace must not overlap in time.
+ */
+#ifndef CASCADE_H
+#define CASCADE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes and device status values. */
+#define CASCADE_OK 0
+#define CASCADE_EINVAL (-1)   /* parameter or request data outside the domain */
+#define CASCADE_ENOSPC (-2)   /* workspace or an output list too small */
+#define CASCADE_EHIP (-3)     /* a HIP launch failed */
+#define CASCADE_ETIMEOUT (-4) /* a cross-workgroup wait exceeded its bound */
+#define CASCADE_EINTERNAL (-5) /* an internal consistency check failed */
+
+/* Request state. */
+#define CASCADE_QUEUED 0
+#define CASCADE_RUNNING_PREFILL 1 /* some prompt tokens computed, KV rows held */
+#define CASCADE_DECODE 2
+/* Queue tier (Section 4 overview: Tier-1 priority queue, Tier-2 best effort). */
+#define CASCADE_QT_NEW 0
+#define CASCADE_QT_TIER1 1
+#define CASCADE_QT_TIER2 2
+/* Residency of a request's matched prefix (Section 4.1: tiers 0, 1, 2). */
+#define CASCADE_KV_HBM 0
+#define CASCADE_KV_DRAM 1
+#define CASCADE_KV_NVME 2
+#define CASCADE_KV_NONE 3
+/* Memory actions (Section 1, Section 4.3, Section 4.4). */
+#define CASCADE_ACT_RETAIN 1          /* KV stays (or is shared) in HBM */
+#define CASCADE_ACT_RESTORE 2         /* admitted: restore_blocks prefix blocks now */
+#define CASCADE_ACT_PREFETCH 3        /* not admitted: start the restore, no HBM yet */
+#define CASCADE_ACT_RECOMPUTE 4       /* recompute the prefix on the GPU */
+#define CASCADE_ACT_PREEMPT_OFFLOAD 5 /* preempted, blocks spilled to DRAM */
+#define CASCADE_ACT_PREEMPT_DROP 6    /* preempted, blocks dropped */
+
+/* Indices into the device info array of cascade_outputs_t. */
+#define CASCADE_INFO_STATUS 0
+#define CASCADE_INFO_N_ADMITTED 1
+#define CASCADE_INFO_N_SLOT_LIST 2
+#define CASCADE_INFO_N_UNPACK 3
+#define CASCADE_INFO_N_PACK 4
+#define CASCADE_INFO_LEN 8
+
+/* Per-request metadata (Section 4.4, "Per-request state"), structure of
+   arrays with n entries each.  Request i's position in these arrays is its
+   tie-break: ids must be strictly increasing, so equal budgets keep id order.
+     slo_class   < num_classes; the class's TTFT target is params.slo_ns[c]
+     state       CASCADE_QUEUED / _RUNNING_PREFILL / _DECODE
+     queue_tier  tier from the previous step (CASCADE_QT_*)
+     prefix_tier deepest tier holding the matched prefix (CASCADE_KV_*)
+     arrival_ns  0 <= arrival <= params.t_now_ns
+     n_in        prompt tokens, 1 .. 2^17
+     n_out_pred  predicted output tokens, 0 .. 2^17
+     n_prefix    matched prefix tokens, multiple of block_tokens, <= n_in - 1;
+                 for a queued request 0 exactly when prefix_tier is NONE
+     n_progress  QUEUED: 0; RUNNING_PREFILL: prompt tokens computed
+                 (1 .. n_in-1); DECODE: tokens generated (0 .. 2^17) */
+typedef struct {
+  int32_t n; /* 0 .. 2^20 */
+  const uint64_t *id;
+  const uint8_t *slo_class, *state, *queue_tier, *prefix_tier;
+  const int64_t *arrival_ns;
+  const int32_t *n_in, *n_out_pred, *n_prefix, *n_progress;
+} cascade_requests_t;
+
+/* Paged KV block table (CSR): request i holds HBM pool slots
+   slots[row_offsets[i] .. row_offsets[i+1]).  row_offsets[0] = 0; the row of
+   a queued request is empty, a running prefill holds ceil(n_progress/bt)
+   blocks and a decode ceil((n_in + n_progress)/bt). */
+typedef struct {
+  const int32_t *row_offsets; /* n + 1 entries */
+  const int32_t *slots;       /* row_offsets[n] entries, each in [0, num_blocks) */
+} cascade_block_table_t;
+
+/* HBM pool state: num_blocks slots, n_free of them listed in free_slots,
+   taken in list order. */
+typedef struct {
+  int32_t num_blocks;
+  int32_t n_free; /* 0 .. num_blocks */
+  const int32_t *free_slots;
+} cascade_tier_state_t;
+
+/* Scheduling parameters (host struct, passed by value to the kernels).
+   Latency estimate (Section 4.2): computing n prompt tokens that start at
+   position s with dd co-scheduled decodes takes, in picoseconds,
+     ceil(n/chunk_tokens)*(c_iter_ps + dd*c_decode_ps) + n*c_token_ps
+       + c_attn_ps * n*(2s+n+1)/2
+   under the actual load dd = load_decodes and the maximum load
+   dd = max_batch - 1.  Links (eq:restore_time): [0] DRAM->HBM, [1]
+   NVMe->DRAM, each a fixed overhead in ns and a time per KV block in ns.
+   Domain: 0 <= t_now < 2^62; 1 <= num_classes <= 16; 0 <= slo_ns <= 2^50;
+   1 <= block_tokens <= 2^16; 16 <= chunk_tokens <= 2^20; 1 <= max_batch <=
+   4096; 0 <= load_decodes < max_batch; 2^16 <= gamma_q16 <= 2^20 (gamma in
+   Q16, >= 1); c_iter, c_decode >= 0 and c_iter + max_batch*c_decode <= 2^36;
+   0 <= c_token <= 2^28; 0 <= c_attn <= 2^16; 0 <= link_delta <= 2^40;
+   1 <= link_blk <= 2^32; 1 <= token_cap <= 2^24; 0 <= tier2_reserve_q16 <=
+   65536 (share of the token cap kept for Tier-2 when Tier-2 is non-empty);
+   max_move_blocks >= 0 (restore + prefetch blocks per step, the link
+   constraint of eq:opt_goal_compact). */
+typedef struct {
+  int64_t t_now_ns;
+  int32_t num_classes;
+  int64_t slo_ns[16];
+  int32_t block_tokens, chunk_tokens, load_decodes, max_batch;
+  int32_t gamma_q16;
+  int64_t c_iter_ps, c_decode_ps, c_token_ps, c_attn_ps;
+  int64_t link_delta_ns[2];
+  int64_t link_blk_ns[2];
+  int32_t token_cap, tier2_reserve_q16, max_move_blocks;
+} cascade_params_t;
+
+/* One KV block move: request, block index within that request, HBM pool slot
+   and staging slot. */
+typedef struct { int32_t req, blk, pool_slot, staging_slot; } cascade_move_t;
+
+/* Outputs (device arrays of n entries unless stated, written by the step).
+     budget_ns       remaining budget B_rem (eq:rem_budget_eq)
+     action          CASCADE_ACT_*
+     queue_tier_out  tier after this step
+     tokens_granted  prompt / decode tokens scheduled this step (0 if not
+                     admitted)
+     restore_blocks  prefix blocks restored (RESTORE) or prefetched
+                     (PREFETCH), 0 otherwise
+     order           request index at each priority position
+     alloc_begin     first slot_list index of the request's new HBM blocks,
+                     -1 if not admitted; its first restore_blocks entries
+                     receive the restored prefix
+     alloc_count     number of new HBM blocks (0 if not admitted)
+     admitted        admitted request indices in priority order
+                     (info[N_ADMITTED] entries)
+     slot_list       free slots, then the preempted requests' slots (back of
+                     the order first, each row in order); capacity entries
+     unpack_moves    one per restored block, admitted order
+     pack_moves      one per block of each request preempted with a spill
+     info            device int32[CASCADE_INFO_LEN]: status and counts.  The
+                     counts are the required sizes even when a list did not
+                     fit its capacity (status CASCADE_ENOSPC). */
+typedef struct {
+  int64_t *budget_ns;
+  uint8_t *action, *queue_tier_out;
+  int32_t *tokens_granted, *restore_blocks, *order, *alloc_begin, *alloc_count, *admitted;
+  int32_t *slot_list;
+  cascade_move_t *unpack_moves, *pack_moves;
+  int32_t slot_list_capacity, unpack_capacity, pack_capacity;
+  int32_t *info;
+} cascade_outputs_t;
+
+/* Paged KV pool: chunk (slot, layer l, kv in {0: K, 1: V}) of chunk_bytes
+   starts at base + l*layer_stride + kv*kv_stride + slot*slot_stride, for
+   slot in [0, num_slots).  Staging slot j holds its 2*num_layers chunks back
+   to back: chunk (j, l, kv) at ((j*num_layers + l)*2 + kv)*chunk_bytes.
+   base, staging, chunk_bytes and the strides must be multiples of 16. */
+typedef struct {
+  void *base;
+  int32_t num_layers;
+  int32_t num_slots;
+  int64_t chunk_bytes, layer_stride, kv_stride, slot_stride;
+} cascade_kv_pool_t;
+
+/* Workspace size in bytes needed by cascade_step for n requests.  The caller
+   allocates it once (device memory, 256-byte aligned) and may reuse it for
+   every step of at most n requests. */
+size_t cascade_step_workspace_bytes(int32_t n);
+
+/* One scheduling step (Algorithm 1, Phase 2 over the whole queue, with the
+   estimator and budget engine of Section 4.2 and the preemption of Section
+   4.4).  Returns CASCADE_OK once enqueued, CASCADE_EINVAL for NULL pointers,
+   parameters out of domain or negative capacities, CASCADE_ENOSPC when
+   workspace_bytes < cascade_step_workspace_bytes(n), CASCADE_EHIP when a
+   launch fails.  Request data, block-table and free-list errors set
+   info[STATUS] = CASCADE_EINVAL; lists longer than their capacity set
+   CASCADE_ENOSPC. */
+int cascade_step(const cascade_requests_t *requests, const cascade_block_table_t *table,
+                 const cascade_tier_state_t *tier, const cascade_params_t *params,
+                 const cascade_outputs_t *out, void *workspace, size_t workspace_bytes,
+                 void *stream);
+
+/* KV block gather (Section 4.4 preemption spill): for each of the first
+   min(*n_moves_dev, max_moves) moves, copy every (layer, K/V) chunk of HBM
+   pool slot moves[m].pool_slot to staging slot moves[m].staging_slot of a
+   staging buffer of staging_slots slots.  A move whose pool slot is outside
+   [0, num_slots) or staging slot outside [0, staging_slots) is skipped and
+   sets *status_dev = CASCADE_EINVAL (status_dev may be NULL).  Enqueue
+   before cascade_unpack of the same step: a preempted request's slots may be
+   restore destinations.  Returns CASCADE_EINVAL for NULL pointers,
+   misalignment or a bad geometry, CASCADE_EHIP on launch failure. */
+int cascade_pack(const cascade_kv_pool_t *pool, void *staging, int32_t staging_slots,
+                 const cascade_move_t *moves, const int32_t *n_moves_dev, int32_t max_moves,
+                 int32_t *status_dev, void *stream);
+
+/* KV block scatter (Section 4.3 restore, final DRAM->HBM hop, Section 4.4):
+   the inverse copy, staging slot -> pool slot, same rules. */
+int cascade_unpack(const cascade_kv_pool_t *pool, const void *staging, int32_t staging_slots,
+                   const cascade_move_t *moves, const int32_t *n_moves_dev, int32_t max_moves,
+                   int32_t *status_dev, void *stream);
+
+/* Short English text for a return code or status value. */
+const char *cascade_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

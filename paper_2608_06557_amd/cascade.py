@@ -1,0 +1,148 @@
+"""ctypes binding of ``libcascade.so`` (see include/cascade.h).
+
+Argument marshalling only: every step of the scheduling path runs in the
+library's gfx950 kernels.  The library must be built (``build.py``); there is
+no fallback, loading fails loudly if it is missing.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcascade.so")
+
+OK, EINVAL, ENOSPC, EHIP, ETIMEOUT, EINTERNAL = 0, -1, -2, -3, -4, -5
+QUEUED, RUNNING_PREFILL, DECODE = 0, 1, 2
+QT_NEW, QT_TIER1, QT_TIER2 = 0, 1, 2
+KV_HBM, KV_DRAM, KV_NVME, KV_NONE = 0, 1, 2, 3
+ACT_RETAIN, ACT_RESTORE, ACT_PREFETCH, ACT_RECOMPUTE = 1, 2, 3, 4
+ACT_PREEMPT_OFFLOAD, ACT_PREEMPT_DROP = 5, 6
+INFO_STATUS, INFO_N_ADMITTED, INFO_N_SLOT_LIST, INFO_N_UNPACK, INFO_N_PACK = 0, 1, 2, 3, 4
+INFO_LEN = 8
+
+EXPORTED = ["cascade_step_workspace_bytes", "cascade_step", "cascade_pack", "cascade_unpack",
+            "cascade_strerror"]
+
+
+class Requests(C.Structure):
+    _fields_ = [("n", C.c_int32), ("id", C.c_void_p), ("slo_class", C.c_void_p),
+                ("state", C.c_void_p), ("queue_tier", C.c_void_p), ("prefix_tier", C.c_void_p),
+                ("arrival_ns", C.c_void_p), ("n_in", C.c_void_p), ("n_out_pred", C.c_void_p),
+                ("n_prefix", C.c_void_p), ("n_progress", C.c_void_p)]
+
+
+class BlockTable(C.Structure):
+    _fields_ = [("row_offsets", C.c_void_p), ("slots", C.c_void_p)]
+
+
+class TierState(C.Structure):
+    _fields_ = [("num_blocks", C.c_int32), ("n_free", C.c_int32), ("free_slots", C.c_void_p)]
+
+
+class Params(C.Structure):
+    _fields_ = [
+        ("t_now_ns", C.c_int64), ("num_classes", C.c_int32), ("slo_ns", C.c_int64 * 16),
+        ("block_tokens", C.c_int32), ("chunk_tokens", C.c_int32),
+        ("load_decodes", C.c_int32), ("max_batch", C.c_int32), ("gamma_q16", C.c_int32),
+        ("c_iter_ps", C.c_int64), ("c_decode_ps", C.c_int64),
+        ("c_token_ps", C.c_int64), ("c_attn_ps", C.c_int64),
+        ("link_delta_ns", C.c_int64 * 2), ("link_blk_ns", C.c_int64 * 2),
+        ("token_cap", C.c_int32), ("tier2_reserve_q16", C.c_int32),
+        ("max_move_blocks", C.c_int32),
+    ]
+
+
+class Move(C.Structure):
+    _fields_ = [("req", C.c_int32), ("blk", C.c_int32), ("pool_slot", C.c_int32),
+                ("staging_slot", C.c_int32)]
+
+
+class Outputs(C.Structure):
+    _fields_ = [
+        ("budget_ns", C.c_void_p), ("action", C.c_void_p), ("queue_tier_out", C.c_void_p),
+        ("tokens_granted", C.c_void_p), ("restore_blocks", C.c_void_p), ("order", C.c_void_p),
+        ("alloc_begin", C.c_void_p), ("alloc_count", C.c_void_p), ("admitted", C.c_void_p),
+        ("slot_list", C.c_void_p), ("unpack_moves", C.c_void_p), ("pack_moves", C.c_void_p),
+        ("slot_list_capacity", C.c_int32), ("unpack_capacity", C.c_int32),
+        ("pack_capacity", C.c_int32), ("info", C.c_void_p),
+    ]
+
+
+class KvPool(C.Structure):
+    _fields_ = [("base", C.c_void_p), ("num_layers", C.c_int32), ("num_slots", C.c_int32),
+                ("chunk_bytes", C.c_int64), ("layer_stride", C.c_int64),
+                ("kv_stride", C.c_int64), ("slot_stride", C.c_int64)]
+
+
+_lib = None
+
+
+def load() -> C.CDLL:
+    """Load the library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2608_06557_amd.build` (no CPU fallback exists)")
+        L = C.CDLL(LIB_PATH)
+        L.cascade_step_workspace_bytes.restype = C.c_size_t
+        L.cascade_step_workspace_bytes.argtypes = [C.c_int32]
+        L.cascade_step.restype = C.c_int
+        L.cascade_step.argtypes = [C.POINTER(Requests), C.POINTER(BlockTable),
+                                   C.POINTER(TierState), C.POINTER(Params), C.POINTER(Outputs),
+                                   C.c_void_p, C.c_size_t, C.c_void_p]
+        for name in ("cascade_pack", "cascade_unpack"):
+            f = getattr(L, name)
+            f.restype = C.c_int
+            f.argtypes = [C.POINTER(KvPool), C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                          C.c_int32, C.c_void_p, C.c_void_p]
+        L.cascade_strerror.restype = C.c_char_p
+        L.cascade_strerror.argtypes = [C.c_int]
+        _lib = L
+    return _lib
+
+
+def cascade_step_workspace_bytes(n: int) -> int:
+    return int(load().cascade_step_workspace_bytes(n))
+
+
+def cascade_step(requests: Requests, table: BlockTable, tier: TierState, params: Params,
+                 outputs: Outputs, workspace: int, workspace_bytes: int, stream: int) -> int:
+    return int(load().cascade_step(C.byref(requests), C.byref(table), C.byref(tier),
+                                   C.byref(params), C.byref(outputs), C.c_void_p(workspace),
+                                   workspace_bytes, C.c_void_p(stream)))
+
+
+def cascade_pack(pool: KvPool, staging: int, staging_slots: int, moves: int, n_moves_dev: int,
+                 max_moves: int, status_dev: int, stream: int) -> int:
+    return int(load().cascade_pack(C.byref(pool), C.c_void_p(staging), staging_slots,
+                                   C.c_void_p(moves), C.c_void_p(n_moves_dev), max_moves,
+                                   C.c_void_p(status_dev), C.c_void_p(stream)))
+
+
+def cascade_unpack(pool: KvPool, staging: int, staging_slots: int, moves: int, n_moves_dev: int,
+                   max_moves: int, status_dev: int, stream: int) -> int:
+    return int(load().cascade_unpack(C.byref(pool), C.c_void_p(staging), staging_slots,
+                                     C.c_void_p(moves), C.c_void_p(n_moves_dev), max_moves,
+                                     C.c_void_p(status_dev), C.c_void_p(stream)))
+
+
+def cascade_strerror(code: int) -> str:
+    return load().cascade_strerror(code).decode()
+
+
+PARAM_KEYS = ["t_now_ns", "num_classes", "block_tokens", "chunk_tokens", "load_decodes",
+              "max_batch", "gamma_q16", "c_iter_ps", "c_decode_ps", "c_token_ps", "c_attn_ps",
+              "token_cap", "tier2_reserve_q16", "max_move_blocks"]
+
+
+def make_params(p: dict) -> Params:
+    s = Params()
+    for k in PARAM_KEYS:
+        setattr(s, k, int(p[k]))
+    for c, v in enumerate(p["slo_ns"]):
+        s.slo_ns[c] = int(v)
+    for l in range(2):
+        s.link_delta_ns[l] = int(p["link_delta_ns"][l])
+        s.link_blk_ns[l] = int(p["link_blk_ns"][l])
+    return s

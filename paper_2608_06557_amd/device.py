@@ -1,0 +1,136 @@
+"""Device-memory plumbing around the C ABI, using torch for allocation and
+streams only.  Uploads a workload (numpy arrays from ``synth``), holds the
+output and workspace buffers, enqueues ``cascade_step`` / ``cascade_pack`` /
+``cascade_unpack`` and reads results back."""
+from __future__ import annotations
+
+import numpy as np
+
+from . import cascade as cx
+
+REQ_FIELDS = [("id", np.int64), ("slo_class", np.uint8), ("state", np.uint8),
+              ("queue_tier", np.uint8), ("prefix_tier", np.uint8), ("arrival_ns", np.int64),
+              ("n_in", np.int32), ("n_out_pred", np.int32), ("n_prefix", np.int32),
+              ("n_progress", np.int32)]
+MOVE_DTYPE = np.dtype([("req", np.int32), ("blk", np.int32), ("pool_slot", np.int32),
+                       ("staging_slot", np.int32)])
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def to_device(a: np.ndarray, device, dtype=None):
+    """Upload an array; empty arrays become a 1-element buffer so that every
+    pointer handed to the library is valid."""
+    torch = _torch()
+    a = np.ascontiguousarray(a if dtype is None else a.astype(dtype, copy=False))
+    if a.dtype == np.uint64:
+        a = a.view(np.int64)
+    if a.size == 0:
+        a = np.zeros(1, a.dtype)
+    return torch.from_numpy(a.copy()).to(device)
+
+
+def stream_handle(stream=None) -> int:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+class DeviceStep:
+    """Buffers for one workload and its cascade_step outputs."""
+
+    def __init__(self, w: dict, device="cuda:0", slot_cap: int | None = None,
+                 unpack_cap: int | None = None, pack_cap: int | None = None):
+        torch = _torch()
+        self.device = torch.device(device)
+        self.n = n = int(len(w["id"]))
+        p = w["params"]
+        self.params = cx.make_params(p)
+        self.num_blocks = int(p["num_blocks"])
+        self.inp = {k: to_device(np.asarray(w[k]), self.device, dt) for k, dt in REQ_FIELDS}
+        self.ro = to_device(np.asarray(w["row_offsets"]), self.device, np.int32)
+        self.slots = to_device(np.asarray(w["slots"]), self.device, np.int32)
+        self.free = to_device(np.asarray(w["free_slots"]), self.device, np.int32)
+        self.n_free = int(len(w["free_slots"]))
+        nb = self.num_blocks
+        self.caps = (nb if slot_cap is None else slot_cap, nb if unpack_cap is None else unpack_cap,
+                     nb if pack_cap is None else pack_cap)
+        nn = max(n, 1)
+        z = lambda k, dt: torch.zeros(max(k, 1), dtype=dt, device=self.device)
+        self.out = {"budget_ns": z(nn, torch.int64), "action": z(nn, torch.uint8),
+                    "queue_tier_out": z(nn, torch.uint8), "tokens_granted": z(nn, torch.int32),
+                    "restore_blocks": z(nn, torch.int32), "order": z(nn, torch.int32),
+                    "alloc_begin": z(nn, torch.int32), "alloc_count": z(nn, torch.int32),
+                    "admitted": z(nn, torch.int32)}
+        self.slot_list = z(self.caps[0], torch.int32)
+        self.unpack_moves = z(4 * self.caps[1], torch.int32)
+        self.pack_moves = z(4 * self.caps[2], torch.int32)
+        self.info = z(cx.INFO_LEN, torch.int32)
+        self.ws_bytes = cx.cascade_step_workspace_bytes(n)
+        self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=self.device)
+        self.ws_ptr = (self.ws.data_ptr() + 255) & ~255
+
+        self.c_req = cx.Requests(n, *[self.inp[k].data_ptr() for k, _ in REQ_FIELDS])
+        self.c_table = cx.BlockTable(self.ro.data_ptr(), self.slots.data_ptr())
+        self.c_tier = cx.TierState(self.num_blocks, self.n_free, self.free.data_ptr())
+        o = self.out
+        self.c_out = cx.Outputs(
+            o["budget_ns"].data_ptr(), o["action"].data_ptr(), o["queue_tier_out"].data_ptr(),
+            o["tokens_granted"].data_ptr(), o["restore_blocks"].data_ptr(), o["order"].data_ptr(),
+            o["alloc_begin"].data_ptr(), o["alloc_count"].data_ptr(), o["admitted"].data_ptr(),
+            self.slot_list.data_ptr(), self.unpack_moves.data_ptr(), self.pack_moves.data_ptr(),
+            self.caps[0], self.caps[1], self.caps[2], self.info.data_ptr())
+
+    def run(self, stream=None) -> int:
+        """Enqueue one step; returns the host-side return code."""
+        return cx.cascade_step(self.c_req, self.c_table, self.c_tier, self.params, self.c_out,
+                               self.ws_ptr, self.ws_bytes, stream_handle(stream))
+
+    def n_unpack_ptr(self) -> int:
+        return self.info.data_ptr() + 4 * cx.INFO_N_UNPACK
+
+    def n_pack_ptr(self) -> int:
+        return self.info.data_ptr() + 4 * cx.INFO_N_PACK
+
+    def fetch(self) -> dict:
+        """Synchronise and return every output as numpy (trimmed to counts)."""
+        torch = _torch()
+        torch.cuda.synchronize(self.device)
+        info = self.info.cpu().numpy()
+        n = self.n
+        res = {k: v.cpu().numpy()[:n] for k, v in self.out.items()}
+        res["status"] = int(info[cx.INFO_STATUS])
+        res["n_admitted"] = int(info[cx.INFO_N_ADMITTED])
+        res["n_slot_list"] = int(info[cx.INFO_N_SLOT_LIST])
+        res["n_unpack"] = int(info[cx.INFO_N_UNPACK])
+        res["n_pack"] = int(info[cx.INFO_N_PACK])
+        res["admitted"] = res["admitted"][:res["n_admitted"]]
+        res["slot_list"] = self.slot_list.cpu().numpy()[:min(res["n_slot_list"], self.caps[0])]
+        um = self.unpack_moves.cpu().numpy().view(MOVE_DTYPE)
+        pm = self.pack_moves.cpu().numpy().view(MOVE_DTYPE)
+        res["unpack_moves"] = um[:min(res["n_unpack"], self.caps[1])]
+        res["pack_moves"] = pm[:min(res["n_pack"], self.caps[2])]
+        return res
+
+
+def kv_pool_struct(base_ptr: int, geom: dict) -> cx.KvPool:
+    return cx.KvPool(base_ptr, int(geom["num_layers"]), int(geom["num_blocks"]),
+                     int(geom["chunk_bytes"]), int(geom["layer_stride"]),
+                     int(geom["kv_stride"]), int(geom["slot_stride"]))
+
+
+def fill_pattern_(t, seed: int, word_offset: int = 0, chunk_words: int = 1 << 26) -> None:
+    """Fill a uint8 device tensor with the counter-based 32-bit pattern of
+    ``synth.hash32_torch`` (word k holds hash32(word_offset + k, seed))."""
+    torch = _torch()
+    from .synth import hash32_torch
+    w = t.view(torch.int32)
+    nw = w.numel()
+    for s in range(0, nw, chunk_words):
+        e = min(nw, s + chunk_words)
+        idx = torch.arange(word_offset + s, word_offset + e, device=t.device, dtype=torch.int64)
+        h = hash32_torch(idx, seed)
+        w[s:e] = (h - ((h >> 31) << 32)).to(torch.int32)

@@ -1,0 +1,167 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/cascade.h declares, the ctypes mirror has the header's exact struct
+layout, and host-side argument checks return their codes before any launch."""
+import ctypes as C
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2608_06557_amd import cascade
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cascade.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(cascade.LIB_PATH):
+        from paper_2608_06557_amd import build
+        build.build()
+    return cascade.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(cascade_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(names) == set(cascade.EXPORTED)
+    out = subprocess.run(["nm", "-D", "--defined-only", cascade.LIB_PATH], check=True,
+                         capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (\w+)$", out, flags=re.M))
+    for n in names:
+        assert n in exported, n
+        assert hasattr(lib, n)
+
+
+STRUCTS = {
+    "cascade_requests_t": cascade.Requests, "cascade_block_table_t": cascade.BlockTable,
+    "cascade_tier_state_t": cascade.TierState, "cascade_params_t": cascade.Params,
+    "cascade_move_t": cascade.Move, "cascade_outputs_t": cascade.Outputs,
+    "cascade_kv_pool_t": cascade.KvPool,
+}
+
+
+def test_struct_layout_matches_header(tmp_path):
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "cascade.h"', "int main(){"]
+    for cname, py in STRUCTS.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for f, _ in py._fields_:
+            lines.append(f'printf("{cname} {f} %zu\\n", offsetof({cname}, {f}));')
+    lines.append("return 0;}")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    got = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split("\n")
+    seen = 0
+    for line in got:
+        if not line:
+            continue
+        cname, field, val = line.split()
+        py = STRUCTS[cname]
+        if field == "size":
+            assert C.sizeof(py) == int(val), cname
+        else:
+            assert getattr(py, field).offset == int(val), (cname, field)
+        seen += 1
+    assert seen == sum(len(p._fields_) + 1 for p in STRUCTS.values())
+
+
+def test_constants_match_header():
+    text = open(HEADER).read()
+    defs = dict((k, int(v)) for k, v in
+                re.findall(r"#define CASCADE_(\w+)\s+\(?(-?\d+)\)?", text))
+    for k, v in defs.items():
+        name = k[5:] if k.startswith("INFO_") and k != "INFO_LEN" else k
+        if k == "INFO_LEN":
+            assert cascade.INFO_LEN == v
+        elif k.startswith("INFO_"):
+            assert getattr(cascade, k) == v, k
+        else:
+            assert getattr(cascade, name) == v, k
+
+
+def test_workspace_size(lib):
+    prev = 0
+    for n in [0, 1, 1000, 65536, 262144, 1 << 20]:
+        b = cascade.cascade_step_workspace_bytes(n)
+        assert b % 256 == 0 and b >= prev
+        prev = b
+    assert cascade.cascade_step_workspace_bytes(-1) == 0
+    assert cascade.cascade_step_workspace_bytes((1 << 20) + 1) == 0
+
+
+def _valid_args():
+    import paper_2608_06557_amd.synth as synth
+    p = cascade.make_params(synth.make_params(0))
+    fake = 4096  # never dereferenced: every case below fails a host-side check
+    req = cascade.Requests(4, *([fake] * 10))
+    table = cascade.BlockTable(fake, fake)
+    tier = cascade.TierState(100, 10, fake)
+    out = cascade.Outputs(*([fake] * 12), 10, 10, 10, fake)
+    return req, table, tier, p, out
+
+
+def test_host_checks_return_einval_without_launch(lib):
+    req, table, tier, p, out = _valid_args()
+    ws = cascade.cascade_step_workspace_bytes(4)
+    f = lambda **kw: cascade.cascade_step(kw.get("req", req), kw.get("table", table),
+                                          kw.get("tier", tier), kw.get("p", p),
+                                          kw.get("out", out), kw.get("ws", 1 << 20),
+                                          kw.get("wsb", ws), 0)
+    assert lib.cascade_step(None, None, None, None, None, None, 0, None) == cascade.EINVAL
+    bad = cascade.Params.from_buffer_copy(p)
+    bad.gamma_q16 = 1000
+    assert f(p=bad) == cascade.EINVAL
+    bad = cascade.Params.from_buffer_copy(p)
+    bad.num_classes = 0
+    assert f(p=bad) == cascade.EINVAL
+    r2 = cascade.Requests.from_buffer_copy(req)
+    r2.n = -1
+    assert f(req=r2) == cascade.EINVAL
+    r2.n = (1 << 20) + 1
+    assert f(req=r2) == cascade.EINVAL
+    r2 = cascade.Requests.from_buffer_copy(req)
+    r2.n_in = None
+    assert f(req=r2) == cascade.EINVAL
+    t2 = cascade.TierState(100, 101, 4096)
+    assert f(tier=t2) == cascade.EINVAL
+    o2 = cascade.Outputs.from_buffer_copy(out)
+    o2.pack_capacity = -1
+    assert f(out=o2) == cascade.EINVAL
+    assert f(ws=(1 << 20) + 8) == cascade.EINVAL       # workspace not 256-byte aligned
+    assert f(wsb=ws - 1) == cascade.ENOSPC
+
+
+def test_copy_host_checks(lib):
+    pool = cascade.KvPool(4096, 32, 10, 32768, 65536, 32768, 32768)
+    n = C.c_int32(1)
+    ok = dict(pool=pool, staging=4096, staging_slots=4, moves=4096,
+              n_moves_dev=C.addressof(n), max_moves=4, status_dev=0, stream=0)
+
+    def call(fn, **kw):
+        a = dict(ok)
+        a.update(kw)
+        return fn(a["pool"], a["staging"], a["staging_slots"], a["moves"], a["n_moves_dev"],
+                  a["max_moves"], a["status_dev"], a["stream"])
+    for fn in (cascade.cascade_pack, cascade.cascade_unpack):
+        assert call(fn, staging=0) == cascade.EINVAL
+        assert call(fn, staging=4100) == cascade.EINVAL            # misaligned
+        assert call(fn, max_moves=-1) == cascade.EINVAL
+        assert call(fn, pool=cascade.KvPool(4096, 0, 10, 32768, 0, 0, 0)) == cascade.EINVAL
+        assert call(fn, pool=cascade.KvPool(4096, 2, 10, 24, 0, 0, 0)) == cascade.EINVAL
+        assert call(fn, pool=cascade.KvPool(4096, 2, 10, 32, 8, 0, 0)) == cascade.EINVAL
+        assert call(fn, max_moves=0) == cascade.OK                   # nothing to launch
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(cascade, "_lib", None)
+    monkeypatch.setattr(cascade, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="no CPU fallback"):
+        cascade.load()
