@@ -66,8 +66,8 @@ class DeviceStep:
                     "alloc_begin": z(nn, torch.int32), "alloc_count": z(nn, torch.int32),
                     "admitted": z(nn, torch.int32)}
         self.slot_list = z(self.caps[0], torch.int32)
-        self.unpack_moves = z(4 * self.caps[1], torch.int32)
-        self.pack_moves = z(4 * self.caps[2], torch.int32)
+        self.unpack_moves = z(4 * max(self.caps[1], 1), torch.int32)
+        self.pack_moves = z(4 * max(self.caps[2], 1), torch.int32)
         self.info = z(cx.INFO_LEN, torch.int32)
         self.ws_bytes = cx.cascade_step_workspace_bytes(n)
         self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=self.device)
