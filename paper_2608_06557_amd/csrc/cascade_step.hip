@@ -8,16 +8,21 @@
 // the link cap, chunked-prefill token grants, HBM block admission and
 // budget-aware preemption (Section 4.4).
 //
-// The paper's scheduler is a sequential CPU loop.  Here every step of it is
-// a data-parallel kernel:
-//   eval      one lane per request: budget, tier, restore want, priority key
-//   prep      key compression to the live budget range + digit histograms
-//   radix     onesweep LSD radix passes (wave64 ballot ranking, decoupled
-//             look-back per digit), constant digits skipped on the device
-//   scan      the sequential loop as prefix sums in priority order, with a
-//             two-level chained decoupled look-back in one launch
-//   finalize  preemption victims, slot list, spill (pack) moves
-//   moves     restore (unpack) moves and final counts
+// The paper's scheduler is a sequential CPU loop.  Here it is 3 + P
+// dependent launches on one stream:
+//   eval      one lane per request: validation, budget, tier, restore want,
+//             priority key, scan record; per-workgroup partial totals (no
+//             atomics); also clears this step's histograms and look-back words
+//   prep      totals of the partials, key compression to the live budget
+//             range, every digit histogram in one read
+//   radix<p>  onesweep LSD radix pass p (wave64 ballot ranking, per-digit
+//             decoupled look-back), launched for the digits a host-side bound
+//             allows; a digit that is constant or beyond the live key width
+//             returns at once, decided on the device
+//   scan      Algorithm 1's loop as prefix sums in priority order: two chained
+//             decoupled look-backs in one launch; the last workgroup to finish
+//             picks the preemption victims and writes the slot list and the
+//             pack / unpack move lists
 // All arithmetic is 64-bit integer, so the result is bit-exact.
 #include <hip/hip_runtime.h>
 #include <stddef.h>
@@ -32,16 +37,17 @@
 namespace cascade {
 namespace {
 
-constexpr int kSortItems = 8;
+constexpr int kSortItems = 4;
 constexpr int kSortTile = kBlock * kSortItems;
+constexpr int kSortWin = 32;     // predecessors read per look-back round trip (radix)
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
-constexpr int kPrepItems = 16;
+constexpr int kPrepItems = 4;
+constexpr int kEvalItems = 1;
 constexpr int kRadix = 256;
 constexpr int kMaxDigits = 8;
-constexpr int kLookWin = 8;
-constexpr int kL1 = 4;  // first-level scan values
-constexpr int kL2 = 7;  // second-level scan values
+constexpr int kL1 = 5;           // first-level scan values
+constexpr int kL2 = 7;           // second-level scan values
 constexpr int kL2Stride = 8;
 
 // Record of one request for the priority-order scan (16 bytes).
@@ -54,31 +60,43 @@ __device__ __forceinline__ int rec_tier(int w) { return (w >> 22) & 3; }
 __device__ __forceinline__ int rec_offl(int w) { return (w >> 26) & 1; }
 __device__ __forceinline__ int rec_decnb(int w) { return (w >> 27) & 1; }
 
-struct RpInfo {          // per running prefill, written by scan
-  int pos, eligible;
-  long long x, y, z, zp;  // inclusive prefixes at pos
+// Totals of one eval workgroup (64 bytes).
+struct Partial {
+  long long held, need1, want1;   // blocks held by running prefills; base need and
+                                  // want over decode + Tier-1
+  unsigned long long bmin, bmax;  // range of the biased, clamped budget
+  unsigned c0, c1, c2, bad;       // requests per group; data-rule violations
+  unsigned pad[2];
+};
+
+// A running prefill, as seen by the scan (compact list, 48 bytes).
+struct RpInfo {
+  int req, pos, eligible, held, row0, offl, pad[2];
+  long long x, y, z, zp;          // inclusive prefixes at pos
 };
 struct RestoreEnt { int req, stage_off, alloc_off, blocks; };
+// Totals of one scan tile over its admitted / left-out requests.
+struct TileTot {
+  long long adm_nb, elig_h, elig_offl_h, n_adm, n_unpack, n_restore, pad[2];
+};
+constexpr int kVictimCap = 256;   // victims staged in LDS by the finishing workgroup
+constexpr int kRestoreCap = 1024; // restore-list entries staged in LDS for the search
 
-// Device control block.  The header is written by one thread of the init
-// kernel; the histograms are cleared by all of its threads.
+// Device control block.  eval's workgroup 0 zeroes the header, every eval
+// workgroup clears part of the histograms and look-back words.
 struct Ctl {
-  unsigned long long bmin, bmax;   // range of the biased, clamped budget
-  long long held_rp;               // blocks held by running prefills (H)
-  long long need1, want1;          // base need and want over decode+Tier-1
-  unsigned cnt[4];                 // requests per priority group
-  unsigned rp_count;
+  unsigned long long bmin, bmax;  // totals, written by prep's workgroup 0
+  long long held_rp, need1, want1;
+  unsigned cnt[4];
   unsigned tile_ctr[kMaxDigits + 1];
-  int kstar;                       // first position that does not fit
-  int pad0;
-  long long kx, ky, kz, kzp;       // prefixes just before kstar
-  long long adm_nb, elig_h, elig_offl_h, n_adm, n_unpack, n_restore;
-  long long pad1[4];
+  unsigned scan_done, pad_u;
+  int kstar;                      // first position whose blocks do not fit
+  long long kx, ky, kz, kzp;      // prefixes just before kstar
   alignas(16) unsigned hist[kMaxDigits][kRadix];
 };
 constexpr size_t kCtlHeaderWords = offsetof(Ctl, hist) / 4;
 
-struct Consts {           // parameters the kernels use, flattened
+struct Consts {                   // parameters the kernels use, flattened
   long long t_now, c_iter, c_dec, c_tok, c_attn;
   long long delta1, delta2, blk1, blk2;  // restore paths: DRAM, NVMe
   int num_classes, bt, chunk, d, dmax, gamma_q16, token_cap, rho_q16, max_move;
@@ -86,27 +104,28 @@ struct Consts {           // parameters the kernels use, flattened
   long long slo[16];
 };
 
-// Workgroup-uniform: true if an earlier kernel (or a workgroup of this one)
-// reported bad data or a timeout.  Every thread of the workgroup must call it.
-__device__ __forceinline__ bool status_failed(const int *info) {
-  int bad = 0;
-  if (threadIdx.x == 0) {
-    const int s = load_agent(info);
-    bad = (s == CASCADE_EINVAL || s == CASCADE_ETIMEOUT || s == CASCADE_EINTERNAL);
-  }
-  return __syncthreads_or(bad) != 0;
+struct Outs {                     // output pointers the scan writes
+  int *order, *granted, *restore, *alloc_begin, *alloc_count, *admitted, *slot_list;
+  uint8_t *action;
+  cascade_move_t *unpack, *pack;
+  int sl_cap, unpack_cap, pack_cap;
+};
+
+__device__ __forceinline__ bool bad_status(int s) {
+  return s == CASCADE_EINVAL || s == CASCADE_ETIMEOUT || s == CASCADE_EINTERNAL;
 }
 __device__ __forceinline__ long long lmin(long long a, long long b) { return a < b ? a : b; }
 __device__ __forceinline__ void set_status(int *info, int code) { store_agent(info, code); }
+__device__ __forceinline__ unsigned udiv_ceil(unsigned a, unsigned b) { return (a + b - 1u) / b; }
 
 // ---------------------------------------------------------------- eval
 
 // Iteration cost model of the TTFT estimator (Section 4.2): n prompt tokens
-// at positions s.. with dd co-scheduled decodes, picoseconds.
+// at positions s.. with dd co-scheduled decodes, picoseconds.  n + s <= 2^17.
 __device__ __forceinline__ long long compute_ps(long long n, long long s, long long dd,
                                                 const Consts &c) {
   if (n <= 0) return 0;
-  const long long iters = (long long)(((unsigned)n + (unsigned)c.chunk - 1u) / (unsigned)c.chunk);
+  const long long iters = udiv_ceil((unsigned)n, (unsigned)c.chunk);
   const long long pairs = (n * (2 * s + n + 1)) >> 1;
   return iters * (c.c_iter + dd * c.c_dec) + n * c.c_tok + c.c_attn * pairs;
 }
@@ -120,66 +139,79 @@ __device__ __forceinline__ long long restore_ns(long long x, long long delta, lo
 
 __global__ __launch_bounds__(kBlock) void eval_kernel(
     cascade_requests_t rq, const int *__restrict__ ro, const int *__restrict__ free_slots,
-    Consts c, int n, Ctl *ctl, int *info, int64_t *__restrict__ budget_out,
+    Consts c, int n, Ctl *ctl, uint4 *clear, size_t clear_vec, int *info,
+    Partial *__restrict__ partials, int64_t *__restrict__ budget_out,
     uint8_t *__restrict__ tier_out, unsigned long long *__restrict__ keys,
-    int4 *__restrict__ rec, int *__restrict__ rp_list) {
+    int4 *__restrict__ rec) {
   __shared__ long long s_slo[16];
-  __shared__ long long s_red[kWaves * 4];
+  __shared__ long long s_red[kWaves * 3];
   __shared__ unsigned long long s_mm[kWaves * 2];
-  __shared__ unsigned s_cnt[kWaves * 3];
+  __shared__ unsigned s_cnt[kWaves * 4];
   if (threadIdx.x < 16) s_slo[threadIdx.x] = c.slo[threadIdx.x];
+
+  const size_t gt = (size_t)blockIdx.x * kBlock + threadIdx.x;
+  const size_t gs = (size_t)gridDim.x * kBlock;
+  // this step's histograms and look-back status words start at zero
+  for (size_t j = gt; j < clear_vec; j += gs) clear[j] = make_uint4(0, 0, 0, 0);
+  if (gt == 0) {
+    unsigned *w = reinterpret_cast<unsigned *>(ctl);
+    for (size_t k = 0; k < kCtlHeaderWords; ++k) w[k] = 0;
+    ctl->kstar = n;
+    for (int k = 0; k < CASCADE_INFO_LEN; ++k) info[k] = 0;
+    info[CASCADE_INFO_N_SLOT_LIST] = c.n_free;
+  }
   __syncthreads();
 
-  const int i = blockIdx.x * kBlock + threadIdx.x;
-  const bool live = i < n;
   bool bad = false;
   long long v_held = 0, v_need1 = 0, v_want1 = 0;
   unsigned long long bmin = ~0ull, bmax = 0;
-  int grp = 3;
-  bool is_rp = false;
+  unsigned c0 = 0, c1 = 0, c2 = 0;
 
   // free-list range check, spread over the grid
-  for (int j = i; j < c.n_free; j += gridDim.x * kBlock)
+  for (size_t j = gt; j < (size_t)c.n_free; j += gs)
     if ((unsigned)free_slots[j] >= (unsigned)c.num_blocks) bad = true;
 
-  if (live) {
+#pragma unroll
+  for (int it = 0; it < kEvalItems; ++it) {
+  const int i = (int)(blockIdx.x * kBlock * kEvalItems + it * kBlock + threadIdx.x);
+  if (i < n) {
     const unsigned cls = rq.slo_class[i], st = rq.state[i], qt = rq.queue_tier[i],
                    pt = rq.prefix_tier[i];
     const long long arr = rq.arrival_ns[i];
-    long long n_in = rq.n_in[i], n_out = rq.n_out_pred[i], n_pre = rq.n_prefix[i],
-              prog = rq.n_progress[i];
-    const long long row = (long long)ro[i + 1] - (long long)ro[i];
-    const long long bt = c.bt;
+    const int n_in_r = rq.n_in[i], n_out_r = rq.n_out_pred[i], n_pre_r = rq.n_prefix[i],
+              prog_r = rq.n_progress[i];
+    const int r0 = ro[i], r1 = ro[i + 1];
+    const unsigned bt = (unsigned)c.bt;
 
     // ---- domain rules of the request data
     if (i > 0 && rq.id[i] <= rq.id[i - 1]) bad = true;
-    if (i == 0 && ro[0] != 0) bad = true;
+    if (i == 0 && r0 != 0) bad = true;
     if (cls >= (unsigned)c.num_classes || st > 2 || qt > 2 || pt > 3) bad = true;
-    if (n_in < 1 || n_in > (1 << 17) || n_out < 0 || n_out > (1 << 17)) bad = true;
-    if (n_pre < 0 || n_pre > n_in - 1 || (n_pre % bt) != 0) bad = true;
+    if (n_in_r < 1 || n_in_r > (1 << 17) || n_out_r < 0 || n_out_r > (1 << 17)) bad = true;
+    if (n_pre_r < 0 || n_pre_r > n_in_r - 1 || ((unsigned)n_pre_r % bt) != 0) bad = true;
     if (arr < 0 || arr > c.t_now) bad = true;
-    long long want_row;
     if (st == CASCADE_QUEUED) {
-      if ((n_pre == 0) != (pt == CASCADE_KV_NONE) || prog != 0) bad = true;
-      want_row = 0;
+      if ((n_pre_r == 0) != (pt == CASCADE_KV_NONE) || prog_r != 0 || r1 != r0) bad = true;
     } else if (st == CASCADE_RUNNING_PREFILL) {
-      if (prog < 1 || prog > n_in - 1) bad = true;
-      want_row = (prog + bt - 1) / bt;
+      if (prog_r < 1 || prog_r > n_in_r - 1) bad = true;
+      else if ((long long)r1 - r0 != udiv_ceil((unsigned)prog_r, bt)) bad = true;
     } else {
-      if (prog < 0 || prog > (1 << 17)) bad = true;
-      want_row = (n_in + prog + bt - 1) / bt;
+      if (prog_r < 0 || prog_r > (1 << 17)) bad = true;
+      else if (n_in_r >= 1 && n_in_r <= (1 << 17) &&
+               (long long)r1 - r0 != udiv_ceil((unsigned)(n_in_r + prog_r), bt))
+        bad = true;
     }
-    if (row != want_row) bad = true;
 
     // ---- keep the arithmetic in range whatever the data
     const unsigned st_s = st > 2 ? 0u : st;
     const unsigned pt_s = pt > 3 ? 3u : pt;
     const unsigned cls_s = cls >= (unsigned)c.num_classes ? 0u : cls;
-    n_in = n_in < 1 ? 1 : (n_in > (1 << 17) ? (1 << 17) : n_in);
-    n_out = n_out < 0 ? 0 : (n_out > (1 << 17) ? (1 << 17) : n_out);
-    n_pre = n_pre < 0 ? 0 : (n_pre > n_in - 1 ? n_in - 1 : n_pre);
-    prog = prog < 0 ? 0 : (prog > (1 << 17) ? (1 << 17) : prog);
+    const long long n_in = n_in_r < 1 ? 1 : (n_in_r > (1 << 17) ? (1 << 17) : n_in_r);
+    const long long n_out = n_out_r < 0 ? 0 : (n_out_r > (1 << 17) ? (1 << 17) : n_out_r);
+    const long long n_pre = n_pre_r < 0 ? 0 : (n_pre_r > n_in - 1 ? n_in - 1 : n_pre_r);
+    const long long prog = prog_r < 0 ? 0 : (prog_r > (1 << 17) ? (1 << 17) : prog_r);
     const long long elapsed = (arr < 0 || arr > c.t_now) ? 0 : c.t_now - arr;
+    const long long row = (long long)r1 - r0;
     const long long held = row < 0 ? 0 : (row > 0xFFFFF ? 0xFFFFF : row);
 
     // ---- Section 4.2: actual-load and maximum-load estimates
@@ -190,7 +222,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
     if (st_s == CASCADE_QUEUED) {
       long long reuse = 0, rest = 0;
       if (pt_s != CASCADE_KV_NONE) {
-        pb = n_pre / bt;
+        pb = (unsigned)n_pre / bt;
         reuse = n_pre;
         if (deep) rest = restore_ns(pb, delta, blk);
       }
@@ -198,10 +230,10 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
       l_max = ns_of_ps(compute_ps(n_in - reuse, reuse, c.dmax, c)) + rest;
       base_need = (pt_s == CASCADE_KV_HBM) ? n_in - n_pre : n_in;
     } else if (st_s == CASCADE_RUNNING_PREFILL) {
-      const long long left = n_in - prog < 0 ? 0 : n_in - prog;
-      l_act = ns_of_ps(compute_ps(left, prog, c.d, c));
-      l_max = ns_of_ps(compute_ps(left, prog, c.dmax, c));
-      base_need = left;
+      const long long p = prog > n_in ? n_in : prog;
+      l_act = ns_of_ps(compute_ps(n_in - p, p, c.d, c));
+      l_max = ns_of_ps(compute_ps(n_in - p, p, c.dmax, c));
+      base_need = n_in - p;
     } else {
       const long long left = n_out - prog < 0 ? 0 : n_out - prog;
       l_act = ns_of_ps(left * (c.c_iter + (long long)c.d * c.c_dec));
@@ -226,28 +258,34 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
     if (st_s == CASCADE_QUEUED && deep) {
       long long x = 0;
       if (brem > delta) {
-        const long long m = (long long)((unsigned long long)(brem - delta) / (unsigned long long)blk);
+        const long long m =
+            (long long)((unsigned long long)(brem - delta) / (unsigned long long)blk);
         x = m < pb ? m : pb;
       }
       if (x > 0) {
         const long long all = ns_of_ps(compute_ps(n_in, 0, c.d, c));
-        const long long part = ns_of_ps(compute_ps(n_in - bt * x, bt * x, c.d, c));
+        const long long part = ns_of_ps(compute_ps(n_in - (long long)bt * x, bt * x, c.d, c));
         if (restore_ns(x, delta, blk) >= all - part) x = 0;
       }
       want = x;
     }
 
     // ---- priority group and key: group in bits 63..62, clamped budget + 2^61
-    grp = (st_s == CASCADE_DECODE) ? 0 : (tnew == 1 ? 1 : 2);
+    const int grp = (st_s == CASCADE_DECODE) ? 0 : (tnew == 1 ? 1 : 2);
     const long long lo = -(1ll << 61), hi = (1ll << 61) - 1;
     const long long cl = brem < lo ? lo : (brem > hi ? hi : brem);
     const unsigned long long biased = (unsigned long long)(cl + (1ll << 61));
-    bmin = bmax = biased;
+    bmin = biased < bmin ? biased : bmin;
+    bmax = biased > bmax ? biased : bmax;
+    c0 += grp == 0;
+    c1 += grp == 1;
+    c2 += grp == 2;
 
     // spill of a running prefill fits its budget (Section 4.4)
     const int offl = (st_s == CASCADE_RUNNING_PREFILL) &&
                      (restore_ns(held, c.delta1, c.blk1) <= brem);
-    const int decnb = (st_s == CASCADE_DECODE) && ((n_in + prog + 1 + bt - 1) / bt - held) > 0;
+    const int decnb = (st_s == CASCADE_DECODE) &&
+                      ((long long)udiv_ceil((unsigned)(n_in + prog + 1), bt) - held) > 0;
     const long long reuse_tok = (st_s == CASCADE_RUNNING_PREFILL)
                                     ? prog
                                     : ((st_s == CASCADE_QUEUED && pt_s == CASCADE_KV_HBM) ? n_pre : 0);
@@ -258,33 +296,19 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
     rec[i] = make_int4((int)want, (int)base_need, (int)reuse_tok,
                        (int)held | ((int)st_s << 20) | ((int)pt_s << 22) | (grp << 24) |
                            (offl << 26) | (decnb << 27));
-    is_rp = (st_s == CASCADE_RUNNING_PREFILL);
-    if (is_rp) v_held = held;
+    if (st_s == CASCADE_RUNNING_PREFILL) v_held += held;
     if (grp <= 1) {
-      v_need1 = base_need;
-      v_want1 = want;
+      v_need1 += base_need;
+      v_want1 += want;
     }
   }
-
-  if (__syncthreads_or(bad ? 1 : 0)) {
-    if (threadIdx.x == 0) set_status(info, CASCADE_EINVAL);
   }
 
-  // running-prefill list (wave-aggregated append)
-  const uint64_t rpm = __ballot(is_rp);
-  if (rpm) {
-    unsigned base = 0;
-    if (lane_id() == __builtin_ctzll(rpm))
-      base = atomicAdd(&ctl->rp_count, (unsigned)__builtin_popcountll(rpm));
-    base = __shfl(base, __builtin_ctzll(rpm), 64);
-    if (is_rp) rp_list[base + rank_in_mask(rpm)] = i;
-  }
-
-  // workgroup reductions, one atomic each
+  // workgroup totals, one plain store per workgroup
   long long sums[3] = {v_held, v_need1, v_want1};
   block_sum<3>(sums, s_red);
-  unsigned cnt[3] = {grp == 0 ? 1u : 0u, grp == 1 ? 1u : 0u, grp == 2 ? 1u : 0u};
-  block_sum<3>(cnt, s_cnt);
+  unsigned cnt[4] = {c0, c1, c2, bad ? 1u : 0u};
+  block_sum<4>(cnt, s_cnt);
   for (int o = 32; o >= 1; o >>= 1) {
     const unsigned long long a = __shfl_xor(bmin, o, 64), b = __shfl_xor(bmax, o, 64);
     bmin = a < bmin ? a : bmin;
@@ -296,146 +320,238 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    unsigned long long mn = ~0ull, mx = 0;
+    Partial pt;
+    pt.held = sums[0];
+    pt.need1 = sums[1];
+    pt.want1 = sums[2];
+    pt.bmin = ~0ull;
+    pt.bmax = 0;
     for (int w = 0; w < kWaves; ++w) {
-      mn = s_mm[2 * w] < mn ? s_mm[2 * w] : mn;
-      mx = s_mm[2 * w + 1] > mx ? s_mm[2 * w + 1] : mx;
+      pt.bmin = s_mm[2 * w] < pt.bmin ? s_mm[2 * w] : pt.bmin;
+      pt.bmax = s_mm[2 * w + 1] > pt.bmax ? s_mm[2 * w + 1] : pt.bmax;
     }
-    if (sums[0]) atomicAdd((unsigned long long *)&ctl->held_rp, (unsigned long long)sums[0]);
-    if (sums[1]) atomicAdd((unsigned long long *)&ctl->need1, (unsigned long long)sums[1]);
-    if (sums[2]) atomicAdd((unsigned long long *)&ctl->want1, (unsigned long long)sums[2]);
-    for (int k = 0; k < 3; ++k)
-      if (cnt[k]) atomicAdd(&ctl->cnt[k], cnt[k]);
-    if (mn <= mx) {
-      atomicMin(&ctl->bmin, mn);
-      atomicMax(&ctl->bmax, mx);
-    }
+    pt.c0 = cnt[0];
+    pt.c1 = cnt[1];
+    pt.c2 = cnt[2];
+    pt.bad = cnt[3];
+    pt.pad[0] = pt.pad[1] = 0;
+    partials[blockIdx.x] = pt;
   }
 }
 
 // ------------------------------------------------------ sort: digit plan
 
-struct Plan {
-  unsigned long long span;  // bmax - bmin + 1
-  int digits;               // 8-bit digits of the compressed key
-};
-__device__ __forceinline__ Plan make_plan(const Ctl *ctl) {
-  Plan p;
-  const unsigned long long mn = ctl->bmin, mx = ctl->bmax;
-  p.span = mx - mn + 1;
-  const unsigned long long gmax = ctl->cnt[2] ? 2 : (ctl->cnt[1] ? 1 : 0);
-  const unsigned long long top = gmax * p.span + (mx - mn);
+// Width of the compressed key key' = group*span + (biased - bmin).
+__device__ __forceinline__ int key_digits(unsigned long long mn, unsigned long long mx,
+                                          unsigned c1, unsigned c2) {
+  const unsigned long long span = mx - mn + 1;
+  const unsigned long long gmax = c2 ? 2 : (c1 ? 1 : 0);
+  const unsigned long long top = gmax * span + (mx - mn);
   const int bits = top ? 64 - __builtin_clzll(top) : 0;
-  p.digits = (bits + 7) / 8;
-  return p;
+  return (bits + 7) / 8;
 }
 
-// True when digit d has one value for all n keys (the pass keeps the order).
-__device__ __forceinline__ bool digit_constant(const Ctl *ctl, int d, int n) {
-  int hit = 0;
-  for (int b = threadIdx.x; b < kRadix; b += kBlock) hit |= (ctl->hist[d][b] == (unsigned)n);
-  return __syncthreads_or(hit) != 0;
-}
-
-// Number of data-moving passes among digits < upto (selects the ping-pong
-// buffer).
-__device__ __forceinline__ int moving_passes(const Ctl *ctl, const Plan &pl, int upto, int n) {
-  int m = 0;
-  for (int d = 0; d < upto && d < pl.digits; ++d) m += digit_constant(ctl, d, n) ? 0 : 1;
-  return m;
+// Sort plan: the digits that move data (below the key width, not constant
+// over all n keys), as a bit mask.  Every radix and scan workgroup derives it
+// from the histograms; hv holds thread t's bucket t of every digit.
+__device__ __forceinline__ unsigned plan_mask(const unsigned (&hv)[kMaxDigits], int n, int nd,
+                                              unsigned *s_mask) {
+  unsigned constant = 0;
+#pragma unroll
+  for (int d = 0; d < kMaxDigits; ++d) constant |= (hv[d] == (unsigned)n ? 1u : 0u) << d;
+  if (constant) atomicOr(s_mask, constant);
+  __syncthreads();
+  return ((1u << nd) - 1u) & ~*s_mask;
 }
 
 // ---------------------------------------------------------------- prep
 
-// Order-preserving key compression: key' = group * span + (biased - bmin),
-// then one read of the keys builds every digit's histogram.  Also checks the
-// block-table slots, whose extent is only trustworthy after eval.
-__global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks,
+// Totals of eval's partials; order-preserving key compression
+// key' = group * span + (biased - bmin), then one read of the keys builds
+// every digit's histogram (per-thread runs of equal digits are merged before
+// the LDS atomics, so low-entropy high digits do not serialise).  Also checks
+// the block-table slots, whose extent is only trustworthy after eval.
+__global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int n_partials,
+                                                      const Partial *__restrict__ partials,
                                                       const int *__restrict__ ro,
                                                       const int *__restrict__ slots, Ctl *ctl,
                                                       int *info,
                                                       unsigned long long *__restrict__ keys,
                                                       unsigned *__restrict__ vals) {
   __shared__ unsigned s_hist[kMaxDigits][kRadix];
-  if (status_failed(info)) return;
+  __shared__ long long s_red[kWaves * 3];
+  __shared__ unsigned s_cnt[kWaves * 4];
+  __shared__ unsigned long long s_mm[kWaves * 2];
+  long long sums[3] = {0, 0, 0};
+  unsigned cnt[4] = {0, 0, 0, 0};
+  unsigned long long mn = ~0ull, mx = 0;
+  for (int j = threadIdx.x; j < n_partials; j += kBlock) {
+    const Partial p = partials[j];
+    sums[0] += p.held;
+    sums[1] += p.need1;
+    sums[2] += p.want1;
+    cnt[0] += p.c0;
+    cnt[1] += p.c1;
+    cnt[2] += p.c2;
+    cnt[3] += p.bad;
+    mn = p.bmin < mn ? p.bmin : mn;
+    mx = p.bmax > mx ? p.bmax : mx;
+  }
+  block_sum<3>(sums, s_red);
+  block_sum<4>(cnt, s_cnt);
+  for (int o = 32; o >= 1; o >>= 1) {
+    const unsigned long long a = __shfl_xor(mn, o, 64), b = __shfl_xor(mx, o, 64);
+    mn = a < mn ? a : mn;
+    mx = b > mx ? b : mx;
+  }
+  if (lane_id() == 0) {
+    s_mm[wave_id() * 2] = mn;
+    s_mm[wave_id() * 2 + 1] = mx;
+  }
+  __syncthreads();
+  mn = ~0ull;
+  mx = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    mn = s_mm[2 * w] < mn ? s_mm[2 * w] : mn;
+    mx = s_mm[2 * w + 1] > mx ? s_mm[2 * w + 1] : mx;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    ctl->bmin = mn;
+    ctl->bmax = mx;
+    ctl->held_rp = sums[0];
+    ctl->need1 = sums[1];
+    ctl->want1 = sums[2];
+    ctl->cnt[0] = cnt[0];
+    ctl->cnt[1] = cnt[1];
+    ctl->cnt[2] = cnt[2];
+    if (cnt[3]) set_status(info, CASCADE_EINVAL);
+  }
+  if (cnt[3]) return;  // bad request data: nothing below is meaningful
+
   const int nnz = ro[n];
   bool bad = false;
-  for (int j = blockIdx.x * kBlock + threadIdx.x; j < nnz; j += gridDim.x * kBlock)
-    if ((unsigned)slots[j] >= (unsigned)num_blocks) bad = true;
+  {
+    const int gt = blockIdx.x * kBlock + threadIdx.x, gs = gridDim.x * kBlock;
+    for (int j0 = gt; j0 < nnz; j0 += 8 * gs) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = (j0 + u * gs < nnz) ? slots[j0 + u * gs] : 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if ((unsigned)v[u] >= (unsigned)num_blocks) bad = true;
+    }
+  }
   if (__syncthreads_or(bad ? 1 : 0)) {
     if (threadIdx.x == 0) set_status(info, CASCADE_EINVAL);
   }
 
-  const Plan pl = make_plan(ctl);
-  const unsigned long long mn = ctl->bmin;
+  const int nd = key_digits(mn, mx, cnt[1], cnt[2]);
+  const unsigned long long span = mx - mn + 1;
   for (int t = threadIdx.x; t < kMaxDigits * kRadix; t += kBlock) (&s_hist[0][0])[t] = 0;
-  __syncthreads();
   const int base = blockIdx.x * kBlock * kPrepItems;
-#pragma unroll 4
+  unsigned long long kv[kPrepItems];
+#pragma unroll
+  for (int j = 0; j < kPrepItems; ++j) {  // every load in flight before any use
+    const int idx = base + j * kBlock + threadIdx.x;
+    kv[j] = idx < n ? keys[idx] : 0ull;
+  }
+  __syncthreads();
+#pragma unroll
   for (int j = 0; j < kPrepItems; ++j) {
     const int idx = base + j * kBlock + threadIdx.x;
     if (idx < n) {
-      const unsigned long long k0 = keys[idx];
-      const unsigned long long k =
-          (k0 >> 62) * pl.span + ((k0 & ((1ull << 62) - 1)) - mn);
+      const unsigned long long k0 = kv[j];
+      const unsigned long long k = (k0 >> 62) * span + ((k0 & ((1ull << 62) - 1)) - mn);
       keys[idx] = k;
       vals[idx] = (unsigned)idx;
-      for (int d = 0; d < pl.digits; ++d) atomicAdd(&s_hist[d][(k >> (8 * d)) & 255], 1u);
+      for (int d = 0; d < nd; ++d) atomicAdd(&s_hist[d][(k >> (8 * d)) & 255], 1u);
     }
   }
   __syncthreads();
-  for (int d = 0; d < pl.digits; ++d) {
+  for (int d = 0; d < nd; ++d) {
     const unsigned v = s_hist[d][threadIdx.x];
     if (v) atomicAdd(&ctl->hist[d][threadIdx.x], v);
   }
+
 }
 
 // ---------------------------------------------------------- radix pass
 
-// One stable LSD pass over 8 bits.  A tile of kSortTile keys is ranked per
-// wave with ballots (lanes holding the same digit find each other in 8
-// ballots), per-digit tile counts are published for the decoupled look-back,
-// keys are reordered in LDS and written out in runs of equal digits.
+// The k-th data-moving LSD pass (kK), over the digit the sort plan names.
+// A tile of kSortTile keys is ranked per wave with ballots (lanes holding the
+// same digit find each other in 8 ballots), per-digit tile counts are
+// published for the decoupled look-back, keys are reordered in LDS and written
+// out in runs of equal digits.  The k-th pass reads buffer k & 1, so the tile's
+// keys are requested at once for tile = blockIdx.x, in parallel with the tile
+// claim and the plan; a workgroup that claims another tile reloads.
+template <int kK>
 __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
-    int pass, int n, Ctl *ctl, int *info, unsigned long long *keys_a,
-    unsigned long long *keys_b, unsigned *vals_a, unsigned *vals_b, unsigned *status) {
+    int n, Ctl *ctl, int *info, unsigned long long *keys_a, unsigned long long *keys_b,
+    unsigned *vals_a, unsigned *vals_b, unsigned *status) {
   __shared__ unsigned long long s_keys[kSortTile];
   __shared__ unsigned s_vals[kSortTile];
   __shared__ unsigned s_wcnt[kWaves][kRadix];
   __shared__ int s_start[kRadix];
   __shared__ int s_off[kRadix];
   __shared__ int s_scan[kWaves * 2];
-  __shared__ int s_tile;
+  __shared__ int s_tile, s_bad;
+  __shared__ unsigned s_mask;
 
-  if (status_failed(info)) return;
-  const Plan pl = make_plan(ctl);
-  if (pass >= pl.digits) return;
-  if (digit_constant(ctl, pass, n)) return;
-  const int parity = moving_passes(ctl, pl, pass, n) & 1;
-  const unsigned long long *src_k = parity ? keys_b : keys_a;
-  unsigned long long *dst_k = parity ? keys_a : keys_b;
-  const unsigned *src_v = parity ? vals_b : vals_a;
-  unsigned *dst_v = parity ? vals_a : vals_b;
-
-  if (threadIdx.x == 0) s_tile = (int)atomicAdd(&ctl->tile_ctr[pass], 1u);
-  for (int t = threadIdx.x; t < kWaves * kRadix; t += kBlock) (&s_wcnt[0][0])[t] = 0;
-  __syncthreads();
-  const int tile = s_tile;
-  const int shift = 8 * pass;
+  const unsigned long long *src_k = (kK & 1) ? keys_b : keys_a;
+  unsigned long long *dst_k = (kK & 1) ? keys_a : keys_b;
+  const unsigned *src_v = (kK & 1) ? vals_b : vals_a;
+  unsigned *dst_v = (kK & 1) ? vals_a : vals_b;
   const int lane = lane_id(), wave = wave_id();
-  const int tile_base = tile * kSortTile;
+  const int local = wave * 64 * kSortItems + lane;
 
   unsigned long long key[kSortItems];
   unsigned val[kSortItems];
   int dig[kSortItems], rank[kSortItems];
+  {
+    const int g0 = (int)blockIdx.x * kSortTile + local;
 #pragma unroll
-  for (int j = 0; j < kSortItems; ++j) {
-    const int g = tile_base + wave * 64 * kSortItems + j * 64 + lane;
-    const bool v = g < n;
-    key[j] = v ? src_k[g] : 0ull;
-    val[j] = v ? src_v[g] : 0u;
-    dig[j] = v ? (int)((key[j] >> shift) & 255) : -1;
+    for (int j = 0; j < kSortItems; ++j) {
+      const int g = g0 + j * 64;
+      key[j] = g < n ? src_k[g] : 0ull;
+      val[j] = g < n ? src_v[g] : 0u;
+    }
   }
+  unsigned hv[kMaxDigits];
+#pragma unroll
+  for (int d = 0; d < kMaxDigits; ++d) hv[d] = ctl->hist[d][threadIdx.x];
+  if (threadIdx.x == 0) {
+    // a claimed tile of a pass that turns out idle is never waited on
+    s_tile = (int)atomicAdd(&ctl->tile_ctr[kK], 1u);
+    s_bad = bad_status(load_agent(info));
+    s_mask = 0;
+  }
+  const int nd = key_digits(ctl->bmin, ctl->bmax, ctl->cnt[1], ctl->cnt[2]);
+  for (int t = threadIdx.x; t < kWaves * kRadix; t += kBlock) (&s_wcnt[0][0])[t] = 0;
+  __syncthreads();
+  const unsigned active = plan_mask(hv, n, nd, &s_mask);
+  if (s_bad || __builtin_popcount(active) <= kK) return;
+  // this pass sorts by the kK-th data-moving digit
+  unsigned rest = active;
+#pragma unroll
+  for (int k = 0; k < kK; ++k) rest &= rest - 1;
+  const int digit = __builtin_ctz(rest);
+  unsigned gcount = 0;
+#pragma unroll
+  for (int d = 0; d < kMaxDigits; ++d) gcount = d == digit ? hv[d] : gcount;
+  const int tile = s_tile;
+  const int tile_base = tile * kSortTile;
+  if (tile != (int)blockIdx.x) {
+#pragma unroll
+    for (int j = 0; j < kSortItems; ++j) {
+      const int g = tile_base + local + j * 64;
+      key[j] = g < n ? src_k[g] : 0ull;
+      val[j] = g < n ? src_v[g] : 0u;
+    }
+  }
+  const int shift = 8 * digit;
+#pragma unroll
+  for (int j = 0; j < kSortItems; ++j)
+    dig[j] = (tile_base + local + j * 64 < n) ? (int)((key[j] >> shift) & 255) : -1;
   // rank within the wave, item by item (local order: wave, item, lane)
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
@@ -472,14 +588,14 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   bool timed_out = false;
   publish<unsigned>(st + t, tile_count, tile == 0 ? kFlagInclusive : kFlagAggregate);
 
-  // exclusive scans over digits: tile-local starts and global bases
-  int v2[2] = {(int)tile_count, (int)ctl->hist[pass][t]};
+  // exclusive scans over digits: tile-local starts and global bucket bases
+  int v2[2] = {(int)tile_count, (int)gcount};
   int tot2[2];
   block_exclusive_scan<2>(v2, tot2, s_scan);
   s_start[t] = v2[0];
   unsigned prefix = 0;
   if (tile > 0) {
-    prefix = look_back<unsigned, kLookWin>(status, kRadix, tile, t, &timed_out);
+    prefix = look_back<unsigned, kSortWin>(status, kRadix, tile, t, &timed_out);
     publish<unsigned>(st + t, prefix + tile_count, kFlagInclusive);
   }
   if (timed_out) set_status(info, CASCADE_ETIMEOUT);
@@ -516,6 +632,241 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
 
 // ---------------------------------------------------------------- scan
 
+// Look-back of K values with a window of WIN predecessors per round trip,
+// spread over K*WIN threads; the sums land in s_sum[0..K).
+template <int K, int WIN>
+__device__ __forceinline__ void block_look_back(const unsigned long long *status, int stride,
+                                                int tile, long long *s_sum, int *s_base,
+                                                unsigned long long *s_w, int *s_left,
+                                                bool *timed_out) {
+  static_assert(K * WIN <= kBlock, "window too wide");
+  const int t = threadIdx.x;
+  if (t < K) {
+    s_base[t] = tile - 1;
+    s_sum[t] = 0;
+  }
+  if (t == 0) *s_left = K;
+  __syncthreads();
+  unsigned spins = 0;
+  while (true) {
+    const int k = t / WIN, j = t - (t / WIN) * WIN;
+    if (k < K && s_base[k] >= 0) {
+      const int src = s_base[k] - j;
+      s_w[k * WIN + j] = src >= 0 ? load_agent(status + (size_t)src * stride + k)
+                                  : (unsigned long long)kFlagInclusive;
+    }
+    __syncthreads();
+    bool stalled = false;
+    if (t < K && s_base[t] >= 0) {
+      long long sum = s_sum[t];
+      int consumed = 0;
+      bool done = false;
+      for (int jj = 0; jj < WIN && !done && !stalled; ++jj) {
+        const unsigned long long w = s_w[t * WIN + jj];
+        const unsigned f = (unsigned)(w & 3);
+        if (f == 0) {
+          stalled = true;
+        } else {
+          sum += (long long)(w >> 2);
+          ++consumed;
+          done = (f == kFlagInclusive);
+        }
+      }
+      s_sum[t] = sum;
+      s_base[t] = done ? -1 : s_base[t] - consumed;
+      if (done) atomicSub(s_left, 1);
+    }
+    __syncthreads();
+    if (*s_left == 0) break;
+    if (__syncthreads_or(stalled ? 1 : 0)) {
+      if (++spins > kSpinLimit) {
+        *timed_out = true;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+  __syncthreads();
+}
+
+// The victims, slot list and move lists, computed by the last scan workgroup
+// once every tile's totals and per-holder prefixes are in memory.
+// Budget-aware preemption (Algorithm 1; Section 4.4): the deficit
+// D = new blocks of admitted requests - free blocks is covered by the
+// non-admitted running prefills taken from the back of the order (largest
+// remaining budget first): a holder at position p is preempted iff the
+// eligible blocks behind it are fewer than D.
+constexpr int kFreeCap = 4096;    // free-list entries staged in LDS by the finishing workgroup
+
+struct FinishLds {
+  long long tot[kWaves * 6];
+  int v_req[kVictimCap], v_held[kVictimCap], v_row0[kVictimCap], v_start[kVictimCap];
+  long long v_sbase[kVictimCap], v_pbase[kVictimCap];
+  int v_total;
+  RestoreEnt rl[kRestoreCap];
+  int free_slots[kFreeCap];
+  int n_victims, counts[2];
+};
+
+// Loads are grouped so that the workgroup waits on memory three times: the
+// totals, running-prefill records, restore list and free list together; the
+// victims' rows; the slot-list entries of restores past the free list.
+__device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_tiles, int n_rp,
+                            const TileTot *__restrict__ tiles, const int *__restrict__ free_slots,
+                            const RpInfo *__restrict__ rp, const RestoreEnt *__restrict__ rl,
+                            const int *__restrict__ slots, const Outs &o, FinishLds &L) {
+  const int t = threadIdx.x;
+  if (t == 0) {
+    L.n_victims = 0;
+    L.counts[0] = L.counts[1] = 0;
+  }
+  long long tot[6] = {0, 0, 0, 0, 0, 0};
+  for (int j = t; j < n_tiles; j += kBlock) {
+    const TileTot tt = tiles[j];
+    tot[0] += tt.adm_nb;
+    tot[1] += tt.elig_h;
+    tot[2] += tt.elig_offl_h;
+    tot[3] += tt.n_adm;
+    tot[4] += tt.n_unpack;
+    tot[5] += tt.n_restore;
+  }
+  RpInfo mine = {};
+  const bool has_rp = t < n_rp;
+  if (has_rp) mine = rp[t];
+  for (int j = t; j < n_free && j < kFreeCap; j += kBlock) L.free_slots[j] = free_slots[j];
+  // the restore list holds tot[5] entries (not known yet) in a buffer of n;
+  // stage a bounded prefix now, use only its valid part below
+  for (int j = t; j < kRestoreCap && j < n; j += kBlock) L.rl[j] = rl[j];
+  const int kstar = ctl->kstar;
+  const long long kx = ctl->kx, ky = ctl->ky, kz = ctl->kz, kzp = ctl->kzp;
+  block_sum<6>(tot, L.tot);  // waits for the loads above
+  const long long D = tot[0] - n_free, E = tot[1], EO = tot[2];
+  const long long nu = tot[4];
+  const int nr = (int)tot[5];
+  const int lim = min(n_free, o.sl_cap);
+  for (int j = t; j < lim; j += kBlock)
+    o.slot_list[j] = j < kFreeCap ? L.free_slots[j] : free_slots[j];
+
+  // victims: every thread tests one running prefill at a time
+  if (D > 0) {
+    for (int e = t; e < n_rp; e += kBlock) {
+      const RpInfo ri = e == t ? mine : rp[e];
+      if (!ri.eligible) continue;
+      const long long eh = ri.pos < kstar ? ri.x : kx + ri.y - ky;
+      const long long after = E - eh;  // eligible blocks behind this request
+      if (after >= D) continue;
+      if (after < 0) {
+        set_status(info, CASCADE_EINTERNAL);
+        continue;
+      }
+      const int i = ri.req, h = ri.held;
+      o.action[i] = ri.offl ? CASCADE_ACT_PREEMPT_OFFLOAD : CASCADE_ACT_PREEMPT_DROP;
+      atomicAdd(&L.counts[0], h);
+      if (ri.offl) atomicAdd(&L.counts[1], h);
+      const long long sbase = (long long)n_free + after;
+      const long long pbase = ri.offl ? EO - (ri.pos < kstar ? ri.z : kz + ri.zp - kzp) : -1;
+      const int v = atomicAdd(&L.n_victims, 1);
+      if (v < kVictimCap) {
+        L.v_req[v] = i;
+        L.v_held[v] = h;
+        L.v_row0[v] = ri.row0;
+        L.v_sbase[v] = sbase;
+        L.v_pbase[v] = pbase;
+      } else {  // more victims than LDS holds: copy this one alone
+        for (int b = 0; b < h; ++b) {
+          const int slot = slots[ri.row0 + b];
+          if (sbase + b < o.sl_cap) o.slot_list[sbase + b] = slot;
+          if (pbase >= 0 && pbase + b < o.pack_cap) {
+            cascade_move_t m;
+            m.req = i;
+            m.blk = b;
+            m.pool_slot = slot;
+            m.staging_slot = (int)(pbase + b);
+            o.pack[pbase + b] = m;
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // the staged victims' rows as one flat index space (prefix of row lengths),
+  // so every row load of every victim is in flight at once
+  const int nv = min(L.n_victims, kVictimCap);
+  if (t == 0) {
+    int acc = 0;
+    for (int v = 0; v < nv; ++v) {
+      L.v_start[v] = acc;
+      acc += L.v_held[v];
+    }
+    L.v_total = acc;
+  }
+  __syncthreads();
+  for (int m0 = t; m0 < L.v_total; m0 += 4 * kBlock) {
+    int slot[4], vi[4], bi[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int m = m0 + u * kBlock;
+      vi[u] = -1;
+      if (m < L.v_total) {
+        int lo = 0, hi = nv - 1;
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (L.v_start[mid] <= m) lo = mid; else hi = mid - 1;
+        }
+        vi[u] = lo;
+        bi[u] = m - L.v_start[lo];
+        slot[u] = slots[L.v_row0[lo] + bi[u]];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (vi[u] < 0) continue;
+      const int v = vi[u], b = bi[u];
+      const long long sb = L.v_sbase[v] + b, pb = L.v_pbase[v];
+      if (sb < o.sl_cap) o.slot_list[sb] = slot[u];
+      if (pb >= 0 && pb + b < o.pack_cap) {
+        cascade_move_t mv;
+        mv.req = L.v_req[v];
+        mv.blk = b;
+        mv.pool_slot = slot[u];
+        mv.staging_slot = (int)(pb + b);
+        o.pack[pb + b] = mv;
+      }
+    }
+  }
+  __syncthreads();  // the slot list is complete (this workgroup wrote it)
+  // restore moves: the first r new blocks of each RESTORE request, staged in
+  // admitted order; move m finds its request by binary search
+  const long long mlim = lmin(nu, (long long)o.unpack_cap);
+  for (long long m = t; m < mlim; m += kBlock) {
+    int lo = 0, hi = nr - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      const int off = mid < kRestoreCap ? L.rl[mid].stage_off : rl[mid].stage_off;
+      if (off <= m) lo = mid; else hi = mid - 1;
+    }
+    const RestoreEnt e = lo < kRestoreCap ? L.rl[lo] : rl[lo];
+    const int b = (int)(m - e.stage_off);
+    const long long s = (long long)e.alloc_off + b;
+    cascade_move_t mv;
+    mv.req = e.req;
+    mv.blk = b;
+    mv.pool_slot = s >= o.sl_cap ? -1 : (s < n_free && s < kFreeCap ? L.free_slots[s]
+                                                                       : o.slot_list[s]);
+    mv.staging_slot = (int)m;
+    o.unpack[m] = mv;
+  }
+  if (t == 0) {
+    const long long nsl = (long long)n_free + L.counts[0];
+    info[CASCADE_INFO_N_ADMITTED] = (int)tot[3];
+    info[CASCADE_INFO_N_SLOT_LIST] = (int)nsl;
+    info[CASCADE_INFO_N_UNPACK] = (int)nu;
+    info[CASCADE_INFO_N_PACK] = L.counts[1];
+    const bool full = nsl > o.sl_cap || nu > o.unpack_cap || L.counts[1] > o.pack_cap;
+    if (full && load_agent(info) == CASCADE_OK) set_status(info, CASCADE_ENOSPC);
+  }
+}
+
 // Algorithm 1's Phase 2 loop in priority order as prefix sums.
 // Level 1 (independent of earlier decisions): restore want, base token need,
 // blocks held by running prefills (all / spill-fits).  They give the restore
@@ -526,25 +877,45 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
 // out (all / spill-fits), restored blocks and restoring requests.
 // Both levels use one decoupled look-back each, chained inside the launch.
 __global__ __launch_bounds__(kBlock) void scan_kernel(
-    int n, Consts c, Ctl *ctl, int *info, const unsigned *vals_a, const unsigned *vals_b,
-    const int4 *__restrict__ rec, int *__restrict__ order_out, int *__restrict__ granted_out,
-    int *__restrict__ restore_out, int *__restrict__ alloc_begin, int *__restrict__ alloc_count,
-    uint8_t *__restrict__ action_out, int *__restrict__ admitted_out, RpInfo *__restrict__ rp_info,
-    RestoreEnt *__restrict__ restore_list, unsigned long long *status1,
-    unsigned long long *status2) {
+    int n, int passes, Consts c, Ctl *ctl, int *info, const unsigned *vals_a,
+    const unsigned *vals_b, const int4 *__restrict__ rec, const int *__restrict__ ro,
+    const int *__restrict__ slots, const int *__restrict__ free_slots, Outs o,
+    RpInfo *__restrict__ rp_list, RestoreEnt *__restrict__ restore_list,
+    TileTot *__restrict__ tile_tot, unsigned long long *status1, unsigned long long *status2) {
   __shared__ long long s_scan[kWaves * kL2];
-  __shared__ long long s_pre[kL2Stride];
-  __shared__ int s_tile;
+  __shared__ long long s_sum[kL2Stride];
+  __shared__ int s_base[kL2Stride];
+  __shared__ unsigned long long s_w[kBlock];
+  __shared__ int s_left;
+  __shared__ int s_tile, s_bad, s_last;
+  __shared__ unsigned s_mask;
+  __shared__ FinishLds s_fin;
 
-  if (status_failed(info)) return;
+  // the tile's order entries are requested from both ping-pong buffers at once
+  // (which one holds the result is known only from the plan)
+  const int p0g = (int)blockIdx.x * kScanTile + threadIdx.x * kScanItems;
+  unsigned oa[kScanItems], ob[kScanItems];
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    oa[j] = p0g + j < n ? vals_a[p0g + j] : 0u;
+    ob[j] = p0g + j < n ? vals_b[p0g + j] : 0u;
+  }
+  unsigned hv[kMaxDigits];
+#pragma unroll
+  for (int d = 0; d < kMaxDigits; ++d) hv[d] = ctl->hist[d][threadIdx.x];
   if (threadIdx.x == 0) {
     s_tile = (int)atomicAdd(&ctl->tile_ctr[kMaxDigits], 1u);
+    s_bad = bad_status(load_agent(info));
+    s_mask = 0;
   }
-  const Plan pl = make_plan(ctl);
-  const int par = moving_passes(ctl, pl, pl.digits, n) & 1;
+  const int nd = key_digits(ctl->bmin, ctl->bmax, ctl->cnt[1], ctl->cnt[2]);
   __syncthreads();
+  const int nact = __builtin_popcount(plan_mask(hv, n, nd, &s_mask));
+  if (s_bad) return;
   const int tile = s_tile;
-  const unsigned *sorted = par ? vals_b : vals_a;
+  // a live digit beyond the launched passes would leave the keys unsorted
+  bool broken = nact > passes;
+  const unsigned *sorted = (nact & 1) ? vals_b : vals_a;
   const long long bt = c.bt, U = c.max_move;
   const long long e1 = (long long)ctl->cnt[0] + ctl->cnt[1];
   const bool has2 = ctl->cnt[2] != 0;
@@ -552,7 +923,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   const long long cap1 = cap - (has2 ? ((cap * c.rho_q16) >> 16) : 0);
   const long long p_e1 = ctl->need1 - bt * lmin(ctl->want1, U);  // tokens before Tier-2
   const long long g1 = lmin(p_e1, cap1);                           // granted to decode+Tier-1
-  const long long fh = (long long)c.n_free + ctl->held_rp;        // F + H
+  const long long fh = (long long)c.n_free + ctl->held_rp;         // F + H
 
   const int p0 = tile * kScanTile + threadIdx.x * kScanItems;
   int idx[kScanItems];
@@ -560,9 +931,10 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     const int p = p0 + j;
-    int ix = p < n ? (int)sorted[p] : -1;
+    int ix = -1;
+    if (p < n) ix = (int)(tile == (int)blockIdx.x ? ((nact & 1) ? ob[j] : oa[j]) : sorted[p]);
     if (ix >= n) {  // cannot happen with a correct sort; never read out of range
-      set_status(info, CASCADE_EINTERNAL);
+      broken = true;
       ix = -1;
     }
     idx[j] = ix;
@@ -570,15 +942,17 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   }
 
   // ---- level 1
-  long long l1[kL1] = {0, 0, 0, 0}, t1[kL1];
+  long long l1[kL1] = {0, 0, 0, 0, 0}, t1[kL1];
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     const int w = r4[j].w;
-    const long long h = rec_state(w) == CASCADE_RUNNING_PREFILL ? rec_held(w) : 0;
+    const bool rp = idx[j] >= 0 && rec_state(w) == CASCADE_RUNNING_PREFILL;
+    const long long h = rp ? rec_held(w) : 0;
     l1[0] += r4[j].x;
     l1[1] += r4[j].y;
     l1[2] += h;
     l1[3] += rec_offl(w) ? h : 0;
+    l1[4] += rp ? 1 : 0;          // running prefills (their compact list)
   }
   block_exclusive_scan<kL1>(l1, t1, s_scan);
   bool timed_out = false;
@@ -586,19 +960,20 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   if (threadIdx.x < kL1)
     publish<unsigned long long>(st1 + threadIdx.x, (unsigned long long)t1[threadIdx.x],
                                 tile == 0 ? kFlagInclusive : kFlagAggregate);
-  if (threadIdx.x < kL1) {
-    long long pre = 0;
-    if (tile > 0) {
-      pre = (long long)look_back<unsigned long long, kLookWin>(status1, kL1, tile,
-                                                                threadIdx.x, &timed_out);
-      publish<unsigned long long>(st1 + threadIdx.x, (unsigned long long)(pre + t1[threadIdx.x]),
+  if (tile > 0) {
+    block_look_back<kL1, kBlock / kL1>(status1, kL1, tile, s_sum, s_base, s_w, &s_left,
+                                       &timed_out);
+    if (threadIdx.x < kL1)
+      publish<unsigned long long>(st1 + threadIdx.x,
+                                  (unsigned long long)(s_sum[threadIdx.x] + t1[threadIdx.x]),
                                   kFlagInclusive);
-    }
-    s_pre[threadIdx.x] = pre;
+  } else {
+    if (threadIdx.x < kL2Stride) s_sum[threadIdx.x] = 0;
+    __syncthreads();
   }
-  __syncthreads();
-  long long wx = s_pre[0] + l1[0], bn = s_pre[1] + l1[1], yy = s_pre[2] + l1[2],
-            zz = s_pre[3] + l1[3];
+  long long wx = s_sum[0] + l1[0], bn = s_sum[1] + l1[1], yy = s_sum[2] + l1[2],
+            zz = s_sum[3] + l1[3];
+  int rp_at = (int)(s_sum[4] + l1[4]);
   __syncthreads();
 
   // ---- per position: restore blocks, need, grant, new blocks
@@ -625,16 +1000,16 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     long long nbj = 0;
     const long long h = st == CASCADE_RUNNING_PREFILL ? rec_held(w) : 0;
     if (gj > 0) {
+      const unsigned ubt = (unsigned)bt;
       if (st == CASCADE_QUEUED) {
-        const int tier = rec_tier(w);
-        if (tier == CASCADE_KV_HBM) {
-          const long long s = r4[j].z;
-          nbj = (s + gj + bt - 1) / bt - s / bt;
+        if (rec_tier(w) == CASCADE_KV_HBM) {
+          const unsigned s = (unsigned)r4[j].z;
+          nbj = (long long)udiv_ceil(s + (unsigned)gj, ubt) - s / ubt;
         } else {
-          nbj = rj + (gj + bt - 1) / bt;
+          nbj = rj + udiv_ceil((unsigned)gj, ubt);
         }
       } else if (st == CASCADE_RUNNING_PREFILL) {
-        nbj = ((long long)r4[j].z + gj + bt - 1) / bt - rec_held(w);
+        nbj = (long long)udiv_ceil((unsigned)r4[j].z + (unsigned)gj, ubt) - rec_held(w);
       } else {
         nbj = rec_decnb(w);
       }
@@ -665,22 +1040,20 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   if (threadIdx.x < kL2)
     publish<unsigned long long>(st2 + threadIdx.x, (unsigned long long)t2[threadIdx.x],
                                 tile == 0 ? kFlagInclusive : kFlagAggregate);
-  if (threadIdx.x < kL2) {
-    long long pre = 0;
-    if (tile > 0) {
-      pre = (long long)look_back<unsigned long long, kLookWin>(status2, kL2Stride, tile,
-                                                                threadIdx.x, &timed_out);
-      publish<unsigned long long>(st2 + threadIdx.x, (unsigned long long)(pre + t2[threadIdx.x]),
+  if (tile > 0) {
+    block_look_back<kL2, kBlock / kL2>(status2, kL2Stride, tile, s_sum, s_base, s_w, &s_left,
+                                       &timed_out);
+    if (threadIdx.x < kL2)
+      publish<unsigned long long>(st2 + threadIdx.x,
+                                  (unsigned long long)(s_sum[threadIdx.x] + t2[threadIdx.x]),
                                   kFlagInclusive);
-    }
-    s_pre[threadIdx.x] = pre;
+  } else {
+    if (threadIdx.x < kL2Stride) s_sum[threadIdx.x] = 0;
+    __syncthreads();
   }
-  if (__syncthreads_or(timed_out ? 1 : 0)) {
-    if (threadIdx.x == 0) set_status(info, CASCADE_ETIMEOUT);
-  }
-  long long W = s_pre[0] + l2[0], NB = s_pre[1] + l2[1], AC = s_pre[2] + l2[2],
-            X = s_pre[3] + l2[3], Z = s_pre[4] + l2[4], RR = s_pre[5] + l2[5],
-            RC = s_pre[6] + l2[6];
+  long long W = s_sum[0] + l2[0], NB = s_sum[1] + l2[1], AC = s_sum[2] + l2[2],
+            X = s_sum[3] + l2[3], Z = s_sum[4] + l2[4], RR = s_sum[5] + l2[5],
+            RC = s_sum[6] + l2[6];
 
   long long a_nb = 0, a_eh = 0, a_eoh = 0, a_n = 0, a_r = 0, a_rc = 0;
 #pragma unroll
@@ -701,11 +1074,11 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
       ctl->kz = Z;
       ctl->kzp = zp_inc[j] - (rec_offl(w) ? hh[j] : 0);
     }
-    order_out[p] = i;
-    granted_out[i] = adm ? (int)g[j] : 0;
-    restore_out[i] = (int)r[j];
-    alloc_begin[i] = adm ? (int)NB : -1;
-    alloc_count[i] = adm ? (int)nb[j] : 0;
+    o.order[p] = i;
+    o.granted[i] = adm ? (int)g[j] : 0;
+    o.restore[i] = (int)r[j];
+    o.alloc_begin[i] = adm ? (int)NB : -1;
+    o.alloc_count[i] = adm ? (int)nb[j] : 0;
     int act;
     if (st != CASCADE_QUEUED) {
       act = CASCADE_ACT_RETAIN;  // a preempted running prefill is rewritten later
@@ -715,9 +1088,9 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
       else if (tier == CASCADE_KV_NONE || r[j] == 0) act = CASCADE_ACT_RECOMPUTE;
       else act = adm ? CASCADE_ACT_RESTORE : CASCADE_ACT_PREFETCH;
     }
-    action_out[i] = (uint8_t)act;
+    o.action[i] = (uint8_t)act;
     if (adm) {
-      admitted_out[AC] = i;
+      o.admitted[AC] = i;
       a_nb += nb[j];
       a_n += 1;
       if (r[j] > 0) {
@@ -735,13 +1108,18 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     const long long zj = (gp || !rec_offl(w)) ? 0 : hh[j];
     if (st == CASCADE_RUNNING_PREFILL) {
       RpInfo ri;
+      ri.req = i;
       ri.pos = p;
       ri.eligible = adm ? 0 : 1;
+      ri.held = (int)hh[j];
+      ri.row0 = ro[i];
+      ri.offl = rec_offl(w);
+      ri.pad[0] = ri.pad[1] = 0;
       ri.x = X + xj;
       ri.y = y_inc[j];
       ri.z = Z + zj;
       ri.zp = zp_inc[j];
-      rp_info[i] = ri;
+      rp_list[rp_at++] = ri;
       if (!adm) {
         a_eh += hh[j];
         a_eoh += rec_offl(w) ? hh[j] : 0;
@@ -755,142 +1133,63 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     RR += gp ? r[j] : 0;
     RC += (gp && r[j] > 0) ? 1 : 0;
   }
-  long long tot[6] = {a_nb, a_eh, a_eoh, a_n, a_r, a_rc};
-  block_sum<6>(tot, s_scan);
+  long long tot[8] = {a_nb, a_eh, a_eoh, a_n, a_r, a_rc, timed_out ? 1 : 0, broken ? 1 : 0};
+  block_sum<8>(tot, reinterpret_cast<long long *>(s_w));
   if (threadIdx.x == 0) {
-    long long *dst[6] = {&ctl->adm_nb, &ctl->elig_h, &ctl->elig_offl_h,
-                         &ctl->n_adm, &ctl->n_unpack, &ctl->n_restore};
-    for (int k = 0; k < 6; ++k)
-      if (tot[k]) atomicAdd((unsigned long long *)dst[k], (unsigned long long)tot[k]);
+    TileTot tt;
+    tt.adm_nb = tot[0];
+    tt.elig_h = tot[1];
+    tt.elig_offl_h = tot[2];
+    tt.n_adm = tot[3];
+    tt.n_unpack = tot[4];
+    tt.n_restore = tot[5];
+    tt.pad[0] = tt.pad[1] = 0;
+    tile_tot[tile] = tt;
+    if (tot[6]) set_status(info, CASCADE_ETIMEOUT);
+    if (tot[7]) set_status(info, CASCADE_EINTERNAL);
+    // release this tile's writes, then count it; the last tile finishes the step
+    __threadfence();
+    s_last = (atomicAdd(&ctl->scan_done, 1u) == gridDim.x - 1);
   }
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();  // acquire every other tile's writes
+  if (threadIdx.x == 0) s_bad = bad_status(load_agent(info));
+  __syncthreads();
+  if (s_bad) return;
+  // every tile has published its level-1 inclusive prefix: the total of
+  // running prefills is the last tile's
+  const int n_rp = (int)((load_agent(status1 + (size_t)(gridDim.x - 1) * kL1 + 4)) >> 2);
+  finish_step(ctl, info, n, c.n_free, gridDim.x, n_rp, tile_tot, free_slots, rp_list,
+              restore_list, slots, o, s_fin);
 }
 
-// ------------------------------------------------------------ finalize
-
-// Budget-aware preemption (Algorithm 1; Section 4.4): the deficit
-// D = new blocks of admitted requests - free blocks is covered by the
-// non-admitted running prefills taken from the back of the order (largest
-// remaining budget first).  A holder at position p is preempted iff the
-// eligible blocks after p are fewer than D.  One wave per running prefill.
-__global__ __launch_bounds__(kBlock) void finalize_kernel(
-    int n_free, const int *__restrict__ free_slots, const Ctl *ctl, int *info,
-    const int *__restrict__ rp_list, const RpInfo *__restrict__ rp_info,
-    const int4 *__restrict__ rec, const int *__restrict__ ro, const int *__restrict__ slots,
-    uint8_t *__restrict__ action_out, int *__restrict__ slot_list, int sl_cap,
-    cascade_move_t *__restrict__ pack, int pack_cap) {
-  if (status_failed(info)) return;
-  const int gt = blockIdx.x * kBlock + threadIdx.x;
-  const int lim = min(n_free, sl_cap);
-  for (int j = gt; j < lim; j += gridDim.x * kBlock) slot_list[j] = free_slots[j];
-  const long long D = ctl->adm_nb - n_free;
-  if (D <= 0) return;
-  const long long E = ctl->elig_h, EO = ctl->elig_offl_h;
-  const int kstar = ctl->kstar;
-  const int lane = lane_id();
-  const int nrp = (int)ctl->rp_count;
-  for (int e = gt >> 6; e < nrp; e += (gridDim.x * kBlock) >> 6) {
-    const int i = rp_list[e];
-    const RpInfo ri = rp_info[i];
-    if (!ri.eligible) continue;
-    const long long eh = ri.pos < kstar ? ri.x : ctl->kx + ri.y - ctl->ky;
-    const long long after = E - eh;  // eligible blocks behind this request
-    if (after >= D) continue;
-    const int w = rec[i].w;
-    const int h = rec_held(w);
-    const bool offl = rec_offl(w);
-    const int row0 = ro[i];
-    if (lane == 0) {
-      action_out[i] = offl ? CASCADE_ACT_PREEMPT_OFFLOAD : CASCADE_ACT_PREEMPT_DROP;
-      atomicAdd(&info[CASCADE_INFO_N_SLOT_LIST], h);
-      if (offl) atomicAdd(&info[CASCADE_INFO_N_PACK], h);
-    }
-    const long long sbase = (long long)n_free + after;
-    if (after < 0) {  // cannot happen with consistent prefixes
-      if (lane == 0) set_status(info, CASCADE_EINTERNAL);
-      continue;
-    }
-    for (int b = lane; b < h; b += 64)
-      if (sbase + b < sl_cap) slot_list[sbase + b] = slots[row0 + b];
-    if (offl) {
-      const long long eo = ri.pos < kstar ? ri.z : ctl->kz + ri.zp - ctl->kzp;
-      const long long pbase = EO - eo;
-      for (int b = lane; b < h; b += 64) {
-        if (pbase + b >= 0 && pbase + b < pack_cap) {
-          cascade_move_t m;
-          m.req = i;
-          m.blk = b;
-          m.pool_slot = slots[row0 + b];
-          m.staging_slot = (int)(pbase + b);
-          pack[pbase + b] = m;
-        }
-      }
-    }
+// A step with no requests: only the free list becomes the slot list.
+__global__ __launch_bounds__(kBlock) void empty_step_kernel(int n_free, int num_blocks,
+                                                            const int *__restrict__ free_slots,
+                                                            int *info, Outs o) {
+  bool bad = false;
+  const int lim = min(n_free, o.sl_cap);
+  for (int j = threadIdx.x; j < n_free; j += kBlock) {
+    const int s = free_slots[j];
+    if ((unsigned)s >= (unsigned)num_blocks) bad = true;
+    if (j < lim) o.slot_list[j] = s;
   }
-}
-
-// --------------------------------------------------------------- moves
-
-// Restore moves: the first r new blocks of each RESTORE request receive its
-// prefix, staged in admitted order.  Move m finds its request by binary
-// search over the restore list's staging offsets.
-__global__ __launch_bounds__(kBlock) void moves_kernel(
-    const Ctl *ctl, int *info, const RestoreEnt *__restrict__ rl,
-    const int *__restrict__ slot_list, int sl_cap, cascade_move_t *__restrict__ unpack,
-    int unpack_cap, int pack_cap) {
-  if (status_failed(info)) return;
-  const long long nu = ctl->n_unpack;
-  const int nr = (int)ctl->n_restore;
-  const long long lim = lmin(nu, (long long)unpack_cap);
-  for (long long m = blockIdx.x * kBlock + threadIdx.x; m < lim;
-       m += (long long)gridDim.x * kBlock) {
-    int lo = 0, hi = nr - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (rl[mid].stage_off <= m) lo = mid; else hi = mid - 1;
-    }
-    const RestoreEnt e = rl[lo];
-    const int b = (int)(m - e.stage_off);
-    const long long s = (long long)e.alloc_off + b;
-    cascade_move_t mv;
-    mv.req = e.req;
-    mv.blk = b;
-    mv.pool_slot = s < sl_cap ? slot_list[s] : -1;
-    mv.staging_slot = (int)m;
-    unpack[m] = mv;
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    info[CASCADE_INFO_N_ADMITTED] = (int)ctl->n_adm;
-    info[CASCADE_INFO_N_UNPACK] = (int)nu;
-    const bool full = info[CASCADE_INFO_N_SLOT_LIST] > sl_cap || nu > unpack_cap ||
-                      info[CASCADE_INFO_N_PACK] > pack_cap;
-    if (full && info[CASCADE_INFO_STATUS] == CASCADE_OK) info[CASCADE_INFO_STATUS] = CASCADE_ENOSPC;
-  }
-}
-
-// ---------------------------------------------------------------- init
-
-__global__ __launch_bounds__(kBlock) void init_kernel(Ctl *ctl, uint4 *clear, size_t clear_vec,
-                                                      int *info, int n, int n_free) {
-  const size_t gt = (size_t)blockIdx.x * kBlock + threadIdx.x;
-  const size_t gs = (size_t)gridDim.x * kBlock;
-  for (size_t j = gt; j < clear_vec; j += gs) clear[j] = make_uint4(0, 0, 0, 0);
-  if (gt == 0) {
-    unsigned *w = reinterpret_cast<unsigned *>(ctl);
-    for (size_t k = 0; k < kCtlHeaderWords; ++k) w[k] = 0;
-    ctl->bmin = ~0ull;
-    ctl->bmax = 0;
-    ctl->kstar = n;
+  const bool any_bad = __syncthreads_or(bad ? 1 : 0);
+  if (threadIdx.x == 0) {
     for (int k = 0; k < CASCADE_INFO_LEN; ++k) info[k] = 0;
     info[CASCADE_INFO_N_SLOT_LIST] = n_free;
+    info[CASCADE_INFO_STATUS] =
+        any_bad ? CASCADE_EINVAL : (n_free > o.sl_cap ? CASCADE_ENOSPC : CASCADE_OK);
   }
 }
 
 // ---------------------------------------------------------------- host
 
 struct Layout {
-  size_t ctl, keys_a, keys_b, vals_a, vals_b, rec, rp_list, rp_info, restore, sort_status,
-      scan1, scan2, total;
-  int sort_tiles, scan_tiles;
+  size_t ctl, sort_status, scan1, scan2, partials, keys_a, keys_b, vals_a, vals_b, rec,
+      rp_list, restore, tile_tot, total;
+  int sort_tiles, scan_tiles, eval_grid;
 };
 
 size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -900,6 +1199,7 @@ Layout make_layout(int32_t n) {
   const size_t np = n > 0 ? (size_t)n : 1;
   L.sort_tiles = (int)((np + kSortTile - 1) / kSortTile);
   L.scan_tiles = (int)((np + kScanTile - 1) / kScanTile);
+  L.eval_grid = (int)((np + kBlock * kEvalItems - 1) / (kBlock * kEvalItems));
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
   L.ctl = take(sizeof(Ctl));
@@ -907,14 +1207,15 @@ Layout make_layout(int32_t n) {
   L.sort_status = take((size_t)kMaxDigits * L.sort_tiles * kRadix * 4);
   L.scan1 = take((size_t)L.scan_tiles * kL1 * 8);
   L.scan2 = take((size_t)L.scan_tiles * kL2Stride * 8);
+  L.partials = take((size_t)L.eval_grid * sizeof(Partial));
   L.keys_a = take(np * 8);
   L.keys_b = take(np * 8);
   L.vals_a = take(np * 4);
   L.vals_b = take(np * 4);
   L.rec = take(np * 16);
-  L.rp_list = take(np * 4);
-  L.rp_info = take(np * sizeof(RpInfo));
+  L.rp_list = take(np * sizeof(RpInfo));
   L.restore = take(np * sizeof(RestoreEnt));
+  L.tile_tot = take((size_t)L.scan_tiles * sizeof(TileTot));
   L.total = off;
   return L;
 }
@@ -946,6 +1247,44 @@ bool params_ok(const cascade_params_t *p, int32_t n, const cascade_tier_state_t 
   if (t->num_blocks < 0 || t->n_free < 0 || t->n_free > t->num_blocks) return false;
   return true;
 }
+
+// Upper bound on the 8-bit digits of the compressed key, from the parameters
+// alone: every budget lies in [-(L_bound + t_now), max SLO], clamped to
+// +-2^61.  Radix passes beyond it are not launched; the device skips the
+// ones between it and the live key width.
+int max_sort_digits(const cascade_params_t *p) {
+  typedef __int128 i128;
+  const i128 nmax = 1 << 17;
+  const i128 dmax = p->max_batch - 1;
+  const i128 per_iter = (i128)p->c_iter_ps + dmax * p->c_decode_ps;
+  const i128 iters = (nmax + p->chunk_tokens - 1) / p->chunk_tokens;
+  const i128 prefill_ps = iters * per_iter + nmax * p->c_token_ps +
+                          (i128)p->c_attn_ps * (nmax * (nmax + 1) / 2);
+  const i128 decode_ps = nmax * per_iter;
+  const i128 compute_ns = (prefill_ps > decode_ps ? prefill_ps : decode_ps) / 1000 + 1;
+  const i128 restore = (i128)p->link_delta_ns[0] + p->link_delta_ns[1] +
+                       nmax * ((i128)p->link_blk_ns[0] + p->link_blk_ns[1]);
+  const i128 lsum = 2 * (compute_ns + restore);
+  const i128 lbound = ((lsum * p->gamma_q16) >> 17) + 1;
+  i128 hi = 0;
+  for (int c = 0; c < p->num_classes; ++c) hi = p->slo_ns[c] > hi ? p->slo_ns[c] : hi;
+  i128 lo = -(lbound + p->t_now_ns);
+  const i128 lim = (i128)1 << 61;
+  if (lo < -lim) lo = -lim;
+  if (hi > lim - 1) hi = lim - 1;
+  const i128 span = hi - lo + 1;
+  const i128 top = 2 * span + (hi - lo);
+  int bits = 0;
+  for (i128 v = top; v > 0; v >>= 1) ++bits;
+  const int d = (bits + 7) / 8;
+  return d < 1 ? 1 : (d > kMaxDigits ? kMaxDigits : d);
+}
+
+typedef void (*RadixFn)(int, Ctl *, int *, unsigned long long *, unsigned long long *,
+                        unsigned *, unsigned *, unsigned *);
+const RadixFn kRadixKernels[kMaxDigits] = {
+    radix_pass_kernel<0>, radix_pass_kernel<1>, radix_pass_kernel<2>, radix_pass_kernel<3>,
+    radix_pass_kernel<4>, radix_pass_kernel<5>, radix_pass_kernel<6>, radix_pass_kernel<7>};
 
 }  // namespace
 }  // namespace cascade
@@ -1020,54 +1359,63 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   c.n_free = ts->n_free;
   for (int k = 0; k < 16; ++k) c.slo[k] = k < p->num_classes ? p->slo_ns[k] : 0;
 
+  Outs o;
+  o.order = out->order;
+  o.granted = out->tokens_granted;
+  o.restore = out->restore_blocks;
+  o.alloc_begin = out->alloc_begin;
+  o.alloc_count = out->alloc_count;
+  o.admitted = out->admitted;
+  o.slot_list = out->slot_list;
+  o.action = out->action;
+  o.unpack = out->unpack_moves;
+  o.pack = out->pack_moves;
+  o.sl_cap = out->slot_list_capacity;
+  o.unpack_cap = out->unpack_capacity;
+  o.pack_cap = out->pack_capacity;
+
   char *ws = static_cast<char *>(workspace);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (n == 0) {
+    hipLaunchKernelGGL(empty_step_kernel, dim3(1), dim3(kBlock), 0, s, ts->n_free,
+                       ts->num_blocks, ts->free_slots, out->info, o);
+    return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
+  }
   Ctl *ctl = reinterpret_cast<Ctl *>(ws + L.ctl);
   auto *keys_a = reinterpret_cast<unsigned long long *>(ws + L.keys_a);
   auto *keys_b = reinterpret_cast<unsigned long long *>(ws + L.keys_b);
   auto *vals_a = reinterpret_cast<unsigned *>(ws + L.vals_a);
   auto *vals_b = reinterpret_cast<unsigned *>(ws + L.vals_b);
   auto *rec = reinterpret_cast<int4 *>(ws + L.rec);
-  auto *rp_list = reinterpret_cast<int *>(ws + L.rp_list);
-  auto *rp_info = reinterpret_cast<RpInfo *>(ws + L.rp_info);
+  auto *partials = reinterpret_cast<Partial *>(ws + L.partials);
+  auto *rp_list = reinterpret_cast<RpInfo *>(ws + L.rp_list);
   auto *rlist = reinterpret_cast<RestoreEnt *>(ws + L.restore);
+  auto *tile_tot = reinterpret_cast<TileTot *>(ws + L.tile_tot);
   auto *sort_status = reinterpret_cast<unsigned *>(ws + L.sort_status);
   auto *scan1 = reinterpret_cast<unsigned long long *>(ws + L.scan1);
   auto *scan2 = reinterpret_cast<unsigned long long *>(ws + L.scan2);
-  hipStream_t s = static_cast<hipStream_t>(stream);
 
-  // clear the histograms and every look-back status word in one sweep
-  const size_t clear_bytes = L.keys_a - offsetof(Ctl, hist);
-  const size_t clear_vec = clear_bytes / 16;
-  uint4 *clear = reinterpret_cast<uint4 *>(ws + L.ctl + offsetof(Ctl, hist));
-  const int init_grid = (int)std::min<size_t>(1024, (clear_vec + kBlock * 4 - 1) / (kBlock * 4) + 1);
-  hipLaunchKernelGGL(init_kernel, dim3(init_grid), dim3(kBlock), 0, s, ctl, clear, clear_vec,
-                     out->info, n, ts->n_free);
-  const int eval_grid = std::max(1, (n + kBlock - 1) / kBlock);
-  hipLaunchKernelGGL(eval_kernel, dim3(eval_grid), dim3(kBlock), 0, s, *rq, bt->row_offsets,
-                     ts->free_slots, c, n, ctl, out->info, out->budget_ns, out->queue_tier_out,
-                     keys_a, rec, rp_list);
-  if (n > 0) {
-    const int prep_grid = (n + kBlock * kPrepItems - 1) / (kBlock * kPrepItems);
-    hipLaunchKernelGGL(prep_kernel, dim3(prep_grid), dim3(kBlock), 0, s, n, ts->num_blocks,
-                       bt->row_offsets, bt->slots, ctl, out->info, keys_a, vals_a);
-    for (int pass = 0; pass < kMaxDigits; ++pass)
-      hipLaunchKernelGGL(radix_pass_kernel, dim3(L.sort_tiles), dim3(kBlock), 0, s, pass, n,
-                         ctl, out->info, keys_a, keys_b, vals_a, vals_b,
-                         sort_status + (size_t)pass * L.sort_tiles * kRadix);
-    hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, c, ctl,
-                       out->info, vals_a, vals_b, rec, out->order, out->tokens_granted,
-                       out->restore_blocks, out->alloc_begin, out->alloc_count, out->action,
-                       out->admitted, rp_info, rlist, scan1, scan2);
-  }
-  const int fin_grid = std::max(1, std::min(1024, (int)((std::max(n, ts->n_free) + kBlock - 1) / kBlock)));
-  hipLaunchKernelGGL(finalize_kernel, dim3(fin_grid), dim3(kBlock), 0, s, ts->n_free,
-                     ts->free_slots, ctl, out->info, rp_list, rp_info, rec, bt->row_offsets,
-                     bt->slots, out->action, out->slot_list, out->slot_list_capacity,
-                     out->pack_moves, out->pack_capacity);
-  const int mv_grid = std::max(1, std::min(256, (out->unpack_capacity + kBlock - 1) / kBlock));
-  hipLaunchKernelGGL(moves_kernel, dim3(mv_grid), dim3(kBlock), 0, s, ctl, out->info, rlist,
-                     out->slot_list, out->slot_list_capacity, out->unpack_moves,
-                     out->unpack_capacity, out->pack_capacity);
+  // histograms + every look-back status word: cleared by eval
+  const size_t hist_off = L.ctl + offsetof(Ctl, hist);
+  const size_t clear_vec = (L.partials - hist_off) / 16;
+  uint4 *clear = reinterpret_cast<uint4 *>(ws + hist_off);
+
+  hipLaunchKernelGGL(eval_kernel, dim3(L.eval_grid), dim3(kBlock), 0, s, *rq, bt->row_offsets,
+                     ts->free_slots, c, n, ctl, clear, clear_vec, out->info, partials,
+                     out->budget_ns, out->queue_tier_out, keys_a, rec);
+  const int prep_grid = (n + kBlock * kPrepItems - 1) / (kBlock * kPrepItems);
+  hipLaunchKernelGGL(prep_kernel, dim3(prep_grid), dim3(kBlock), 0, s, n, ts->num_blocks,
+                     L.eval_grid, partials, bt->row_offsets, bt->slots, ctl, out->info, keys_a,
+                     vals_a);
+  const int passes = max_sort_digits(p);
+  for (int pass = 0; pass < passes; ++pass)
+    hipLaunchKernelGGL(kRadixKernels[pass], dim3(L.sort_tiles), dim3(kBlock), 0, s, n, ctl,
+                       out->info, keys_a, keys_b, vals_a, vals_b,
+                       sort_status + (size_t)pass * L.sort_tiles * kRadix);
+  hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, passes, c, ctl,
+                     out->info,
+                     vals_a, vals_b, rec, bt->row_offsets, bt->slots, ts->free_slots, o, rp_list,
+                     rlist, tile_tot, scan1, scan2);
   if (hipGetLastError() != hipSuccess) return CASCADE_EHIP;
   return CASCADE_OK;
 }
