@@ -39,6 +39,26 @@ WORKLOADS = {
 }
 
 
+def measured_traffic(cfg, layout):
+    """HBM bytes per KV-copy launch from the committed rocprofv3 counter
+    passes (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads for a
+    plain copy of known size), or None when the workload differs or the
+    kernel source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "kvcopy_counters_headline_65536.md")
+    try:
+        text = open(path).read()
+        rec = json.loads(text.rsplit("```json", 1)[1].split("```", 1)[0])
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, IndexError, ValueError, KeyError):
+        return None
+    if cfg != 2 or layout != "layer_major":
+        return None
+    if hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
+        return None
+    return float(rec["traffic_bytes_per_launch"])
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -220,7 +240,8 @@ def main():
         "step_total_us_p50": float(np.median(t_all)),
         "roofline": {"bound": "hbm", "kernel": "kvcopy_kernel (pack + unpack launches)",
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": measured_traffic(cfg, args.layout),
                      "bytes_per_launch": (bytes_pack + bytes_unpack) / 2.0,
                      "us_per_launch": copy_us / 2.0},
     }
