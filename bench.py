@@ -3,13 +3,14 @@
 
 One timed step = the whole hot path on one synthetic queue, inputs resident in
 HBM: cascade_step (budgets, actions, least-budget-first order, admission,
-preemption, move lists), then cascade_pack of the spill moves and
-cascade_unpack of the restore moves it emitted, on one stream.
+preemption, move lists), then the KV copies it emitted, on one stream: by
+default cascade_pack_unpack (spills and restores in one launch, ordered by the
+step's hazard pairs); with --copy separate, cascade_pack then cascade_unpack.
 
 Prints one JSON line: requests/s of the whole step, the step (parts 1-3)
-latency, pack/unpack GB/s, a roofline record for the dominant kernel (the KV
-copy, measured with HIP events on its stream) and the CPU oracle timed on this
-host as a reported baseline.
+latency, copy GB/s, a roofline record for the dominant kernel (the KV copy,
+measured with HIP events on its stream) and the CPU oracle timed on this host
+as a reported baseline.
 """
 from __future__ import annotations
 
@@ -39,24 +40,29 @@ WORKLOADS = {
 }
 
 
-def measured_traffic(cfg, layout):
+def measured_traffic(cfg, layout, kernel):
     """HBM bytes per KV-copy launch from the committed rocprofv3 counter
     passes (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads for a
-    plain copy of known size), or None when the workload differs or the
-    kernel source has changed since the counters were taken."""
+    plain copy of known size), or None when the workload or kernel differs or
+    the kernel source has changed since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "kvcopy_counters_headline_65536.md")
+    path = os.path.join(ROOT, "profiles", "kvmove_counters_headline_65536.md")
     try:
         text = open(path).read()
         rec = json.loads(text.rsplit("```json", 1)[1].split("```", 1)[0])
         src = open(os.path.join(ROOT, rec["source"]), "rb").read()
     except (OSError, IndexError, ValueError, KeyError):
         return None
-    if cfg != 2 or layout != "layer_major":
+    if cfg != 2 or layout != "layer_major" or rec.get("kernel") != kernel:
         return None
     if hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
         return None
     return float(rec["traffic_bytes_per_launch"])
+
+
+def progress(msg):
+    """One line per phase on stderr (the JSON line alone goes to stdout)."""
+    print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
 def parse():
@@ -66,6 +72,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--layout", default="layer_major", choices=["layer_major", "block_major"])
+    ap.add_argument("--copy", default="fused", choices=["fused", "separate"],
+                    help="one cascade_pack_unpack launch, or cascade_pack then cascade_unpack")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent on the oracle baseline")
@@ -153,8 +161,9 @@ def main():
     n_pack, n_unpack = res["n_pack"], res["n_unpack"]
     block_bytes = 2 * geom["num_layers"] * geom["chunk_bytes"]
 
+    progress(f"step done: {n} requests, {n_pack} spill / {n_unpack} restore blocks")
     pool = torch.empty(geom["pool_bytes"], dtype=torch.uint8, device=dev)
-    device.fill_pattern_(pool, seed=1)
+    device.fill_pattern_(pool, seed=1, progress=progress)
     st_out = torch.empty(max(n_pack, 1) * block_bytes, dtype=torch.uint8, device=dev)
     st_in = torch.empty(max(n_unpack, 1) * block_bytes, dtype=torch.uint8, device=dev)
     device.fill_pattern_(st_in, seed=2)
@@ -162,27 +171,40 @@ def main():
     pl = device.kv_pool_struct(pool.data_ptr(), geom)
     torch.cuda.synchronize()
 
+    fused = args.copy == "fused"
+
     def one_step(ev=None):
         if ev is not None:
             ev[0].record(stream)
         rc = d.run(stream)
         if ev is not None:
             ev[1].record(stream)
-        rc |= cascade.cascade_pack(pl, st_out.data_ptr(), max(n_pack, 1),
-                                   d.pack_moves.data_ptr(), d.n_pack_ptr(), d.caps[2],
-                                   cstat.data_ptr(), sh)
-        if ev is not None:
-            ev[2].record(stream)
-        rc |= cascade.cascade_unpack(pl, st_in.data_ptr(), max(n_unpack, 1),
-                                     d.unpack_moves.data_ptr(), d.n_unpack_ptr(), d.caps[1],
-                                     cstat.data_ptr(), sh)
+        if fused:
+            rc |= cascade.cascade_pack_unpack(
+                pl, st_out.data_ptr(), max(n_pack, 1), d.pack_moves.data_ptr(), d.n_pack_ptr(),
+                d.caps[2], d.pack_hazard.data_ptr(), st_in.data_ptr(), max(n_unpack, 1),
+                d.unpack_moves.data_ptr(), d.n_unpack_ptr(), d.caps[1],
+                d.unpack_hazard.data_ptr(), cstat.data_ptr(), sh)
+            if ev is not None:
+                ev[2].record(stream)
+        else:
+            rc |= cascade.cascade_pack(pl, st_out.data_ptr(), max(n_pack, 1),
+                                       d.pack_moves.data_ptr(), d.n_pack_ptr(), d.caps[2],
+                                       cstat.data_ptr(), sh)
+            if ev is not None:
+                ev[2].record(stream)
+            rc |= cascade.cascade_unpack(pl, st_in.data_ptr(), max(n_unpack, 1),
+                                         d.unpack_moves.data_ptr(), d.n_unpack_ptr(), d.caps[1],
+                                         cstat.data_ptr(), sh)
         if ev is not None:
             ev[3].record(stream)
         return rc
 
+    progress("pool and staging filled")
     for _ in range(args.warmup):
         assert one_step() == 0
     torch.cuda.synchronize()
+    progress(f"{args.warmup} warm-up steps done")
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -190,19 +212,21 @@ def main():
         assert one_step(evs[k]) == 0
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    progress(f"{args.steps} timed steps done")
     res2 = d.fetch()
     assert res2["status"] == 0 and int(cstat.item()) == 0
     assert res2["n_pack"] == n_pack and res2["n_unpack"] == n_unpack
 
     t_step = np.array([e[0].elapsed_time(e[1]) for e in evs]) * 1e3      # us
-    t_pack = np.array([e[1].elapsed_time(e[2]) for e in evs]) * 1e3
-    t_unpack = np.array([e[2].elapsed_time(e[3]) for e in evs]) * 1e3
+    t_c1 = np.array([e[1].elapsed_time(e[2]) for e in evs]) * 1e3
+    t_c2 = np.array([e[2].elapsed_time(e[3]) for e in evs]) * 1e3
     t_all = np.array([e[0].elapsed_time(e[3]) for e in evs]) * 1e3
     ms_per_step = wall * 1e3 / args.steps
     bytes_pack = 2.0 * n_pack * block_bytes
     bytes_unpack = 2.0 * n_unpack * block_bytes
     gbps = lambda b, us: b / (us * 1e-6) / 1e9 if us > 0 else 0.0
-    copy_us = float(np.mean(t_pack) + np.mean(t_unpack))
+    copy_us = float(np.mean(t_c1) + np.mean(t_c2))          # all copy launches of a step
+    launches = 1 if fused else 2
     achieved = gbps(bytes_pack + bytes_unpack, copy_us)
     extra = None
     if args.calib_copy_gb > 0:
@@ -218,6 +242,14 @@ def main():
         extra = {"bytes": nbytes, "us": e0.elapsed_time(e1) * 1e3,
                  "GBps": gbps(2.0 * nbytes, e0.elapsed_time(e1) * 1e3)}
         del a, b
+    kernel = "kvmove_kernel" if fused else "kvcopy_kernel"
+    copies = {"mode": args.copy, "pack_blocks": n_pack, "unpack_blocks": n_unpack,
+              "paired_blocks": int((res["unpack_hazard"] >= 0).sum()),
+              "copy_us_p50": float(np.median(t_c1 + t_c2)),
+              "copy_GBps": gbps(bytes_pack + bytes_unpack, float(np.median(t_c1 + t_c2)))}
+    if not fused:
+        copies["pack_GBps"] = gbps(bytes_pack, float(np.median(t_c1)))
+        copies["unpack_GBps"] = gbps(bytes_unpack, float(np.median(t_c2)))
     out = {
         "metric": METRIC,
         "value": n * args.steps / wall,
@@ -234,16 +266,15 @@ def main():
         "sched_step_us_p50": float(np.median(t_step)),
         "sched_step_us_p90": float(np.percentile(t_step, 90)),
         "sched_req_per_s": n / (float(np.median(t_step)) * 1e-6),
-        "pack_blocks": n_pack, "unpack_blocks": n_unpack,
-        "pack_GBps": gbps(bytes_pack, float(np.median(t_pack))),
-        "unpack_GBps": gbps(bytes_unpack, float(np.median(t_unpack))),
+        "kv_copy": copies,
         "step_total_us_p50": float(np.median(t_all)),
-        "roofline": {"bound": "hbm", "kernel": "kvcopy_kernel (pack + unpack launches)",
+        "roofline": {"bound": "hbm", "kernel": kernel + (" (one launch: pack and unpack)" if fused
+                                                          else " (pack + unpack launches)"),
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": measured_traffic(cfg, args.layout),
-                     "bytes_per_launch": (bytes_pack + bytes_unpack) / 2.0,
-                     "us_per_launch": copy_us / 2.0},
+                     "traffic": measured_traffic(cfg, args.layout, kernel) if fused else None,
+                     "bytes_per_launch": (bytes_pack + bytes_unpack) / launches,
+                     "us_per_launch": copy_us / launches},
     }
     if extra:
         out["calib_copy"] = extra

@@ -13,8 +13,9 @@
  *      preempted with a spill to DRAM or a drop (Section 4.4),
  *   3. least-remaining-budget-first order and admission under the batch token
  *      cap (chunked prefill) and the HBM KV-block capacity,
- *   4. the KV block moves, executed by cascade_pack / cascade_unpack between
- *      the paged HBM pool and contiguous staging buffers.
+ *   4. the KV block moves, executed by cascade_pack / cascade_unpack (or both
+ *      in one launch by cascade_pack_unpack) between the paged HBM pool and
+ *      contiguous staging buffers.
  *
  * Conventions for every entry point:
  *   - Pointers named *_dev and every array in the structs below are DEVICE
@@ -168,6 +169,14 @@ typedef struct { int32_t req, blk, pool_slot, staging_slot; } cascade_move_t;
                      the order first, each row in order); capacity entries
      unpack_moves    one per restored block, admitted order
      pack_moves      one per block of each request preempted with a spill
+     unpack_hazard   per unpack move: index of the pack move that reads the
+                     pool slot this move overwrites (a preempted request's
+                     slot handed to a restore), else -1; unpack_capacity
+                     entries
+     pack_hazard     per pack move: index of the unpack move that later
+                     overwrites the slot it reads, else -1; pack_capacity
+                     entries.  Both NULL (not written) or both set; they are
+                     meaningful when the step ends with status CASCADE_OK.
      info            device int32[CASCADE_INFO_LEN]: status and counts.  The
                      counts are the required sizes even when a list did not
                      fit its capacity (status CASCADE_ENOSPC). */
@@ -179,6 +188,7 @@ typedef struct {
   cascade_move_t *unpack_moves, *pack_moves;
   int32_t slot_list_capacity, unpack_capacity, pack_capacity;
   int32_t *info;
+  int32_t *unpack_hazard, *pack_hazard;
 } cascade_outputs_t;
 
 /* Paged KV pool: chunk (slot, layer l, kv in {0: K, 1: V}) of chunk_bytes
@@ -200,8 +210,9 @@ size_t cascade_step_workspace_bytes(int32_t n);
 
 /* One scheduling step (Algorithm 1, Phase 2 over the whole queue, with the
    estimator and budget engine of Section 4.2 and the preemption of Section
-   4.4).  Returns CASCADE_OK once enqueued, CASCADE_EINVAL for NULL pointers,
-   parameters out of domain or negative capacities, CASCADE_ENOSPC when
+   4.4).  Returns CASCADE_OK once enqueued, CASCADE_EINVAL for NULL pointers
+   (or exactly one hazard array), parameters out of domain or negative
+   capacities, CASCADE_ENOSPC when
    workspace_bytes < cascade_step_workspace_bytes(n), CASCADE_EHIP when a
    launch fails.  Request data, block-table and free-list errors set
    info[STATUS] = CASCADE_EINVAL; lists longer than their capacity set
@@ -229,6 +240,30 @@ int cascade_pack(const cascade_kv_pool_t *pool, void *staging, int32_t staging_s
 int cascade_unpack(const cascade_kv_pool_t *pool, const void *staging, int32_t staging_slots,
                    const cascade_move_t *moves, const int32_t *n_moves_dev, int32_t max_moves,
                    int32_t *status_dev, void *stream);
+
+/* Both copies of one step in a single launch (Section 4.4: spill of the
+   preempted prefills and the final DRAM->HBM hop of the restores).  The
+   result equals cascade_pack(pack list) followed by cascade_unpack(unpack
+   list): chunks of the two lists are interleaved over the GPU, and an unpack
+   move m paired with a pack move j (unpack_hazard[m] == j and
+   pack_hazard[j] == m, as cascade_step writes them) is copied by the thread
+   that has just read the same chunk for pack move j, so the slot is read
+   before it is overwritten.  Every unpack move is performed exactly once
+   whatever the hazard arrays hold; the pack-before-unpack order is
+   guaranteed for the pairs they declare, which must cover every pool slot
+   that is both a pack source and an unpack destination.  Move, count and
+   staging rules as for cascade_pack / cascade_unpack, each list with its own
+   staging buffer; a bad move sets *status_dev = CASCADE_EINVAL and is
+   skipped.  The hazard arrays hold max_pack / max_unpack entries (device).
+   Returns CASCADE_EINVAL for NULL pointers, misalignment or a bad geometry,
+   CASCADE_EHIP on launch failure. */
+int cascade_pack_unpack(const cascade_kv_pool_t *pool, void *pack_staging,
+                        int32_t pack_staging_slots, const cascade_move_t *pack_moves,
+                        const int32_t *n_pack_dev, int32_t max_pack, const int32_t *pack_hazard,
+                        const void *unpack_staging, int32_t unpack_staging_slots,
+                        const cascade_move_t *unpack_moves, const int32_t *n_unpack_dev,
+                        int32_t max_unpack, const int32_t *unpack_hazard, int32_t *status_dev,
+                        void *stream);
 
 /* Short English text for a return code or status value. */
 const char *cascade_strerror(int code);

@@ -406,6 +406,23 @@ int32_t cref_step(int32_t n, const uint64_t *id, const uint8_t *cls, const uint8
   out->n_pack = (int32_t)npk;
   if (npk > out->pack_capacity) status = CREF_ENOSPC;
 
+  /* Copy-order hazards: a preempted request's slot that a restore receives
+     is read by the spill and written by the restore (Section 4.4), so the
+     spill of that slot must come first.  Found by pool slot, with a table
+     over the whole pool. */
+  if (status == CREF_OK && (out->unpack_hazard || out->pack_hazard)) {
+    int32_t *by_slot = (int32_t *)malloc(sizeof(int32_t) * (size_t)(p->num_blocks > 0 ? p->num_blocks : 1));
+    for (int32_t s = 0; s < p->num_blocks; s++) by_slot[s] = -1;
+    for (int32_t j = 0; j < npk; j++) by_slot[out->pack_moves[j].pool_slot] = j;
+    if (out->unpack_hazard)
+      for (int32_t m = 0; m < nu; m++) out->unpack_hazard[m] = by_slot[out->unpack_moves[m].pool_slot];
+    for (int32_t s = 0; s < p->num_blocks; s++) by_slot[s] = -1;
+    for (int32_t m = 0; m < nu; m++) by_slot[out->unpack_moves[m].pool_slot] = m;
+    if (out->pack_hazard)
+      for (int32_t j = 0; j < npk; j++) out->pack_hazard[j] = by_slot[out->pack_moves[j].pool_slot];
+    free(by_slot);
+  }
+
   free(ev); free(pq); free(r); free(g); free(nb); free(adm); free(victim);
   return status;
 }

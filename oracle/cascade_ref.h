@@ -81,6 +81,12 @@ typedef struct {
   int32_t *slot_list; int32_t slot_list_capacity; int32_t n_slot_list;
   cref_move *unpack_moves; int32_t unpack_capacity; int32_t n_unpack;
   cref_move *pack_moves;   int32_t pack_capacity;   int32_t n_pack;
+  /* Copy-order hazards (written only when the step returns CREF_OK; either
+     pointer may be NULL): unpack_hazard[m] = the pack move reading the pool
+     slot that unpack move m writes, pack_hazard[j] = the unpack move writing
+     the slot that pack move j reads, -1 where there is none. */
+  int32_t *unpack_hazard;
+  int32_t *pack_hazard;
 } cref_outputs;
 
 /* Intermediate values of the per-request evaluation, exposed for pinning. */

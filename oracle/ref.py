@@ -68,6 +68,7 @@ class Outputs(C.Structure):
         ("slot_list", C.c_void_p), ("slot_list_capacity", C.c_int32), ("n_slot_list", C.c_int32),
         ("unpack_moves", C.c_void_p), ("unpack_capacity", C.c_int32), ("n_unpack", C.c_int32),
         ("pack_moves", C.c_void_p), ("pack_capacity", C.c_int32), ("n_pack", C.c_int32),
+        ("unpack_hazard", C.c_void_p), ("pack_hazard", C.c_void_p),
     ]
 
 
@@ -197,12 +198,15 @@ def step(w: dict, slot_cap: int | None = None, unpack_cap: int | None = None,
     sl = np.zeros(max(slot_cap, 1), np.int32)
     um = np.zeros(max(unpack_cap, 1), MOVE_DTYPE)
     pm = np.zeros(max(pack_cap, 1), MOVE_DTYPE)
+    uh = np.full(max(unpack_cap, 1), -7, np.int32)
+    ph = np.full(max(pack_cap, 1), -7, np.int32)
     out = Outputs()
     for k in o:
         setattr(out, k, _ptr(o[k]))
     out.slot_list, out.slot_list_capacity = _ptr(sl), slot_cap
     out.unpack_moves, out.unpack_capacity = _ptr(um), unpack_cap
     out.pack_moves, out.pack_capacity = _ptr(pm), pack_cap
+    out.unpack_hazard, out.pack_hazard = _ptr(uh), _ptr(ph)
     args = [_ptr(req[k]) for k, _ in REQ_FIELDS] + [_ptr(ro), _ptr(slots)]
     rc = lib().cref_step(n, *args, n_free, _ptr(free), C.byref(make_params(p)), C.byref(out))
     res = {k: v[:n] for k, v in o.items()}
@@ -213,6 +217,9 @@ def step(w: dict, slot_cap: int | None = None, unpack_cap: int | None = None,
     res["slot_list"] = sl[: min(out.n_slot_list, slot_cap)]
     res["unpack_moves"] = um[: min(out.n_unpack, unpack_cap)]
     res["pack_moves"] = pm[: min(out.n_pack, pack_cap)]
+    if rc == OK:
+        res["unpack_hazard"] = uh[: out.n_unpack]
+        res["pack_hazard"] = ph[: out.n_pack]
     return res
 
 

@@ -21,7 +21,7 @@ INFO_STATUS, INFO_N_ADMITTED, INFO_N_SLOT_LIST, INFO_N_UNPACK, INFO_N_PACK = 0, 
 INFO_LEN = 8
 
 EXPORTED = ["cascade_step_workspace_bytes", "cascade_step", "cascade_pack", "cascade_unpack",
-            "cascade_strerror"]
+            "cascade_pack_unpack", "cascade_strerror"]
 
 
 class Requests(C.Structure):
@@ -65,6 +65,7 @@ class Outputs(C.Structure):
         ("slot_list", C.c_void_p), ("unpack_moves", C.c_void_p), ("pack_moves", C.c_void_p),
         ("slot_list_capacity", C.c_int32), ("unpack_capacity", C.c_int32),
         ("pack_capacity", C.c_int32), ("info", C.c_void_p),
+        ("unpack_hazard", C.c_void_p), ("pack_hazard", C.c_void_p),
     ]
 
 
@@ -96,6 +97,13 @@ def load() -> C.CDLL:
             f.restype = C.c_int
             f.argtypes = [C.POINTER(KvPool), C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
                           C.c_int32, C.c_void_p, C.c_void_p]
+        L.cascade_pack_unpack.restype = C.c_int
+        L.cascade_pack_unpack.argtypes = [C.POINTER(KvPool),
+                                          C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                                          C.c_int32, C.c_void_p,
+                                          C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                                          C.c_int32, C.c_void_p,
+                                          C.c_void_p, C.c_void_p]
         L.cascade_strerror.restype = C.c_char_p
         L.cascade_strerror.argtypes = [C.c_int]
         _lib = L
@@ -125,6 +133,18 @@ def cascade_unpack(pool: KvPool, staging: int, staging_slots: int, moves: int, n
     return int(load().cascade_unpack(C.byref(pool), C.c_void_p(staging), staging_slots,
                                      C.c_void_p(moves), C.c_void_p(n_moves_dev), max_moves,
                                      C.c_void_p(status_dev), C.c_void_p(stream)))
+
+
+def cascade_pack_unpack(pool: KvPool, pack_staging: int, pack_staging_slots: int,
+                        pack_moves: int, n_pack_dev: int, max_pack: int, pack_hazard: int,
+                        unpack_staging: int, unpack_staging_slots: int, unpack_moves: int,
+                        n_unpack_dev: int, max_unpack: int, unpack_hazard: int,
+                        status_dev: int, stream: int) -> int:
+    v = C.c_void_p
+    return int(load().cascade_pack_unpack(
+        C.byref(pool), v(pack_staging), pack_staging_slots, v(pack_moves), v(n_pack_dev),
+        max_pack, v(pack_hazard), v(unpack_staging), unpack_staging_slots, v(unpack_moves),
+        v(n_unpack_dev), max_unpack, v(unpack_hazard), v(status_dev), v(stream)))
 
 
 def cascade_strerror(code: int) -> str:

@@ -13,6 +13,11 @@
 // chunks with up to kMaxGrid workgroups (about 32 per CU): measured on MI355X,
 // a plain copy peaks near that occupancy.  The move count is read on the
 // device, so the step's output count drives the copy without a host sync.
+//
+// The fused entry point interleaves the chunks of both lists.  On MI355X a
+// stream of scattered pool reads (spill) and one of scattered pool writes
+// (restore) sharing the chip move more bytes per second than either alone,
+// and one launch has one tail instead of two.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -28,6 +33,83 @@ constexpr long long kMaxGrid = 8192;
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 
+// One chunk of vecs 16-byte vectors; thread t moves vectors t + kBlock*i, so
+// a thread that copies the same chunk twice touches the same addresses.
+__device__ __forceinline__ void copy_chunk(const char *src_c, char *dst_c, int vecs) {
+  const v4i *src = reinterpret_cast<const v4i *>(src_c);
+  v4i *dst = reinterpret_cast<v4i *>(dst_c);
+  for (int base = 0; base < vecs; base += kBlock * kUnroll) {
+    v4i t[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int k = base + u * kBlock + threadIdx.x;
+      if (k < vecs) t[u] = __builtin_nontemporal_load(src + k);
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int k = base + u * kBlock + threadIdx.x;
+      if (k < vecs) __builtin_nontemporal_store(t[u], dst + k);
+    }
+  }
+}
+
+// A spill and the restore into the same chunk in one pass: both loads of a
+// batch are issued together, then the spill's stores, then the restore's.
+// Each thread stores to a pool address only after its own load of that
+// address has returned (the spill's store needed the loaded value), so the
+// spill reads the old bytes.  Half the unroll per stream keeps the same
+// kUnroll vectors in flight and the kernel's register count at the level
+// of a plain copy (full occupancy).
+__device__ __forceinline__ void copy_pair(char *pool_c, char *spill_c, const char *fill_c,
+                                          int vecs) {
+  constexpr int kHalf = kUnroll / 2;
+  v4i *pool = reinterpret_cast<v4i *>(pool_c);
+  v4i *spill = reinterpret_cast<v4i *>(spill_c);
+  const v4i *fill = reinterpret_cast<const v4i *>(fill_c);
+  for (int base = 0; base < vecs; base += kBlock * kHalf) {
+    v4i a[kHalf], b[kHalf];
+#pragma unroll
+    for (int u = 0; u < kHalf; ++u) {
+      const int k = base + u * kBlock + threadIdx.x;
+      if (k < vecs) {
+        a[u] = __builtin_nontemporal_load(pool + k);
+        b[u] = __builtin_nontemporal_load(fill + k);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kHalf; ++u) {
+      const int k = base + u * kBlock + threadIdx.x;
+      if (k < vecs) __builtin_nontemporal_store(a[u], spill + k);
+    }
+#pragma unroll
+    for (int u = 0; u < kHalf; ++u) {
+      const int k = base + u * kBlock + threadIdx.x;
+      if (k < vecs) __builtin_nontemporal_store(b[u], pool + k);
+    }
+  }
+}
+
+__device__ __forceinline__ char *pool_chunk(const cascade_kv_pool_t &pool, int slot, int l,
+                                            int kv) {
+  return static_cast<char *>(pool.base) + (long long)l * pool.layer_stride +
+         (long long)kv * pool.kv_stride + (long long)slot * pool.slot_stride;
+}
+
+__device__ __forceinline__ char *staging_chunk(char *staging, const cascade_kv_pool_t &pool,
+                                               int slot, int l, int kv) {
+  return staging + (((long long)slot * pool.num_layers + l) * 2 + kv) * pool.chunk_bytes;
+}
+
+__device__ __forceinline__ bool move_ok(const cascade_move_t &mv, int num_slots,
+                                        int staging_slots) {
+  return (unsigned)mv.pool_slot < (unsigned)num_slots &&
+         (unsigned)mv.staging_slot < (unsigned)staging_slots;
+}
+
+__device__ __forceinline__ void flag_bad(int *status) {
+  if (threadIdx.x == 0 && status) *status = CASCADE_EINVAL;
+}
+
 template <bool kToStaging>
 __global__ __launch_bounds__(kBlock) void kvcopy_kernel(cascade_kv_pool_t pool, char *staging,
                                                         int staging_slots,
@@ -38,61 +120,129 @@ __global__ __launch_bounds__(kBlock) void kvcopy_kernel(cascade_kv_pool_t pool, 
   if (nm <= 0) return;
   const int per_move = 2 * pool.num_layers;
   const long long total = (long long)nm * per_move;
-  const long long cb = pool.chunk_bytes;
-  const int vecs = (int)(cb >> 4);
+  const int vecs = (int)(pool.chunk_bytes >> 4);
   for (long long c = blockIdx.x; c < total; c += gridDim.x) {
     const int m = (int)(c / per_move);
     const int r = (int)(c - (long long)m * per_move);
     const int l = r >> 1, kv = r & 1;
     const cascade_move_t mv = moves[m];
-    if ((unsigned)mv.pool_slot >= (unsigned)pool.num_slots ||
-        (unsigned)mv.staging_slot >= (unsigned)staging_slots) {
-      if (threadIdx.x == 0 && status) *status = CASCADE_EINVAL;
+    if (!move_ok(mv, pool.num_slots, staging_slots)) {
+      flag_bad(status);
       continue;
     }
-    char *pc = static_cast<char *>(pool.base) + (long long)l * pool.layer_stride +
-               (long long)kv * pool.kv_stride + (long long)mv.pool_slot * pool.slot_stride;
-    char *sc = staging + (((long long)mv.staging_slot * pool.num_layers + l) * 2 + kv) * cb;
-    const v4i *src = reinterpret_cast<const v4i *>(kToStaging ? pc : sc);
-    v4i *dst = reinterpret_cast<v4i *>(kToStaging ? sc : pc);
-    for (int base = 0; base < vecs; base += kBlock * kUnroll) {
-      v4i t[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int k = base + u * kBlock + threadIdx.x;
-        if (k < vecs) t[u] = __builtin_nontemporal_load(src + k);
+    char *pc = pool_chunk(pool, mv.pool_slot, l, kv);
+    char *sc = staging_chunk(staging, pool, mv.staging_slot, l, kv);
+    copy_chunk(kToStaging ? pc : sc, kToStaging ? sc : pc, vecs);
+  }
+}
+
+// Pack and unpack chunks interleaved: the common range holds one pack and
+// one unpack chunk per item pair, the rest belongs to the longer list.
+// Unpack move m paired with pack move j (phz[j] == m and uhz[m] == j) is
+// copied by the item of chunk (j, l, kv), in the same pass as the spill and
+// by the same threads, each of which has read the slot's old bytes before it
+// overwrites them: the wait is inside the thread, none crosses workgroups.
+// The pairing test reads the same two words from both sides, so every
+// unpack move is copied exactly once.
+__global__ __launch_bounds__(kBlock) void kvmove_kernel(
+    cascade_kv_pool_t pool, char *pst, int pst_slots, const cascade_move_t *__restrict__ pm,
+    const int *__restrict__ pn_dev, int pmax, const int *__restrict__ phz, char *ust,
+    int ust_slots, const cascade_move_t *__restrict__ um, const int *__restrict__ un_dev,
+    int umax, const int *__restrict__ uhz, int *status) {
+  const int np = max(0, min(*pn_dev, pmax));
+  const int nu = max(0, min(*un_dev, umax));
+  const int per_move = 2 * pool.num_layers;
+  const long long tp = (long long)np * per_move, tu = (long long)nu * per_move;
+  const long long both = 2 * (tp < tu ? tp : tu), total = tp + tu;
+  const int vecs = (int)(pool.chunk_bytes >> 4);
+  // the grid is even (2 * num_layers divides every chunk count), so c and
+  // c ^ 1 fall in the same iteration: flipping the low bit on odd iterations
+  // is a bijection that makes every workgroup alternate between pack and
+  // unpack items, whatever share of the pack items carries a paired unpack
+  const long long flip = (gridDim.x & 1) == 0 ? 1 : 0;
+  long long it = 0;
+  for (long long c = blockIdx.x; c < total; c += gridDim.x, ++it) {
+    bool is_pack;
+    long long ci;
+    if (c < both) {
+      const long long cc = c ^ (it & flip);
+      is_pack = (cc & 1) == 0;
+      ci = cc >> 1;
+    } else {
+      is_pack = tp > tu;
+      ci = c - both + (both >> 1);
+    }
+    const int mi = (int)(ci / per_move);
+    const int r = (int)(ci - (long long)mi * per_move);
+    const int l = r >> 1, kv = r & 1;
+    // the item's move and hazard word are requested together
+    const cascade_move_t mv = is_pack ? pm[mi] : um[mi];
+    const int partner = is_pack ? phz[mi] : uhz[mi];
+    if (is_pack) {
+      const bool ok = move_ok(mv, pool.num_slots, pst_slots);
+      if (!ok) flag_bad(status);
+      bool paired = false;
+      cascade_move_t mu;
+      if (partner >= 0 && partner < nu) {
+        mu = um[partner];
+        paired = uhz[partner] == mi;
       }
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int k = base + u * kBlock + threadIdx.x;
-        if (k < vecs) __builtin_nontemporal_store(t[u], dst + k);
+      if (paired && !move_ok(mu, pool.num_slots, ust_slots)) {
+        flag_bad(status);
+        paired = false;  // the restore is skipped; the spill still runs
       }
+      if (ok && paired && mu.pool_slot == mv.pool_slot) {
+        copy_pair(pool_chunk(pool, mv.pool_slot, l, kv),
+                  staging_chunk(pst, pool, mv.staging_slot, l, kv),
+                  staging_chunk(ust, pool, mu.staging_slot, l, kv), vecs);
+      } else {
+        if (ok)
+          copy_chunk(pool_chunk(pool, mv.pool_slot, l, kv),
+                     staging_chunk(pst, pool, mv.staging_slot, l, kv), vecs);
+        if (paired)
+          copy_chunk(staging_chunk(ust, pool, mu.staging_slot, l, kv),
+                     pool_chunk(pool, mu.pool_slot, l, kv), vecs);
+      }
+    } else {
+      if (partner >= 0 && partner < np && phz[partner] == mi) continue;  // after its pack
+      if (move_ok(mv, pool.num_slots, ust_slots))
+        copy_chunk(staging_chunk(ust, pool, mv.staging_slot, l, kv),
+                   pool_chunk(pool, mv.pool_slot, l, kv), vecs);
+      else
+        flag_bad(status);
     }
   }
 }
 
-bool geometry_ok(const cascade_kv_pool_t *p, const void *staging, int32_t staging_slots,
-                 const cascade_move_t *moves, const int32_t *n_dev, int32_t max_moves) {
-  if (!p || !staging || !n_dev || max_moves < 0 || staging_slots < 0) return false;
-  if (max_moves > 0 && !moves) return false;
-  if (!p->base || p->num_layers < 1 || p->num_slots < 0) return false;
+bool pool_ok(const cascade_kv_pool_t *p) {
+  if (!p || !p->base || p->num_layers < 1 || p->num_slots < 0) return false;
   if (p->chunk_bytes < 16 || (p->chunk_bytes & 15) || p->chunk_bytes > (1ll << 30)) return false;
   if ((p->layer_stride & 15) || (p->kv_stride & 15) || (p->slot_stride & 15)) return false;
   if (p->layer_stride < 0 || p->kv_stride < 0 || p->slot_stride < 0) return false;
-  if (((uintptr_t)p->base & 15) || ((uintptr_t)staging & 15)) return false;
-  return true;
+  return ((uintptr_t)p->base & 15) == 0;
+}
+
+bool list_ok(const void *staging, int32_t staging_slots, const cascade_move_t *moves,
+             const int32_t *n_dev, int32_t max_moves) {
+  if (!staging || !n_dev || max_moves < 0 || staging_slots < 0) return false;
+  if (max_moves > 0 && !moves) return false;
+  return ((uintptr_t)staging & 15) == 0;
+}
+
+int grid_for(const cascade_kv_pool_t *pool, long long moves) {
+  const long long chunks = moves * 2 * pool->num_layers;
+  return (int)std::max<long long>(1, std::min(chunks, kMaxGrid));
 }
 
 template <bool kToStaging>
 int launch(const cascade_kv_pool_t *pool, const void *staging, int32_t staging_slots,
            const cascade_move_t *moves, const int32_t *n_dev, int32_t max_moves,
            int32_t *status, void *stream) {
-  if (!geometry_ok(pool, staging, staging_slots, moves, n_dev, max_moves)) return CASCADE_EINVAL;
+  if (!pool_ok(pool) || !list_ok(staging, staging_slots, moves, n_dev, max_moves))
+    return CASCADE_EINVAL;
   if (max_moves == 0) return CASCADE_OK;
-  const long long chunks = (long long)max_moves * 2 * pool->num_layers;
-  const int grid = (int)std::max<long long>(1, std::min(chunks, kMaxGrid));
-  hipLaunchKernelGGL(kvcopy_kernel<kToStaging>, dim3(grid), dim3(kBlock), 0,
-                     static_cast<hipStream_t>(stream), *pool,
+  hipLaunchKernelGGL(kvcopy_kernel<kToStaging>, dim3(grid_for(pool, max_moves)), dim3(kBlock),
+                     0, static_cast<hipStream_t>(stream), *pool,
                      const_cast<char *>(static_cast<const char *>(staging)), staging_slots, moves,
                      n_dev, max_moves, status);
   return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
@@ -113,4 +263,29 @@ extern "C" int cascade_unpack(const cascade_kv_pool_t *pool, const void *staging
                               void *stream) {
   return launch<false>(pool, staging, staging_slots, moves, n_moves_dev, max_moves, status_dev,
                        stream);
+}
+
+extern "C" int cascade_pack_unpack(const cascade_kv_pool_t *pool, void *pack_staging,
+                                   int32_t pack_staging_slots, const cascade_move_t *pack_moves,
+                                   const int32_t *n_pack_dev, int32_t max_pack,
+                                   const int32_t *pack_hazard, const void *unpack_staging,
+                                   int32_t unpack_staging_slots,
+                                   const cascade_move_t *unpack_moves,
+                                   const int32_t *n_unpack_dev, int32_t max_unpack,
+                                   const int32_t *unpack_hazard, int32_t *status_dev,
+                                   void *stream) {
+  if (!pool_ok(pool) ||
+      !list_ok(pack_staging, pack_staging_slots, pack_moves, n_pack_dev, max_pack) ||
+      !list_ok(unpack_staging, unpack_staging_slots, unpack_moves, n_unpack_dev, max_unpack))
+    return CASCADE_EINVAL;
+  if ((max_pack > 0 && !pack_hazard) || (max_unpack > 0 && !unpack_hazard)) return CASCADE_EINVAL;
+  if (max_pack == 0 && max_unpack == 0) return CASCADE_OK;
+  hipLaunchKernelGGL(kvmove_kernel, dim3(grid_for(pool, (long long)max_pack + max_unpack)),
+                     dim3(kBlock), 0, static_cast<hipStream_t>(stream), *pool,
+                     static_cast<char *>(pack_staging), pack_staging_slots, pack_moves,
+                     n_pack_dev, max_pack, pack_hazard,
+                     const_cast<char *>(static_cast<const char *>(unpack_staging)),
+                     unpack_staging_slots, unpack_moves, n_unpack_dev, max_unpack, unpack_hazard,
+                     status_dev);
+  return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
 }

@@ -108,6 +108,7 @@ struct Outs {                     // output pointers the scan writes
   int *order, *granted, *restore, *alloc_begin, *alloc_count, *admitted, *slot_list;
   uint8_t *action;
   cascade_move_t *unpack, *pack;
+  int *unpack_hazard, *pack_hazard;  // may be null
   int sl_cap, unpack_cap, pack_cap;
 };
 
@@ -708,6 +709,26 @@ struct FinishLds {
   int n_victims, counts[2];
 };
 
+// Restore entry k, staged in LDS for k < kRestoreCap.
+__device__ __forceinline__ RestoreEnt restore_entry(const FinishLds &L, const RestoreEnt *rl,
+                                                    int k) {
+  return k < kRestoreCap ? L.rl[k] : rl[k];
+}
+
+// The unpack move that writes slot-list entry s, or -1: restore entries are
+// in admitted order, so their allocation offsets increase and the entry that
+// covers s is the last one starting at or before it.
+__device__ int unpack_move_at(long long s, int nr, const FinishLds &L, const RestoreEnt *rl) {
+  if (nr <= 0 || restore_entry(L, rl, 0).alloc_off > s) return -1;
+  int lo = 0, hi = nr - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (restore_entry(L, rl, mid).alloc_off <= s) lo = mid; else hi = mid - 1;
+  }
+  const RestoreEnt e = restore_entry(L, rl, lo);
+  return s < (long long)e.alloc_off + e.blocks ? e.stage_off + (int)(s - e.alloc_off) : -1;
+}
+
 // Loads are grouped so that the workgroup waits on memory three times: the
 // totals, running-prefill records, restore list and free list together; the
 // victims' rows; the slot-list entries of restores past the free list.
@@ -783,6 +804,7 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
             m.pool_slot = slot;
             m.staging_slot = (int)(pbase + b);
             o.pack[pbase + b] = m;
+            if (o.pack_hazard) o.pack_hazard[pbase + b] = unpack_move_at(sbase + b, nr, L, rl);
           }
         }
       }
@@ -831,6 +853,8 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
         mv.pool_slot = slot[u];
         mv.staging_slot = (int)(pb + b);
         o.pack[pb + b] = mv;
+        // the restore that receives this slot must wait for this spill
+        if (o.pack_hazard) o.pack_hazard[pb + b] = unpack_move_at(sb, nr, L, rl);
       }
     }
   }
@@ -855,6 +879,17 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
                                                                        : o.slot_list[s]);
     mv.staging_slot = (int)m;
     o.unpack[m] = mv;
+    if (o.unpack_hazard) o.unpack_hazard[m] = -1;
+  }
+  // the pairs, from the pack side (the barrier orders these stores after the
+  // defaults above and makes the pack-side entries visible)
+  __syncthreads();
+  if (o.unpack_hazard && o.pack_hazard) {
+    const int np = min(L.counts[1], o.pack_cap);
+    for (int j = t; j < np; j += kBlock) {
+      const int m = o.pack_hazard[j];
+      if (m >= 0 && m < o.unpack_cap) o.unpack_hazard[m] = j;
+    }
   }
   if (t == 0) {
     const long long nsl = (long long)n_free + L.counts[0];
@@ -1330,6 +1365,7 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
       (out->unpack_capacity > 0 && !out->unpack_moves) ||
       (out->pack_capacity > 0 && !out->pack_moves))
     return CASCADE_EINVAL;
+  if ((out->unpack_hazard == nullptr) != (out->pack_hazard == nullptr)) return CASCADE_EINVAL;
   if (((uintptr_t)workspace & 255) != 0) return CASCADE_EINVAL;
   const Layout L = make_layout(n);
   if (workspace_bytes < L.total) return CASCADE_ENOSPC;
@@ -1370,6 +1406,8 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   o.action = out->action;
   o.unpack = out->unpack_moves;
   o.pack = out->pack_moves;
+  o.unpack_hazard = out->unpack_hazard;
+  o.pack_hazard = out->pack_hazard;
   o.sl_cap = out->slot_list_capacity;
   o.unpack_cap = out->unpack_capacity;
   o.pack_cap = out->pack_capacity;

@@ -68,6 +68,8 @@ class DeviceStep:
         self.slot_list = z(self.caps[0], torch.int32)
         self.unpack_moves = z(4 * max(self.caps[1], 1), torch.int32)
         self.pack_moves = z(4 * max(self.caps[2], 1), torch.int32)
+        self.unpack_hazard = z(self.caps[1], torch.int32)
+        self.pack_hazard = z(self.caps[2], torch.int32)
         self.info = z(cx.INFO_LEN, torch.int32)
         self.ws_bytes = cx.cascade_step_workspace_bytes(n)
         self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=self.device)
@@ -82,7 +84,8 @@ class DeviceStep:
             o["tokens_granted"].data_ptr(), o["restore_blocks"].data_ptr(), o["order"].data_ptr(),
             o["alloc_begin"].data_ptr(), o["alloc_count"].data_ptr(), o["admitted"].data_ptr(),
             self.slot_list.data_ptr(), self.unpack_moves.data_ptr(), self.pack_moves.data_ptr(),
-            self.caps[0], self.caps[1], self.caps[2], self.info.data_ptr())
+            self.caps[0], self.caps[1], self.caps[2], self.info.data_ptr(),
+            self.unpack_hazard.data_ptr(), self.pack_hazard.data_ptr())
 
     def run(self, stream=None) -> int:
         """Enqueue one step; returns the host-side return code."""
@@ -113,6 +116,8 @@ class DeviceStep:
         pm = self.pack_moves.cpu().numpy().view(MOVE_DTYPE)
         res["unpack_moves"] = um[:min(res["n_unpack"], self.caps[1])]
         res["pack_moves"] = pm[:min(res["n_pack"], self.caps[2])]
+        res["unpack_hazard"] = self.unpack_hazard.cpu().numpy()[:len(res["unpack_moves"])]
+        res["pack_hazard"] = self.pack_hazard.cpu().numpy()[:len(res["pack_moves"])]
         return res
 
 
@@ -122,15 +127,21 @@ def kv_pool_struct(base_ptr: int, geom: dict) -> cx.KvPool:
                      int(geom["kv_stride"]), int(geom["slot_stride"]))
 
 
-def fill_pattern_(t, seed: int, word_offset: int = 0, chunk_words: int = 1 << 26) -> None:
+def fill_pattern_(t, seed: int, word_offset: int = 0, chunk_words: int = 1 << 26,
+                  progress=None) -> None:
     """Fill a uint8 device tensor with the counter-based 32-bit pattern of
-    ``synth.hash32_torch`` (word k holds hash32(word_offset + k, seed))."""
+    ``synth.hash32_torch`` (word k holds hash32(word_offset + k, seed)).
+    ``progress(msg)``, if given, is called about every 16 GB."""
     torch = _torch()
     from .synth import hash32_torch
     w = t.view(torch.int32)
     nw = w.numel()
-    for s in range(0, nw, chunk_words):
+    every = max(1, (4 << 30) // chunk_words)
+    for k, s in enumerate(range(0, nw, chunk_words)):
         e = min(nw, s + chunk_words)
         idx = torch.arange(word_offset + s, word_offset + e, device=t.device, dtype=torch.int64)
         h = hash32_torch(idx, seed)
         w[s:e] = (h - ((h >> 31) << 32)).to(torch.int32)
+        if progress is not None and (k + 1) % every == 0:
+            torch.cuda.synchronize(t.device)
+            progress(f"filled {4 * e / 1e9:.0f} of {4 * nw / 1e9:.0f} GB")

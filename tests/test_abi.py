@@ -135,6 +135,9 @@ def test_host_checks_return_einval_without_launch(lib):
     o2 = cascade.Outputs.from_buffer_copy(out)
     o2.pack_capacity = -1
     assert f(out=o2) == cascade.EINVAL
+    o2 = cascade.Outputs.from_buffer_copy(out)
+    o2.unpack_hazard = 4096                           # one hazard array without the other
+    assert f(out=o2) == cascade.EINVAL
     assert f(ws=(1 << 20) + 8) == cascade.EINVAL       # workspace not 256-byte aligned
     assert f(wsb=ws - 1) == cascade.ENOSPC
 
@@ -158,6 +161,27 @@ def test_copy_host_checks(lib):
         assert call(fn, pool=cascade.KvPool(4096, 2, 10, 24, 0, 0, 0)) == cascade.EINVAL
         assert call(fn, pool=cascade.KvPool(4096, 2, 10, 32, 8, 0, 0)) == cascade.EINVAL
         assert call(fn, max_moves=0) == cascade.OK                   # nothing to launch
+
+
+def test_fused_copy_host_checks(lib):
+    pool = cascade.KvPool(4096, 32, 10, 32768, 65536, 32768, 32768)
+    n = C.c_int32(1)
+    nd = C.addressof(n)
+    ok = [pool, 4096, 4, 4096, nd, 4, 4096, 4096, 4, 4096, nd, 4, 4096, 0, 0]
+
+    def call(**kw):
+        a = list(ok)
+        for i, v in kw.items():
+            a[int(i[1:])] = v
+        return cascade.cascade_pack_unpack(*a)
+    assert call(a1=0) == cascade.EINVAL                  # pack staging missing
+    assert call(a7=4100) == cascade.EINVAL               # unpack staging misaligned
+    assert call(a6=0) == cascade.EINVAL                  # pack hazards missing
+    assert call(a12=0) == cascade.EINVAL                 # unpack hazards missing
+    assert call(a5=-1) == cascade.EINVAL
+    assert call(a0=cascade.KvPool(4096, 2, 10, 24, 0, 0, 0)) == cascade.EINVAL
+    assert call(a5=0, a11=0) == cascade.OK               # nothing to launch
+    assert call(a5=0, a6=0, a11=0, a12=0) == cascade.OK  # empty lists need no hazards
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):

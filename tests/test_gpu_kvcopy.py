@@ -181,3 +181,182 @@ def test_headline_step_moves_full_size(dev):
         assert np.array_equal(got.view(np.uint32), synth.hash32_np(words, 1))
     del pool, st_in, st_out
     torch.cuda.empty_cache()
+
+
+# ------------------------------------------------- pack and unpack in one launch
+
+def _hazards(pm, um):
+    """Copy-order pairs by pool slot, the way the step defines them."""
+    ph = np.full(len(pm), -1, np.int32)
+    uh = np.full(len(um), -1, np.int32)
+    for j in range(len(pm)):
+        for m in range(len(um)):
+            if pm["pool_slot"][j] == um["pool_slot"][m]:
+                ph[j], uh[m] = m, j
+    return ph, uh
+
+
+def _fused(dev, pool_t, geom, pst, np_slots, pm, ph, ust, nu_slots, um, uh, caps=None):
+    import torch
+    from paper_2608_06557_amd import cascade
+    cp = len(pm) if caps is None else caps[0]
+    cu = len(um) if caps is None else caps[1]
+    dv = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int32).copy()
+                                    if a.size else np.zeros(4, np.int32)).cuda()
+    pm_d, um_d, ph_d, uh_d = dv(pm), dv(um), dv(ph), dv(uh)
+    np_d = torch.tensor([len(pm)], dtype=torch.int32, device="cuda")
+    nu_d = torch.tensor([len(um)], dtype=torch.int32, device="cuda")
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pl = dev.kv_pool_struct(pool_t.data_ptr(), geom)
+    rc = cascade.cascade_pack_unpack(pl, pst.data_ptr(), np_slots, pm_d.data_ptr(),
+                                     np_d.data_ptr(), cp, ph_d.data_ptr(), ust.data_ptr(),
+                                     nu_slots, um_d.data_ptr(), nu_d.data_ptr(), cu,
+                                     uh_d.data_ptr(), status.data_ptr(), dev.stream_handle())
+    torch.cuda.synchronize()
+    return rc, int(status.item())
+
+
+@pytest.mark.parametrize("layout", ["layer_major", "block_major"])
+@pytest.mark.parametrize("chunk", [16, 48, 8192])
+@pytest.mark.parametrize("n_pack,n_unpack,shared", [(23, 17, 9), (5, 31, 5), (31, 0, 0),
+                                                    (0, 12, 0), (40, 40, 40), (1, 1, 1)])
+def test_fused_equals_pack_then_unpack(dev, layout, chunk, n_pack, n_unpack, shared):
+    """One launch gives the bytes of cascade_pack followed by cascade_unpack,
+    also where unpack destinations are pack sources (the shared slots)."""
+    import torch
+    rng = np.random.default_rng(chunk + 7 * n_pack + n_unpack)
+    nb, L = 90, 3
+    g = _geom(layout, nb, L, chunk)
+    perm = rng.permutation(nb).astype(np.int32)
+    p_slots = perm[:n_pack]
+    u_slots = np.concatenate([rng.permutation(p_slots)[:shared],
+                              perm[n_pack:n_pack + n_unpack - shared]]).astype(np.int32)
+    rng.shuffle(u_slots)
+    pm = _moves(p_slots, rng.permutation(n_pack + 3)[:n_pack].astype(np.int32))
+    um = _moves(u_slots, rng.permutation(n_unpack + 2)[:n_unpack].astype(np.int32))
+    ph, uh = _hazards(pm, um)
+    assert (uh >= 0).sum() == shared
+    pool_h = rng.integers(0, 256, 2 * L * nb * chunk, dtype=np.uint8)
+    pst_h = np.zeros((n_pack + 3) * 2 * L * chunk, np.uint8)
+    ust_h = rng.integers(0, 256, (n_unpack + 2) * 2 * L * chunk, dtype=np.uint8)
+    exp_pool, exp_pst = pool_h.copy(), pst_h.copy()
+    ref.pack(exp_pool, g, exp_pst, pm)
+    ref.unpack(exp_pool, g, ust_h, um)
+    pool = torch.from_numpy(pool_h.copy()).cuda()
+    pst = torch.from_numpy(pst_h.copy()).cuda()
+    ust = torch.from_numpy(ust_h.copy()).cuda()
+    rc, status = _fused(dev, pool, g, pst, n_pack + 3, pm, ph, ust, n_unpack + 2, um, uh)
+    assert rc == 0 and status == 0
+    assert np.array_equal(pst.cpu().numpy(), exp_pst)
+    assert np.array_equal(pool.cpu().numpy(), exp_pool)
+
+
+def test_fused_any_hazard_arrays_copy_every_move_once(dev):
+    """Hazard arrays that declare no real pair (garbage, out of range, or
+    one-sided) still leave every move copied exactly once."""
+    import torch
+    rng = np.random.default_rng(3)
+    nb, L, chunk = 60, 2, 64
+    g = _geom("layer_major", nb, L, chunk)
+    perm = rng.permutation(nb).astype(np.int32)
+    pm, um = _moves(perm[:20]), _moves(perm[20:45])
+    pool_h = rng.integers(0, 256, 2 * L * nb * chunk, dtype=np.uint8)
+    ust_h = rng.integers(0, 256, 25 * 2 * L * chunk, dtype=np.uint8)
+    exp_pool, exp_pst = pool_h.copy(), np.zeros(20 * 2 * L * chunk, np.uint8)
+    ref.pack(exp_pool, g, exp_pst, pm)
+    ref.unpack(exp_pool, g, ust_h, um)
+    cases = [(rng.integers(-5, 40, 20), rng.integers(-5, 40, 25)),
+             (np.arange(20), np.full(25, -1)),            # pack side only
+             (np.full(20, -1), np.arange(25) % 20),       # unpack side only
+             (np.full(20, 1 << 30), np.full(25, -(1 << 30)))]
+    for ph, uh in cases:
+        pool = torch.from_numpy(pool_h.copy()).cuda()
+        pst = torch.zeros(exp_pst.size, dtype=torch.uint8, device="cuda")
+        ust = torch.from_numpy(ust_h.copy()).cuda()
+        rc, status = _fused(dev, pool, g, pst, 20, pm, ph.astype(np.int32), ust, 25, um,
+                            uh.astype(np.int32))
+        assert rc == 0 and status == 0
+        assert np.array_equal(pst.cpu().numpy(), exp_pst)
+        assert np.array_equal(pool.cpu().numpy(), exp_pool)
+
+
+def test_fused_bad_moves_skipped(dev):
+    import torch
+    from paper_2608_06557_amd import cascade
+    nb, L, chunk = 8, 2, 64
+    g = _geom("layer_major", nb, L, chunk)
+    pool_h = (np.arange(2 * L * nb * chunk) % 251).astype(np.uint8)
+    pm = _moves(np.array([1, 9, 3], np.int32), np.array([0, 1, 5], np.int32))   # 9, 5 bad
+    um = _moves(np.array([3, -2, 6], np.int32), np.array([0, 1, 2], np.int32))  # -2 bad
+    ph, uh = _hazards(pm, um)            # pack 2 (bad staging) pairs with unpack 0
+    ust_h = np.full(3 * 2 * L * chunk, 77, np.uint8)
+    pool = torch.from_numpy(pool_h.copy()).cuda()
+    pst = torch.zeros(3 * 2 * L * chunk, dtype=torch.uint8, device="cuda")
+    ust = torch.from_numpy(ust_h.copy()).cuda()
+    rc, status = _fused(dev, pool, g, pst, 3, pm, ph, ust, 3, um, uh)
+    assert rc == 0 and status == cascade.EINVAL
+    exp_pool, exp_pst = pool_h.copy(), np.zeros(pst.numel(), np.uint8)
+    ref.pack(exp_pool, g, exp_pst, pm[:1])
+    ref.unpack(exp_pool, g, ust_h, um[[0, 2]])  # the pair's unpack still happens
+    assert np.array_equal(pst.cpu().numpy(), exp_pst)
+    assert np.array_equal(pool.cpu().numpy(), exp_pool)
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_fused_step_moves_full_size(dev, cfg):
+    """The step's own lists at full size (200 GB / 250 GB pools), hazards
+    included: every spilled block that a restore overwrites is checked to
+    hold the old bytes in staging, plus samples of the rest."""
+    import torch
+    import paper_2608_06557_amd.synth as synth
+    w = synth.make_workload(cfg)
+    geom = w["geometry"]
+    d = dev.DeviceStep(w, unpack_cap=geom["num_blocks"], pack_cap=geom["num_blocks"])
+    assert d.run() == 0
+    res = d.fetch()
+    assert res["status"] == 0
+    npk, nup = res["n_pack"], res["n_unpack"]
+    paired = np.flatnonzero(res["pack_hazard"] >= 0)
+    assert len(paired) > 100
+    print(f"config {cfg}: pool {geom['pool_bytes'] / 1e9:.1f} GB, pack {npk}, unpack {nup}, "
+          f"paired {len(paired)}", flush=True)
+    pool = torch.empty(geom["pool_bytes"], dtype=torch.uint8, device="cuda")
+    dev.fill_pattern_(pool, seed=1)
+    blk = 2 * geom["num_layers"] * geom["chunk_bytes"]
+    st_out = torch.zeros(npk * blk, dtype=torch.uint8, device="cuda")
+    st_in = torch.empty(nup * blk, dtype=torch.uint8, device="cuda")
+    dev.fill_pattern_(st_in, seed=2)
+    from paper_2608_06557_amd import cascade
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pl = dev.kv_pool_struct(pool.data_ptr(), geom)
+    assert cascade.cascade_pack_unpack(
+        pl, st_out.data_ptr(), npk, d.pack_moves.data_ptr(), d.n_pack_ptr(), d.caps[2],
+        d.pack_hazard.data_ptr(), st_in.data_ptr(), nup, d.unpack_moves.data_ptr(),
+        d.n_unpack_ptr(), d.caps[1], d.unpack_hazard.data_ptr(), status.data_ptr(),
+        dev.stream_handle()) == 0
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    rng = np.random.default_rng(11)
+    L = geom["num_layers"]
+    cw = geom["chunk_bytes"] // 4
+    pm, um = res["pack_moves"], res["unpack_moves"]
+    sample_p = np.unique(np.concatenate([paired, rng.choice(npk, 24, replace=False)]))
+    for k in sample_p:
+        m = pm[k]
+        for l, kv in [(0, 0), (L - 1, 1), (int(rng.integers(L)), int(rng.integers(2)))]:
+            soff = ((int(m["staging_slot"]) * L + l) * 2 + kv) * cw
+            got = st_out[4 * soff:4 * (soff + cw)].view(torch.int32).cpu().numpy()
+            exp = synth.hash32_np(_chunk_words(geom, int(m["pool_slot"]), l, kv), 1)
+            assert np.array_equal(got.view(np.uint32), exp), (cfg, int(k), l, kv)
+    sample_u = np.unique(np.concatenate([res["pack_hazard"][paired],
+                                         rng.choice(nup, 24, replace=False)]))
+    for k in sample_u:
+        m = um[k]
+        for l, kv in [(0, 1), (L - 1, 0), (int(rng.integers(L)), int(rng.integers(2)))]:
+            words = _chunk_words(geom, int(m["pool_slot"]), l, kv)
+            got = pool[4 * words[0]:4 * (words[-1] + 1)].view(torch.int32).cpu().numpy()
+            soff = ((int(m["staging_slot"]) * L + l) * 2 + kv) * cw
+            exp = synth.hash32_np(np.arange(soff, soff + cw, dtype=np.int64), 2)
+            assert np.array_equal(got.view(np.uint32), exp), (cfg, int(k), l, kv)
+    del pool, st_in, st_out
+    torch.cuda.empty_cache()

@@ -52,6 +52,8 @@ def assert_same(g, o, label=""):
     assert np.array_equal(g["slot_list"], o["slot_list"]), label
     for k in ["unpack_moves", "pack_moves"]:
         assert np.array_equal(g[k].view(np.int32), o[k].view(np.int32)), (label, k)
+    for k in ["unpack_hazard", "pack_hazard"]:
+        assert np.array_equal(g[k], o[k]), (label, k)
 
 
 @pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
@@ -109,6 +111,22 @@ def test_config3_ties_are_stable(dev):
     ties = np.flatnonzero(np.diff(b) == 0)
     assert len(ties) > 1000
     assert_same(g, o, "config 3")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_many_victims_every_restore_in_a_spilled_slot(dev, seed):
+    """No free slots, zero elapsed time: hundreds of running prefills are
+    preempted (more than the finishing workgroup stages in LDS) and every
+    restore lands in a spilled slot, so every unpack move has a hazard."""
+    rng = np.random.default_rng(seed)
+    p = helpers.base_params(token_cap=20000, max_move_blocks=5000, tier2_reserve_q16=0)
+    w = helpers.random_workload(rng, 3000, params=p, n_free=0)
+    w["arrival_ns"] = np.full(3000, p["t_now_ns"], np.int64)
+    g, o = run_both(dev, w)
+    assert_same(g, o, f"victims seed {seed}")
+    victims = np.isin(o["action"], [ref.ACT_PREEMPT_OFFLOAD, ref.ACT_PREEMPT_DROP]).sum()
+    assert victims > 256 and o["n_unpack"] > 300
+    assert np.all(o["unpack_hazard"] >= 0)
 
 
 def test_empty_queue(dev):

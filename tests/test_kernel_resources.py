@@ -1,0 +1,35 @@
+"""Register use of the HBM-bound copy kernels (no GPU): each must keep the
+full 8 waves per SIMD, since every wave in flight holds part of the bytes the
+copy needs to cover HBM latency.  Read from the compiler's resource-usage
+remarks of a gfx950 build of the copy source."""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "paper_2608_06557_amd", "csrc", "cascade_kvcopy.hip")
+
+
+@pytest.mark.skipif(shutil.which("hipcc") is None, reason="hipcc not installed")
+def test_copy_kernels_keep_full_occupancy(tmp_path):
+    cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           "-I", os.path.join(ROOT, "include"), "-c", SRC, "-o", str(tmp_path / "k.o"),
+           "-Rpass-analysis=kernel-resource-usage"]
+    out = subprocess.run(cmd, capture_output=True, text=True, timeout=600)
+    assert out.returncode == 0, out.stderr[-2000:]
+    occ = {}
+    name = None
+    for line in out.stderr.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+        m = re.search(r"Occupancy \[waves/SIMD\]: (\d+)", line)
+        if m and name:
+            occ[name] = int(m.group(1))
+    kernels = {k: v for k, v in occ.items() if "kvcopy_kernel" in k or "kvmove_kernel" in k}
+    assert len(kernels) == 3, occ
+    assert all(v == 8 for v in kernels.values()), kernels

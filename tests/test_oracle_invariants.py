@@ -65,6 +65,24 @@ def _check_invariants(w, r):
     assert r["n_pack"] == int(rows[r["action"] == ref.ACT_PREEMPT_OFFLOAD].sum())
     # every request gets an action; Tier-2 requests are never dropped
     assert np.all((r["action"] >= 1) & (r["action"] <= 6))
+    _check_hazards(r)
+
+
+def _check_hazards(r):
+    """Copy-order hazards by brute force over the two move lists: the pack
+    move reading the slot an unpack move writes, and back; -1 if none."""
+    um, pm = r["unpack_moves"], r["pack_moves"]
+    uh, ph = r["unpack_hazard"], r["pack_hazard"]
+    assert len(uh) == len(um) and len(ph) == len(pm)
+    for m in range(len(um)):
+        js = [j for j in range(len(pm)) if pm["pool_slot"][j] == um["pool_slot"][m]]
+        assert uh[m] == (js[0] if js else -1)
+    for j in range(len(pm)):
+        ms = [m for m in range(len(um)) if um["pool_slot"][m] == pm["pool_slot"][j]]
+        assert ph[j] == (ms[0] if ms else -1)
+    # pairs are mutual
+    for m in np.flatnonzero(uh >= 0):
+        assert ph[uh[m]] == m
 
 
 @settings(max_examples=300, deadline=None)
@@ -85,6 +103,26 @@ def test_invariants_on_synthetic_configs():
     for cfg in range(4):
         w = synth.make_workload(cfg, n=2048)
         _check_invariants(w, ref.step(w))
+
+
+def test_hazards_present_on_tiny_config():
+    """The tiny workload hands preempted requests' slots to restores, so the
+    copy order matters there: every such slot is a victim's slot that the
+    step spills (Section 4.4) and a restore then receives."""
+    import paper_2608_06557_amd.synth as synth
+    w = synth.make_workload(0)
+    r = ref.step(w)
+    _check_hazards(r)
+    uh = r["unpack_hazard"]
+    assert (uh >= 0).sum() > 10
+    nf = len(w["free_slots"])
+    sl = r["slot_list"]
+    victims_region = set(sl[nf:].tolist())
+    for m in np.flatnonzero(uh >= 0):
+        assert int(r["unpack_moves"]["pool_slot"][m]) in victims_region
+    for m in np.flatnonzero(uh < 0):
+        s = int(r["unpack_moves"]["pool_slot"][m])
+        assert s in set(sl[:nf].tolist()) or s not in set(r["pack_moves"]["pool_slot"].tolist())
 
 
 def test_empty_queue():
