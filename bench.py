@@ -40,7 +40,7 @@ WORKLOADS = {
 }
 
 
-def measured_traffic(cfg, layout, kernel):
+def measured_traffic(cfg, layout, kernel, chunk_bytes):
     """HBM bytes per KV-copy launch from the committed rocprofv3 counter
     passes (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads for a
     plain copy of known size), or None when the workload or kernel differs or
@@ -53,7 +53,8 @@ def measured_traffic(cfg, layout, kernel):
         src = open(os.path.join(ROOT, rec["source"]), "rb").read()
     except (OSError, IndexError, ValueError, KeyError):
         return None
-    if cfg != 2 or layout != "layer_major" or rec.get("kernel") != kernel:
+    if (cfg != 2 or layout != "layer_major" or chunk_bytes != 32768
+            or rec.get("kernel") != kernel):
         return None
     if hashlib.sha256(src).hexdigest() != rec["source_sha256"]:
         return None
@@ -72,6 +73,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--layout", default="layer_major", choices=["layer_major", "block_major"])
+    ap.add_argument("--chunk-bytes", type=int, default=0,
+                    help="KV chunk per (block, layer, K/V); default the model's bf16 chunk "
+                         "(32768). 8192 = one GPU's share under 4-way tensor parallelism, "
+                         "16384 = FP8 KV")
     ap.add_argument("--copy", default="fused", choices=["fused", "separate"],
                     help="one cascade_pack_unpack launch, or cascade_pack then cascade_unpack")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -146,7 +151,8 @@ def main():
     cfg = args.config
     w = synth.make_workload(cfg)
     c = synth.CONFIGS[cfg]
-    geom = synth.kv_geometry(c["model"], c["pool"], args.layout)
+    geom = (synth.kv_geometry(c["model"], c["pool"], args.layout, args.chunk_bytes)
+            if args.chunk_bytes else synth.kv_geometry(c["model"], c["pool"], args.layout))
     n = len(w["id"])
     nb = geom["num_blocks"]
     d = device.DeviceStep(w, slot_cap=nb, unpack_cap=max(1, min(nb, c["max_move"])),
@@ -242,11 +248,45 @@ def main():
         extra = {"bytes": nbytes, "us": e0.elapsed_time(e1) * 1e3,
                  "GBps": gbps(2.0 * nbytes, e0.elapsed_time(e1) * 1e3)}
         del a, b
+    # outside the timed region: the step with a cold last-level cache (a 1 GB
+    # write between runs evicts the 256 MB MALL), and a plain device-to-device
+    # copy of the bytes one step moves (capped to what memory allows)
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    cold = []
+    ce = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for k in range(20):
+        flush.fill_(k & 255)
+        ce[0].record(stream)
+        assert d.run(stream) == 0
+        ce[1].record(stream)
+        torch.cuda.synchronize()
+        cold.append(ce[0].elapsed_time(ce[1]) * 1e3)
+    del flush
+    moved = (n_pack + n_unpack) * block_bytes
+    free_b = torch.cuda.mem_get_info(dev)[0]
+    nb_copy = int(min(moved, (free_b - (2 << 30)) // 2)) // 16 * 16
+    dtod = None
+    if nb_copy >= (64 << 20):
+        a = torch.empty(nb_copy, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        ce[0].record(stream)
+        for _ in range(5):
+            b.copy_(a)
+        ce[1].record(stream)
+        torch.cuda.synchronize()
+        us = ce[0].elapsed_time(ce[1]) * 1e3 / 5
+        dtod = {"bytes": nb_copy, "GBps": gbps(2.0 * nb_copy, us)}
+        del a, b
+    progress("cold-cache steps and device copy done")
     kernel = "kvmove_kernel" if fused else "kvcopy_kernel"
     copies = {"mode": args.copy, "pack_blocks": n_pack, "unpack_blocks": n_unpack,
               "paired_blocks": int((res["unpack_hazard"] >= 0).sum()),
               "copy_us_p50": float(np.median(t_c1 + t_c2)),
               "copy_GBps": gbps(bytes_pack + bytes_unpack, float(np.median(t_c1 + t_c2)))}
+    if dtod:
+        copies["device_copy_same_bytes_GBps"] = dtod["GBps"]
+        copies["device_copy_bytes"] = dtod["bytes"]
     if not fused:
         copies["pack_GBps"] = gbps(bytes_pack, float(np.median(t_c1)))
         copies["unpack_GBps"] = gbps(bytes_unpack, float(np.median(t_c2)))
@@ -261,10 +301,12 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"config {cfg}: " + WORKLOADS[cfg], "requests": n,
                    "kv_layout": args.layout, "pool_blocks": nb,
+                   "chunk_bytes": geom["chunk_bytes"],
                    "block_bytes": block_bytes, "token_cap": c["token_cap"],
                    "move_cap_blocks": c["max_move"]},
         "sched_step_us_p50": float(np.median(t_step)),
         "sched_step_us_p90": float(np.percentile(t_step, 90)),
+        "sched_step_us_cold_p50": float(np.median(cold)),
         "sched_req_per_s": n / (float(np.median(t_step)) * 1e-6),
         "kv_copy": copies,
         "step_total_us_p50": float(np.median(t_all)),
@@ -272,7 +314,8 @@ def main():
                                                           else " (pack + unpack launches)"),
                      "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS,
-                     "traffic": measured_traffic(cfg, args.layout, kernel) if fused else None,
+                     "traffic": (measured_traffic(cfg, args.layout, kernel, geom["chunk_bytes"])
+                                 if fused else None),
                      "bytes_per_launch": (bytes_pack + bytes_unpack) / launches,
                      "us_per_launch": copy_us / launches},
     }

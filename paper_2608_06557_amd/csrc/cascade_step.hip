@@ -138,6 +138,147 @@ __device__ __forceinline__ long long restore_ns(long long x, long long delta, lo
   return x == 0 ? 0 : delta + x * blk;
 }
 
+// Section 4.2-4.4 for request i: validation of its data, the actual- and
+// maximum-load estimates, eq:est_latency, eq:budget_eq, eq:rem_budget_eq, the
+// tier transition, eq:max_restorable (kept only if cheaper than recompute),
+// the priority group and the record the scan reads.
+struct ReqEval {
+  long long brem, held, need1, want1;  // need1 / want1: contributions of groups 0-1
+  unsigned long long biased;           // clamped budget + 2^61
+  int4 rec;
+  unsigned tnew;
+  int grp;
+  bool bad;
+};
+
+__device__ __forceinline__ ReqEval eval_request(const cascade_requests_t &rq,
+                                                const int *__restrict__ ro, const Consts &c,
+                                                const long long *s_slo, int i) {
+  ReqEval r;
+  r.bad = false;
+  const unsigned cls = rq.slo_class[i], st = rq.state[i], qt = rq.queue_tier[i],
+                 pt = rq.prefix_tier[i];
+  const long long arr = rq.arrival_ns[i];
+  const int n_in_r = rq.n_in[i], n_out_r = rq.n_out_pred[i], n_pre_r = rq.n_prefix[i],
+            prog_r = rq.n_progress[i];
+  const int r0 = ro[i], r1 = ro[i + 1];
+  const unsigned bt = (unsigned)c.bt;
+
+  // ---- domain rules of the request data
+  if (i > 0 && rq.id[i] <= rq.id[i - 1]) r.bad = true;
+  if (i == 0 && r0 != 0) r.bad = true;
+  if (cls >= (unsigned)c.num_classes || st > 2 || qt > 2 || pt > 3) r.bad = true;
+  if (n_in_r < 1 || n_in_r > (1 << 17) || n_out_r < 0 || n_out_r > (1 << 17)) r.bad = true;
+  if (n_pre_r < 0 || n_pre_r > n_in_r - 1 || ((unsigned)n_pre_r % bt) != 0) r.bad = true;
+  if (arr < 0 || arr > c.t_now) r.bad = true;
+  if (st == CASCADE_QUEUED) {
+    if ((n_pre_r == 0) != (pt == CASCADE_KV_NONE) || prog_r != 0 || r1 != r0) r.bad = true;
+  } else if (st == CASCADE_RUNNING_PREFILL) {
+    if (prog_r < 1 || prog_r > n_in_r - 1) r.bad = true;
+    else if ((long long)r1 - r0 != udiv_ceil((unsigned)prog_r, bt)) r.bad = true;
+  } else {
+    if (prog_r < 0 || prog_r > (1 << 17)) r.bad = true;
+    else if (n_in_r >= 1 && n_in_r <= (1 << 17) &&
+             (long long)r1 - r0 != udiv_ceil((unsigned)(n_in_r + prog_r), bt))
+      r.bad = true;
+  }
+
+  // ---- keep the arithmetic in range whatever the data
+  const unsigned st_s = st > 2 ? 0u : st;
+  const unsigned pt_s = pt > 3 ? 3u : pt;
+  const unsigned cls_s = cls >= (unsigned)c.num_classes ? 0u : cls;
+  const long long n_in = n_in_r < 1 ? 1 : (n_in_r > (1 << 17) ? (1 << 17) : n_in_r);
+  const long long n_out = n_out_r < 0 ? 0 : (n_out_r > (1 << 17) ? (1 << 17) : n_out_r);
+  const long long n_pre = n_pre_r < 0 ? 0 : (n_pre_r > n_in - 1 ? n_in - 1 : n_pre_r);
+  const long long prog = prog_r < 0 ? 0 : (prog_r > (1 << 17) ? (1 << 17) : prog_r);
+  const long long elapsed = (arr < 0 || arr > c.t_now) ? 0 : c.t_now - arr;
+  const long long row = (long long)r1 - r0;
+  const long long held = row < 0 ? 0 : (row > 0xFFFFF ? 0xFFFFF : row);
+
+  // ---- Section 4.2: actual-load and maximum-load estimates
+  long long l_act, l_max, pb = 0, base_need;
+  const long long delta = (pt_s == CASCADE_KV_NVME) ? c.delta2 : c.delta1;
+  const long long blk = (pt_s == CASCADE_KV_NVME) ? c.blk2 : c.blk1;
+  const bool deep = (pt_s == CASCADE_KV_DRAM || pt_s == CASCADE_KV_NVME);
+  if (st_s == CASCADE_QUEUED) {
+    long long reuse = 0, rest = 0;
+    if (pt_s != CASCADE_KV_NONE) {
+      pb = (unsigned)n_pre / bt;
+      reuse = n_pre;
+      if (deep) rest = restore_ns(pb, delta, blk);
+    }
+    l_act = ns_of_ps(compute_ps(n_in - reuse, reuse, c.d, c)) + rest;
+    l_max = ns_of_ps(compute_ps(n_in - reuse, reuse, c.dmax, c)) + rest;
+    base_need = (pt_s == CASCADE_KV_HBM) ? n_in - n_pre : n_in;
+  } else if (st_s == CASCADE_RUNNING_PREFILL) {
+    const long long p = prog > n_in ? n_in : prog;
+    l_act = ns_of_ps(compute_ps(n_in - p, p, c.d, c));
+    l_max = ns_of_ps(compute_ps(n_in - p, p, c.dmax, c));
+    base_need = n_in - p;
+  } else {
+    const long long left = n_out - prog < 0 ? 0 : n_out - prog;
+    l_act = ns_of_ps(left * (c.c_iter + (long long)c.d * c.c_dec));
+    l_max = ns_of_ps(left * (c.c_iter + (long long)c.dmax * c.c_dec));
+    base_need = 1;
+  }
+  // ---- eq:est_latency, floor((L_act + L_max) * gamma / 2^17), exact in
+  //      64 bits: split the sum at bit 17
+  const unsigned long long sum = (unsigned long long)(l_act + l_max);
+  const unsigned long long g = (unsigned)c.gamma_q16;
+  const long long L = (long long)((sum >> 17) * g + (((sum & 0x1FFFFull) * g) >> 17));
+  // ---- eq:budget_eq and eq:rem_budget_eq
+  const long long b0 = s_slo[cls_s] - L;
+  const long long brem = b0 - elapsed;
+
+  // ---- Tier-1 / Tier-2 (Tier-1 iff B > 0, Tier-1 sticky, Tier-2 promoted)
+  unsigned tnew = qt;
+  if (st_s != CASCADE_DECODE) tnew = (qt == CASCADE_QT_TIER1 || b0 > 0) ? 1u : 2u;
+
+  // ---- eq:max_restorable in blocks, kept only if cheaper than recompute
+  long long want = 0;
+  if (st_s == CASCADE_QUEUED && deep) {
+    long long x = 0;
+    if (brem > delta) {
+      const long long m =
+          (long long)((unsigned long long)(brem - delta) / (unsigned long long)blk);
+      x = m < pb ? m : pb;
+    }
+    if (x > 0) {
+      const long long all = ns_of_ps(compute_ps(n_in, 0, c.d, c));
+      const long long part = ns_of_ps(compute_ps(n_in - (long long)bt * x, bt * x, c.d, c));
+      if (restore_ns(x, delta, blk) >= all - part) x = 0;
+    }
+    want = x;
+  }
+
+  // ---- priority group and key: group in bits 63..62, clamped budget + 2^61
+  const int grp = (st_s == CASCADE_DECODE) ? 0 : (tnew == 1 ? 1 : 2);
+  const long long lo = -(1ll << 61), hi = (1ll << 61) - 1;
+  const long long cl = brem < lo ? lo : (brem > hi ? hi : brem);
+  const unsigned long long biased = (unsigned long long)(cl + (1ll << 61));
+
+  // spill of a running prefill fits its budget (Section 4.4)
+  const int offl = (st_s == CASCADE_RUNNING_PREFILL) &&
+                   (restore_ns(held, c.delta1, c.blk1) <= brem);
+  const int decnb = (st_s == CASCADE_DECODE) &&
+                    ((long long)udiv_ceil((unsigned)(n_in + prog + 1), bt) - held) > 0;
+  const long long reuse_tok = (st_s == CASCADE_RUNNING_PREFILL)
+                                  ? prog
+                                  : ((st_s == CASCADE_QUEUED && pt_s == CASCADE_KV_HBM) ? n_pre : 0);
+
+  r.brem = brem;
+  r.tnew = tnew;
+  r.grp = grp;
+  r.biased = biased;
+  r.rec = make_int4((int)want, (int)base_need, (int)reuse_tok,
+                    (int)held | ((int)st_s << 20) | ((int)pt_s << 22) | (grp << 24) |
+                        (offl << 26) | (decnb << 27));
+  r.held = st_s == CASCADE_RUNNING_PREFILL ? held : 0;
+  r.need1 = grp <= 1 ? base_need : 0;
+  r.want1 = grp <= 1 ? want : 0;
+  return r;
+}
+
 __global__ __launch_bounds__(kBlock) void eval_kernel(
     cascade_requests_t rq, const int *__restrict__ ro, const int *__restrict__ free_slots,
     Consts c, int n, Ctl *ctl, uint4 *clear, size_t clear_vec, int *info,
@@ -174,147 +315,30 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
 
 #pragma unroll
   for (int it = 0; it < kEvalItems; ++it) {
-  const int i = (int)(blockIdx.x * kBlock * kEvalItems + it * kBlock + threadIdx.x);
-  if (i < n) {
-    const unsigned cls = rq.slo_class[i], st = rq.state[i], qt = rq.queue_tier[i],
-                   pt = rq.prefix_tier[i];
-    const long long arr = rq.arrival_ns[i];
-    const int n_in_r = rq.n_in[i], n_out_r = rq.n_out_pred[i], n_pre_r = rq.n_prefix[i],
-              prog_r = rq.n_progress[i];
-    const int r0 = ro[i], r1 = ro[i + 1];
-    const unsigned bt = (unsigned)c.bt;
-
-    // ---- domain rules of the request data
-    if (i > 0 && rq.id[i] <= rq.id[i - 1]) bad = true;
-    if (i == 0 && r0 != 0) bad = true;
-    if (cls >= (unsigned)c.num_classes || st > 2 || qt > 2 || pt > 3) bad = true;
-    if (n_in_r < 1 || n_in_r > (1 << 17) || n_out_r < 0 || n_out_r > (1 << 17)) bad = true;
-    if (n_pre_r < 0 || n_pre_r > n_in_r - 1 || ((unsigned)n_pre_r % bt) != 0) bad = true;
-    if (arr < 0 || arr > c.t_now) bad = true;
-    if (st == CASCADE_QUEUED) {
-      if ((n_pre_r == 0) != (pt == CASCADE_KV_NONE) || prog_r != 0 || r1 != r0) bad = true;
-    } else if (st == CASCADE_RUNNING_PREFILL) {
-      if (prog_r < 1 || prog_r > n_in_r - 1) bad = true;
-      else if ((long long)r1 - r0 != udiv_ceil((unsigned)prog_r, bt)) bad = true;
-    } else {
-      if (prog_r < 0 || prog_r > (1 << 17)) bad = true;
-      else if (n_in_r >= 1 && n_in_r <= (1 << 17) &&
-               (long long)r1 - r0 != udiv_ceil((unsigned)(n_in_r + prog_r), bt))
-        bad = true;
-    }
-
-    // ---- keep the arithmetic in range whatever the data
-    const unsigned st_s = st > 2 ? 0u : st;
-    const unsigned pt_s = pt > 3 ? 3u : pt;
-    const unsigned cls_s = cls >= (unsigned)c.num_classes ? 0u : cls;
-    const long long n_in = n_in_r < 1 ? 1 : (n_in_r > (1 << 17) ? (1 << 17) : n_in_r);
-    const long long n_out = n_out_r < 0 ? 0 : (n_out_r > (1 << 17) ? (1 << 17) : n_out_r);
-    const long long n_pre = n_pre_r < 0 ? 0 : (n_pre_r > n_in - 1 ? n_in - 1 : n_pre_r);
-    const long long prog = prog_r < 0 ? 0 : (prog_r > (1 << 17) ? (1 << 17) : prog_r);
-    const long long elapsed = (arr < 0 || arr > c.t_now) ? 0 : c.t_now - arr;
-    const long long row = (long long)r1 - r0;
-    const long long held = row < 0 ? 0 : (row > 0xFFFFF ? 0xFFFFF : row);
-
-    // ---- Section 4.2: actual-load and maximum-load estimates
-    long long l_act, l_max, pb = 0, base_need;
-    const long long delta = (pt_s == CASCADE_KV_NVME) ? c.delta2 : c.delta1;
-    const long long blk = (pt_s == CASCADE_KV_NVME) ? c.blk2 : c.blk1;
-    const bool deep = (pt_s == CASCADE_KV_DRAM || pt_s == CASCADE_KV_NVME);
-    if (st_s == CASCADE_QUEUED) {
-      long long reuse = 0, rest = 0;
-      if (pt_s != CASCADE_KV_NONE) {
-        pb = (unsigned)n_pre / bt;
-        reuse = n_pre;
-        if (deep) rest = restore_ns(pb, delta, blk);
-      }
-      l_act = ns_of_ps(compute_ps(n_in - reuse, reuse, c.d, c)) + rest;
-      l_max = ns_of_ps(compute_ps(n_in - reuse, reuse, c.dmax, c)) + rest;
-      base_need = (pt_s == CASCADE_KV_HBM) ? n_in - n_pre : n_in;
-    } else if (st_s == CASCADE_RUNNING_PREFILL) {
-      const long long p = prog > n_in ? n_in : prog;
-      l_act = ns_of_ps(compute_ps(n_in - p, p, c.d, c));
-      l_max = ns_of_ps(compute_ps(n_in - p, p, c.dmax, c));
-      base_need = n_in - p;
-    } else {
-      const long long left = n_out - prog < 0 ? 0 : n_out - prog;
-      l_act = ns_of_ps(left * (c.c_iter + (long long)c.d * c.c_dec));
-      l_max = ns_of_ps(left * (c.c_iter + (long long)c.dmax * c.c_dec));
-      base_need = 1;
-    }
-    // ---- eq:est_latency, floor((L_act + L_max) * gamma / 2^17), exact in
-    //      64 bits: split the sum at bit 17
-    const unsigned long long sum = (unsigned long long)(l_act + l_max);
-    const unsigned long long g = (unsigned)c.gamma_q16;
-    const long long L = (long long)((sum >> 17) * g + (((sum & 0x1FFFFull) * g) >> 17));
-    // ---- eq:budget_eq and eq:rem_budget_eq
-    const long long b0 = s_slo[cls_s] - L;
-    const long long brem = b0 - elapsed;
-
-    // ---- Tier-1 / Tier-2 (Tier-1 iff B > 0, Tier-1 sticky, Tier-2 promoted)
-    unsigned tnew = qt;
-    if (st_s != CASCADE_DECODE) tnew = (qt == CASCADE_QT_TIER1 || b0 > 0) ? 1u : 2u;
-
-    // ---- eq:max_restorable in blocks, kept only if cheaper than recompute
-    long long want = 0;
-    if (st_s == CASCADE_QUEUED && deep) {
-      long long x = 0;
-      if (brem > delta) {
-        const long long m =
-            (long long)((unsigned long long)(brem - delta) / (unsigned long long)blk);
-        x = m < pb ? m : pb;
-      }
-      if (x > 0) {
-        const long long all = ns_of_ps(compute_ps(n_in, 0, c.d, c));
-        const long long part = ns_of_ps(compute_ps(n_in - (long long)bt * x, bt * x, c.d, c));
-        if (restore_ns(x, delta, blk) >= all - part) x = 0;
-      }
-      want = x;
-    }
-
-    // ---- priority group and key: group in bits 63..62, clamped budget + 2^61
-    const int grp = (st_s == CASCADE_DECODE) ? 0 : (tnew == 1 ? 1 : 2);
-    const long long lo = -(1ll << 61), hi = (1ll << 61) - 1;
-    const long long cl = brem < lo ? lo : (brem > hi ? hi : brem);
-    const unsigned long long biased = (unsigned long long)(cl + (1ll << 61));
-    bmin = biased < bmin ? biased : bmin;
-    bmax = biased > bmax ? biased : bmax;
-    c0 += grp == 0;
-    c1 += grp == 1;
-    c2 += grp == 2;
-
-    // spill of a running prefill fits its budget (Section 4.4)
-    const int offl = (st_s == CASCADE_RUNNING_PREFILL) &&
-                     (restore_ns(held, c.delta1, c.blk1) <= brem);
-    const int decnb = (st_s == CASCADE_DECODE) &&
-                      ((long long)udiv_ceil((unsigned)(n_in + prog + 1), bt) - held) > 0;
-    const long long reuse_tok = (st_s == CASCADE_RUNNING_PREFILL)
-                                    ? prog
-                                    : ((st_s == CASCADE_QUEUED && pt_s == CASCADE_KV_HBM) ? n_pre : 0);
-
-    budget_out[i] = brem;
-    tier_out[i] = (uint8_t)tnew;
-    keys[i] = ((unsigned long long)grp << 62) | biased;
-    rec[i] = make_int4((int)want, (int)base_need, (int)reuse_tok,
-                       (int)held | ((int)st_s << 20) | ((int)pt_s << 22) | (grp << 24) |
-                           (offl << 26) | (decnb << 27));
-    if (st_s == CASCADE_RUNNING_PREFILL) v_held += held;
-    if (grp <= 1) {
-      v_need1 += base_need;
-      v_want1 += want;
-    }
+    const int i = (int)(blockIdx.x * kBlock * kEvalItems + it * kBlock + threadIdx.x);
+    if (i >= n) continue;
+    const ReqEval r = eval_request(rq, ro, c, s_slo, i);
+    bad |= r.bad;
+    bmin = r.biased < bmin ? r.biased : bmin;
+    bmax = r.biased > bmax ? r.biased : bmax;
+    c0 += r.grp == 0;
+    c1 += r.grp == 1;
+    c2 += r.grp == 2;
+    budget_out[i] = r.brem;
+    tier_out[i] = (uint8_t)r.tnew;
+    keys[i] = ((unsigned long long)r.grp << 62) | r.biased;
+    rec[i] = r.rec;
+    v_held += r.held;
+    v_need1 += r.need1;
+    v_want1 += r.want1;
   }
-  }
-
   // workgroup totals, one plain store per workgroup
   long long sums[3] = {v_held, v_need1, v_want1};
   block_sum<3>(sums, s_red);
   unsigned cnt[4] = {c0, c1, c2, bad ? 1u : 0u};
   block_sum<4>(cnt, s_cnt);
-  for (int o = 32; o >= 1; o >>= 1) {
-    const unsigned long long a = __shfl_xor(bmin, o, 64), b = __shfl_xor(bmax, o, 64);
-    bmin = a < bmin ? a : bmin;
-    bmax = b > bmax ? b : bmax;
-  }
+  bmin = wave_min(bmin);
+  bmax = wave_max(bmax);
   if (lane_id() == 0) {
     s_mm[wave_id() * 2] = bmin;
     s_mm[wave_id() * 2 + 1] = bmax;
@@ -400,11 +424,8 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
   }
   block_sum<3>(sums, s_red);
   block_sum<4>(cnt, s_cnt);
-  for (int o = 32; o >= 1; o >>= 1) {
-    const unsigned long long a = __shfl_xor(mn, o, 64), b = __shfl_xor(mx, o, 64);
-    mn = a < mn ? a : mn;
-    mx = b > mx ? b : mx;
-  }
+  mn = wave_min(mn);
+  mx = wave_max(mx);
   if (lane_id() == 0) {
     s_mm[wave_id() * 2] = mn;
     s_mm[wave_id() * 2 + 1] = mx;
@@ -633,14 +654,16 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
 
 // ---------------------------------------------------------------- scan
 
-// Look-back of K values with a window of WIN predecessors per round trip,
-// spread over K*WIN threads; the sums land in s_sum[0..K).
+// Look-back of K values with a window of WIN predecessors per round trip;
+// the K*WIN window slots are spread over the workgroup (several per thread
+// when the window is wider than kBlock / K).  The sums land in s_sum[0..K).
 template <int K, int WIN>
 __device__ __forceinline__ void block_look_back(const unsigned long long *status, int stride,
                                                 int tile, long long *s_sum, int *s_base,
                                                 unsigned long long *s_w, int *s_left,
                                                 bool *timed_out) {
-  static_assert(K * WIN <= kBlock, "window too wide");
+  constexpr int kSlots = K * WIN;
+  constexpr int kPer = (kSlots + kBlock - 1) / kBlock;
   const int t = threadIdx.x;
   if (t < K) {
     s_base[t] = tile - 1;
@@ -650,11 +673,22 @@ __device__ __forceinline__ void block_look_back(const unsigned long long *status
   __syncthreads();
   unsigned spins = 0;
   while (true) {
-    const int k = t / WIN, j = t - (t / WIN) * WIN;
-    if (k < K && s_base[k] >= 0) {
-      const int src = s_base[k] - j;
-      s_w[k * WIN + j] = src >= 0 ? load_agent(status + (size_t)src * stride + k)
-                                  : (unsigned long long)kFlagInclusive;
+    unsigned long long w[kPer];
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int slot = t + i * kBlock;
+      const int k = slot / WIN, j = slot - (slot / WIN) * WIN;
+      w[i] = 0;
+      if (slot < kSlots && s_base[k] >= 0) {
+        const int src = s_base[k] - j;
+        w[i] = src >= 0 ? load_agent(status + (size_t)src * stride + k)
+                        : (unsigned long long)kFlagInclusive;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int slot = t + i * kBlock;
+      if (slot < kSlots) s_w[slot] = w[i];
     }
     __syncthreads();
     bool stalled = false;
@@ -663,12 +697,12 @@ __device__ __forceinline__ void block_look_back(const unsigned long long *status
       int consumed = 0;
       bool done = false;
       for (int jj = 0; jj < WIN && !done && !stalled; ++jj) {
-        const unsigned long long w = s_w[t * WIN + jj];
-        const unsigned f = (unsigned)(w & 3);
+        const unsigned long long v = s_w[t * WIN + jj];
+        const unsigned f = (unsigned)(v & 3);
         if (f == 0) {
           stalled = true;
         } else {
-          sum += (long long)(w >> 2);
+          sum += (long long)(v >> 2);
           ++consumed;
           done = (f == kFlagInclusive);
         }
@@ -698,14 +732,19 @@ __device__ __forceinline__ void block_look_back(const unsigned long long *status
 // remaining budget first): a holder at position p is preempted iff the
 // eligible blocks behind it are fewer than D.
 constexpr int kFreeCap = 4096;    // free-list entries staged in LDS by the finishing workgroup
+constexpr int kTailCap = 2048;    // victims' slot-list entries kept in LDS for the restores
+constexpr int kRowBatch = 8;      // victims' row entries each thread requests at once
+static_assert(kVictimCap == kBlock, "one staged victim per thread in the row-offset scan");
 
 struct FinishLds {
   long long tot[kWaves * 6];
   int v_req[kVictimCap], v_held[kVictimCap], v_row0[kVictimCap], v_start[kVictimCap];
   long long v_sbase[kVictimCap], v_pbase[kVictimCap];
   int v_total;
-  RestoreEnt rl[kRestoreCap];
+  alignas(16) RestoreEnt rl[kRestoreCap];  // stored as int4
   int free_slots[kFreeCap];
+  int tail[kTailCap];  // slot-list entries n_free + i: the victims' slots
+  int scan_tmp[kWaves];
   int n_victims, counts[2];
 };
 
@@ -729,9 +768,38 @@ __device__ int unpack_move_at(long long s, int nr, const FinishLds &L, const Res
   return s < (long long)e.alloc_off + e.blocks ? e.stage_off + (int)(s - e.alloc_off) : -1;
 }
 
-// Loads are grouped so that the workgroup waits on memory three times: the
-// totals, running-prefill records, restore list and free list together; the
-// victims' rows; the slot-list entries of restores past the free list.
+// Block b of a victim: its slot-list entry sb (and the LDS copy of it), its
+// pack move pb + b when the victim spills (pb >= 0), and the copy-order
+// hazard between that pack move and the restore that receives the slot.
+// Every restore into a victim's slot gets its hazard entry here (-1 when
+// the victim is dropped); restores into free slots get theirs later, so no
+// hazard entry is written twice.
+__device__ void place_victim_block(int req, int b, int slot, long long sb, long long pb,
+                                   int n_free, int nr, const Outs &o, FinishLds &L,
+                                   const RestoreEnt *rl) {
+  if (sb < o.sl_cap) o.slot_list[sb] = slot;
+  if (sb - n_free < kTailCap) L.tail[sb - n_free] = slot;
+  const long long j = pb >= 0 ? pb + b : -1;
+  const bool packed = j >= 0 && j < o.pack_cap;
+  if (packed) {
+    cascade_move_t mv;
+    mv.req = req;
+    mv.blk = b;
+    mv.pool_slot = slot;
+    mv.staging_slot = (int)j;
+    o.pack[j] = mv;
+  }
+  if (o.pack_hazard) {
+    const int m = unpack_move_at(sb, nr, L, rl);
+    if (packed) o.pack_hazard[j] = m;
+    if (m >= 0 && m < o.unpack_cap) o.unpack_hazard[m] = packed ? (int)j : -1;
+  }
+}
+
+// Loads are grouped so that the workgroup waits on memory twice in the
+// common case: the totals, running-prefill records, restore list and free
+// list together (each thread's share requested before any is stored), then
+// the victims' rows, up to kRowBatch per thread at once.
 __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_tiles, int n_rp,
                             const TileTot *__restrict__ tiles, const int *__restrict__ free_slots,
                             const RpInfo *__restrict__ rp, const RestoreEnt *__restrict__ rl,
@@ -740,6 +808,20 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
   if (t == 0) {
     L.n_victims = 0;
     L.counts[0] = L.counts[1] = 0;
+  }
+  // first batch of the free list and the restore list, requested together
+  // with the tile totals below; the rest (long lists only) follows
+  constexpr int kStage = 2;
+  const int n_fs = min(n_free, kFreeCap), n_rs = min(n, kRestoreCap);
+  static_assert(sizeof(RestoreEnt) == sizeof(int4), "restore entries move as int4");
+  const int4 *rl4 = reinterpret_cast<const int4 *>(rl);
+  int fv[kStage];
+  int4 rv[kStage];
+#pragma unroll
+  for (int u = 0; u < kStage; ++u) {
+    const int j = t + u * kBlock;
+    fv[u] = j < n_fs ? free_slots[j] : 0;
+    rv[u] = j < n_rs ? rl4[j] : make_int4(0, 0, 0, 0);
   }
   long long tot[6] = {0, 0, 0, 0, 0, 0};
   for (int j = t; j < n_tiles; j += kBlock) {
@@ -754,10 +836,16 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
   RpInfo mine = {};
   const bool has_rp = t < n_rp;
   if (has_rp) mine = rp[t];
-  for (int j = t; j < n_free && j < kFreeCap; j += kBlock) L.free_slots[j] = free_slots[j];
+#pragma unroll
+  for (int u = 0; u < kStage; ++u) {
+    const int j = t + u * kBlock;
+    if (j < n_fs) L.free_slots[j] = fv[u];
+    if (j < n_rs) reinterpret_cast<int4 *>(L.rl)[j] = rv[u];
+  }
+  for (int j = t + kStage * kBlock; j < n_fs; j += kBlock) L.free_slots[j] = free_slots[j];
   // the restore list holds tot[5] entries (not known yet) in a buffer of n;
   // stage a bounded prefix now, use only its valid part below
-  for (int j = t; j < kRestoreCap && j < n; j += kBlock) L.rl[j] = rl[j];
+  for (int j = t + kStage * kBlock; j < n_rs; j += kBlock) L.rl[j] = rl[j];
   const int kstar = ctl->kstar;
   const long long kx = ctl->kx, ky = ctl->ky, kz = ctl->kz, kzp = ctl->kzp;
   block_sum<6>(tot, L.tot);  // waits for the loads above
@@ -793,20 +881,9 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
         L.v_row0[v] = ri.row0;
         L.v_sbase[v] = sbase;
         L.v_pbase[v] = pbase;
-      } else {  // more victims than LDS holds: copy this one alone
-        for (int b = 0; b < h; ++b) {
-          const int slot = slots[ri.row0 + b];
-          if (sbase + b < o.sl_cap) o.slot_list[sbase + b] = slot;
-          if (pbase >= 0 && pbase + b < o.pack_cap) {
-            cascade_move_t m;
-            m.req = i;
-            m.blk = b;
-            m.pool_slot = slot;
-            m.staging_slot = (int)(pbase + b);
-            o.pack[pbase + b] = m;
-            if (o.pack_hazard) o.pack_hazard[pbase + b] = unpack_move_at(sbase + b, nr, L, rl);
-          }
-        }
+      } else {  // more victims than LDS holds: place this one alone
+        for (int b = 0; b < h; ++b)
+          place_victim_block(i, b, slots[ri.row0 + b], sbase + b, pbase, n_free, nr, o, L, rl);
       }
     }
   }
@@ -814,19 +891,17 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
   // the staged victims' rows as one flat index space (prefix of row lengths),
   // so every row load of every victim is in flight at once
   const int nv = min(L.n_victims, kVictimCap);
-  if (t == 0) {
-    int acc = 0;
-    for (int v = 0; v < nv; ++v) {
-      L.v_start[v] = acc;
-      acc += L.v_held[v];
-    }
-    L.v_total = acc;
+  {
+    int hv[1] = {t < nv ? L.v_held[t] : 0}, tot1[1];
+    block_exclusive_scan<1>(hv, tot1, L.scan_tmp);  // kVictimCap == kBlock
+    if (t < nv) L.v_start[t] = hv[0];
+    if (t == 0) L.v_total = tot1[0];
   }
   __syncthreads();
-  for (int m0 = t; m0 < L.v_total; m0 += 4 * kBlock) {
-    int slot[4], vi[4], bi[4];
+  for (int m0 = t; m0 < L.v_total; m0 += kRowBatch * kBlock) {
+    int slot[kRowBatch], vi[kRowBatch], bi[kRowBatch];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kRowBatch; ++u) {
       const int m = m0 + u * kBlock;
       vi[u] = -1;
       if (m < L.v_total) {
@@ -841,21 +916,11 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
       }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kRowBatch; ++u) {
       if (vi[u] < 0) continue;
-      const int v = vi[u], b = bi[u];
-      const long long sb = L.v_sbase[v] + b, pb = L.v_pbase[v];
-      if (sb < o.sl_cap) o.slot_list[sb] = slot[u];
-      if (pb >= 0 && pb + b < o.pack_cap) {
-        cascade_move_t mv;
-        mv.req = L.v_req[v];
-        mv.blk = b;
-        mv.pool_slot = slot[u];
-        mv.staging_slot = (int)(pb + b);
-        o.pack[pb + b] = mv;
-        // the restore that receives this slot must wait for this spill
-        if (o.pack_hazard) o.pack_hazard[pb + b] = unpack_move_at(sb, nr, L, rl);
-      }
+      const int v = vi[u];
+      place_victim_block(L.v_req[v], bi[u], slot[u], L.v_sbase[v] + bi[u], L.v_pbase[v], n_free,
+                         nr, o, L, rl);
     }
   }
   __syncthreads();  // the slot list is complete (this workgroup wrote it)
@@ -875,21 +940,15 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
     cascade_move_t mv;
     mv.req = e.req;
     mv.blk = b;
-    mv.pool_slot = s >= o.sl_cap ? -1 : (s < n_free && s < kFreeCap ? L.free_slots[s]
-                                                                       : o.slot_list[s]);
+    int ps;
+    if (s >= o.sl_cap) ps = -1;
+    else if (s < n_free) ps = s < kFreeCap ? L.free_slots[s] : free_slots[s];
+    else ps = s - n_free < kTailCap ? L.tail[s - n_free] : o.slot_list[s];
+    mv.pool_slot = ps;
     mv.staging_slot = (int)m;
     o.unpack[m] = mv;
-    if (o.unpack_hazard) o.unpack_hazard[m] = -1;
-  }
-  // the pairs, from the pack side (the barrier orders these stores after the
-  // defaults above and makes the pack-side entries visible)
-  __syncthreads();
-  if (o.unpack_hazard && o.pack_hazard) {
-    const int np = min(L.counts[1], o.pack_cap);
-    for (int j = t; j < np; j += kBlock) {
-      const int m = o.pack_hazard[j];
-      if (m >= 0 && m < o.unpack_cap) o.unpack_hazard[m] = j;
-    }
+    // a free slot is read by no pack move (victims' slots got theirs above)
+    if (o.unpack_hazard && s < n_free) o.unpack_hazard[m] = -1;
   }
   if (t == 0) {
     const long long nsl = (long long)n_free + L.counts[0];
@@ -902,80 +961,51 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
   }
 }
 
-// Algorithm 1's Phase 2 loop in priority order as prefix sums.
-// Level 1 (independent of earlier decisions): restore want, base token need,
-// blocks held by running prefills (all / spill-fits).  They give the restore
-// blocks r (eq:max_restorable under the per-step cap U), the exact token need
-// and the chunked-prefill grant g of every position.
-// Level 2 (functions of g): block weight of the admission test, new blocks
-// of admitted requests, admitted count, held blocks of running prefills left
-// out (all / spill-fits), restored blocks and restoring requests.
-// Both levels use one decoupled look-back each, chained inside the launch.
-__global__ __launch_bounds__(kBlock) void scan_kernel(
-    int n, int passes, Consts c, Ctl *ctl, int *info, const unsigned *vals_a,
-    const unsigned *vals_b, const int4 *__restrict__ rec, const int *__restrict__ ro,
-    const int *__restrict__ slots, const int *__restrict__ free_slots, Outs o,
-    RpInfo *__restrict__ rp_list, RestoreEnt *__restrict__ restore_list,
-    TileTot *__restrict__ tile_tot, unsigned long long *status1, unsigned long long *status2) {
-  __shared__ long long s_scan[kWaves * kL2];
-  __shared__ long long s_sum[kL2Stride];
-  __shared__ int s_base[kL2Stride];
-  __shared__ unsigned long long s_w[kBlock];
-  __shared__ int s_left;
-  __shared__ int s_tile, s_bad, s_last;
-  __shared__ unsigned s_mask;
-  __shared__ FinishLds s_fin;
+// Algorithm 1's Phase 2 over the kScanTile positions of one tile, given
+// each position's request index (idx < 0: past the end) and record; thread
+// t holds positions t*jn .. t*jn + jn - 1 of the tile (jn <= kScanItems).  With
+// kChained the tile's level-1 and level-2 prefixes come from the decoupled
+// look-back over the tiles before it; without, the tile is the whole queue.
+// Writes every per-request output of the tile, k*, the running-prefill and
+// restore-list entries and the tile's totals; returns the number of running
+// prefills up to and including this tile.
+struct ScanLds {
+  long long scan[kWaves * kL2];
+  long long sum[kL2Stride];
+  int base[kL2Stride];
+  unsigned long long w[kBlock];
+  int left;
+};
 
-  // the tile's order entries are requested from both ping-pong buffers at once
-  // (which one holds the result is known only from the plan)
-  const int p0g = (int)blockIdx.x * kScanTile + threadIdx.x * kScanItems;
-  unsigned oa[kScanItems], ob[kScanItems];
-#pragma unroll
-  for (int j = 0; j < kScanItems; ++j) {
-    oa[j] = p0g + j < n ? vals_a[p0g + j] : 0u;
-    ob[j] = p0g + j < n ? vals_b[p0g + j] : 0u;
-  }
-  unsigned hv[kMaxDigits];
-#pragma unroll
-  for (int d = 0; d < kMaxDigits; ++d) hv[d] = ctl->hist[d][threadIdx.x];
-  if (threadIdx.x == 0) {
-    s_tile = (int)atomicAdd(&ctl->tile_ctr[kMaxDigits], 1u);
-    s_bad = bad_status(load_agent(info));
-    s_mask = 0;
-  }
-  const int nd = key_digits(ctl->bmin, ctl->bmax, ctl->cnt[1], ctl->cnt[2]);
-  __syncthreads();
-  const int nact = __builtin_popcount(plan_mask(hv, n, nd, &s_mask));
-  if (s_bad) return;
-  const int tile = s_tile;
-  // a live digit beyond the launched passes would leave the keys unsorted
-  bool broken = nact > passes;
-  const unsigned *sorted = (nact & 1) ? vals_b : vals_a;
-  const long long bt = c.bt, U = c.max_move;
-  const long long e1 = (long long)ctl->cnt[0] + ctl->cnt[1];
+struct ScanConsts {
+  long long bt, U, e1, cap, cap1, p_e1, g1, fh;
+};
+
+__device__ __forceinline__ ScanConsts scan_consts(const Consts &c, const Ctl *ctl) {
+  ScanConsts k;
+  k.bt = c.bt;
+  k.U = c.max_move;
+  k.e1 = (long long)ctl->cnt[0] + ctl->cnt[1];
   const bool has2 = ctl->cnt[2] != 0;
-  const long long cap = c.token_cap;
-  const long long cap1 = cap - (has2 ? ((cap * c.rho_q16) >> 16) : 0);
-  const long long p_e1 = ctl->need1 - bt * lmin(ctl->want1, U);  // tokens before Tier-2
-  const long long g1 = lmin(p_e1, cap1);                           // granted to decode+Tier-1
-  const long long fh = (long long)c.n_free + ctl->held_rp;         // F + H
+  k.cap = c.token_cap;
+  k.cap1 = k.cap - (has2 ? ((k.cap * c.rho_q16) >> 16) : 0);
+  k.p_e1 = ctl->need1 - k.bt * lmin(ctl->want1, k.U);  // tokens before Tier-2
+  k.g1 = lmin(k.p_e1, k.cap1);                          // granted to decode+Tier-1
+  k.fh = (long long)c.n_free + ctl->held_rp;            // F + H
+  return k;
+}
 
-  const int p0 = tile * kScanTile + threadIdx.x * kScanItems;
-  int idx[kScanItems];
-  int4 r4[kScanItems];
-#pragma unroll
-  for (int j = 0; j < kScanItems; ++j) {
-    const int p = p0 + j;
-    int ix = -1;
-    if (p < n) ix = (int)(tile == (int)blockIdx.x ? ((nact & 1) ? ob[j] : oa[j]) : sorted[p]);
-    if (ix >= n) {  // cannot happen with a correct sort; never read out of range
-      broken = true;
-      ix = -1;
-    }
-    idx[j] = ix;
-    r4[j] = ix >= 0 ? rec[ix] : make_int4(0, 0, 0, 0);
-  }
-
+template <bool kChained>
+__device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, int *info,
+                               const int (&idx)[kScanItems], const int4 (&r4)[kScanItems],
+                               bool broken, const int *__restrict__ ro, const Outs &o,
+                               RpInfo *__restrict__ rp_list,
+                               RestoreEnt *__restrict__ restore_list,
+                               TileTot *__restrict__ tile_tot, unsigned long long *status1,
+                               unsigned long long *status2, ScanLds &S) {
+  const long long bt = K.bt, U = K.U, e1 = K.e1, cap = K.cap, cap1 = K.cap1, p_e1 = K.p_e1,
+                  g1 = K.g1, fh = K.fh;
+  const int p0 = tile * kScanTile + threadIdx.x * jn;  // items j < jn; the rest absent
   // ---- level 1
   long long l1[kL1] = {0, 0, 0, 0, 0}, t1[kL1];
 #pragma unroll
@@ -989,30 +1019,33 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     l1[3] += rec_offl(w) ? h : 0;
     l1[4] += rp ? 1 : 0;          // running prefills (their compact list)
   }
-  block_exclusive_scan<kL1>(l1, t1, s_scan);
+  block_exclusive_scan<kL1>(l1, t1, S.scan);
   bool timed_out = false;
-  unsigned long long *st1 = status1 + (size_t)tile * kL1;
-  if (threadIdx.x < kL1)
-    publish<unsigned long long>(st1 + threadIdx.x, (unsigned long long)t1[threadIdx.x],
+  if (kChained && threadIdx.x < kL1)
+    publish<unsigned long long>(status1 + (size_t)tile * kL1 + threadIdx.x,
+                                (unsigned long long)t1[threadIdx.x],
                                 tile == 0 ? kFlagInclusive : kFlagAggregate);
-  if (tile > 0) {
-    block_look_back<kL1, kBlock / kL1>(status1, kL1, tile, s_sum, s_base, s_w, &s_left,
-                                       &timed_out);
+  if (kChained && tile > 0) {
+    block_look_back<kL1, kBlock / kL1>(status1, kL1, tile, S.sum, S.base, S.w, &S.left,
+                                   &timed_out);
     if (threadIdx.x < kL1)
-      publish<unsigned long long>(st1 + threadIdx.x,
-                                  (unsigned long long)(s_sum[threadIdx.x] + t1[threadIdx.x]),
+      publish<unsigned long long>(status1 + (size_t)tile * kL1 + threadIdx.x,
+                                  (unsigned long long)(S.sum[threadIdx.x] + t1[threadIdx.x]),
                                   kFlagInclusive);
   } else {
-    if (threadIdx.x < kL2Stride) s_sum[threadIdx.x] = 0;
+    if (threadIdx.x < kL2Stride) S.sum[threadIdx.x] = 0;
     __syncthreads();
   }
-  long long wx = s_sum[0] + l1[0], bn = s_sum[1] + l1[1], yy = s_sum[2] + l1[2],
-            zz = s_sum[3] + l1[3];
-  int rp_at = (int)(s_sum[4] + l1[4]);
+  long long wx = S.sum[0] + l1[0], bn = S.sum[1] + l1[1], yy = S.sum[2] + l1[2],
+            zz = S.sum[3] + l1[3];
+  int rp_at = (int)(S.sum[4] + l1[4]);
+  const long long rp_incl = S.sum[4] + t1[4];  // running prefills up to this tile
   __syncthreads();
 
   // ---- per position: restore blocks, need, grant, new blocks
-  long long r[kScanItems], g[kScanItems], nb[kScanItems], hh[kScanItems];
+  // per item: restore blocks (<= want), grant (<= token cap), new blocks and
+  // held blocks (< 2^20) all fit 32 bits; prefix sums stay 64-bit
+  int r[kScanItems], g[kScanItems], nb[kScanItems], hh[kScanItems];
   long long y_inc[kScanItems], zp_inc[kScanItems];
   long long l2[kL2] = {0, 0, 0, 0, 0, 0, 0}, t2[kL2];
 #pragma unroll
@@ -1049,10 +1082,10 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
         nbj = rec_decnb(w);
       }
     }
-    r[j] = rj;
-    g[j] = gj;
-    nb[j] = nbj;
-    hh[j] = h;
+    r[j] = (int)rj;
+    g[j] = (int)gj;
+    nb[j] = (int)nbj;
+    hh[j] = (int)h;
     wx += want;
     bn += r4[j].y;
     yy += h;
@@ -1070,25 +1103,25 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   }
 
   // ---- level 2
-  block_exclusive_scan<kL2>(l2, t2, s_scan);
+  block_exclusive_scan<kL2>(l2, t2, S.scan);
   unsigned long long *st2 = status2 + (size_t)tile * kL2Stride;
-  if (threadIdx.x < kL2)
+  if (kChained && threadIdx.x < kL2)
     publish<unsigned long long>(st2 + threadIdx.x, (unsigned long long)t2[threadIdx.x],
                                 tile == 0 ? kFlagInclusive : kFlagAggregate);
-  if (tile > 0) {
-    block_look_back<kL2, kBlock / kL2>(status2, kL2Stride, tile, s_sum, s_base, s_w, &s_left,
-                                       &timed_out);
+  if (kChained && tile > 0) {
+    block_look_back<kL2, kBlock / kL2>(status2, kL2Stride, tile, S.sum, S.base, S.w, &S.left,
+                                   &timed_out);
     if (threadIdx.x < kL2)
       publish<unsigned long long>(st2 + threadIdx.x,
-                                  (unsigned long long)(s_sum[threadIdx.x] + t2[threadIdx.x]),
+                                  (unsigned long long)(S.sum[threadIdx.x] + t2[threadIdx.x]),
                                   kFlagInclusive);
   } else {
-    if (threadIdx.x < kL2Stride) s_sum[threadIdx.x] = 0;
+    if (threadIdx.x < kL2Stride) S.sum[threadIdx.x] = 0;
     __syncthreads();
   }
-  long long W = s_sum[0] + l2[0], NB = s_sum[1] + l2[1], AC = s_sum[2] + l2[2],
-            X = s_sum[3] + l2[3], Z = s_sum[4] + l2[4], RR = s_sum[5] + l2[5],
-            RC = s_sum[6] + l2[6];
+  long long W = S.sum[0] + l2[0], NB = S.sum[1] + l2[1], AC = S.sum[2] + l2[2],
+            X = S.sum[3] + l2[3], Z = S.sum[4] + l2[4], RR = S.sum[5] + l2[5],
+            RC = S.sum[6] + l2[6];
 
   long long a_nb = 0, a_eh = 0, a_eoh = 0, a_n = 0, a_r = 0, a_rc = 0;
 #pragma unroll
@@ -1169,7 +1202,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     RC += (gp && r[j] > 0) ? 1 : 0;
   }
   long long tot[8] = {a_nb, a_eh, a_eoh, a_n, a_r, a_rc, timed_out ? 1 : 0, broken ? 1 : 0};
-  block_sum<8>(tot, reinterpret_cast<long long *>(s_w));
+  block_sum<8>(tot, reinterpret_cast<long long *>(S.w));
   if (threadIdx.x == 0) {
     TileTot tt;
     tt.adm_nb = tot[0];
@@ -1182,6 +1215,76 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     tile_tot[tile] = tt;
     if (tot[6]) set_status(info, CASCADE_ETIMEOUT);
     if (tot[7]) set_status(info, CASCADE_EINTERNAL);
+  }
+  return rp_incl;
+}
+
+// Algorithm 1's Phase 2 loop in priority order as prefix sums.
+// Level 1 (independent of earlier decisions): restore want, base token need,
+// blocks held by running prefills (all / spill-fits).  They give the restore
+// blocks r (eq:max_restorable under the per-step cap U), the exact token need
+// and the chunked-prefill grant g of every position.
+// Level 2 (functions of g): block weight of the admission test, new blocks
+// of admitted requests, admitted count, held blocks of running prefills left
+// out (all / spill-fits), restored blocks and restoring requests.
+// Both levels use one decoupled look-back each, chained inside the launch.
+__global__ __launch_bounds__(kBlock) void scan_kernel(
+    int n, int passes, Consts c, Ctl *ctl, int *info, const unsigned *vals_a,
+    const unsigned *vals_b, const int4 *__restrict__ rec, const int *__restrict__ ro,
+    const int *__restrict__ slots, const int *__restrict__ free_slots, Outs o,
+    RpInfo *__restrict__ rp_list, RestoreEnt *__restrict__ restore_list,
+    TileTot *__restrict__ tile_tot, unsigned long long *status1, unsigned long long *status2) {
+  __shared__ ScanLds s_lds;
+  __shared__ int s_tile, s_bad, s_last;
+  __shared__ unsigned s_mask;
+  __shared__ FinishLds s_fin;
+
+  // the tile's order entries are requested from both ping-pong buffers at once
+  // (which one holds the result is known only from the plan)
+  const int p0g = (int)blockIdx.x * kScanTile + threadIdx.x * kScanItems;
+  unsigned oa[kScanItems], ob[kScanItems];
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    oa[j] = p0g + j < n ? vals_a[p0g + j] : 0u;
+    ob[j] = p0g + j < n ? vals_b[p0g + j] : 0u;
+  }
+  unsigned hv[kMaxDigits];
+#pragma unroll
+  for (int d = 0; d < kMaxDigits; ++d) hv[d] = ctl->hist[d][threadIdx.x];
+  if (threadIdx.x == 0) {
+    s_tile = (int)atomicAdd(&ctl->tile_ctr[kMaxDigits], 1u);
+    s_bad = bad_status(load_agent(info));
+    s_mask = 0;
+  }
+  const int nd = key_digits(ctl->bmin, ctl->bmax, ctl->cnt[1], ctl->cnt[2]);
+  __syncthreads();
+  const int nact = __builtin_popcount(plan_mask(hv, n, nd, &s_mask));
+  if (s_bad) return;
+  const int tile = s_tile;
+  // a live digit beyond the launched passes would leave the keys unsorted
+  bool broken = nact > passes;
+  const unsigned *sorted = (nact & 1) ? vals_b : vals_a;
+  const ScanConsts K = scan_consts(c, ctl);
+
+  const int p0 = tile * kScanTile + threadIdx.x * kScanItems;
+  int idx[kScanItems];
+  int4 r4[kScanItems];
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    const int p = p0 + j;
+    int ix = -1;
+    if (p < n) ix = (int)(tile == (int)blockIdx.x ? ((nact & 1) ? ob[j] : oa[j]) : sorted[p]);
+    if (ix >= n) {  // cannot happen with a correct sort; never read out of range
+      broken = true;
+      ix = -1;
+    }
+    idx[j] = ix;
+    r4[j] = ix >= 0 ? rec[ix] : make_int4(0, 0, 0, 0);
+  }
+
+  scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, broken, ro, o, rp_list, restore_list,
+                  tile_tot, status1, status2, s_lds);
+  if (threadIdx.x == 0) {
     // release this tile's writes, then count it; the last tile finishes the step
     __threadfence();
     s_last = (atomicAdd(&ctl->scan_done, 1u) == gridDim.x - 1);
@@ -1197,6 +1300,277 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   const int n_rp = (int)((load_agent(status1 + (size_t)(gridDim.x - 1) * kL1 + 4)) >> 2);
   finish_step(ctl, info, n, c.n_free, gridDim.x, n_rp, tile_tot, free_slots, rp_list,
               restore_list, slots, o, s_fin);
+}
+
+// ------------------------------------------------------------ small queues
+
+// A queue of at most kScanTile requests is one sort tile and one scan tile,
+// so the whole step runs in one workgroup: keys, records and the order stay
+// in LDS, and nothing waits on another workgroup.  Same arithmetic and the
+// same device functions as the multi-launch path, so the result is the same.
+constexpr int kSmallMax = kScanTile;
+constexpr int kSmallCheckBlocks = 16384;  // pools up to this size are checked in-kernel
+constexpr int kCheckGrid = 64;
+static_assert(kSortTile == kScanTile && kSortItems == kScanItems, "one tile per small queue");
+
+struct SmallSortLds {
+  unsigned long long key[kSmallMax];
+  unsigned val[kSmallMax];
+  int4 rec[kSmallMax];
+  unsigned wcnt[kWaves][kRadix];
+  int start[kRadix];
+};
+union SmallLds {  // the sort is finished before the finish stages anything
+  SmallSortLds sort;
+  FinishLds fin;
+};
+
+// Rank of this lane's item among the wave's items with the same 8-bit digit
+// (dig < 0: no item), items taken in (call, lane) order; wcnt[d] counts the
+// wave's items of digit d seen so far.
+__device__ __forceinline__ int wave_digit_rank(int dig, unsigned *wcnt) {
+  const bool v = dig >= 0;
+  uint64_t peers = __ballot(v);
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const bool bit = (dig >> b) & 1;
+    const uint64_t bal = __ballot(bit);
+    peers &= bit ? bal : ~bal;
+  }
+  const int d = v ? dig : 0;
+  unsigned before = 0;
+  if (v) before = wcnt[d];
+  __builtin_amdgcn_wave_barrier();
+  const int below = rank_in_mask(peers);
+  if (v && below == 0) wcnt[d] = before + (unsigned)__builtin_popcountll(peers);
+  __builtin_amdgcn_wave_barrier();
+  return (int)before + below;
+}
+
+// Range checks of the free list and of the block-table slots (num_blocks),
+// 8 loads per thread in flight; true if any entry is out of range.
+__device__ __forceinline__ bool any_out_of_range(const int *__restrict__ a, int count,
+                                                 int num_blocks, int first, int stride) {
+  bool bad = false;
+  for (int j0 = first; j0 < count; j0 += 8 * stride) {
+    int v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = (j0 + u * stride < count) ? a[j0 + u * stride] : 0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if ((unsigned)v[u] >= (unsigned)num_blocks) bad = true;
+  }
+  return bad;
+}
+
+// The same checks spread over a grid, for a small queue over a large pool:
+// run after the step, they can only turn its status into CASCADE_EINVAL
+// (outputs are unspecified then), and they read the block table only when
+// the step found the row structure valid.
+__global__ __launch_bounds__(kBlock) void check_lists_kernel(int n, int num_blocks, int n_free,
+                                                             const int *__restrict__ free_slots,
+                                                             const int *__restrict__ ro,
+                                                             const int *__restrict__ slots,
+                                                             int *info) {
+  __shared__ int s_skip;
+  if (threadIdx.x == 0) s_skip = load_agent(info) == CASCADE_EINVAL;
+  __syncthreads();
+  if (s_skip) return;
+  const int first = blockIdx.x * kBlock + threadIdx.x, stride = gridDim.x * kBlock;
+  bool bad = any_out_of_range(free_slots, n_free, num_blocks, first, stride);
+  bad |= any_out_of_range(slots, ro[n], num_blocks, first, stride);
+  if (bad) set_status(info, CASCADE_EINVAL);
+}
+
+__global__ __launch_bounds__(kBlock) void step_small_kernel(
+    cascade_requests_t rq, const int *__restrict__ ro, const int *__restrict__ slots,
+    const int *__restrict__ free_slots, Consts c, int n, int check_lists, Ctl *ctl, int *info,
+    Outs o, int64_t *__restrict__ budget_out, uint8_t *__restrict__ tier_out,
+    RpInfo *__restrict__ rp_list, RestoreEnt *__restrict__ restore_list,
+    TileTot *__restrict__ tile_tot) {
+  __shared__ long long s_slo[16];
+  __shared__ long long s_red[kWaves * 3];
+  __shared__ unsigned s_cnt[kWaves * 4];
+  __shared__ unsigned long long s_mm[kWaves * 4];
+  __shared__ int s_scan1[kWaves];
+  __shared__ ScanLds s_lds;
+  __shared__ SmallLds U;
+  const int t = threadIdx.x, lane = lane_id(), wave = wave_id();
+  if (t < 16) s_slo[t] = c.slo[t];
+  if (t == 0) {
+    unsigned *w = reinterpret_cast<unsigned *>(ctl);
+    for (size_t k = 0; k < kCtlHeaderWords; ++k) w[k] = 0;
+    ctl->kstar = n;
+    for (int k = 0; k < CASCADE_INFO_LEN; ++k) info[k] = 0;
+    info[CASCADE_INFO_N_SLOT_LIST] = c.n_free;
+  }
+  __syncthreads();
+
+  // ---- evaluation, request j*kBlock + t on thread t (every wave busy); the
+  //      raw keys and the records wait in LDS for the sort
+  bool bad = check_lists && any_out_of_range(free_slots, c.n_free, c.num_blocks, t, kBlock);
+  long long sums[3] = {0, 0, 0};
+  unsigned cnt[4] = {0, 0, 0, 0};
+  unsigned long long mn = ~0ull, mx = 0;
+#pragma unroll
+  for (int j = 0; j < kSortItems; ++j) {
+    const int i = j * kBlock + t;
+    if (i >= n) continue;
+    const ReqEval r = eval_request(rq, ro, c, s_slo, i);
+    bad |= r.bad;
+    mn = r.biased < mn ? r.biased : mn;
+    mx = r.biased > mx ? r.biased : mx;
+    cnt[r.grp] += 1;
+    budget_out[i] = r.brem;
+    tier_out[i] = (uint8_t)r.tnew;
+    U.sort.key[i] = ((unsigned long long)r.grp << 62) | r.biased;
+    U.sort.rec[i] = r.rec;
+    sums[0] += r.held;
+    sums[1] += r.need1;
+    sums[2] += r.want1;
+  }
+  cnt[3] = bad ? 1u : 0u;
+  block_sum<3>(sums, s_red);
+  block_sum<4>(cnt, s_cnt);
+  mn = wave_min(mn);
+  mx = wave_max(mx);
+  if (lane == 0) {
+    s_mm[wave * 2] = mn;
+    s_mm[wave * 2 + 1] = mx;
+  }
+  __syncthreads();
+  mn = ~0ull;
+  mx = 0;
+  for (int w = 0; w < kWaves; ++w) {
+    mn = s_mm[2 * w] < mn ? s_mm[2 * w] : mn;
+    mx = s_mm[2 * w + 1] > mx ? s_mm[2 * w + 1] : mx;
+  }
+  if (cnt[3]) {  // bad request data or free list: nothing below is meaningful
+    if (t == 0) set_status(info, CASCADE_EINVAL);
+    return;
+  }
+  // block-table slots, whose extent is only trustworthy now (a large pool's
+  // lists are checked by a grid launched after this kernel)
+  if (check_lists) {
+    const bool bad_slot = any_out_of_range(slots, ro[n], c.num_blocks, t, kBlock);
+    if (__syncthreads_or(bad_slot ? 1 : 0)) {
+      if (t == 0) set_status(info, CASCADE_EINVAL);
+      return;
+    }
+  }
+  if (t == 0) {
+    ctl->bmin = mn;
+    ctl->bmax = mx;
+    ctl->held_rp = sums[0];
+    ctl->need1 = sums[1];
+    ctl->want1 = sums[2];
+    ctl->cnt[0] = cnt[0];
+    ctl->cnt[1] = cnt[1];
+    ctl->cnt[2] = cnt[2];
+  }
+
+  // ---- order-preserving key compression, then LSD radix passes in LDS over
+  //      the digits that are not uniform across the queue.  A thread holds
+  //      jn = ceil(n / kBlock) items, item j at position (wave*jn + j)*64 +
+  //      lane: the order in which wave_digit_rank ranks them.
+  const int jn = (n + kBlock - 1) / kBlock;
+  const unsigned long long span = mx - mn + 1;
+  unsigned long long key[kSortItems];
+  unsigned val[kSortItems];
+  unsigned long long k_and = ~0ull, k_or = 0;
+#pragma unroll
+  for (int j = 0; j < kSortItems; ++j) {
+    const int p = (wave * jn + j) * 64 + lane;
+    key[j] = 0;
+    val[j] = (unsigned)p;
+    if (j >= jn || p >= n) continue;
+    const unsigned long long k0 = U.sort.key[p];
+    key[j] = (k0 >> 62) * span + ((k0 & ((1ull << 62) - 1)) - mn);
+    k_and &= key[j];
+    k_or |= key[j];
+  }
+  for (int off = 32; off >= 1; off >>= 1) {
+    k_and &= __shfl_xor(k_and, off, 64);
+    k_or |= __shfl_xor(k_or, off, 64);
+  }
+  if (lane == 0) {
+    s_mm[2 * kWaves + wave] = k_and;
+    s_mm[3 * kWaves + wave] = k_or;
+  }
+  __syncthreads();
+  unsigned long long varying = 0;
+  {
+    unsigned long long a = ~0ull, b = 0;
+    for (int w = 0; w < kWaves; ++w) {
+      a &= s_mm[2 * kWaves + w];
+      b |= s_mm[3 * kWaves + w];
+    }
+    varying = a ^ b;  // bits that differ between two keys of the queue
+  }
+  const int nd = key_digits(mn, mx, cnt[1], cnt[2]);
+  bool moved = false;
+  for (int d = 0; d < nd; ++d) {
+    if (((varying >> (8 * d)) & 255) == 0) continue;  // uniform: order unchanged
+    moved = true;
+    for (int k = t; k < kWaves * kRadix; k += kBlock) (&U.sort.wcnt[0][0])[k] = 0;
+    __syncthreads();
+    int dig[kSortItems], rank[kSortItems];
+#pragma unroll
+    for (int j = 0; j < kSortItems; ++j) {
+      const int p = (wave * jn + j) * 64 + lane;
+      dig[j] = (j < jn && p < n) ? (int)((key[j] >> (8 * d)) & 255) : -1;
+      rank[j] = j < jn ? wave_digit_rank(dig[j], U.sort.wcnt[wave]) : 0;
+    }
+    __syncthreads();
+    // thread t = digit t: earlier waves' counts, then the digit's start
+    unsigned run = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const unsigned cw = U.sort.wcnt[w][t];
+      U.sort.wcnt[w][t] = run;
+      run += cw;
+    }
+    int st[1] = {(int)run}, tot1[1];
+    block_exclusive_scan<1>(st, tot1, s_scan1);
+    U.sort.start[t] = st[0];
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kSortItems; ++j) {
+      if (dig[j] < 0) continue;
+      const int pos = U.sort.start[dig[j]] + (int)U.sort.wcnt[wave][dig[j]] + rank[j];
+      U.sort.key[pos] = key[j];
+      U.sort.val[pos] = val[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kSortItems; ++j) {
+      const int p = (wave * jn + j) * 64 + lane;
+      if (j < jn && p < n) {
+        key[j] = U.sort.key[p];
+        val[j] = U.sort.val[p];
+      }
+    }
+  }
+
+  // ---- Algorithm 1's Phase 2 as one tile: thread t holds positions
+  //      t*jn .. t*jn + jn - 1
+  int idx[kScanItems];
+  int4 r4[kScanItems];
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    const int p = t * jn + j;
+    idx[j] = (j < jn && p < n) ? (moved ? (int)U.sort.val[p] : p) : -1;
+    r4[j] = idx[j] >= 0 ? U.sort.rec[idx[j]] : make_int4(0, 0, 0, 0);
+  }
+  const ScanConsts K = scan_consts(c, ctl);
+  const long long n_rp = scan_tile<false>(0, jn, K, ctl, info, idx, r4, false, ro, o, rp_list,
+                                          restore_list, tile_tot, nullptr, nullptr, s_lds);
+  __syncthreads();
+  if (t == 0) s_cnt[0] = bad_status(load_agent(info)) ? 1u : 0u;
+  __syncthreads();
+  if (s_cnt[0]) return;
+  finish_step(ctl, info, n, c.n_free, 1, (int)n_rp, tile_tot, free_slots, rp_list, restore_list,
+              slots, o, U.fin);
 }
 
 // A step with no requests: only the free list becomes the slot list.
@@ -1433,6 +1807,19 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   auto *scan1 = reinterpret_cast<unsigned long long *>(ws + L.scan1);
   auto *scan2 = reinterpret_cast<unsigned long long *>(ws + L.scan2);
 
+  if (n <= kSmallMax) {
+    // one workgroup; it checks the free list and the slots itself unless the
+    // pool is large enough for that to dominate
+    const int in_kernel = ts->num_blocks <= kSmallCheckBlocks;
+    hipLaunchKernelGGL(step_small_kernel, dim3(1), dim3(kBlock), 0, s, *rq, bt->row_offsets,
+                       bt->slots, ts->free_slots, c, n, in_kernel, ctl, out->info, o,
+                       out->budget_ns, out->queue_tier_out, rp_list, rlist, tile_tot);
+    if (!in_kernel)
+      hipLaunchKernelGGL(check_lists_kernel, dim3(kCheckGrid), dim3(kBlock), 0, s, n,
+                         ts->num_blocks, ts->n_free, ts->free_slots, bt->row_offsets, bt->slots,
+                         out->info);
+    return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
+  }
   // histograms + every look-back status word: cleared by eval
   const size_t hist_off = L.ctl + offsetof(Ctl, hist);
   const size_t clear_vec = (L.partials - hist_off) / 16;

@@ -28,22 +28,89 @@ __device__ __forceinline__ int rank_in_mask(uint64_t m) {
                                    __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
 }
 
+// Wave64 scans on DPP lane moves (GFX9 data-parallel primitives), register
+// to register: Hillis-Steele doubling inside each row of 16 lanes (row_shr
+// 1, 2, 4, 8), then row 0's total into row 1 and row 2's into row 3
+// (row_bcast:15), then rows 0-1's total into rows 2-3 (row_bcast:31).  A
+// lane with no source reads `ident`.  64-bit values move as two halves.
+enum : int {
+  kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118,
+  kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143
+};
+
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ unsigned dpp_move(unsigned ident, unsigned x) {
+  return (unsigned)__builtin_amdgcn_update_dpp((int)ident, (int)x, kCtrl, kRowMask, 0xf, false);
+}
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ unsigned long long dpp_move(unsigned long long ident,
+                                                       unsigned long long x) {
+  const unsigned lo = dpp_move<kCtrl, kRowMask>((unsigned)ident, (unsigned)x);
+  const unsigned hi = dpp_move<kCtrl, kRowMask>((unsigned)(ident >> 32), (unsigned)(x >> 32));
+  return ((unsigned long long)hi << 32) | lo;
+}
+
+struct OpAdd {
+  template <typename U> __device__ __forceinline__ U operator()(U a, U b) const { return a + b; }
+};
+struct OpMin {
+  template <typename U> __device__ __forceinline__ U operator()(U a, U b) const {
+    return b < a ? b : a;
+  }
+};
+struct OpMax {
+  template <typename U> __device__ __forceinline__ U operator()(U a, U b) const {
+    return b > a ? b : a;
+  }
+};
+
+// Inclusive scan of an associative op over the 64 lanes (U: unsigned or
+// unsigned long long; signed sums go through their two's-complement bits).
+template <typename Op, typename U>
+__device__ __forceinline__ U wave_inclusive_scan(U x, U ident) {
+  const Op op;
+  x = op(x, dpp_move<kDppRowShr1, 0xf>(ident, x));
+  x = op(x, dpp_move<kDppRowShr2, 0xf>(ident, x));
+  x = op(x, dpp_move<kDppRowShr4, 0xf>(ident, x));
+  x = op(x, dpp_move<kDppRowShr8, 0xf>(ident, x));
+  x = op(x, dpp_move<kDppRowBcast15, 0xa>(ident, x));
+  x = op(x, dpp_move<kDppRowBcast31, 0xc>(ident, x));
+  return x;
+}
+
+// Lane 63's value, as a wave-uniform result.
+__device__ __forceinline__ unsigned last_lane(unsigned x) {
+  return (unsigned)__builtin_amdgcn_readlane((int)x, 63);
+}
+__device__ __forceinline__ unsigned long long last_lane(unsigned long long x) {
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)x, 63);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(x >> 32), 63);
+  return ((unsigned long long)hi << 32) | lo;
+}
+
+template <typename T> struct UnsignedOf;
+template <> struct UnsignedOf<int> { typedef unsigned type; };
+template <> struct UnsignedOf<unsigned> { typedef unsigned type; };
+template <> struct UnsignedOf<long long> { typedef unsigned long long type; };
+template <> struct UnsignedOf<unsigned long long> { typedef unsigned long long type; };
+
 template <typename T>
 __device__ __forceinline__ T wave_inclusive_sum(T x) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    T y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  return x;
+  typedef typename UnsignedOf<T>::type U;
+  return (T)wave_inclusive_scan<OpAdd, U>((U)x, (U)0);
 }
 
 template <typename T>
 __device__ __forceinline__ T wave_sum(T x) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
-  return x;
+  typedef typename UnsignedOf<T>::type U;
+  return (T)last_lane(wave_inclusive_scan<OpAdd, U>((U)x, (U)0));
+}
+
+__device__ __forceinline__ unsigned long long wave_min(unsigned long long x) {
+  return last_lane(wave_inclusive_scan<OpMin, unsigned long long>(x, ~0ull));
+}
+__device__ __forceinline__ unsigned long long wave_max(unsigned long long x) {
+  return last_lane(wave_inclusive_scan<OpMax, unsigned long long>(x, 0ull));
 }
 
 // Exclusive prefix sums of K values per thread over the workgroup, in

@@ -173,6 +173,26 @@ def test_einval_matches(dev, name, mutate):
     assert status == ref.EINVAL, name
 
 
+@pytest.mark.parametrize("which", ["slot", "free_slot", "none"])
+def test_small_queue_large_pool_list_checks(dev, which):
+    """A queue of at most 1024 requests runs as one workgroup; over a pool
+    larger than it checks itself, a separate grid checks the free list and
+    the block table.  Out-of-range entries must still give EINVAL."""
+    w, _ = helpers.worked_example()
+    w["params"] = dict(w["params"], num_blocks=100_000)
+    if which == "slot":
+        assert len(w["slots"]) > 0
+        w["slots"] = w["slots"].copy()
+        w["slots"][-1] = 100_000
+    elif which == "free_slot":
+        w["free_slots"] = w["free_slots"].copy()
+        w["free_slots"][0] = 100_000
+    o = ref.step(w)
+    assert o["rc"] == (ref.OK if which == "none" else ref.EINVAL)
+    g, o = run_both(dev, w)
+    assert_same(g, o, which)
+
+
 def test_enospc_matches(dev):
     w, _ = helpers.worked_example()
     for caps in [(71, 100, 100), (100, 19, 100), (100, 100, 31), (0, 0, 0), (72, 20, 32)]:
