@@ -962,7 +962,8 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
 }
 
 // Algorithm 1's Phase 2 over the kScanTile positions of one tile, given
-// each position's request index (idx < 0: past the end) and record; thread
+// each position's request index (idx < 0: past the end), record and block-
+// table row offset (gathered with the record by the caller); thread
 // t holds positions t*jn .. t*jn + jn - 1 of the tile (jn <= kScanItems).  With
 // kChained the tile's level-1 and level-2 prefixes come from the decoupled
 // look-back over the tiles before it; without, the tile is the whole queue.
@@ -998,7 +999,7 @@ __device__ __forceinline__ ScanConsts scan_consts(const Consts &c, const Ctl *ct
 template <bool kChained>
 __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, int *info,
                                const int (&idx)[kScanItems], const int4 (&r4)[kScanItems],
-                               bool broken, const int *__restrict__ ro, const Outs &o,
+                               const int (&row0)[kScanItems], bool broken, const Outs &o,
                                RpInfo *__restrict__ rp_list,
                                RestoreEnt *__restrict__ restore_list,
                                TileTot *__restrict__ tile_tot, unsigned long long *status1,
@@ -1180,7 +1181,7 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
       ri.pos = p;
       ri.eligible = adm ? 0 : 1;
       ri.held = (int)hh[j];
-      ri.row0 = ro[i];
+      ri.row0 = row0[j];
       ri.offl = rec_offl(w);
       ri.pad[0] = ri.pad[1] = 0;
       ri.x = X + xj;
@@ -1267,7 +1268,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   const ScanConsts K = scan_consts(c, ctl);
 
   const int p0 = tile * kScanTile + threadIdx.x * kScanItems;
-  int idx[kScanItems];
+  int idx[kScanItems], rw[kScanItems];
   int4 r4[kScanItems];
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
@@ -1280,9 +1281,10 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     }
     idx[j] = ix;
     r4[j] = ix >= 0 ? rec[ix] : make_int4(0, 0, 0, 0);
+    rw[j] = ix >= 0 ? ro[ix] : 0;
   }
 
-  scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, broken, ro, o, rp_list, restore_list,
+  scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, rw, broken, o, rp_list, restore_list,
                   tile_tot, status1, status2, s_lds);
   if (threadIdx.x == 0) {
     // release this tile's writes, then count it; the last tile finishes the step
@@ -1408,7 +1410,7 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
 
   // ---- evaluation, request j*kBlock + t on thread t (every wave busy); the
   //      raw keys and the records wait in LDS for the sort
-  bool bad = check_lists && any_out_of_range(free_slots, c.n_free, c.num_blocks, t, kBlock);
+  bool bad = false;
   long long sums[3] = {0, 0, 0};
   unsigned cnt[4] = {0, 0, 0, 0};
   unsigned long long mn = ~0ull, mx = 0;
@@ -1429,6 +1431,8 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
     sums[1] += r.need1;
     sums[2] += r.want1;
   }
+  // the free list in range (large pools: checked by a grid after this kernel)
+  if (check_lists) bad |= any_out_of_range(free_slots, c.n_free, c.num_blocks, t, kBlock);
   cnt[3] = bad ? 1u : 0u;
   block_sum<3>(sums, s_red);
   block_sum<4>(cnt, s_cnt);
@@ -1554,16 +1558,17 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
 
   // ---- Algorithm 1's Phase 2 as one tile: thread t holds positions
   //      t*jn .. t*jn + jn - 1
-  int idx[kScanItems];
+  int idx[kScanItems], rw[kScanItems];
   int4 r4[kScanItems];
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     const int p = t * jn + j;
     idx[j] = (j < jn && p < n) ? (moved ? (int)U.sort.val[p] : p) : -1;
     r4[j] = idx[j] >= 0 ? U.sort.rec[idx[j]] : make_int4(0, 0, 0, 0);
+    rw[j] = idx[j] >= 0 ? ro[idx[j]] : 0;
   }
   const ScanConsts K = scan_consts(c, ctl);
-  const long long n_rp = scan_tile<false>(0, jn, K, ctl, info, idx, r4, false, ro, o, rp_list,
+  const long long n_rp = scan_tile<false>(0, jn, K, ctl, info, idx, r4, rw, false, o, rp_list,
                                           restore_list, tile_tot, nullptr, nullptr, s_lds);
   __syncthreads();
   if (t == 0) s_cnt[0] = bad_status(load_agent(info)) ? 1u : 0u;
