@@ -95,9 +95,106 @@ __device__ __forceinline__ char *pool_chunk(const cascade_kv_pool_t &pool, int s
          (long long)kv * pool.kv_stride + (long long)slot * pool.slot_stride;
 }
 
-__device__ __forceinline__ char *staging_chunk(char *staging, const cascade_kv_pool_t &pool,
-                                               int slot, int l, int kv) {
-  return staging + (((long long)slot * pool.num_layers + l) * 2 + kv) * pool.chunk_bytes;
+// Chunks r = 2*l + kv of a block, in the pool and in a staging slot (the
+// staging slot's chunks are consecutive).
+__device__ __forceinline__ char *pool_r(const cascade_kv_pool_t &pool, int slot, int r) {
+  return pool_chunk(pool, slot, r >> 1, r & 1);
+}
+__device__ __forceinline__ char *stage_r(char *staging, const cascade_kv_pool_t &pool, int slot,
+                                         int r) {
+  return staging + ((long long)slot * 2 * pool.num_layers + r) * pool.chunk_bytes;
+}
+
+// A work item ("unit") is g consecutive chunks r0 .. r0+g-1 of one block.
+// Chunks of 32 KiB or more, or of a size that does not tile 32 KiB, are one
+// unit each and move with copy_chunk.  Smaller chunks of a multiple of 4 KiB
+// are grouped g = 32 KiB / chunk to a unit, so that each thread still has
+// kUnroll vectors in flight: vector slot u of a thread is vector
+// ((u & (per - 1)) * kBlock + t) of chunk r0 + (u >> lg), per = 2^lg =
+// chunk / 4 KiB.
+struct Units {
+  int g, lg, per_move;  // chunks per unit, log2(vectors per chunk / kBlock), units per block
+};
+
+template <int kLg>
+__device__ __forceinline__ int unit_off(int u) {
+  return ((u & ((1 << kLg) - 1)) * kBlock) + (int)threadIdx.x;
+}
+
+// one unit of g = kUnroll >> kLg chunks from pool slot to staging slot (or back)
+template <bool kToStaging, int kLg>
+__device__ __forceinline__ void copy_group(const cascade_kv_pool_t &pool, int slot, char *stg,
+                                           int sslot, int r0) {
+  v4i t[kUnroll];
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    const int r = r0 + (u >> kLg);
+    const char *src = kToStaging ? pool_r(pool, slot, r) : stage_r(stg, pool, sslot, r);
+    t[u] = __builtin_nontemporal_load(reinterpret_cast<const v4i *>(src) + unit_off<kLg>(u));
+  }
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    const int r = r0 + (u >> kLg);
+    char *dst = kToStaging ? stage_r(stg, pool, sslot, r) : pool_r(pool, slot, r);
+    __builtin_nontemporal_store(t[u], reinterpret_cast<v4i *>(dst) + unit_off<kLg>(u));
+  }
+}
+
+// spill and the restore into the same unit, as copy_pair: half the slots per
+// stream at a time, the spill's stores before the restore's
+template <int kLg>
+__device__ __forceinline__ void copy_pair_group(const cascade_kv_pool_t &pool, int slot,
+                                                char *spill, int spill_slot, char *fill,
+                                                int fill_slot, int r0) {
+  constexpr int kHalf = kUnroll / 2;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    v4i a[kHalf], b[kHalf];
+#pragma unroll
+    for (int u = 0; u < kHalf; ++u) {
+      const int uu = h * kHalf + u, r = r0 + (uu >> kLg), k = unit_off<kLg>(uu);
+      a[u] = __builtin_nontemporal_load(reinterpret_cast<const v4i *>(pool_r(pool, slot, r)) + k);
+      b[u] = __builtin_nontemporal_load(
+          reinterpret_cast<const v4i *>(stage_r(fill, pool, fill_slot, r)) + k);
+    }
+#pragma unroll
+    for (int u = 0; u < kHalf; ++u) {
+      const int uu = h * kHalf + u, r = r0 + (uu >> kLg), k = unit_off<kLg>(uu);
+      __builtin_nontemporal_store(a[u],
+                                  reinterpret_cast<v4i *>(stage_r(spill, pool, spill_slot, r)) + k);
+    }
+#pragma unroll
+    for (int u = 0; u < kHalf; ++u) {
+      const int uu = h * kHalf + u, r = r0 + (uu >> kLg), k = unit_off<kLg>(uu);
+      __builtin_nontemporal_store(b[u], reinterpret_cast<v4i *>(pool_r(pool, slot, r)) + k);
+    }
+  }
+}
+
+// The unit shape is a template parameter of the kernels, so each compiled
+// kernel holds one copy path: kLg < 0 whole chunks (g == 1), else a group of
+// g = kUnroll >> kLg chunks.
+template <bool kToStaging, int kLg>
+__device__ __forceinline__ void copy_unit(const cascade_kv_pool_t &pool, int slot, char *stg,
+                                          int sslot, int r0, int vecs) {
+  if constexpr (kLg < 0) {
+    char *pc = pool_r(pool, slot, r0);
+    char *sc = stage_r(stg, pool, sslot, r0);
+    copy_chunk(kToStaging ? pc : sc, kToStaging ? sc : pc, vecs);
+  } else {
+    copy_group<kToStaging, kLg>(pool, slot, stg, sslot, r0);
+  }
+}
+
+template <int kLg>
+__device__ __forceinline__ void copy_pair_unit(const cascade_kv_pool_t &pool, int slot,
+                                               char *spill, int spill_slot, char *fill,
+                                               int fill_slot, int r0, int vecs) {
+  if constexpr (kLg < 0)
+    copy_pair(pool_r(pool, slot, r0), stage_r(spill, pool, spill_slot, r0),
+              stage_r(fill, pool, fill_slot, r0), vecs);
+  else
+    copy_pair_group<kLg>(pool, slot, spill, spill_slot, fill, fill_slot, r0);
 }
 
 __device__ __forceinline__ bool move_ok(const cascade_move_t &mv, int num_slots,
@@ -110,29 +207,25 @@ __device__ __forceinline__ void flag_bad(int *status) {
   if (threadIdx.x == 0 && status) *status = CASCADE_EINVAL;
 }
 
-template <bool kToStaging>
-__global__ __launch_bounds__(kBlock) void kvcopy_kernel(cascade_kv_pool_t pool, char *staging,
-                                                        int staging_slots,
+template <bool kToStaging, int kLg>
+__global__ __launch_bounds__(kBlock) void kvcopy_kernel(cascade_kv_pool_t pool, Units un,
+                                                        char *staging, int staging_slots,
                                                         const cascade_move_t *__restrict__ moves,
                                                         const int *__restrict__ n_dev,
                                                         int max_moves, int *status) {
   const int nm = min(*n_dev, max_moves);
   if (nm <= 0) return;
-  const int per_move = 2 * pool.num_layers;
-  const long long total = (long long)nm * per_move;
+  const long long total = (long long)nm * un.per_move;
   const int vecs = (int)(pool.chunk_bytes >> 4);
   for (long long c = blockIdx.x; c < total; c += gridDim.x) {
-    const int m = (int)(c / per_move);
-    const int r = (int)(c - (long long)m * per_move);
-    const int l = r >> 1, kv = r & 1;
+    const int m = (int)(c / un.per_move);
+    const int r0 = (int)(c - (long long)m * un.per_move) * un.g;
     const cascade_move_t mv = moves[m];
     if (!move_ok(mv, pool.num_slots, staging_slots)) {
       flag_bad(status);
       continue;
     }
-    char *pc = pool_chunk(pool, mv.pool_slot, l, kv);
-    char *sc = staging_chunk(staging, pool, mv.staging_slot, l, kv);
-    copy_chunk(kToStaging ? pc : sc, kToStaging ? sc : pc, vecs);
+    copy_unit<kToStaging, kLg>(pool, mv.pool_slot, staging, mv.staging_slot, r0, vecs);
   }
 }
 
@@ -144,18 +237,20 @@ __global__ __launch_bounds__(kBlock) void kvcopy_kernel(cascade_kv_pool_t pool, 
 // overwrites them: the wait is inside the thread, none crosses workgroups.
 // The pairing test reads the same two words from both sides, so every
 // unpack move is copied exactly once.
+template <int kLg>
 __global__ __launch_bounds__(kBlock) void kvmove_kernel(
-    cascade_kv_pool_t pool, char *pst, int pst_slots, const cascade_move_t *__restrict__ pm,
+    cascade_kv_pool_t pool, Units un, char *pst, int pst_slots,
+    const cascade_move_t *__restrict__ pm,
     const int *__restrict__ pn_dev, int pmax, const int *__restrict__ phz, char *ust,
     int ust_slots, const cascade_move_t *__restrict__ um, const int *__restrict__ un_dev,
     int umax, const int *__restrict__ uhz, int *status) {
   const int np = max(0, min(*pn_dev, pmax));
   const int nu = max(0, min(*un_dev, umax));
-  const int per_move = 2 * pool.num_layers;
+  const int per_move = un.per_move;
   const long long tp = (long long)np * per_move, tu = (long long)nu * per_move;
   const long long both = 2 * (tp < tu ? tp : tu), total = tp + tu;
   const int vecs = (int)(pool.chunk_bytes >> 4);
-  // the grid is even (2 * num_layers divides every chunk count), so c and
+  // the grid is even when it is below the item count, so c and
   // c ^ 1 fall in the same iteration: flipping the low bit on odd iterations
   // is a bijection that makes every workgroup alternate between pack and
   // unpack items, whatever share of the pack items carries a paired unpack
@@ -173,8 +268,7 @@ __global__ __launch_bounds__(kBlock) void kvmove_kernel(
       ci = c - both + (both >> 1);
     }
     const int mi = (int)(ci / per_move);
-    const int r = (int)(ci - (long long)mi * per_move);
-    const int l = r >> 1, kv = r & 1;
+    const int r0 = (int)(ci - (long long)mi * per_move) * un.g;
     // the item's move and hazard word are requested together
     const cascade_move_t mv = is_pack ? pm[mi] : um[mi];
     const int partner = is_pack ? phz[mi] : uhz[mi];
@@ -192,22 +286,16 @@ __global__ __launch_bounds__(kBlock) void kvmove_kernel(
         paired = false;  // the restore is skipped; the spill still runs
       }
       if (ok && paired && mu.pool_slot == mv.pool_slot) {
-        copy_pair(pool_chunk(pool, mv.pool_slot, l, kv),
-                  staging_chunk(pst, pool, mv.staging_slot, l, kv),
-                  staging_chunk(ust, pool, mu.staging_slot, l, kv), vecs);
+        copy_pair_unit<kLg>(pool, mv.pool_slot, pst, mv.staging_slot, ust, mu.staging_slot, r0,
+                            vecs);
       } else {
-        if (ok)
-          copy_chunk(pool_chunk(pool, mv.pool_slot, l, kv),
-                     staging_chunk(pst, pool, mv.staging_slot, l, kv), vecs);
-        if (paired)
-          copy_chunk(staging_chunk(ust, pool, mu.staging_slot, l, kv),
-                     pool_chunk(pool, mu.pool_slot, l, kv), vecs);
+        if (ok) copy_unit<true, kLg>(pool, mv.pool_slot, pst, mv.staging_slot, r0, vecs);
+        if (paired) copy_unit<false, kLg>(pool, mu.pool_slot, ust, mu.staging_slot, r0, vecs);
       }
     } else {
       if (partner >= 0 && partner < np && phz[partner] == mi) continue;  // after its pack
       if (move_ok(mv, pool.num_slots, ust_slots))
-        copy_chunk(staging_chunk(ust, pool, mv.staging_slot, l, kv),
-                   pool_chunk(pool, mv.pool_slot, l, kv), vecs);
+        copy_unit<false, kLg>(pool, mv.pool_slot, ust, mv.staging_slot, r0, vecs);
       else
         flag_bad(status);
     }
@@ -229,9 +317,26 @@ bool list_ok(const void *staging, int32_t staging_slots, const cascade_move_t *m
   return ((uintptr_t)staging & 15) == 0;
 }
 
-int grid_for(const cascade_kv_pool_t *pool, long long moves) {
-  const long long chunks = moves * 2 * pool->num_layers;
-  return (int)std::max<long long>(1, std::min(chunks, kMaxGrid));
+Units units_for(const cascade_kv_pool_t *pool) {
+  Units u;
+  u.g = 1;
+  u.lg = 0;
+  const long long vecs = pool->chunk_bytes >> 4;
+  const int chunks = 2 * pool->num_layers;
+  const int full = kBlock * kUnroll;  // vectors one thread batch covers
+  if (vecs < full && vecs % kBlock == 0 && full % vecs == 0 && chunks % (full / vecs) == 0) {
+    u.g = (int)(full / vecs);
+    while ((kBlock << u.lg) < vecs) ++u.lg;
+  }
+  u.per_move = chunks / u.g;
+  return u;
+}
+
+int grid_for(const Units &u, long long moves) {
+  const long long items = moves * u.per_move;
+  long long g = std::max<long long>(1, std::min(items, kMaxGrid));
+  if (g > 1 && (g & 1)) --g;  // even: the fused kernel alternates its lists by iteration
+  return (int)g;
 }
 
 template <bool kToStaging>
@@ -241,8 +346,13 @@ int launch(const cascade_kv_pool_t *pool, const void *staging, int32_t staging_s
   if (!pool_ok(pool) || !list_ok(staging, staging_slots, moves, n_dev, max_moves))
     return CASCADE_EINVAL;
   if (max_moves == 0) return CASCADE_OK;
-  hipLaunchKernelGGL(kvcopy_kernel<kToStaging>, dim3(grid_for(pool, max_moves)), dim3(kBlock),
-                     0, static_cast<hipStream_t>(stream), *pool,
+  const Units u = units_for(pool);
+  auto kernel = u.g == 1 ? kvcopy_kernel<kToStaging, -1>
+                : u.lg == 0 ? kvcopy_kernel<kToStaging, 0>
+                : u.lg == 1 ? kvcopy_kernel<kToStaging, 1>
+                            : kvcopy_kernel<kToStaging, 2>;
+  hipLaunchKernelGGL(kernel, dim3(grid_for(u, max_moves)), dim3(kBlock), 0,
+                     static_cast<hipStream_t>(stream), *pool, u,
                      const_cast<char *>(static_cast<const char *>(staging)), staging_slots, moves,
                      n_dev, max_moves, status);
   return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
@@ -280,8 +390,13 @@ extern "C" int cascade_pack_unpack(const cascade_kv_pool_t *pool, void *pack_sta
     return CASCADE_EINVAL;
   if ((max_pack > 0 && !pack_hazard) || (max_unpack > 0 && !unpack_hazard)) return CASCADE_EINVAL;
   if (max_pack == 0 && max_unpack == 0) return CASCADE_OK;
-  hipLaunchKernelGGL(kvmove_kernel, dim3(grid_for(pool, (long long)max_pack + max_unpack)),
-                     dim3(kBlock), 0, static_cast<hipStream_t>(stream), *pool,
+  const Units u = units_for(pool);
+  auto kernel = u.g == 1 ? kvmove_kernel<-1>
+                : u.lg == 0 ? kvmove_kernel<0>
+                : u.lg == 1 ? kvmove_kernel<1>
+                            : kvmove_kernel<2>;
+  hipLaunchKernelGGL(kernel, dim3(grid_for(u, (long long)max_pack + max_unpack)),
+                     dim3(kBlock), 0, static_cast<hipStream_t>(stream), *pool, u,
                      static_cast<char *>(pack_staging), pack_staging_slots, pack_moves,
                      n_pack_dev, max_pack, pack_hazard,
                      const_cast<char *>(static_cast<const char *>(unpack_staging)),

@@ -37,7 +37,7 @@ def _moves(slots, staging=None):
 
 
 @pytest.mark.parametrize("layout", ["layer_major", "block_major"])
-@pytest.mark.parametrize("chunk", [16, 48, 8192, 32768])
+@pytest.mark.parametrize("chunk", [16, 48, 4096, 8192, 16384, 32768, 65536])
 def test_pack_unpack_small(dev, layout, chunk):
     import torch
     from paper_2608_06557_amd import cascade
@@ -217,7 +217,7 @@ def _fused(dev, pool_t, geom, pst, np_slots, pm, ph, ust, nu_slots, um, uh, caps
 
 
 @pytest.mark.parametrize("layout", ["layer_major", "block_major"])
-@pytest.mark.parametrize("chunk", [16, 48, 8192])
+@pytest.mark.parametrize("chunk", [16, 48, 4096, 8192, 16384])
 @pytest.mark.parametrize("n_pack,n_unpack,shared", [(23, 17, 9), (5, 31, 5), (31, 0, 0),
                                                     (0, 12, 0), (40, 40, 40), (1, 1, 1)])
 def test_fused_equals_pack_then_unpack(dev, layout, chunk, n_pack, n_unpack, shared):
