@@ -452,3 +452,65 @@ void cref_unpack(const cref_pool *pl, const uint8_t *staging, const cref_move *m
         memcpy(pool_chunk(pl, mv[m].pool_slot, l, kv),
                staging + staging_off(pl, mv[m].staging_slot, l, kv), (size_t)pl->chunk_bytes);
 }
+
+/* ------------------------------------------------- prefix hit detection */
+
+typedef struct { uint64_t hash; uint8_t tier; } cref_ientry;
+
+static int cmp_ientry(const void *a, const void *b) {
+  const uint64_t x = ((const cref_ientry *)a)->hash, y = ((const cref_ientry *)b)->hash;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+static int cmp_key(const void *k, const void *e) {
+  const uint64_t x = *(const uint64_t *)k, y = ((const cref_ientry *)e)->hash;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+int32_t cref_prefix_probe(int32_t n_entries, const uint64_t *index_hashes,
+                          const uint8_t *index_tiers, int32_t n, const int32_t *block_offsets,
+                          const uint64_t *block_hashes, const int32_t *n_in,
+                          int32_t block_tokens, int32_t *n_prefix_out,
+                          uint8_t *prefix_tier_out) {
+  if (n_entries < 0 || n < 0 || block_tokens < 1) return CREF_EINVAL;
+  if (n > 0 && block_offsets[0] != 0) return CREF_EINVAL;
+  for (int32_t i = 0; i < n; i++) {
+    if (block_offsets[i + 1] < block_offsets[i] || n_in[i] < 1) return CREF_EINVAL;
+    for (int32_t b = block_offsets[i]; b < block_offsets[i + 1]; b++)
+      if (block_hashes[b] == 0) return CREF_EINVAL;
+  }
+  /* the index: one entry per distinct hash, holding its deepest tier */
+  cref_ientry *idx = (cref_ientry *)malloc(sizeof(cref_ientry) * (size_t)(n_entries ? n_entries : 1));
+  for (int32_t e = 0; e < n_entries; e++) {
+    if (index_hashes[e] == 0 || index_tiers[e] > CREF_KV_NVME) { free(idx); return CREF_EINVAL; }
+    idx[e].hash = index_hashes[e];
+    idx[e].tier = index_tiers[e];
+  }
+  qsort(idx, (size_t)n_entries, sizeof(cref_ientry), cmp_ientry);
+  int32_t m = 0;
+  for (int32_t e = 0; e < n_entries; e++) {
+    if (m > 0 && idx[m - 1].hash == idx[e].hash) {
+      if (idx[e].tier > idx[m - 1].tier) idx[m - 1].tier = idx[e].tier;
+    } else {
+      idx[m++] = idx[e];
+    }
+  }
+  /* each request: leading blocks while they are cached, up to the cap */
+  for (int32_t i = 0; i < n; i++) {
+    const int32_t have = block_offsets[i + 1] - block_offsets[i];
+    const int32_t cap = (n_in[i] - 1) / block_tokens;
+    const int32_t lim = have < cap ? have : cap;
+    int32_t matched = 0;
+    uint8_t tier = 0;
+    while (matched < lim) {
+      const cref_ientry *hit = (const cref_ientry *)bsearch(
+          &block_hashes[block_offsets[i] + matched], idx, (size_t)m, sizeof(cref_ientry), cmp_key);
+      if (!hit) break;
+      if (hit->tier > tier) tier = hit->tier;
+      matched++;
+    }
+    n_prefix_out[i] = matched * block_tokens;
+    prefix_tier_out[i] = matched > 0 ? tier : (uint8_t)CREF_KV_NONE;
+  }
+  free(idx);
+  return CREF_OK;
+}

@@ -121,6 +121,22 @@ typedef struct {
   uint8_t *base; int32_t num_layers;
   int64_t chunk_bytes, layer_stride, kv_stride, slot_stride;
 } cref_pool;
+/* Prefix hit detection (Section 4.4): an index records, for each cached KV
+   block (by its prefix hash), the deepest tier holding it; a request's
+   matched prefix is its longest run of leading blocks all in the index,
+   capped at floor((n_in - 1) / block_tokens) blocks so that at least one
+   prompt token is computed; its tier is the deepest over those blocks
+   (CREF_KV_NONE when nothing matches).  index_hashes/index_tiers list
+   n_entries cached (block, tier) facts, duplicates allowed.  Request i's
+   block hashes are block_hashes[block_offsets[i] .. block_offsets[i+1]).
+   Returns CREF_EINVAL for a negative count, a tier outside HBM..NVMe, hash
+   0 (reserved for empty index slots), or offsets that are not monotone. */
+int32_t cref_prefix_probe(int32_t n_entries, const uint64_t *index_hashes,
+                          const uint8_t *index_tiers, int32_t n, const int32_t *block_offsets,
+                          const uint64_t *block_hashes, const int32_t *n_in,
+                          int32_t block_tokens, int32_t *n_prefix_out,
+                          uint8_t *prefix_tier_out);
+
 void cref_pack(const cref_pool *pool, uint8_t *staging, const cref_move *moves, int32_t n);
 void cref_unpack(const cref_pool *pool, const uint8_t *staging, const cref_move *moves, int32_t n);
 

@@ -111,6 +111,10 @@ def lib():
         L.cref_pack.argtypes = [C.POINTER(Pool), C.c_void_p, C.c_void_p, C.c_int32]
         L.cref_unpack.restype = None
         L.cref_unpack.argtypes = [C.POINTER(Pool), C.c_void_p, C.c_void_p, C.c_int32]
+        L.cref_prefix_probe.restype = C.c_int32
+        L.cref_prefix_probe.argtypes = [C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
+                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                        C.c_void_p, C.c_void_p]
         _lib = L
     return _lib
 
@@ -242,3 +246,22 @@ def pack(pool: np.ndarray, geom: dict, staging: np.ndarray, moves: np.ndarray) -
 def unpack(pool: np.ndarray, geom: dict, staging: np.ndarray, moves: np.ndarray) -> None:
     moves = np.ascontiguousarray(moves, dtype=MOVE_DTYPE)
     lib().cref_unpack(C.byref(make_pool(pool, geom)), _ptr(staging), _ptr(moves), len(moves))
+
+
+def prefix_probe(index_hashes: np.ndarray, index_tiers: np.ndarray, block_offsets: np.ndarray,
+                 block_hashes: np.ndarray, n_in: np.ndarray, block_tokens: int) -> dict:
+    """Matched prefix length (tokens) and tier of every request (Section 4.4,
+    prefix hit detection), from the oracle."""
+    ih = np.ascontiguousarray(index_hashes, dtype=np.uint64)
+    it = np.ascontiguousarray(index_tiers, dtype=np.uint8)
+    off = np.ascontiguousarray(block_offsets, dtype=np.int32)
+    bh = np.ascontiguousarray(block_hashes, dtype=np.uint64)
+    ni = np.ascontiguousarray(n_in, dtype=np.int32)
+    n = len(off) - 1
+    npre = np.zeros(max(n, 1), np.int32)
+    tier = np.zeros(max(n, 1), np.uint8)
+    keep = [ih, it, off, bh, ni]
+    ptr = [_ptr(a if a.size else np.zeros(1, a.dtype)) for a in keep]
+    rc = lib().cref_prefix_probe(len(ih), ptr[0], ptr[1], n, ptr[2], ptr[3], ptr[4],
+                                 int(block_tokens), _ptr(npre), _ptr(tier))
+    return {"rc": rc, "n_prefix": npre[:n], "prefix_tier": tier[:n]}

@@ -300,3 +300,72 @@ def hash32_torch(word_index, seed: int):
     x = (x * 0x346CA68B) & m
     x = x ^ (x >> 16)
     return x.to(torch.int64)
+
+
+def block_hash64(req: np.ndarray, blk: np.ndarray, seed: int) -> np.ndarray:
+    """Stand-in for a chained per-block prefix hash: a nonzero 64-bit value
+    per (request or shared-prefix id, block index), two counter-based words."""
+    key = (req.astype(np.int64) * np.int64(1 << 20) + blk.astype(np.int64)).astype(np.uint64)
+    k_lo = (key & np.uint64(0xFFFFFFFF)).astype(np.int64)
+    k_hi = (key >> np.uint64(32)).astype(np.int64)
+    x1 = hash32_np(k_lo, seed).astype(np.int64)
+    x2 = hash32_np(k_hi ^ x1, seed + 1).astype(np.uint64)
+    x3 = hash32_np(k_lo ^ x2.astype(np.int64), seed + 2).astype(np.uint64)
+    h = (x2 << np.uint64(32)) | x3
+    return np.where(h == 0, np.uint64(1), h)
+
+
+def make_prefix_workload(cfg: int, seed: int | None = None, n: int | None = None,
+                         shared_frac: float = 0.0, dup_frac: float = 0.3,
+                         gap_frac: float = 0.2, noise: int = 0) -> dict:
+    """Inputs of the prefix-hit lookup: every request's prompt block hashes
+    (its full blocks, CSR) and a cache index of (block hash, tier) facts.
+
+    A request's cached run is the first n_prefix / bt blocks of the step
+    workload, in its prefix tier.  Extras that a lookup must see through:
+    shallower duplicates of cached blocks (dup_frac of the requests), a
+    cached block past the first uncached one (gap_frac), unrelated entries
+    (noise), and families of requests sharing leading blocks (shared_frac;
+    members take their family head's cached run and tier)."""
+    w = make_workload(cfg, seed=seed, n=n)
+    rng = np.random.Generator(np.random.PCG64((7919 + cfg) if seed is None else seed + 7919))
+    bt = BLOCK_TOKENS
+    n = len(w["n_in"])
+    n_in = np.asarray(w["n_in"], np.int64)
+    full = n_in // bt
+    pre_blocks = np.asarray(w["n_prefix"], np.int64) // bt
+    tier = np.asarray(w["prefix_tier"], np.uint8).copy()
+    owner = np.arange(n, dtype=np.int64)      # whose hash sequence a request's blocks use
+    if shared_frac > 0 and n > 1:
+        members = np.flatnonzero(rng.random(n) < shared_frac)
+        heads = rng.integers(0, n, len(members))
+        for m, hd in zip(members, heads):
+            owner[m] = owner[hd]
+            cap = (n_in[m] - 1) // bt
+            pre_blocks[m] = min(pre_blocks[hd], cap, full[m])
+            tier[m] = tier[hd]
+    offsets = np.zeros(n + 1, np.int64)
+    offsets[1:] = np.cumsum(full)
+    req_of = np.repeat(np.arange(n), full)
+    blk_of = np.arange(offsets[-1]) - offsets[req_of]
+    hashes = block_hash64(owner[req_of], blk_of, 17 + cfg)
+    cached = blk_of < pre_blocks[req_of]
+    cached &= tier[req_of] <= 2
+    ih = [hashes[cached]]
+    it = [tier[req_of][cached]]
+    dup = cached & (rng.random(len(hashes)) < dup_frac)
+    ih.append(hashes[dup])
+    it.append(rng.integers(0, 3, int(dup.sum())).astype(np.uint8) % (tier[req_of][dup] + 1))
+    gap = (blk_of == pre_blocks[req_of] + 1) & (rng.random(len(hashes)) < gap_frac)
+    ih.append(hashes[gap])
+    it.append(rng.integers(0, 3, int(gap.sum())).astype(np.uint8))
+    if noise:
+        ih.append(block_hash64(np.full(noise, -1), np.arange(noise), 29 + cfg))
+        it.append(rng.integers(0, 3, noise).astype(np.uint8))
+    ih = np.concatenate(ih)
+    it = np.concatenate(it)
+    pre_blocks = np.where(tier <= 2, pre_blocks, 0)
+    order = rng.permutation(len(ih))
+    return {"n_in": w["n_in"].astype(np.int32), "block_offsets": offsets.astype(np.int32),
+            "block_hashes": hashes, "index_hashes": ih[order], "index_tiers": it[order],
+            "block_tokens": bt, "expect_blocks": pre_blocks, "expect_tier": tier}
