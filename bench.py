@@ -66,6 +66,46 @@ def progress(msg):
     print(f"bench: {msg}", file=sys.stderr, flush=True)
 
 
+def measure_prefix_probe(cfg, stream, reps=20):
+    """The step's inputs n_prefix / prefix_tier from block hashes: index build
+    (clear + insert) and lookup on the workload's requests, HIP events on the
+    stream that runs them (outside the step's timed region)."""
+    import torch
+    import paper_2608_06557_amd.synth as synth
+    from paper_2608_06557_amd import device
+    pw = synth.make_prefix_workload(cfg, shared_frac=0.3)
+    d = device.DevicePrefix(pw)
+    assert d.build(stream) == 0 and d.probe(stream) == 0
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    tb, tp = [], []
+    for _ in range(reps):
+        ev[0].record(stream)
+        assert d.build(stream) == 0
+        ev[1].record(stream)
+        assert d.probe(stream) == 0
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        tb.append(ev[0].elapsed_time(ev[1]) * 1e3)
+        tp.append(ev[1].elapsed_time(ev[2]) * 1e3)
+    g = d.fetch()
+    assert g["status"] == 0
+    n = d.n
+    bt = pw["block_tokens"]
+    full = np.diff(pw["block_offsets"])
+    lim = np.minimum(full, (pw["n_in"] - 1) // bt)
+    matched = g["n_prefix"] // bt
+    looked = np.minimum(lim, matched + 1)       # blocks a lookup must examine
+    us = float(np.median(tp))
+    progress("prefix lookup measured")
+    return {"requests": n, "index_facts": d.n_entries, "index_slots": d.capacity,
+            "prompt_blocks": int(full.sum()), "blocks_examined": int(looked.sum()),
+            "matched_blocks": int(matched.sum()),
+            "build_us_p50": float(np.median(tb)), "probe_us_p50": us,
+            "probe_req_per_s": n / (us * 1e-6),
+            "blocks_examined_per_s": float(looked.sum()) / (us * 1e-6)}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -82,6 +122,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent on the oracle baseline")
+    ap.add_argument("--no-prefix-probe", action="store_true",
+                    help="skip the prefix-hit lookup measurement")
     ap.add_argument("--calib-copy-gb", type=float, default=0.0,
                     help="also run a plain torch copy of this size (counter calibration)")
     return ap.parse_args()
@@ -279,6 +321,7 @@ def main():
         dtod = {"bytes": nb_copy, "GBps": gbps(2.0 * nb_copy, us)}
         del a, b
     progress("cold-cache steps and device copy done")
+    probe = None if args.no_prefix_probe else measure_prefix_probe(cfg, stream)
     kernel = "kvmove_kernel" if fused else "kvcopy_kernel"
     copies = {"mode": args.copy, "pack_blocks": n_pack, "unpack_blocks": n_unpack,
               "paired_blocks": int((res["unpack_hazard"] >= 0).sum()),
@@ -319,6 +362,8 @@ def main():
                      "bytes_per_launch": (bytes_pack + bytes_unpack) / launches,
                      "us_per_launch": copy_us / launches},
     }
+    if probe:
+        out["prefix_probe"] = probe
     if extra:
         out["calib_copy"] = extra
     if not args.no_cpu_baseline:

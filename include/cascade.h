@@ -265,6 +265,42 @@ int cascade_pack_unpack(const cascade_kv_pool_t *pool, void *pack_staging,
                         int32_t max_unpack, const int32_t *unpack_hazard, int32_t *status_dev,
                         void *stream);
 
+/* Prefix hit detection (Section 4.4): an index that records, for every
+   cached KV block (keyed by its nonzero 64-bit prefix hash), the deepest
+   tier holding it (CASCADE_KV_HBM < DRAM < NVME).  A request's matched
+   prefix is the longest run of its leading prompt blocks that are all in the
+   index, capped at floor((n_in - 1) / block_tokens) blocks so that at least
+   one prompt token is computed; its tier is the deepest over that run.  The
+   results are the n_prefix / prefix_tier inputs of cascade_step.
+
+   The index is caller-owned device memory of cascade_prefix_index_bytes()
+   bytes (16-byte aligned), an open-addressing table of `capacity` slots
+   (a power of two in [64, 2^30]; keep it at least twice the number of
+   distinct cached blocks).  cascade_prefix_index_clear empties it (a fill
+   kernel, so it may be captured in a graph).  cascade_prefix_index_insert
+   adds n (hash, tier) facts; a block inserted several times keeps its
+   deepest tier; inserts may run concurrently with each other but not with
+   a probe.  Hash 0 or a tier above CASCADE_KV_NVME sets *status_dev =
+   CASCADE_EINVAL and is skipped; a full table sets CASCADE_ENOSPC.
+   cascade_prefix_probe looks up request i's block hashes
+   block_hashes[block_offsets[i] .. block_offsets[i+1]) (device CSR, offsets
+   starting at 0) and writes n_prefix_out[i] (tokens, a multiple of
+   block_tokens) and prefix_tier_out[i] (CASCADE_KV_NONE when nothing
+   matches).  Decreasing offsets, n_in < 1 or a zero hash set
+   CASCADE_EINVAL.  status_dev may be NULL.  All return CASCADE_EINVAL for
+   NULL pointers, a bad capacity or misalignment, CASCADE_EHIP on a failed
+   launch. */
+#define CASCADE_INDEX_SLOT_BYTES 16
+size_t cascade_prefix_index_bytes(int32_t capacity);
+int cascade_prefix_index_clear(void *index, int32_t capacity, void *stream);
+int cascade_prefix_index_insert(void *index, int32_t capacity, const uint64_t *hashes,
+                                const uint8_t *tiers, int32_t n, int32_t *status_dev,
+                                void *stream);
+int cascade_prefix_probe(const void *index, int32_t capacity, int32_t n,
+                         const int32_t *block_offsets, const uint64_t *block_hashes,
+                         const int32_t *n_in, int32_t block_tokens, int32_t *n_prefix_out,
+                         uint8_t *prefix_tier_out, int32_t *status_dev, void *stream);
+
 /* Short English text for a return code or status value. */
 const char *cascade_strerror(int code);
 

@@ -21,7 +21,9 @@ INFO_STATUS, INFO_N_ADMITTED, INFO_N_SLOT_LIST, INFO_N_UNPACK, INFO_N_PACK = 0, 
 INFO_LEN = 8
 
 EXPORTED = ["cascade_step_workspace_bytes", "cascade_step", "cascade_pack", "cascade_unpack",
-            "cascade_pack_unpack", "cascade_strerror"]
+            "cascade_pack_unpack", "cascade_prefix_index_bytes", "cascade_prefix_index_clear",
+            "cascade_prefix_index_insert", "cascade_prefix_probe", "cascade_strerror"]
+INDEX_SLOT_BYTES = 16
 
 
 class Requests(C.Structure):
@@ -104,6 +106,17 @@ def load() -> C.CDLL:
                                           C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
                                           C.c_int32, C.c_void_p,
                                           C.c_void_p, C.c_void_p]
+        L.cascade_prefix_index_bytes.restype = C.c_size_t
+        L.cascade_prefix_index_bytes.argtypes = [C.c_int32]
+        L.cascade_prefix_index_clear.restype = C.c_int
+        L.cascade_prefix_index_clear.argtypes = [C.c_void_p, C.c_int32, C.c_void_p]
+        L.cascade_prefix_index_insert.restype = C.c_int
+        L.cascade_prefix_index_insert.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                                                  C.c_int32, C.c_void_p, C.c_void_p]
+        L.cascade_prefix_probe.restype = C.c_int
+        L.cascade_prefix_probe.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
+                                           C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p,
+                                           C.c_void_p, C.c_void_p, C.c_void_p]
         L.cascade_strerror.restype = C.c_char_p
         L.cascade_strerror.argtypes = [C.c_int]
         _lib = L
@@ -145,6 +158,31 @@ def cascade_pack_unpack(pool: KvPool, pack_staging: int, pack_staging_slots: int
         C.byref(pool), v(pack_staging), pack_staging_slots, v(pack_moves), v(n_pack_dev),
         max_pack, v(pack_hazard), v(unpack_staging), unpack_staging_slots, v(unpack_moves),
         v(n_unpack_dev), max_unpack, v(unpack_hazard), v(status_dev), v(stream)))
+
+
+def cascade_prefix_index_bytes(capacity: int) -> int:
+    return int(load().cascade_prefix_index_bytes(capacity))
+
+
+def cascade_prefix_index_clear(index: int, capacity: int, stream: int) -> int:
+    return int(load().cascade_prefix_index_clear(C.c_void_p(index), capacity, C.c_void_p(stream)))
+
+
+def cascade_prefix_index_insert(index: int, capacity: int, hashes: int, tiers: int, n: int,
+                                status_dev: int, stream: int) -> int:
+    v = C.c_void_p
+    return int(load().cascade_prefix_index_insert(v(index), capacity, v(hashes), v(tiers), n,
+                                                  v(status_dev), v(stream)))
+
+
+def cascade_prefix_probe(index: int, capacity: int, n: int, block_offsets: int,
+                         block_hashes: int, n_in: int, block_tokens: int, n_prefix_out: int,
+                         prefix_tier_out: int, status_dev: int, stream: int) -> int:
+    v = C.c_void_p
+    return int(load().cascade_prefix_probe(v(index), capacity, n, v(block_offsets),
+                                           v(block_hashes), v(n_in), block_tokens,
+                                           v(n_prefix_out), v(prefix_tier_out), v(status_dev),
+                                           v(stream)))
 
 
 def cascade_strerror(code: int) -> str:

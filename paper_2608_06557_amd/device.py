@@ -145,3 +145,56 @@ def fill_pattern_(t, seed: int, word_offset: int = 0, chunk_words: int = 1 << 26
         if progress is not None and (k + 1) % every == 0:
             torch.cuda.synchronize(t.device)
             progress(f"filled {4 * e / 1e9:.0f} of {4 * nw / 1e9:.0f} GB")
+
+
+def index_capacity(n_entries: int) -> int:
+    """Slots for an index of n_entries facts: a power of two, load <= 1/2."""
+    cap = 64
+    while cap < 2 * max(n_entries, 1):
+        cap *= 2
+    return cap
+
+
+class DevicePrefix:
+    """Device buffers of one prefix-hit lookup: the index built from
+    (hash, tier) facts and the requests' block-hash CSR."""
+
+    def __init__(self, pw: dict, device="cuda:0", capacity: int | None = None):
+        torch = _torch()
+        self.device = torch.device(device)
+        self.n = int(len(pw["n_in"]))
+        self.n_entries = int(len(pw["index_hashes"]))
+        self.capacity = capacity or index_capacity(self.n_entries)
+        self.bt = int(pw["block_tokens"])
+        nbytes = cx.cascade_prefix_index_bytes(self.capacity)
+        assert nbytes > 0, self.capacity
+        self.index = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+        self.ih = to_device(np.asarray(pw["index_hashes"]), self.device)
+        self.it = to_device(np.asarray(pw["index_tiers"]), self.device, np.uint8)
+        self.off = to_device(np.asarray(pw["block_offsets"]), self.device, np.int32)
+        self.bh = to_device(np.asarray(pw["block_hashes"]), self.device)
+        self.n_in = to_device(np.asarray(pw["n_in"]), self.device, np.int32)
+        self.n_prefix = torch.zeros(max(self.n, 1), dtype=torch.int32, device=self.device)
+        self.tier = torch.zeros(max(self.n, 1), dtype=torch.uint8, device=self.device)
+        self.status = torch.zeros(1, dtype=torch.int32, device=self.device)
+
+    def build(self, stream=None) -> int:
+        s = stream_handle(stream)
+        rc = cx.cascade_prefix_index_clear(self.index.data_ptr(), self.capacity, s)
+        return rc or cx.cascade_prefix_index_insert(self.index.data_ptr(), self.capacity,
+                                                    self.ih.data_ptr(), self.it.data_ptr(),
+                                                    self.n_entries, self.status.data_ptr(), s)
+
+    def probe(self, stream=None) -> int:
+        return cx.cascade_prefix_probe(self.index.data_ptr(), self.capacity, self.n,
+                                       self.off.data_ptr(), self.bh.data_ptr(),
+                                       self.n_in.data_ptr(), self.bt, self.n_prefix.data_ptr(),
+                                       self.tier.data_ptr(), self.status.data_ptr(),
+                                       stream_handle(stream))
+
+    def fetch(self) -> dict:
+        torch = _torch()
+        torch.cuda.synchronize(self.device)
+        return {"status": int(self.status.item()),
+                "n_prefix": self.n_prefix.cpu().numpy()[:self.n],
+                "prefix_tier": self.tier.cpu().numpy()[:self.n]}
