@@ -106,6 +106,72 @@ def measure_prefix_probe(cfg, stream, reps=20):
             "blocks_examined_per_s": float(looked.sum()) / (us * 1e-6)}
 
 
+def measure_host_tier(pl, d, st_in, st_out, n_unpack, n_pack, block_bytes, stream,
+                      batch=64, reps=3):
+    """The DRAM tier's side of the step's restores and spills: pinned host
+    blocks (one 2-MiB-class block per move, at shuffled host places) over the
+    host link, pipelined in batches with the on-GPU unpack / pack
+    (cascade_restore_from_host / cascade_spill_to_host), against the link
+    alone and the kernel alone.  Outside the step's timed region."""
+    import torch
+    from paper_2608_06557_amd import cascade, device
+    out = {"batch_moves": batch}
+    copy_s = torch.cuda.Stream()
+    evs, handles = device.event_handles(4, stream)
+    st = torch.zeros(1, dtype=torch.int32, device=stream.device)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rng = np.random.default_rng(0)
+    for name, n, fn, stage, n_ptr, moves in [
+            ("restore", n_unpack, cascade.cascade_restore_from_host, st_in, d.n_unpack_ptr(),
+             d.unpack_moves.data_ptr()),
+            ("spill", n_pack, cascade.cascade_spill_to_host, st_out, d.n_pack_ptr(),
+             d.pack_moves.data_ptr())]:
+        if n == 0:
+            continue
+        host = torch.empty(n * block_bytes, dtype=torch.uint8, pin_memory=True)
+        offs = rng.permutation(n).astype(np.int64) * block_bytes
+
+        def run(bm):
+            e0.record(stream)
+            copy_s.wait_event(e0)
+            rc = fn(pl, stage.data_ptr(), n, host.data_ptr(), offs, moves, n_ptr, n, bm,
+                    st.data_ptr(), copy_s.cuda_stream, stream.cuda_stream, handles)
+            assert rc == 0
+            # a restore ends with an unpack on the compute stream, a spill with
+            # a host copy on the copy stream
+            e1.record(stream if name == "restore" else copy_s)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) * 1e3
+        run(batch)
+        piped = float(np.median([run(batch) for _ in range(reps)]))
+        whole = float(np.median([run(n) for _ in range(reps)]))   # one batch: no overlap
+        # the link alone: the same DMA copies with no kernel
+        def dma_only():
+            with torch.cuda.stream(copy_s):
+                e0.record(copy_s)
+                for m in range(n):
+                    dev_b = stage[m * block_bytes:(m + 1) * block_bytes]
+                    host_b = host[int(offs[m]):int(offs[m]) + block_bytes]
+                    if name == "restore":
+                        dev_b.copy_(host_b, non_blocking=True)
+                    else:
+                        host_b.copy_(dev_b, non_blocking=True)
+                e1.record(copy_s)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) * 1e3
+        dma_only()
+        link = float(np.median([dma_only() for _ in range(reps)]))
+        nbytes = n * block_bytes
+        out[name] = {"blocks": n, "bytes": nbytes, "pipelined_us": piped,
+                     "pipelined_GBps": nbytes / (piped * 1e-6) / 1e9,
+                     "unbatched_us": whole, "link_only_us": link,
+                     "link_only_GBps": nbytes / (link * 1e-6) / 1e9}
+        del host
+    assert int(st.item()) == 0
+    progress("host-tier restore and spill measured")
+    return out
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -124,6 +190,8 @@ def parse():
                     help="approximate CPU time spent on the oracle baseline")
     ap.add_argument("--no-prefix-probe", action="store_true",
                     help="skip the prefix-hit lookup measurement")
+    ap.add_argument("--no-host-tier", action="store_true",
+                    help="skip the DRAM-tier (pinned host) restore/spill measurement")
     ap.add_argument("--calib-copy-gb", type=float, default=0.0,
                     help="also run a plain torch copy of this size (counter calibration)")
     return ap.parse_args()
@@ -322,6 +390,8 @@ def main():
         del a, b
     progress("cold-cache steps and device copy done")
     probe = None if args.no_prefix_probe else measure_prefix_probe(cfg, stream)
+    host_tier = None if args.no_host_tier else measure_host_tier(
+        pl, d, st_in, st_out, n_unpack, n_pack, block_bytes, stream)
     kernel = "kvmove_kernel" if fused else "kvcopy_kernel"
     copies = {"mode": args.copy, "pack_blocks": n_pack, "unpack_blocks": n_unpack,
               "paired_blocks": int((res["unpack_hazard"] >= 0).sum()),
@@ -364,6 +434,8 @@ def main():
     }
     if probe:
         out["prefix_probe"] = probe
+    if host_tier:
+        out["host_tier"] = host_tier
     if extra:
         out["calib_copy"] = extra
     if not args.no_cpu_baseline:

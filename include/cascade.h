@@ -265,6 +265,39 @@ int cascade_pack_unpack(const cascade_kv_pool_t *pool, void *pack_staging,
                         int32_t max_unpack, const int32_t *unpack_hazard, int32_t *status_dev,
                         void *stream);
 
+/* The DRAM tier's side of a restore and of a spill (Section 4.4: HBM is
+   allocated only at the final DRAM->HBM hop, eq:restore_time's DRAM link;
+   preempted prefills are spilled to DRAM).  host_blocks is pinned host memory
+   (hipHostMalloc) owned by the caller; move m's block lives at byte
+   host_offsets[m] of it (host array of n_moves entries, 2*num_layers*
+   chunk_bytes bytes per block, in the staging order of one block), and the
+   moves must use staging slot m for move m, as cascade_step's lists do.
+   cascade_restore_from_host copies each batch of batch_moves blocks host ->
+   staging on copy_stream, records events[k % n_events] there, makes
+   compute_stream wait on it and unpacks the batch on compute_stream, so the
+   host link of batch k+1 overlaps the unpack of batch k.
+   cascade_spill_to_host packs each batch on compute_stream, then copies it
+   staging -> host on copy_stream after an event.  n_moves is the host-known
+   move count (e.g. info[CASCADE_INFO_N_UNPACK] read back); n_moves_dev the
+   step's device count.  streams and events (hipEvent_t) are the caller's;
+   any work before the call on compute_stream (the step) is ordered before
+   the copies, and the caller synchronises copy_stream (spill) or
+   compute_stream (restore) before using the results.  Returns CASCADE_EINVAL
+   for NULL pointers or bad sizes, CASCADE_ENOSPC when n_moves exceeds
+   staging_slots, CASCADE_EHIP when a copy or launch fails. */
+int cascade_restore_from_host(const cascade_kv_pool_t *pool, void *staging,
+                              int32_t staging_slots, const void *host_blocks,
+                              const int64_t *host_offsets, const cascade_move_t *moves_dev,
+                              const int32_t *n_moves_dev, int32_t n_moves, int32_t batch_moves,
+                              int32_t *status_dev, void *copy_stream, void *compute_stream,
+                              void *const *events, int32_t n_events);
+int cascade_spill_to_host(const cascade_kv_pool_t *pool, void *staging, int32_t staging_slots,
+                          void *host_blocks, const int64_t *host_offsets,
+                          const cascade_move_t *moves_dev, const int32_t *n_moves_dev,
+                          int32_t n_moves, int32_t batch_moves, int32_t *status_dev,
+                          void *copy_stream, void *compute_stream, void *const *events,
+                          int32_t n_events);
+
 /* Prefix hit detection (Section 4.4): an index that records, for every
    cached KV block (keyed by its nonzero 64-bit prefix hash), the deepest
    tier holding it (CASCADE_KV_HBM < DRAM < NVME).  A request's matched

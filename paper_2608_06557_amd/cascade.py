@@ -9,6 +9,8 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+import numpy as np
+
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libcascade.so")
 
 OK, EINVAL, ENOSPC, EHIP, ETIMEOUT, EINTERNAL = 0, -1, -2, -3, -4, -5
@@ -22,7 +24,8 @@ INFO_LEN = 8
 
 EXPORTED = ["cascade_step_workspace_bytes", "cascade_step", "cascade_pack", "cascade_unpack",
             "cascade_pack_unpack", "cascade_prefix_index_bytes", "cascade_prefix_index_clear",
-            "cascade_prefix_index_insert", "cascade_prefix_probe", "cascade_strerror"]
+            "cascade_prefix_index_insert", "cascade_prefix_probe", "cascade_restore_from_host",
+            "cascade_spill_to_host", "cascade_strerror"]
 INDEX_SLOT_BYTES = 16
 
 
@@ -117,6 +120,12 @@ def load() -> C.CDLL:
         L.cascade_prefix_probe.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
                                            C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p,
                                            C.c_void_p, C.c_void_p, C.c_void_p]
+        for name in ("cascade_restore_from_host", "cascade_spill_to_host"):
+            f = getattr(L, name)
+            f.restype = C.c_int
+            f.argtypes = [C.POINTER(KvPool), C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                          C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
+                          C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32]
         L.cascade_strerror.restype = C.c_char_p
         L.cascade_strerror.argtypes = [C.c_int]
         _lib = L
@@ -183,6 +192,35 @@ def cascade_prefix_probe(index: int, capacity: int, n: int, block_offsets: int,
                                            v(block_hashes), v(n_in), block_tokens,
                                            v(n_prefix_out), v(prefix_tier_out), v(status_dev),
                                            v(stream)))
+
+
+def _host_tier(fn, pool, staging, staging_slots, host_blocks, host_offsets, moves_dev,
+               n_moves_dev, n_moves, batch_moves, status_dev, copy_stream, compute_stream,
+               events):
+    offs = np.ascontiguousarray(host_offsets, dtype=np.int64)
+    ev = (C.c_void_p * max(len(events), 1))(*[C.c_void_p(e) for e in events])
+    v = C.c_void_p
+    return int(fn(C.byref(pool), v(staging), staging_slots, v(host_blocks),
+                  offs.ctypes.data_as(v), v(moves_dev), v(n_moves_dev), n_moves, batch_moves,
+                  v(status_dev), v(copy_stream), v(compute_stream), ev, len(events)))
+
+
+def cascade_restore_from_host(pool: KvPool, staging: int, staging_slots: int, host_blocks: int,
+                              host_offsets, moves_dev: int, n_moves_dev: int, n_moves: int,
+                              batch_moves: int, status_dev: int, copy_stream: int,
+                              compute_stream: int, events) -> int:
+    return _host_tier(load().cascade_restore_from_host, pool, staging, staging_slots,
+                      host_blocks, host_offsets, moves_dev, n_moves_dev, n_moves, batch_moves,
+                      status_dev, copy_stream, compute_stream, events)
+
+
+def cascade_spill_to_host(pool: KvPool, staging: int, staging_slots: int, host_blocks: int,
+                          host_offsets, moves_dev: int, n_moves_dev: int, n_moves: int,
+                          batch_moves: int, status_dev: int, copy_stream: int,
+                          compute_stream: int, events) -> int:
+    return _host_tier(load().cascade_spill_to_host, pool, staging, staging_slots, host_blocks,
+                      host_offsets, moves_dev, n_moves_dev, n_moves, batch_moves, status_dev,
+                      copy_stream, compute_stream, events)
 
 
 def cascade_strerror(code: int) -> str:

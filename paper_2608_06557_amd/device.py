@@ -198,3 +198,14 @@ class DevicePrefix:
         return {"status": int(self.status.item()),
                 "n_prefix": self.n_prefix.cpu().numpy()[:self.n],
                 "prefix_tier": self.tier.cpu().numpy()[:self.n]}
+
+
+def event_handles(k: int, stream=None) -> list:
+    """k HIP events (torch-owned), recorded once so that each has a handle."""
+    torch = _torch()
+    evs = [torch.cuda.Event() for _ in range(k)]
+    s = stream if stream is not None else torch.cuda.current_stream()
+    for e in evs:
+        e.record(s)
+    torch.cuda.synchronize()
+    return evs, [int(e.cuda_event) for e in evs]
