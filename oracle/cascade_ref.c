@@ -514,3 +514,111 @@ int32_t cref_prefix_probe(int32_t n_entries, const uint64_t *index_hashes,
   free(idx);
   return CREF_OK;
 }
+
+/* ------------------------------------------------ per-tier LRU reclamation */
+
+/* reclamation order of a free slot: empty before cached, then least recent
+   use, then the lower slot */
+typedef struct { int32_t cached; int64_t last_use; int32_t slot; } cref_lru;
+
+static int cmp_lru(const void *a, const void *b) {
+  const cref_lru *x = (const cref_lru *)a, *y = (const cref_lru *)b;
+  if (x->cached != y->cached) return x->cached < y->cached ? -1 : 1;
+  if (x->last_use != y->last_use) return x->last_use < y->last_use ? -1 : 1;
+  return x->slot < y->slot ? -1 : (x->slot > y->slot ? 1 : 0);
+}
+static int cmp_i32(const void *a, const void *b) {
+  const int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+static int cmp_u64(const void *k, const void *e) {
+  const uint64_t x = *(const uint64_t *)k, y = *(const uint64_t *)e;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+int32_t cref_tier_reclaim(int32_t tier, int32_t n_slots, uint64_t *block_hash,
+                          int64_t *last_use_ns, const uint8_t *held, int32_t need,
+                          int32_t n_incoming, const cref_demotion *incoming,
+                          int32_t max_outgoing, cref_demotion *outgoing, int32_t *n_outgoing,
+                          int32_t *freed, int32_t *placed, int32_t n_index,
+                          const uint64_t *index_keys, uint8_t *index_masks) {
+  if (tier < 0 || tier > 2 || n_slots < 0 || need < 0 || n_incoming < 0 || n_index < 0)
+    return CREF_EINVAL;
+  const int64_t total64 = (int64_t)need + n_incoming;
+  if (tier < 2 && max_outgoing < total64) return CREF_EINVAL;
+  for (int32_t s = 0; s < n_slots; s++)
+    if (last_use_ns[s] < 0) return CREF_EINVAL;
+  for (int32_t j = 0; j < n_incoming; j++)
+    if (incoming[j].hash == 0) return CREF_EINVAL;
+  for (int32_t e = 0; e < n_index; e++)
+    if (index_keys[e] == 0 || index_masks[e] > 7 || (e > 0 && index_keys[e] <= index_keys[e - 1]))
+      return CREF_EINVAL;
+
+  /* the free slots in reclamation order */
+  cref_lru *cand = (cref_lru *)malloc(sizeof(cref_lru) * (size_t)(n_slots ? n_slots : 1));
+  int32_t n_free = 0;
+  for (int32_t s = 0; s < n_slots; s++) {
+    if (held[s]) continue;
+    cand[n_free].cached = block_hash[s] != 0;
+    cand[n_free].last_use = block_hash[s] != 0 ? last_use_ns[s] : 0;
+    cand[n_free].slot = s;
+    n_free++;
+  }
+  if (total64 > n_free) { free(cand); return CREF_ENOSPC; }
+  const int32_t total = (int32_t)total64;
+  qsort(cand, (size_t)n_free, sizeof(cref_lru), cmp_lru);
+
+  /* the `total` first, listed by slot */
+  int32_t *rec = (int32_t *)malloc(sizeof(int32_t) * (size_t)(total ? total : 1));
+  for (int32_t i = 0; i < total; i++) rec[i] = cand[i].slot;
+  qsort(rec, (size_t)total, sizeof(int32_t), cmp_i32);
+
+  /* demotion decisions on the index as it was when the call began */
+  uint8_t *demote = (uint8_t *)calloc((size_t)(total ? total : 1), 1);
+  int32_t n_out = 0;
+  for (int32_t i = 0; i < total; i++) {
+    const int32_t s = rec[i];
+    if (block_hash[s] == 0 || tier == 2) continue;
+    const uint64_t *hit = n_index ? (const uint64_t *)bsearch(&block_hash[s], index_keys,
+                                                              (size_t)n_index, sizeof(uint64_t),
+                                                              cmp_u64)
+                                  : NULL;
+    const uint8_t mask = hit ? index_masks[hit - index_keys] : 0;
+    if ((mask >> (tier + 1)) == 0) {
+      demote[i] = 1;
+      outgoing[n_out].hash = block_hash[s];
+      outgoing[n_out].last_use_ns = last_use_ns[s];
+      outgoing[n_out].src_slot = s;
+      outgoing[n_out].pad = 0;
+      n_out++;
+    }
+  }
+  /* index updates: the tier loses every reclaimed block, the next tier
+     gains the demoted ones */
+  for (int32_t i = 0; i < total; i++) {
+    const int32_t s = rec[i];
+    if (block_hash[s] == 0 || n_index == 0) continue;
+    const uint64_t *hit = (const uint64_t *)bsearch(&block_hash[s], index_keys, (size_t)n_index,
+                                                    sizeof(uint64_t), cmp_u64);
+    if (!hit) continue;
+    uint8_t *m = &index_masks[hit - index_keys];
+    *m = (uint8_t)(*m & ~(1u << tier));
+    if (demote[i]) *m = (uint8_t)(*m | (1u << (tier + 1)));
+  }
+  /* slot table: the caller's slots empty, the rest take the incoming blocks */
+  for (int32_t i = 0; i < total; i++) {
+    const int32_t s = rec[i];
+    if (i < need) {
+      freed[i] = s;
+      block_hash[s] = 0;
+      last_use_ns[s] = 0;
+    } else {
+      placed[i - need] = s;
+      block_hash[s] = incoming[i - need].hash;
+      last_use_ns[s] = incoming[i - need].last_use_ns;
+    }
+  }
+  *n_outgoing = n_out;
+  free(demote); free(rec); free(cand);
+  return CREF_OK;
+}

@@ -137,6 +137,41 @@ int32_t cref_prefix_probe(int32_t n_entries, const uint64_t *index_hashes,
                           int32_t block_tokens, int32_t *n_prefix_out,
                           uint8_t *prefix_tier_out);
 
+/* Per-tier LRU reclamation (Section 4.4, prefix hit detection: free blocks
+   are reclaimed least-recently-used within each tier, hot prefixes stay in
+   the fast tiers and cold ones spill one tier deeper).  One call reclaims
+   need + n_incoming slots of one tier (0 HBM, 1 DRAM, 2 NVMe):
+     - candidates are the slots with held[s] == 0; empty slots (hash 0)
+       come first, then cached blocks by ascending last use, ties by the
+       lower slot;
+     - the reclaimed set, listed by ascending slot, gives the caller its
+       first `need` slots (freed) and places incoming[j] (blocks demoted
+       from the tier above) into the rest (placed[j]);
+     - a reclaimed cached block of tier 0 or 1 that no deeper tier holds
+       (index mask bits above `tier` clear, judged on the index as it was
+       when the call began; a hash missing from the index counts as held
+       nowhere deeper) is demoted: appended to outgoing in slot order;
+       tier 2 drops its reclaimed blocks;
+     - the index (n_index entries, keys ascending and nonzero, mask bit k =
+       tier k holds the block) loses bit `tier` for every reclaimed cached
+       block and gains bit tier+1 for every demoted one; hashes missing
+       from it are skipped;
+     - freed slots become empty (hash 0, last use 0); placed slots take
+       their incoming block's hash and last use.
+   Returns CREF_EINVAL for a tier outside 0..2, negative counts, a negative
+   last use, an incoming hash 0, index keys not strictly ascending or a
+   mask above 7, or max_outgoing < need + n_incoming on tiers 0 and 1;
+   CREF_ENOSPC when fewer than need + n_incoming slots are free.  Nothing is
+   written on error. */
+typedef struct { uint64_t hash; int64_t last_use_ns; int32_t src_slot, pad; } cref_demotion;
+
+int32_t cref_tier_reclaim(int32_t tier, int32_t n_slots, uint64_t *block_hash,
+                          int64_t *last_use_ns, const uint8_t *held, int32_t need,
+                          int32_t n_incoming, const cref_demotion *incoming,
+                          int32_t max_outgoing, cref_demotion *outgoing, int32_t *n_outgoing,
+                          int32_t *freed, int32_t *placed, int32_t n_index,
+                          const uint64_t *index_keys, uint8_t *index_masks);
+
 void cref_pack(const cref_pool *pool, uint8_t *staging, const cref_move *moves, int32_t n);
 void cref_unpack(const cref_pool *pool, const uint8_t *staging, const cref_move *moves, int32_t n);
 

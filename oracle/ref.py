@@ -115,6 +115,11 @@ def lib():
         L.cref_prefix_probe.argtypes = [C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
                                         C.c_void_p, C.c_void_p]
+        L.cref_tier_reclaim.restype = C.c_int32
+        L.cref_tier_reclaim.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
+                                        C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
+                                        C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                        C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
         _lib = L
     return _lib
 
@@ -265,3 +270,45 @@ def prefix_probe(index_hashes: np.ndarray, index_tiers: np.ndarray, block_offset
     rc = lib().cref_prefix_probe(len(ih), ptr[0], ptr[1], n, ptr[2], ptr[3], ptr[4],
                                  int(block_tokens), _ptr(npre), _ptr(tier))
     return {"rc": rc, "n_prefix": npre[:n], "prefix_tier": tier[:n]}
+
+
+# one block demoted to the next tier: its hash, last use and source slot
+DEMOTION_DTYPE = np.dtype([("hash", np.uint64), ("last_use_ns", np.int64),
+                           ("src_slot", np.int32), ("pad", np.int32)])
+
+
+def tier_reclaim(tier: int, block_hash: np.ndarray, last_use_ns: np.ndarray, held: np.ndarray,
+                 need: int, incoming: np.ndarray | None = None, max_outgoing: int | None = None,
+                 index_keys: np.ndarray | None = None, index_masks: np.ndarray | None = None
+                 ) -> dict:
+    """One tier's LRU reclamation (Section 4.4: free blocks reclaimed least
+    recently used within each tier, cold ones spilled one tier deeper), from
+    the oracle.  Inputs are not modified: the updated slot table and index
+    come back as copies."""
+    bh = np.array(block_hash, dtype=np.uint64, copy=True)
+    lu = np.array(last_use_ns, dtype=np.int64, copy=True)
+    hd = np.ascontiguousarray(held, dtype=np.uint8)
+    inc = (np.zeros(0, DEMOTION_DTYPE) if incoming is None
+           else np.ascontiguousarray(incoming, dtype=DEMOTION_DTYPE))
+    n_inc = len(inc)
+    if max_outgoing is None:
+        max_outgoing = int(need) + n_inc
+    keys = (np.zeros(0, np.uint64) if index_keys is None
+            else np.ascontiguousarray(index_keys, dtype=np.uint64))
+    masks = (np.zeros(0, np.uint8) if index_masks is None
+             else np.array(index_masks, dtype=np.uint8, copy=True))
+    n_tot = max(int(need) + n_inc, 0)
+    out = np.zeros(max(int(max_outgoing), 1), DEMOTION_DTYPE)
+    freed = np.zeros(max(int(need), 1), np.int32)
+    placed = np.zeros(max(n_inc, 1), np.int32)
+    n_out = np.zeros(1, np.int32)
+    keep = [bh, lu, hd, inc, keys, masks]
+    ptr = [_ptr(a if a.size else np.zeros(1, a.dtype)) for a in keep]
+    rc = lib().cref_tier_reclaim(int(tier), len(bh), ptr[0], ptr[1], ptr[2], int(need), n_inc,
+                                 ptr[3], int(max_outgoing), _ptr(out), _ptr(n_out), _ptr(freed),
+                                 _ptr(placed), len(keys), ptr[4], ptr[5])
+    no = int(n_out[0]) if rc == OK else 0
+    return {"rc": rc, "freed": freed[:max(int(need), 0)] if rc == OK else freed[:0],
+            "placed": placed[:n_inc] if rc == OK else placed[:0], "outgoing": out[:no],
+            "n_outgoing": no, "block_hash": bh, "last_use_ns": lu, "index_keys": keys,
+            "index_masks": masks, "n_reclaimed": n_tot if rc == OK else 0}
