@@ -299,21 +299,23 @@ int cascade_spill_to_host(const cascade_kv_pool_t *pool, void *staging, int32_t 
                           int32_t n_events);
 
 /* Prefix hit detection (Section 4.4): an index that records, for every
-   cached KV block (keyed by its nonzero 64-bit prefix hash), the deepest
-   tier holding it (CASCADE_KV_HBM < DRAM < NVME).  A request's matched
-   prefix is the longest run of its leading prompt blocks that are all in the
-   index, capped at floor((n_in - 1) / block_tokens) blocks so that at least
-   one prompt token is computed; its tier is the deepest over that run.  The
-   results are the n_prefix / prefix_tier inputs of cascade_step.
+   cached KV block (keyed by its nonzero 64-bit prefix hash), the set of
+   tiers holding it; the lookup reads its deepest tier (CASCADE_KV_HBM <
+   DRAM < NVME), and a block whose set has become empty (every copy
+   reclaimed, cascade_tier_reclaim) counts as not cached.  A request's
+   matched prefix is the longest run of its leading prompt blocks that are
+   all cached, capped at floor((n_in - 1) / block_tokens) blocks so that at
+   least one prompt token is computed; its tier is the deepest over that run.
+   The results are the n_prefix / prefix_tier inputs of cascade_step.
 
    The index is caller-owned device memory of cascade_prefix_index_bytes()
    bytes (16-byte aligned), an open-addressing table of `capacity` slots
    (a power of two in [64, 2^30]; keep it at least twice the number of
    distinct cached blocks).  cascade_prefix_index_clear empties it (a fill
    kernel, so it may be captured in a graph).  cascade_prefix_index_insert
-   adds n (hash, tier) facts; a block inserted several times keeps its
-   deepest tier; inserts may run concurrently with each other but not with
-   a probe.  Hash 0 or a tier above CASCADE_KV_NVME sets *status_dev =
+   adds n (hash, tier) facts, each adding the tier to the block's set;
+   inserts may run concurrently with each other but not with a probe or a
+   reclamation.  Hash 0 or a tier above CASCADE_KV_NVME sets *status_dev =
    CASCADE_EINVAL and is skipped; a full table sets CASCADE_ENOSPC.
    cascade_prefix_probe looks up request i's block hashes
    block_hashes[block_offsets[i] .. block_offsets[i+1]) (device CSR, offsets
@@ -333,6 +335,78 @@ int cascade_prefix_probe(const void *index, int32_t capacity, int32_t n,
                          const int32_t *block_offsets, const uint64_t *block_hashes,
                          const int32_t *n_in, int32_t block_tokens, int32_t *n_prefix_out,
                          uint8_t *prefix_tier_out, int32_t *status_dev, void *stream);
+
+/* Per-tier LRU reclamation (Section 4.4, prefix hit detection: free blocks
+   are reclaimed least-recently-used within each tier, so hot prefixes stay
+   in the fast tiers and cold ones spill deeper).  One call frees
+   need + n_incoming slots of one tier (0 HBM, 1 DRAM, 2 NVMe), all device
+   memory:
+     - candidates are the slots with held[s] == 0: empty slots (hash 0)
+       first, then cached blocks by ascending last_use_ns, ties by the lower
+       slot; the first need + n_incoming are reclaimed;
+     - the reclaimed slots in ascending order give the caller freed[0 ..
+       need) and receive incoming[j] (blocks the tier above demoted) in
+       placed[j], j < n_incoming;
+     - a reclaimed cached block of tier 0 or 1 is demoted, appended to
+       outgoing in slot order, unless the index (as it was when the call
+       began) has it in a deeper tier; a hash absent from the index, or no
+       index, counts as held nowhere deeper.  Tier 2 drops what it reclaims.
+       The caller copies each demoted block from slot src_slot of this tier
+       before anything is written into that slot (for the HBM tier:
+       cascade_pack / cascade_spill_to_host before the step's restores);
+     - the index loses this tier for every reclaimed cached block and gains
+       tier + 1 for every demoted one (hashes absent from it are skipped);
+     - the slot table is updated in place: freed slots become empty (hash 0,
+       last use 0), placed slots take their block's hash and last use.
+   A chain HBM -> DRAM -> NVMe passes each call's outgoing / n_outgoing_dev
+   as the next call's incoming / n_incoming_dev, with one status word.
+   Hashes are assumed unique within a tier (one copy of a block per tier).
+
+   table        the tier's slot table (n_slots in [0, 2^30]).
+   need         slots for the caller (>= 0).
+   incoming     blocks demoted into this tier, *n_incoming_dev of them
+                (<= max_incoming); NULL with max_incoming 0 for none.
+   outgoing     demoted blocks; max_outgoing >= need + max_incoming on tiers
+                0 and 1; *n_outgoing_dev receives their count (tier 2: 0,
+                outgoing may be NULL).
+   freed        device int32[need]; placed device int32[max_incoming].
+   index        the prefix index (NULL = none) and its capacity.
+   workspace    device memory of cascade_reclaim_workspace_bytes(n_slots)
+                bytes, 256-byte aligned, zero-filled once before its first
+                use; every call leaves it that way.  One call at a time per
+                workspace.
+   status_dev   device int32, cleared by the caller before the first call of
+                a chain.  A call that finds it nonzero does nothing.  A call
+                sets CASCADE_EINVAL for a negative last use, an incoming
+                hash 0 or *n_incoming_dev outside [0, max_incoming], and
+                CASCADE_ENOSPC when fewer than need + n_incoming slots are
+                free; then it writes nothing else.  CASCADE_ETIMEOUT or
+                CASCADE_EINTERNAL report a failed cross-workgroup wait or
+                consistency check.
+   Alignment: block_hash and last_use_ns 16 bytes, held 8 bytes.
+   Returns CASCADE_EINVAL for bad host arguments, CASCADE_EHIP on a failed
+   launch.  Asynchronous on `stream`. */
+typedef struct {
+  int32_t n_slots;
+  uint64_t *block_hash;   /* [n_slots] block in the slot, 0 = empty */
+  int64_t *last_use_ns;   /* [n_slots] last access, >= 0 */
+  const uint8_t *held;    /* [n_slots] nonzero = in use, never reclaimed */
+} cascade_tier_table_t;
+
+/* one demoted block: its hash, last use, and slot in the tier it leaves */
+typedef struct {
+  uint64_t hash;
+  int64_t last_use_ns;
+  int32_t src_slot, pad;
+} cascade_demotion_t;
+
+size_t cascade_reclaim_workspace_bytes(int32_t n_slots);
+int cascade_tier_reclaim(int32_t tier, const cascade_tier_table_t *table, int32_t need,
+                         const cascade_demotion_t *incoming, const int32_t *n_incoming_dev,
+                         int32_t max_incoming, cascade_demotion_t *outgoing,
+                         int32_t *n_outgoing_dev, int32_t max_outgoing, int32_t *freed,
+                         int32_t *placed, void *index, int32_t index_capacity, void *workspace,
+                         size_t workspace_bytes, int32_t *status_dev, void *stream);
 
 /* Short English text for a return code or status value. */
 const char *cascade_strerror(int code);

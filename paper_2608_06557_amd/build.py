@@ -10,7 +10,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libcascade.so")
-SOURCES = ["cascade_step.hip", "cascade_kvcopy.hip", "cascade_prefix.hip",
+SOURCES = ["cascade_step.hip", "cascade_kvcopy.hip", "cascade_prefix.hip", "cascade_reclaim.hip",
            "cascade_hosttier.hip"]
 ARCH = "gfx950"
 

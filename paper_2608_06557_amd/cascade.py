@@ -25,8 +25,19 @@ INFO_LEN = 8
 EXPORTED = ["cascade_step_workspace_bytes", "cascade_step", "cascade_pack", "cascade_unpack",
             "cascade_pack_unpack", "cascade_prefix_index_bytes", "cascade_prefix_index_clear",
             "cascade_prefix_index_insert", "cascade_prefix_probe", "cascade_restore_from_host",
-            "cascade_spill_to_host", "cascade_strerror"]
+            "cascade_spill_to_host", "cascade_reclaim_workspace_bytes", "cascade_tier_reclaim",
+            "cascade_strerror"]
 INDEX_SLOT_BYTES = 16
+
+
+class TierTable(C.Structure):
+    _fields_ = [("n_slots", C.c_int32), ("block_hash", C.c_void_p), ("last_use_ns", C.c_void_p),
+                ("held", C.c_void_p)]
+
+
+# cascade_demotion_t: hash, last use, source slot (24 bytes)
+DEMOTION_DTYPE = np.dtype([("hash", np.uint64), ("last_use_ns", np.int64),
+                           ("src_slot", np.int32), ("pad", np.int32)])
 
 
 class Requests(C.Structure):
@@ -126,6 +137,14 @@ def load() -> C.CDLL:
             f.argtypes = [C.POINTER(KvPool), C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
                           C.c_void_p, C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
                           C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32]
+        L.cascade_reclaim_workspace_bytes.restype = C.c_size_t
+        L.cascade_reclaim_workspace_bytes.argtypes = [C.c_int32]
+        L.cascade_tier_reclaim.restype = C.c_int
+        L.cascade_tier_reclaim.argtypes = [C.c_int32, C.POINTER(TierTable), C.c_int32,
+                                           C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p,
+                                           C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
+                                           C.c_void_p, C.c_int32, C.c_void_p, C.c_size_t,
+                                           C.c_void_p, C.c_void_p]
         L.cascade_strerror.restype = C.c_char_p
         L.cascade_strerror.argtypes = [C.c_int]
         _lib = L
@@ -221,6 +240,22 @@ def cascade_spill_to_host(pool: KvPool, staging: int, staging_slots: int, host_b
     return _host_tier(load().cascade_spill_to_host, pool, staging, staging_slots, host_blocks,
                       host_offsets, moves_dev, n_moves_dev, n_moves, batch_moves, status_dev,
                       copy_stream, compute_stream, events)
+
+
+def cascade_reclaim_workspace_bytes(n_slots: int) -> int:
+    return int(load().cascade_reclaim_workspace_bytes(n_slots))
+
+
+def cascade_tier_reclaim(tier: int, table: TierTable, need: int, incoming: int,
+                         n_incoming_dev: int, max_incoming: int, outgoing: int,
+                         n_outgoing_dev: int, max_outgoing: int, freed: int, placed: int,
+                         index: int, index_capacity: int, workspace: int, workspace_bytes: int,
+                         status_dev: int, stream: int) -> int:
+    v = C.c_void_p
+    return int(load().cascade_tier_reclaim(
+        tier, C.byref(table), need, v(incoming), v(n_incoming_dev), max_incoming, v(outgoing),
+        v(n_outgoing_dev), max_outgoing, v(freed), v(placed), v(index), index_capacity,
+        v(workspace), workspace_bytes, v(status_dev), v(stream)))
 
 
 def cascade_strerror(code: int) -> str:

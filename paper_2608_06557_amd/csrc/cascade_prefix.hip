@@ -2,17 +2,20 @@
 // detection).
 //
 // On top of per-block prefix hashing, an index records for every cached KV
-// block the deepest tier holding it.  A request's prefix-hit profile is the
-// longest run of its leading blocks present in the index (capped so that at
-// least one prompt token is computed) and the deepest tier over that run:
-// the n_prefix / prefix_tier inputs of the scheduling step.
+// block the tiers holding it, of which the lookup reads the deepest (per-tier
+// reclamation removes a tier's copy: cascade_reclaim.hip).  A request's
+// prefix-hit profile is the longest run of its leading blocks present in the
+// index (capped so that at least one prompt token is computed) and the
+// deepest tier over that run: the n_prefix / prefix_tier inputs of the
+// scheduling step.
 //
-// The index is an open-addressing hash table of 16-byte slots (key, tier) in
-// device memory, linear probing from the murmur3 64-bit finalizer of the
-// key; key 0 marks an empty slot.  Insert claims a slot with a 64-bit CAS
-// and keeps the deepest tier with atomicMax.  The probe gives each request
-// one wave: 64 leading blocks are looked up at once, a ballot finds the first
-// miss, and the wave stops there, so blocks past a miss cost nothing.
+// The index is an open-addressing hash table of 16-byte slots (key, set of
+// tiers holding the block) in device memory (index_table.h); key 0 marks an
+// empty slot.  Insert claims a slot with a 64-bit CAS and adds the tier to the
+// set with atomicOr; the block's deepest tier is the highest tier in its set.
+// The probe gives each request one wave: 64 leading blocks are looked up at
+// once, a ballot finds the first miss (a block absent, or whose set is empty),
+// and the wave stops there, so blocks past a miss cost nothing.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -20,26 +23,10 @@
 
 #include "cascade.h"
 #include "device_util.h"
+#include "index_table.h"
 
 namespace cascade {
 namespace {
-
-struct alignas(16) IndexSlot {
-  unsigned long long key;  // block hash, 0 = empty
-  unsigned tier;           // deepest tier holding the block
-  unsigned pad;
-};
-static_assert(sizeof(IndexSlot) == CASCADE_INDEX_SLOT_BYTES, "slot layout");
-
-// murmur3's 64-bit finalizer (Appleby), the home slot of a key
-__device__ __forceinline__ unsigned long long fmix64(unsigned long long k) {
-  k ^= k >> 33;
-  k *= 0xff51afd7ed558ccdull;
-  k ^= k >> 33;
-  k *= 0xc4ceb9fe1a85ec53ull;
-  k ^= k >> 33;
-  return k;
-}
 
 __global__ __launch_bounds__(kBlock) void index_clear_kernel(uint4 *slots, long long n_vec) {
   for (long long j = (long long)blockIdx.x * kBlock + threadIdx.x; j < n_vec;
@@ -63,7 +50,7 @@ __global__ __launch_bounds__(kBlock) void index_insert_kernel(IndexSlot *slots, 
   for (unsigned p = 0; p <= mask; ++p, s = (s + 1) & mask) {
     const unsigned long long cur = atomicCAS(&slots[s].key, 0ull, h);
     if (cur == 0ull || cur == h) {
-      atomicMax(&slots[s].tier, t);
+      atomicOr(&slots[s].tiers, 1u << t);
       return;
     }
   }
@@ -104,8 +91,8 @@ __global__ __launch_bounds__(kBlock) void probe_kernel(const IndexSlot *__restri
         for (unsigned p = 0; p <= mask; ++p, s = (s + 1) & mask) {
           const IndexSlot e = slots[s];
           if (e.key == h) {
-            hit = true;
-            t = e.tier;
+            hit = e.tiers != 0u;
+            t = hit ? 31u - (unsigned)__builtin_clz(e.tiers) : 0u;
             break;
           }
           if (e.key == 0ull) break;

@@ -209,3 +209,116 @@ def event_handles(k: int, stream=None) -> list:
         e.record(s)
     torch.cuda.synchronize()
     return evs, [int(e.cuda_event) for e in evs]
+
+
+def index_facts(keys: np.ndarray, masks: np.ndarray):
+    """(hash, tier) facts whose insertion gives each key its tier set."""
+    keys = np.asarray(keys, np.uint64)
+    masks = np.asarray(masks, np.uint8)
+    hs, ts = [], []
+    for t in range(3):
+        sel = (masks >> t) & 1 == 1
+        hs.append(keys[sel])
+        ts.append(np.full(int(sel.sum()), t, np.uint8))
+    return np.concatenate(hs), np.concatenate(ts)
+
+
+def index_contents(index_bytes: np.ndarray):
+    """Keys (ascending) and tier sets of the occupied slots of a device index
+    read back."""
+    slots = np.frombuffer(index_bytes.tobytes(), dtype=np.dtype(
+        [("key", np.uint64), ("tiers", np.uint32), ("pad", np.uint32)]))
+    occ = slots[slots["key"] != 0]
+    order = np.argsort(occ["key"], kind="stable")
+    return occ["key"][order], occ["tiers"][order]
+
+
+class DeviceTiers:
+    """Slot tables of the three tiers (HBM, DRAM, NVMe), the prefix index and
+    the buffers of one reclamation chain HBM -> DRAM -> NVMe: each tier's
+    demoted blocks are the next tier's incoming ones, one status word."""
+
+    def __init__(self, tables: list, needs, index_keys=None, index_masks=None,
+                 device="cuda:0", capacity: int | None = None):
+        torch = _torch()
+        self.device = torch.device(device)
+        self.n = [int(len(t["block_hash"])) for t in tables]
+        self.needs = [int(x) for x in needs]
+        self.bh = [to_device(np.asarray(t["block_hash"], np.uint64), self.device)
+                   for t in tables]
+        self.lu = [to_device(np.asarray(t["last_use_ns"], np.int64), self.device)
+                   for t in tables]
+        self.held = [to_device(np.asarray(t["held"], np.uint8), self.device) for t in tables]
+        self.tabs = [cx.TierTable(self.n[t], self.bh[t].data_ptr(), self.lu[t].data_ptr(),
+                                  self.held[t].data_ptr()) for t in range(3)]
+        # tier t takes at most the previous tier's outgoing capacity
+        self.max_in = [0, 0, 0]
+        self.max_out = [0, 0, 0]
+        for t in range(3):
+            self.max_in[t] = self.max_out[t - 1] if t > 0 else 0
+            self.max_out[t] = self.needs[t] + self.max_in[t] if t < 2 else 0
+        self.out = [torch.zeros(max(self.max_out[t], 1) * cx.DEMOTION_DTYPE.itemsize,
+                                dtype=torch.uint8, device=self.device) for t in range(3)]
+        self.n_out = torch.zeros(3, dtype=torch.int32, device=self.device)
+        self.freed = [torch.full((max(self.needs[t], 1),), -1, dtype=torch.int32,
+                                 device=self.device) for t in range(3)]
+        self.placed = [torch.full((max(self.max_in[t], 1),), -1, dtype=torch.int32,
+                                  device=self.device) for t in range(3)]
+        self.ws_bytes = max(cx.cascade_reclaim_workspace_bytes(n) for n in self.n)
+        self.ws = torch.zeros(self.ws_bytes, dtype=torch.uint8, device=self.device)
+        self.status = torch.zeros(1, dtype=torch.int32, device=self.device)
+        self.index = None
+        self.capacity = 0
+        if index_keys is not None:
+            hs, ts = index_facts(index_keys, index_masks)
+            self.capacity = capacity or index_capacity(len(index_keys))
+            self.index = torch.empty(cx.cascade_prefix_index_bytes(self.capacity),
+                                     dtype=torch.uint8, device=self.device)
+            s = stream_handle()
+            rc = cx.cascade_prefix_index_clear(self.index.data_ptr(), self.capacity, s)
+            ih = to_device(hs, self.device)
+            it = to_device(ts, self.device, np.uint8)
+            rc = rc or cx.cascade_prefix_index_insert(self.index.data_ptr(), self.capacity,
+                                                      ih.data_ptr(), it.data_ptr(), len(hs),
+                                                      self.status.data_ptr(), s)
+            assert rc == 0, rc
+            torch.cuda.synchronize(self.device)
+            assert int(self.status.item()) == 0
+
+    def call(self, t: int, stream=None) -> int:
+        """Enqueue tier t's reclamation (its incoming = tier t-1's outgoing)."""
+        v = self
+        inc = v.out[t - 1].data_ptr() if t > 0 else 0
+        n_inc = v.n_out[t - 1:t].data_ptr() if t > 0 else 0
+        return cx.cascade_tier_reclaim(
+            t, v.tabs[t], v.needs[t], inc, n_inc, v.max_in[t],
+            v.out[t].data_ptr() if t < 2 else 0, v.n_out[t:t + 1].data_ptr(), v.max_out[t],
+            v.freed[t].data_ptr(), v.placed[t].data_ptr(),
+            v.index.data_ptr() if v.index is not None else 0, v.capacity, v.ws.data_ptr(),
+            v.ws_bytes, v.status.data_ptr(), stream_handle(stream))
+
+    def run(self, stream=None, tiers=(0, 1, 2)) -> int:
+        for t in tiers:
+            rc = self.call(t, stream)
+            if rc:
+                return rc
+        return 0
+
+    def fetch(self) -> dict:
+        torch = _torch()
+        torch.cuda.synchronize(self.device)
+        n_out = self.n_out.cpu().numpy()
+        res = {"status": int(self.status.item()), "tiers": []}
+        for t in range(3):
+            n_in = int(n_out[t - 1]) if t > 0 else 0
+            no = int(n_out[t]) if t < 2 else 0
+            out = np.frombuffer(self.out[t].cpu().numpy().tobytes(), cx.DEMOTION_DTYPE)[:no]
+            res["tiers"].append({
+                "freed": self.freed[t].cpu().numpy()[:self.needs[t]],
+                "placed": self.placed[t].cpu().numpy()[:n_in],
+                "outgoing": out, "n_outgoing": no,
+                "block_hash": self.bh[t].cpu().numpy().view(np.uint64)[:self.n[t]],
+                "last_use_ns": self.lu[t].cpu().numpy()[:self.n[t]]})
+        if self.index is not None:
+            res["index"] = index_contents(self.index.cpu().numpy())
+        return res

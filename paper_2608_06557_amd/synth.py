@@ -369,3 +369,81 @@ def make_prefix_workload(cfg: int, seed: int | None = None, n: int | None = None
     return {"n_in": w["n_in"].astype(np.int32), "block_offsets": offsets.astype(np.int32),
             "block_hashes": hashes, "index_hashes": ih[order], "index_tiers": it[order],
             "block_tokens": bt, "expect_blocks": pre_blocks, "expect_tier": tier}
+
+
+# Capacities of the deeper tiers, in KV blocks: 1 TiB of host DRAM and 8 TiB
+# of NVMe per instance, of the model's block size.
+TIER_BYTES = (None, 1 << 40, 8 << 40)
+
+
+def tier_sizes(cfg: int) -> tuple[int, int, int]:
+    p = make_params(cfg)
+    bb = block_bytes(CONFIGS[cfg]["model"])
+    return int(p["num_blocks"]), TIER_BYTES[1] // bb, TIER_BYTES[2] // bb
+
+
+def make_tier_workload(cfg: int = 2, seed: int | None = None, sizes=None, needs=None,
+                       held=(0.6, 0.05, 0.01), empty=(0.002, 0.001, 0.0002),
+                       overlap=(0.3, 0.2), index_frac: float = 1.0,
+                       stamp_scale_s=(30.0, 600.0, 3600.0)) -> dict:
+    """Slot tables of HBM, DRAM and NVMe for one reclamation chain.
+
+    Every tier holds distinct block hashes; a share `overlap[k]` of tier k's
+    blocks also sits one tier deeper (copies kept after a restore).  A share
+    `held[k]` of the slots is in use and `empty[k]` holds nothing (near full:
+    in steady state every tier reclaims cached blocks).  Last uses
+    are nanosecond stamps before t_now, exponentially spread with a mean of
+    stamp_scale_s[k] seconds for HBM and DRAM (recent blocks sit high) and
+    uniform over that many seconds for NVMe.  The index holds the tier set of
+    a share `index_frac` of the blocks.  Default needs are what one step can
+    take: HBM the token cap's blocks plus the restore cap, DRAM the restore
+    cap (spills of preempted prefills), NVMe nothing beyond the demotions;
+    both at most half of HBM's free slots."""
+    cfg_seed = (6007 + cfg) if seed is None else seed
+    rng = np.random.Generator(np.random.PCG64(cfg_seed + 7001))
+    p = make_params(cfg)
+    if sizes is None:
+        sizes = tier_sizes(cfg)
+    sizes = [int(x) for x in sizes]
+    if needs is None:
+        u = min(int(p["max_move_blocks"]), sizes[0])
+        # at most half of HBM's free slots (a small pool is mostly held)
+        room = int(sizes[0] * (1.0 - held[0]) / 2)
+        needs = (min(int(p["token_cap"]) // int(p["block_tokens"]) + u, room), min(u, room), 0)
+    t_now = np.int64(1_700_000_000_000_000_000)
+    ids = []
+    next_id = 1
+    for k, n in enumerate(sizes):
+        n_copy = int(round(overlap[k - 1] * len(ids[k - 1]))) if k > 0 else 0
+        n_copy = min(n_copy, n)
+        copy = rng.choice(ids[k - 1], n_copy, replace=False) if n_copy else np.zeros(0, np.int64)
+        fresh = np.arange(next_id, next_id + (n - n_copy), dtype=np.int64)
+        next_id += n - n_copy
+        ids.append(rng.permutation(np.concatenate([copy, fresh])))
+    tables = []
+    for k, n in enumerate(sizes):
+        bh = block_hash64(ids[k], np.zeros(n, np.int64), cfg_seed + 11)
+        bh[rng.random(n) < empty[k]] = 0
+        # one copy of a block per tier, even if two ids hashed alike
+        _, first = np.unique(bh, return_index=True)
+        dup = np.ones(n, bool)
+        dup[first] = False
+        bh[dup] = 0
+        scale = stamp_scale_s[k] * 1e9
+        age = rng.exponential(scale, n) if k < 2 else rng.uniform(0, scale, n)
+        lu = (t_now - age.astype(np.int64)).astype(np.int64)
+        lu[bh == 0] = rng.integers(0, 1 << 40, int((bh == 0).sum()))  # ignored for empty slots
+        hd = (rng.random(n) < held[k]).astype(np.uint8)
+        tables.append({"block_hash": bh, "last_use_ns": lu, "held": hd})
+    # tier sets: each hash sits at most once per tier, so summing bits is OR
+    hs = np.concatenate([t["block_hash"][t["block_hash"] != 0] for t in tables])
+    bits = np.concatenate([np.full(int((t["block_hash"] != 0).sum()), 1 << k, np.uint8)
+                           for k, t in enumerate(tables)])
+    keys, inv = np.unique(hs, return_inverse=True)
+    masks = np.zeros(len(keys), np.uint8)
+    np.add.at(masks, inv, bits)
+    if index_frac < 1.0:
+        keep = rng.random(len(keys)) < index_frac
+        keys, masks = keys[keep], masks[keep]
+    return {"tables": tables, "index_keys": keys.astype(np.uint64), "index_masks": masks,
+            "needs": tuple(int(x) for x in needs), "sizes": tuple(sizes)}

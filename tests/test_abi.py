@@ -43,8 +43,24 @@ STRUCTS = {
     "cascade_requests_t": cascade.Requests, "cascade_block_table_t": cascade.BlockTable,
     "cascade_tier_state_t": cascade.TierState, "cascade_params_t": cascade.Params,
     "cascade_move_t": cascade.Move, "cascade_outputs_t": cascade.Outputs,
-    "cascade_kv_pool_t": cascade.KvPool,
+    "cascade_kv_pool_t": cascade.KvPool, "cascade_tier_table_t": cascade.TierTable,
 }
+
+
+def test_demotion_record_layout_matches_header(tmp_path):
+    dt = cascade.DEMOTION_DTYPE
+    src = tmp_path / "dem.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "cascade.h"\n'
+                   'int main(){printf("%zu %zu %zu %zu %zu\\n", sizeof(cascade_demotion_t),'
+                   'offsetof(cascade_demotion_t, hash), offsetof(cascade_demotion_t, last_use_ns),'
+                   'offsetof(cascade_demotion_t, src_slot), offsetof(cascade_demotion_t, pad));'
+                   'return 0;}')
+    exe = tmp_path / "dem"
+    subprocess.run(["gcc", "-I", os.path.dirname(HEADER), str(src), "-o", str(exe)], check=True)
+    got = [int(x) for x in subprocess.run([str(exe)], check=True, capture_output=True,
+                                          text=True).stdout.split()]
+    assert got == [dt.itemsize] + [dt.fields[f][1] for f in ("hash", "last_use_ns", "src_slot",
+                                                              "pad")]
 
 
 def test_struct_layout_matches_header(tmp_path):
@@ -189,3 +205,47 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(cascade, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="no CPU fallback"):
         cascade.load()
+
+
+def test_reclaim_workspace_size(lib):
+    prev = 0
+    for n in [0, 1, 2048, 2049, 95367, 1 << 22, 1 << 30]:
+        b = cascade.cascade_reclaim_workspace_bytes(n)
+        assert b % 256 == 0 and b >= prev and b > 0
+        prev = b
+    assert cascade.cascade_reclaim_workspace_bytes(-1) == 0
+    assert cascade.cascade_reclaim_workspace_bytes((1 << 30) + 1) == 0
+
+
+def test_reclaim_host_checks(lib):
+    fake = 4096  # never dereferenced: every case below fails a host-side check
+    ws_bytes = cascade.cascade_reclaim_workspace_bytes(100)
+    tab = cascade.TierTable(100, fake, fake, fake)
+
+    def call(tier=0, table=tab, need=10, inc=0, n_inc=0, max_in=0, out=fake, n_out=fake,
+             max_out=10, freed=fake, placed=0, index=0, cap=0, ws=fake * 2, wsb=ws_bytes,
+             status=fake):
+        return cascade.cascade_tier_reclaim(tier, table, need, inc, n_inc, max_in, out, n_out,
+                                            max_out, freed, placed, index, cap, ws, wsb, status, 0)
+
+    E = cascade.EINVAL
+    assert call(tier=3) == E
+    assert call(tier=-1) == E
+    assert call(need=-1) == E
+    assert call(status=0) == E
+    assert call(table=cascade.TierTable(-1, fake, fake, fake)) == E
+    assert call(table=cascade.TierTable(100, 0, fake, fake)) == E
+    assert call(table=cascade.TierTable(100, fake + 8, fake, fake)) == E  # misaligned
+    assert call(max_in=5) == E                       # incoming buffers missing
+    assert call(max_in=5, inc=fake, n_inc=fake) == E  # placed missing
+    assert call(max_out=9) == E                      # room for need demotions
+    assert call(n_out=0) == E
+    assert call(freed=0) == E
+    assert call(index=fake, cap=100) == E            # capacity not a power of two
+    assert call(index=fake + 8, cap=1024) == E       # misaligned index
+    assert call(ws=0) == E
+    assert call(ws=fake + 16) == E                   # workspace not 256-byte aligned
+    assert call(wsb=ws_bytes - 1) == E
+    assert call(need=2**31 - 1, max_in=1, inc=fake, n_inc=fake, placed=fake) == E
+    # NVMe demotes nothing: no outgoing room needed, but the rest still checked
+    assert call(tier=2, max_out=0, out=0, n_out=0, wsb=ws_bytes - 1) == E
