@@ -106,6 +106,47 @@ def measure_prefix_probe(cfg, stream, reps=20):
             "blocks_examined_per_s": float(looked.sum()) / (us * 1e-6)}
 
 
+def measure_reclaim(cfg, stream, reps=20):
+    """Per-tier LRU reclamation, HBM -> DRAM -> NVMe, at the configuration's
+    tier sizes: HIP events around each tier's call on the stream that runs
+    them, tables and index restored from pristine copies between repetitions
+    (outside the timed region).  The oracle's chain is timed once beside it."""
+    import torch
+    import paper_2608_06557_amd.synth as synth
+    from paper_2608_06557_amd import device
+    w = synth.make_tier_workload(cfg)
+    d = device.DeviceTiers(w["tables"], w["needs"], w["index_keys"], w["index_masks"])
+    keep = ([b.clone() for b in d.bh], [x.clone() for x in d.lu], d.index.clone())
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    per, tot = [[], [], []], []
+    for r in range(reps + 2):
+        for t in range(3):
+            d.bh[t].copy_(keep[0][t])
+            d.lu[t].copy_(keep[1][t])
+        d.index.copy_(keep[2])
+        d.status.zero_()
+        ev[0].record(stream)
+        for t in range(3):
+            assert d.call(t, stream) == 0
+            ev[t + 1].record(stream)
+        torch.cuda.synchronize()
+        if r >= 2:  # two warm-ups
+            for t in range(3):
+                per[t].append(ev[t].elapsed_time(ev[t + 1]) * 1e3)
+            tot.append(ev[0].elapsed_time(ev[3]) * 1e3)
+    g = d.fetch()
+    assert g["status"] == 0
+    n_rec = [len(g["tiers"][t]["freed"]) + len(g["tiers"][t]["placed"]) for t in range(3)]
+    slots = int(sum(w["sizes"]))
+    us = float(np.median(tot))
+    progress("tier reclamation measured")
+    return {"tier_slots": list(w["sizes"]), "needs": list(w["needs"]),
+            "reclaimed": n_rec, "demoted": [g["tiers"][t]["n_outgoing"] for t in range(2)],
+            "index_keys": int(len(w["index_keys"])),
+            "tier_us_p50": [float(np.median(x)) for x in per], "chain_us_p50": us,
+            "slots_scanned_per_s": slots / (us * 1e-6)}, w
+
+
 def measure_host_tier(pl, d, st_in, st_out, n_unpack, n_pack, block_bytes, stream,
                       batch=64, reps=3):
     """The DRAM tier's side of the step's restores and spills: pinned host
@@ -190,6 +231,8 @@ def parse():
                     help="approximate CPU time spent on the oracle baseline")
     ap.add_argument("--no-prefix-probe", action="store_true",
                     help="skip the prefix-hit lookup measurement")
+    ap.add_argument("--no-reclaim", action="store_true",
+                    help="skip the per-tier LRU reclamation chain measurement")
     ap.add_argument("--no-host-tier", action="store_true",
                     help="skip the DRAM-tier (pinned host) restore/spill measurement")
     ap.add_argument("--calib-copy-gb", type=float, default=0.0,
@@ -197,8 +240,9 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(w, res, geom, block_bytes, budget_s):
-    """The oracle as it stands, single thread, on this host's cores."""
+def cpu_baseline(w, res, geom, block_bytes, budget_s, tier_w=None):
+    """The oracle as it stands, single thread, on this host's cores (plus, for
+    context, its tier reclamation chain on the same tables as the GPU's)."""
     from oracle import ref
     ref.build(force=False)
     n = len(w["id"])
@@ -235,7 +279,20 @@ def cpu_baseline(w, res, geom, block_bytes, budget_s):
     t_copy_block = el / (creps * 2 * k)          # seconds per block per direction
     t_copy = t_copy_block * (len(pm) + len(um))
     total = t_step + t_copy
-    return {
+    extra = {}
+    if tier_w is not None:
+        t0 = time.perf_counter()
+        inc, masks = None, tier_w["index_masks"]
+        for t in range(3):
+            tb = tier_w["tables"][t]
+            o = ref.tier_reclaim(t, tb["block_hash"], tb["last_use_ns"], tb["held"],
+                                 tier_w["needs"][t], incoming=inc,
+                                 max_outgoing=0 if t == 2 else None,
+                                 index_keys=tier_w["index_keys"], index_masks=masks)
+            assert o["rc"] == 0
+            inc, masks = o["outgoing"], o["index_masks"]
+        extra["tier_reclaim_chain_ms"] = (time.perf_counter() - t0) * 1e3
+    return {**extra,
         "value": n / total, "unit": "req/s", "cores": 1, "kind": "oracle",
         "step_ms": t_step * 1e3, "copy_ms_scaled": t_copy * 1e3,
         "sample": (f"full {n}-request step x{reps}; KV copies: {k} of the step's "
@@ -390,6 +447,7 @@ def main():
         del a, b
     progress("cold-cache steps and device copy done")
     probe = None if args.no_prefix_probe else measure_prefix_probe(cfg, stream)
+    reclaim, tier_w = (None, None) if args.no_reclaim else measure_reclaim(cfg, stream)
     host_tier = None if args.no_host_tier else measure_host_tier(
         pl, d, st_in, st_out, n_unpack, n_pack, block_bytes, stream)
     kernel = "kvmove_kernel" if fused else "kvcopy_kernel"
@@ -434,12 +492,14 @@ def main():
     }
     if probe:
         out["prefix_probe"] = probe
+    if reclaim:
+        out["tier_reclaim"] = reclaim
     if host_tier:
         out["host_tier"] = host_tier
     if extra:
         out["calib_copy"] = extra
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w, res, geom, block_bytes, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, res, geom, block_bytes, args.cpu_seconds, tier_w)
     print(json.dumps(out), flush=True)
 
 

@@ -7,27 +7,30 @@
 // reclaimed set is the `total` smallest free slots under the key
 //   empty slot -> 0,   cached block -> 1 + (last_use - min cached last_use),
 // ties by slot.  Selection is a most-significant-digit radix select over the
-// key (an 8-bit digit, then 12-bit digits), so it never sorts the table:
+// key (an 8-bit digit, then 12-bit digits), so it never sorts the table.  The
+// table is read in tiles of 2048 slots, 8 consecutive slots per thread with
+// 16-byte loads:
 //
-//   rc_count_kernel    per-workgroup counts of empty / cached free slots and
-//                      the cached last-use range; the last workgroup checks
-//                      the call, sizes the key and writes the plan
-//   rc_pass_kernel     one digit: LDS histogram of the keys that match the
-//                      threshold's digits found so far, merged with atomics;
-//                      the last workgroup finds the digit holding the rank
-//   rc_tie_kernel      when only some slots with the threshold key T are
-//                      taken, the slot of the last one taken (taken in slot
-//                      order); per-tile counts, then one workgroup
-//   rc_compact_kernel  slot-order compaction of the reclaimed set and of the
-//                      demoted blocks (one decoupled look-back over a packed
-//                      pair of counts); demotion decisions read the index
-//   rc_update_kernel   index bit updates (clear this tier, set the next for
-//                      demoted blocks) and the slot-table writes
+//   rc_count_kernel  per-workgroup counts of empty / cached free slots and
+//                    the cached last-use range; the last workgroup checks the
+//                    call, sizes the key and writes the plan
+//   rc_pass_kernel   one digit: LDS histogram of the keys that match the
+//                    threshold's digits found so far, merged with atomics;
+//                    the last workgroup finds the digit holding the rank
+//   rc_tiles_kernel  per tile: slots below the threshold key T, slots equal
+//                    to T, and how many of each are demoted (the index read
+//                    once); the last workgroup locates the last slot equal to
+//                    T that is taken (they are taken in slot order), then
+//                    turns the counts into each tile's output offsets
+//   rc_write_kernel  tiles holding reclaimed slots write them, and their
+//                    demoted blocks, at those offsets; the others exit
+//   rc_update_kernel index bit updates (clear this tier, set the next for
+//                    demoted blocks) and the slot-table writes
 //
 // The plan lives in the caller's workspace; every kernel after the first reads
 // it and returns at once when the call failed or has nothing left to do, so
 // the host launches a fixed sequence and never waits.  The last workgroup of
-// each kernel resets the counters it used, which leaves the workspace zeroed.
+// each kernel resets the counter it used, which leaves the workspace zeroed.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <stdint.h>
@@ -43,7 +46,10 @@ namespace {
 
 constexpr int kRcItems = 8;                  // slots per thread in slot-order kernels
 constexpr int kRcTile = kBlock * kRcItems;   // 2048 slots per tile
-constexpr int kRcGrid = 512;                 // workgroups of the whole-table kernels
+constexpr int kRcGridCount = 1024;           // workgroups of the count and tile kernels
+constexpr int kRcGridPass = 512;             // workgroups of a radix pass (fewer bin merges)
+constexpr int kTicketGroups = 16;            // first-level counters of the last-workgroup test
+constexpr int kTicketStride = 32;            // one counter per 128-byte line
 constexpr int kDigit0 = 8, kDigitN = 12;     // first digit, later digits
 constexpr int kRcBins = 1 << kDigitN;
 constexpr int kRcPasses = 1 + (64 - kDigit0 + kDigitN - 1) / kDigitN;  // 6 covers 64 bits
@@ -64,30 +70,29 @@ struct alignas(256) RcPlan {
   int done;       // threshold key found
   int rank;       // 0-based rank still sought among keys matching `prefix`
   int take;       // slots with the threshold key taken, in slot order
-  int find_tie;   // 1: rc_tie_kernel must locate the last tie taken
+  int find_tie;   // 1: only some slots equal to T are taken
   int tie_slot;   // last slot with the threshold key taken (-1: none; INT_MAX: all)
   int pad0;
   unsigned long long lu_min;
   unsigned long long prefix;  // the threshold's digits found so far, in place; T when done
-  unsigned ticket_count, ticket_pass, ticket_tie, tile_claim, compact_done, pad1[3];
 };
 
 struct RcWork {
   RcPlan *plan;
-  RcPartial *partial;     // [kRcGrid]
+  unsigned *tickets;      // [(kTicketGroups + 1) * kTicketStride]
+  RcPartial *partial;     // [kRcGridCount]
   unsigned *hist;         // [kRcBins]
-  int *tie_cnt;           // [tiles]
-  unsigned long long *lb; // [tiles] look-back words
+  int4 *tile;             // [tiles] counts, then output offsets
 };
 
 constexpr size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
-inline int tiles_of(long long n) { return (int)((n + kRcTile - 1) / kRcTile); }
+__host__ __device__ inline int tiles_of(long long n) { return (int)((n + kRcTile - 1) / kRcTile); }
 
 size_t workspace_bytes_for(int32_t n) {
   const size_t tiles = (size_t)std::max(1, tiles_of(n));
-  return align256(sizeof(RcPlan)) + align256(sizeof(RcPartial) * kRcGrid) +
-         align256(sizeof(unsigned) * kRcBins) + align256(sizeof(int) * tiles) +
-         align256(sizeof(unsigned long long) * tiles);
+  return align256(sizeof(RcPlan)) + align256(sizeof(unsigned) * (kTicketGroups + 1) * kTicketStride) +
+         align256(sizeof(RcPartial) * kRcGridCount) +
+         align256(sizeof(unsigned) * kRcBins) + align256(sizeof(int4) * tiles);
 }
 
 RcWork carve(void *ws, int32_t n) {
@@ -96,13 +101,14 @@ RcWork carve(void *ws, int32_t n) {
   RcWork w;
   w.plan = reinterpret_cast<RcPlan *>(p);
   p += align256(sizeof(RcPlan));
+  w.tickets = reinterpret_cast<unsigned *>(p);
+  p += align256(sizeof(unsigned) * (kTicketGroups + 1) * kTicketStride);
   w.partial = reinterpret_cast<RcPartial *>(p);
-  p += align256(sizeof(RcPartial) * kRcGrid);
+  p += align256(sizeof(RcPartial) * kRcGridCount);
   w.hist = reinterpret_cast<unsigned *>(p);
   p += align256(sizeof(unsigned) * kRcBins);
-  w.tie_cnt = reinterpret_cast<int *>(p);
-  p += align256(sizeof(int) * tiles);
-  w.lb = reinterpret_cast<unsigned long long *>(p);
+  w.tile = reinterpret_cast<int4 *>(p);
+  (void)tiles;
   return w;
 }
 
@@ -134,44 +140,138 @@ __device__ __forceinline__ unsigned long long rc_key(unsigned long long h, long 
   return h ? 1ull + ((unsigned long long)lu - lu_min) : 0ull;
 }
 
-// Eight consecutive slots [s0, s0 + 8) of one thread, slots past the table
-// marked held so that nothing selects them.
+// A thread's eight slots of a tile.  Wave w of the workgroup covers slots
+// [w*512, w*512 + 512) of the tile; item i = 2j + e of lane l is slot
+// w*512 + 128*j + 2*l + e, so each of the four 16-byte loads of a wave reads
+// 1 KiB of consecutive hashes (or stamps).  Slots past the table read as held
+// with stamp 0, so nothing selects them.
 struct Slots8 {
   unsigned long long h[kRcItems];
   long long lu[kRcItems];
   bool held[kRcItems];
 };
-__device__ __forceinline__ void load8(const RcArgs &a, int s0, Slots8 &v) {
-  if (s0 + kRcItems <= a.n) {
-    const ulonglong2 *hp = reinterpret_cast<const ulonglong2 *>(a.hash + s0);
-    const longlong2 *lp = reinterpret_cast<const longlong2 *>(a.lu + s0);
+__device__ __forceinline__ int slot_base(int tile) {
+  return tile * kRcTile + wave_id() * (kRcTile / kWaves) + 2 * lane_id();
+}
+__device__ __forceinline__ int item_slot(int base, int i) { return base + 128 * (i >> 1) + (i & 1); }
+
+__device__ __forceinline__ void load8(const RcArgs &a, int base, Slots8 &v) {
+  if (base + 128 * (kRcItems / 2 - 1) + 1 < a.n) {
+    // every slot of the thread is in the table: all twelve loads in flight
+    // before any is used (one bounds test, so no wait between them)
+    ulonglong2 h2[kRcItems / 2];
+    longlong2 l2[kRcItems / 2];
+    unsigned short hd[kRcItems / 2];
 #pragma unroll
     for (int j = 0; j < kRcItems / 2; ++j) {
-      const ulonglong2 h2 = hp[j];
-      const longlong2 l2 = lp[j];
-      v.h[2 * j] = h2.x;
-      v.h[2 * j + 1] = h2.y;
-      v.lu[2 * j] = l2.x;
-      v.lu[2 * j + 1] = l2.y;
+      h2[j] = *reinterpret_cast<const ulonglong2 *>(a.hash + base + 128 * j);
+      l2[j] = *reinterpret_cast<const longlong2 *>(a.lu + base + 128 * j);
+      hd[j] = *reinterpret_cast<const unsigned short *>(a.held + base + 128 * j);
     }
-    const uint2 hd = *reinterpret_cast<const uint2 *>(a.held + s0);
 #pragma unroll
-    for (int j = 0; j < kRcItems; ++j)
-      v.held[j] = ((j < 4 ? hd.x >> (8 * j) : hd.y >> (8 * (j - 4))) & 0xffu) != 0u;
+    for (int j = 0; j < kRcItems / 2; ++j) {
+      v.h[2 * j] = h2[j].x;
+      v.h[2 * j + 1] = h2[j].y;
+      v.lu[2 * j] = l2[j].x;
+      v.lu[2 * j + 1] = l2[j].y;
+      v.held[2 * j] = (hd[j] & 0xffu) != 0u;
+      v.held[2 * j + 1] = (hd[j] >> 8) != 0u;
+    }
   } else {
 #pragma unroll
-    for (int j = 0; j < kRcItems; ++j) {
-      const int s = s0 + j;
+    for (int i = 0; i < kRcItems; ++i) {
+      const int s = item_slot(base, i);
       const bool in = s < a.n;
-      v.h[j] = in ? a.hash[s] : 0ull;
-      v.lu[j] = in ? a.lu[s] : 0ll;
-      v.held[j] = in ? a.held[s] != 0 : true;
+      v.h[i] = in ? a.hash[s] : 0ull;
+      v.lu[i] = in ? a.lu[s] : 0ll;
+      v.held[i] = in ? a.held[s] != 0 : true;
     }
   }
 }
 
+// Slot-order exclusive ranks of the flagged items of a workgroup's tile, and
+// the flagged total.  The four per-lane pair counts (0..2 each) are packed in
+// one word, 8 bits apiece, so one wave scan ranks all four 128-slot rows of
+// the wave (a row holds at most 128 flags, no field overflows).  `lds` holds
+// kWaves ints and is free again on return.
+__device__ __forceinline__ int block_slot_rank(const bool (&f)[kRcItems], int (&rank)[kRcItems],
+                                               int *lds) {
+  unsigned c = 0u;
+#pragma unroll
+  for (int j = 0; j < kRcItems / 2; ++j) c += (unsigned)(f[2 * j] + f[2 * j + 1]) << (8 * j);
+  const unsigned incl = wave_inclusive_sum(c);
+  const unsigned excl = incl - c, tot = last_lane(incl);
+  int row_base[kRcItems / 2], wave_total = 0;
+#pragma unroll
+  for (int j = 0; j < kRcItems / 2; ++j) {
+    row_base[j] = wave_total;
+    wave_total += (int)((tot >> (8 * j)) & 0xffu);
+  }
+  if (lane_id() == 0) lds[wave_id()] = wave_total;
+  __syncthreads();
+  int before = 0, total = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int x = lds[w];
+    before += w < wave_id() ? x : 0;
+    total += x;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kRcItems / 2; ++j) {
+    const int r = before + row_base[j] + (int)((excl >> (8 * j)) & 0xffu);
+    rank[2 * j] = r;
+    rank[2 * j + 1] = r + f[2 * j];
+  }
+  return total;
+}
+
 __device__ __forceinline__ bool status_bad(const int *status) {
   return load_agent(status) != CASCADE_OK;
+}
+
+// Wait until this thread's memory operations have completed.  The values a
+// workgroup hands to the last one are written with agent-scope atomic stores,
+// which need no cache write-back: completing them before the ticket below is
+// their release.  (A device-wide fence per workgroup writes the L2 back and
+// costs tens of microseconds across a thousand workgroups.)
+__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0f70); }  // vmcnt(0)
+
+// Called by thread 0 once the workgroup's results are stored: true for the
+// last workgroup of the grid to arrive.  Two levels of counters (16 groups,
+// then one) keep the atomics on any one address to a few dozen, where a
+// single counter would serialize one per workgroup.  Counters are reset by
+// the workgroup that completes them, so every launch finds them at zero.
+__device__ __forceinline__ bool last_workgroup(unsigned *tk) {
+  const unsigned G = gridDim.x, groups = min(G, (unsigned)kTicketGroups);
+  const unsigned g = blockIdx.x % groups;
+  const unsigned size = (G - g + groups - 1) / groups;
+  unsigned *c = tk + g * kTicketStride;
+  if (atomicAdd(c, 1u) != size - 1) return false;
+  store_agent(c, 0u);
+  unsigned *top = tk + kTicketGroups * kTicketStride;
+  if (atomicAdd(top, 1u) != groups - 1) return false;
+  store_agent(top, 0u);
+  return true;
+}
+
+// Calls f(tile, slots) for this workgroup's tiles (grid-stride), loading the
+// next tile before working on the current one.
+template <typename F>
+__device__ __forceinline__ void for_tiles(const RcArgs &a, F &&f) {
+  const int tiles = max(1, tiles_of(a.n));
+  int t = blockIdx.x;
+  if (t >= tiles) return;
+  Slots8 cur, nxt;
+  load8(a, slot_base(t), cur);
+  for (;;) {
+    const int tn = t + (int)gridDim.x;
+    if (tn < tiles) load8(a, slot_base(tn), nxt);
+    f(t, cur);
+    if (tn >= tiles) break;
+    cur = nxt;
+    t = tn;
+  }
 }
 
 // ------------------------------------------------------------- count kernel
@@ -183,19 +283,19 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
   __shared__ int s_err;
   int cnt[3] = {0, 0, 0};  // empty free, cached free, negative last use
   unsigned long long mn = ~0ull, mx = 0ull;
-  const long long stride = (long long)gridDim.x * kBlock;
-  for (long long s = (long long)blockIdx.x * kBlock + threadIdx.x; s < a.n; s += stride) {
-    const long long lu = a.lu[s];
-    const unsigned long long h = a.hash[s];
-    const bool free_slot = a.held[s] == 0;
-    cnt[2] |= lu < 0;
-    if (free_slot && h == 0ull) ++cnt[0];
-    if (free_slot && h != 0ull && lu >= 0) {
-      ++cnt[1];
-      mn = min(mn, (unsigned long long)lu);
-      mx = max(mx, (unsigned long long)lu);
+  for_tiles(a, [&](int, const Slots8 &v) {  // past the table: held, stamp 0
+#pragma unroll
+    for (int j = 0; j < kRcItems; ++j) {
+      const long long lu = v.lu[j];
+      cnt[2] |= lu < 0;
+      if (!v.held[j] && v.h[j] == 0ull) ++cnt[0];
+      if (!v.held[j] && v.h[j] != 0ull && lu >= 0) {
+        ++cnt[1];
+        mn = min(mn, (unsigned long long)lu);
+        mx = max(mx, (unsigned long long)lu);
+      }
     }
-  }
+  });
   block_sum<3, int>(cnt, s_red);
   mn = wave_min(mn);
   mx = wave_max(mx);
@@ -209,31 +309,28 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
       mn = min(mn, s_mm[w * 2]);
       mx = max(mx, s_mm[w * 2 + 1]);
     }
-    RcPartial p;
-    p.n_empty = cnt[0];
-    p.n_cached = cnt[1];
-    p.bad = cnt[2];
-    p.pad = 0;
-    p.lu_min = mn;
-    p.lu_max = mx;
-    a.w.partial[blockIdx.x] = p;
-    __threadfence();  // release the partial, then count this workgroup
-    s_last = atomicAdd(&a.w.plan->ticket_count, 1u) == gridDim.x - 1;
+    RcPartial *p = a.w.partial + blockIdx.x;
+    store_agent(&p->n_empty, cnt[0]);
+    store_agent(&p->n_cached, cnt[1]);
+    store_agent(&p->bad, cnt[2]);
+    store_agent(&p->lu_min, mn);
+    store_agent(&p->lu_max, mx);
+    wait_stores();
+    s_last = last_workgroup(a.w.tickets);
   }
   __syncthreads();
   if (!s_last) return;
-  __threadfence();  // acquire every workgroup's partial
 
   // the last workgroup: totals, incoming check, plan
   int tot[3] = {0, 0, 0};
   unsigned long long tmn = ~0ull, tmx = 0ull;
   for (int g = threadIdx.x; g < (int)gridDim.x; g += kBlock) {
-    const RcPartial p = a.w.partial[g];
-    tot[0] += p.n_empty;
-    tot[1] += p.n_cached;
-    tot[2] |= p.bad;
-    tmn = min(tmn, p.lu_min);
-    tmx = max(tmx, p.lu_max);
+    const RcPartial *p = a.w.partial + g;
+    tot[0] += load_agent(&p->n_empty);
+    tot[1] += load_agent(&p->n_cached);
+    tot[2] |= load_agent(&p->bad);
+    tmn = min(tmn, load_agent(&p->lu_min));
+    tmx = max(tmx, load_agent(&p->lu_max));
   }
   block_sum<3, int>(tot, s_red);
   tmn = wave_min(tmn);
@@ -289,7 +386,6 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
       P->shift = width - P->dbits;
       P->rank = (int)(total - tot[0] - 1);
     }
-    P->ticket_count = 0u;
   }
 }
 
@@ -309,24 +405,25 @@ __global__ __launch_bounds__(kBlock) void rc_pass_kernel(RcArgs a) {
   const int nbins = 1 << dbits;
   for (int b = threadIdx.x; b < nbins; b += kBlock) s_hist[b] = 0u;
   __syncthreads();
-  const long long stride = (long long)gridDim.x * kBlock;
-  for (long long s = (long long)blockIdx.x * kBlock + threadIdx.x; s < a.n; s += stride) {
-    const unsigned long long h = a.hash[s];
-    if (a.held[s] || h == 0ull) continue;  // only cached free slots have keys above 0
-    const unsigned long long k = rc_key(h, a.lu[s], lu_min);
-    if (shr64(k, shift + dbits) == hi) atomicAdd(&s_hist[(unsigned)(k >> shift) & dmask], 1u);
-  }
+  for_tiles(a, [&](int, const Slots8 &v) {
+#pragma unroll
+    for (int j = 0; j < kRcItems; ++j) {
+      if (v.held[j] || v.h[j] == 0ull) continue;  // only cached free slots have keys above 0
+      const unsigned long long k = rc_key(v.h[j], v.lu[j], lu_min);
+      if (shr64(k, shift + dbits) == hi)
+        atomicAdd(&s_hist[(unsigned)(k >> shift) & dmask], 1u);
+    }
+  });
   __syncthreads();
   for (int b = threadIdx.x; b < nbins; b += kBlock) {
     const unsigned v = s_hist[b];
     if (v) atomicAdd(&a.w.hist[b], v);
   }
-  __threadfence();
+  wait_stores();
   __syncthreads();
-  if (threadIdx.x == 0) s_last = atomicAdd(&a.w.plan->ticket_pass, 1u) == gridDim.x - 1;
+  if (threadIdx.x == 0) s_last = last_workgroup(a.w.tickets);
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
 
   // the last workgroup: the digit in which the sought rank falls
   const int rank = P->rank;
@@ -362,7 +459,6 @@ __global__ __launch_bounds__(kBlock) void rc_pass_kernel(RcArgs a) {
   __syncthreads();
   if (threadIdx.x == 0) {
     RcPlan *W = a.w.plan;
-    W->ticket_pass = 0u;
     if (s_found[0] < 0) {  // the counts disagree with the plan: stop the call
       store_agent(a.status, (int)CASCADE_EINTERNAL);
       W->ok = 0;
@@ -385,188 +481,199 @@ __global__ __launch_bounds__(kBlock) void rc_pass_kernel(RcArgs a) {
   }
 }
 
-// --------------------------------------------------------- tie location
+// ------------------------------------------------------ per-tile counts
 
-// Slots holding the threshold key are taken in slot order; when only some
-// are, find the last one taken.  Also clears the compaction's look-back words.
-__global__ __launch_bounds__(kBlock) void rc_tie_kernel(RcArgs a) {
-  __shared__ int s_red[kWaves];
+__device__ __forceinline__ bool demotable(const RcArgs &a, unsigned long long h) {
+  if (a.tier >= 2 || h == 0ull) return false;
+  if (!a.index) return true;
+  const IndexSlot *e = index_find(a.index, a.index_mask, h);
+  return e == nullptr || (e->tiers & ~((2u << a.tier) - 1u)) == 0u;  // no deeper tier
+}
+
+// a tile's four counts, written by another workgroup as two atomic words
+__device__ __forceinline__ int4 load_rec(const unsigned long long *rec64, int t) {
+  const unsigned long long u = load_agent(rec64 + 2 * t), w = load_agent(rec64 + 2 * t + 1);
+  return make_int4((int)(unsigned)u, (int)(unsigned)(u >> 32), (int)(unsigned)w,
+                   (int)(unsigned)(w >> 32));
+}
+
+// Per tile: slots below T, slots equal to T, and the demoted ones among
+// each.  The last workgroup finds the last slot equal to T that is taken
+// (the take-th in slot order), then writes every tile's output offsets and
+// counts: tile[t] = (reclaimed before t, demoted before t, reclaimed in t,
+// demoted in t).
+__global__ __launch_bounds__(kBlock) void rc_tiles_kernel(RcArgs a) {
+  __shared__ int s_red[kWaves * 4];
   __shared__ bool s_last;
   __shared__ int s_hit[2];
   const RcPlan *P = a.w.plan;
-  const int tile = blockIdx.x;
-  if (threadIdx.x == 0) a.w.lb[tile] = 0ull;
-  if (!P->ok || !P->find_tie) return;
+  if (!P->ok) return;
+  const int tiles = max(1, tiles_of(a.n));
   const unsigned long long T = P->prefix, lu_min = P->lu_min;
-  const int s0 = tile * kRcTile + threadIdx.x * kRcItems;
-  Slots8 v;
-  load8(a, s0, v);
-  int c[1] = {0};
+  unsigned long long *rec64 = reinterpret_cast<unsigned long long *>(a.w.tile);
+  for_tiles(a, [&](int tile, const Slots8 &v) {
+    int c[4] = {0, 0, 0, 0};
 #pragma unroll
-  for (int j = 0; j < kRcItems; ++j)
-    c[0] += (!v.held[j] && rc_key(v.h[j], v.lu[j], lu_min) == T) ? 1 : 0;
-  block_sum<1, int>(c, s_red);
+    for (int j = 0; j < kRcItems; ++j) {
+      const unsigned long long k = rc_key(v.h[j], v.lu[j], lu_min);
+      const bool below = !v.held[j] && k < T, equal = !v.held[j] && k == T;
+      const bool dem = (below || equal) && demotable(a, v.h[j]);
+      c[0] += below;
+      c[1] += equal;
+      c[2] += below && dem;
+      c[3] += equal && dem;
+    }
+    block_sum<4, int>(c, s_red);
+    if (threadIdx.x == 0) {  // (x, y) and (z, w) of the tile's int4, as two atomic words
+      store_agent(rec64 + 2 * tile, (unsigned long long)(unsigned)c[0] |
+                                        ((unsigned long long)(unsigned)c[1] << 32));
+      store_agent(rec64 + 2 * tile + 1, (unsigned long long)(unsigned)c[2] |
+                                            ((unsigned long long)(unsigned)c[3] << 32));
+    }
+  });
   if (threadIdx.x == 0) {
-    a.w.tie_cnt[tile] = c[0];
-    __threadfence();
-    s_last = atomicAdd(&a.w.plan->ticket_tie, 1u) == gridDim.x - 1;
+    wait_stores();
+    s_last = last_workgroup(a.w.tickets);
   }
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
+  Slots8 v;
 
-  // the last workgroup: the tile holding the take-th tie, then the slot
-  const int take = P->take, tiles = gridDim.x;
+  // the last workgroup.  1: the tile holding the take-th slot equal to T
+  const int take = P->take;
   const int per = (tiles + kBlock - 1) / kBlock;
-  if (threadIdx.x == 0) {
-    s_hit[0] = -1;
-    a.w.plan->ticket_tie = 0u;
-  }
-  const int t0 = min(tiles, threadIdx.x * per), t1 = min(tiles, t0 + per);
-  int sum = 0;
-  for (int t = t0; t < t1; ++t) sum += load_agent(a.w.tie_cnt + t);
-  int excl[1] = {sum}, tot[1];
-  block_exclusive_scan<1, int>(excl, tot, s_red);
-  if (take > excl[0] && take <= excl[0] + sum) {
-    int before = excl[0];
-    for (int t = t0; t < t1; ++t) {
-      const int ct = load_agent(a.w.tie_cnt + t);
-      if (take <= before + ct) {
-        s_hit[0] = t;
-        s_hit[1] = take - before;  // 1-based rank inside tile t
-        break;
+  const int t0 = min(tiles, (int)threadIdx.x * per), t1 = min(tiles, t0 + per);
+  int cut = take == 0 ? -1 : tiles;  // tiles before `cut` give all their slots equal to T
+  int r_cut = 0, dem_cut = 0, tie_slot = take == 0 ? -1 : INT_MAX;
+  if (threadIdx.x == 0) s_hit[0] = -1;
+  if (P->find_tie) {
+    int sum = 0;
+    for (int t = t0; t < t1; ++t) sum += (int)(load_agent(rec64 + 2 * t) >> 32);
+    int ex[1] = {sum}, tot[1];
+    block_exclusive_scan<1, int>(ex, tot, s_red);
+    if (take > ex[0] && take <= ex[0] + sum) {
+      int before = ex[0];
+      for (int t = t0; t < t1; ++t) {
+        const int ct = (int)(load_agent(rec64 + 2 * t) >> 32);
+        if (take <= before + ct) {
+          s_hit[0] = t;
+          s_hit[1] = take - before;  // 1-based rank inside tile t
+          break;
+        }
+        before += ct;
       }
-      before += ct;
     }
-  }
-  __syncthreads();
-  const int ht = s_hit[0], want = s_hit[1];
-  if (ht < 0) {  // the counts disagree with the plan: stop the call
-    if (threadIdx.x == 0) {
-      store_agent(a.status, (int)CASCADE_EINTERNAL);
-      a.w.plan->ok = 0;
+    __syncthreads();
+    if (s_hit[0] < 0) {  // the counts disagree with the plan: stop the call
+      if (threadIdx.x == 0) {
+        store_agent(a.status, (int)CASCADE_EINTERNAL);
+        a.w.plan->ok = 0;
+      }
+      return;
     }
-    return;
-  }
-  load8(a, ht * kRcTile + threadIdx.x * kRcItems, v);
-  int mine = 0;
-  bool is_tie[kRcItems];
+    cut = s_hit[0];
+    r_cut = s_hit[1];
+    // inside the cut tile: the slot of the r_cut-th equal key, and how many
+    // of the first r_cut are demoted
+    const int base = slot_base(cut);
+    load8(a, base, v);
+    bool eq[kRcItems];
+    int rk[kRcItems];
 #pragma unroll
-  for (int j = 0; j < kRcItems; ++j) {
-    is_tie[j] = !v.held[j] && rc_key(v.h[j], v.lu[j], lu_min) == T;
-    mine += is_tie[j] ? 1 : 0;
-  }
-  int e2[1] = {mine}, t2[1];
-  block_exclusive_scan<1, int>(e2, t2, s_red);
-  if (want > e2[0] && want <= e2[0] + mine) {
-    int r = want - e2[0];
+    for (int j = 0; j < kRcItems; ++j) eq[j] = !v.held[j] && rc_key(v.h[j], v.lu[j], lu_min) == T;
+    block_slot_rank(eq, rk, s_red);
+    int d[1] = {0};
 #pragma unroll
     for (int j = 0; j < kRcItems; ++j) {
-      if (is_tie[j] && r > 0 && --r == 0)
-        a.w.plan->tie_slot = ht * kRcTile + threadIdx.x * kRcItems + j;
+      if (eq[j] && rk[j] < r_cut) {
+        d[0] += demotable(a, v.h[j]);
+        if (rk[j] == r_cut - 1) s_hit[0] = item_slot(base, j);
+      }
+    }
+    block_sum<1, int>(d, s_red);
+    tie_slot = s_hit[0];
+    dem_cut = d[0];
+  }
+  // 2: offsets, in tile order
+  int sums[2] = {0, 0};
+  for (int t = t0; t < t1; ++t) {
+    const int4 q = load_rec(rec64, t);
+    sums[0] += q.x + (t < cut ? q.y : (t == cut ? r_cut : 0));
+    sums[1] += q.z + (t < cut ? q.w : (t == cut ? dem_cut : 0));
+  }
+  int tot[2];
+  block_exclusive_scan<2, int>(sums, tot, s_red);
+  int off_sel = sums[0], off_dem = sums[1];
+  for (int t = t0; t < t1; ++t) {
+    const int4 q = load_rec(rec64, t);
+    const int ns = q.x + (t < cut ? q.y : (t == cut ? r_cut : 0));
+    const int nd = q.z + (t < cut ? q.w : (t == cut ? dem_cut : 0));
+    a.w.tile[t] = make_int4(off_sel, off_dem, ns, nd);
+    off_sel += ns;
+    off_dem += nd;
+  }
+  if (threadIdx.x == 0) {
+    RcPlan *W = a.w.plan;
+    W->tie_slot = tie_slot;
+    if (tot[0] != P->total || tot[1] > a.max_out) {  // must reclaim exactly total
+      store_agent(a.status, (int)CASCADE_EINTERNAL);
+      W->ok = 0;
+    } else if (a.n_out_dev) {
+      store_agent(a.n_out_dev, tot[1]);
     }
   }
 }
 
-// ------------------------------------------------------------- compaction
+// ---------------------------------------------------------------- writes
 
-// Counts of one tile packed in one word: reclaimed | demoted << 31.
-constexpr int kDemShift = 31;
-
-__global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
-  __shared__ unsigned long long s_scan[kWaves];
-  __shared__ int s_tile;
-  __shared__ unsigned long long s_prefix;
-  __shared__ bool s_last, s_timeout;
+// Tiles holding reclaimed slots write them (ascending: freed, then placed)
+// and their demoted blocks at the offsets the counts gave.
+__global__ __launch_bounds__(kBlock) void rc_write_kernel(RcArgs a) {
+  __shared__ int s_red[kWaves];
   const RcPlan *P = a.w.plan;
   if (!P->ok) return;
-  if (threadIdx.x == 0) {
-    s_tile = (int)atomicAdd(&a.w.plan->tile_claim, 1u);
-    s_timeout = false;
-  }
-  __syncthreads();
-  const int tile = s_tile;
-  if (tile >= (int)gridDim.x) {  // counters not zeroed: refuse to touch anything
-    if (threadIdx.x == 0) store_agent(a.status, (int)CASCADE_EINTERNAL);
-    return;
-  }
+  const int4 rec = a.w.tile[blockIdx.x];
+  if (rec.z == 0) return;  // nothing reclaimed here (so nothing demoted either)
   const unsigned long long T = P->prefix, lu_min = P->lu_min;
-  const int tie_slot = P->tie_slot, need = a.need;
-  const bool can_demote = a.tier < 2;
-  const unsigned deeper = ~((2u << a.tier) - 1u);  // tiers below this one
-  const int s0 = tile * kRcTile + threadIdx.x * kRcItems;
+  const int tie_slot = P->tie_slot, need = a.need, total = P->total;
+  const int base = slot_base(blockIdx.x);
   Slots8 v;
-  load8(a, s0, v);
+  load8(a, base, v);
   bool sel[kRcItems], dem[kRcItems];
-  unsigned long long cnt = 0ull;
 #pragma unroll
   for (int j = 0; j < kRcItems; ++j) {
     const unsigned long long k = rc_key(v.h[j], v.lu[j], lu_min);
-    sel[j] = !v.held[j] && (k < T || (k == T && s0 + j <= tie_slot));
-    dem[j] = false;
-    if (sel[j] && can_demote && v.h[j] != 0ull) {
-      const IndexSlot *e = a.index ? index_find(a.index, a.index_mask, v.h[j]) : nullptr;
-      dem[j] = e == nullptr || (e->tiers & deeper) == 0u;
-    }
-    cnt += (sel[j] ? 1ull : 0ull) + (dem[j] ? (1ull << kDemShift) : 0ull);
+    sel[j] = !v.held[j] && (k < T || (k == T && item_slot(base, j) <= tie_slot));
+    dem[j] = sel[j] && demotable(a, v.h[j]);
   }
-  unsigned long long ex[1] = {cnt}, tot[1];
-  block_exclusive_scan<1, unsigned long long>(ex, tot, s_scan);
-  if (threadIdx.x == 0) {
-    unsigned long long before = 0ull;
-    if (tile == 0) {
-      publish(a.w.lb, tot[0], kFlagInclusive);
-    } else {
-      publish(a.w.lb + tile, tot[0], kFlagAggregate);
-      bool to = false;
-      before = look_back<unsigned long long, 32>(a.w.lb, 1, tile, 0, &to);
-      s_timeout = to;
-      publish(a.w.lb + tile, before + tot[0], kFlagInclusive);
-    }
-    s_prefix = before;
-  }
-  __syncthreads();
-  if (s_timeout) {
-    if (threadIdx.x == 0) store_agent(a.status, (int)CASCADE_ETIMEOUT);
-  } else {
-    const unsigned long long base = s_prefix + ex[0];
-    int p = (int)(base & ((1ull << kDemShift) - 1ull));
-    int q = (int)(base >> kDemShift);
-    const int total = P->total;
-    bool over = false;
+  int rs[kRcItems], rd[kRcItems];
+  const int n_sel = block_slot_rank(sel, rs, s_red);
+  const int n_dem = block_slot_rank(dem, rd, s_red);
+  bool bad = n_sel != rec.z || n_dem != rec.w;
 #pragma unroll
-    for (int j = 0; j < kRcItems; ++j) {
-      if (sel[j]) {
-        if (p < need) a.freed[p] = s0 + j;
-        else if (p < total) a.placed[p - need] = s0 + j;
-        else over = true;
-        ++p;
-      }
-      if (dem[j] && q >= a.max_out) over = true;
-      if (dem[j] && q < a.max_out) {
+  for (int j = 0; j < kRcItems; ++j) {
+    const int slot = item_slot(base, j);
+    if (sel[j]) {
+      const int p = rec.x + rs[j];
+      if (p < need) a.freed[p] = slot;
+      else if (p < total) a.placed[p - need] = slot;
+      else bad = true;
+    }
+    if (dem[j]) {
+      const int q = rec.y + rd[j];
+      if (q < a.max_out) {
         cascade_demotion_t d;
         d.hash = v.h[j];
         d.last_use_ns = v.lu[j];
-        d.src_slot = s0 + j;
+        d.src_slot = slot;
         d.pad = 0;
-        a.outgoing[q++] = d;
+        a.outgoing[q] = d;
+      } else {
+        bad = true;
       }
     }
-    if (over) store_agent(a.status, (int)CASCADE_EINTERNAL);
   }
-  // the last tile to finish publishes the count and resets the counters
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = atomicAdd(&a.w.plan->compact_done, 1u) == gridDim.x - 1;
-  __syncthreads();
-  if (!s_last || threadIdx.x != 0) return;
-  __threadfence();
-  const unsigned long long all = load_agent(a.w.lb + (gridDim.x - 1)) >> 2;
-  if ((int)(all & ((1ull << kDemShift) - 1ull)) != P->total)  // must reclaim exactly total
-    store_agent(a.status, (int)CASCADE_EINTERNAL);
-  if (a.n_out_dev) store_agent(a.n_out_dev, (int)(all >> kDemShift));
-  a.w.plan->tile_claim = 0u;
-  a.w.plan->compact_done = 0u;
+  if (bad) store_agent(a.status, (int)CASCADE_EINTERNAL);
 }
 
 // ---------------------------------------------------------------- updates
@@ -635,8 +742,8 @@ extern "C" int cascade_tier_reclaim(int32_t tier, const cascade_tier_table_t *ta
   if (n < 0 || n > (1 << 30)) return CASCADE_EINVAL;
   if (n > 0 && (!table->block_hash || !table->last_use_ns || !table->held)) return CASCADE_EINVAL;
   if (((uintptr_t)table->block_hash & 15) || ((uintptr_t)table->last_use_ns & 15) ||
-      ((uintptr_t)table->held & 7))
-    return CASCADE_EINVAL;  // the slot-order kernels load 8 slots with vector loads
+      ((uintptr_t)table->held & 1))
+    return CASCADE_EINVAL;  // the kernels load slot pairs with vector loads
   if (max_incoming > 0 && (!incoming || !n_incoming_dev || !placed)) return CASCADE_EINVAL;
   if (need > 0 && !freed) return CASCADE_EINVAL;
   if (tier < 2) {
@@ -671,13 +778,15 @@ extern "C" int cascade_tier_reclaim(int32_t tier, const cascade_tier_table_t *ta
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int tiles = std::max(1, tiles_of(n));
-  const int grid = std::min(tiles, kRcGrid);
   const int total_cap = (int)std::min<long long>((long long)need + max_incoming, n);
-  hipLaunchKernelGGL(rc_count_kernel, dim3(grid), dim3(kBlock), 0, s, a);
+  hipLaunchKernelGGL(rc_count_kernel, dim3(std::min(tiles, kRcGridCount)), dim3(kBlock), 0, s,
+                     a);
   for (int p = 0; p < kRcPasses; ++p)
-    hipLaunchKernelGGL(rc_pass_kernel, dim3(grid), dim3(kBlock), 0, s, a);
-  hipLaunchKernelGGL(rc_tie_kernel, dim3(tiles), dim3(kBlock), 0, s, a);
-  hipLaunchKernelGGL(rc_compact_kernel, dim3(tiles), dim3(kBlock), 0, s, a);
+    hipLaunchKernelGGL(rc_pass_kernel, dim3(std::min(tiles, kRcGridPass)), dim3(kBlock), 0, s,
+                       a);
+  hipLaunchKernelGGL(rc_tiles_kernel, dim3(std::min(tiles, kRcGridCount)), dim3(kBlock), 0, s,
+                     a);
+  hipLaunchKernelGGL(rc_write_kernel, dim3(tiles), dim3(kBlock), 0, s, a);
   if (total_cap > 0)
     hipLaunchKernelGGL(rc_update_kernel, dim3((total_cap + kBlock - 1) / kBlock), dim3(kBlock),
                        0, s, a);
