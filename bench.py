@@ -29,13 +29,13 @@ METRIC = ("scheduling-step latency (µs) & requests/s at N=65536; "
           "KV pack/unpack GB/s vs HBM peak")
 HBM_PEAK_GBPS = 8000.0
 WORKLOADS = {
-    0: "tiny: 256 chat requests, 3 SLO classes, 8B-class KV (32 layers), 4096-block pool",
-    1: "mid: 8192 chat requests, 5 SLO classes, 65536-block (128 GiB) pool, token cap 16384",
-    2: ("headline: 65536 requests, 80% chat / 20% agentic, 8B-class KV (32 layers x 8 heads x "
+    0: "256 chat requests, 3 SLO classes, 8B-class KV (32 layers), 4096-block pool",
+    1: "8192 chat requests, 5 SLO classes, 65536-block (128 GiB) pool, token cap 16384",
+    2: ("65536 requests, 80% chat / 20% agentic, 8B-class KV (32 layers x 8 heads x "
         "128 x bf16, 16-token blocks), 200 GB pool, token cap 16384, ~2 GB packed and unpacked"),
-    3: ("reasoning-heavy: 65536 requests, 30% sharing 512 prefixes of 1k-32k tokens, high load, "
+    3: ("65536 requests, reasoning-heavy, 30% sharing 512 prefixes of 1k-32k tokens, high load, "
         "exact budget ties, 200 GB pool"),
-    4: ("scale: 262144 requests, 70B-class KV (80 layers), 250 GB pool, token cap 32768, "
+    4: ("262144 requests, 70B-class KV (80 layers), 250 GB pool, token cap 32768, "
         "~8 GB packed and unpacked"),
 }
 
@@ -46,7 +46,7 @@ def measured_traffic(cfg, layout, kernel, chunk_bytes):
     plain copy of known size), or None when the workload or kernel differs or
     the kernel source has changed since the counters were taken."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "kvmove_counters_headline_65536.md")
+    path = os.path.join(ROOT, "profiles", "kvmove_counters_65536req_8b_200gb.md")
     try:
         text = open(path).read()
         rec = json.loads(text.rsplit("```json", 1)[1].split("```", 1)[0])
@@ -470,7 +470,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic",
-        "config": {"workload": f"config {cfg}: " + WORKLOADS[cfg], "requests": n,
+        "config": {"workload": WORKLOADS[cfg], "requests": n,
                    "kv_layout": args.layout, "pool_blocks": nb,
                    "chunk_bytes": geom["chunk_bytes"],
                    "block_bytes": block_bytes, "token_cap": c["token_cap"],

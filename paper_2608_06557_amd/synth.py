@@ -12,11 +12,11 @@ ChatBot / Tool&Agent / Coder / Reasoning), Table 3 (seconds-scale TTFT
 targets) and Section 5's serving setup (chunk 512, max batch 128).
 
 Five workloads (``make_workload(cfg)``):
-  0  tiny: 256 chat requests, 3 SLO classes, 8B-class KV, 4096-block pool
-  1  mid: 8192 chat requests, 5 classes, 65536-block pool, token cap 16384
-  2  headline: 65536 requests, 80% chat / 20% agentic, 200 GB pool
+  0  256 chat requests, 3 SLO classes, 8B-class KV, 4096-block pool
+  1  8192 chat requests, 5 classes, 65536-block pool, token cap 16384
+  2  65536 requests, 80% chat / 20% agentic, 200 GB pool
   3  reasoning-heavy, prefix-shared, high load, exact budget ties
-  4  scale: 262144 requests, 70B-class KV, 250 GB pool, token cap 32768
+  4  262144 requests, 70B-class KV, 250 GB pool, token cap 32768
 """
 from __future__ import annotations
 

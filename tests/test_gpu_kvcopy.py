@@ -1,6 +1,6 @@
 """GPU parity of the paged-KV pack / unpack kernels against the oracle's
 per-chunk memcpy (byte-exact).  Small pools are compared in full; the
-headline workload's 200 GB pool is checked on sampled chunks, whose expected
+65536-request workload's 200 GB pool is checked on sampled chunks, whose expected
 bytes the CPU regenerates from the counter-based fill."""
 import numpy as np
 import pytest
@@ -119,7 +119,7 @@ def _chunk_words(geom, slot, l, kv):
     return np.arange(off // 4, (off + geom["chunk_bytes"]) // 4, dtype=np.int64)
 
 
-def test_headline_step_moves_full_size(dev):
+def test_65536_request_step_moves_full_size(dev):
     """Config 2 at full size: 200 GB pool, the step's own move lists, pack
     then unpack as the benchmark runs them; sampled chunks checked."""
     import torch
