@@ -383,7 +383,7 @@ int cascade_prefix_probe(const void *index, int32_t capacity, int32_t n,
                 free; then it writes nothing else.  CASCADE_ETIMEOUT or
                 CASCADE_EINTERNAL report a failed cross-workgroup wait or
                 consistency check.
-   Alignment: block_hash and last_use_ns 16 bytes, held 8 bytes.
+   Alignment: block_hash and last_use_ns 16 bytes, held 2 bytes.
    Returns CASCADE_EINVAL for bad host arguments, CASCADE_EHIP on a failed
    launch.  Asynchronous on `stream`. */
 typedef struct {

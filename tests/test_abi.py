@@ -236,6 +236,8 @@ def test_reclaim_host_checks(lib):
     assert call(table=cascade.TierTable(-1, fake, fake, fake)) == E
     assert call(table=cascade.TierTable(100, 0, fake, fake)) == E
     assert call(table=cascade.TierTable(100, fake + 8, fake, fake)) == E  # misaligned
+    assert call(table=cascade.TierTable(100, fake, fake + 8, fake)) == E
+    assert call(table=cascade.TierTable(100, fake, fake, fake + 1)) == E
     assert call(max_in=5) == E                       # incoming buffers missing
     assert call(max_in=5, inc=fake, n_inc=fake) == E  # placed missing
     assert call(max_out=9) == E                      # room for need demotions
