@@ -304,7 +304,7 @@ def cpu_baseline(w, res, geom, block_bytes, budget_s, tier_w=None):
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only; the step is independent per "
+        print("bench.py: runs on one GPU only; the step is independent per "
               "serving instance (no cross-GPU exchange), so --gpus must be 1", file=sys.stderr)
         sys.exit(2)
     import torch
