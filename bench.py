@@ -139,8 +139,12 @@ def measure_reclaim(cfg, stream, reps=20):
     n_rec = [len(g["tiers"][t]["freed"]) + len(g["tiers"][t]["placed"]) for t in range(3)]
     slots = int(sum(w["sizes"]))
     us = float(np.median(tot))
+    # compulsory traffic: every slot's hash, stamp and held flag read once
+    compulsory = 17 * slots
     progress("tier reclamation measured")
     return {"tier_slots": list(w["sizes"]), "needs": list(w["needs"]),
+            "compulsory_bytes": compulsory,
+            "compulsory_us_at_peak": compulsory / (HBM_PEAK_GBPS * 1e3),
             "reclaimed": n_rec, "demoted": [g["tiers"][t]["n_outgoing"] for t in range(2)],
             "index_keys": int(len(w["index_keys"])),
             "tier_us_p50": [float(np.median(x)) for x in per], "chain_us_p50": us,
