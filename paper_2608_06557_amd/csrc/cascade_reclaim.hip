@@ -48,8 +48,6 @@ constexpr int kRcItems = 8;                  // slots per thread in slot-order k
 constexpr int kRcTile = kBlock * kRcItems;   // 2048 slots per tile
 constexpr int kRcGridCount = 1024;           // workgroups of the count and tile kernels
 constexpr int kRcGridPass = 512;             // workgroups of a radix pass (fewer bin merges)
-constexpr int kTicketGroups = 16;            // first-level counters of the last-workgroup test
-constexpr int kTicketStride = 32;            // one counter per 128-byte line
 constexpr int kDigit0 = 8, kDigitN = 12;     // first digit, later digits
 constexpr int kRcBins = 1 << kDigitN;
 constexpr int kRcPasses = 1 + (64 - kDigit0 + kDigitN - 1) / kDigitN;  // 6 covers 64 bits
@@ -228,31 +226,6 @@ __device__ __forceinline__ int block_slot_rank(const bool (&f)[kRcItems], int (&
 
 __device__ __forceinline__ bool status_bad(const int *status) {
   return load_agent(status) != CASCADE_OK;
-}
-
-// Wait until this thread's memory operations have completed.  The values a
-// workgroup hands to the last one are written with agent-scope atomic stores,
-// which need no cache write-back: completing them before the ticket below is
-// their release.  (A device-wide fence per workgroup writes the L2 back and
-// costs tens of microseconds across a thousand workgroups.)
-__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0f70); }  // vmcnt(0)
-
-// Called by thread 0 once the workgroup's results are stored: true for the
-// last workgroup of the grid to arrive.  Two levels of counters (16 groups,
-// then one) keep the atomics on any one address to a few dozen, where a
-// single counter would serialize one per workgroup.  Counters are reset by
-// the workgroup that completes them, so every launch finds them at zero.
-__device__ __forceinline__ bool last_workgroup(unsigned *tk) {
-  const unsigned G = gridDim.x, groups = min(G, (unsigned)kTicketGroups);
-  const unsigned g = blockIdx.x % groups;
-  const unsigned size = (G - g + groups - 1) / groups;
-  unsigned *c = tk + g * kTicketStride;
-  if (atomicAdd(c, 1u) != size - 1) return false;
-  store_agent(c, 0u);
-  unsigned *top = tk + kTicketGroups * kTicketStride;
-  if (atomicAdd(top, 1u) != groups - 1) return false;
-  store_agent(top, 0u);
-  return true;
 }
 
 // Calls f(tile, slots) for this workgroup's tiles (grid-stride), loading the

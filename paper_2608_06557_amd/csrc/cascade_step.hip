@@ -44,9 +44,10 @@ constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
 constexpr int kPrepItems = 4;
 constexpr int kEvalItems = 1;
-constexpr int kRadix = 256;
+constexpr int kRadix = 256;      // 8-bit digits
 constexpr int kMaxDigits = 8;
 constexpr int kL1 = 5;           // first-level scan values
+constexpr int kMaxScanTiles = ((1 << 20) + kScanTile - 1) / kScanTile;
 constexpr int kL2 = 7;           // second-level scan values
 constexpr int kL2Stride = 8;
 
@@ -69,12 +70,12 @@ struct Partial {
   unsigned pad[2];
 };
 
-// A running prefill, as seen by the scan (compact list, 48 bytes).
+// A running prefill, as seen by the scan (compact list, 64 bytes).
 struct RpInfo {
   int req, pos, eligible, held, row0, offl, pad[2];
   long long x, y, z, zp;          // inclusive prefixes at pos
 };
-struct RestoreEnt { int req, stage_off, alloc_off, blocks; };
+struct alignas(16) RestoreEnt { int req, stage_off, alloc_off, blocks; };
 // Totals of one scan tile over its admitted / left-out requests.
 struct TileTot {
   long long adm_nb, elig_h, elig_offl_h, n_adm, n_unpack, n_restore, pad[2];
@@ -82,19 +83,28 @@ struct TileTot {
 constexpr int kVictimCap = 256;   // victims staged in LDS by the finishing workgroup
 constexpr int kRestoreCap = 1024; // restore-list entries staged in LDS for the search
 
-// Device control block.  eval's workgroup 0 zeroes the header, every eval
+// Device control block.  eval's first thread zeroes the header, every eval
 // workgroup clears part of the histograms and look-back words.
 struct Ctl {
   unsigned long long bmin, bmax;  // totals, written by prep's workgroup 0
   long long held_rp, need1, want1;
   unsigned cnt[4];
-  unsigned tile_ctr[kMaxDigits + 1];
-  unsigned scan_done, pad_u;
+  unsigned tile_ctr[kMaxDigits];  // radix tiles claimed per pass
+  unsigned nact;                  // data-moving radix passes, from the sort plan
+  int n_rp;                       // running prefills in the queue (last scan tile)
   int kstar;                      // first position whose blocks do not fit
   long long kx, ky, kz, kzp;      // prefixes just before kstar
-  alignas(16) unsigned hist[kMaxDigits][kRadix];
+  alignas(16) unsigned hist[kMaxDigits][kRadix];  // cleared by eval's grid
 };
 constexpr size_t kCtlHeaderWords = offsetof(Ctl, hist) / 4;
+
+// Sorted order with each request's scan record and block-table row offset,
+// written by the last data-moving radix pass.
+struct Sorted {
+  unsigned *order;
+  int4 *rec;
+  int *ro;
+};
 
 struct Consts {                   // parameters the kernels use, flattened
   long long t_now, c_iter, c_dec, c_tok, c_attn;
@@ -111,6 +121,29 @@ struct Outs {                     // output pointers the scan writes
   int *unpack_hazard, *pack_hazard;  // may be null
   int sl_cap, unpack_cap, pack_cap;
 };
+
+// Records handed to the finishing workgroup within a launch move as 8-byte
+// agent-scope atomic words (no cache write-back needed to publish them).
+template <typename T>
+__device__ __forceinline__ void store_agent_rec(T *dst, const T &v) {
+  static_assert(sizeof(T) % 8 == 0 && alignof(T) >= 4, "whole 8-byte words");
+  unsigned long long w[sizeof(T) / 8];
+  __builtin_memcpy(w, &v, sizeof(T));
+  unsigned long long *d = reinterpret_cast<unsigned long long *>(dst);
+#pragma unroll
+  for (int k = 0; k < (int)(sizeof(T) / 8); ++k) store_agent(d + k, w[k]);
+}
+template <typename T>
+__device__ __forceinline__ T load_agent_rec(const T *src) {
+  static_assert(sizeof(T) % 8 == 0 && alignof(T) >= 4, "whole 8-byte words");
+  unsigned long long w[sizeof(T) / 8];
+  const unsigned long long *p = reinterpret_cast<const unsigned long long *>(src);
+#pragma unroll
+  for (int k = 0; k < (int)(sizeof(T) / 8); ++k) w[k] = load_agent(p + k);
+  T v;
+  __builtin_memcpy(&v, w, sizeof(T));
+  return v;
+}
 
 __device__ __forceinline__ bool bad_status(int s) {
   return s == CASCADE_EINVAL || s == CASCADE_ETIMEOUT || s == CASCADE_EINTERNAL;
@@ -366,19 +399,22 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
 
 // ------------------------------------------------------ sort: digit plan
 
-// Width of the compressed key key' = group*span + (biased - bmin).
-__device__ __forceinline__ int key_digits(unsigned long long mn, unsigned long long mx,
-                                          unsigned c1, unsigned c2) {
+// Width in bits of the compressed key key' = group*span + (biased - bmin).
+__device__ __forceinline__ int key_bits(unsigned long long mn, unsigned long long mx,
+                                        unsigned c1, unsigned c2) {
   const unsigned long long span = mx - mn + 1;
   const unsigned long long gmax = c2 ? 2 : (c1 ? 1 : 0);
   const unsigned long long top = gmax * span + (mx - mn);
-  const int bits = top ? 64 - __builtin_clzll(top) : 0;
-  return (bits + 7) / 8;
+  return top ? 64 - __builtin_clzll(top) : 0;
+}
+__device__ __forceinline__ int key_digits(unsigned long long mn, unsigned long long mx,
+                                          unsigned c1, unsigned c2) {
+  return (key_bits(mn, mx, c1, c2) + 7) / 8;
 }
 
 // Sort plan: the digits that move data (below the key width, not constant
-// over all n keys), as a bit mask.  Every radix and scan workgroup derives it
-// from the histograms; hv holds thread t's bucket t of every digit.
+// over all n keys), as a bit mask.  Every radix workgroup derives it from the
+// histograms; hv holds thread t's bucket t of every digit.
 __device__ __forceinline__ unsigned plan_mask(const unsigned (&hv)[kMaxDigits], int n, int nd,
                                               unsigned *s_mask) {
   unsigned constant = 0;
@@ -393,9 +429,10 @@ __device__ __forceinline__ unsigned plan_mask(const unsigned (&hv)[kMaxDigits], 
 
 // Totals of eval's partials; order-preserving key compression
 // key' = group * span + (biased - bmin), then one read of the keys builds
-// every digit's histogram (per-thread runs of equal digits are merged before
-// the LDS atomics, so low-entropy high digits do not serialise).  Also checks
-// the block-table slots, whose extent is only trustworthy after eval.
+// every digit's histogram (LDS counts, then one global add per non-empty
+// bucket).  The keys are requested before the totals they are compressed
+// with.  Also checks the block-table slots, whose extent is only trustworthy
+// after eval.
 __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int n_partials,
                                                       const Partial *__restrict__ partials,
                                                       const int *__restrict__ ro,
@@ -407,10 +444,19 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
   __shared__ long long s_red[kWaves * 3];
   __shared__ unsigned s_cnt[kWaves * 4];
   __shared__ unsigned long long s_mm[kWaves * 2];
+  const int t = threadIdx.x;
+  const int base = blockIdx.x * kBlock * kPrepItems;
+  unsigned long long kv[kPrepItems];
+#pragma unroll
+  for (int j = 0; j < kPrepItems; ++j) {
+    const int idx = base + j * kBlock + t;
+    kv[j] = idx < n ? keys[idx] : 0ull;
+  }
   long long sums[3] = {0, 0, 0};
   unsigned cnt[4] = {0, 0, 0, 0};
   unsigned long long mn = ~0ull, mx = 0;
-  for (int j = threadIdx.x; j < n_partials; j += kBlock) {
+#pragma unroll 1
+  for (int j = t; j < n_partials; j += kBlock) {
     const Partial p = partials[j];
     sums[0] += p.held;
     sums[1] += p.need1;
@@ -422,6 +468,7 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
     mn = p.bmin < mn ? p.bmin : mn;
     mx = p.bmax > mx ? p.bmax : mx;
   }
+  for (int k = t; k < kMaxDigits * kRadix; k += kBlock) (&s_hist[0][0])[k] = 0;
   block_sum<3>(sums, s_red);
   block_sum<4>(cnt, s_cnt);
   mn = wave_min(mn);
@@ -437,7 +484,7 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
     mn = s_mm[2 * w] < mn ? s_mm[2 * w] : mn;
     mx = s_mm[2 * w + 1] > mx ? s_mm[2 * w + 1] : mx;
   }
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
+  if (blockIdx.x == 0 && t == 0) {
     ctl->bmin = mn;
     ctl->bmax = mx;
     ctl->held_rp = sums[0];
@@ -453,7 +500,8 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
   const int nnz = ro[n];
   bool bad = false;
   {
-    const int gt = blockIdx.x * kBlock + threadIdx.x, gs = gridDim.x * kBlock;
+    const int gt = blockIdx.x * kBlock + t, gs = gridDim.x * kBlock;
+#pragma unroll 1
     for (int j0 = gt; j0 < nnz; j0 += 8 * gs) {
       int v[8];
 #pragma unroll
@@ -464,58 +512,82 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
     }
   }
   if (__syncthreads_or(bad ? 1 : 0)) {
-    if (threadIdx.x == 0) set_status(info, CASCADE_EINVAL);
+    if (t == 0) set_status(info, CASCADE_EINVAL);
   }
 
   const int nd = key_digits(mn, mx, cnt[1], cnt[2]);
   const unsigned long long span = mx - mn + 1;
-  for (int t = threadIdx.x; t < kMaxDigits * kRadix; t += kBlock) (&s_hist[0][0])[t] = 0;
-  const int base = blockIdx.x * kBlock * kPrepItems;
-  unsigned long long kv[kPrepItems];
-#pragma unroll
-  for (int j = 0; j < kPrepItems; ++j) {  // every load in flight before any use
-    const int idx = base + j * kBlock + threadIdx.x;
-    kv[j] = idx < n ? keys[idx] : 0ull;
-  }
-  __syncthreads();
 #pragma unroll
   for (int j = 0; j < kPrepItems; ++j) {
-    const int idx = base + j * kBlock + threadIdx.x;
-    if (idx < n) {
-      const unsigned long long k0 = kv[j];
-      const unsigned long long k = (k0 >> 62) * span + ((k0 & ((1ull << 62) - 1)) - mn);
+    const int idx = base + j * kBlock + t;
+    const bool v = idx < n;
+    const unsigned long long k0 = kv[j];
+    const unsigned long long k = (k0 >> 62) * span + ((k0 & ((1ull << 62) - 1)) - mn);
+    if (v) {
       keys[idx] = k;
       vals[idx] = (unsigned)idx;
-      for (int d = 0; d < nd; ++d) atomicAdd(&s_hist[d][(k >> (8 * d)) & 255], 1u);
     }
+    if (v)
+      for (int d = 0; d < nd; ++d) atomicAdd(&s_hist[d][(k >> (8 * d)) & 255], 1u);
   }
   __syncthreads();
   for (int d = 0; d < nd; ++d) {
-    const unsigned v = s_hist[d][threadIdx.x];
-    if (v) atomicAdd(&ctl->hist[d][threadIdx.x], v);
+    const unsigned v = s_hist[d][t];
+    if (v) atomicAdd(&ctl->hist[d][t], v);
   }
-
 }
 
 // ---------------------------------------------------------- radix pass
 
+// Level-1 scan values of one request (record r), added to scan tile `tile`'s
+// totals in LDS (tile < 0: no request).  Lanes whose tile is the wave's first
+// lane's add wave sums with one atomic per value; the others add their own.
+__device__ __forceinline__ void l1_contrib(unsigned *s_l1, int tile, const int4 &r) {
+  const bool v = tile >= 0;
+  const bool rp = v && rec_state(r.w) == CASCADE_RUNNING_PREFILL;
+  const unsigned h = rp ? (unsigned)rec_held(r.w) : 0u;
+  unsigned c[kL1] = {v ? (unsigned)r.x : 0u, v ? (unsigned)r.y : 0u, h,
+                     rec_offl(r.w) ? h : 0u, rp ? 1u : 0u};
+  const int t0 = __builtin_amdgcn_readfirstlane(tile);
+  const bool same = tile == t0;
+  if (t0 >= 0) {
+#pragma unroll
+    for (int k = 0; k < kL1; ++k) {
+      const unsigned sum = wave_sum(same ? c[k] : 0u);
+      if (lane_id() == 0 && sum) atomicAdd(s_l1 + t0 * kL1 + k, sum);
+    }
+  }
+  if (v && !same) {
+#pragma unroll
+    for (int k = 0; k < kL1; ++k)
+      if (c[k]) atomicAdd(s_l1 + tile * kL1 + k, c[k]);
+  }
+}
+
 // The k-th data-moving LSD pass (kK), over the digit the sort plan names.
-// A tile of kSortTile keys is ranked per wave with ballots (lanes holding the
-// same digit find each other in 8 ballots), per-digit tile counts are
-// published for the decoupled look-back, keys are reordered in LDS and written
-// out in runs of equal digits.  The k-th pass reads buffer k & 1, so the tile's
-// keys are requested at once for tile = blockIdx.x, in parallel with the tile
-// claim and the plan; a workgroup that claims another tile reloads.
+// A tile of kSortTile keys: its digit counts (LDS) are published first, so
+// the look-back's first round trip runs while the keys are ranked per wave
+// with ballots (lanes holding the same digit find each other in 8 ballots).
+// Keys are then reordered in LDS and written out in runs of equal digits.
+// The last pass writes the sorted order with each request's scan record and
+// row offset (gathered while the tile is ranked) instead of the keys.  The
+// k-th pass reads buffer k & 1, so the tile's keys are requested at once for
+// tile = blockIdx.x, in parallel with the tile claim and the plan; a
+// workgroup that claims another tile reloads.
 template <int kK>
 __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
     int n, Ctl *ctl, int *info, unsigned long long *keys_a, unsigned long long *keys_b,
-    unsigned *vals_a, unsigned *vals_b, unsigned *status) {
+    unsigned *vals_a, unsigned *vals_b, unsigned *status, const int4 *__restrict__ rec,
+    const int *__restrict__ ro, Sorted srt, unsigned *__restrict__ l1_tot) {
   __shared__ unsigned long long s_keys[kSortTile];
   __shared__ unsigned s_vals[kSortTile];
+  __shared__ int4 s_rec[kSortTile];
+  __shared__ int s_ro[kSortTile];
   __shared__ unsigned s_wcnt[kWaves][kRadix];
   __shared__ int s_start[kRadix];
   __shared__ int s_off[kRadix];
   __shared__ int s_scan[kWaves * 2];
+  __shared__ unsigned s_l1[kMaxScanTiles * kL1];  // last pass: level-1 totals per scan tile
   __shared__ int s_tile, s_bad;
   __shared__ unsigned s_mask;
 
@@ -523,7 +595,7 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   unsigned long long *dst_k = (kK & 1) ? keys_a : keys_b;
   const unsigned *src_v = (kK & 1) ? vals_b : vals_a;
   unsigned *dst_v = (kK & 1) ? vals_a : vals_b;
-  const int lane = lane_id(), wave = wave_id();
+  const int t = threadIdx.x, lane = lane_id(), wave = wave_id();
   const int local = wave * 64 * kSortItems + lane;
 
   unsigned long long key[kSortItems];
@@ -540,18 +612,44 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   }
   unsigned hv[kMaxDigits];
 #pragma unroll
-  for (int d = 0; d < kMaxDigits; ++d) hv[d] = ctl->hist[d][threadIdx.x];
-  if (threadIdx.x == 0) {
+  for (int d = 0; d < kMaxDigits; ++d) hv[d] = ctl->hist[d][t];
+  if (t == 0) {
     // a claimed tile of a pass that turns out idle is never waited on
     s_tile = (int)atomicAdd(&ctl->tile_ctr[kK], 1u);
     s_bad = bad_status(load_agent(info));
     s_mask = 0;
   }
   const int nd = key_digits(ctl->bmin, ctl->bmax, ctl->cnt[1], ctl->cnt[2]);
-  for (int t = threadIdx.x; t < kWaves * kRadix; t += kBlock) (&s_wcnt[0][0])[t] = 0;
+  for (int k = t; k < kWaves * kRadix; k += kBlock) (&s_wcnt[0][0])[k] = 0;
   __syncthreads();
   const unsigned active = plan_mask(hv, n, nd, &s_mask);
-  if (s_bad || __builtin_popcount(active) <= kK) return;
+  const int nact = __builtin_popcount(active);
+  if (kK == 0 && blockIdx.x == 0 && t == 0) store_agent(&ctl->nact, (unsigned)nact);
+  if (s_bad) return;
+  if (kK == 0 && nact == 0) {
+    // every key equal: the order is the identity, sort tile j is scan tile j
+    static_assert(kSortTile == kScanTile, "one scan tile per sort tile");
+    const int p0 = (int)blockIdx.x * kScanTile;
+    unsigned c[kL1] = {0, 0, 0, 0, 0};
+    for (int p = p0 + t; p < min(n, p0 + kScanTile); p += kBlock) {
+      const int4 r = rec[p];
+      const bool rp = rec_state(r.w) == CASCADE_RUNNING_PREFILL;
+      const unsigned h = rp ? (unsigned)rec_held(r.w) : 0u;
+      c[0] += (unsigned)r.x;
+      c[1] += (unsigned)r.y;
+      c[2] += h;
+      c[3] += rec_offl(r.w) ? h : 0u;
+      c[4] += rp ? 1u : 0u;
+    }
+    block_sum<kL1>(c, &s_wcnt[0][0]);
+    if (t == 0) {
+#pragma unroll
+      for (int k = 0; k < kL1; ++k) l1_tot[(size_t)blockIdx.x * kL1 + k] = c[k];
+    }
+    return;
+  }
+  if (nact <= kK) return;
+  const bool last = nact == kK + 1;
   // this pass sorts by the kK-th data-moving digit
   unsigned rest = active;
 #pragma unroll
@@ -571,9 +669,26 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
     }
   }
   const int shift = 8 * digit;
+  bool broken = false;
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j)
     dig[j] = (tile_base + local + j * 64 < n) ? (int)((key[j] >> shift) & 255) : -1;
+  // the last pass carries each request's scan record and row offset along;
+  // the loads are unconditional (index 0 when not needed) so that nothing
+  // waits for them before the tile is ranked
+  int rx[kSortItems], ry[kSortItems], rz[kSortItems], rv[kSortItems], rw[kSortItems];
+#pragma unroll
+  for (int j = 0; j < kSortItems; ++j) {
+    const bool want = last && dig[j] >= 0;
+    broken |= want && val[j] >= (unsigned)n;
+    const unsigned gi = (want && val[j] < (unsigned)n) ? val[j] : 0u;
+    const int4 r = rec[gi];
+    rx[j] = r.x;
+    ry[j] = r.y;
+    rz[j] = r.z;
+    rv[j] = r.w;
+    rw[j] = ro[gi];
+  }
   // rank within the wave, item by item (local order: wave, item, lane)
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
@@ -596,8 +711,7 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   }
   __syncthreads();
 
-  // per-digit totals of the tile (thread t = digit t)
-  const int t = threadIdx.x;
+  // earlier waves' counts of digit t; the tile's count is published at once
   unsigned run = 0;
 #pragma unroll
   for (int w = 0; w < kWaves; ++w) {
@@ -607,122 +721,114 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   }
   const unsigned tile_count = run;
   unsigned *st = status + (size_t)tile * kRadix;
-  bool timed_out = false;
   publish<unsigned>(st + t, tile_count, tile == 0 ? kFlagInclusive : kFlagAggregate);
-
+  if (last) {
+    for (int k = t; k < kMaxScanTiles * kL1; k += kBlock) s_l1[k] = 0;
+  }
   // exclusive scans over digits: tile-local starts and global bucket bases
   int v2[2] = {(int)tile_count, (int)gcount};
   int tot2[2];
   block_exclusive_scan<2>(v2, tot2, s_scan);
   s_start[t] = v2[0];
+  // the earlier tiles' counts, kSortWin predecessors per round trip
+  bool timed_out = false;
   unsigned prefix = 0;
   if (tile > 0) {
-    prefix = look_back<unsigned, kSortWin>(status, kRadix, tile, t, &timed_out);
+    unsigned lbw[kSortWin];
+    int lb_next = tile - 1;
+    unsigned spins = 0;
+    for (;;) {
+#pragma unroll
+      for (int i = 0; i < kSortWin; ++i)
+        lbw[i] = lb_next - i >= 0 ? load_agent(status + (size_t)(lb_next - i) * kRadix + t)
+                                  : kFlagInclusive;
+      int consumed = 0;
+      bool done = false, stalled = false;
+#pragma unroll
+      for (int i = 0; i < kSortWin; ++i) {
+        if (!done && !stalled) {
+          const unsigned f = lbw[i] & 3u;
+          if (f == 0) {
+            stalled = true;
+          } else {
+            prefix += lbw[i] >> 2;
+            ++consumed;
+            done = f == kFlagInclusive;
+          }
+        }
+      }
+      if (done) break;
+      lb_next -= consumed;
+      if (stalled) {
+        if (++spins > kSpinLimit) {
+          timed_out = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
     publish<unsigned>(st + t, prefix + tile_count, kFlagInclusive);
   }
   if (timed_out) set_status(info, CASCADE_ETIMEOUT);
   s_off[t] = v2[1] + (int)prefix - v2[0];
   __syncthreads();
-
-  bool broken = false;
+  // reorder the tile in LDS by digit
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
-    if (dig[j] >= 0) {
-      const int pos = s_start[dig[j]] + (int)s_wcnt[wave][dig[j]] + rank[j];
-      if ((unsigned)pos < (unsigned)kSortTile) {
-        s_keys[pos] = key[j];
-        s_vals[pos] = val[j];
-      } else {
-        broken = true;
-      }
+    const bool v = dig[j] >= 0;
+    const int d = v ? dig[j] : 0;
+    const int pos = s_start[d] + (int)s_wcnt[wave][d] + rank[j];
+    const bool ok = v && (unsigned)pos < (unsigned)kSortTile;
+    broken |= v && !ok;
+    if (ok) {
+      s_keys[pos] = key[j];
+      s_vals[pos] = val[j];
+    }
+    if (ok && last) {
+      s_rec[pos] = make_int4(rx[j], ry[j], rz[j], rv[j]);
+      s_ro[pos] = rw[j];
     }
   }
   __syncthreads();
   const int count = min(kSortTile, n - tile_base);
-  for (int s = threadIdx.x; s < count; s += kBlock) {
-    const unsigned long long k = s_keys[s];
-    const int o = s_off[(k >> shift) & 255] + s;
-    if ((unsigned)o < (unsigned)n) {
+  static_assert(kSortTile % kBlock == 0, "every lane runs every iteration (wave sums below)");
+  for (int s = t; s < kSortTile; s += kBlock) {
+    int o = -1;
+    unsigned long long k = 0;
+    if (s < count) {
+      k = s_keys[s];
+      o = s_off[(k >> shift) & 255] + s;
+      if ((unsigned)o >= (unsigned)n) {
+        broken = true;
+        o = -1;
+      }
+    }
+    if (last) {
+      int4 r = make_int4(0, 0, 0, 0);
+      if (o >= 0) {
+        r = s_rec[s];
+        srt.order[o] = s_vals[s];
+        srt.rec[o] = r;
+        srt.ro[o] = s_ro[s];
+      }
+      l1_contrib(s_l1, o >= 0 ? o / kScanTile : -1, r);
+    } else if (o >= 0) {
       dst_k[o] = k;
       dst_v[o] = s_vals[s];
-    } else {
-      broken = true;
     }
   }
   if (broken) set_status(info, CASCADE_EINTERNAL);
+  if (last) {
+    __syncthreads();
+    const int n_tot = ((n + kScanTile - 1) / kScanTile) * kL1;
+    for (int k = t; k < n_tot; k += kBlock) {
+      const unsigned v = s_l1[k];
+      if (v) atomicAdd(l1_tot + k, v);
+    }
+  }
 }
 
 // ---------------------------------------------------------------- scan
-
-// Look-back of K values with a window of WIN predecessors per round trip;
-// the K*WIN window slots are spread over the workgroup (several per thread
-// when the window is wider than kBlock / K).  The sums land in s_sum[0..K).
-template <int K, int WIN>
-__device__ __forceinline__ void block_look_back(const unsigned long long *status, int stride,
-                                                int tile, long long *s_sum, int *s_base,
-                                                unsigned long long *s_w, int *s_left,
-                                                bool *timed_out) {
-  constexpr int kSlots = K * WIN;
-  constexpr int kPer = (kSlots + kBlock - 1) / kBlock;
-  const int t = threadIdx.x;
-  if (t < K) {
-    s_base[t] = tile - 1;
-    s_sum[t] = 0;
-  }
-  if (t == 0) *s_left = K;
-  __syncthreads();
-  unsigned spins = 0;
-  while (true) {
-    unsigned long long w[kPer];
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int slot = t + i * kBlock;
-      const int k = slot / WIN, j = slot - (slot / WIN) * WIN;
-      w[i] = 0;
-      if (slot < kSlots && s_base[k] >= 0) {
-        const int src = s_base[k] - j;
-        w[i] = src >= 0 ? load_agent(status + (size_t)src * stride + k)
-                        : (unsigned long long)kFlagInclusive;
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int slot = t + i * kBlock;
-      if (slot < kSlots) s_w[slot] = w[i];
-    }
-    __syncthreads();
-    bool stalled = false;
-    if (t < K && s_base[t] >= 0) {
-      long long sum = s_sum[t];
-      int consumed = 0;
-      bool done = false;
-      for (int jj = 0; jj < WIN && !done && !stalled; ++jj) {
-        const unsigned long long v = s_w[t * WIN + jj];
-        const unsigned f = (unsigned)(v & 3);
-        if (f == 0) {
-          stalled = true;
-        } else {
-          sum += (long long)(v >> 2);
-          ++consumed;
-          done = (f == kFlagInclusive);
-        }
-      }
-      s_sum[t] = sum;
-      s_base[t] = done ? -1 : s_base[t] - consumed;
-      if (done) atomicSub(s_left, 1);
-    }
-    __syncthreads();
-    if (*s_left == 0) break;
-    if (__syncthreads_or(stalled ? 1 : 0)) {
-      if (++spins > kSpinLimit) {
-        *timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-  __syncthreads();
-}
 
 // The victims, slot list and move lists, computed by the last scan workgroup
 // once every tile's totals and per-holder prefixes are in memory.
@@ -739,8 +845,8 @@ static_assert(kVictimCap == kBlock, "one staged victim per thread in the row-off
 struct FinishLds {
   long long tot[kWaves * 6];
   int v_req[kVictimCap], v_held[kVictimCap], v_row0[kVictimCap], v_start[kVictimCap];
+  int v_offl[kVictimCap];
   long long v_sbase[kVictimCap], v_pbase[kVictimCap];
-  int v_total;
   alignas(16) RestoreEnt rl[kRestoreCap];  // stored as int4
   int free_slots[kFreeCap];
   int tail[kTailCap];  // slot-list entries n_free + i: the victims' slots
@@ -748,16 +854,42 @@ struct FinishLds {
   int n_victims, counts[2];
 };
 
+// Last index i < n with key(i) <= x (index 0 when none), in a fixed number of
+// branch-free steps, so that a thread's independent searches overlap their
+// LDS latencies.  n <= 2^kSteps.
+template <int kSteps, typename KeyAt>
+__device__ __forceinline__ int last_at_or_below(int n, long long x, KeyAt key) {
+  int lo = 0;
+#pragma unroll
+  for (int step = 1 << (kSteps - 1); step > 0; step >>= 1) {
+    const int mid = lo + step;
+    lo = (mid < n && (long long)key(mid) <= x) ? mid : lo;
+  }
+  return lo;
+}
+constexpr int kRestoreSteps = 10;
+static_assert((1 << kRestoreSteps) == kRestoreCap, "restore searches cover the LDS copy");
+
 // Restore entry k, staged in LDS for k < kRestoreCap.
 __device__ __forceinline__ RestoreEnt restore_entry(const FinishLds &L, const RestoreEnt *rl,
                                                     int k) {
-  return k < kRestoreCap ? L.rl[k] : rl[k];
+  return k < kRestoreCap ? L.rl[k] : load_agent_rec(rl + k);
+}
+
+// The unpack move that writes slot-list entry s, or -1, for a restore list
+// that fits its LDS copy (nr <= kRestoreCap).
+__device__ __forceinline__ int unpack_move_at_lds(long long s, int nr, const FinishLds &L) {
+  if (nr <= 0 || L.rl[0].alloc_off > s) return -1;
+  const int lo = last_at_or_below<kRestoreSteps>(nr, s, [&](int k) { return L.rl[k].alloc_off; });
+  const RestoreEnt e = L.rl[lo];
+  return s < (long long)e.alloc_off + e.blocks ? e.stage_off + (int)(s - e.alloc_off) : -1;
 }
 
 // The unpack move that writes slot-list entry s, or -1: restore entries are
 // in admitted order, so their allocation offsets increase and the entry that
 // covers s is the last one starting at or before it.
-__device__ int unpack_move_at(long long s, int nr, const FinishLds &L, const RestoreEnt *rl) {
+__device__ __forceinline__ int unpack_move_at(long long s, int nr, const FinishLds &L,
+                                              const RestoreEnt *rl) {
   if (nr <= 0 || restore_entry(L, rl, 0).alloc_off > s) return -1;
   int lo = 0, hi = nr - 1;
   while (lo < hi) {
@@ -774,11 +906,16 @@ __device__ int unpack_move_at(long long s, int nr, const FinishLds &L, const Res
 // Every restore into a victim's slot gets its hazard entry here (-1 when
 // the victim is dropped); restores into free slots get theirs later, so no
 // hazard entry is written twice.
-__device__ void place_victim_block(int req, int b, int slot, long long sb, long long pb,
-                                   int n_free, int nr, const Outs &o, FinishLds &L,
-                                   const RestoreEnt *rl) {
+// kInTail: the entry lies in the LDS copy of the victims' region and the
+// restore list fits its LDS copy, so nothing is read from memory (a read
+// from memory would first wait for every store issued before it).
+template <bool kInTail>
+__device__ __forceinline__ void place_victim_block_at(int req, int b, int slot, long long sb,
+                                                      long long pb, int n_free, int nr,
+                                                      const Outs &o, FinishLds &L,
+                                                      const RestoreEnt *rl) {
   if (sb < o.sl_cap) o.slot_list[sb] = slot;
-  if (sb - n_free < kTailCap) L.tail[sb - n_free] = slot;
+  if (kInTail) L.tail[sb - n_free] = slot;
   const long long j = pb >= 0 ? pb + b : -1;
   const bool packed = j >= 0 && j < o.pack_cap;
   if (packed) {
@@ -790,9 +927,60 @@ __device__ void place_victim_block(int req, int b, int slot, long long sb, long 
     o.pack[j] = mv;
   }
   if (o.pack_hazard) {
-    const int m = unpack_move_at(sb, nr, L, rl);
+    const int m = kInTail ? unpack_move_at_lds(sb, nr, L) : unpack_move_at(sb, nr, L, rl);
     if (packed) o.pack_hazard[j] = m;
     if (m >= 0 && m < o.unpack_cap) o.unpack_hazard[m] = packed ? (int)j : -1;
+  }
+}
+__device__ __forceinline__ void place_victim_block(int req, int b, int slot, long long sb,
+                                                   long long pb, int n_free, int nr,
+                                                   const Outs &o, FinishLds &L,
+                                                   const RestoreEnt *rl) {
+  if (sb - n_free < kTailCap && nr <= kRestoreCap)
+    place_victim_block_at<true>(req, b, slot, sb, pb, n_free, nr, o, L, rl);
+  else
+    place_victim_block_at<false>(req, b, slot, sb, pb, n_free, nr, o, L, rl);
+}
+
+// Unpack move m of restore entry e; kLds: the pool slot it receives is in
+// the LDS copies of the free list and the victims' region.
+template <bool kLds>
+__device__ __forceinline__ void emit_restore_move(long long m, const RestoreEnt &e, int n_free,
+                                                  const int *__restrict__ free_slots,
+                                                  const Outs &o, const FinishLds &L) {
+  const int b = (int)(m - e.stage_off);
+  const long long s = (long long)e.alloc_off + b;
+  cascade_move_t mv;
+  mv.req = e.req;
+  mv.blk = b;
+  int ps;
+  if (s >= o.sl_cap) ps = -1;
+  else if (kLds) ps = s < n_free ? L.free_slots[s] : L.tail[s - n_free];
+  else if (s < n_free) ps = s < kFreeCap ? L.free_slots[s] : free_slots[s];
+  else ps = s - n_free < kTailCap ? L.tail[s - n_free] : o.slot_list[s];
+  mv.pool_slot = ps;
+  mv.staging_slot = (int)m;
+  o.unpack[m] = mv;
+  // a free slot is read by no pack move (victims' slots got theirs above)
+  if (o.unpack_hazard && s < n_free) o.unpack_hazard[m] = -1;
+}
+
+// Request the victims' row entries m = m0 + u*kBlock (u < kRowBatch): the
+// owning victim (search of the staged victims' row starts), block and slot.
+__device__ __forceinline__ void request_rows(int m0, int v_total, int nv,
+                                             const int *__restrict__ slots, const FinishLds &L,
+                                             int (&slot)[kRowBatch], int (&vi)[kRowBatch],
+                                             int (&bi)[kRowBatch]) {
+#pragma unroll
+  for (int u = 0; u < kRowBatch; ++u) {
+    const int m = m0 + u * kBlock;
+    vi[u] = -1;
+    if (m < v_total) {
+      const int lo = last_at_or_below<8>(nv, m, [&](int k) { return L.v_start[k]; });
+      vi[u] = lo;
+      bi[u] = m - L.v_start[lo];
+      slot[u] = slots[L.v_row0[lo] + bi[u]];
+    }
   }
 }
 
@@ -800,7 +988,7 @@ __device__ void place_victim_block(int req, int b, int slot, long long sb, long 
 // common case: the totals, running-prefill records, restore list and free
 // list together (each thread's share requested before any is stored), then
 // the victims' rows, up to kRowBatch per thread at once.
-__device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_tiles, int n_rp,
+__device__ __forceinline__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_tiles, int n_rp,
                             const TileTot *__restrict__ tiles, const int *__restrict__ free_slots,
                             const RpInfo *__restrict__ rp, const RestoreEnt *__restrict__ rl,
                             const int *__restrict__ slots, const Outs &o, FinishLds &L) {
@@ -809,23 +997,26 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
     L.n_victims = 0;
     L.counts[0] = L.counts[1] = 0;
   }
-  // first batch of the free list and the restore list, requested together
-  // with the tile totals below; the rest (long lists only) follows
-  constexpr int kStage = 2;
+  // every list the finish reads is requested at once: the free list and a
+  // bounded prefix of the restore list (tot[5] entries, not known yet, in a
+  // buffer of n), the tile totals, k* and the last kBlock running prefills
+  constexpr int kFreePer = kFreeCap / kBlock, kRestPer = kRestoreCap / kBlock;
   const int n_fs = min(n_free, kFreeCap), n_rs = min(n, kRestoreCap);
-  static_assert(sizeof(RestoreEnt) == sizeof(int4), "restore entries move as int4");
-  const int4 *rl4 = reinterpret_cast<const int4 *>(rl);
-  int fv[kStage];
-  int4 rv[kStage];
+  int fv[kFreePer];
+  RestoreEnt rv[kRestPer];
 #pragma unroll
-  for (int u = 0; u < kStage; ++u) {
+  for (int u = 0; u < kFreePer; ++u) {
     const int j = t + u * kBlock;
     fv[u] = j < n_fs ? free_slots[j] : 0;
-    rv[u] = j < n_rs ? rl4[j] : make_int4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int u = 0; u < kRestPer; ++u) {
+    const int j = t + u * kBlock;
+    rv[u] = j < n_rs ? load_agent_rec(rl + j) : RestoreEnt{0, 0, 0, 0};
   }
   long long tot[6] = {0, 0, 0, 0, 0, 0};
   for (int j = t; j < n_tiles; j += kBlock) {
-    const TileTot tt = tiles[j];
+    const TileTot tt = load_agent_rec(tiles + j);
     tot[0] += tt.adm_nb;
     tot[1] += tt.elig_h;
     tot[2] += tt.elig_offl_h;
@@ -833,43 +1024,50 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
     tot[4] += tt.n_unpack;
     tot[5] += tt.n_restore;
   }
-  RpInfo mine = {};
-  const bool has_rp = t < n_rp;
-  if (has_rp) mine = rp[t];
+  const int kstar = load_agent(&ctl->kstar);
+  const long long kx = load_agent(&ctl->kx), ky = load_agent(&ctl->ky),
+                  kz = load_agent(&ctl->kz), kzp = load_agent(&ctl->kzp);
+  // running prefills from the back of the order: thread t holds entry top-1-t
+  int top = n_rp;
+  RpInfo ri = {};
+  if (top - 1 - t >= 0) ri = load_agent_rec(rp + (top - 1 - t));
+  const int lim = min(n_free, o.sl_cap);
 #pragma unroll
-  for (int u = 0; u < kStage; ++u) {
+  for (int u = 0; u < kFreePer; ++u) {
     const int j = t + u * kBlock;
     if (j < n_fs) L.free_slots[j] = fv[u];
-    if (j < n_rs) reinterpret_cast<int4 *>(L.rl)[j] = rv[u];
   }
-  for (int j = t + kStage * kBlock; j < n_fs; j += kBlock) L.free_slots[j] = free_slots[j];
-  // the restore list holds tot[5] entries (not known yet) in a buffer of n;
-  // stage a bounded prefix now, use only its valid part below
-  for (int j = t + kStage * kBlock; j < n_rs; j += kBlock) L.rl[j] = rl[j];
-  const int kstar = ctl->kstar;
-  const long long kx = ctl->kx, ky = ctl->ky, kz = ctl->kz, kzp = ctl->kzp;
+#pragma unroll
+  for (int u = 0; u < kRestPer; ++u) {
+    const int j = t + u * kBlock;
+    if (j < n_rs) L.rl[j] = rv[u];
+  }
   block_sum<6>(tot, L.tot);  // waits for the loads above
   const long long D = tot[0] - n_free, E = tot[1], EO = tot[2];
   const long long nu = tot[4];
   const int nr = (int)tot[5];
-  const int lim = min(n_free, o.sl_cap);
-  for (int j = t; j < lim; j += kBlock)
-    o.slot_list[j] = j < kFreeCap ? L.free_slots[j] : free_slots[j];
 
-  // victims: every thread tests one running prefill at a time
-  if (D > 0) {
-    for (int e = t; e < n_rp; e += kBlock) {
-      const RpInfo ri = e == t ? mine : rp[e];
-      if (!ri.eligible) continue;
+  // victims: the eligible holders whose eligible blocks behind them are
+  // fewer than D.  That count only grows towards the front of the order, so
+  // they are the last ones: windows of kBlock entries are taken from the
+  // back until one holds an eligible entry that is not a victim.
+  while (D > 0 && top > 0) {
+    const int e = top - 1 - t;
+    if (top != n_rp && e >= 0) ri = load_agent_rec(rp + e);
+    bool kept = false;
+    do {
+      if (e < 0 || !ri.eligible) break;
       const long long eh = ri.pos < kstar ? ri.x : kx + ri.y - ky;
       const long long after = E - eh;  // eligible blocks behind this request
-      if (after >= D) continue;
+      if (after >= D) {
+        kept = true;
+        break;
+      }
       if (after < 0) {
         set_status(info, CASCADE_EINTERNAL);
-        continue;
+        break;
       }
       const int i = ri.req, h = ri.held;
-      o.action[i] = ri.offl ? CASCADE_ACT_PREEMPT_OFFLOAD : CASCADE_ACT_PREEMPT_DROP;
       atomicAdd(&L.counts[0], h);
       if (ri.offl) atomicAdd(&L.counts[1], h);
       const long long sbase = (long long)n_free + after;
@@ -877,44 +1075,36 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
       const int v = atomicAdd(&L.n_victims, 1);
       if (v < kVictimCap) {
         L.v_req[v] = i;
+        L.v_offl[v] = ri.offl;
         L.v_held[v] = h;
         L.v_row0[v] = ri.row0;
         L.v_sbase[v] = sbase;
         L.v_pbase[v] = pbase;
       } else {  // more victims than LDS holds: place this one alone
+        store_agent(&o.action[i], (uint8_t)(ri.offl ? CASCADE_ACT_PREEMPT_OFFLOAD
+                                                    : CASCADE_ACT_PREEMPT_DROP));
         for (int b = 0; b < h; ++b)
           place_victim_block(i, b, slots[ri.row0 + b], sbase + b, pbase, n_free, nr, o, L, rl);
       }
-    }
+    } while (false);
+    if (__syncthreads_or(kept ? 1 : 0)) break;  // every earlier holder is kept too
+    top -= kBlock;
   }
   __syncthreads();
   // the staged victims' rows as one flat index space (prefix of row lengths),
   // so every row load of every victim is in flight at once
   const int nv = min(L.n_victims, kVictimCap);
+  int v_total;
   {
     int hv[1] = {t < nv ? L.v_held[t] : 0}, tot1[1];
     block_exclusive_scan<1>(hv, tot1, L.scan_tmp);  // kVictimCap == kBlock
     if (t < nv) L.v_start[t] = hv[0];
-    if (t == 0) L.v_total = tot1[0];
+    v_total = tot1[0];
   }
   __syncthreads();
-  for (int m0 = t; m0 < L.v_total; m0 += kRowBatch * kBlock) {
-    int slot[kRowBatch], vi[kRowBatch], bi[kRowBatch];
-#pragma unroll
-    for (int u = 0; u < kRowBatch; ++u) {
-      const int m = m0 + u * kBlock;
-      vi[u] = -1;
-      if (m < L.v_total) {
-        int lo = 0, hi = nv - 1;
-        while (lo < hi) {
-          const int mid = (lo + hi + 1) >> 1;
-          if (L.v_start[mid] <= m) lo = mid; else hi = mid - 1;
-        }
-        vi[u] = lo;
-        bi[u] = m - L.v_start[lo];
-        slot[u] = slots[L.v_row0[lo] + bi[u]];
-      }
-    }
+  int slot[kRowBatch], vi[kRowBatch], bi[kRowBatch];
+  request_rows(t, v_total, nv, slots, L, slot, vi, bi);
+  for (int m0 = t;;) {
 #pragma unroll
     for (int u = 0; u < kRowBatch; ++u) {
       if (vi[u] < 0) continue;
@@ -922,33 +1112,40 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
       place_victim_block(L.v_req[v], bi[u], slot[u], L.v_sbase[v] + bi[u], L.v_pbase[v], n_free,
                          nr, o, L, rl);
     }
+    m0 += kRowBatch * kBlock;
+    if (m0 >= v_total) break;
+    request_rows(m0, v_total, nv, slots, L, slot, vi, bi);
   }
+  // stores that waited for every load above: the staged victims' actions
+  // (replacing the RETAIN their scan tiles stored before their tickets) and
+  // the free-list part of the slot list
+  if (t < nv)
+    store_agent(&o.action[L.v_req[t]], (uint8_t)(L.v_offl[t] ? CASCADE_ACT_PREEMPT_OFFLOAD
+                                                             : CASCADE_ACT_PREEMPT_DROP));
+  for (int j = t; j < lim; j += kBlock)
+    o.slot_list[j] = j < kFreeCap ? L.free_slots[j] : free_slots[j];
   __syncthreads();  // the slot list is complete (this workgroup wrote it)
   // restore moves: the first r new blocks of each RESTORE request, staged in
-  // admitted order; move m finds its request by binary search
+  // admitted order; move m finds its request by a search of the staged list
   const long long mlim = lmin(nu, (long long)o.unpack_cap);
   for (long long m = t; m < mlim; m += kBlock) {
+    if (nr <= kRestoreCap) {
+      const int lo =
+          last_at_or_below<kRestoreSteps>(nr, m, [&](int k) { return L.rl[k].stage_off; });
+      const RestoreEnt e = L.rl[lo];
+      const long long s = (long long)e.alloc_off + (m - e.stage_off);
+      if (s < min(n_free, kFreeCap) || (s >= n_free && s - n_free < kTailCap)) {
+        emit_restore_move<true>(m, e, n_free, free_slots, o, L);
+        continue;
+      }
+    }
     int lo = 0, hi = nr - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
-      const int off = mid < kRestoreCap ? L.rl[mid].stage_off : rl[mid].stage_off;
+      const int off = restore_entry(L, rl, mid).stage_off;
       if (off <= m) lo = mid; else hi = mid - 1;
     }
-    const RestoreEnt e = lo < kRestoreCap ? L.rl[lo] : rl[lo];
-    const int b = (int)(m - e.stage_off);
-    const long long s = (long long)e.alloc_off + b;
-    cascade_move_t mv;
-    mv.req = e.req;
-    mv.blk = b;
-    int ps;
-    if (s >= o.sl_cap) ps = -1;
-    else if (s < n_free) ps = s < kFreeCap ? L.free_slots[s] : free_slots[s];
-    else ps = s - n_free < kTailCap ? L.tail[s - n_free] : o.slot_list[s];
-    mv.pool_slot = ps;
-    mv.staging_slot = (int)m;
-    o.unpack[m] = mv;
-    // a free slot is read by no pack move (victims' slots got theirs above)
-    if (o.unpack_hazard && s < n_free) o.unpack_hazard[m] = -1;
+    emit_restore_move<false>(m, restore_entry(L, rl, lo), n_free, free_slots, o, L);
   }
   if (t == 0) {
     const long long nsl = (long long)n_free + L.counts[0];
@@ -965,18 +1162,41 @@ __device__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_
 // each position's request index (idx < 0: past the end), record and block-
 // table row offset (gathered with the record by the caller); thread
 // t holds positions t*jn .. t*jn + jn - 1 of the tile (jn <= kScanItems).  With
-// kChained the tile's level-1 and level-2 prefixes come from the decoupled
-// look-back over the tiles before it; without, the tile is the whole queue.
-// Writes every per-request output of the tile, k*, the running-prefill and
-// restore-list entries and the tile's totals; returns the number of running
-// prefills up to and including this tile.
+// kChained the tile's level-1 and level-2 prefixes pre1 and pre2 are the
+// earlier tiles' totals; without, the tile is the whole queue (both zero).
+// Writes what the finishing workgroup reads (k*, the running-prefill and
+// restore-list entries, the running prefills' actions and the tile's totals)
+// with agent-scope stores, and leaves every other per-request output in `out`
+// for write_tile_outputs; returns the number of running prefills up to and
+// including this tile.
 struct ScanLds {
   long long scan[kWaves * kL2];
-  long long sum[kL2Stride];
-  int base[kL2Stride];
-  unsigned long long w[kBlock];
-  int left;
+  long long red[kWaves * (kL1 + kL2)];
 };
+
+// Per-request outputs of one thread's positions, stored after the hand-over.
+struct TileOut {
+  int req[kScanItems];      // request index, -1: no position
+  int granted[kScanItems], restore[kScanItems], alloc_begin[kScanItems], alloc_count[kScanItems];
+  int admitted_at[kScanItems];  // index in the admitted list, -1: not admitted
+  int action[kScanItems];       // -1: a running prefill (stored before the hand-over)
+  int p0;
+};
+
+__device__ __forceinline__ void write_tile_outputs(const TileOut &out, const Outs &o) {
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    const int i = out.req[j];
+    if (i < 0) continue;
+    o.order[out.p0 + j] = i;
+    o.granted[i] = out.granted[j];
+    o.restore[i] = out.restore[j];
+    o.alloc_begin[i] = out.alloc_begin[j];
+    o.alloc_count[i] = out.alloc_count[j];
+    if (out.action[j] >= 0) o.action[i] = (uint8_t)out.action[j];
+    if (out.admitted_at[j] >= 0) o.admitted[out.admitted_at[j]] = i;
+  }
+}
 
 struct ScanConsts {
   long long bt, U, e1, cap, cap1, p_e1, g1, fh;
@@ -996,16 +1216,24 @@ __device__ __forceinline__ ScanConsts scan_consts(const Consts &c, const Ctl *ct
   return k;
 }
 
-template <bool kChained>
-__device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, int *info,
-                               const int (&idx)[kScanItems], const int4 (&r4)[kScanItems],
-                               const int (&row0)[kScanItems], bool broken, const Outs &o,
-                               RpInfo *__restrict__ rp_list,
-                               RestoreEnt *__restrict__ restore_list,
-                               TileTot *__restrict__ tile_tot, unsigned long long *status1,
-                               unsigned long long *status2, ScanLds &S) {
+// Level-1 scan of one tile and every position's restore blocks, grant, new
+// blocks and level-2 values (this thread's partial sums in v.l2), given the
+// tile's level-1 prefix pre1.
+struct PosVals {
+  int r[kScanItems], g[kScanItems], nb[kScanItems], hh[kScanItems];
+  long long y_inc[kScanItems], zp_inc[kScanItems];
+  long long l2[kL2];
+  long long rp_incl;  // running prefills up to and including this tile
+  int rp_at;          // compact-list index of this thread's first running prefill
+};
+
+__device__ __forceinline__ void scan_positions(int tile, int jn, const ScanConsts &K,
+                                               const int (&idx)[kScanItems],
+                                               const int4 (&r4)[kScanItems],
+                                               const long long (&pre1)[kL1], ScanLds &S,
+                                               PosVals &v) {
   const long long bt = K.bt, U = K.U, e1 = K.e1, cap = K.cap, cap1 = K.cap1, p_e1 = K.p_e1,
-                  g1 = K.g1, fh = K.fh;
+                  g1 = K.g1;
   const int p0 = tile * kScanTile + threadIdx.x * jn;  // items j < jn; the rest absent
   // ---- level 1
   long long l1[kL1] = {0, 0, 0, 0, 0}, t1[kL1];
@@ -1021,34 +1249,16 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
     l1[4] += rp ? 1 : 0;          // running prefills (their compact list)
   }
   block_exclusive_scan<kL1>(l1, t1, S.scan);
-  bool timed_out = false;
-  if (kChained && threadIdx.x < kL1)
-    publish<unsigned long long>(status1 + (size_t)tile * kL1 + threadIdx.x,
-                                (unsigned long long)t1[threadIdx.x],
-                                tile == 0 ? kFlagInclusive : kFlagAggregate);
-  if (kChained && tile > 0) {
-    block_look_back<kL1, kBlock / kL1>(status1, kL1, tile, S.sum, S.base, S.w, &S.left,
-                                   &timed_out);
-    if (threadIdx.x < kL1)
-      publish<unsigned long long>(status1 + (size_t)tile * kL1 + threadIdx.x,
-                                  (unsigned long long)(S.sum[threadIdx.x] + t1[threadIdx.x]),
-                                  kFlagInclusive);
-  } else {
-    if (threadIdx.x < kL2Stride) S.sum[threadIdx.x] = 0;
-    __syncthreads();
-  }
-  long long wx = S.sum[0] + l1[0], bn = S.sum[1] + l1[1], yy = S.sum[2] + l1[2],
-            zz = S.sum[3] + l1[3];
-  int rp_at = (int)(S.sum[4] + l1[4]);
-  const long long rp_incl = S.sum[4] + t1[4];  // running prefills up to this tile
-  __syncthreads();
+  long long wx = pre1[0] + l1[0], bn = pre1[1] + l1[1], yy = pre1[2] + l1[2],
+            zz = pre1[3] + l1[3];
+  v.rp_at = (int)(pre1[4] + l1[4]);
+  v.rp_incl = pre1[4] + t1[4];
 
   // ---- per position: restore blocks, need, grant, new blocks
   // per item: restore blocks (<= want), grant (<= token cap), new blocks and
   // held blocks (< 2^20) all fit 32 bits; prefix sums stay 64-bit
-  int r[kScanItems], g[kScanItems], nb[kScanItems], hh[kScanItems];
-  long long y_inc[kScanItems], zp_inc[kScanItems];
-  long long l2[kL2] = {0, 0, 0, 0, 0, 0, 0}, t2[kL2];
+#pragma unroll
+  for (int k = 0; k < kL2; ++k) v.l2[k] = 0;
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     const int w = r4[j].w;
@@ -1083,50 +1293,58 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
         nbj = rec_decnb(w);
       }
     }
-    r[j] = (int)rj;
-    g[j] = (int)gj;
-    nb[j] = (int)nbj;
-    hh[j] = (int)h;
+    v.r[j] = (int)rj;
+    v.g[j] = (int)gj;
+    v.nb[j] = (int)nbj;
+    v.hh[j] = (int)h;
     wx += want;
     bn += r4[j].y;
     yy += h;
     zz += rec_offl(w) ? h : 0;
-    y_inc[j] = yy;
-    zp_inc[j] = zz;
+    v.y_inc[j] = yy;
+    v.zp_inc[j] = zz;
     const bool gp = gj > 0;
-    l2[0] += gp ? nbj + h : 0;              // admission weight
-    l2[1] += gp ? nbj : 0;                  // new blocks
-    l2[2] += gp ? 1 : 0;                    // admitted count
-    l2[3] += gp ? 0 : h;                    // held, not granted
-    l2[4] += (gp || !rec_offl(w)) ? 0 : h;  // held, not granted, spill fits
-    l2[5] += gp ? rj : 0;                   // restored blocks
-    l2[6] += (gp && rj > 0) ? 1 : 0;        // restoring requests
+    v.l2[0] += gp ? nbj + h : 0;              // admission weight
+    v.l2[1] += gp ? nbj : 0;                  // new blocks
+    v.l2[2] += gp ? 1 : 0;                    // admitted count
+    v.l2[3] += gp ? 0 : h;                    // held, not granted
+    v.l2[4] += (gp || !rec_offl(w)) ? 0 : h;  // held, not granted, spill fits
+    v.l2[5] += gp ? rj : 0;                   // restored blocks
+    v.l2[6] += (gp && rj > 0) ? 1 : 0;        // restoring requests
   }
+}
 
-  // ---- level 2
+template <bool kChained>
+__device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, int *info,
+                               const int (&idx)[kScanItems], const int4 (&r4)[kScanItems],
+                               const int (&row0)[kScanItems], bool broken, const Outs &o,
+                               RpInfo *__restrict__ rp_list,
+                               RestoreEnt *__restrict__ restore_list,
+                               TileTot *__restrict__ tile_tot, const long long (&pre1)[kL1],
+                               const long long (&pre2)[kL2], ScanLds &S, TileOut &out) {
+  const long long fh = K.fh;
+  const int p0 = tile * kScanTile + threadIdx.x * jn;
+  PosVals v;
+  scan_positions(tile, jn, K, idx, r4, pre1, S, v);
+  int rp_at = v.rp_at;
+  const long long rp_incl = v.rp_incl;
+  long long l2[kL2], t2[kL2];
+#pragma unroll
+  for (int k = 0; k < kL2; ++k) l2[k] = v.l2[k];
+  const int *r = v.r, *g = v.g, *nb = v.nb, *hh = v.hh;
+  const long long *y_inc = v.y_inc, *zp_inc = v.zp_inc;
+
+  // ---- level 2: the earlier tiles' totals (scan_reduce) plus this tile's
   block_exclusive_scan<kL2>(l2, t2, S.scan);
-  unsigned long long *st2 = status2 + (size_t)tile * kL2Stride;
-  if (kChained && threadIdx.x < kL2)
-    publish<unsigned long long>(st2 + threadIdx.x, (unsigned long long)t2[threadIdx.x],
-                                tile == 0 ? kFlagInclusive : kFlagAggregate);
-  if (kChained && tile > 0) {
-    block_look_back<kL2, kBlock / kL2>(status2, kL2Stride, tile, S.sum, S.base, S.w, &S.left,
-                                   &timed_out);
-    if (threadIdx.x < kL2)
-      publish<unsigned long long>(st2 + threadIdx.x,
-                                  (unsigned long long)(S.sum[threadIdx.x] + t2[threadIdx.x]),
-                                  kFlagInclusive);
-  } else {
-    if (threadIdx.x < kL2Stride) S.sum[threadIdx.x] = 0;
-    __syncthreads();
-  }
-  long long W = S.sum[0] + l2[0], NB = S.sum[1] + l2[1], AC = S.sum[2] + l2[2],
-            X = S.sum[3] + l2[3], Z = S.sum[4] + l2[4], RR = S.sum[5] + l2[5],
-            RC = S.sum[6] + l2[6];
+  long long W = pre2[0] + l2[0], NB = pre2[1] + l2[1], AC = pre2[2] + l2[2],
+            X = pre2[3] + l2[3], Z = pre2[4] + l2[4], RR = pre2[5] + l2[5],
+            RC = pre2[6] + l2[6];
 
   long long a_nb = 0, a_eh = 0, a_eoh = 0, a_n = 0, a_r = 0, a_rc = 0;
+  out.p0 = p0;
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
+    out.req[j] = idx[j];
     if (idx[j] < 0) continue;
     const int i = idx[j];
     const int p = p0 + j;
@@ -1137,17 +1355,17 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
     const bool adm = gp && (W + wj <= fh);
     if (W <= fh && W + wj > fh) {
       // the first request that does not fit: everything after it waits
-      ctl->kstar = p;
-      ctl->kx = X;
-      ctl->ky = y_inc[j] - hh[j];
-      ctl->kz = Z;
-      ctl->kzp = zp_inc[j] - (rec_offl(w) ? hh[j] : 0);
+      store_agent(&ctl->kstar, p);
+      store_agent(&ctl->kx, X);
+      store_agent(&ctl->ky, y_inc[j] - hh[j]);
+      store_agent(&ctl->kz, Z);
+      store_agent(&ctl->kzp, zp_inc[j] - (rec_offl(w) ? hh[j] : 0));
     }
-    o.order[p] = i;
-    o.granted[i] = adm ? (int)g[j] : 0;
-    o.restore[i] = (int)r[j];
-    o.alloc_begin[i] = adm ? (int)NB : -1;
-    o.alloc_count[i] = adm ? (int)nb[j] : 0;
+    out.granted[j] = adm ? (int)g[j] : 0;
+    out.restore[j] = (int)r[j];
+    out.alloc_begin[j] = adm ? (int)NB : -1;
+    out.alloc_count[j] = adm ? (int)nb[j] : 0;
+    out.admitted_at[j] = adm ? (int)AC : -1;
     int act;
     if (st != CASCADE_QUEUED) {
       act = CASCADE_ACT_RETAIN;  // a preempted running prefill is rewritten later
@@ -1157,9 +1375,14 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
       else if (tier == CASCADE_KV_NONE || r[j] == 0) act = CASCADE_ACT_RECOMPUTE;
       else act = adm ? CASCADE_ACT_RESTORE : CASCADE_ACT_PREFETCH;
     }
-    o.action[i] = (uint8_t)act;
+    if (st == CASCADE_RUNNING_PREFILL) {
+      // the finishing workgroup rewrites a preempted one: store it now
+      store_agent(&o.action[i], (uint8_t)act);
+      out.action[j] = -1;
+    } else {
+      out.action[j] = act;
+    }
     if (adm) {
-      o.admitted[AC] = i;
       a_nb += nb[j];
       a_n += 1;
       if (r[j] > 0) {
@@ -1168,7 +1391,7 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
         e.stage_off = (int)RR;
         e.alloc_off = (int)NB;
         e.blocks = (int)r[j];
-        restore_list[RC] = e;
+        store_agent_rec(restore_list + RC, e);
         a_r += r[j];
         a_rc += 1;
       }
@@ -1188,7 +1411,8 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
       ri.y = y_inc[j];
       ri.z = Z + zj;
       ri.zp = zp_inc[j];
-      rp_list[rp_at++] = ri;
+      store_agent_rec(rp_list + rp_at, ri);
+      ++rp_at;
       if (!adm) {
         a_eh += hh[j];
         a_eoh += rec_offl(w) ? hh[j] : 0;
@@ -1202,8 +1426,8 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
     RR += gp ? r[j] : 0;
     RC += (gp && r[j] > 0) ? 1 : 0;
   }
-  long long tot[8] = {a_nb, a_eh, a_eoh, a_n, a_r, a_rc, timed_out ? 1 : 0, broken ? 1 : 0};
-  block_sum<8>(tot, reinterpret_cast<long long *>(S.w));
+  long long tot[8] = {a_nb, a_eh, a_eoh, a_n, a_r, a_rc, 0, broken ? 1 : 0};
+  block_sum<8>(tot, S.red);
   if (threadIdx.x == 0) {
     TileTot tt;
     tt.adm_nb = tot[0];
@@ -1213,8 +1437,7 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
     tt.n_unpack = tot[4];
     tt.n_restore = tot[5];
     tt.pad[0] = tt.pad[1] = 0;
-    tile_tot[tile] = tt;
-    if (tot[6]) set_status(info, CASCADE_ETIMEOUT);
+    store_agent_rec(tile_tot + tile, tt);
     if (tot[7]) set_status(info, CASCADE_EINTERNAL);
   }
   return rp_incl;
@@ -1229,79 +1452,460 @@ __device__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, 
 // of admitted requests, admitted count, held blocks of running prefills left
 // out (all / spill-fits), restored blocks and restoring requests.
 // Both levels use one decoupled look-back each, chained inside the launch.
-__global__ __launch_bounds__(kBlock) void scan_kernel(
-    int n, int passes, Consts c, Ctl *ctl, int *info, const unsigned *vals_a,
-    const unsigned *vals_b, const int4 *__restrict__ rec, const int *__restrict__ ro,
-    const int *__restrict__ slots, const int *__restrict__ free_slots, Outs o,
-    RpInfo *__restrict__ rp_list, RestoreEnt *__restrict__ restore_list,
-    TileTot *__restrict__ tile_tot, unsigned long long *status1, unsigned long long *status2) {
-  __shared__ ScanLds s_lds;
-  __shared__ int s_tile, s_bad, s_last;
-  __shared__ unsigned s_mask;
-  __shared__ FinishLds s_fin;
-
-  // the tile's order entries are requested from both ping-pong buffers at once
-  // (which one holds the result is known only from the plan)
-  const int p0g = (int)blockIdx.x * kScanTile + threadIdx.x * kScanItems;
-  unsigned oa[kScanItems], ob[kScanItems];
+// The sorted order, records and row offsets come from the last radix pass
+// (the identity order when every key is equal), so one coalesced read feeds
+// the tile.  Each tile hands its results to the finishing workgroup with
+// agent-scope stores and a ticket, then writes its other outputs.
+// Sums over tiles j < tile of both levels' per-tile totals (l1[j*kL1 + k],
+// l2[j*kL2Stride + k]), over the workgroup.  Up to 2*kBlock tiles of both
+// are requested at once (one round trip); an earlier launch wrote them, so
+// nothing is polled.  l2 may be null (level 1 only).
+__device__ __forceinline__ void earlier_totals(const unsigned *__restrict__ l1,
+                                               const long long *__restrict__ l2, int tile,
+                                               long long (&pre1)[kL1], long long (&pre2)[kL2],
+                                               long long *s_red) {
+  constexpr int kPer = 2, K = kL1 + kL2;
+  long long v[K];
 #pragma unroll
-  for (int j = 0; j < kScanItems; ++j) {
-    oa[j] = p0g + j < n ? vals_a[p0g + j] : 0u;
-    ob[j] = p0g + j < n ? vals_b[p0g + j] : 0u;
-  }
-  unsigned hv[kMaxDigits];
+  for (int k = 0; k < K; ++k) v[k] = 0;
+  for (int b0 = 0; b0 < tile; b0 += kPer * kBlock) {
+    unsigned w1[kPer][kL1];
+    long long w2[kPer][kL2];
 #pragma unroll
-  for (int d = 0; d < kMaxDigits; ++d) hv[d] = ctl->hist[d][threadIdx.x];
-  if (threadIdx.x == 0) {
-    s_tile = (int)atomicAdd(&ctl->tile_ctr[kMaxDigits], 1u);
-    s_bad = bad_status(load_agent(info));
-    s_mask = 0;
+    for (int u = 0; u < kPer; ++u) {
+      const int j = b0 + u * kBlock + (int)threadIdx.x;
+      const bool in = j < tile;
+#pragma unroll
+      for (int k = 0; k < kL1; ++k) w1[u][k] = in ? l1[(size_t)j * kL1 + k] : 0u;
+#pragma unroll
+      for (int k = 0; k < kL2; ++k) w2[u][k] = (in && l2) ? l2[(size_t)j * kL2Stride + k] : 0ll;
+    }
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+#pragma unroll
+      for (int k = 0; k < kL1; ++k) v[k] += (long long)w1[u][k];
+#pragma unroll
+      for (int k = 0; k < kL2; ++k) v[kL1 + k] += w2[u][k];
+    }
   }
-  const int nd = key_digits(ctl->bmin, ctl->bmax, ctl->cnt[1], ctl->cnt[2]);
-  __syncthreads();
-  const int nact = __builtin_popcount(plan_mask(hv, n, nd, &s_mask));
-  if (s_bad) return;
-  const int tile = s_tile;
-  // a live digit beyond the launched passes would leave the keys unsorted
-  bool broken = nact > passes;
-  const unsigned *sorted = (nact & 1) ? vals_b : vals_a;
-  const ScanConsts K = scan_consts(c, ctl);
+  block_sum<K>(v, s_red);
+#pragma unroll
+  for (int k = 0; k < kL1; ++k) pre1[k] = v[k];
+#pragma unroll
+  for (int k = 0; k < kL2; ++k) pre2[k] = v[kL1 + k];
+}
 
-  const int p0 = tile * kScanTile + threadIdx.x * kScanItems;
-  int idx[kScanItems], rw[kScanItems];
-  int4 r4[kScanItems];
+// The tile's positions in priority order: request index, scan record and
+// row offset, from the last radix pass (sorted buffers) or, when every key
+// is equal (no pass moved data), the identity order.  Positions past n get
+// index -1.  `broken` is set on an index out of range.
+__device__ __forceinline__ void tile_positions(int n, int tile, int nact, const Sorted &srt,
+                                               const int4 *__restrict__ rec,
+                                               const int *__restrict__ ro,
+                                               const unsigned (&so)[kScanItems],
+                                               const int4 (&sr)[kScanItems],
+                                               const int (&sw)[kScanItems],
+                                               int (&idx)[kScanItems], int4 (&r4)[kScanItems],
+                                               int (&rw)[kScanItems], bool &broken) {
+  const int p0 = tile * kScanTile + (int)threadIdx.x * kScanItems;
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     const int p = p0 + j;
     int ix = -1;
-    if (p < n) ix = (int)(tile == (int)blockIdx.x ? ((nact & 1) ? ob[j] : oa[j]) : sorted[p]);
-    if (ix >= n) {  // cannot happen with a correct sort; never read out of range
-      broken = true;
+    int4 r = make_int4(0, 0, 0, 0);
+    int w = 0;
+    if (p < n) {
+      if (nact == 0) {
+        ix = p;
+        r = rec[p];
+        w = ro[p];
+      } else {
+        ix = (int)so[j];
+        r = sr[j];
+        w = sw[j];
+      }
+    }
+    if ((unsigned)ix >= (unsigned)n) {  // cannot happen with a correct sort
+      broken = broken || ix != -1;
       ix = -1;
     }
     idx[j] = ix;
-    r4[j] = ix >= 0 ? rec[ix] : make_int4(0, 0, 0, 0);
-    rw[j] = ix >= 0 ? ro[ix] : 0;
+    r4[j] = ix >= 0 ? r : make_int4(0, 0, 0, 0);
+    rw[j] = ix >= 0 ? w : 0;
   }
+}
 
-  scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, rw, broken, o, rp_list, restore_list,
-                  tile_tot, status1, status2, s_lds);
-  if (threadIdx.x == 0) {
-    // release this tile's writes, then count it; the last tile finishes the step
-    __threadfence();
-    s_last = (atomicAdd(&ctl->scan_done, 1u) == gridDim.x - 1);
+// The sorted entries of the tile's positions (blockIdx.x), requested before
+// anything else.
+__device__ __forceinline__ void load_sorted(int n, const Sorted &srt, unsigned (&so)[kScanItems],
+                                            int4 (&sr)[kScanItems], int (&sw)[kScanItems]) {
+  const int p0 = (int)blockIdx.x * kScanTile + (int)threadIdx.x * kScanItems;
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    const int p = p0 + j;
+    so[j] = p < n ? srt.order[p] : 0u;
+    sr[j] = p < n ? srt.rec[p] : make_int4(0, 0, 0, 0);
+    sw[j] = p < n ? srt.ro[p] : 0;
+  }
+}
+
+// Level-2 totals of every scan tile (Algorithm 1's Phase 2 values that
+// depend on the grants: admission weight, new blocks, admitted count, held
+// blocks left out (all / spill-fits), restored blocks, restoring requests).
+// A tile's grants need only its level-1 prefix, which the sort's totals
+// give, so no workgroup waits on another.
+__global__ __launch_bounds__(kBlock) void scan_reduce_kernel(
+    int n, Consts c, Ctl *ctl, int *info, Sorted srt, const int4 *__restrict__ rec,
+    const int *__restrict__ ro, const unsigned *__restrict__ l1_tot,
+    long long *__restrict__ l2_tot) {
+  __shared__ ScanLds s_lds;
+  __shared__ int s_bad;
+  const int t = threadIdx.x, tile = (int)blockIdx.x;
+  unsigned so[kScanItems];
+  int4 sr[kScanItems];
+  int sw[kScanItems];
+  load_sorted(n, srt, so, sr, sw);
+  if (t == 0) s_bad = bad_status(load_agent(info));
+  const int nact = (int)ctl->nact;
+  long long pre1[kL1], pre2_unused[kL2];
+  earlier_totals(l1_tot, nullptr, tile, pre1, pre2_unused, s_lds.red);
+  if (s_bad) return;
+  bool broken = false;
+  int idx[kScanItems], rw[kScanItems];
+  int4 r4[kScanItems];
+  tile_positions(n, tile, nact, srt, rec, ro, so, sr, sw, idx, r4, rw, broken);
+  const ScanConsts K = scan_consts(c, ctl);
+  PosVals v;
+  scan_positions(tile, kScanItems, K, idx, r4, pre1, s_lds, v);
+  block_sum<kL2>(v.l2, s_lds.red);
+  if (t < kL2) {
+    long long x = 0;
+#pragma unroll
+    for (int k = 0; k < kL2; ++k) x = k == t ? v.l2[k] : x;
+    l2_tot[(size_t)tile * kL2Stride + t] = x;
+  }
+  if (broken) set_status(info, CASCADE_EINTERNAL);
+}
+
+// Algorithm 1's Phase 2 loop in priority order as prefix sums.
+// Level 1 (independent of earlier decisions): restore want, base token need,
+// blocks held by running prefills (all / spill-fits).  They give the restore
+// blocks r (eq:max_restorable under the per-step cap U), the exact token need
+// and the chunked-prefill grant g of every position.
+// Level 2 (functions of g): block weight of the admission test, new blocks
+// of admitted requests, admitted count, held blocks of running prefills left
+// out (all / spill-fits), restored blocks and restoring requests.
+// A tile's prefixes of both levels are sums of the earlier tiles' totals
+// (the sort's and scan_reduce's), requested with its sorted records, so no
+// workgroup waits on another.  The victims, slot list and move lists follow
+// in finish_kernel.
+__global__ __launch_bounds__(kBlock) void scan_kernel(
+    int n, int passes, Consts c, Ctl *ctl, int *info, Sorted srt, const int4 *__restrict__ rec,
+    const int *__restrict__ ro, Outs o, RpInfo *__restrict__ rp_list,
+    RestoreEnt *__restrict__ restore_list, TileTot *__restrict__ tile_tot,
+    const unsigned *__restrict__ l1_tot, const long long *__restrict__ l2_tot) {
+  __shared__ ScanLds s_lds;
+  __shared__ int s_bad;
+
+  const int t = threadIdx.x, tile = (int)blockIdx.x;
+  unsigned so[kScanItems];
+  int4 sr[kScanItems];
+  int sw[kScanItems];
+  load_sorted(n, srt, so, sr, sw);
+  if (t == 0) s_bad = bad_status(load_agent(info));
+  const int nact = (int)ctl->nact;
+  long long pre1[kL1], pre2[kL2];
+  earlier_totals(l1_tot, l2_tot, tile, pre1, pre2, s_lds.red);
+  if (s_bad) return;
+  // a live digit beyond the launched passes would leave the keys unsorted
+  bool broken = nact > passes;
+  int idx[kScanItems], rw[kScanItems];
+  int4 r4[kScanItems];
+  tile_positions(n, tile, nact, srt, rec, ro, so, sr, sw, idx, r4, rw, broken);
+  const ScanConsts K = scan_consts(c, ctl);
+
+  TileOut out;
+  const long long rp_incl =
+      scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, rw, broken, o, rp_list,
+                      restore_list, tile_tot, pre1, pre2, s_lds, out);
+  if (tile == (int)gridDim.x - 1 && t == 0) ctl->n_rp = (int)rp_incl;
+  write_tile_outputs(out, o);
+}
+
+// ---------------------------------------------------------------- finish
+
+// The victims, slot list and move lists of a large queue, computed after the
+// scan by a small grid.  Every workgroup derives the same victims (the
+// running prefills at the back of the order whose eligible blocks behind
+// them are fewer than the deficit D, in a fixed order), then handles its
+// slice of the outputs: the free part of the slot list, the victims' blocks
+// (slot-list entries, pack moves, their copy-order hazards) and the restore
+// moves (pool slot, hazard).  Each output entry has one owner, found by
+// branch-free searches of the staged victims and restore list.  A queue whose
+// victims or restore list outgrow the LDS copies is finished by workgroup 0
+// alone with the sequential finish.
+constexpr int kFinishGrid = 32;
+constexpr int kFinVictims = 1024;   // victims staged by each finishing workgroup
+constexpr int kFinVictimSteps = 10;
+static_assert((1 << kFinVictimSteps) == kFinVictims, "victim searches cover the staged list");
+constexpr int kFinItems = 4;        // output entries per thread and round
+
+struct FinishKLds {
+  long long red[kWaves * 8];
+  int scan_tmp[kWaves];
+  int v_req[kFinVictims], v_held[kFinVictims], v_row0[kFinVictims], v_start[kFinVictims];
+  int v_offl[kFinVictims];
+  long long v_sbase[kFinVictims], v_pbase[kFinVictims];
+  alignas(16) RestoreEnt rl[kRestoreCap];
+};
+union FinishAnyLds {
+  FinishKLds par;
+  FinishLds seq;
+};
+
+// The unpack move that writes slot-list entry s (restore list in LDS), or -1.
+__device__ __forceinline__ int fin_unpack_move_at(long long s, int nr, const FinishKLds &L) {
+  if (nr <= 0 || L.rl[0].alloc_off > s) return -1;
+  const int lo = last_at_or_below<kRestoreSteps>(nr, s, [&](int k) { return L.rl[k].alloc_off; });
+  const RestoreEnt e = L.rl[lo];
+  return s < (long long)e.alloc_off + e.blocks ? e.stage_off + (int)(s - e.alloc_off) : -1;
+}
+
+__global__ __launch_bounds__(kBlock) void finish_kernel(int n, int n_free, int n_tiles, Ctl *ctl,
+                                                        int *info,
+                                                        const TileTot *__restrict__ tiles,
+                                                        const int *__restrict__ free_slots,
+                                                        const RpInfo *__restrict__ rp,
+                                                        const RestoreEnt *__restrict__ rl,
+                                                        const int *__restrict__ slots, Outs o) {
+  __shared__ FinishAnyLds U;
+  __shared__ int s_bad;
+  FinishKLds &L = U.par;
+  const int t = threadIdx.x, g = (int)blockIdx.x, G = (int)gridDim.x;
+  if (t == 0) s_bad = bad_status(info[0]);
+  const int n_rp = ctl->n_rp, kstar = ctl->kstar;
+  const long long kx = ctl->kx, ky = ctl->ky, kz = ctl->kz, kzp = ctl->kzp;
+  // tile totals, the staged part of the restore list and the last kBlock
+  // running prefills, all requested before any is used
+  constexpr int kTilePer = 4, kRestPer = kRestoreCap / kBlock;
+  long long tot[6] = {0, 0, 0, 0, 0, 0};
+  for (int j0 = 0; j0 < n_tiles; j0 += kTilePer * kBlock) {
+    TileTot tt[kTilePer];
+#pragma unroll
+    for (int u = 0; u < kTilePer; ++u) {
+      const int j = j0 + u * kBlock + t;
+      tt[u] = j < n_tiles ? tiles[j] : TileTot{0, 0, 0, 0, 0, 0, {0, 0}};
+    }
+#pragma unroll
+    for (int u = 0; u < kTilePer; ++u) {
+      tot[0] += tt[u].adm_nb;
+      tot[1] += tt[u].elig_h;
+      tot[2] += tt[u].elig_offl_h;
+      tot[3] += tt[u].n_adm;
+      tot[4] += tt[u].n_unpack;
+      tot[5] += tt[u].n_restore;
+    }
+  }
+  const int n_rs = min(n, kRestoreCap);
+  RestoreEnt rv[kRestPer];
+#pragma unroll
+  for (int u = 0; u < kRestPer; ++u) {
+    const int j = t + u * kBlock;
+    rv[u] = j < n_rs ? rl[j] : RestoreEnt{0, 0, 0, 0};
+  }
+  int top = n_rp;
+  RpInfo ri = {};
+  if (top - 1 - t >= 0) ri = rp[top - 1 - t];
+#pragma unroll
+  for (int u = 0; u < kRestPer; ++u) {
+    const int j = t + u * kBlock;
+    if (j < n_rs) L.rl[j] = rv[u];
+  }
+  block_sum<6>(tot, L.red);
+  if (s_bad) return;
+  const long long D = tot[0] - n_free, E = tot[1], EO = tot[2];
+  const long long nu = tot[4];
+  const int nr = (int)tot[5];
+
+  // victims, in order from the back of the queue
+  int nv_all = 0;                // victims found (staged or not)
+  long long held_all = 0, held_offl = 0;
+  while (D > 0 && top > 0) {
+    const int e = top - 1 - t;
+    if (top != n_rp && e >= 0) ri = rp[e];
+    bool victim = false, kept = false;
+    long long after = 0;
+    if (e >= 0 && ri.eligible) {
+      const long long eh = ri.pos < kstar ? ri.x : kx + ri.y - ky;
+      after = E - eh;  // eligible blocks behind this request
+      if (after >= D) {
+        kept = true;
+      } else if (after < 0) {
+        set_status(info, CASCADE_EINTERNAL);
+      } else {
+        victim = true;
+      }
+    }
+    int vr[1] = {victim ? 1 : 0}, vt[1];
+    block_exclusive_scan<1>(vr, vt, L.scan_tmp);
+    const int v = nv_all + vr[0];
+    if (victim && v < kFinVictims) {
+      L.v_req[v] = ri.req;
+      L.v_held[v] = ri.held;
+      L.v_row0[v] = ri.row0;
+      L.v_offl[v] = ri.offl;
+      L.v_sbase[v] = (long long)n_free + after;
+      L.v_pbase[v] = ri.offl ? EO - (ri.pos < kstar ? ri.z : kz + ri.zp - kzp) : -1;
+    }
+    long long hs[2] = {victim ? ri.held : 0, (victim && ri.offl) ? ri.held : 0};
+    block_sum<2>(hs, L.red);
+    held_all += hs[0];
+    held_offl += hs[1];
+    nv_all += vt[0];
+    if (__syncthreads_or(kept ? 1 : 0)) break;  // every earlier holder is kept too
+    top -= kBlock;
+  }
+  if (g == 0 && t == 0) {
+    const long long nsl = (long long)n_free + held_all;
+    info[CASCADE_INFO_N_ADMITTED] = (int)tot[3];
+    info[CASCADE_INFO_N_SLOT_LIST] = (int)nsl;
+    info[CASCADE_INFO_N_UNPACK] = (int)nu;
+    info[CASCADE_INFO_N_PACK] = (int)held_offl;
+    const bool full = nsl > o.sl_cap || nu > o.unpack_cap || held_offl > o.pack_cap;
+    if (full && load_agent(info) == CASCADE_OK) set_status(info, CASCADE_ENOSPC);
+  }
+  if (nv_all > kFinVictims || nr > kRestoreCap) {
+    // beyond the LDS copies: the sequential finish, in workgroup 0 only
+    __syncthreads();
+    if (g == 0)
+      finish_step(ctl, info, n, n_free, n_tiles, n_rp, tiles, free_slots, rp, rl, slots, o,
+                  U.seq);
+    return;
+  }
+  const int nv = nv_all;
+  int v_total;
+  {
+    constexpr int kPer = kFinVictims / kBlock;
+    int h[kPer], run = 0;
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int v = t * kPer + u;
+      h[u] = v < nv ? L.v_held[v] : 0;
+      run += h[u];
+    }
+    int ex[1] = {run}, tt1[1];
+    block_exclusive_scan<1>(ex, tt1, L.scan_tmp);
+    int acc = ex[0];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int v = t * kPer + u;
+      if (v < nv) L.v_start[v] = acc;
+      acc += h[u];
+    }
+    v_total = tt1[0];
+  }
+  if (g == 0 && t < kFinVictims) {
+    for (int v = t; v < nv; v += kBlock)
+      o.action[L.v_req[v]] = (uint8_t)(L.v_offl[v] ? CASCADE_ACT_PREEMPT_OFFLOAD
+                                                  : CASCADE_ACT_PREEMPT_DROP);
   }
   __syncthreads();
-  if (!s_last) return;
-  __threadfence();  // acquire every other tile's writes
-  if (threadIdx.x == 0) s_bad = bad_status(load_agent(info));
-  __syncthreads();
-  if (s_bad) return;
-  // every tile has published its level-1 inclusive prefix: the total of
-  // running prefills is the last tile's
-  const int n_rp = (int)((load_agent(status1 + (size_t)(gridDim.x - 1) * kL1 + 4)) >> 2);
-  finish_step(ctl, info, n, c.n_free, gridDim.x, n_rp, tile_tot, free_slots, rp_list,
-              restore_list, slots, o, s_fin);
+
+  // this workgroup's slice of the output entries: [0, lim) free part of the
+  // slot list, then v_total victim blocks, then nu restore moves
+  const long long lim = min(n_free, o.sl_cap);
+  const long long total = lim + v_total + nu;
+  const long long chunk = (total + G - 1) / G;
+  const long long i_end = lmin(total, (long long)(g + 1) * chunk);
+  for (long long i0 = (long long)g * chunk; i0 < i_end; i0 += kFinItems * kBlock) {
+    // pass 1: the owner of every entry and the one load it needs
+    int kind[kFinItems], aux[kFinItems], ld[kFinItems];
+    long long idx[kFinItems];
+#pragma unroll
+    for (int u = 0; u < kFinItems; ++u) {
+      const long long i = i0 + u * kBlock + t;
+      kind[u] = -1;
+      ld[u] = 0;
+      idx[u] = 0;
+      aux[u] = 0;
+      if (i >= i_end) continue;
+      if (i < lim) {  // free part of the slot list
+        kind[u] = 0;
+        idx[u] = i;
+        ld[u] = free_slots[i];
+      } else if (i < lim + v_total) {  // victim block
+        const int m = (int)(i - lim);
+        const int v = last_at_or_below<kFinVictimSteps>(nv, m, [&](int k) { return L.v_start[k]; });
+        kind[u] = 1;
+        idx[u] = m;
+        aux[u] = v;
+        ld[u] = slots[L.v_row0[v] + (m - L.v_start[v])];
+      } else {  // restore move
+        const long long m = i - lim - v_total;
+        const int k = last_at_or_below<kRestoreSteps>(nr, m, [&](int q) { return L.rl[q].stage_off; });
+        const RestoreEnt re = L.rl[k];
+        const long long s = (long long)re.alloc_off + (m - re.stage_off);
+        kind[u] = 2;
+        idx[u] = m;
+        aux[u] = k;
+        if (s < o.sl_cap) {
+          if (s < n_free) {
+            ld[u] = free_slots[s];
+          } else {
+            const int mv = (int)(s - n_free);
+            const int v = last_at_or_below<kFinVictimSteps>(nv, mv, [&](int q) { return L.v_start[q]; });
+            ld[u] = slots[L.v_row0[v] + (mv - L.v_start[v])];
+          }
+        }
+      }
+    }
+    // pass 2: the entries
+#pragma unroll
+    for (int u = 0; u < kFinItems; ++u) {
+      if (kind[u] == 0) {
+        o.slot_list[idx[u]] = ld[u];
+      } else if (kind[u] == 1) {
+        const int m = (int)idx[u], v = aux[u], b = m - L.v_start[v], slot = ld[u];
+        const long long sb = L.v_sbase[v] + b;
+        if (sb < o.sl_cap) o.slot_list[sb] = slot;
+        const long long pb = L.v_pbase[v];
+        const long long j = pb >= 0 ? pb + b : -1;
+        if (j >= 0 && j < o.pack_cap) {
+          cascade_move_t mv;
+          mv.req = L.v_req[v];
+          mv.blk = b;
+          mv.pool_slot = slot;
+          mv.staging_slot = (int)j;
+          o.pack[j] = mv;
+          if (o.pack_hazard) o.pack_hazard[j] = fin_unpack_move_at(sb, nr, L);
+        }
+      } else if (kind[u] == 2) {
+        const long long m = idx[u];
+        const RestoreEnt re = L.rl[aux[u]];
+        const int b = (int)(m - re.stage_off);
+        const long long s = (long long)re.alloc_off + b;
+        if (m < o.unpack_cap) {
+          cascade_move_t mv;
+          mv.req = re.req;
+          mv.blk = b;
+          mv.pool_slot = s < o.sl_cap ? ld[u] : -1;
+          mv.staging_slot = (int)m;
+          o.unpack[m] = mv;
+          if (o.unpack_hazard) {
+            int hz = -1;  // a free slot is read by no pack move
+            if (s >= n_free) {
+              const int mv2 = (int)(s - n_free);
+              const int v = last_at_or_below<kFinVictimSteps>(nv, mv2, [&](int q) { return L.v_start[q]; });
+              const long long pb = L.v_pbase[v];
+              const long long j = pb >= 0 ? pb + (mv2 - L.v_start[v]) : -1;
+              hz = (j >= 0 && j < o.pack_cap) ? (int)j : -1;
+            }
+            o.unpack_hazard[m] = hz;
+          }
+        }
+      }
+    }
+  }
 }
 
 // ------------------------------------------------------------ small queues
@@ -1313,7 +1917,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
 constexpr int kSmallMax = kScanTile;
 constexpr int kSmallCheckBlocks = 16384;  // pools up to this size are checked in-kernel
 constexpr int kCheckGrid = 64;
-static_assert(kSortTile == kScanTile && kSortItems == kScanItems, "one tile per small queue");
+constexpr int kSmallItems = kScanItems;  // one sort tile and one scan tile per small queue
 
 struct SmallSortLds {
   unsigned long long key[kSmallMax];
@@ -1415,7 +2019,7 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
   unsigned cnt[4] = {0, 0, 0, 0};
   unsigned long long mn = ~0ull, mx = 0;
 #pragma unroll
-  for (int j = 0; j < kSortItems; ++j) {
+  for (int j = 0; j < kSmallItems; ++j) {
     const int i = j * kBlock + t;
     if (i >= n) continue;
     const ReqEval r = eval_request(rq, ro, c, s_slo, i);
@@ -1479,11 +2083,11 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
   //      lane: the order in which wave_digit_rank ranks them.
   const int jn = (n + kBlock - 1) / kBlock;
   const unsigned long long span = mx - mn + 1;
-  unsigned long long key[kSortItems];
-  unsigned val[kSortItems];
+  unsigned long long key[kSmallItems];
+  unsigned val[kSmallItems];
   unsigned long long k_and = ~0ull, k_or = 0;
 #pragma unroll
-  for (int j = 0; j < kSortItems; ++j) {
+  for (int j = 0; j < kSmallItems; ++j) {
     const int p = (wave * jn + j) * 64 + lane;
     key[j] = 0;
     val[j] = (unsigned)p;
@@ -1518,9 +2122,9 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
     moved = true;
     for (int k = t; k < kWaves * kRadix; k += kBlock) (&U.sort.wcnt[0][0])[k] = 0;
     __syncthreads();
-    int dig[kSortItems], rank[kSortItems];
+    int dig[kSmallItems], rank[kSmallItems];
 #pragma unroll
-    for (int j = 0; j < kSortItems; ++j) {
+    for (int j = 0; j < kSmallItems; ++j) {
       const int p = (wave * jn + j) * 64 + lane;
       dig[j] = (j < jn && p < n) ? (int)((key[j] >> (8 * d)) & 255) : -1;
       rank[j] = j < jn ? wave_digit_rank(dig[j], U.sort.wcnt[wave]) : 0;
@@ -1539,7 +2143,7 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
     U.sort.start[t] = st[0];
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < kSortItems; ++j) {
+    for (int j = 0; j < kSmallItems; ++j) {
       if (dig[j] < 0) continue;
       const int pos = U.sort.start[dig[j]] + (int)U.sort.wcnt[wave][dig[j]] + rank[j];
       U.sort.key[pos] = key[j];
@@ -1547,7 +2151,7 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
     }
     __syncthreads();
 #pragma unroll
-    for (int j = 0; j < kSortItems; ++j) {
+    for (int j = 0; j < kSmallItems; ++j) {
       const int p = (wave * jn + j) * 64 + lane;
       if (j < jn && p < n) {
         key[j] = U.sort.key[p];
@@ -1568,8 +2172,11 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
     rw[j] = idx[j] >= 0 ? ro[idx[j]] : 0;
   }
   const ScanConsts K = scan_consts(c, ctl);
+  TileOut out;
+  const long long zero1[kL1] = {0, 0, 0, 0, 0}, zero2[kL2] = {0, 0, 0, 0, 0, 0, 0};
   const long long n_rp = scan_tile<false>(0, jn, K, ctl, info, idx, r4, rw, false, o, rp_list,
-                                          restore_list, tile_tot, nullptr, nullptr, s_lds);
+                                          restore_list, tile_tot, zero1, zero2, s_lds, out);
+  write_tile_outputs(out, o);
   __syncthreads();
   if (t == 0) s_cnt[0] = bad_status(load_agent(info)) ? 1u : 0u;
   __syncthreads();
@@ -1601,8 +2208,8 @@ __global__ __launch_bounds__(kBlock) void empty_step_kernel(int n_free, int num_
 // ---------------------------------------------------------------- host
 
 struct Layout {
-  size_t ctl, sort_status, scan1, scan2, partials, keys_a, keys_b, vals_a, vals_b, rec,
-      rp_list, restore, tile_tot, total;
+  size_t ctl, scan1, scan2, sort_status, partials, keys_a, keys_b, vals_a, vals_b, rec,
+      s_order, s_rec, s_ro, rp_list, restore, tile_tot, total;
   int sort_tiles, scan_tiles, eval_grid;
 };
 
@@ -1617,16 +2224,20 @@ Layout make_layout(int32_t n) {
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes); return o; };
   L.ctl = take(sizeof(Ctl));
-  // the look-back status words follow the control block: one clear covers all
+  // the look-back status words follow the control block: one clear covers
+  // them, the sort's words last (only the launched passes' are cleared)
+  L.scan1 = take((size_t)L.scan_tiles * kL1 * 4);  // level-1 totals per scan tile
+  L.scan2 = take((size_t)L.scan_tiles * kL2Stride * 8);  // level-2 totals per scan tile
   L.sort_status = take((size_t)kMaxDigits * L.sort_tiles * kRadix * 4);
-  L.scan1 = take((size_t)L.scan_tiles * kL1 * 8);
-  L.scan2 = take((size_t)L.scan_tiles * kL2Stride * 8);
   L.partials = take((size_t)L.eval_grid * sizeof(Partial));
   L.keys_a = take(np * 8);
   L.keys_b = take(np * 8);
   L.vals_a = take(np * 4);
   L.vals_b = take(np * 4);
   L.rec = take(np * 16);
+  L.s_order = take(np * 4);
+  L.s_rec = take(np * 16);
+  L.s_ro = take(np * 4);
   L.rp_list = take(np * sizeof(RpInfo));
   L.restore = take(np * sizeof(RestoreEnt));
   L.tile_tot = take((size_t)L.scan_tiles * sizeof(TileTot));
@@ -1695,7 +2306,9 @@ int max_sort_digits(const cascade_params_t *p) {
 }
 
 typedef void (*RadixFn)(int, Ctl *, int *, unsigned long long *, unsigned long long *,
-                        unsigned *, unsigned *, unsigned *);
+                        unsigned *, unsigned *, unsigned *, const int4 *, const int *, Sorted,
+                        unsigned *);
+static_assert(kMaxDigits == 8, "one radix kernel per digit");
 const RadixFn kRadixKernels[kMaxDigits] = {
     radix_pass_kernel<0>, radix_pass_kernel<1>, radix_pass_kernel<2>, radix_pass_kernel<3>,
     radix_pass_kernel<4>, radix_pass_kernel<5>, radix_pass_kernel<6>, radix_pass_kernel<7>};
@@ -1809,8 +2422,12 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   auto *rlist = reinterpret_cast<RestoreEnt *>(ws + L.restore);
   auto *tile_tot = reinterpret_cast<TileTot *>(ws + L.tile_tot);
   auto *sort_status = reinterpret_cast<unsigned *>(ws + L.sort_status);
-  auto *scan1 = reinterpret_cast<unsigned long long *>(ws + L.scan1);
-  auto *scan2 = reinterpret_cast<unsigned long long *>(ws + L.scan2);
+  Sorted srt;
+  srt.order = reinterpret_cast<unsigned *>(ws + L.s_order);
+  srt.rec = reinterpret_cast<int4 *>(ws + L.s_rec);
+  srt.ro = reinterpret_cast<int *>(ws + L.s_ro);
+  auto *l1_tot = reinterpret_cast<unsigned *>(ws + L.scan1);
+  auto *l2_tot = reinterpret_cast<long long *>(ws + L.scan2);
 
   if (n <= kSmallMax) {
     // one workgroup; it checks the free list and the slots itself unless the
@@ -1825,27 +2442,35 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
                          out->info);
     return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
   }
-  // histograms + every look-back status word: cleared by eval
-  const size_t hist_off = L.ctl + offsetof(Ctl, hist);
-  const size_t clear_vec = (L.partials - hist_off) / 16;
-  uint4 *clear = reinterpret_cast<uint4 *>(ws + hist_off);
+  // histograms, level-1 totals and the launched passes' look-back words:
+  // cleared by eval
+  const int passes = max_sort_digits(p);
+  const size_t clear_off = L.ctl + offsetof(Ctl, hist);
+  const size_t clear_end = L.sort_status + (size_t)passes * L.sort_tiles * kRadix * 4;
+  const size_t clear_vec = (clear_end - clear_off) / 16;
+  uint4 *clear = reinterpret_cast<uint4 *>(ws + clear_off);
+  static_assert(offsetof(Ctl, hist) % 16 == 0, "16-byte clears");
 
   hipLaunchKernelGGL(eval_kernel, dim3(L.eval_grid), dim3(kBlock), 0, s, *rq, bt->row_offsets,
                      ts->free_slots, c, n, ctl, clear, clear_vec, out->info, partials,
                      out->budget_ns, out->queue_tier_out, keys_a, rec);
-  const int prep_grid = (n + kBlock * kPrepItems - 1) / (kBlock * kPrepItems);
-  hipLaunchKernelGGL(prep_kernel, dim3(prep_grid), dim3(kBlock), 0, s, n, ts->num_blocks,
+  static_assert(kPrepItems == kSortItems, "prep: one sort tile per workgroup");
+  hipLaunchKernelGGL(prep_kernel, dim3(L.sort_tiles), dim3(kBlock), 0, s, n, ts->num_blocks,
                      L.eval_grid, partials, bt->row_offsets, bt->slots, ctl, out->info, keys_a,
                      vals_a);
-  const int passes = max_sort_digits(p);
   for (int pass = 0; pass < passes; ++pass)
     hipLaunchKernelGGL(kRadixKernels[pass], dim3(L.sort_tiles), dim3(kBlock), 0, s, n, ctl,
                        out->info, keys_a, keys_b, vals_a, vals_b,
-                       sort_status + (size_t)pass * L.sort_tiles * kRadix);
+                       sort_status + (size_t)pass * L.sort_tiles * kRadix, rec,
+                       bt->row_offsets, srt, l1_tot);
+  hipLaunchKernelGGL(scan_reduce_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, c, ctl,
+                     out->info, srt, rec, bt->row_offsets, l1_tot, l2_tot);
   hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, passes, c, ctl,
-                     out->info,
-                     vals_a, vals_b, rec, bt->row_offsets, bt->slots, ts->free_slots, o, rp_list,
-                     rlist, tile_tot, scan1, scan2);
+                     out->info, srt, rec, bt->row_offsets, o, rp_list, rlist, tile_tot, l1_tot,
+                     l2_tot);
+  hipLaunchKernelGGL(finish_kernel, dim3(kFinishGrid), dim3(kBlock), 0, s, n, ts->n_free,
+                     L.scan_tiles, ctl, out->info, tile_tot, ts->free_slots, rp_list, rlist,
+                     bt->slots, o);
   if (hipGetLastError() != hipSuccess) return CASCADE_EHIP;
   return CASCADE_OK;
 }

@@ -113,10 +113,24 @@ __device__ __forceinline__ unsigned long long wave_max(unsigned long long x) {
   return last_lane(wave_inclusive_scan<OpMax, unsigned long long>(x, 0ull));
 }
 
-// Exclusive prefix sums of K values per thread over the workgroup, in
-// thread order; also returns the workgroup totals.  `lds` holds kWaves*K.
-template <int K, typename T>
+// Lane `src` (wave-uniform) of x.
+__device__ __forceinline__ unsigned lane_value(unsigned x, int src) {
+  return (unsigned)__builtin_amdgcn_readlane((int)x, src);
+}
+__device__ __forceinline__ unsigned long long lane_value(unsigned long long x, int src) {
+  const unsigned lo = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)x, src);
+  const unsigned hi = (unsigned)__builtin_amdgcn_readlane((int)(unsigned)(x >> 32), src);
+  return ((unsigned long long)hi << 32) | lo;
+}
+
+// Exclusive prefix sums of K values per thread over a workgroup of NW waves,
+// in thread order; also returns the workgroup totals.  `lds` holds NW*K.
+// The per-wave totals are combined by a wave scan (lane w holds wave w's),
+// so the register use does not grow with NW.
+template <int K, typename T, int NW = kWaves>
 __device__ __forceinline__ void block_exclusive_scan(T (&v)[K], T (&total)[K], T *lds) {
+  static_assert(NW <= 64, "one wave combines the wave totals");
+  typedef typename UnsignedOf<T>::type U;
   const int lane = lane_id(), wave = wave_id();
   T inc[K];
 #pragma unroll
@@ -128,22 +142,19 @@ __device__ __forceinline__ void block_exclusive_scan(T (&v)[K], T (&total)[K], T
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < K; ++k) {
-    T before = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      T x = lds[w * K + k];
-      before += (w < wave) ? x : T(0);
-      tot += x;
-    }
+    const T x = lane < NW ? lds[lane * K + k] : T(0);
+    const U xs = (U)wave_inclusive_sum(x);
+    const T before = wave > 0 ? (T)lane_value(xs, wave - 1) : T(0);
+    total[k] = (T)lane_value(xs, NW - 1);
     v[k] = before + inc[k] - v[k];
-    total[k] = tot;
   }
   __syncthreads();
 }
 
-// Workgroup sums of K values; every thread receives the totals.
-template <int K, typename T>
+// Workgroup sums of K values over NW waves; every thread receives the totals.
+template <int K, typename T, int NW = kWaves>
 __device__ __forceinline__ void block_sum(T (&v)[K], T *lds) {
+  static_assert(NW <= 64, "one wave combines the wave totals");
   const int lane = lane_id(), wave = wave_id();
 #pragma unroll
   for (int k = 0; k < K; ++k) v[k] = wave_sum(v[k]);
@@ -153,13 +164,39 @@ __device__ __forceinline__ void block_sum(T (&v)[K], T *lds) {
   }
   __syncthreads();
 #pragma unroll
-  for (int k = 0; k < K; ++k) {
-    T tot = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) tot += lds[w * K + k];
-    v[k] = tot;
-  }
+  for (int k = 0; k < K; ++k) v[k] = wave_sum(lane < NW ? lds[lane * K + k] : T(0));
   __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// Hand-over to the last workgroup of a grid.  Values another workgroup reads
+// within the same launch are written with agent-scope atomic stores, which
+// need no cache write-back: completing them (wait_stores) before the ticket
+// is their release.  A device-wide fence per workgroup would write the whole
+// L2 back, and costs far more than the stores themselves.
+constexpr int kTicketGroups = 16;  // first-level counters of the last-workgroup test
+constexpr int kTicketStride = 32;  // one counter per 128-byte line
+
+// Wait until this thread's memory operations have completed.
+__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0f70); }  // vmcnt(0)
+
+// Called by one thread per workgroup once its results are stored: true for
+// the last workgroup of the grid to arrive.  Two levels of counters (16
+// groups, then one) keep the atomics on any one address to a few dozen,
+// where a single counter would serialize one per workgroup.  Counters are
+// reset by the workgroup that completes them, so every launch finds them at
+// zero.  `tk` holds (kTicketGroups + 1) * kTicketStride words.
+__device__ __forceinline__ bool last_workgroup(unsigned *tk) {
+  const unsigned G = gridDim.x, groups = min(G, (unsigned)kTicketGroups);
+  const unsigned g = blockIdx.x % groups;
+  const unsigned size = (G - g + groups - 1) / groups;
+  unsigned *c = tk + g * kTicketStride;
+  if (atomicAdd(c, 1u) != size - 1) return false;
+  store_agent(c, 0u);
+  unsigned *top = tk + kTicketGroups * kTicketStride;
+  if (atomicAdd(top, 1u) != groups - 1) return false;
+  store_agent(top, 0u);
+  return true;
 }
 
 // ---------------------------------------------------------------------------

@@ -66,7 +66,8 @@ def test_configs_full_size(dev, cfg):
 
 
 @pytest.mark.parametrize("n", [1, 2, 63, 64, 65, 255, 256, 257, 1023, 1024, 1025, 2047, 2048,
-                               2049, 4097, 16385, 65535, 65537, 131073])
+                               2049, 4095, 4096, 4097, 8193, 12289, 16385, 65535, 65537,
+                               131073])
 def test_fuzz_sizes(dev, n):
     import paper_2608_06557_amd.synth as synth
     w = synth.make_workload(2, seed=7000 + n, n=n)
@@ -127,6 +128,37 @@ def test_many_victims_every_restore_in_a_spilled_slot(dev, seed):
     victims = np.isin(o["action"], [ref.ACT_PREEMPT_OFFLOAD, ref.ACT_PREEMPT_DROP]).sum()
     assert victims > 256 and o["n_unpack"] > 300
     assert np.all(o["unpack_hazard"] >= 0)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_finish_more_victims_than_staged(dev, seed):
+    """Thousands of preempted running prefills: more victims than the parallel
+    finish stages, so one workgroup finishes the step sequentially."""
+    rng = np.random.default_rng(seed)
+    n = 12000
+    p = helpers.base_params(token_cap=200000, max_move_blocks=60000, tier2_reserve_q16=0,
+                            num_blocks=100000)
+    w = helpers.random_workload(rng, n, params=p, n_free=0)
+    w["arrival_ns"] = np.full(n, p["t_now_ns"], np.int64)
+    g, o = run_both(dev, w)
+    assert_same(g, o, f"victims {seed}")
+    victims = np.isin(o["action"], [ref.ACT_PREEMPT_OFFLOAD, ref.ACT_PREEMPT_DROP]).sum()
+    assert victims > 1024
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_finish_long_restore_list(dev, seed):
+    """More restoring requests than the restore list's LDS copy holds."""
+    rng = np.random.default_rng(seed)
+    n = 12000
+    p = helpers.base_params(token_cap=1_000_000, max_move_blocks=200000, tier2_reserve_q16=0,
+                            num_blocks=400000, slo_ns=[10 ** 9] * 3 + [0] * 13,
+                            link_blk_ns=[1, 1], link_delta_ns=[1, 1])
+    w = helpers.random_workload(rng, n, params=p, n_free=300000)
+    w["arrival_ns"] = np.full(n, p["t_now_ns"], np.int64)
+    g, o = run_both(dev, w)
+    assert_same(g, o, f"restores {seed}")
+    assert (o["restore_blocks"][o["admitted"]] > 0).sum() > 1024
 
 
 def test_empty_queue(dev):
