@@ -37,8 +37,10 @@
 namespace cascade {
 namespace {
 
+constexpr int kSortBlock = 512;  // radix workgroups: 8 waves, one 2048-key tile
+constexpr int kSortWaves = kSortBlock / 64;
 constexpr int kSortItems = 4;
-constexpr int kSortTile = kBlock * kSortItems;
+constexpr int kSortTile = kSortBlock * kSortItems;
 constexpr int kSortWin = 32;     // predecessors read per look-back round trip (radix)
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
@@ -95,6 +97,9 @@ struct Ctl {
   int kstar;                      // first position whose blocks do not fit
   long long kx, ky, kz, kzp;      // prefixes just before kstar
   alignas(16) unsigned hist[kMaxDigits][kRadix];  // cleared by eval's grid
+  // scan tiles whose hand-over is complete: kTicketGroups counters, then the
+  // count of complete groups (cleared by eval's grid)
+  alignas(128) unsigned done[(kTicketGroups + 1) * kTicketStride];
 };
 constexpr size_t kCtlHeaderWords = offsetof(Ctl, hist) / 4;
 
@@ -414,7 +419,7 @@ __device__ __forceinline__ int key_digits(unsigned long long mn, unsigned long l
 
 // Sort plan: the digits that move data (below the key width, not constant
 // over all n keys), as a bit mask.  Every radix workgroup derives it from the
-// histograms; hv holds thread t's bucket t of every digit.
+// histograms; hv holds thread t's bucket t of every digit (zeros past kRadix).
 __device__ __forceinline__ unsigned plan_mask(const unsigned (&hv)[kMaxDigits], int n, int nd,
                                               unsigned *s_mask) {
   unsigned constant = 0;
@@ -575,7 +580,7 @@ __device__ __forceinline__ void l1_contrib(unsigned *s_l1, int tile, const int4 
 // tile = blockIdx.x, in parallel with the tile claim and the plan; a
 // workgroup that claims another tile reloads.
 template <int kK>
-__global__ __launch_bounds__(kBlock) void radix_pass_kernel(
+__global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     int n, Ctl *ctl, int *info, unsigned long long *keys_a, unsigned long long *keys_b,
     unsigned *vals_a, unsigned *vals_b, unsigned *status, const int4 *__restrict__ rec,
     const int *__restrict__ ro, Sorted srt, unsigned *__restrict__ l1_tot) {
@@ -583,10 +588,10 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   __shared__ unsigned s_vals[kSortTile];
   __shared__ int4 s_rec[kSortTile];
   __shared__ int s_ro[kSortTile];
-  __shared__ unsigned s_wcnt[kWaves][kRadix];
+  __shared__ unsigned s_wcnt[kSortWaves][kRadix];
   __shared__ int s_start[kRadix];
   __shared__ int s_off[kRadix];
-  __shared__ int s_scan[kWaves * 2];
+  __shared__ int s_scan[kSortWaves * 2];
   __shared__ unsigned s_l1[kMaxScanTiles * kL1];  // last pass: level-1 totals per scan tile
   __shared__ int s_tile, s_bad;
   __shared__ unsigned s_mask;
@@ -612,7 +617,7 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   }
   unsigned hv[kMaxDigits];
 #pragma unroll
-  for (int d = 0; d < kMaxDigits; ++d) hv[d] = ctl->hist[d][t];
+  for (int d = 0; d < kMaxDigits; ++d) hv[d] = t < kRadix ? ctl->hist[d][t] : 0u;
   if (t == 0) {
     // a claimed tile of a pass that turns out idle is never waited on
     s_tile = (int)atomicAdd(&ctl->tile_ctr[kK], 1u);
@@ -620,31 +625,35 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
     s_mask = 0;
   }
   const int nd = key_digits(ctl->bmin, ctl->bmax, ctl->cnt[1], ctl->cnt[2]);
-  for (int k = t; k < kWaves * kRadix; k += kBlock) (&s_wcnt[0][0])[k] = 0;
+  for (int k = t; k < kSortWaves * kRadix; k += kSortBlock) (&s_wcnt[0][0])[k] = 0;
   __syncthreads();
   const unsigned active = plan_mask(hv, n, nd, &s_mask);
   const int nact = __builtin_popcount(active);
   if (kK == 0 && blockIdx.x == 0 && t == 0) store_agent(&ctl->nact, (unsigned)nact);
   if (s_bad) return;
   if (kK == 0 && nact == 0) {
-    // every key equal: the order is the identity, sort tile j is scan tile j
-    static_assert(kSortTile == kScanTile, "one scan tile per sort tile");
-    const int p0 = (int)blockIdx.x * kScanTile;
-    unsigned c[kL1] = {0, 0, 0, 0, 0};
-    for (int p = p0 + t; p < min(n, p0 + kScanTile); p += kBlock) {
-      const int4 r = rec[p];
-      const bool rp = rec_state(r.w) == CASCADE_RUNNING_PREFILL;
-      const unsigned h = rp ? (unsigned)rec_held(r.w) : 0u;
-      c[0] += (unsigned)r.x;
-      c[1] += (unsigned)r.y;
-      c[2] += h;
-      c[3] += rec_offl(r.w) ? h : 0u;
-      c[4] += rp ? 1u : 0u;
-    }
-    block_sum<kL1>(c, &s_wcnt[0][0]);
-    if (t == 0) {
+    // every key equal: the order is the identity; this sort tile's scan
+    // tiles get their level-1 totals here
+    static_assert(kSortTile % kScanTile == 0, "whole scan tiles per sort tile");
+    for (int q = 0; q < kSortTile / kScanTile; ++q) {
+      const int p0 = (int)blockIdx.x * kSortTile + q * kScanTile;
+      if (p0 >= n) break;
+      unsigned c[kL1] = {0, 0, 0, 0, 0};
+      for (int p = p0 + t; p < min(n, p0 + kScanTile); p += kSortBlock) {
+        const int4 r = rec[p];
+        const bool rp = rec_state(r.w) == CASCADE_RUNNING_PREFILL;
+        const unsigned h = rp ? (unsigned)rec_held(r.w) : 0u;
+        c[0] += (unsigned)r.x;
+        c[1] += (unsigned)r.y;
+        c[2] += h;
+        c[3] += rec_offl(r.w) ? h : 0u;
+        c[4] += rp ? 1u : 0u;
+      }
+      block_sum<kL1, unsigned, kSortWaves>(c, &s_wcnt[0][0]);
+      if (t == 0) {
 #pragma unroll
-      for (int k = 0; k < kL1; ++k) l1_tot[(size_t)blockIdx.x * kL1 + k] = c[k];
+        for (int k = 0; k < kL1; ++k) l1_tot[(size_t)(p0 / kScanTile) * kL1 + k] = c[k];
+      }
     }
     return;
   }
@@ -655,7 +664,7 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
 #pragma unroll
   for (int k = 0; k < kK; ++k) rest &= rest - 1;
   const int digit = __builtin_ctz(rest);
-  unsigned gcount = 0;
+  unsigned gcount = 0;  // (threads t < kRadix: digit t)
 #pragma unroll
   for (int d = 0; d < kMaxDigits; ++d) gcount = d == digit ? hv[d] : gcount;
   const int tile = s_tile;
@@ -711,29 +720,33 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   }
   __syncthreads();
 
-  // earlier waves' counts of digit t; the tile's count is published at once
+  // earlier waves' counts of digit t (threads t < kRadix); the tile's count
+  // is published at once
+  const bool dt = t < kRadix;
   unsigned run = 0;
+  if (dt) {
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    const unsigned c = s_wcnt[w][t];
-    s_wcnt[w][t] = run;
-    run += c;
+    for (int w = 0; w < kSortWaves; ++w) {
+      const unsigned c = s_wcnt[w][t];
+      s_wcnt[w][t] = run;
+      run += c;
+    }
   }
   const unsigned tile_count = run;
   unsigned *st = status + (size_t)tile * kRadix;
-  publish<unsigned>(st + t, tile_count, tile == 0 ? kFlagInclusive : kFlagAggregate);
+  if (dt) publish<unsigned>(st + t, tile_count, tile == 0 ? kFlagInclusive : kFlagAggregate);
   if (last) {
-    for (int k = t; k < kMaxScanTiles * kL1; k += kBlock) s_l1[k] = 0;
+    for (int k = t; k < kMaxScanTiles * kL1; k += kSortBlock) s_l1[k] = 0;
   }
   // exclusive scans over digits: tile-local starts and global bucket bases
   int v2[2] = {(int)tile_count, (int)gcount};
   int tot2[2];
-  block_exclusive_scan<2>(v2, tot2, s_scan);
-  s_start[t] = v2[0];
+  block_exclusive_scan<2, int, kSortWaves>(v2, tot2, s_scan);
+  if (dt) s_start[t] = v2[0];
   // the earlier tiles' counts, kSortWin predecessors per round trip
   bool timed_out = false;
   unsigned prefix = 0;
-  if (tile > 0) {
+  if (dt && tile > 0) {
     unsigned lbw[kSortWin];
     int lb_next = tile - 1;
     unsigned spins = 0;
@@ -770,7 +783,7 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
     publish<unsigned>(st + t, prefix + tile_count, kFlagInclusive);
   }
   if (timed_out) set_status(info, CASCADE_ETIMEOUT);
-  s_off[t] = v2[1] + (int)prefix - v2[0];
+  if (dt) s_off[t] = v2[1] + (int)prefix - v2[0];
   __syncthreads();
   // reorder the tile in LDS by digit
 #pragma unroll
@@ -791,8 +804,8 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   }
   __syncthreads();
   const int count = min(kSortTile, n - tile_base);
-  static_assert(kSortTile % kBlock == 0, "every lane runs every iteration (wave sums below)");
-  for (int s = t; s < kSortTile; s += kBlock) {
+  static_assert(kSortTile % kSortBlock == 0, "every lane runs every iteration (wave sums below)");
+  for (int s = t; s < kSortTile; s += kSortBlock) {
     int o = -1;
     unsigned long long k = 0;
     if (s < count) {
@@ -821,7 +834,7 @@ __global__ __launch_bounds__(kBlock) void radix_pass_kernel(
   if (last) {
     __syncthreads();
     const int n_tot = ((n + kScanTile - 1) / kScanTile) * kL1;
-    for (int k = t; k < n_tot; k += kBlock) {
+    for (int k = t; k < n_tot; k += kSortBlock) {
       const unsigned v = s_l1[k];
       if (v) atomicAdd(l1_tot + k, v);
     }
@@ -1456,186 +1469,11 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
 // (the identity order when every key is equal), so one coalesced read feeds
 // the tile.  Each tile hands its results to the finishing workgroup with
 // agent-scope stores and a ticket, then writes its other outputs.
-// Sums over tiles j < tile of both levels' per-tile totals (l1[j*kL1 + k],
-// l2[j*kL2Stride + k]), over the workgroup.  Up to 2*kBlock tiles of both
-// are requested at once (one round trip); an earlier launch wrote them, so
-// nothing is polled.  l2 may be null (level 1 only).
-__device__ __forceinline__ void earlier_totals(const unsigned *__restrict__ l1,
-                                               const long long *__restrict__ l2, int tile,
-                                               long long (&pre1)[kL1], long long (&pre2)[kL2],
-                                               long long *s_red) {
-  constexpr int kPer = 2, K = kL1 + kL2;
-  long long v[K];
-#pragma unroll
-  for (int k = 0; k < K; ++k) v[k] = 0;
-  for (int b0 = 0; b0 < tile; b0 += kPer * kBlock) {
-    unsigned w1[kPer][kL1];
-    long long w2[kPer][kL2];
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-      const int j = b0 + u * kBlock + (int)threadIdx.x;
-      const bool in = j < tile;
-#pragma unroll
-      for (int k = 0; k < kL1; ++k) w1[u][k] = in ? l1[(size_t)j * kL1 + k] : 0u;
-#pragma unroll
-      for (int k = 0; k < kL2; ++k) w2[u][k] = (in && l2) ? l2[(size_t)j * kL2Stride + k] : 0ll;
-    }
-#pragma unroll
-    for (int u = 0; u < kPer; ++u) {
-#pragma unroll
-      for (int k = 0; k < kL1; ++k) v[k] += (long long)w1[u][k];
-#pragma unroll
-      for (int k = 0; k < kL2; ++k) v[kL1 + k] += w2[u][k];
-    }
-  }
-  block_sum<K>(v, s_red);
-#pragma unroll
-  for (int k = 0; k < kL1; ++k) pre1[k] = v[k];
-#pragma unroll
-  for (int k = 0; k < kL2; ++k) pre2[k] = v[kL1 + k];
-}
-
-// The tile's positions in priority order: request index, scan record and
-// row offset, from the last radix pass (sorted buffers) or, when every key
-// is equal (no pass moved data), the identity order.  Positions past n get
-// index -1.  `broken` is set on an index out of range.
-__device__ __forceinline__ void tile_positions(int n, int tile, int nact, const Sorted &srt,
-                                               const int4 *__restrict__ rec,
-                                               const int *__restrict__ ro,
-                                               const unsigned (&so)[kScanItems],
-                                               const int4 (&sr)[kScanItems],
-                                               const int (&sw)[kScanItems],
-                                               int (&idx)[kScanItems], int4 (&r4)[kScanItems],
-                                               int (&rw)[kScanItems], bool &broken) {
-  const int p0 = tile * kScanTile + (int)threadIdx.x * kScanItems;
-#pragma unroll
-  for (int j = 0; j < kScanItems; ++j) {
-    const int p = p0 + j;
-    int ix = -1;
-    int4 r = make_int4(0, 0, 0, 0);
-    int w = 0;
-    if (p < n) {
-      if (nact == 0) {
-        ix = p;
-        r = rec[p];
-        w = ro[p];
-      } else {
-        ix = (int)so[j];
-        r = sr[j];
-        w = sw[j];
-      }
-    }
-    if ((unsigned)ix >= (unsigned)n) {  // cannot happen with a correct sort
-      broken = broken || ix != -1;
-      ix = -1;
-    }
-    idx[j] = ix;
-    r4[j] = ix >= 0 ? r : make_int4(0, 0, 0, 0);
-    rw[j] = ix >= 0 ? w : 0;
-  }
-}
-
-// The sorted entries of the tile's positions (blockIdx.x), requested before
-// anything else.
-__device__ __forceinline__ void load_sorted(int n, const Sorted &srt, unsigned (&so)[kScanItems],
-                                            int4 (&sr)[kScanItems], int (&sw)[kScanItems]) {
-  const int p0 = (int)blockIdx.x * kScanTile + (int)threadIdx.x * kScanItems;
-#pragma unroll
-  for (int j = 0; j < kScanItems; ++j) {
-    const int p = p0 + j;
-    so[j] = p < n ? srt.order[p] : 0u;
-    sr[j] = p < n ? srt.rec[p] : make_int4(0, 0, 0, 0);
-    sw[j] = p < n ? srt.ro[p] : 0;
-  }
-}
-
-// Level-2 totals of every scan tile (Algorithm 1's Phase 2 values that
-// depend on the grants: admission weight, new blocks, admitted count, held
-// blocks left out (all / spill-fits), restored blocks, restoring requests).
-// A tile's grants need only its level-1 prefix, which the sort's totals
-// give, so no workgroup waits on another.
-__global__ __launch_bounds__(kBlock) void scan_reduce_kernel(
-    int n, Consts c, Ctl *ctl, int *info, Sorted srt, const int4 *__restrict__ rec,
-    const int *__restrict__ ro, const unsigned *__restrict__ l1_tot,
-    long long *__restrict__ l2_tot) {
-  __shared__ ScanLds s_lds;
-  __shared__ int s_bad;
-  const int t = threadIdx.x, tile = (int)blockIdx.x;
-  unsigned so[kScanItems];
-  int4 sr[kScanItems];
-  int sw[kScanItems];
-  load_sorted(n, srt, so, sr, sw);
-  if (t == 0) s_bad = bad_status(load_agent(info));
-  const int nact = (int)ctl->nact;
-  long long pre1[kL1], pre2_unused[kL2];
-  earlier_totals(l1_tot, nullptr, tile, pre1, pre2_unused, s_lds.red);
-  if (s_bad) return;
-  bool broken = false;
-  int idx[kScanItems], rw[kScanItems];
-  int4 r4[kScanItems];
-  tile_positions(n, tile, nact, srt, rec, ro, so, sr, sw, idx, r4, rw, broken);
-  const ScanConsts K = scan_consts(c, ctl);
-  PosVals v;
-  scan_positions(tile, kScanItems, K, idx, r4, pre1, s_lds, v);
-  block_sum<kL2>(v.l2, s_lds.red);
-  if (t < kL2) {
-    long long x = 0;
-#pragma unroll
-    for (int k = 0; k < kL2; ++k) x = k == t ? v.l2[k] : x;
-    l2_tot[(size_t)tile * kL2Stride + t] = x;
-  }
-  if (broken) set_status(info, CASCADE_EINTERNAL);
-}
-
-// Algorithm 1's Phase 2 loop in priority order as prefix sums.
-// Level 1 (independent of earlier decisions): restore want, base token need,
-// blocks held by running prefills (all / spill-fits).  They give the restore
-// blocks r (eq:max_restorable under the per-step cap U), the exact token need
-// and the chunked-prefill grant g of every position.
-// Level 2 (functions of g): block weight of the admission test, new blocks
-// of admitted requests, admitted count, held blocks of running prefills left
-// out (all / spill-fits), restored blocks and restoring requests.
-// A tile's prefixes of both levels are sums of the earlier tiles' totals
-// (the sort's and scan_reduce's), requested with its sorted records, so no
-// workgroup waits on another.  The victims, slot list and move lists follow
-// in finish_kernel.
-__global__ __launch_bounds__(kBlock) void scan_kernel(
-    int n, int passes, Consts c, Ctl *ctl, int *info, Sorted srt, const int4 *__restrict__ rec,
-    const int *__restrict__ ro, Outs o, RpInfo *__restrict__ rp_list,
-    RestoreEnt *__restrict__ restore_list, TileTot *__restrict__ tile_tot,
-    const unsigned *__restrict__ l1_tot, const long long *__restrict__ l2_tot) {
-  __shared__ ScanLds s_lds;
-  __shared__ int s_bad;
-
-  const int t = threadIdx.x, tile = (int)blockIdx.x;
-  unsigned so[kScanItems];
-  int4 sr[kScanItems];
-  int sw[kScanItems];
-  load_sorted(n, srt, so, sr, sw);
-  if (t == 0) s_bad = bad_status(load_agent(info));
-  const int nact = (int)ctl->nact;
-  long long pre1[kL1], pre2[kL2];
-  earlier_totals(l1_tot, l2_tot, tile, pre1, pre2, s_lds.red);
-  if (s_bad) return;
-  // a live digit beyond the launched passes would leave the keys unsorted
-  bool broken = nact > passes;
-  int idx[kScanItems], rw[kScanItems];
-  int4 r4[kScanItems];
-  tile_positions(n, tile, nact, srt, rec, ro, so, sr, sw, idx, r4, rw, broken);
-  const ScanConsts K = scan_consts(c, ctl);
-
-  TileOut out;
-  const long long rp_incl =
-      scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, rw, broken, o, rp_list,
-                      restore_list, tile_tot, pre1, pre2, s_lds, out);
-  if (tile == (int)gridDim.x - 1 && t == 0) ctl->n_rp = (int)rp_incl;
-  write_tile_outputs(out, o);
-}
-
 // ---------------------------------------------------------------- finish
 
-// The victims, slot list and move lists of a large queue, computed after the
-// scan by a small grid.  Every workgroup derives the same victims (the
+// The victims, slot list and move lists of a large queue, computed by
+// kFinishGrid extra workgroups of the scan launch once every scan tile has
+// handed over its results.  Every workgroup derives the same victims (the
 // running prefills at the back of the order whose eligible blocks behind
 // them are fewer than the deficit D, in a fixed order), then handles its
 // slice of the outputs: the free part of the slot list, the victims' blocks
@@ -1671,20 +1509,20 @@ __device__ __forceinline__ int fin_unpack_move_at(long long s, int nr, const Fin
   return s < (long long)e.alloc_off + e.blocks ? e.stage_off + (int)(s - e.alloc_off) : -1;
 }
 
-__global__ __launch_bounds__(kBlock) void finish_kernel(int n, int n_free, int n_tiles, Ctl *ctl,
-                                                        int *info,
-                                                        const TileTot *__restrict__ tiles,
-                                                        const int *__restrict__ free_slots,
-                                                        const RpInfo *__restrict__ rp,
-                                                        const RestoreEnt *__restrict__ rl,
-                                                        const int *__restrict__ slots, Outs o) {
-  __shared__ FinishAnyLds U;
-  __shared__ int s_bad;
+__device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int n_tiles,
+                                            Ctl *ctl, int *info,
+                                            const TileTot *__restrict__ tiles,
+                                            const int *__restrict__ free_slots,
+                                            const RpInfo *__restrict__ rp,
+                                            const RestoreEnt *__restrict__ rl,
+                                            const int *__restrict__ slots, const Outs &o,
+                                            FinishAnyLds &U, int &s_bad) {
   FinishKLds &L = U.par;
-  const int t = threadIdx.x, g = (int)blockIdx.x, G = (int)gridDim.x;
-  if (t == 0) s_bad = bad_status(info[0]);
-  const int n_rp = ctl->n_rp, kstar = ctl->kstar;
-  const long long kx = ctl->kx, ky = ctl->ky, kz = ctl->kz, kzp = ctl->kzp;
+  const int t = threadIdx.x;
+  if (t == 0) s_bad = bad_status(load_agent(info));
+  const int n_rp = load_agent(&ctl->n_rp), kstar = load_agent(&ctl->kstar);
+  const long long kx = load_agent(&ctl->kx), ky = load_agent(&ctl->ky),
+                  kz = load_agent(&ctl->kz), kzp = load_agent(&ctl->kzp);
   // tile totals, the staged part of the restore list and the last kBlock
   // running prefills, all requested before any is used
   constexpr int kTilePer = 4, kRestPer = kRestoreCap / kBlock;
@@ -1694,7 +1532,7 @@ __global__ __launch_bounds__(kBlock) void finish_kernel(int n, int n_free, int n
 #pragma unroll
     for (int u = 0; u < kTilePer; ++u) {
       const int j = j0 + u * kBlock + t;
-      tt[u] = j < n_tiles ? tiles[j] : TileTot{0, 0, 0, 0, 0, 0, {0, 0}};
+      tt[u] = j < n_tiles ? load_agent_rec(tiles + j) : TileTot{0, 0, 0, 0, 0, 0, {0, 0}};
     }
 #pragma unroll
     for (int u = 0; u < kTilePer; ++u) {
@@ -1711,11 +1549,11 @@ __global__ __launch_bounds__(kBlock) void finish_kernel(int n, int n_free, int n
 #pragma unroll
   for (int u = 0; u < kRestPer; ++u) {
     const int j = t + u * kBlock;
-    rv[u] = j < n_rs ? rl[j] : RestoreEnt{0, 0, 0, 0};
+    rv[u] = j < n_rs ? load_agent_rec(rl + j) : RestoreEnt{0, 0, 0, 0};
   }
   int top = n_rp;
   RpInfo ri = {};
-  if (top - 1 - t >= 0) ri = rp[top - 1 - t];
+  if (top - 1 - t >= 0) ri = load_agent_rec(rp + (top - 1 - t));
 #pragma unroll
   for (int u = 0; u < kRestPer; ++u) {
     const int j = t + u * kBlock;
@@ -1732,7 +1570,7 @@ __global__ __launch_bounds__(kBlock) void finish_kernel(int n, int n_free, int n
   long long held_all = 0, held_offl = 0;
   while (D > 0 && top > 0) {
     const int e = top - 1 - t;
-    if (top != n_rp && e >= 0) ri = rp[e];
+    if (top != n_rp && e >= 0) ri = load_agent_rec(rp + e);
     bool victim = false, kept = false;
     long long after = 0;
     if (e >= 0 && ri.eligible) {
@@ -1906,6 +1744,224 @@ __global__ __launch_bounds__(kBlock) void finish_kernel(int n, int n_free, int n
       }
     }
   }
+}
+
+// Sums over tiles j < tile of both levels' per-tile totals (l1[j*kL1 + k],
+// l2[j*kL2Stride + k]), over the workgroup.  Up to 2*kBlock tiles of both
+// are requested at once (one round trip); an earlier launch wrote them, so
+// nothing is polled.  l2 may be null (level 1 only).
+__device__ __forceinline__ void earlier_totals(const unsigned *__restrict__ l1,
+                                               const long long *__restrict__ l2, int tile,
+                                               long long (&pre1)[kL1], long long (&pre2)[kL2],
+                                               long long *s_red) {
+  constexpr int kPer = 2, K = kL1 + kL2;
+  long long v[K];
+#pragma unroll
+  for (int k = 0; k < K; ++k) v[k] = 0;
+  for (int b0 = 0; b0 < tile; b0 += kPer * kBlock) {
+    unsigned w1[kPer][kL1];
+    long long w2[kPer][kL2];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int j = b0 + u * kBlock + (int)threadIdx.x;
+      const bool in = j < tile;
+#pragma unroll
+      for (int k = 0; k < kL1; ++k) w1[u][k] = in ? l1[(size_t)j * kL1 + k] : 0u;
+#pragma unroll
+      for (int k = 0; k < kL2; ++k) w2[u][k] = (in && l2) ? l2[(size_t)j * kL2Stride + k] : 0ll;
+    }
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+#pragma unroll
+      for (int k = 0; k < kL1; ++k) v[k] += (long long)w1[u][k];
+#pragma unroll
+      for (int k = 0; k < kL2; ++k) v[kL1 + k] += w2[u][k];
+    }
+  }
+  block_sum<K>(v, s_red);
+#pragma unroll
+  for (int k = 0; k < kL1; ++k) pre1[k] = v[k];
+#pragma unroll
+  for (int k = 0; k < kL2; ++k) pre2[k] = v[kL1 + k];
+}
+
+// The tile's positions in priority order: request index, scan record and
+// row offset, from the last radix pass (sorted buffers) or, when every key
+// is equal (no pass moved data), the identity order.  Positions past n get
+// index -1.  `broken` is set on an index out of range.
+__device__ __forceinline__ void tile_positions(int n, int tile, int nact, const Sorted &srt,
+                                               const int4 *__restrict__ rec,
+                                               const int *__restrict__ ro,
+                                               const unsigned (&so)[kScanItems],
+                                               const int4 (&sr)[kScanItems],
+                                               const int (&sw)[kScanItems],
+                                               int (&idx)[kScanItems], int4 (&r4)[kScanItems],
+                                               int (&rw)[kScanItems], bool &broken) {
+  const int p0 = tile * kScanTile + (int)threadIdx.x * kScanItems;
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    const int p = p0 + j;
+    int ix = -1;
+    int4 r = make_int4(0, 0, 0, 0);
+    int w = 0;
+    if (p < n) {
+      if (nact == 0) {
+        ix = p;
+        r = rec[p];
+        w = ro[p];
+      } else {
+        ix = (int)so[j];
+        r = sr[j];
+        w = sw[j];
+      }
+    }
+    if ((unsigned)ix >= (unsigned)n) {  // cannot happen with a correct sort
+      broken = broken || ix != -1;
+      ix = -1;
+    }
+    idx[j] = ix;
+    r4[j] = ix >= 0 ? r : make_int4(0, 0, 0, 0);
+    rw[j] = ix >= 0 ? w : 0;
+  }
+}
+
+// The sorted entries of the tile's positions (blockIdx.x), requested before
+// anything else.
+__device__ __forceinline__ void load_sorted(int n, const Sorted &srt, unsigned (&so)[kScanItems],
+                                            int4 (&sr)[kScanItems], int (&sw)[kScanItems]) {
+  const int p0 = (int)blockIdx.x * kScanTile + (int)threadIdx.x * kScanItems;
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    const int p = p0 + j;
+    so[j] = p < n ? srt.order[p] : 0u;
+    sr[j] = p < n ? srt.rec[p] : make_int4(0, 0, 0, 0);
+    sw[j] = p < n ? srt.ro[p] : 0;
+  }
+}
+
+// Level-2 totals of every scan tile (Algorithm 1's Phase 2 values that
+// depend on the grants: admission weight, new blocks, admitted count, held
+// blocks left out (all / spill-fits), restored blocks, restoring requests).
+// A tile's grants need only its level-1 prefix, which the sort's totals
+// give, so no workgroup waits on another.
+__global__ __launch_bounds__(kBlock) void scan_reduce_kernel(
+    int n, Consts c, Ctl *ctl, int *info, Sorted srt, const int4 *__restrict__ rec,
+    const int *__restrict__ ro, const unsigned *__restrict__ l1_tot,
+    long long *__restrict__ l2_tot) {
+  __shared__ ScanLds s_lds;
+  __shared__ int s_bad;
+  const int t = threadIdx.x, tile = (int)blockIdx.x;
+  unsigned so[kScanItems];
+  int4 sr[kScanItems];
+  int sw[kScanItems];
+  load_sorted(n, srt, so, sr, sw);
+  if (t == 0) s_bad = bad_status(load_agent(info));
+  const int nact = (int)ctl->nact;
+  long long pre1[kL1], pre2_unused[kL2];
+  earlier_totals(l1_tot, nullptr, tile, pre1, pre2_unused, s_lds.red);
+  if (s_bad) return;
+  bool broken = false;
+  int idx[kScanItems], rw[kScanItems];
+  int4 r4[kScanItems];
+  tile_positions(n, tile, nact, srt, rec, ro, so, sr, sw, idx, r4, rw, broken);
+  const ScanConsts K = scan_consts(c, ctl);
+  PosVals v;
+  scan_positions(tile, kScanItems, K, idx, r4, pre1, s_lds, v);
+  block_sum<kL2>(v.l2, s_lds.red);
+  if (t < kL2) {
+    long long x = 0;
+#pragma unroll
+    for (int k = 0; k < kL2; ++k) x = k == t ? v.l2[k] : x;
+    l2_tot[(size_t)tile * kL2Stride + t] = x;
+  }
+  if (broken) set_status(info, CASCADE_EINTERNAL);
+}
+
+// Algorithm 1's Phase 2 loop in priority order as prefix sums.
+// Level 1 (independent of earlier decisions): restore want, base token need,
+// blocks held by running prefills (all / spill-fits).  They give the restore
+// blocks r (eq:max_restorable under the per-step cap U), the exact token need
+// and the chunked-prefill grant g of every position.
+// Level 2 (functions of g): block weight of the admission test, new blocks
+// of admitted requests, admitted count, held blocks of running prefills left
+// out (all / spill-fits), restored blocks and restoring requests.
+// A tile's prefixes of both levels are sums of the earlier tiles' totals
+// (the sort's and scan_reduce's), requested with its sorted records, so no
+// workgroup waits on another.  The victims, slot list and move lists follow
+// in finish_kernel.
+__global__ __launch_bounds__(kBlock) void scan_kernel(
+    int n, int passes, int n_tiles, Consts c, Ctl *ctl, int *info, Sorted srt,
+    const int4 *__restrict__ rec, const int *__restrict__ ro, const int *__restrict__ slots,
+    const int *__restrict__ free_slots, Outs o, RpInfo *__restrict__ rp_list,
+    RestoreEnt *__restrict__ restore_list, TileTot *__restrict__ tile_tot,
+    const unsigned *__restrict__ l1_tot, const long long *__restrict__ l2_tot) {
+  __shared__ ScanLds s_lds;
+  __shared__ FinishAnyLds s_fin;
+  __shared__ int s_bad;
+
+  const int t = threadIdx.x, tile = (int)blockIdx.x;
+  const unsigned groups = min((unsigned)n_tiles, (unsigned)kTicketGroups);
+  if (tile >= n_tiles) {
+    // a finishing workgroup: wait until every scan tile has handed over
+    if (t == 0) {
+      unsigned spins = 0;
+      s_bad = 0;
+      while (load_agent(ctl->done + kTicketGroups * kTicketStride) < groups) {
+        if (++spins > kSpinLimit) {
+          set_status(info, CASCADE_ETIMEOUT);
+          s_bad = 1;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
+      }
+    }
+    __syncthreads();
+    if (s_bad) return;
+    finish_grid(tile - n_tiles, (int)gridDim.x - n_tiles, n, c.n_free, n_tiles, ctl, info,
+                tile_tot, free_slots, rp_list, restore_list, slots, o, s_fin, s_bad);
+    return;
+  }
+  unsigned so[kScanItems];
+  int4 sr[kScanItems];
+  int sw[kScanItems];
+  load_sorted(n, srt, so, sr, sw);
+  if (t == 0) s_bad = bad_status(load_agent(info));
+  const int nact = (int)ctl->nact;
+  long long pre1[kL1], pre2[kL2];
+  earlier_totals(l1_tot, l2_tot, tile, pre1, pre2, s_lds.red);
+  if (s_bad) {
+    // counted all the same, so that the finishing workgroups stop waiting
+    if (t == 0) {
+      const unsigned gi = (unsigned)tile % groups;
+      const unsigned size = ((unsigned)n_tiles - gi + groups - 1) / groups;
+      if (atomicAdd(ctl->done + gi * kTicketStride, 1u) == size - 1)
+        atomicAdd(ctl->done + kTicketGroups * kTicketStride, 1u);
+    }
+    return;
+  }
+  // a live digit beyond the launched passes would leave the keys unsorted
+  bool broken = nact > passes;
+  int idx[kScanItems], rw[kScanItems];
+  int4 r4[kScanItems];
+  tile_positions(n, tile, nact, srt, rec, ro, so, sr, sw, idx, r4, rw, broken);
+  const ScanConsts K = scan_consts(c, ctl);
+
+  TileOut out;
+  const long long rp_incl =
+      scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, rw, broken, o, rp_list,
+                      restore_list, tile_tot, pre1, pre2, s_lds, out);
+  if (tile == n_tiles - 1 && t == 0) store_agent(&ctl->n_rp, (int)rp_incl);
+  // hand-over: this tile's agent-scope stores complete, then it is counted
+  // (two levels of counters); its other outputs follow
+  wait_stores();
+  __syncthreads();
+  if (t == 0) {
+    const unsigned gi = (unsigned)tile % groups;
+    const unsigned size = ((unsigned)n_tiles - gi + groups - 1) / groups;
+    if (atomicAdd(ctl->done + gi * kTicketStride, 1u) == size - 1)
+      atomicAdd(ctl->done + kTicketGroups * kTicketStride, 1u);
+  }
+  write_tile_outputs(out, o);
 }
 
 // ------------------------------------------------------------ small queues
@@ -2454,23 +2510,20 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   hipLaunchKernelGGL(eval_kernel, dim3(L.eval_grid), dim3(kBlock), 0, s, *rq, bt->row_offsets,
                      ts->free_slots, c, n, ctl, clear, clear_vec, out->info, partials,
                      out->budget_ns, out->queue_tier_out, keys_a, rec);
-  static_assert(kPrepItems == kSortItems, "prep: one sort tile per workgroup");
-  hipLaunchKernelGGL(prep_kernel, dim3(L.sort_tiles), dim3(kBlock), 0, s, n, ts->num_blocks,
+  const int prep_grid = (n + kBlock * kPrepItems - 1) / (kBlock * kPrepItems);
+  hipLaunchKernelGGL(prep_kernel, dim3(prep_grid), dim3(kBlock), 0, s, n, ts->num_blocks,
                      L.eval_grid, partials, bt->row_offsets, bt->slots, ctl, out->info, keys_a,
                      vals_a);
   for (int pass = 0; pass < passes; ++pass)
-    hipLaunchKernelGGL(kRadixKernels[pass], dim3(L.sort_tiles), dim3(kBlock), 0, s, n, ctl,
+    hipLaunchKernelGGL(kRadixKernels[pass], dim3(L.sort_tiles), dim3(kSortBlock), 0, s, n, ctl,
                        out->info, keys_a, keys_b, vals_a, vals_b,
                        sort_status + (size_t)pass * L.sort_tiles * kRadix, rec,
                        bt->row_offsets, srt, l1_tot);
   hipLaunchKernelGGL(scan_reduce_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, c, ctl,
                      out->info, srt, rec, bt->row_offsets, l1_tot, l2_tot);
-  hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, passes, c, ctl,
-                     out->info, srt, rec, bt->row_offsets, o, rp_list, rlist, tile_tot, l1_tot,
-                     l2_tot);
-  hipLaunchKernelGGL(finish_kernel, dim3(kFinishGrid), dim3(kBlock), 0, s, n, ts->n_free,
-                     L.scan_tiles, ctl, out->info, tile_tot, ts->free_slots, rp_list, rlist,
-                     bt->slots, o);
+  hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles + kFinishGrid), dim3(kBlock), 0, s, n,
+                     passes, L.scan_tiles, c, ctl, out->info, srt, rec, bt->row_offsets,
+                     bt->slots, ts->free_slots, o, rp_list, rlist, tile_tot, l1_tot, l2_tot);
   if (hipGetLastError() != hipSuccess) return CASCADE_EHIP;
   return CASCADE_OK;
 }
