@@ -46,8 +46,10 @@ constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
 constexpr int kPrepItems = 4;
 constexpr int kEvalItems = 1;
-constexpr int kRadix = 256;      // 8-bit digits
-constexpr int kMaxDigits = 8;
+constexpr int kMaxW = 9;         // widest digit of the multi-launch sort
+constexpr int kMaxBins = 1 << kMaxW;
+constexpr int kMaxPasses = (64 + kMaxW - 1) / kMaxW;  // passes of the multi-launch sort, at most
+constexpr int kRadix = 256;      // one workgroup's LDS sort of a small queue: 8-bit digits
 constexpr int kL1 = 5;           // first-level scan values
 constexpr int kMaxScanTiles = ((1 << 20) + kScanTile - 1) / kScanTile;
 constexpr int kL2 = 7;           // second-level scan values
@@ -91,12 +93,12 @@ struct Ctl {
   unsigned long long bmin, bmax;  // totals, written by prep's workgroup 0
   long long held_rp, need1, want1;
   unsigned cnt[4];
-  unsigned tile_ctr[kMaxDigits];  // radix tiles claimed per pass
+  unsigned tile_ctr[kMaxPasses];  // radix tiles claimed per pass
   unsigned nact;                  // data-moving radix passes, from the sort plan
   int n_rp;                       // running prefills in the queue (last scan tile)
   int kstar;                      // first position whose blocks do not fit
   long long kx, ky, kz, kzp;      // prefixes just before kstar
-  alignas(16) unsigned hist[kMaxDigits][kRadix];  // cleared by eval's grid
+  alignas(16) unsigned hist[kMaxPasses][kMaxBins];  // cleared by eval's grid
   // scan tiles whose hand-over is complete: kTicketGroups counters, then the
   // count of complete groups (cleared by eval's grid)
   alignas(128) unsigned done[(kTicketGroups + 1) * kTicketStride];
@@ -412,22 +414,21 @@ __device__ __forceinline__ int key_bits(unsigned long long mn, unsigned long lon
   const unsigned long long top = gmax * span + (mx - mn);
   return top ? 64 - __builtin_clzll(top) : 0;
 }
-__device__ __forceinline__ int key_digits(unsigned long long mn, unsigned long long mx,
-                                          unsigned c1, unsigned c2) {
-  return (key_bits(mn, mx, c1, c2) + 7) / 8;
-}
 
-// Sort plan: the digits that move data (below the key width, not constant
-// over all n keys), as a bit mask.  Every radix workgroup derives it from the
-// histograms; hv holds thread t's bucket t of every digit (zeros past kRadix).
-__device__ __forceinline__ unsigned plan_mask(const unsigned (&hv)[kMaxDigits], int n, int nd,
-                                              unsigned *s_mask) {
-  unsigned constant = 0;
-#pragma unroll
-  for (int d = 0; d < kMaxDigits; ++d) constant |= (hv[d] == (unsigned)n ? 1u : 0u) << d;
-  if (constant) atomicOr(s_mask, constant);
-  __syncthreads();
-  return ((1u << nd) - 1u) & ~*s_mask;
+// Digits of the multi-launch sort: the live key width W spread over the
+// `passes` launched passes: 8 bits wide where that suffices, else kMaxW
+// (which the host's bound on the key width makes enough).
+struct DigitPlan {
+  int w, nd;      // digit width, digits below the key width
+  unsigned bins;  // 2^w
+};
+__device__ __forceinline__ DigitPlan digit_plan(const Ctl *ctl, int passes) {
+  const int W = key_bits(ctl->bmin, ctl->bmax, ctl->cnt[1], ctl->cnt[2]);
+  DigitPlan d;
+  d.w = W <= 8 * passes ? 8 : kMaxW;
+  d.nd = (W + d.w - 1) / d.w;
+  d.bins = 1u << d.w;
+  return d;
 }
 
 // ---------------------------------------------------------------- prep
@@ -439,13 +440,14 @@ __device__ __forceinline__ unsigned plan_mask(const unsigned (&hv)[kMaxDigits], 
 // with.  Also checks the block-table slots, whose extent is only trustworthy
 // after eval.
 __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int n_partials,
+                                                      int passes,
                                                       const Partial *__restrict__ partials,
                                                       const int *__restrict__ ro,
                                                       const int *__restrict__ slots, Ctl *ctl,
                                                       int *info,
                                                       unsigned long long *__restrict__ keys,
                                                       unsigned *__restrict__ vals) {
-  __shared__ unsigned s_hist[kMaxDigits][kRadix];
+  __shared__ unsigned s_hist[kMaxPasses * kMaxBins];
   __shared__ long long s_red[kWaves * 3];
   __shared__ unsigned s_cnt[kWaves * 4];
   __shared__ unsigned long long s_mm[kWaves * 2];
@@ -473,7 +475,6 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
     mn = p.bmin < mn ? p.bmin : mn;
     mx = p.bmax > mx ? p.bmax : mx;
   }
-  for (int k = t; k < kMaxDigits * kRadix; k += kBlock) (&s_hist[0][0])[k] = 0;
   block_sum<3>(sums, s_red);
   block_sum<4>(cnt, s_cnt);
   mn = wave_min(mn);
@@ -520,26 +521,32 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
     if (t == 0) set_status(info, CASCADE_EINVAL);
   }
 
-  const int nd = key_digits(mn, mx, cnt[1], cnt[2]);
+  // the digit plan, from the totals just reduced (the same in every kernel)
+  const int W = key_bits(mn, mx, cnt[1], cnt[2]);
+  const int w = W <= 8 * passes ? 8 : kMaxW;
+  const int nd = min((W + w - 1) / w, kMaxPasses);
+  const unsigned bins = 1u << w;
+  for (int k = t; k < nd * (int)bins; k += kBlock) s_hist[k] = 0;
+  __syncthreads();
   const unsigned long long span = mx - mn + 1;
 #pragma unroll
   for (int j = 0; j < kPrepItems; ++j) {
     const int idx = base + j * kBlock + t;
-    const bool v = idx < n;
     const unsigned long long k0 = kv[j];
     const unsigned long long k = (k0 >> 62) * span + ((k0 & ((1ull << 62) - 1)) - mn);
-    if (v) {
+    if (idx < n) {
       keys[idx] = k;
       vals[idx] = (unsigned)idx;
+      for (int d = 0; d < nd; ++d)
+        atomicAdd(&s_hist[d * bins + ((k >> (w * d)) & (bins - 1))], 1u);
     }
-    if (v)
-      for (int d = 0; d < nd; ++d) atomicAdd(&s_hist[d][(k >> (8 * d)) & 255], 1u);
   }
   __syncthreads();
-  for (int d = 0; d < nd; ++d) {
-    const unsigned v = s_hist[d][t];
-    if (v) atomicAdd(&ctl->hist[d][t], v);
-  }
+  for (int d = 0; d < nd; ++d)
+    for (unsigned b = t; b < bins; b += kBlock) {
+      const unsigned v = s_hist[d * bins + b];
+      if (v) atomicAdd(&ctl->hist[d][b], v);
+    }
 }
 
 // ---------------------------------------------------------- radix pass
@@ -569,32 +576,36 @@ __device__ __forceinline__ void l1_contrib(unsigned *s_l1, int tile, const int4 
   }
 }
 
-// The k-th data-moving LSD pass (kK), over the digit the sort plan names.
-// A tile of kSortTile keys: its digit counts (LDS) are published first, so
-// the look-back's first round trip runs while the keys are ranked per wave
-// with ballots (lanes holding the same digit find each other in 8 ballots).
-// Keys are then reordered in LDS and written out in runs of equal digits.
-// The last pass writes the sorted order with each request's scan record and
-// row offset (gathered while the tile is ranked) instead of the keys.  The
-// k-th pass reads buffer k & 1, so the tile's keys are requested at once for
-// tile = blockIdx.x, in parallel with the tile claim and the plan; a
-// workgroup that claims another tile reloads.
+// The k-th data-moving LSD pass (kK), over the digit the sort plan names:
+// digits are w bits wide (8 or 9, chosen on the device from the live key
+// width), thread t owning bin t.  A tile of kSortTile keys is ranked per
+// wave with w ballots; the tile's digit counts are published for the
+// decoupled look-back; keys are reordered in LDS and written out in runs of
+// equal digits.  The last pass writes the sorted order with each request's
+// scan record and row offset (gathered while the tile is ranked) instead of
+// the keys, and adds every scan tile's level-1 totals.  The k-th pass reads
+// buffer k & 1, so the tile's keys are requested at once for tile =
+// blockIdx.x, in parallel with the tile claim and the plan; a workgroup that
+// claims another tile reloads.
 template <int kK>
 __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
-    int n, Ctl *ctl, int *info, unsigned long long *keys_a, unsigned long long *keys_b,
-    unsigned *vals_a, unsigned *vals_b, unsigned *status, const int4 *__restrict__ rec,
-    const int *__restrict__ ro, Sorted srt, unsigned *__restrict__ l1_tot) {
+    int n, int passes, Ctl *ctl, int *info, unsigned long long *keys_a,
+    unsigned long long *keys_b, unsigned *vals_a, unsigned *vals_b, unsigned *status,
+    const int4 *__restrict__ rec, const int *__restrict__ ro, Sorted srt,
+    unsigned *__restrict__ l1_tot) {
   __shared__ unsigned long long s_keys[kSortTile];
   __shared__ unsigned s_vals[kSortTile];
   __shared__ int4 s_rec[kSortTile];
   __shared__ int s_ro[kSortTile];
-  __shared__ unsigned s_wcnt[kSortWaves][kRadix];
-  __shared__ int s_start[kRadix];
-  __shared__ int s_off[kRadix];
+  __shared__ unsigned s_wcnt[kSortWaves][kMaxBins];  // per-wave counts, then starts
+  __shared__ int s_start[kMaxBins];  // tile-local start of each digit
+  __shared__ int s_off[kMaxBins];    // output offset of each digit
   __shared__ int s_scan[kSortWaves * 2];
+  __shared__ unsigned s_sum[kSortWaves * kL1];
   __shared__ unsigned s_l1[kMaxScanTiles * kL1];  // last pass: level-1 totals per scan tile
   __shared__ int s_tile, s_bad;
   __shared__ unsigned s_mask;
+  static_assert(kMaxBins == kSortBlock, "one bin per thread");
 
   const unsigned long long *src_k = (kK & 1) ? keys_b : keys_a;
   unsigned long long *dst_k = (kK & 1) ? keys_a : keys_b;
@@ -615,19 +626,30 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
       val[j] = g < n ? src_v[g] : 0u;
     }
   }
-  unsigned hv[kMaxDigits];
+  // every digit's count of bin t (the plan, and this pass's bucket base)
+  unsigned hv[kMaxPasses];
 #pragma unroll
-  for (int d = 0; d < kMaxDigits; ++d) hv[d] = t < kRadix ? ctl->hist[d][t] : 0u;
+  for (int d = 0; d < kMaxPasses; ++d) hv[d] = ctl->hist[d][t];
   if (t == 0) {
     // a claimed tile of a pass that turns out idle is never waited on
     s_tile = (int)atomicAdd(&ctl->tile_ctr[kK], 1u);
     s_bad = bad_status(load_agent(info));
     s_mask = 0;
   }
-  const int nd = key_digits(ctl->bmin, ctl->bmax, ctl->cnt[1], ctl->cnt[2]);
-  for (int k = t; k < kSortWaves * kRadix; k += kSortBlock) (&s_wcnt[0][0])[k] = 0;
+  const DigitPlan P = digit_plan(ctl, passes);
+  const unsigned bins = P.bins;
+  const bool dt = t < (int)bins;
+#pragma unroll
+  for (int w = 0; w < kSortWaves; ++w) s_wcnt[w][t] = 0;
+  // the plan: digits that move data (below the key width, not constant)
+  {
+    unsigned constant = 0;
+#pragma unroll
+    for (int d = 0; d < kMaxPasses; ++d) constant |= (hv[d] == (unsigned)n ? 1u : 0u) << d;
+    if (constant) atomicOr(&s_mask, constant);
+  }
   __syncthreads();
-  const unsigned active = plan_mask(hv, n, nd, &s_mask);
+  const unsigned active = ((1u << P.nd) - 1u) & ~s_mask;
   const int nact = __builtin_popcount(active);
   if (kK == 0 && blockIdx.x == 0 && t == 0) store_agent(&ctl->nact, (unsigned)nact);
   if (s_bad) return;
@@ -649,7 +671,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
         c[3] += rec_offl(r.w) ? h : 0u;
         c[4] += rp ? 1u : 0u;
       }
-      block_sum<kL1, unsigned, kSortWaves>(c, &s_wcnt[0][0]);
+      block_sum<kL1, unsigned, kSortWaves>(c, s_sum);
       if (t == 0) {
 #pragma unroll
         for (int k = 0; k < kL1; ++k) l1_tot[(size_t)(p0 / kScanTile) * kL1 + k] = c[k];
@@ -664,9 +686,9 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
 #pragma unroll
   for (int k = 0; k < kK; ++k) rest &= rest - 1;
   const int digit = __builtin_ctz(rest);
-  unsigned gcount = 0;  // (threads t < kRadix: digit t)
+  unsigned gcount = 0;
 #pragma unroll
-  for (int d = 0; d < kMaxDigits; ++d) gcount = d == digit ? hv[d] : gcount;
+  for (int d = 0; d < kMaxPasses; ++d) gcount = d == digit ? hv[d] : gcount;
   const int tile = s_tile;
   const int tile_base = tile * kSortTile;
   if (tile != (int)blockIdx.x) {
@@ -677,11 +699,12 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
       val[j] = g < n ? src_v[g] : 0u;
     }
   }
-  const int shift = 8 * digit;
+  const int shift = P.w * digit;
+  const unsigned dmask = bins - 1;
   bool broken = false;
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j)
-    dig[j] = (tile_base + local + j * 64 < n) ? (int)((key[j] >> shift) & 255) : -1;
+    dig[j] = (tile_base + local + j * 64 < n) ? (int)((key[j] >> shift) & dmask) : -1;
   // the last pass carries each request's scan record and row offset along;
   // the loads are unconditional (index 0 when not needed) so that nothing
   // waits for them before the tile is ranked
@@ -704,10 +727,12 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     const bool v = dig[j] >= 0;
     uint64_t peers = __ballot(v);
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const bool bit = (dig[j] >> b) & 1;
-      const uint64_t bal = __ballot(bit);
-      peers &= bit ? bal : ~bal;
+    for (int b = 0; b < kMaxW; ++b) {
+      if (b < P.w) {
+        const bool bit = (dig[j] >> b) & 1;
+        const uint64_t bal = __ballot(bit);
+        peers &= bit ? bal : ~bal;
+      }
     }
     const int d = v ? dig[j] : 0;
     unsigned before = 0;
@@ -720,70 +745,34 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   }
   __syncthreads();
 
-  // earlier waves' counts of digit t (threads t < kRadix); the tile's count
-  // is published at once
-  const bool dt = t < kRadix;
-  unsigned run = 0;
+  // earlier waves' counts of digit t; the tile's count is published at once
+  unsigned *st = status + (size_t)tile * kMaxBins;
+  unsigned tcount = 0;
   if (dt) {
 #pragma unroll
     for (int w = 0; w < kSortWaves; ++w) {
       const unsigned c = s_wcnt[w][t];
-      s_wcnt[w][t] = run;
-      run += c;
+      s_wcnt[w][t] = tcount;
+      tcount += c;
     }
+    publish<unsigned>(st + t, tcount, tile == 0 ? kFlagInclusive : kFlagAggregate);
   }
-  const unsigned tile_count = run;
-  unsigned *st = status + (size_t)tile * kRadix;
-  if (dt) publish<unsigned>(st + t, tile_count, tile == 0 ? kFlagInclusive : kFlagAggregate);
   if (last) {
     for (int k = t; k < kMaxScanTiles * kL1; k += kSortBlock) s_l1[k] = 0;
   }
-  // exclusive scans over digits: tile-local starts and global bucket bases
-  int v2[2] = {(int)tile_count, (int)gcount};
-  int tot2[2];
+  // tile-local starts and global bucket bases, in digit order
+  int v2[2] = {(int)tcount, dt ? (int)gcount : 0}, tot2[2];
   block_exclusive_scan<2, int, kSortWaves>(v2, tot2, s_scan);
-  if (dt) s_start[t] = v2[0];
   // the earlier tiles' counts, kSortWin predecessors per round trip
   bool timed_out = false;
-  unsigned prefix = 0;
-  if (dt && tile > 0) {
-    unsigned lbw[kSortWin];
-    int lb_next = tile - 1;
-    unsigned spins = 0;
-    for (;;) {
-#pragma unroll
-      for (int i = 0; i < kSortWin; ++i)
-        lbw[i] = lb_next - i >= 0 ? load_agent(status + (size_t)(lb_next - i) * kRadix + t)
-                                  : kFlagInclusive;
-      int consumed = 0;
-      bool done = false, stalled = false;
-#pragma unroll
-      for (int i = 0; i < kSortWin; ++i) {
-        if (!done && !stalled) {
-          const unsigned f = lbw[i] & 3u;
-          if (f == 0) {
-            stalled = true;
-          } else {
-            prefix += lbw[i] >> 2;
-            ++consumed;
-            done = f == kFlagInclusive;
-          }
-        }
-      }
-      if (done) break;
-      lb_next -= consumed;
-      if (stalled) {
-        if (++spins > kSpinLimit) {
-          timed_out = true;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-    }
-    publish<unsigned>(st + t, prefix + tile_count, kFlagInclusive);
+  const unsigned pre =
+      (dt && tile > 0) ? look_back<unsigned, kSortWin>(status, kMaxBins, tile, t, &timed_out) : 0u;
+  if (dt) {
+    if (tile > 0) publish<unsigned>(st + t, pre + tcount, kFlagInclusive);
+    s_start[t] = v2[0];
+    s_off[t] = v2[1] + (int)pre - v2[0];
   }
   if (timed_out) set_status(info, CASCADE_ETIMEOUT);
-  if (dt) s_off[t] = v2[1] + (int)prefix - v2[0];
   __syncthreads();
   // reorder the tile in LDS by digit
 #pragma unroll
@@ -810,7 +799,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     unsigned long long k = 0;
     if (s < count) {
       k = s_keys[s];
-      o = s_off[(k >> shift) & 255] + s;
+      o = s_off[(k >> shift) & dmask] + s;
       if ((unsigned)o >= (unsigned)n) {
         broken = true;
         o = -1;
@@ -2171,7 +2160,7 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
     }
     varying = a ^ b;  // bits that differ between two keys of the queue
   }
-  const int nd = key_digits(mn, mx, cnt[1], cnt[2]);
+  const int nd = (key_bits(mn, mx, cnt[1], cnt[2]) + 7) / 8;  // 8-bit digits
   bool moved = false;
   for (int d = 0; d < nd; ++d) {
     if (((varying >> (8 * d)) & 255) == 0) continue;  // uniform: order unchanged
@@ -2284,7 +2273,7 @@ Layout make_layout(int32_t n) {
   // them, the sort's words last (only the launched passes' are cleared)
   L.scan1 = take((size_t)L.scan_tiles * kL1 * 4);  // level-1 totals per scan tile
   L.scan2 = take((size_t)L.scan_tiles * kL2Stride * 8);  // level-2 totals per scan tile
-  L.sort_status = take((size_t)kMaxDigits * L.sort_tiles * kRadix * 4);
+  L.sort_status = take((size_t)kMaxPasses * L.sort_tiles * kMaxBins * 4);
   L.partials = take((size_t)L.eval_grid * sizeof(Partial));
   L.keys_a = take(np * 8);
   L.keys_b = take(np * 8);
@@ -2329,11 +2318,12 @@ bool params_ok(const cascade_params_t *p, int32_t n, const cascade_tier_state_t 
   return true;
 }
 
-// Upper bound on the 8-bit digits of the compressed key, from the parameters
-// alone: every budget lies in [-(L_bound + t_now), max SLO], clamped to
-// +-2^61.  Radix passes beyond it are not launched; the device skips the
-// ones between it and the live key width.
-int max_sort_digits(const cascade_params_t *p) {
+// Radix passes launched: the compressed key's width is bounded from the
+// parameters alone (every budget lies in [-(L_bound + t_now), max SLO],
+// clamped to +-2^61), and the passes are as few as digits of up to kMaxW
+// bits allow.  The device spreads the live key width over them; a pass it
+// does not need returns at once.
+int sort_passes(const cascade_params_t *p) {
   typedef __int128 i128;
   const i128 nmax = 1 << 17;
   const i128 dmax = p->max_batch - 1;
@@ -2357,15 +2347,15 @@ int max_sort_digits(const cascade_params_t *p) {
   const i128 top = 2 * span + (hi - lo);
   int bits = 0;
   for (i128 v = top; v > 0; v >>= 1) ++bits;
-  const int d = (bits + 7) / 8;
-  return d < 1 ? 1 : (d > kMaxDigits ? kMaxDigits : d);
+  const int d = (bits + kMaxW - 1) / kMaxW;
+  return d < 1 ? 1 : (d > kMaxPasses ? kMaxPasses : d);
 }
 
-typedef void (*RadixFn)(int, Ctl *, int *, unsigned long long *, unsigned long long *,
+typedef void (*RadixFn)(int, int, Ctl *, int *, unsigned long long *, unsigned long long *,
                         unsigned *, unsigned *, unsigned *, const int4 *, const int *, Sorted,
                         unsigned *);
-static_assert(kMaxDigits == 8, "one radix kernel per digit");
-const RadixFn kRadixKernels[kMaxDigits] = {
+static_assert(kMaxPasses == 8, "one radix kernel per pass");
+const RadixFn kRadixKernels[kMaxPasses] = {
     radix_pass_kernel<0>, radix_pass_kernel<1>, radix_pass_kernel<2>, radix_pass_kernel<3>,
     radix_pass_kernel<4>, radix_pass_kernel<5>, radix_pass_kernel<6>, radix_pass_kernel<7>};
 
@@ -2500,9 +2490,9 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   }
   // histograms, level-1 totals and the launched passes' look-back words:
   // cleared by eval
-  const int passes = max_sort_digits(p);
+  const int passes = sort_passes(p);
   const size_t clear_off = L.ctl + offsetof(Ctl, hist);
-  const size_t clear_end = L.sort_status + (size_t)passes * L.sort_tiles * kRadix * 4;
+  const size_t clear_end = L.sort_status + (size_t)passes * L.sort_tiles * kMaxBins * 4;
   const size_t clear_vec = (clear_end - clear_off) / 16;
   uint4 *clear = reinterpret_cast<uint4 *>(ws + clear_off);
   static_assert(offsetof(Ctl, hist) % 16 == 0, "16-byte clears");
@@ -2512,12 +2502,12 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
                      out->budget_ns, out->queue_tier_out, keys_a, rec);
   const int prep_grid = (n + kBlock * kPrepItems - 1) / (kBlock * kPrepItems);
   hipLaunchKernelGGL(prep_kernel, dim3(prep_grid), dim3(kBlock), 0, s, n, ts->num_blocks,
-                     L.eval_grid, partials, bt->row_offsets, bt->slots, ctl, out->info, keys_a,
+                     L.eval_grid, passes, partials, bt->row_offsets, bt->slots, ctl, out->info, keys_a,
                      vals_a);
   for (int pass = 0; pass < passes; ++pass)
-    hipLaunchKernelGGL(kRadixKernels[pass], dim3(L.sort_tiles), dim3(kSortBlock), 0, s, n, ctl,
-                       out->info, keys_a, keys_b, vals_a, vals_b,
-                       sort_status + (size_t)pass * L.sort_tiles * kRadix, rec,
+    hipLaunchKernelGGL(kRadixKernels[pass], dim3(L.sort_tiles), dim3(kSortBlock), 0, s, n,
+                       passes, ctl, out->info, keys_a, keys_b, vals_a, vals_b,
+                       sort_status + (size_t)pass * L.sort_tiles * kMaxBins, rec,
                        bt->row_offsets, srt, l1_tot);
   hipLaunchKernelGGL(scan_reduce_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, c, ctl,
                      out->info, srt, rec, bt->row_offsets, l1_tot, l2_tot);

@@ -161,6 +161,33 @@ def test_finish_long_restore_list(dev, seed):
     assert (o["restore_blocks"][o["admitted"]] > 0).sum() > 1024
 
 
+def _key_width(w, o):
+    """Bits of the sort key over (group, budget) that the step orders by."""
+    b = np.clip(o["budget_ns"].astype(np.int64), -(1 << 61), (1 << 61) - 1)
+    st = np.asarray(w["state"])
+    grp = np.where(st == ref.DECODE, 0,
+                   np.where(o["queue_tier_out"] == 1, 1, 2)).astype(np.int64)
+    span = int(b.max()) - int(b.min()) + 1
+    return int((grp * span + (b - b.min())).max()).bit_length()
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_wide_keys_nine_bit_digits(dev, seed):
+    """Requests that arrived long ago widen the key beyond what 8-bit digits
+    cover in the passes the parameters allow for, so the sort runs on 9-bit
+    digits."""
+    import paper_2608_06557_amd.synth as synth
+    rng = np.random.default_rng(seed)
+    n = 20000
+    w = synth.make_workload(2, seed=11 + seed, n=n)
+    idx = rng.choice(n, 300, replace=False)
+    w["arrival_ns"] = w["arrival_ns"].copy()
+    w["arrival_ns"][idx] = rng.integers(0, 1000, 300)
+    g, o = run_both(dev, w)
+    assert_same(g, o, f"wide keys {seed}")
+    assert _key_width(w, o) > 40
+
+
 def test_empty_queue(dev):
     w = helpers.random_workload(np.random.default_rng(0), 1)
     for k in [f for f, _ in ref.REQ_FIELDS]:
