@@ -93,7 +93,6 @@ struct Ctl {
   unsigned long long bmin, bmax;  // totals, written by prep's workgroup 0
   long long held_rp, need1, want1;
   unsigned cnt[4];
-  unsigned tile_ctr[kMaxPasses];  // radix tiles claimed per pass
   unsigned nact;                  // data-moving radix passes, from the sort plan
   int n_rp;                       // running prefills in the queue (last scan tile)
   int kstar;                      // first position whose blocks do not fit
@@ -584,9 +583,11 @@ __device__ __forceinline__ void l1_contrib(unsigned *s_l1, int tile, const int4 
 // equal digits.  The last pass writes the sorted order with each request's
 // scan record and row offset (gathered while the tile is ranked) instead of
 // the keys, and adds every scan tile's level-1 totals.  The k-th pass reads
-// buffer k & 1, so the tile's keys are requested at once for tile =
-// blockIdx.x, in parallel with the tile claim and the plan; a workgroup that
-// claims another tile reloads.
+// buffer k & 1, so the tile's keys are requested at once, in parallel with
+// the plan.  Workgroup b sorts tile b: workgroups are dispatched in index
+// order (on each XCD), so every tile a look-back waits on belongs to a
+// workgroup that is running or done, and the lowest unfinished one waits on
+// nothing.
 template <int kK>
 __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     int n, int passes, Ctl *ctl, int *info, unsigned long long *keys_a,
@@ -603,7 +604,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   __shared__ int s_scan[kSortWaves * 2];
   __shared__ unsigned s_sum[kSortWaves * kL1];
   __shared__ unsigned s_l1[kMaxScanTiles * kL1];  // last pass: level-1 totals per scan tile
-  __shared__ int s_tile, s_bad;
+  __shared__ int s_bad;
   __shared__ unsigned s_mask;
   static_assert(kMaxBins == kSortBlock, "one bin per thread");
 
@@ -631,8 +632,6 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
 #pragma unroll
   for (int d = 0; d < kMaxPasses; ++d) hv[d] = ctl->hist[d][t];
   if (t == 0) {
-    // a claimed tile of a pass that turns out idle is never waited on
-    s_tile = (int)atomicAdd(&ctl->tile_ctr[kK], 1u);
     s_bad = bad_status(load_agent(info));
     s_mask = 0;
   }
@@ -689,16 +688,8 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   unsigned gcount = 0;
 #pragma unroll
   for (int d = 0; d < kMaxPasses; ++d) gcount = d == digit ? hv[d] : gcount;
-  const int tile = s_tile;
+  const int tile = (int)blockIdx.x;
   const int tile_base = tile * kSortTile;
-  if (tile != (int)blockIdx.x) {
-#pragma unroll
-    for (int j = 0; j < kSortItems; ++j) {
-      const int g = tile_base + local + j * 64;
-      key[j] = g < n ? src_k[g] : 0ull;
-      val[j] = g < n ? src_v[g] : 0u;
-    }
-  }
   const int shift = P.w * digit;
   const unsigned dmask = bins - 1;
   bool broken = false;

@@ -213,9 +213,9 @@ __device__ __forceinline__ void publish(W *word, W value, unsigned flag) {
 }
 
 // Sum of `value k` over tiles 0 .. tile-1, reading up to WIN predecessors per
-// round trip.  Tiles are claimed in increasing order by running workgroups
-// and publish their aggregate before they wait on anything, so every poll
-// ends; the poll count is still bounded and a timeout is reported.
+// round trip.  Workgroup b owns tile b; workgroups are dispatched in index
+// order and publish their aggregate before they wait on anything, so every
+// poll ends; the poll count is still bounded and a timeout is reported.
 template <typename W, int WIN>
 __device__ __forceinline__ W look_back(const W *status, int stride, int tile, int k,
                                        bool *timed_out) {
