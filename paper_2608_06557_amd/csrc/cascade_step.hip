@@ -44,7 +44,7 @@ constexpr int kSortTile = kSortBlock * kSortItems;
 constexpr int kSortWin = 32;     // predecessors read per look-back round trip (radix)
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
-constexpr int kPrepItems = 4;
+constexpr int kPrepItems = 8;
 constexpr int kEvalItems = 1;
 constexpr int kMaxW = 9;         // widest digit of the multi-launch sort
 constexpr int kMaxBins = 1 << kMaxW;
@@ -447,10 +447,8 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
                                                       unsigned long long *__restrict__ keys,
                                                       unsigned *__restrict__ vals) {
   __shared__ unsigned s_hist[kMaxPasses * kMaxBins];
-  __shared__ long long s_red[kWaves * 3];
-  __shared__ unsigned s_cnt[kWaves * 4];
-  __shared__ unsigned long long s_mm[kWaves * 2];
-  const int t = threadIdx.x;
+  __shared__ unsigned long long s_red[kWaves * 9];
+  const int t = threadIdx.x, lane = lane_id(), wave = wave_id();
   const int base = blockIdx.x * kBlock * kPrepItems;
   unsigned long long kv[kPrepItems];
 #pragma unroll
@@ -458,70 +456,65 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
     const int idx = base + j * kBlock + t;
     kv[j] = idx < n ? keys[idx] : 0ull;
   }
-  long long sums[3] = {0, 0, 0};
-  unsigned cnt[4] = {0, 0, 0, 0};
-  unsigned long long mn = ~0ull, mx = 0;
+  // totals of eval's partials: sums (held, need1, want1, three group counts,
+  // bad), then min and max, reduced per wave and combined after one barrier
+  unsigned long long v[9] = {0, 0, 0, 0, 0, 0, 0, ~0ull, 0};
 #pragma unroll 1
   for (int j = t; j < n_partials; j += kBlock) {
     const Partial p = partials[j];
-    sums[0] += p.held;
-    sums[1] += p.need1;
-    sums[2] += p.want1;
-    cnt[0] += p.c0;
-    cnt[1] += p.c1;
-    cnt[2] += p.c2;
-    cnt[3] += p.bad;
-    mn = p.bmin < mn ? p.bmin : mn;
-    mx = p.bmax > mx ? p.bmax : mx;
+    v[0] += (unsigned long long)p.held;
+    v[1] += (unsigned long long)p.need1;
+    v[2] += (unsigned long long)p.want1;
+    v[3] += p.c0;
+    v[4] += p.c1;
+    v[5] += p.c2;
+    v[6] += p.bad;
+    v[7] = p.bmin < v[7] ? p.bmin : v[7];
+    v[8] = p.bmax > v[8] ? p.bmax : v[8];
   }
-  block_sum<3>(sums, s_red);
-  block_sum<4>(cnt, s_cnt);
-  mn = wave_min(mn);
-  mx = wave_max(mx);
-  if (lane_id() == 0) {
-    s_mm[wave_id() * 2] = mn;
-    s_mm[wave_id() * 2 + 1] = mx;
+#pragma unroll
+  for (int k = 0; k < 7; ++k) v[k] = wave_sum(v[k]);
+  v[7] = wave_min(v[7]);
+  v[8] = wave_max(v[8]);
+  if (lane == 0) {
+#pragma unroll
+    for (int k = 0; k < 9; ++k) s_red[wave * 9 + k] = v[k];
   }
   __syncthreads();
-  mn = ~0ull;
-  mx = 0;
-  for (int w = 0; w < kWaves; ++w) {
-    mn = s_mm[2 * w] < mn ? s_mm[2 * w] : mn;
-    mx = s_mm[2 * w + 1] > mx ? s_mm[2 * w + 1] : mx;
+#pragma unroll
+  for (int k = 0; k < 9; ++k) v[k] = s_red[k];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) {
+#pragma unroll
+    for (int k = 0; k < 7; ++k) v[k] += s_red[w * 9 + k];
+    v[7] = s_red[w * 9 + 7] < v[7] ? s_red[w * 9 + 7] : v[7];
+    v[8] = s_red[w * 9 + 8] > v[8] ? s_red[w * 9 + 8] : v[8];
   }
+  const unsigned long long mn = v[7], mx = v[8];
+  const unsigned c1 = (unsigned)v[4], c2 = (unsigned)v[5];
+  const bool bad_data = v[6] != 0;
   if (blockIdx.x == 0 && t == 0) {
     ctl->bmin = mn;
     ctl->bmax = mx;
-    ctl->held_rp = sums[0];
-    ctl->need1 = sums[1];
-    ctl->want1 = sums[2];
-    ctl->cnt[0] = cnt[0];
-    ctl->cnt[1] = cnt[1];
-    ctl->cnt[2] = cnt[2];
-    if (cnt[3]) set_status(info, CASCADE_EINVAL);
+    ctl->held_rp = (long long)v[0];
+    ctl->need1 = (long long)v[1];
+    ctl->want1 = (long long)v[2];
+    ctl->cnt[0] = (unsigned)v[3];
+    ctl->cnt[1] = c1;
+    ctl->cnt[2] = c2;
+    if (bad_data) set_status(info, CASCADE_EINVAL);
   }
-  if (cnt[3]) return;  // bad request data: nothing below is meaningful
+  if (bad_data) return;  // bad request data: nothing below is meaningful
 
+  // block-table slots in range: requested here, checked after the histograms
   const int nnz = ro[n];
-  bool bad = false;
-  {
-    const int gt = blockIdx.x * kBlock + t, gs = gridDim.x * kBlock;
-#pragma unroll 1
-    for (int j0 = gt; j0 < nnz; j0 += 8 * gs) {
-      int v[8];
+  const int gt = blockIdx.x * kBlock + t, gs = gridDim.x * kBlock;
+  int sv[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = (j0 + u * gs < nnz) ? slots[j0 + u * gs] : 0;
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if ((unsigned)v[u] >= (unsigned)num_blocks) bad = true;
-    }
-  }
-  if (__syncthreads_or(bad ? 1 : 0)) {
-    if (t == 0) set_status(info, CASCADE_EINVAL);
-  }
+  for (int u = 0; u < 8; ++u) sv[u] = (gt + u * gs < nnz) ? slots[gt + u * gs] : 0;
 
   // the digit plan, from the totals just reduced (the same in every kernel)
-  const int W = key_bits(mn, mx, cnt[1], cnt[2]);
+  const int W = key_bits(mn, mx, c1, c2);
   const int w = W <= 8 * passes ? 8 : kMaxW;
   const int nd = min((W + w - 1) / w, kMaxPasses);
   const unsigned bins = 1u << w;
@@ -531,21 +524,42 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
 #pragma unroll
   for (int j = 0; j < kPrepItems; ++j) {
     const int idx = base + j * kBlock + t;
+    const bool in = idx < n;
     const unsigned long long k0 = kv[j];
     const unsigned long long k = (k0 >> 62) * span + ((k0 & ((1ull << 62) - 1)) - mn);
-    if (idx < n) {
+    if (in) {
       keys[idx] = k;
       vals[idx] = (unsigned)idx;
+    }
+    if (in) {
       for (int d = 0; d < nd; ++d)
         atomicAdd(&s_hist[d * bins + ((k >> (w * d)) & (bins - 1))], 1u);
     }
   }
-  __syncthreads();
-  for (int d = 0; d < nd; ++d)
-    for (unsigned b = t; b < bins; b += kBlock) {
-      const unsigned v = s_hist[d * bins + b];
-      if (v) atomicAdd(&ctl->hist[d][b], v);
-    }
+  bool bad = false;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) bad |= (unsigned)sv[u] >= (unsigned)num_blocks;
+#pragma unroll 1
+  for (int j0 = gt + 8 * gs; j0 < nnz; j0 += 8 * gs) {
+    int x[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = (j0 + u * gs < nnz) ? slots[j0 + u * gs] : 0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) bad |= (unsigned)x[u] >= (unsigned)num_blocks;
+  }
+  if (__syncthreads_or(bad ? 1 : 0)) {
+    if (t == 0) set_status(info, CASCADE_EINVAL);
+  }
+  // two neighbouring buckets per 64-bit add (a count never exceeds n < 2^32,
+  // so nothing carries into the upper word): half the global atomics
+  const int half = (int)bins >> 1;
+  for (int k = t; k < nd * half; k += kBlock) {
+    const int d = k >> (w - 1), b = (k & (half - 1)) * 2;
+    const unsigned lo = s_hist[d * bins + b], hi = s_hist[d * bins + b + 1];
+    if (lo | hi)
+      atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->hist[d][b]),
+                ((unsigned long long)hi << 32) | lo);
+  }
 }
 
 // ---------------------------------------------------------- radix pass
