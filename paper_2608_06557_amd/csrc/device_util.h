@@ -219,6 +219,7 @@ __device__ __forceinline__ void publish(W *word, W value, unsigned flag) {
 template <typename W, int WIN>
 __device__ __forceinline__ W look_back(const W *status, int stride, int tile, int k,
                                        bool *timed_out) {
+  static_assert(WIN <= 32, "flags of one window fit a 32-bit mask");
   W sum = 0;
   int j = tile - 1;
   unsigned spins = 0;
@@ -228,24 +229,24 @@ __device__ __forceinline__ W look_back(const W *status, int stride, int tile, in
     for (int w = 0; w < WIN; ++w)
       v[w] = (j - w >= 0) ? load_agent(status + (size_t)(j - w) * stride + k)
                           : (W)kFlagInclusive;
-    int consumed = 0;
-    bool done = false, stalled = false;
+    // the window's flags as masks: consume up to the first inclusive prefix,
+    // or up to the first word not yet published
+    unsigned missing = 0, inclusive = 0;
 #pragma unroll
     for (int w = 0; w < WIN; ++w) {
-      if (!done && !stalled) {
-        const unsigned f = (unsigned)(v[w] & 3);
-        if (f == 0) {
-          stalled = true;
-        } else {
-          sum += v[w] >> 2;
-          ++consumed;
-          done = (f == kFlagInclusive);
-        }
-      }
+      const unsigned f = (unsigned)(v[w] & 3);
+      missing |= (f == 0 ? 1u : 0u) << w;
+      inclusive |= (f == kFlagInclusive ? 1u : 0u) << w;
     }
+    const int first_missing = missing ? __builtin_ctz(missing) : WIN;
+    const int first_inclusive = inclusive ? __builtin_ctz(inclusive) : WIN;
+    const bool done = first_inclusive < first_missing;
+    const int take = done ? first_inclusive + 1 : first_missing;
+#pragma unroll
+    for (int w = 0; w < WIN; ++w) sum += w < take ? (v[w] >> 2) : (W)0;
     if (done) return sum;
-    j -= consumed;
-    if (stalled) {
+    j -= take;
+    if (first_missing < WIN) {
       if (++spins > kSpinLimit) {
         *timed_out = true;
         return sum;
