@@ -56,11 +56,16 @@ constexpr int kL2 = 7;           // second-level scan values
 constexpr int kL2Stride = 8;
 
 // Record of one request for the priority-order scan (16 bytes).
-//   x want_blocks, y base_need, z reuse_tokens (HBM prefix or progress)
+//   x want_blocks; for a running prefill (which never restores) the first
+//     entry of its block-table row instead
+//   y base_need, z reuse_tokens (HBM prefix or progress)
 //   w bits 0..19 held blocks, 20..21 state, 22..23 prefix tier,
 //     24..25 group, 26 spill-fits-budget, 27 decode needs a new block
 __device__ __forceinline__ int rec_held(int w) { return w & 0xFFFFF; }
 __device__ __forceinline__ int rec_state(int w) { return (w >> 20) & 3; }
+__device__ __forceinline__ int rec_want(const int4 &r) {
+  return rec_state(r.w) == CASCADE_RUNNING_PREFILL ? 0 : r.x;
+}
 __device__ __forceinline__ int rec_tier(int w) { return (w >> 22) & 3; }
 __device__ __forceinline__ int rec_offl(int w) { return (w >> 26) & 1; }
 __device__ __forceinline__ int rec_decnb(int w) { return (w >> 27) & 1; }
@@ -109,7 +114,6 @@ constexpr size_t kCtlHeaderWords = offsetof(Ctl, hist) / 4;
 struct Sorted {
   unsigned *order;
   int4 *rec;
-  int *ro;
 };
 
 struct Consts {                   // parameters the kernels use, flattened
@@ -309,7 +313,8 @@ __device__ __forceinline__ ReqEval eval_request(const cascade_requests_t &rq,
   r.tnew = tnew;
   r.grp = grp;
   r.biased = biased;
-  r.rec = make_int4((int)want, (int)base_need, (int)reuse_tok,
+  r.rec = make_int4(st_s == CASCADE_RUNNING_PREFILL ? r0 : (int)want, (int)base_need,
+                    (int)reuse_tok,
                     (int)held | ((int)st_s << 20) | ((int)pt_s << 22) | (grp << 24) |
                         (offl << 26) | (decnb << 27));
   r.held = st_s == CASCADE_RUNNING_PREFILL ? held : 0;
@@ -571,7 +576,7 @@ __device__ __forceinline__ void l1_contrib(unsigned *s_l1, int tile, const int4 
   const bool v = tile >= 0;
   const bool rp = v && rec_state(r.w) == CASCADE_RUNNING_PREFILL;
   const unsigned h = rp ? (unsigned)rec_held(r.w) : 0u;
-  unsigned c[kL1] = {v ? (unsigned)r.x : 0u, v ? (unsigned)r.y : 0u, h,
+  unsigned c[kL1] = {v ? (unsigned)rec_want(r) : 0u, v ? (unsigned)r.y : 0u, h,
                      rec_offl(r.w) ? h : 0u, rp ? 1u : 0u};
   const int t0 = __builtin_amdgcn_readfirstlane(tile);
   const bool same = tile == t0;
@@ -606,12 +611,10 @@ template <int kK>
 __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     int n, int passes, Ctl *ctl, int *info, unsigned long long *keys_a,
     unsigned long long *keys_b, unsigned *vals_a, unsigned *vals_b, unsigned *status,
-    const int4 *__restrict__ rec, const int *__restrict__ ro, Sorted srt,
-    unsigned *__restrict__ l1_tot) {
+    const int4 *__restrict__ rec, Sorted srt, unsigned *__restrict__ l1_tot) {
   __shared__ unsigned long long s_keys[kSortTile];
   __shared__ unsigned s_vals[kSortTile];
   __shared__ int4 s_rec[kSortTile];
-  __shared__ int s_ro[kSortTile];
   __shared__ unsigned s_wcnt[kSortWaves][kMaxBins];  // per-wave counts, then starts
   __shared__ int s_start[kMaxBins];  // tile-local start of each digit
   __shared__ int s_off[kMaxBins];    // output offset of each digit
@@ -678,7 +681,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
         const int4 r = rec[p];
         const bool rp = rec_state(r.w) == CASCADE_RUNNING_PREFILL;
         const unsigned h = rp ? (unsigned)rec_held(r.w) : 0u;
-        c[0] += (unsigned)r.x;
+        c[0] += (unsigned)rec_want(r);
         c[1] += (unsigned)r.y;
         c[2] += h;
         c[3] += rec_offl(r.w) ? h : 0u;
@@ -710,10 +713,10 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j)
     dig[j] = (tile_base + local + j * 64 < n) ? (int)((key[j] >> shift) & dmask) : -1;
-  // the last pass carries each request's scan record and row offset along;
-  // the loads are unconditional (index 0 when not needed) so that nothing
-  // waits for them before the tile is ranked
-  int rx[kSortItems], ry[kSortItems], rz[kSortItems], rv[kSortItems], rw[kSortItems];
+  // the last pass carries each request's scan record along; the loads are
+  // unconditional (index 0 when not needed) so that nothing waits for them
+  // before the tile is ranked
+  int rx[kSortItems], ry[kSortItems], rz[kSortItems], rv[kSortItems];
 #pragma unroll
   for (int j = 0; j < kSortItems; ++j) {
     const bool want = last && dig[j] >= 0;
@@ -724,7 +727,6 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     ry[j] = r.y;
     rz[j] = r.z;
     rv[j] = r.w;
-    rw[j] = ro[gi];
   }
   // rank within the wave, item by item (local order: wave, item, lane)
 #pragma unroll
@@ -791,10 +793,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
       s_keys[pos] = key[j];
       s_vals[pos] = val[j];
     }
-    if (ok && last) {
-      s_rec[pos] = make_int4(rx[j], ry[j], rz[j], rv[j]);
-      s_ro[pos] = rw[j];
-    }
+    if (ok && last) s_rec[pos] = make_int4(rx[j], ry[j], rz[j], rv[j]);
   }
   __syncthreads();
   const int count = min(kSortTile, n - tile_base);
@@ -816,7 +815,6 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
         r = s_rec[s];
         srt.order[o] = s_vals[s];
         srt.rec[o] = r;
-        srt.ro[o] = s_ro[s];
       }
       l1_contrib(s_l1, o >= 0 ? o / kScanTile : -1, r);
     } else if (o >= 0) {
@@ -1249,7 +1247,7 @@ __device__ __forceinline__ void scan_positions(int tile, int jn, const ScanConst
     const int w = r4[j].w;
     const bool rp = idx[j] >= 0 && rec_state(w) == CASCADE_RUNNING_PREFILL;
     const long long h = rp ? rec_held(w) : 0;
-    l1[0] += r4[j].x;
+    l1[0] += rec_want(r4[j]);
     l1[1] += r4[j].y;
     l1[2] += h;
     l1[3] += rec_offl(w) ? h : 0;
@@ -1270,7 +1268,7 @@ __device__ __forceinline__ void scan_positions(int tile, int jn, const ScanConst
   for (int j = 0; j < kScanItems; ++j) {
     const int w = r4[j].w;
     const int st = rec_state(w);
-    const long long want = r4[j].x;
+    const long long want = rec_want(r4[j]);
     const long long rj = lmin(wx + want, U) - lmin(wx, U);
     const long long need = (long long)r4[j].y - bt * rj;
     const long long P = bn - bt * lmin(wx, U);  // tokens needed before p
@@ -1324,7 +1322,7 @@ __device__ __forceinline__ void scan_positions(int tile, int jn, const ScanConst
 template <bool kChained>
 __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, int *info,
                                const int (&idx)[kScanItems], const int4 (&r4)[kScanItems],
-                               const int (&row0)[kScanItems], bool broken, const Outs &o,
+                               bool broken, const Outs &o,
                                RpInfo *__restrict__ rp_list,
                                RestoreEnt *__restrict__ restore_list,
                                TileTot *__restrict__ tile_tot, const long long (&pre1)[kL1],
@@ -1411,7 +1409,7 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
       ri.pos = p;
       ri.eligible = adm ? 0 : 1;
       ri.held = (int)hh[j];
-      ri.row0 = row0[j];
+      ri.row0 = r4[j].x;
       ri.offl = rec_offl(w);
       ri.pad[0] = ri.pad[1] = 0;
       ri.x = X + xj;
@@ -1785,28 +1783,23 @@ __device__ __forceinline__ void earlier_totals(const unsigned *__restrict__ l1,
 // index -1.  `broken` is set on an index out of range.
 __device__ __forceinline__ void tile_positions(int n, int tile, int nact, const Sorted &srt,
                                                const int4 *__restrict__ rec,
-                                               const int *__restrict__ ro,
                                                const unsigned (&so)[kScanItems],
                                                const int4 (&sr)[kScanItems],
-                                               const int (&sw)[kScanItems],
                                                int (&idx)[kScanItems], int4 (&r4)[kScanItems],
-                                               int (&rw)[kScanItems], bool &broken) {
+                                               bool &broken) {
   const int p0 = tile * kScanTile + (int)threadIdx.x * kScanItems;
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     const int p = p0 + j;
     int ix = -1;
     int4 r = make_int4(0, 0, 0, 0);
-    int w = 0;
     if (p < n) {
       if (nact == 0) {
         ix = p;
         r = rec[p];
-        w = ro[p];
       } else {
         ix = (int)so[j];
         r = sr[j];
-        w = sw[j];
       }
     }
     if ((unsigned)ix >= (unsigned)n) {  // cannot happen with a correct sort
@@ -1815,21 +1808,19 @@ __device__ __forceinline__ void tile_positions(int n, int tile, int nact, const 
     }
     idx[j] = ix;
     r4[j] = ix >= 0 ? r : make_int4(0, 0, 0, 0);
-    rw[j] = ix >= 0 ? w : 0;
   }
 }
 
 // The sorted entries of the tile's positions (blockIdx.x), requested before
 // anything else.
 __device__ __forceinline__ void load_sorted(int n, const Sorted &srt, unsigned (&so)[kScanItems],
-                                            int4 (&sr)[kScanItems], int (&sw)[kScanItems]) {
+                                            int4 (&sr)[kScanItems]) {
   const int p0 = (int)blockIdx.x * kScanTile + (int)threadIdx.x * kScanItems;
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     const int p = p0 + j;
     so[j] = p < n ? srt.order[p] : 0u;
     sr[j] = p < n ? srt.rec[p] : make_int4(0, 0, 0, 0);
-    sw[j] = p < n ? srt.ro[p] : 0;
   }
 }
 
@@ -1840,24 +1831,23 @@ __device__ __forceinline__ void load_sorted(int n, const Sorted &srt, unsigned (
 // give, so no workgroup waits on another.
 __global__ __launch_bounds__(kBlock) void scan_reduce_kernel(
     int n, Consts c, Ctl *ctl, int *info, Sorted srt, const int4 *__restrict__ rec,
-    const int *__restrict__ ro, const unsigned *__restrict__ l1_tot,
+    const unsigned *__restrict__ l1_tot,
     long long *__restrict__ l2_tot) {
   __shared__ ScanLds s_lds;
   __shared__ int s_bad;
   const int t = threadIdx.x, tile = (int)blockIdx.x;
   unsigned so[kScanItems];
   int4 sr[kScanItems];
-  int sw[kScanItems];
-  load_sorted(n, srt, so, sr, sw);
+  load_sorted(n, srt, so, sr);
   if (t == 0) s_bad = bad_status(load_agent(info));
   const int nact = (int)ctl->nact;
   long long pre1[kL1], pre2_unused[kL2];
   earlier_totals(l1_tot, nullptr, tile, pre1, pre2_unused, s_lds.red);
   if (s_bad) return;
   bool broken = false;
-  int idx[kScanItems], rw[kScanItems];
+  int idx[kScanItems];
   int4 r4[kScanItems];
-  tile_positions(n, tile, nact, srt, rec, ro, so, sr, sw, idx, r4, rw, broken);
+  tile_positions(n, tile, nact, srt, rec, so, sr, idx, r4, broken);
   const ScanConsts K = scan_consts(c, ctl);
   PosVals v;
   scan_positions(tile, kScanItems, K, idx, r4, pre1, s_lds, v);
@@ -1885,7 +1875,7 @@ __global__ __launch_bounds__(kBlock) void scan_reduce_kernel(
 // in finish_kernel.
 __global__ __launch_bounds__(kBlock) void scan_kernel(
     int n, int passes, int n_tiles, Consts c, Ctl *ctl, int *info, Sorted srt,
-    const int4 *__restrict__ rec, const int *__restrict__ ro, const int *__restrict__ slots,
+    const int4 *__restrict__ rec, const int *__restrict__ slots,
     const int *__restrict__ free_slots, Outs o, RpInfo *__restrict__ rp_list,
     RestoreEnt *__restrict__ restore_list, TileTot *__restrict__ tile_tot,
     const unsigned *__restrict__ l1_tot, const long long *__restrict__ l2_tot) {
@@ -1917,8 +1907,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   }
   unsigned so[kScanItems];
   int4 sr[kScanItems];
-  int sw[kScanItems];
-  load_sorted(n, srt, so, sr, sw);
+  load_sorted(n, srt, so, sr);
   if (t == 0) s_bad = bad_status(load_agent(info));
   const int nact = (int)ctl->nact;
   long long pre1[kL1], pre2[kL2];
@@ -1935,14 +1924,14 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   }
   // a live digit beyond the launched passes would leave the keys unsorted
   bool broken = nact > passes;
-  int idx[kScanItems], rw[kScanItems];
+  int idx[kScanItems];
   int4 r4[kScanItems];
-  tile_positions(n, tile, nact, srt, rec, ro, so, sr, sw, idx, r4, rw, broken);
+  tile_positions(n, tile, nact, srt, rec, so, sr, idx, r4, broken);
   const ScanConsts K = scan_consts(c, ctl);
 
   TileOut out;
   const long long rp_incl =
-      scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, rw, broken, o, rp_list,
+      scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, broken, o, rp_list,
                       restore_list, tile_tot, pre1, pre2, s_lds, out);
   if (tile == n_tiles - 1 && t == 0) store_agent(&ctl->n_rp, (int)rp_incl);
   // hand-over: this tile's agent-scope stores complete, then it is counted
@@ -2212,19 +2201,18 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
 
   // ---- Algorithm 1's Phase 2 as one tile: thread t holds positions
   //      t*jn .. t*jn + jn - 1
-  int idx[kScanItems], rw[kScanItems];
+  int idx[kScanItems];
   int4 r4[kScanItems];
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     const int p = t * jn + j;
     idx[j] = (j < jn && p < n) ? (moved ? (int)U.sort.val[p] : p) : -1;
     r4[j] = idx[j] >= 0 ? U.sort.rec[idx[j]] : make_int4(0, 0, 0, 0);
-    rw[j] = idx[j] >= 0 ? ro[idx[j]] : 0;
   }
   const ScanConsts K = scan_consts(c, ctl);
   TileOut out;
   const long long zero1[kL1] = {0, 0, 0, 0, 0}, zero2[kL2] = {0, 0, 0, 0, 0, 0, 0};
-  const long long n_rp = scan_tile<false>(0, jn, K, ctl, info, idx, r4, rw, false, o, rp_list,
+  const long long n_rp = scan_tile<false>(0, jn, K, ctl, info, idx, r4, false, o, rp_list,
                                           restore_list, tile_tot, zero1, zero2, s_lds, out);
   write_tile_outputs(out, o);
   __syncthreads();
@@ -2259,7 +2247,7 @@ __global__ __launch_bounds__(kBlock) void empty_step_kernel(int n_free, int num_
 
 struct Layout {
   size_t ctl, scan1, scan2, sort_status, partials, keys_a, keys_b, vals_a, vals_b, rec,
-      s_order, s_rec, s_ro, rp_list, restore, tile_tot, total;
+      s_order, s_rec, rp_list, restore, tile_tot, total;
   int sort_tiles, scan_tiles, eval_grid;
 };
 
@@ -2287,7 +2275,6 @@ Layout make_layout(int32_t n) {
   L.rec = take(np * 16);
   L.s_order = take(np * 4);
   L.s_rec = take(np * 16);
-  L.s_ro = take(np * 4);
   L.rp_list = take(np * sizeof(RpInfo));
   L.restore = take(np * sizeof(RestoreEnt));
   L.tile_tot = take((size_t)L.scan_tiles * sizeof(TileTot));
@@ -2357,8 +2344,7 @@ int sort_passes(const cascade_params_t *p) {
 }
 
 typedef void (*RadixFn)(int, int, Ctl *, int *, unsigned long long *, unsigned long long *,
-                        unsigned *, unsigned *, unsigned *, const int4 *, const int *, Sorted,
-                        unsigned *);
+                        unsigned *, unsigned *, unsigned *, const int4 *, Sorted, unsigned *);
 static_assert(kMaxPasses == 8, "one radix kernel per pass");
 const RadixFn kRadixKernels[kMaxPasses] = {
     radix_pass_kernel<0>, radix_pass_kernel<1>, radix_pass_kernel<2>, radix_pass_kernel<3>,
@@ -2476,7 +2462,6 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   Sorted srt;
   srt.order = reinterpret_cast<unsigned *>(ws + L.s_order);
   srt.rec = reinterpret_cast<int4 *>(ws + L.s_rec);
-  srt.ro = reinterpret_cast<int *>(ws + L.s_ro);
   auto *l1_tot = reinterpret_cast<unsigned *>(ws + L.scan1);
   auto *l2_tot = reinterpret_cast<long long *>(ws + L.scan2);
 
@@ -2512,13 +2497,13 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   for (int pass = 0; pass < passes; ++pass)
     hipLaunchKernelGGL(kRadixKernels[pass], dim3(L.sort_tiles), dim3(kSortBlock), 0, s, n,
                        passes, ctl, out->info, keys_a, keys_b, vals_a, vals_b,
-                       sort_status + (size_t)pass * L.sort_tiles * kMaxBins, rec,
-                       bt->row_offsets, srt, l1_tot);
+                       sort_status + (size_t)pass * L.sort_tiles * kMaxBins, rec, srt,
+                       l1_tot);
   hipLaunchKernelGGL(scan_reduce_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, c, ctl,
-                     out->info, srt, rec, bt->row_offsets, l1_tot, l2_tot);
+                     out->info, srt, rec, l1_tot, l2_tot);
   hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles + kFinishGrid), dim3(kBlock), 0, s, n,
-                     passes, L.scan_tiles, c, ctl, out->info, srt, rec, bt->row_offsets,
-                     bt->slots, ts->free_slots, o, rp_list, rlist, tile_tot, l1_tot, l2_tot);
+                     passes, L.scan_tiles, c, ctl, out->info, srt, rec, bt->slots,
+                     ts->free_slots, o, rp_list, rlist, tile_tot, l1_tot, l2_tot);
   if (hipGetLastError() != hipSuccess) return CASCADE_EHIP;
   return CASCADE_OK;
 }
