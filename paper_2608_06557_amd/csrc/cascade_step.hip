@@ -1176,7 +1176,7 @@ __device__ __forceinline__ void finish_step(const Ctl *ctl, int *info, int n, in
 // including this tile.
 struct ScanLds {
   long long scan[kWaves * kL2];
-  long long red[kWaves * (kL1 + kL2)];
+  long long red[kWaves * (kL1 + kL2 + 1)];  // earlier tiles' totals and the status flag
 };
 
 // Per-request outputs of one thread's positions, stored after the hand-over.
@@ -1739,14 +1739,18 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
 }
 
 // Sums over tiles j < tile of both levels' per-tile totals (l1[j*kL1 + k],
-// l2[j*kL2Stride + k]), over the workgroup.  Up to 2*kBlock tiles of both
-// are requested at once (one round trip); an earlier launch wrote them, so
-// nothing is polled.  l2 may be null (level 1 only).
-__device__ __forceinline__ void earlier_totals(const unsigned *__restrict__ l1,
+// l2[j*kL2Stride + k]; level 1 only without kWithL2), over the workgroup.
+// Up to 2*kBlock tiles are requested at once (one round trip); an earlier
+// launch wrote them, so nothing is polled.  The step's status word rides
+// along in the same reduction: the return value says whether an earlier
+// kernel reported a failure, the same in every thread.
+template <bool kWithL2>
+__device__ __forceinline__ bool earlier_totals(const unsigned *__restrict__ l1,
                                                const long long *__restrict__ l2, int tile,
-                                               long long (&pre1)[kL1], long long (&pre2)[kL2],
-                                               long long *s_red) {
-  constexpr int kPer = 2, K = kL1 + kL2;
+                                               const int *info, long long (&pre1)[kL1],
+                                               long long (&pre2)[kL2], long long *s_red) {
+  constexpr int kPer = 2, K = kL1 + kL2 + 1;
+  const int st = load_agent(info);
   long long v[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) v[k] = 0;
@@ -1755,26 +1759,30 @@ __device__ __forceinline__ void earlier_totals(const unsigned *__restrict__ l1,
     long long w2[kPer][kL2];
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
+      // unconditional loads (tile 0 stands in past the end), masked after
       const int j = b0 + u * kBlock + (int)threadIdx.x;
-      const bool in = j < tile;
+      const int jc = j < tile ? j : 0;
 #pragma unroll
-      for (int k = 0; k < kL1; ++k) w1[u][k] = in ? l1[(size_t)j * kL1 + k] : 0u;
+      for (int k = 0; k < kL1; ++k) w1[u][k] = l1[(size_t)jc * kL1 + k];
 #pragma unroll
-      for (int k = 0; k < kL2; ++k) w2[u][k] = (in && l2) ? l2[(size_t)j * kL2Stride + k] : 0ll;
+      for (int k = 0; k < kL2; ++k) w2[u][k] = kWithL2 ? l2[(size_t)jc * kL2Stride + k] : 0ll;
     }
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
+      const bool in = b0 + u * kBlock + (int)threadIdx.x < tile;
 #pragma unroll
-      for (int k = 0; k < kL1; ++k) v[k] += (long long)w1[u][k];
+      for (int k = 0; k < kL1; ++k) v[k] += in ? (long long)w1[u][k] : 0ll;
 #pragma unroll
-      for (int k = 0; k < kL2; ++k) v[kL1 + k] += w2[u][k];
+      for (int k = 0; k < kL2; ++k) v[kL1 + k] += in ? w2[u][k] : 0ll;
     }
   }
+  v[K - 1] = (threadIdx.x == 0 && bad_status(st)) ? 1 : 0;
   block_sum<K>(v, s_red);
 #pragma unroll
   for (int k = 0; k < kL1; ++k) pre1[k] = v[k];
 #pragma unroll
   for (int k = 0; k < kL2; ++k) pre2[k] = v[kL1 + k];
+  return v[K - 1] != 0;
 }
 
 // The tile's positions in priority order: request index, scan record and
@@ -1834,16 +1842,13 @@ __global__ __launch_bounds__(kBlock) void scan_reduce_kernel(
     const unsigned *__restrict__ l1_tot,
     long long *__restrict__ l2_tot) {
   __shared__ ScanLds s_lds;
-  __shared__ int s_bad;
   const int t = threadIdx.x, tile = (int)blockIdx.x;
   unsigned so[kScanItems];
   int4 sr[kScanItems];
   load_sorted(n, srt, so, sr);
-  if (t == 0) s_bad = bad_status(load_agent(info));
   const int nact = (int)ctl->nact;
   long long pre1[kL1], pre2_unused[kL2];
-  earlier_totals(l1_tot, nullptr, tile, pre1, pre2_unused, s_lds.red);
-  if (s_bad) return;
+  if (earlier_totals<false>(l1_tot, nullptr, tile, info, pre1, pre2_unused, s_lds.red)) return;
   bool broken = false;
   int idx[kScanItems];
   int4 r4[kScanItems];
@@ -1908,11 +1913,9 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   unsigned so[kScanItems];
   int4 sr[kScanItems];
   load_sorted(n, srt, so, sr);
-  if (t == 0) s_bad = bad_status(load_agent(info));
   const int nact = (int)ctl->nact;
   long long pre1[kL1], pre2[kL2];
-  earlier_totals(l1_tot, l2_tot, tile, pre1, pre2, s_lds.red);
-  if (s_bad) {
+  if (earlier_totals<true>(l1_tot, l2_tot, tile, info, pre1, pre2, s_lds.red)) {
     // counted all the same, so that the finishing workgroups stop waiting
     if (t == 0) {
       const unsigned gi = (unsigned)tile % groups;
