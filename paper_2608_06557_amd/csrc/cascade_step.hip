@@ -103,9 +103,9 @@ struct Ctl {
   int kstar;                      // first position whose blocks do not fit
   long long kx, ky, kz, kzp;      // prefixes just before kstar
   alignas(16) unsigned hist[kMaxPasses][kMaxBins];  // cleared by eval's grid
-  // scan tiles whose hand-over is complete: kTicketGroups counters, then the
-  // count of complete groups (cleared by eval's grid)
-  alignas(128) unsigned done[(kTicketGroups + 1) * kTicketStride];
+  // scan tiles whose hand-over is complete, tile t counted in counter
+  // t % kTicketGroups, one per 128-byte line (cleared by eval's grid)
+  alignas(128) unsigned done[kTicketGroups * kTicketStride];
 };
 constexpr size_t kCtlHeaderWords = offsetof(Ctl, hist) / 4;
 
@@ -1891,17 +1891,25 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   const int t = threadIdx.x, tile = (int)blockIdx.x;
   const unsigned groups = min((unsigned)n_tiles, (unsigned)kTicketGroups);
   if (tile >= n_tiles) {
-    // a finishing workgroup: wait until every scan tile has handed over
-    if (t == 0) {
+    // a finishing workgroup: wait until every scan tile has handed over;
+    // lane g of the first wave watches the counter of tiles g, g + groups, ..
+    if (t < 64) {
+      const unsigned size =
+          (unsigned)t < groups ? ((unsigned)n_tiles - t + groups - 1) / groups : 0u;
       unsigned spins = 0;
-      s_bad = 0;
-      while (load_agent(ctl->done + kTicketGroups * kTicketStride) < groups) {
+      bool late = false;
+      while (true) {
+        const unsigned got = (unsigned)t < groups ? load_agent(ctl->done + t * kTicketStride) : 0u;
+        if (__ballot(got < size) == 0) break;
         if (++spins > kSpinLimit) {
-          set_status(info, CASCADE_ETIMEOUT);
-          s_bad = 1;
+          late = true;
           break;
         }
         __builtin_amdgcn_s_sleep(2);
+      }
+      if (t == 0) {
+        s_bad = late ? 1 : 0;
+        if (late) set_status(info, CASCADE_ETIMEOUT);
       }
     }
     __syncthreads();
@@ -1917,12 +1925,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   long long pre1[kL1], pre2[kL2];
   if (earlier_totals<true>(l1_tot, l2_tot, tile, info, pre1, pre2, s_lds.red)) {
     // counted all the same, so that the finishing workgroups stop waiting
-    if (t == 0) {
-      const unsigned gi = (unsigned)tile % groups;
-      const unsigned size = ((unsigned)n_tiles - gi + groups - 1) / groups;
-      if (atomicAdd(ctl->done + gi * kTicketStride, 1u) == size - 1)
-        atomicAdd(ctl->done + kTicketGroups * kTicketStride, 1u);
-    }
+    if (t == 0) atomicAdd(ctl->done + ((unsigned)tile % groups) * kTicketStride, 1u);
     return;
   }
   // a live digit beyond the launched passes would leave the keys unsorted
@@ -1938,15 +1941,11 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
                       restore_list, tile_tot, pre1, pre2, s_lds, out);
   if (tile == n_tiles - 1 && t == 0) store_agent(&ctl->n_rp, (int)rp_incl);
   // hand-over: this tile's agent-scope stores complete, then it is counted
-  // (two levels of counters); its other outputs follow
+  // (one of kTicketGroups counters, so that no address takes more than a few
+  // dozen adds); its other outputs follow
   wait_stores();
   __syncthreads();
-  if (t == 0) {
-    const unsigned gi = (unsigned)tile % groups;
-    const unsigned size = ((unsigned)n_tiles - gi + groups - 1) / groups;
-    if (atomicAdd(ctl->done + gi * kTicketStride, 1u) == size - 1)
-      atomicAdd(ctl->done + kTicketGroups * kTicketStride, 1u);
-  }
+  if (t == 0) atomicAdd(ctl->done + ((unsigned)tile % groups) * kTicketStride, 1u);
   write_tile_outputs(out, o);
 }
 
