@@ -1240,20 +1240,22 @@ __device__ __forceinline__ void scan_positions(int tile, int jn, const ScanConst
   const long long bt = K.bt, U = K.U, e1 = K.e1, cap = K.cap, cap1 = K.cap1, p_e1 = K.p_e1,
                   g1 = K.g1;
   const int p0 = tile * kScanTile + threadIdx.x * jn;  // items j < jn; the rest absent
-  // ---- level 1
-  long long l1[kL1] = {0, 0, 0, 0, 0}, t1[kL1];
+  // ---- level 1, scanned in 32 bits within the tile: per request the want
+  // and the need are below 2^18 and the held blocks below 2^20, so a tile of
+  // kScanTile requests sums to less than 2^31
+  unsigned l1[kL1] = {0, 0, 0, 0, 0}, t1[kL1];
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     const int w = r4[j].w;
     const bool rp = idx[j] >= 0 && rec_state(w) == CASCADE_RUNNING_PREFILL;
-    const long long h = rp ? rec_held(w) : 0;
-    l1[0] += rec_want(r4[j]);
-    l1[1] += r4[j].y;
+    const unsigned h = rp ? (unsigned)rec_held(w) : 0u;
+    l1[0] += (unsigned)rec_want(r4[j]);
+    l1[1] += (unsigned)r4[j].y;
     l1[2] += h;
-    l1[3] += rec_offl(w) ? h : 0;
-    l1[4] += rp ? 1 : 0;          // running prefills (their compact list)
+    l1[3] += rec_offl(w) ? h : 0u;
+    l1[4] += rp ? 1u : 0u;        // running prefills (their compact list)
   }
-  block_exclusive_scan<kL1>(l1, t1, S.scan);
+  block_exclusive_scan<kL1>(l1, t1, reinterpret_cast<unsigned *>(S.scan));
   long long wx = pre1[0] + l1[0], bn = pre1[1] + l1[1], yy = pre1[2] + l1[2],
             zz = pre1[3] + l1[3];
   v.rp_at = (int)(pre1[4] + l1[4]);
@@ -1333,14 +1335,16 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
   scan_positions(tile, jn, K, idx, r4, pre1, S, v);
   int rp_at = v.rp_at;
   const long long rp_incl = v.rp_incl;
-  long long l2[kL2], t2[kL2];
+  // level-2 values of a tile stay below 2^31 (per request: new blocks plus
+  // held blocks below 2^21), so the tile is scanned in 32 bits
+  unsigned l2[kL2], t2[kL2];
 #pragma unroll
-  for (int k = 0; k < kL2; ++k) l2[k] = v.l2[k];
+  for (int k = 0; k < kL2; ++k) l2[k] = (unsigned)v.l2[k];
   const int *r = v.r, *g = v.g, *nb = v.nb, *hh = v.hh;
   const long long *y_inc = v.y_inc, *zp_inc = v.zp_inc;
 
   // ---- level 2: the earlier tiles' totals (scan_reduce) plus this tile's
-  block_exclusive_scan<kL2>(l2, t2, S.scan);
+  block_exclusive_scan<kL2>(l2, t2, reinterpret_cast<unsigned *>(S.scan));
   long long W = pre2[0] + l2[0], NB = pre2[1] + l2[1], AC = pre2[2] + l2[2],
             X = pre2[3] + l2[3], Z = pre2[4] + l2[4], RR = pre2[5] + l2[5],
             RC = pre2[6] + l2[6];
@@ -1856,11 +1860,14 @@ __global__ __launch_bounds__(kBlock) void scan_reduce_kernel(
   const ScanConsts K = scan_consts(c, ctl);
   PosVals v;
   scan_positions(tile, kScanItems, K, idx, r4, pre1, s_lds, v);
-  block_sum<kL2>(v.l2, s_lds.red);
+  unsigned l2[kL2];  // a tile's level-2 totals stay below 2^31
+#pragma unroll
+  for (int k = 0; k < kL2; ++k) l2[k] = (unsigned)v.l2[k];
+  block_sum<kL2>(l2, reinterpret_cast<unsigned *>(s_lds.red));
   if (t < kL2) {
     long long x = 0;
 #pragma unroll
-    for (int k = 0; k < kL2; ++k) x = k == t ? v.l2[k] : x;
+    for (int k = 0; k < kL2; ++k) x = k == t ? (long long)l2[k] : x;
     l2_tot[(size_t)tile * kL2Stride + t] = x;
   }
   if (broken) set_status(info, CASCADE_EINTERNAL);
