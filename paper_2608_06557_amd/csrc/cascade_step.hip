@@ -1435,8 +1435,10 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
     RR += gp ? r[j] : 0;
     RC += (gp && r[j] > 0) ? 1 : 0;
   }
-  long long tot[8] = {a_nb, a_eh, a_eoh, a_n, a_r, a_rc, 0, broken ? 1 : 0};
-  block_sum<8>(tot, S.red);
+  // a tile's totals stay below 2^31 (per request below 2^21), so 32-bit lanes
+  unsigned tot[8] = {(unsigned)a_nb, (unsigned)a_eh, (unsigned)a_eoh, (unsigned)a_n,
+                     (unsigned)a_r, (unsigned)a_rc, 0u, broken ? 1u : 0u};
+  block_sum<8>(tot, reinterpret_cast<unsigned *>(S.red));
   if (threadIdx.x == 0) {
     TileTot tt;
     tt.adm_nb = tot[0];
@@ -1966,6 +1968,10 @@ constexpr int kSmallMax = kScanTile;
 constexpr int kSmallCheckBlocks = 16384;  // pools up to this size are checked in-kernel
 constexpr int kCheckGrid = 64;
 constexpr int kSmallItems = kScanItems;  // one sort tile and one scan tile per small queue
+constexpr int kSmallRankMax = 512;  // queues up to this size are ordered by counting ranks
+constexpr int kSmallFreeHead = 8;   // list entries per thread requested ahead of their check
+constexpr int kSmallIdxBits = 10;   // request index below the key in the rank sort
+constexpr int kRankRound = 16;      // keys compared per round of LDS reads in the rank sort
 
 struct SmallSortLds {
   unsigned long long key[kSmallMax];
@@ -1978,6 +1984,26 @@ union SmallLds {  // the sort is finished before the finish stages anything
   SmallSortLds sort;
   FinishLds fin;
 };
+
+// Per item j < J: how many of the n keys (the LDS array, padded with
+// all-ones keys to whole rounds) are below mine[j].
+template <int J, int K>
+__device__ __forceinline__ void rank_count(const ulonglong2 *pairs, int n,
+                                           const unsigned long long (&mine)[K], int (&below)[K]) {
+  for (int m = 0; m < n; m += kRankRound) {
+    unsigned long long other[kRankRound];
+#pragma unroll
+    for (int u = 0; u < kRankRound / 2; ++u) {
+      const ulonglong2 q = pairs[m / 2 + u];
+      other[2 * u] = q.x;
+      other[2 * u + 1] = q.y;
+    }
+#pragma unroll
+    for (int u = 0; u < kRankRound; ++u)
+#pragma unroll
+      for (int j = 0; j < J; ++j) below[j] += other[u] < mine[j] ? 1 : 0;
+  }
+}
 
 // Rank of this lane's item among the wave's items with the same 8-bit digit
 // (dig < 0: no item), items taken in (call, lane) order; wcnt[d] counts the
@@ -2043,13 +2069,19 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
     RpInfo *__restrict__ rp_list, RestoreEnt *__restrict__ restore_list,
     TileTot *__restrict__ tile_tot) {
   __shared__ long long s_slo[16];
-  __shared__ long long s_red[kWaves * 3];
-  __shared__ unsigned s_cnt[kWaves * 4];
+  __shared__ unsigned long long s_red[kWaves * 9];
   __shared__ unsigned long long s_mm[kWaves * 4];
   __shared__ int s_scan1[kWaves];
   __shared__ ScanLds s_lds;
   __shared__ SmallLds U;
   const int t = threadIdx.x, lane = lane_id(), wave = wave_id();
+  // the head of the free list is requested first (checked after eval)
+  int fl[kSmallFreeHead];
+#pragma unroll
+  for (int u = 0; u < kSmallFreeHead; ++u) {
+    const int j = t + u * kBlock;
+    fl[u] = (check_lists && j < c.n_free) ? free_slots[j] : 0;
+  }
   if (t < 16) s_slo[t] = c.slo[t];
   if (t == 0) {
     unsigned *w = reinterpret_cast<unsigned *>(ctl);
@@ -2063,148 +2095,212 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
   // ---- evaluation, request j*kBlock + t on thread t (every wave busy); the
   //      raw keys and the records wait in LDS for the sort
   bool bad = false;
-  long long sums[3] = {0, 0, 0};
-  unsigned cnt[4] = {0, 0, 0, 0};
-  unsigned long long mn = ~0ull, mx = 0;
+  // sums (held, need1, want1, three group counts, bad), then min and max
+  unsigned long long v[9] = {0, 0, 0, 0, 0, 0, 0, ~0ull, 0};
 #pragma unroll
   for (int j = 0; j < kSmallItems; ++j) {
     const int i = j * kBlock + t;
     if (i >= n) continue;
     const ReqEval r = eval_request(rq, ro, c, s_slo, i);
     bad |= r.bad;
-    mn = r.biased < mn ? r.biased : mn;
-    mx = r.biased > mx ? r.biased : mx;
-    cnt[r.grp] += 1;
+    v[7] = r.biased < v[7] ? r.biased : v[7];
+    v[8] = r.biased > v[8] ? r.biased : v[8];
+    v[3 + r.grp] += 1;
     budget_out[i] = r.brem;
     tier_out[i] = (uint8_t)r.tnew;
     U.sort.key[i] = ((unsigned long long)r.grp << 62) | r.biased;
     U.sort.rec[i] = r.rec;
-    sums[0] += r.held;
-    sums[1] += r.need1;
-    sums[2] += r.want1;
+    v[0] += (unsigned long long)r.held;
+    v[1] += (unsigned long long)r.need1;
+    v[2] += (unsigned long long)r.want1;
   }
   // the free list in range (large pools: checked by a grid after this kernel)
-  if (check_lists) bad |= any_out_of_range(free_slots, c.n_free, c.num_blocks, t, kBlock);
-  cnt[3] = bad ? 1u : 0u;
-  block_sum<3>(sums, s_red);
-  block_sum<4>(cnt, s_cnt);
-  mn = wave_min(mn);
-  mx = wave_max(mx);
+  if (check_lists) {
+#pragma unroll
+    for (int u = 0; u < kSmallFreeHead; ++u) bad |= (unsigned)fl[u] >= (unsigned)c.num_blocks;
+    const int done = kSmallFreeHead * kBlock;
+    if (c.n_free > done)
+      bad |= any_out_of_range(free_slots + done, c.n_free - done, c.num_blocks, t, kBlock);
+  }
+  v[6] = bad ? 1 : 0;
+#pragma unroll
+  for (int k = 0; k < 7; ++k) v[k] = wave_sum(v[k]);
+  v[7] = wave_min(v[7]);
+  v[8] = wave_max(v[8]);
   if (lane == 0) {
-    s_mm[wave * 2] = mn;
-    s_mm[wave * 2 + 1] = mx;
+#pragma unroll
+    for (int k = 0; k < 9; ++k) s_red[wave * 9 + k] = v[k];
   }
   __syncthreads();
-  mn = ~0ull;
-  mx = 0;
-  for (int w = 0; w < kWaves; ++w) {
-    mn = s_mm[2 * w] < mn ? s_mm[2 * w] : mn;
-    mx = s_mm[2 * w + 1] > mx ? s_mm[2 * w + 1] : mx;
+#pragma unroll
+  for (int k = 0; k < 9; ++k) v[k] = s_red[k];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) {
+#pragma unroll
+    for (int k = 0; k < 7; ++k) v[k] += s_red[w * 9 + k];
+    v[7] = s_red[w * 9 + 7] < v[7] ? s_red[w * 9 + 7] : v[7];
+    v[8] = s_red[w * 9 + 8] > v[8] ? s_red[w * 9 + 8] : v[8];
   }
-  if (cnt[3]) {  // bad request data or free list: nothing below is meaningful
+  const unsigned long long mn = v[7], mx = v[8];
+  const unsigned cnt1 = (unsigned)v[4], cnt2 = (unsigned)v[5];
+  if (v[6]) {  // bad request data or free list: nothing below is meaningful
     if (t == 0) set_status(info, CASCADE_EINVAL);
     return;
-  }
-  // block-table slots, whose extent is only trustworthy now (a large pool's
-  // lists are checked by a grid launched after this kernel)
-  if (check_lists) {
-    const bool bad_slot = any_out_of_range(slots, ro[n], c.num_blocks, t, kBlock);
-    if (__syncthreads_or(bad_slot ? 1 : 0)) {
-      if (t == 0) set_status(info, CASCADE_EINVAL);
-      return;
-    }
   }
   if (t == 0) {
     ctl->bmin = mn;
     ctl->bmax = mx;
-    ctl->held_rp = sums[0];
-    ctl->need1 = sums[1];
-    ctl->want1 = sums[2];
-    ctl->cnt[0] = cnt[0];
-    ctl->cnt[1] = cnt[1];
-    ctl->cnt[2] = cnt[2];
+    ctl->held_rp = (long long)v[0];
+    ctl->need1 = (long long)v[1];
+    ctl->want1 = (long long)v[2];
+    ctl->cnt[0] = (unsigned)v[3];
+    ctl->cnt[1] = cnt1;
+    ctl->cnt[2] = cnt2;
+  }
+  // block-table slots, whose extent is only trustworthy now: requested here,
+  // checked after the sort (a large pool's lists are checked by a grid
+  // launched after this kernel)
+  int sv[kSmallFreeHead];
+  const int nnz = check_lists ? ro[n] : 0;
+#pragma unroll
+  for (int u = 0; u < kSmallFreeHead; ++u) {
+    const int j = t + u * kBlock;
+    sv[u] = j < nnz ? slots[j] : 0;
   }
 
-  // ---- order-preserving key compression, then LSD radix passes in LDS over
-  //      the digits that are not uniform across the queue.  A thread holds
-  //      jn = ceil(n / kBlock) items, item j at position (wave*jn + j)*64 +
-  //      lane: the order in which wave_digit_rank ranks them.
   const int jn = (n + kBlock - 1) / kBlock;
   const unsigned long long span = mx - mn + 1;
-  unsigned long long key[kSmallItems];
-  unsigned val[kSmallItems];
-  unsigned long long k_and = ~0ull, k_or = 0;
-#pragma unroll
-  for (int j = 0; j < kSmallItems; ++j) {
-    const int p = (wave * jn + j) * 64 + lane;
-    key[j] = 0;
-    val[j] = (unsigned)p;
-    if (j >= jn || p >= n) continue;
-    const unsigned long long k0 = U.sort.key[p];
-    key[j] = (k0 >> 62) * span + ((k0 & ((1ull << 62) - 1)) - mn);
-    k_and &= key[j];
-    k_or |= key[j];
-  }
-  for (int off = 32; off >= 1; off >>= 1) {
-    k_and &= __shfl_xor(k_and, off, 64);
-    k_or |= __shfl_xor(k_or, off, 64);
-  }
-  if (lane == 0) {
-    s_mm[2 * kWaves + wave] = k_and;
-    s_mm[3 * kWaves + wave] = k_or;
-  }
-  __syncthreads();
-  unsigned long long varying = 0;
-  {
-    unsigned long long a = ~0ull, b = 0;
-    for (int w = 0; w < kWaves; ++w) {
-      a &= s_mm[2 * kWaves + w];
-      b |= s_mm[3 * kWaves + w];
-    }
-    varying = a ^ b;  // bits that differ between two keys of the queue
-  }
-  const int nd = (key_bits(mn, mx, cnt[1], cnt[2]) + 7) / 8;  // 8-bit digits
+  const int width = key_bits(mn, mx, cnt1, cnt2);
   bool moved = false;
-  for (int d = 0; d < nd; ++d) {
-    if (((varying >> (8 * d)) & 255) == 0) continue;  // uniform: order unchanged
-    moved = true;
-    for (int k = t; k < kWaves * kRadix; k += kBlock) (&U.sort.wcnt[0][0])[k] = 0;
-    __syncthreads();
-    int dig[kSmallItems], rank[kSmallItems];
+  if (n <= kSmallRankMax && width <= 64 - kSmallIdxBits) {
+    // ---- a short queue: every request's place is the number of (key,
+    //      index) pairs below its own, counted over LDS broadcast reads;
+    //      the index below the compressed key keeps equal keys in queue order
 #pragma unroll
     for (int j = 0; j < kSmallItems; ++j) {
-      const int p = (wave * jn + j) * 64 + lane;
-      dig[j] = (j < jn && p < n) ? (int)((key[j] >> (8 * d)) & 255) : -1;
-      rank[j] = j < jn ? wave_digit_rank(dig[j], U.sort.wcnt[wave]) : 0;
-    }
-    __syncthreads();
-    // thread t = digit t: earlier waves' counts, then the digit's start
-    unsigned run = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const unsigned cw = U.sort.wcnt[w][t];
-      U.sort.wcnt[w][t] = run;
-      run += cw;
-    }
-    int st[1] = {(int)run}, tot1[1];
-    block_exclusive_scan<1>(st, tot1, s_scan1);
-    U.sort.start[t] = st[0];
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kSmallItems; ++j) {
-      if (dig[j] < 0) continue;
-      const int pos = U.sort.start[dig[j]] + (int)U.sort.wcnt[wave][dig[j]] + rank[j];
-      U.sort.key[pos] = key[j];
-      U.sort.val[pos] = val[j];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int j = 0; j < kSmallItems; ++j) {
-      const int p = (wave * jn + j) * 64 + lane;
-      if (j < jn && p < n) {
-        key[j] = U.sort.key[p];
-        val[j] = U.sort.val[p];
+      const int i = j * kBlock + t;
+      if (j < jn && i < n) {
+        const unsigned long long k0 = U.sort.key[i];
+        const unsigned long long k = (k0 >> 62) * span + ((k0 & ((1ull << 62) - 1)) - mn);
+        U.sort.key[i] = (k << kSmallIdxBits) | (unsigned)i;
       }
+    }
+    if (t < kRankRound) U.sort.key[n + t] = ~0ull;  // pad to whole rounds: above every key
+    __syncthreads();
+    unsigned long long mine[kSmallRankMax / kBlock];
+    int below[kSmallRankMax / kBlock];
+#pragma unroll
+    for (int j = 0; j < kSmallRankMax / kBlock; ++j) {
+      const int i = j * kBlock + t;
+      mine[j] = i < n ? U.sort.key[i] : ~0ull;
+      below[j] = 0;
+    }
+    // kRankRound keys per round of LDS reads (two per 16-byte read); the
+    // comparisons are VALU-bound, so a thread compares only the items it has
+    const ulonglong2 *pairs = reinterpret_cast<const ulonglong2 *>(U.sort.key);
+    if (jn == 1) {
+      rank_count<1>(pairs, n, mine, below);
+    } else {
+      rank_count<kSmallRankMax / kBlock>(pairs, n, mine, below);
+    }
+#pragma unroll
+    for (int j = 0; j < kSmallRankMax / kBlock; ++j) {
+      const int i = j * kBlock + t;
+      if (i < n) U.sort.val[below[j]] = (unsigned)i;
+    }
+    __syncthreads();
+    moved = true;
+  } else {
+    // ---- order-preserving key compression, then LSD radix passes in LDS over
+    //      the digits that are not uniform across the queue.  A thread holds
+    //      jn = ceil(n / kBlock) items, item j at position (wave*jn + j)*64 +
+    //      lane: the order in which wave_digit_rank ranks them.
+    unsigned long long key[kSmallItems];
+    unsigned val[kSmallItems];
+    unsigned long long k_and = ~0ull, k_or = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallItems; ++j) {
+      const int p = (wave * jn + j) * 64 + lane;
+      key[j] = 0;
+      val[j] = (unsigned)p;
+      if (j >= jn || p >= n) continue;
+      const unsigned long long k0 = U.sort.key[p];
+      key[j] = (k0 >> 62) * span + ((k0 & ((1ull << 62) - 1)) - mn);
+      k_and &= key[j];
+      k_or |= key[j];
+    }
+    for (int off = 32; off >= 1; off >>= 1) {
+      k_and &= __shfl_xor(k_and, off, 64);
+      k_or |= __shfl_xor(k_or, off, 64);
+    }
+    if (lane == 0) {
+      s_mm[2 * kWaves + wave] = k_and;
+      s_mm[3 * kWaves + wave] = k_or;
+    }
+    __syncthreads();
+    unsigned long long varying = 0;
+    {
+      unsigned long long a = ~0ull, b = 0;
+      for (int w = 0; w < kWaves; ++w) {
+        a &= s_mm[2 * kWaves + w];
+        b |= s_mm[3 * kWaves + w];
+      }
+      varying = a ^ b;  // bits that differ between two keys of the queue
+    }
+    const int nd = (width + 7) / 8;  // 8-bit digits
+    for (int d = 0; d < nd; ++d) {
+      if (((varying >> (8 * d)) & 255) == 0) continue;  // uniform: order unchanged
+      moved = true;
+      for (int k = t; k < kWaves * kRadix; k += kBlock) (&U.sort.wcnt[0][0])[k] = 0;
+      __syncthreads();
+      int dig[kSmallItems], rank[kSmallItems];
+#pragma unroll
+      for (int j = 0; j < kSmallItems; ++j) {
+        const int p = (wave * jn + j) * 64 + lane;
+        dig[j] = (j < jn && p < n) ? (int)((key[j] >> (8 * d)) & 255) : -1;
+        rank[j] = j < jn ? wave_digit_rank(dig[j], U.sort.wcnt[wave]) : 0;
+      }
+      __syncthreads();
+      // thread t = digit t: earlier waves' counts, then the digit's start
+      unsigned run = 0;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const unsigned cw = U.sort.wcnt[w][t];
+        U.sort.wcnt[w][t] = run;
+        run += cw;
+      }
+      int st[1] = {(int)run}, tot1[1];
+      block_exclusive_scan<1>(st, tot1, s_scan1);
+      U.sort.start[t] = st[0];
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < kSmallItems; ++j) {
+        if (dig[j] < 0) continue;
+        const int pos = U.sort.start[dig[j]] + (int)U.sort.wcnt[wave][dig[j]] + rank[j];
+        U.sort.key[pos] = key[j];
+        U.sort.val[pos] = val[j];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int j = 0; j < kSmallItems; ++j) {
+        const int p = (wave * jn + j) * 64 + lane;
+        if (j < jn && p < n) {
+          key[j] = U.sort.key[p];
+          val[j] = U.sort.val[p];
+        }
+      }
+    }
+  }
+
+  if (check_lists) {
+    bool bad_slot = false;
+#pragma unroll
+    for (int u = 0; u < kSmallFreeHead; ++u) bad_slot |= (unsigned)sv[u] >= (unsigned)c.num_blocks;
+    const int done = kSmallFreeHead * kBlock;
+    if (nnz > done) bad_slot |= any_out_of_range(slots + done, nnz - done, c.num_blocks, t, kBlock);
+    if (__syncthreads_or(bad_slot ? 1 : 0)) {
+      if (t == 0) set_status(info, CASCADE_EINVAL);
+      return;
     }
   }
 
@@ -2223,11 +2319,11 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
   const long long zero1[kL1] = {0, 0, 0, 0, 0}, zero2[kL2] = {0, 0, 0, 0, 0, 0, 0};
   const long long n_rp = scan_tile<false>(0, jn, K, ctl, info, idx, r4, false, o, rp_list,
                                           restore_list, tile_tot, zero1, zero2, s_lds, out);
+  // the tile's hand-over records (other waves read them in finish_step) are
+  // complete before the barrier; its per-request outputs follow
+  wait_stores();
+  __syncthreads();
   write_tile_outputs(out, o);
-  __syncthreads();
-  if (t == 0) s_cnt[0] = bad_status(load_agent(info)) ? 1u : 0u;
-  __syncthreads();
-  if (s_cnt[0]) return;
   finish_step(ctl, info, n, c.n_free, 1, (int)n_rp, tile_tot, free_slots, rp_list, restore_list,
               slots, o, U.fin);
 }

@@ -65,7 +65,8 @@ def test_configs_full_size(dev, cfg):
     assert_same(g, o, f"config {cfg}")
 
 
-@pytest.mark.parametrize("n", [1, 2, 63, 64, 65, 255, 256, 257, 1023, 1024, 1025, 2047, 2048,
+@pytest.mark.parametrize("n", [1, 2, 63, 64, 65, 255, 256, 257, 511, 512, 513, 1023, 1024, 1025,
+                               2047, 2048,
                                2049, 4095, 4096, 4097, 8193, 12289, 16385, 65535, 65537,
                                131073])
 def test_fuzz_sizes(dev, n):
@@ -186,6 +187,22 @@ def test_wide_keys_nine_bit_digits(dev, seed):
     g, o = run_both(dev, w)
     assert_same(g, o, f"wide keys {seed}")
     assert _key_width(w, o) > 40
+
+
+@pytest.mark.parametrize("n", [37, 300, 512, 700])
+def test_small_queue_keys_over_54_bits(dev, n):
+    """Requests that arrived at time zero under a clock near 2^61 ns clamp their
+    budgets far below the others: keys wider than 54 bits leave no room for
+    the request index below them, so short queues sort by digits instead of
+    counting ranks."""
+    rng = np.random.default_rng(n)
+    p = helpers.base_params(t_now_ns=(1 << 61) + 12345)
+    w = helpers.random_workload(rng, n, params=p)
+    old = rng.random(n) < 0.3
+    w["arrival_ns"] = np.where(old, 0, w["arrival_ns"]).astype(np.int64)
+    g, o = run_both(dev, w)
+    assert_same(g, o, f"wide small {n}")
+    assert _key_width(w, o) > 54
 
 
 def test_empty_queue(dev):
