@@ -42,6 +42,7 @@ constexpr int kSortWaves = kSortBlock / 64;
 constexpr int kSortItems = 4;
 constexpr int kSortTile = kSortBlock * kSortItems;
 constexpr int kSortWin = 32;     // predecessors read per look-back round trip (radix)
+constexpr int kScanWin = 32;     // the same for the scan tiles' level-2 look-back
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
 constexpr int kPrepItems = 8;
@@ -1177,6 +1178,7 @@ __device__ __forceinline__ void finish_step(const Ctl *ctl, int *info, int n, in
 struct ScanLds {
   long long scan[kWaves * kL2];
   long long red[kWaves * (kL1 + kL2 + 1)];  // earlier tiles' totals and the status flag
+  long long pre2[kL2];                      // the earlier tiles' level-2 totals (look-back)
 };
 
 // Per-request outputs of one thread's positions, stored after the hand-over.
@@ -1328,7 +1330,7 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
                                RpInfo *__restrict__ rp_list,
                                RestoreEnt *__restrict__ restore_list,
                                TileTot *__restrict__ tile_tot, const long long (&pre1)[kL1],
-                               const long long (&pre2)[kL2], ScanLds &S, TileOut &out) {
+                               unsigned long long *l2_status, ScanLds &S, TileOut &out) {
   const long long fh = K.fh;
   const int p0 = tile * kScanTile + threadIdx.x * jn;
   PosVals v;
@@ -1343,8 +1345,35 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
   const int *r = v.r, *g = v.g, *nb = v.nb, *hh = v.hh;
   const long long *y_inc = v.y_inc, *zp_inc = v.zp_inc;
 
-  // ---- level 2: the earlier tiles' totals (scan_reduce) plus this tile's
+  // ---- level 2: the earlier tiles' totals plus this tile's.  Chained, the
+  //      tile publishes its totals and takes the earlier tiles' from a
+  //      decoupled look-back (thread k for value k); alone, they are zero.
   block_exclusive_scan<kL2>(l2, t2, reinterpret_cast<unsigned *>(S.scan));
+  long long pre2[kL2] = {0, 0, 0, 0, 0, 0, 0};
+  if (kChained) {
+    const int t = threadIdx.x;
+    if (t < kL2) {
+      unsigned agg = 0;
+#pragma unroll
+      for (int k = 0; k < kL2; ++k) agg = k == t ? t2[k] : agg;
+      unsigned long long *st = l2_status + (size_t)tile * kL2Stride + t;
+      unsigned long long before = 0;
+      if (tile == 0) {
+        publish<unsigned long long>(st, agg, kFlagInclusive);
+      } else {
+        publish<unsigned long long>(st, agg, kFlagAggregate);
+        bool timed_out = false;
+        before = look_back<unsigned long long, kScanWin>(l2_status, kL2Stride, tile, t,
+                                                         &timed_out);
+        publish<unsigned long long>(st, before + agg, kFlagInclusive);
+        if (timed_out) set_status(info, CASCADE_ETIMEOUT);
+      }
+      S.pre2[t] = (long long)before;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kL2; ++k) pre2[k] = S.pre2[k];
+  }
   long long W = pre2[0] + l2[0], NB = pre2[1] + l2[1], AC = pre2[2] + l2[2],
             X = pre2[3] + l2[3], Z = pre2[4] + l2[4], RR = pre2[5] + l2[5],
             RC = pre2[6] + l2[6];
@@ -1454,19 +1483,6 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
   return rp_incl;
 }
 
-// Algorithm 1's Phase 2 loop in priority order as prefix sums.
-// Level 1 (independent of earlier decisions): restore want, base token need,
-// blocks held by running prefills (all / spill-fits).  They give the restore
-// blocks r (eq:max_restorable under the per-step cap U), the exact token need
-// and the chunked-prefill grant g of every position.
-// Level 2 (functions of g): block weight of the admission test, new blocks
-// of admitted requests, admitted count, held blocks of running prefills left
-// out (all / spill-fits), restored blocks and restoring requests.
-// Both levels use one decoupled look-back each, chained inside the launch.
-// The sorted order, records and row offsets come from the last radix pass
-// (the identity order when every key is equal), so one coalesced read feeds
-// the tile.  Each tile hands its results to the finishing workgroup with
-// agent-scope stores and a ticket, then writes its other outputs.
 // ---------------------------------------------------------------- finish
 
 // The victims, slot list and move lists of a large queue, computed by
@@ -1838,43 +1854,6 @@ __device__ __forceinline__ void load_sorted(int n, const Sorted &srt, unsigned (
   }
 }
 
-// Level-2 totals of every scan tile (Algorithm 1's Phase 2 values that
-// depend on the grants: admission weight, new blocks, admitted count, held
-// blocks left out (all / spill-fits), restored blocks, restoring requests).
-// A tile's grants need only its level-1 prefix, which the sort's totals
-// give, so no workgroup waits on another.
-__global__ __launch_bounds__(kBlock) void scan_reduce_kernel(
-    int n, Consts c, Ctl *ctl, int *info, Sorted srt, const int4 *__restrict__ rec,
-    const unsigned *__restrict__ l1_tot,
-    long long *__restrict__ l2_tot) {
-  __shared__ ScanLds s_lds;
-  const int t = threadIdx.x, tile = (int)blockIdx.x;
-  unsigned so[kScanItems];
-  int4 sr[kScanItems];
-  load_sorted(n, srt, so, sr);
-  const int nact = (int)ctl->nact;
-  long long pre1[kL1], pre2_unused[kL2];
-  if (earlier_totals<false>(l1_tot, nullptr, tile, info, pre1, pre2_unused, s_lds.red)) return;
-  bool broken = false;
-  int idx[kScanItems];
-  int4 r4[kScanItems];
-  tile_positions(n, tile, nact, srt, rec, so, sr, idx, r4, broken);
-  const ScanConsts K = scan_consts(c, ctl);
-  PosVals v;
-  scan_positions(tile, kScanItems, K, idx, r4, pre1, s_lds, v);
-  unsigned l2[kL2];  // a tile's level-2 totals stay below 2^31
-#pragma unroll
-  for (int k = 0; k < kL2; ++k) l2[k] = (unsigned)v.l2[k];
-  block_sum<kL2>(l2, reinterpret_cast<unsigned *>(s_lds.red));
-  if (t < kL2) {
-    long long x = 0;
-#pragma unroll
-    for (int k = 0; k < kL2; ++k) x = k == t ? (long long)l2[k] : x;
-    l2_tot[(size_t)tile * kL2Stride + t] = x;
-  }
-  if (broken) set_status(info, CASCADE_EINTERNAL);
-}
-
 // Algorithm 1's Phase 2 loop in priority order as prefix sums.
 // Level 1 (independent of earlier decisions): restore want, base token need,
 // blocks held by running prefills (all / spill-fits).  They give the restore
@@ -1883,16 +1862,17 @@ __global__ __launch_bounds__(kBlock) void scan_reduce_kernel(
 // Level 2 (functions of g): block weight of the admission test, new blocks
 // of admitted requests, admitted count, held blocks of running prefills left
 // out (all / spill-fits), restored blocks and restoring requests.
-// A tile's prefixes of both levels are sums of the earlier tiles' totals
-// (the sort's and scan_reduce's), requested with its sorted records, so no
-// workgroup waits on another.  The victims, slot list and move lists follow
-// in finish_kernel.
+// A tile's level-1 prefix is the sum of the earlier tiles' totals (added by
+// the last radix pass), requested with its sorted records; its level-2
+// prefix comes from a decoupled look-back over the totals the earlier tiles
+// publish.  Workgroups past the last tile finish the step (victims, slot
+// list, move lists) once every tile has handed over.
 __global__ __launch_bounds__(kBlock) void scan_kernel(
     int n, int passes, int n_tiles, Consts c, Ctl *ctl, int *info, Sorted srt,
     const int4 *__restrict__ rec, const int *__restrict__ slots,
     const int *__restrict__ free_slots, Outs o, RpInfo *__restrict__ rp_list,
     RestoreEnt *__restrict__ restore_list, TileTot *__restrict__ tile_tot,
-    const unsigned *__restrict__ l1_tot, const long long *__restrict__ l2_tot) {
+    const unsigned *__restrict__ l1_tot, unsigned long long *l2_status) {
   __shared__ ScanLds s_lds;
   __shared__ FinishAnyLds s_fin;
   __shared__ int s_bad;
@@ -1931,9 +1911,12 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   int4 sr[kScanItems];
   load_sorted(n, srt, so, sr);
   const int nact = (int)ctl->nact;
-  long long pre1[kL1], pre2[kL2];
-  if (earlier_totals<true>(l1_tot, l2_tot, tile, info, pre1, pre2, s_lds.red)) {
-    // counted all the same, so that the finishing workgroups stop waiting
+  long long pre1[kL1], pre2_unused[kL2];
+  if (earlier_totals<false>(l1_tot, nullptr, tile, info, pre1, pre2_unused, s_lds.red)) {
+    // a failed step: the look-back words say "nothing before me", so no later
+    // tile waits, and the tile is counted, so the finishing workgroups stop
+    if (t < kL2) publish<unsigned long long>(l2_status + (size_t)tile * kL2Stride + t, 0ull,
+                                             kFlagInclusive);
     if (t == 0) atomicAdd(ctl->done + ((unsigned)tile % groups) * kTicketStride, 1u);
     return;
   }
@@ -1947,7 +1930,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   TileOut out;
   const long long rp_incl =
       scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, broken, o, rp_list,
-                      restore_list, tile_tot, pre1, pre2, s_lds, out);
+                      restore_list, tile_tot, pre1, l2_status, s_lds, out);
   if (tile == n_tiles - 1 && t == 0) store_agent(&ctl->n_rp, (int)rp_incl);
   // hand-over: this tile's agent-scope stores complete, then it is counted
   // (one of kTicketGroups counters, so that no address takes more than a few
@@ -2316,9 +2299,9 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
   }
   const ScanConsts K = scan_consts(c, ctl);
   TileOut out;
-  const long long zero1[kL1] = {0, 0, 0, 0, 0}, zero2[kL2] = {0, 0, 0, 0, 0, 0, 0};
+  const long long zero1[kL1] = {0, 0, 0, 0, 0};
   const long long n_rp = scan_tile<false>(0, jn, K, ctl, info, idx, r4, false, o, rp_list,
-                                          restore_list, tile_tot, zero1, zero2, s_lds, out);
+                                          restore_list, tile_tot, zero1, nullptr, s_lds, out);
   // the tile's hand-over records (other waves read them in finish_step) are
   // complete before the barrier; its per-request outputs follow
   wait_stores();
@@ -2370,7 +2353,7 @@ Layout make_layout(int32_t n) {
   // the look-back status words follow the control block: one clear covers
   // them, the sort's words last (only the launched passes' are cleared)
   L.scan1 = take((size_t)L.scan_tiles * kL1 * 4);  // level-1 totals per scan tile
-  L.scan2 = take((size_t)L.scan_tiles * kL2Stride * 8);  // level-2 totals per scan tile
+  L.scan2 = take((size_t)L.scan_tiles * kL2Stride * 8);  // level-2 look-back words per scan tile
   L.sort_status = take((size_t)kMaxPasses * L.sort_tiles * kMaxBins * 4);
   L.partials = take((size_t)L.eval_grid * sizeof(Partial));
   L.keys_a = take(np * 8);
@@ -2568,7 +2551,7 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   srt.order = reinterpret_cast<unsigned *>(ws + L.s_order);
   srt.rec = reinterpret_cast<int4 *>(ws + L.s_rec);
   auto *l1_tot = reinterpret_cast<unsigned *>(ws + L.scan1);
-  auto *l2_tot = reinterpret_cast<long long *>(ws + L.scan2);
+  auto *l2_status = reinterpret_cast<unsigned long long *>(ws + L.scan2);
 
   if (n <= kSmallMax) {
     // one workgroup; it checks the free list and the slots itself unless the
@@ -2604,11 +2587,9 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
                        passes, ctl, out->info, keys_a, keys_b, vals_a, vals_b,
                        sort_status + (size_t)pass * L.sort_tiles * kMaxBins, rec, srt,
                        l1_tot);
-  hipLaunchKernelGGL(scan_reduce_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, c, ctl,
-                     out->info, srt, rec, l1_tot, l2_tot);
   hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles + kFinishGrid), dim3(kBlock), 0, s, n,
                      passes, L.scan_tiles, c, ctl, out->info, srt, rec, bt->slots,
-                     ts->free_slots, o, rp_list, rlist, tile_tot, l1_tot, l2_tot);
+                     ts->free_slots, o, rp_list, rlist, tile_tot, l1_tot, l2_status);
   if (hipGetLastError() != hipSuccess) return CASCADE_EHIP;
   return CASCADE_OK;
 }

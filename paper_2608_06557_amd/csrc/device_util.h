@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace cascade {
 
 constexpr int kBlock = 256;          // threads per workgroup (4 wave64s)
@@ -219,7 +221,7 @@ __device__ __forceinline__ void publish(W *word, W value, unsigned flag) {
 template <typename W, int WIN>
 __device__ __forceinline__ W look_back(const W *status, int stride, int tile, int k,
                                        bool *timed_out) {
-  static_assert(WIN <= 32, "flags of one window fit a 32-bit mask");
+  static_assert(WIN <= 64, "flags of one window fit a 64-bit mask");
   W sum = 0;
   int j = tile - 1;
   unsigned spins = 0;
@@ -231,15 +233,16 @@ __device__ __forceinline__ W look_back(const W *status, int stride, int tile, in
                           : (W)kFlagInclusive;
     // the window's flags as masks: consume up to the first inclusive prefix,
     // or up to the first word not yet published
-    unsigned missing = 0, inclusive = 0;
+    typedef typename std::conditional<(WIN > 32), unsigned long long, unsigned>::type Mask;
+    Mask missing = 0, inclusive = 0;
 #pragma unroll
     for (int w = 0; w < WIN; ++w) {
       const unsigned f = (unsigned)(v[w] & 3);
-      missing |= (f == 0 ? 1u : 0u) << w;
-      inclusive |= (f == kFlagInclusive ? 1u : 0u) << w;
+      missing |= (Mask)(f == 0 ? 1u : 0u) << w;
+      inclusive |= (Mask)(f == kFlagInclusive ? 1u : 0u) << w;
     }
-    const int first_missing = missing ? __builtin_ctz(missing) : WIN;
-    const int first_inclusive = inclusive ? __builtin_ctz(inclusive) : WIN;
+    const int first_missing = missing ? __builtin_ctzll(missing) : WIN;
+    const int first_inclusive = inclusive ? __builtin_ctzll(inclusive) : WIN;
     const bool done = first_inclusive < first_missing;
     const int take = done ? first_inclusive + 1 : first_missing;
 #pragma unroll
