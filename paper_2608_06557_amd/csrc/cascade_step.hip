@@ -669,7 +669,13 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   const unsigned active = ((1u << P.nd) - 1u) & ~s_mask;
   const int nact = __builtin_popcount(active);
   if (kK == 0 && blockIdx.x == 0 && t == 0) store_agent(&ctl->nact, (unsigned)nact);
-  if (s_bad) return;
+  if (s_bad) {
+    // a failed step: "nothing before me" in every bin, so no later tile of
+    // this pass waits on this one
+    if (nact > kK)
+      publish<unsigned>(status + (size_t)blockIdx.x * kMaxBins + t, 0u, kFlagInclusive);
+    return;
+  }
   if (kK == 0 && nact == 0) {
     // every key equal: the order is the identity; this sort tile's scan
     // tiles get their level-1 totals here

@@ -249,6 +249,36 @@ def test_einval_matches(dev, name, mutate):
     assert status == ref.EINVAL, name
 
 
+@pytest.mark.parametrize("field", ["state", "slot", "row"])
+def test_einval_on_the_multi_launch_path(dev, field):
+    """Bad request data in a queue of 20000 requests: the radix passes and
+    the scan tiles stop at the failed status without waiting on each other
+    (a wait would run to its poll limit and report a timeout instead)."""
+    import time
+    import torch
+    import paper_2608_06557_amd.synth as synth
+    w = synth.make_workload(2, seed=5, n=20000)
+    if field == "state":
+        w["state"] = w["state"].copy()
+        w["state"][12345] = 7
+    elif field == "slot":
+        w["slots"] = w["slots"].copy()
+        w["slots"][len(w["slots"]) // 2] = w["params"]["num_blocks"]
+    else:
+        w["row_offsets"] = w["row_offsets"].copy()
+        w["row_offsets"][9000:] += 1
+    assert ref.step(w)["rc"] == ref.EINVAL
+    d = dev.DeviceStep(w)
+    assert d.run() == 0
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    assert d.run() == 0
+    status = d.fetch()["status"]
+    elapsed = time.perf_counter() - t0
+    assert status == ref.EINVAL, (field, status)
+    assert elapsed < 0.05, elapsed
+
+
 @pytest.mark.parametrize("which", ["slot", "free_slot", "none"])
 def test_small_queue_large_pool_list_checks(dev, which):
     """A queue of at most 1024 requests runs as one workgroup; over a pool
