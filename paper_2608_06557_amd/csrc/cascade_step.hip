@@ -12,18 +12,24 @@
 // dependent launches on one stream:
 //   eval      one lane per request: validation, budget, tier, restore want,
 //             priority key, scan record; per-workgroup partial totals (no
-//             atomics); also clears this step's histograms and look-back words
+//             atomics); also clears this step's histograms, tile totals and
+//             look-back words
 //   prep      totals of the partials, key compression to the live budget
-//             range, every digit histogram in one read
-//   radix<p>  onesweep LSD radix pass p (wave64 ballot ranking, per-digit
-//             decoupled look-back), launched for the digits a host-side bound
-//             allows; a digit that is constant or beyond the live key width
-//             returns at once, decided on the device
-//   scan      Algorithm 1's loop as prefix sums in priority order: two chained
-//             decoupled look-backs in one launch; the last workgroup to finish
-//             picks the preemption victims and writes the slot list and the
-//             pack / unpack move lists
-// All arithmetic is 64-bit integer, so the result is bit-exact.
+//             range, every digit histogram in one read, block-table checks
+//   radix<p>  onesweep LSD radix pass p over 2048-key tiles (wave64 ballot
+//             ranking, per-digit decoupled look-back), launched for the
+//             passes a host-side bound on the key width allows; 8- or 9-bit
+//             digits and the digits that move data are decided on the device.
+//             The last data-moving pass writes the sorted order with each
+//             request's scan record and adds every scan tile's level-1 totals
+//   scan      Algorithm 1's loop as prefix sums in priority order over
+//             1024-position tiles (level-2 prefix by a decoupled look-back);
+//             the launch's last 32 workgroups wait for every tile's hand-over,
+//             then pick the preemption victims and write the slot list and
+//             the pack / unpack move lists
+// A queue of at most 1024 requests runs the whole step in one workgroup.
+// All arithmetic is integer (64-bit, or 32-bit where a bound allows it), so
+// the result is bit-exact.
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
