@@ -48,7 +48,6 @@ constexpr int kSortWaves = kSortBlock / 64;
 constexpr int kSortItems = 4;
 constexpr int kSortTile = kSortBlock * kSortItems;
 constexpr int kSortWin = 32;     // predecessors read per look-back round trip (radix)
-constexpr int kScanWin = 32;     // the same for the scan tiles' level-2 look-back
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
 constexpr int kPrepItems = 8;
@@ -60,7 +59,7 @@ constexpr int kRadix = 256;      // one workgroup's LDS sort of a small queue: 8
 constexpr int kL1 = 5;           // first-level scan values
 constexpr int kMaxScanTiles = ((1 << 20) + kScanTile - 1) / kScanTile;
 constexpr int kL2 = 7;           // second-level scan values
-constexpr int kL2Stride = 8;
+constexpr int kL2Stride = 16;    // level-2 look-back words: one 128-byte line per tile
 
 // Record of one request for the priority-order scan (16 bytes).
 //   x want_blocks; for a running prefill (which never restores) the first
@@ -1335,6 +1334,56 @@ __device__ __forceinline__ void scan_positions(int tile, int jn, const ScanConst
   }
 }
 
+// The earlier tiles' level-2 totals, by one wave: lane l reads tile
+// next - l, so a round trip covers 64 predecessors.  Each of the kL2 values
+// has its own flags and its own stopping point (the words of one tile are
+// published separately): a ballot finds the first unpublished and the first
+// inclusive word, and a wave sum adds the words before it.  Called by all 64
+// lanes of one wave; the sums come back in every lane.
+__device__ __forceinline__ void wave_look_back(const unsigned long long *status, int tile,
+                                               unsigned long long (&pre)[kL2], bool *timed_out) {
+  const int lane = lane_id();
+  int next[kL2];
+#pragma unroll
+  for (int k = 0; k < kL2; ++k) next[k] = tile - 1;
+  unsigned spins = 0;
+  while (true) {
+    bool pending = false;
+#pragma unroll
+    for (int k = 0; k < kL2; ++k) pending |= next[k] >= 0;
+    if (!pending) return;
+    unsigned long long w[kL2];
+#pragma unroll
+    for (int k = 0; k < kL2; ++k) {
+      const int j = next[k] - lane;
+      w[k] = j >= 0 ? load_agent(status + (size_t)j * kL2Stride + k)
+                    : (unsigned long long)kFlagInclusive;
+    }
+    bool stalled = false;
+#pragma unroll
+    for (int k = 0; k < kL2; ++k) {
+      if (next[k] < 0) continue;
+      const unsigned f = (unsigned)(w[k] & 3);
+      const uint64_t missing = __ballot(f == 0);
+      const uint64_t inclusive = __ballot(f == kFlagInclusive);
+      const int first_missing = missing ? __builtin_ctzll(missing) : 64;
+      const int first_inclusive = inclusive ? __builtin_ctzll(inclusive) : 64;
+      const bool done = first_inclusive < first_missing;
+      const int take = done ? first_inclusive + 1 : first_missing;
+      pre[k] += wave_sum(lane < take ? (w[k] >> 2) : 0ull);
+      next[k] = done ? -1 : next[k] - take;
+      stalled |= first_missing < 64 && !done;
+    }
+    if (stalled) {
+      if (++spins > kSpinLimit) {
+        *timed_out = true;
+        return;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  }
+}
+
 template <bool kChained>
 __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, int *info,
                                const int (&idx)[kScanItems], const int4 (&r4)[kScanItems],
@@ -1364,23 +1413,26 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
   long long pre2[kL2] = {0, 0, 0, 0, 0, 0, 0};
   if (kChained) {
     const int t = threadIdx.x;
-    if (t < kL2) {
+    if (t < 64) {
       unsigned agg = 0;
 #pragma unroll
       for (int k = 0; k < kL2; ++k) agg = k == t ? t2[k] : agg;
       unsigned long long *st = l2_status + (size_t)tile * kL2Stride + t;
-      unsigned long long before = 0;
-      if (tile == 0) {
-        publish<unsigned long long>(st, agg, kFlagInclusive);
-      } else {
-        publish<unsigned long long>(st, agg, kFlagAggregate);
+      if (t < kL2) publish<unsigned long long>(st, agg, tile == 0 ? kFlagInclusive : kFlagAggregate);
+      unsigned long long before[kL2] = {0, 0, 0, 0, 0, 0, 0};
+      if (tile > 0) {
         bool timed_out = false;
-        before = look_back<unsigned long long, kScanWin>(l2_status, kL2Stride, tile, t,
-                                                         &timed_out);
-        publish<unsigned long long>(st, before + agg, kFlagInclusive);
-        if (timed_out) set_status(info, CASCADE_ETIMEOUT);
+        wave_look_back(l2_status, tile, before, &timed_out);
+        unsigned long long mine = 0;
+#pragma unroll
+        for (int k = 0; k < kL2; ++k) mine = k == t ? before[k] : mine;
+        if (t < kL2) publish<unsigned long long>(st, mine + agg, kFlagInclusive);
+        if (timed_out && t == 0) set_status(info, CASCADE_ETIMEOUT);
       }
-      S.pre2[t] = (long long)before;
+      if (t == 0) {
+#pragma unroll
+        for (int k = 0; k < kL2; ++k) S.pre2[k] = (long long)before[k];
+      }
     }
     __syncthreads();
 #pragma unroll
@@ -1772,25 +1824,21 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
   }
 }
 
-// Sums over tiles j < tile of both levels' per-tile totals (l1[j*kL1 + k],
-// l2[j*kL2Stride + k]; level 1 only without kWithL2), over the workgroup.
-// Up to 2*kBlock tiles are requested at once (one round trip); an earlier
-// launch wrote them, so nothing is polled.  The step's status word rides
-// along in the same reduction: the return value says whether an earlier
-// kernel reported a failure, the same in every thread.
-template <bool kWithL2>
-__device__ __forceinline__ bool earlier_totals(const unsigned *__restrict__ l1,
-                                               const long long *__restrict__ l2, int tile,
+// Sums over tiles j < tile of the level-1 totals (l1[j*kL1 + k]), over the
+// workgroup.  Up to 2*kBlock tiles are requested at once (one round trip);
+// an earlier launch wrote them, so nothing is polled.  The step's status
+// word rides along in the same reduction: the return value says whether an
+// earlier kernel reported a failure, the same in every thread.
+__device__ __forceinline__ bool earlier_totals(const unsigned *__restrict__ l1, int tile,
                                                const int *info, long long (&pre1)[kL1],
-                                               long long (&pre2)[kL2], long long *s_red) {
-  constexpr int kPer = 2, K = kL1 + kL2 + 1;
+                                               long long *s_red) {
+  constexpr int kPer = 2, K = kL1 + 1;
   const int st = load_agent(info);
   long long v[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) v[k] = 0;
   for (int b0 = 0; b0 < tile; b0 += kPer * kBlock) {
     unsigned w1[kPer][kL1];
-    long long w2[kPer][kL2];
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
       // unconditional loads (tile 0 stands in past the end), masked after
@@ -1798,24 +1846,18 @@ __device__ __forceinline__ bool earlier_totals(const unsigned *__restrict__ l1,
       const int jc = j < tile ? j : 0;
 #pragma unroll
       for (int k = 0; k < kL1; ++k) w1[u][k] = l1[(size_t)jc * kL1 + k];
-#pragma unroll
-      for (int k = 0; k < kL2; ++k) w2[u][k] = kWithL2 ? l2[(size_t)jc * kL2Stride + k] : 0ll;
     }
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
       const bool in = b0 + u * kBlock + (int)threadIdx.x < tile;
 #pragma unroll
       for (int k = 0; k < kL1; ++k) v[k] += in ? (long long)w1[u][k] : 0ll;
-#pragma unroll
-      for (int k = 0; k < kL2; ++k) v[kL1 + k] += in ? w2[u][k] : 0ll;
     }
   }
   v[K - 1] = (threadIdx.x == 0 && bad_status(st)) ? 1 : 0;
   block_sum<K>(v, s_red);
 #pragma unroll
   for (int k = 0; k < kL1; ++k) pre1[k] = v[k];
-#pragma unroll
-  for (int k = 0; k < kL2; ++k) pre2[k] = v[kL1 + k];
   return v[K - 1] != 0;
 }
 
@@ -1923,8 +1965,8 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   int4 sr[kScanItems];
   load_sorted(n, srt, so, sr);
   const int nact = (int)ctl->nact;
-  long long pre1[kL1], pre2_unused[kL2];
-  if (earlier_totals<false>(l1_tot, nullptr, tile, info, pre1, pre2_unused, s_lds.red)) {
+  long long pre1[kL1];
+  if (earlier_totals(l1_tot, tile, info, pre1, s_lds.red)) {
     // a failed step: the look-back words say "nothing before me", so no later
     // tile waits, and the tile is counted, so the finishing workgroups stop
     if (t < kL2) publish<unsigned long long>(l2_status + (size_t)tile * kL2Stride + t, 0ull,
