@@ -52,6 +52,7 @@ constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
 constexpr int kPrepItems = 8;
 constexpr int kEvalItems = 1;
+static_assert(kBlock * kEvalItems <= 2048, "an eval workgroup's sums fit 32 bits");
 constexpr int kMaxW = 9;         // widest digit of the multi-launch sort
 constexpr int kMaxBins = 1 << kMaxW;
 constexpr int kMaxPasses = (64 + kMaxW - 1) / kMaxW;  // passes of the multi-launch sort, at most
@@ -336,21 +337,22 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
     uint8_t *__restrict__ tier_out, unsigned long long *__restrict__ keys,
     int4 *__restrict__ rec) {
   __shared__ long long s_slo[16];
-  __shared__ long long s_red[kWaves * 3];
   __shared__ unsigned long long s_mm[kWaves * 2];
-  __shared__ unsigned s_cnt[kWaves * 4];
+  __shared__ unsigned s_cnt[kWaves * 7];
   if (threadIdx.x < 16) s_slo[threadIdx.x] = c.slo[threadIdx.x];
 
   const size_t gt = (size_t)blockIdx.x * kBlock + threadIdx.x;
   const size_t gs = (size_t)gridDim.x * kBlock;
-  // this step's histograms and look-back status words start at zero
+  // this step's histograms and look-back status words start at zero; the
+  // first workgroup resets the control block's header and the info words
   for (size_t j = gt; j < clear_vec; j += gs) clear[j] = make_uint4(0, 0, 0, 0);
-  if (gt == 0) {
-    unsigned *w = reinterpret_cast<unsigned *>(ctl);
-    for (size_t k = 0; k < kCtlHeaderWords; ++k) w[k] = 0;
-    ctl->kstar = n;
-    for (int k = 0; k < CASCADE_INFO_LEN; ++k) info[k] = 0;
-    info[CASCADE_INFO_N_SLOT_LIST] = c.n_free;
+  if (blockIdx.x == 0) {
+    const int t = threadIdx.x;
+    constexpr int kKstarWord = offsetof(Ctl, kstar) / 4;
+    static_assert(kCtlHeaderWords <= kBlock && CASCADE_INFO_LEN <= kBlock, "one word per thread");
+    if (t < (int)kCtlHeaderWords)
+      reinterpret_cast<unsigned *>(ctl)[t] = t == kKstarWord ? (unsigned)n : 0u;
+    if (t < CASCADE_INFO_LEN) info[t] = t == CASCADE_INFO_N_SLOT_LIST ? c.n_free : 0;
   }
   __syncthreads();
 
@@ -382,33 +384,41 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
     v_need1 += r.need1;
     v_want1 += r.want1;
   }
-  // workgroup totals, one plain store per workgroup
-  long long sums[3] = {v_held, v_need1, v_want1};
-  block_sum<3>(sums, s_red);
-  unsigned cnt[4] = {c0, c1, c2, bad ? 1u : 0u};
-  block_sum<4>(cnt, s_cnt);
+  // workgroup totals, one plain store per workgroup: wave sums, then thread
+  // 0 adds the waves' after one barrier.  A workgroup's sums stay below
+  // 2^29 (held blocks below 2^20, token needs and restore wants below 2^18
+  // per request), so they add in 32 bits.
+  unsigned u[7] = {(unsigned)v_held, (unsigned)v_need1, (unsigned)v_want1, c0, c1, c2,
+                   bad ? 1u : 0u};
+#pragma unroll
+  for (int k = 0; k < 7; ++k) u[k] = wave_sum(u[k]);
   bmin = wave_min(bmin);
   bmax = wave_max(bmax);
   if (lane_id() == 0) {
+#pragma unroll
+    for (int k = 0; k < 7; ++k) s_cnt[wave_id() * 7 + k] = u[k];
     s_mm[wave_id() * 2] = bmin;
     s_mm[wave_id() * 2 + 1] = bmax;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
+    unsigned tot[7] = {0, 0, 0, 0, 0, 0, 0};
     Partial pt;
-    pt.held = sums[0];
-    pt.need1 = sums[1];
-    pt.want1 = sums[2];
     pt.bmin = ~0ull;
     pt.bmax = 0;
     for (int w = 0; w < kWaves; ++w) {
+#pragma unroll
+      for (int k = 0; k < 7; ++k) tot[k] += s_cnt[w * 7 + k];
       pt.bmin = s_mm[2 * w] < pt.bmin ? s_mm[2 * w] : pt.bmin;
       pt.bmax = s_mm[2 * w + 1] > pt.bmax ? s_mm[2 * w + 1] : pt.bmax;
     }
-    pt.c0 = cnt[0];
-    pt.c1 = cnt[1];
-    pt.c2 = cnt[2];
-    pt.bad = cnt[3];
+    pt.held = tot[0];
+    pt.need1 = tot[1];
+    pt.want1 = tot[2];
+    pt.c0 = tot[3];
+    pt.c1 = tot[4];
+    pt.c2 = tot[5];
+    pt.bad = tot[6];
     pt.pad[0] = pt.pad[1] = 0;
     partials[blockIdx.x] = pt;
   }
