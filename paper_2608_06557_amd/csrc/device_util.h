@@ -127,12 +127,12 @@ __device__ __forceinline__ unsigned long long lane_value(unsigned long long x, i
 
 // Exclusive prefix sums of K values per thread over a workgroup of NW waves,
 // in thread order; also returns the workgroup totals.  `lds` holds NW*K.
-// The per-wave totals are combined by a wave scan (lane w holds wave w's),
-// so the register use does not grow with NW.
+// Each wave scans its lanes (DPP); every thread then reads the NW wave
+// totals from LDS (broadcast reads) and adds those of the waves before its
+// own, so the register use does not grow with NW.
 template <int K, typename T, int NW = kWaves>
 __device__ __forceinline__ void block_exclusive_scan(T (&v)[K], T (&total)[K], T *lds) {
-  static_assert(NW <= 64, "one wave combines the wave totals");
-  typedef typename UnsignedOf<T>::type U;
+  static_assert(NW <= 64, "at most 64 waves");
   const int lane = lane_id(), wave = wave_id();
   T inc[K];
 #pragma unroll
@@ -144,10 +144,14 @@ __device__ __forceinline__ void block_exclusive_scan(T (&v)[K], T (&total)[K], T
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < K; ++k) {
-    const T x = lane < NW ? lds[lane * K + k] : T(0);
-    const U xs = (U)wave_inclusive_sum(x);
-    const T before = wave > 0 ? (T)lane_value(xs, wave - 1) : T(0);
-    total[k] = (T)lane_value(xs, NW - 1);
+    T before = T(0), all = T(0);
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const T x = lds[w * K + k];
+      before += w < wave ? x : T(0);
+      all += x;
+    }
+    total[k] = all;
     v[k] = before + inc[k] - v[k];
   }
   __syncthreads();
@@ -156,7 +160,7 @@ __device__ __forceinline__ void block_exclusive_scan(T (&v)[K], T (&total)[K], T
 // Workgroup sums of K values over NW waves; every thread receives the totals.
 template <int K, typename T, int NW = kWaves>
 __device__ __forceinline__ void block_sum(T (&v)[K], T *lds) {
-  static_assert(NW <= 64, "one wave combines the wave totals");
+  static_assert(NW <= 64, "at most 64 waves");
   const int lane = lane_id(), wave = wave_id();
 #pragma unroll
   for (int k = 0; k < K; ++k) v[k] = wave_sum(v[k]);
@@ -166,7 +170,12 @@ __device__ __forceinline__ void block_sum(T (&v)[K], T *lds) {
   }
   __syncthreads();
 #pragma unroll
-  for (int k = 0; k < K; ++k) v[k] = wave_sum(lane < NW ? lds[lane * K + k] : T(0));
+  for (int k = 0; k < K; ++k) {
+    T all = T(0);
+#pragma unroll
+    for (int w = 0; w < NW; ++w) all += lds[w * K + k];
+    v[k] = all;
+  }
   __syncthreads();
 }
 
