@@ -1054,10 +1054,11 @@ __device__ __forceinline__ void finish_step(const Ctl *ctl, int *info, int n, in
   const int kstar = load_agent(&ctl->kstar);
   const long long kx = load_agent(&ctl->kx), ky = load_agent(&ctl->ky),
                   kz = load_agent(&ctl->kz), kzp = load_agent(&ctl->kzp);
-  // running prefills from the back of the order: thread t holds entry top-1-t
-  int top = n_rp;
+  // running prefills from the back of the order (the list is stored that
+  // way): thread t holds entry back + t
+  int back = 0;
   RpInfo ri = {};
-  if (top - 1 - t >= 0) ri = load_agent_rec(rp + (top - 1 - t));
+  if (t < n_rp) ri = load_agent_rec(rp + t);
   const int lim = min(n_free, o.sl_cap);
 #pragma unroll
   for (int u = 0; u < kFreePer; ++u) {
@@ -1078,12 +1079,12 @@ __device__ __forceinline__ void finish_step(const Ctl *ctl, int *info, int n, in
   // fewer than D.  That count only grows towards the front of the order, so
   // they are the last ones: windows of kBlock entries are taken from the
   // back until one holds an eligible entry that is not a victim.
-  while (D > 0 && top > 0) {
-    const int e = top - 1 - t;
-    if (top != n_rp && e >= 0) ri = load_agent_rec(rp + e);
+  while (D > 0 && back < n_rp) {
+    const int e = back + t;
+    if (back != 0 && e < n_rp) ri = load_agent_rec(rp + e);
     bool kept = false;
     do {
-      if (e < 0 || !ri.eligible) break;
+      if (e >= n_rp || !ri.eligible) break;
       const long long eh = ri.pos < kstar ? ri.x : kx + ri.y - ky;
       const long long after = E - eh;  // eligible blocks behind this request
       if (after >= D) {
@@ -1115,7 +1116,7 @@ __device__ __forceinline__ void finish_step(const Ctl *ctl, int *info, int n, in
       }
     } while (false);
     if (__syncthreads_or(kept ? 1 : 0)) break;  // every earlier holder is kept too
-    top -= kBlock;
+    back += kBlock;
   }
   __syncthreads();
   // the staged victims' rows as one flat index space (prefix of row lengths),
@@ -1401,13 +1402,18 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
                                RpInfo *__restrict__ rp_list,
                                RestoreEnt *__restrict__ restore_list,
                                TileTot *__restrict__ tile_tot, const long long (&pre1)[kL1],
-                               unsigned long long *l2_status, ScanLds &S, TileOut &out) {
+                               long long rp_total, unsigned long long *l2_status, ScanLds &S,
+                               TileOut &out) {
   const long long fh = K.fh;
   const int p0 = tile * kScanTile + threadIdx.x * jn;
   PosVals v;
   scan_positions(tile, jn, K, idx, r4, pre1, S, v);
   int rp_at = v.rp_at;
   const long long rp_incl = v.rp_incl;
+  // the running-prefill list is stored from the back of the order (entry 0:
+  // the last one), so the finish reads its tail without knowing its length;
+  // alone, the tile holds every running prefill
+  const long long rp_last = (kChained ? rp_total : rp_incl) - 1;
   // level-2 values of a tile stay below 2^31 (per request: new blocks plus
   // held blocks below 2^21), so the tile is scanned in 32 bits
   unsigned l2[kL2], t2[kL2];
@@ -1523,7 +1529,7 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
       ri.y = y_inc[j];
       ri.z = Z + zj;
       ri.zp = zp_inc[j];
-      store_agent_rec(rp_list + rp_at, ri);
+      store_agent_rec(rp_list + (rp_last - rp_at), ri);
       ++rp_at;
       if (!adm) {
         a_eh += hh[j];
@@ -1604,17 +1610,17 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
                                             const RpInfo *__restrict__ rp,
                                             const RestoreEnt *__restrict__ rl,
                                             const int *__restrict__ slots, const Outs &o,
-                                            FinishAnyLds &U, int &s_bad) {
+                                            FinishAnyLds &U) {
   FinishKLds &L = U.par;
   const int t = threadIdx.x;
-  if (t == 0) s_bad = bad_status(load_agent(info));
+  const int st = load_agent(info);
   const int n_rp = load_agent(&ctl->n_rp), kstar = load_agent(&ctl->kstar);
   const long long kx = load_agent(&ctl->kx), ky = load_agent(&ctl->ky),
                   kz = load_agent(&ctl->kz), kzp = load_agent(&ctl->kzp);
   // tile totals, the staged part of the restore list and the last kBlock
   // running prefills, all requested before any is used
   constexpr int kTilePer = 4, kRestPer = kRestoreCap / kBlock;
-  long long tot[6] = {0, 0, 0, 0, 0, 0};
+  long long tot[7] = {0, 0, 0, 0, 0, 0, 0};
   for (int j0 = 0; j0 < n_tiles; j0 += kTilePer * kBlock) {
     TileTot tt[kTilePer];
 #pragma unroll
@@ -1639,16 +1645,19 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
     const int j = t + u * kBlock;
     rv[u] = j < n_rs ? load_agent_rec(rl + j) : RestoreEnt{0, 0, 0, 0};
   }
-  int top = n_rp;
-  RpInfo ri = {};
-  if (top - 1 - t >= 0) ri = load_agent_rec(rp + (top - 1 - t));
+  // the running-prefill list is stored from the back of the order, so its
+  // last kBlock entries are requested before their count is known (a queue
+  // on this path holds more than kBlock requests)
+  int back = 0;
+  RpInfo ri = load_agent_rec(rp + t);
 #pragma unroll
   for (int u = 0; u < kRestPer; ++u) {
     const int j = t + u * kBlock;
     if (j < n_rs) L.rl[j] = rv[u];
   }
-  block_sum<6>(tot, L.red);
-  if (s_bad) return;
+  tot[6] = (t == 0 && bad_status(st)) ? 1 : 0;
+  block_sum<7>(tot, L.red);
+  if (tot[6]) return;
   const long long D = tot[0] - n_free, E = tot[1], EO = tot[2];
   const long long nu = tot[4];
   const int nr = (int)tot[5];
@@ -1656,12 +1665,12 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
   // victims, in order from the back of the queue
   int nv_all = 0;                // victims found (staged or not)
   long long held_all = 0, held_offl = 0;
-  while (D > 0 && top > 0) {
-    const int e = top - 1 - t;
-    if (top != n_rp && e >= 0) ri = load_agent_rec(rp + e);
+  while (D > 0 && back < n_rp) {
+    const int e = back + t;
+    if (back != 0 && e < n_rp) ri = load_agent_rec(rp + e);
     bool victim = false, kept = false;
     long long after = 0;
-    if (e >= 0 && ri.eligible) {
+    if (e < n_rp && ri.eligible) {
       const long long eh = ri.pos < kstar ? ri.x : kx + ri.y - ky;
       after = E - eh;  // eligible blocks behind this request
       if (after >= D) {
@@ -1689,7 +1698,7 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
     held_offl += hs[1];
     nv_all += vt[0];
     if (__syncthreads_or(kept ? 1 : 0)) break;  // every earlier holder is kept too
-    top -= kBlock;
+    back += kBlock;
   }
   if (g == 0 && t == 0) {
     const long long nsl = (long long)n_free + held_all;
@@ -1835,39 +1844,43 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
 }
 
 // Sums over tiles j < tile of the level-1 totals (l1[j*kL1 + k]), over the
-// workgroup.  Up to 2*kBlock tiles are requested at once (one round trip);
-// an earlier launch wrote them, so nothing is polled.  The step's status
-// word rides along in the same reduction: the return value says whether an
-// earlier kernel reported a failure, the same in every thread.
+// workgroup, and the running prefills of all n_tiles tiles.  Up to 2*kBlock
+// tiles are requested at once (one round trip); an earlier launch wrote
+// them, so nothing is polled.  The step's status word rides along in the
+// same reduction: the return value says whether an earlier kernel reported
+// a failure, the same in every thread.
 __device__ __forceinline__ bool earlier_totals(const unsigned *__restrict__ l1, int tile,
-                                               const int *info, long long (&pre1)[kL1],
+                                               int n_tiles, const int *info,
+                                               long long (&pre1)[kL1], long long &rp_total,
                                                long long *s_red) {
-  constexpr int kPer = 2, K = kL1 + 1;
+  constexpr int kPer = 2, K = kL1 + 2;
   const int st = load_agent(info);
   long long v[K];
 #pragma unroll
   for (int k = 0; k < K; ++k) v[k] = 0;
-  for (int b0 = 0; b0 < tile; b0 += kPer * kBlock) {
+  for (int b0 = 0; b0 < n_tiles; b0 += kPer * kBlock) {
     unsigned w1[kPer][kL1];
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
       // unconditional loads (tile 0 stands in past the end), masked after
       const int j = b0 + u * kBlock + (int)threadIdx.x;
-      const int jc = j < tile ? j : 0;
+      const int jc = j < n_tiles ? j : 0;
 #pragma unroll
       for (int k = 0; k < kL1; ++k) w1[u][k] = l1[(size_t)jc * kL1 + k];
     }
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
-      const bool in = b0 + u * kBlock + (int)threadIdx.x < tile;
+      const int j = b0 + u * kBlock + (int)threadIdx.x;
 #pragma unroll
-      for (int k = 0; k < kL1; ++k) v[k] += in ? (long long)w1[u][k] : 0ll;
+      for (int k = 0; k < kL1; ++k) v[k] += j < tile ? (long long)w1[u][k] : 0ll;
+      v[kL1] += j < n_tiles ? (long long)w1[u][4] : 0ll;
     }
   }
   v[K - 1] = (threadIdx.x == 0 && bad_status(st)) ? 1 : 0;
   block_sum<K>(v, s_red);
 #pragma unroll
   for (int k = 0; k < kL1; ++k) pre1[k] = v[k];
+  rp_total = v[kL1];
   return v[K - 1] != 0;
 }
 
@@ -1968,15 +1981,15 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     __syncthreads();
     if (s_bad) return;
     finish_grid(tile - n_tiles, (int)gridDim.x - n_tiles, n, c.n_free, n_tiles, ctl, info,
-                tile_tot, free_slots, rp_list, restore_list, slots, o, s_fin, s_bad);
+                tile_tot, free_slots, rp_list, restore_list, slots, o, s_fin);
     return;
   }
   unsigned so[kScanItems];
   int4 sr[kScanItems];
   load_sorted(n, srt, so, sr);
   const int nact = (int)ctl->nact;
-  long long pre1[kL1];
-  if (earlier_totals(l1_tot, tile, info, pre1, s_lds.red)) {
+  long long pre1[kL1], rp_total;
+  if (earlier_totals(l1_tot, tile, n_tiles, info, pre1, rp_total, s_lds.red)) {
     // a failed step: the look-back words say "nothing before me", so no later
     // tile waits, and the tile is counted, so the finishing workgroups stop
     if (t < kL2) publish<unsigned long long>(l2_status + (size_t)tile * kL2Stride + t, 0ull,
@@ -1994,7 +2007,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   TileOut out;
   const long long rp_incl =
       scan_tile<true>(tile, kScanItems, K, ctl, info, idx, r4, broken, o, rp_list,
-                      restore_list, tile_tot, pre1, l2_status, s_lds, out);
+                      restore_list, tile_tot, pre1, rp_total, l2_status, s_lds, out);
   if (tile == n_tiles - 1 && t == 0) store_agent(&ctl->n_rp, (int)rp_incl);
   // hand-over: this tile's agent-scope stores complete, then it is counted
   // (one of kTicketGroups counters, so that no address takes more than a few
@@ -2012,6 +2025,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
 // in LDS, and nothing waits on another workgroup.  Same arithmetic and the
 // same device functions as the multi-launch path, so the result is the same.
 constexpr int kSmallMax = kScanTile;
+static_assert(kSmallMax >= kBlock, "finish_grid reads kBlock list entries unchecked");
 constexpr int kSmallCheckBlocks = 16384;  // pools up to this size are checked in-kernel
 constexpr int kCheckGrid = 64;
 constexpr int kSmallItems = kScanItems;  // one sort tile and one scan tile per small queue
@@ -2365,7 +2379,7 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
   TileOut out;
   const long long zero1[kL1] = {0, 0, 0, 0, 0};
   const long long n_rp = scan_tile<false>(0, jn, K, ctl, info, idx, r4, false, o, rp_list,
-                                          restore_list, tile_tot, zero1, nullptr, s_lds, out);
+                                          restore_list, tile_tot, zero1, 0, nullptr, s_lds, out);
   // the tile's hand-over records (other waves read them in finish_step) are
   // complete before the barrier; its per-request outputs follow
   wait_stores();
