@@ -88,10 +88,12 @@ def test_random_small_queues(dev):
         assert_same(g, o, f"case {t}")
 
 
-def test_all_equal_keys_large(dev):
+@pytest.mark.parametrize("n", [3000, 9000])
+def test_all_equal_keys_large(dev, n):
+    """Every key equal: no radix pass moves data, so the order is the queue
+    order (queues of two and of five sort tiles)."""
     import paper_2608_06557_amd.synth as synth
     w = synth.make_workload(0, n=1)
-    n = 9000
     for k in ["slo_class", "state", "queue_tier", "prefix_tier", "arrival_ns", "n_in",
               "n_out_pred", "n_prefix", "n_progress"]:
         w[k] = np.repeat(w[k][:1], n)
@@ -189,12 +191,12 @@ def test_wide_keys_nine_bit_digits(dev, seed):
     assert _key_width(w, o) > 40
 
 
-@pytest.mark.parametrize("n", [37, 300, 512, 700])
+@pytest.mark.parametrize("n", [37, 300, 512, 700, 3000, 8192])
 def test_small_queue_keys_over_54_bits(dev, n):
     """Requests that arrived at time zero under a clock near 2^61 ns clamp their
     budgets far below the others: keys wider than 54 bits leave no room for
     the request index below them, so short queues sort by digits instead of
-    counting ranks."""
+    counting ranks; longer queues take seven radix passes of 9-bit digits."""
     rng = np.random.default_rng(n)
     p = helpers.base_params(t_now_ns=(1 << 61) + 12345)
     w = helpers.random_workload(rng, n, params=p)
@@ -249,24 +251,26 @@ def test_einval_matches(dev, name, mutate):
     assert status == ref.EINVAL, name
 
 
+@pytest.mark.parametrize("n", [6000, 20000])
 @pytest.mark.parametrize("field", ["state", "slot", "row"])
-def test_einval_on_the_multi_launch_path(dev, field):
-    """Bad request data in a queue of 20000 requests: the radix passes and
-    the scan tiles stop at the failed status without waiting on each other
-    (a wait would run to its poll limit and report a timeout instead)."""
+def test_einval_on_the_multi_launch_path(dev, field, n):
+    """Bad request data in a queue of 6000 or 20000 requests: the radix
+    passes and the scan tiles stop at the failed status without waiting on
+    each other (a wait would run to its poll limit and report a timeout
+    instead)."""
     import time
     import torch
     import paper_2608_06557_amd.synth as synth
-    w = synth.make_workload(2, seed=5, n=20000)
+    w = synth.make_workload(2, seed=5, n=n)
     if field == "state":
         w["state"] = w["state"].copy()
-        w["state"][12345] = 7
+        w["state"][n // 2 + 345] = 7
     elif field == "slot":
         w["slots"] = w["slots"].copy()
         w["slots"][len(w["slots"]) // 2] = w["params"]["num_blocks"]
     else:
         w["row_offsets"] = w["row_offsets"].copy()
-        w["row_offsets"][9000:] += 1
+        w["row_offsets"][n // 2:] += 1
     assert ref.step(w)["rc"] == ref.EINVAL
     d = dev.DeviceStep(w)
     assert d.run() == 0
