@@ -610,6 +610,101 @@ __device__ __forceinline__ void l1_contrib(unsigned *s_l1, int tile, const int4 
   }
 }
 
+// One look-back window of digit b: the counts of tiles start, start - 1,
+// .. (kSortWin of them; below tile 0 an inclusive zero), read at once and
+// consumed up to the first inclusive prefix or the first unpublished word.
+struct SortWindow {
+  unsigned part;  // the consumed words' counts
+  int take;       // words consumed
+  bool done;      // an inclusive prefix ended the window
+  bool stalled;   // an unpublished word ended it
+};
+__device__ __forceinline__ SortWindow sort_window(const unsigned *status, int start, int b) {
+  unsigned v[kSortWin];
+#pragma unroll
+  for (int i = 0; i < kSortWin; ++i) {
+    const int j = start - i;
+    v[i] = j >= 0 ? load_agent(status + (size_t)j * kMaxBins + b) : kFlagInclusive;
+  }
+  unsigned missing = 0, inclusive = 0;
+#pragma unroll
+  for (int i = 0; i < kSortWin; ++i) {
+    missing |= ((v[i] & 3u) == 0 ? 1u : 0u) << i;
+    inclusive |= ((v[i] & 3u) == kFlagInclusive ? 1u : 0u) << i;
+  }
+  const int fm = missing ? __builtin_ctz(missing) : kSortWin;
+  const int fi = inclusive ? __builtin_ctz(inclusive) : kSortWin;
+  SortWindow w;
+  w.done = fi < fm;
+  w.take = w.done ? fi + 1 : fm;
+  w.stalled = !w.done && fm < kSortWin;
+  w.part = 0;
+#pragma unroll
+  for (int i = 0; i < kSortWin; ++i) w.part += i < w.take ? (v[i] >> 2) : 0u;
+  return w;
+}
+
+// Decoupled look-back of a pass with at most kSortBlock/2 bins, by thread
+// pairs: thread b reads the window of the pair's next predecessors and
+// thread b + kSortBlock/2 the window behind it, so a round trip covers
+// 2 * kSortWin tiles.  The second thread's result goes through LDS; the
+// first adds it only when its own window ended on neither an inclusive
+// prefix nor an unpublished word.  Called by every thread of the
+// workgroup; the sum is valid in threads t < bins.
+static_assert(2 * kRadix == kSortBlock, "an 8-bit pass pairs its threads");
+__device__ __forceinline__ unsigned paired_look_back(const unsigned *status, int tile,
+                                                     unsigned bins, unsigned *s_px, int *s_pc,
+                                                     int *s_pn, bool *timed_out) {
+  const int t = threadIdx.x, b = t % (kSortBlock / 2), half = t / (kSortBlock / 2);
+  const bool act = b < (int)bins && tile > 0;
+  int next = tile - 1;
+  bool done = !act;
+  unsigned sum = 0, spins = 0;
+  while (true) {
+    SortWindow w = {0u, 0, true, false};
+    if (!done) w = sort_window(status, next - half * kSortWin, b);
+    if (half == 1) {
+      s_px[b] = w.part;
+      s_pc[b] = w.take | (w.done ? 256 : 0) | (w.stalled ? 512 : 0);
+    }
+    __syncthreads();
+    bool stall = false;
+    if (half == 0 && !done) {
+      sum += w.part;
+      if (w.done) {
+        done = true;
+      } else if (w.stalled) {
+        next -= w.take;
+        stall = true;
+      } else {  // the first window was consumed whole: the second follows it
+        const int c = s_pc[b];
+        sum += s_px[b];
+        if (c & 256) {
+          done = true;
+        } else if (c & 512) {
+          next -= kSortWin + (c & 255);
+          stall = true;
+        } else {
+          next -= 2 * kSortWin;
+        }
+      }
+      s_pn[b] = done ? -1 : next;
+    }
+    __syncthreads();
+    if (half == 1 && act) {
+      next = s_pn[b];
+      done = next < 0;
+    }
+    if (!__syncthreads_or(done ? 0 : 1)) break;
+    if (++spins > kSpinLimit) {
+      *timed_out = true;
+      break;
+    }
+    if (stall) __builtin_amdgcn_s_sleep(1);
+  }
+  return sum;
+}
+
 // The k-th data-moving LSD pass (kK), over the digit the sort plan names:
 // digits are w bits wide (8 or 9, chosen on the device from the live key
 // width), thread t owning bin t.  A tile of kSortTile keys is ranked per
@@ -639,6 +734,9 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   __shared__ unsigned s_l1[kMaxScanTiles * kL1];  // last pass: level-1 totals per scan tile
   __shared__ int s_bad;
   __shared__ unsigned s_mask;
+  __shared__ unsigned s_px[kSortBlock / 2];  // paired look-back: the second window's sum,
+  __shared__ int s_pc[kSortBlock / 2];       // how it ended,
+  __shared__ int s_pn[kSortBlock / 2];       // and where the pair reads next
   static_assert(kMaxBins == kSortBlock, "one bin per thread");
 
   const unsigned long long *src_k = (kK & 1) ? keys_b : keys_a;
@@ -792,10 +890,16 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   // tile-local starts and global bucket bases, in digit order
   int v2[2] = {(int)tcount, dt ? (int)gcount : 0}, tot2[2];
   block_exclusive_scan<2, int, kSortWaves>(v2, tot2, s_scan);
-  // the earlier tiles' counts, kSortWin predecessors per round trip
+  // the earlier tiles' counts, kSortWin predecessors per round trip; with
+  // 8-bit digits and more tiles than one window reaches, two threads share
+  // a bin and read two windows
   bool timed_out = false;
-  const unsigned pre =
-      (dt && tile > 0) ? look_back<unsigned, kSortWin>(status, kMaxBins, tile, t, &timed_out) : 0u;
+  unsigned pre = 0;
+  if (bins * 2 <= kSortBlock && (int)gridDim.x > kSortWin + 1) {
+    pre = paired_look_back(status, tile, bins, s_px, s_pc, s_pn, &timed_out);
+  } else if (dt && tile > 0) {
+    pre = look_back<unsigned, kSortWin>(status, kMaxBins, tile, t, &timed_out);
+  }
   if (dt) {
     if (tile > 0) publish<unsigned>(st + t, pre + tcount, kFlagInclusive);
     s_start[t] = v2[0];

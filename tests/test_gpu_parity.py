@@ -67,7 +67,7 @@ def test_configs_full_size(dev, cfg):
 
 @pytest.mark.parametrize("n", [1, 2, 63, 64, 65, 255, 256, 257, 511, 512, 513, 1023, 1024, 1025,
                                2047, 2048,
-                               2049, 4095, 4096, 4097, 8193, 12289, 16385, 65535, 65537,
+                               2049, 4095, 4096, 4097, 8193, 12289, 16385, 65535, 65537, 69633,
                                131073])
 def test_fuzz_sizes(dev, n):
     import paper_2608_06557_amd.synth as synth
