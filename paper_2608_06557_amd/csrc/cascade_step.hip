@@ -250,27 +250,35 @@ __device__ __forceinline__ ReqEval eval_request(const cascade_requests_t &rq,
   const long long delta = (pt_s == CASCADE_KV_NVME) ? c.delta2 : c.delta1;
   const long long blk = (pt_s == CASCADE_KV_NVME) ? c.blk2 : c.blk1;
   const bool deep = (pt_s == CASCADE_KV_DRAM || pt_s == CASCADE_KV_NVME);
+  // The three regimes share one form: `iters` iterations of the batch with
+  // d (actual) or dmax (maximum) co-scheduled decodes, plus the prompt
+  // tokens' own cost (compute_ps with the two decode counts), plus a restore
+  // for a queued request whose prefix is in DRAM or NVMe.  Computed once
+  // for every lane, so the regimes do not diverge.
+  long long reuse = 0, rest = 0, n_tok = 0, iters;
   if (st_s == CASCADE_QUEUED) {
-    long long reuse = 0, rest = 0;
     if (pt_s != CASCADE_KV_NONE) {
       pb = (unsigned)n_pre / bt;
       reuse = n_pre;
       if (deep) rest = restore_ns(pb, delta, blk);
     }
-    l_act = ns_of_ps(compute_ps(n_in - reuse, reuse, c.d, c)) + rest;
-    l_max = ns_of_ps(compute_ps(n_in - reuse, reuse, c.dmax, c)) + rest;
+    n_tok = n_in - reuse;
     base_need = (pt_s == CASCADE_KV_HBM) ? n_in - n_pre : n_in;
   } else if (st_s == CASCADE_RUNNING_PREFILL) {
-    const long long p = prog > n_in ? n_in : prog;
-    l_act = ns_of_ps(compute_ps(n_in - p, p, c.d, c));
-    l_max = ns_of_ps(compute_ps(n_in - p, p, c.dmax, c));
-    base_need = n_in - p;
+    reuse = prog > n_in ? n_in : prog;
+    n_tok = n_in - reuse;
+    base_need = n_tok;
   } else {
-    const long long left = n_out - prog < 0 ? 0 : n_out - prog;
-    l_act = ns_of_ps(left * (c.c_iter + (long long)c.d * c.c_dec));
-    l_max = ns_of_ps(left * (c.c_iter + (long long)c.dmax * c.c_dec));
     base_need = 1;
   }
+  if (st_s == CASCADE_DECODE) {
+    iters = n_out - prog < 0 ? 0 : n_out - prog;
+  } else {
+    iters = udiv_ceil((unsigned)n_tok, (unsigned)c.chunk);
+  }
+  const long long tok_ps = n_tok * c.c_tok + c.c_attn * ((n_tok * (2 * reuse + n_tok + 1)) >> 1);
+  l_act = ns_of_ps(iters * (c.c_iter + (long long)c.d * c.c_dec) + tok_ps) + rest;
+  l_max = ns_of_ps(iters * (c.c_iter + (long long)c.dmax * c.c_dec) + tok_ps) + rest;
   // ---- eq:est_latency, floor((L_act + L_max) * gamma / 2^17), exact in
   //      64 bits: split the sum at bit 17
   const unsigned long long sum = (unsigned long long)(l_act + l_max);
@@ -289,9 +297,19 @@ __device__ __forceinline__ ReqEval eval_request(const cascade_requests_t &rq,
   if (st_s == CASCADE_QUEUED && deep) {
     long long x = 0;
     if (brem > delta) {
-      const long long m =
-          (long long)((unsigned long long)(brem - delta) / (unsigned long long)blk);
-      x = m < pb ? m : pb;
+      // x = min(floor((brem - delta) / blk), pb).  At or past pb + 1 blocks
+      // the cap decides; below, the quotient is under 2^18 and the dividend
+      // under 2^51, so the double quotient is off by at most one and two
+      // integer checks make it exact
+      const long long num = brem - delta;
+      if (num >= (pb + 1) * blk) {
+        x = pb;
+      } else {
+        long long q = (long long)((double)num / (double)blk);
+        if (q * blk > num) --q;
+        else if ((q + 1) * blk <= num) ++q;
+        x = q;
+      }
     }
     if (x > 0) {
       const long long all = ns_of_ps(compute_ps(n_in, 0, c.d, c));
