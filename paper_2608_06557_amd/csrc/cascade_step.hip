@@ -43,10 +43,15 @@
 namespace cascade {
 namespace {
 
-constexpr int kSortBlock = 512;  // radix workgroups: 8 waves, one 2048-key tile
+constexpr int kSortBlock = 512;  // radix workgroups: 8 waves, one tile of 1024 or 2048 keys
 constexpr int kSortWaves = kSortBlock / 64;
 constexpr int kSortItems = 4;
 constexpr int kSortTile = kSortBlock * kSortItems;
+// Queues up to kSmallTileMax requests sort 1024-key tiles (half the work per
+// workgroup; at most 64 tiles, so the look-back stays short); longer ones
+// 2048-key tiles (more tiles would lengthen the look-back more than they save).
+constexpr int kSortTileSmall = kSortTile / 2;
+constexpr int kSmallTileMax = 65536;
 constexpr int kSortWin = 32;     // predecessors read per look-back round trip (radix)
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
@@ -330,9 +335,9 @@ __device__ __forceinline__ ReqEval eval_request(const cascade_requests_t &rq,
                    (restore_ns(held, c.delta1, c.blk1) <= brem);
   const int decnb = (st_s == CASCADE_DECODE) &&
                     ((long long)udiv_ceil((unsigned)(n_in + prog + 1), bt) - held) > 0;
-  const long long reuse_tok = (st_s == CASCADE_RUNNING_PREFILL)
-                                  ? prog
-                                  : ((st_s == CASCADE_QUEUED && pt_s == CASCADE_KV_HBM) ? n_pre : 0);
+  const bool hbm_prefix = st_s == CASCADE_QUEUED && pt_s == CASCADE_KV_HBM;
+  const long long reuse_tok =
+      (st_s == CASCADE_RUNNING_PREFILL) ? prog : (hbm_prefix ? n_pre : 0);
 
   r.brem = brem;
   r.tnew = tnew;
@@ -725,25 +730,26 @@ __device__ __forceinline__ unsigned paired_look_back(const unsigned *status, int
 
 // The k-th data-moving LSD pass (kK), over the digit the sort plan names:
 // digits are w bits wide (8 or 9, chosen on the device from the live key
-// width), thread t owning bin t.  A tile of kSortTile keys is ranked per
-// wave with w ballots; the tile's digit counts are published for the
+// width), thread t owning bin t.  A tile of kTile = kItems * kSortBlock keys
+// is ranked per wave with w ballots; the tile's digit counts are published for the
 // decoupled look-back; keys are reordered in LDS and written out in runs of
 // equal digits.  The last pass writes the sorted order with each request's
-// scan record and row offset (gathered while the tile is ranked) instead of
+// scan record (gathered while the tile is ranked) instead of
 // the keys, and adds every scan tile's level-1 totals.  The k-th pass reads
 // buffer k & 1, so the tile's keys are requested at once, in parallel with
 // the plan.  Workgroup b sorts tile b: workgroups are dispatched in index
 // order (on each XCD), so every tile a look-back waits on belongs to a
 // workgroup that is running or done, and the lowest unfinished one waits on
 // nothing.
-template <int kK>
+template <int kK, int kItems>
 __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     int n, int passes, Ctl *ctl, int *info, unsigned long long *keys_a,
     unsigned long long *keys_b, unsigned *vals_a, unsigned *vals_b, unsigned *status,
     const int4 *__restrict__ rec, Sorted srt, unsigned *__restrict__ l1_tot) {
-  __shared__ unsigned long long s_keys[kSortTile];
-  __shared__ unsigned s_vals[kSortTile];
-  __shared__ int4 s_rec[kSortTile];
+  constexpr int kTile = kSortBlock * kItems;  // keys per tile
+  __shared__ unsigned long long s_keys[kTile];
+  __shared__ unsigned s_vals[kTile];
+  __shared__ int4 s_rec[kTile];
   __shared__ unsigned s_wcnt[kSortWaves][kMaxBins];  // per-wave counts, then starts
   __shared__ int s_start[kMaxBins];  // tile-local start of each digit
   __shared__ int s_off[kMaxBins];    // output offset of each digit
@@ -762,15 +768,15 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   const unsigned *src_v = (kK & 1) ? vals_b : vals_a;
   unsigned *dst_v = (kK & 1) ? vals_a : vals_b;
   const int t = threadIdx.x, lane = lane_id(), wave = wave_id();
-  const int local = wave * 64 * kSortItems + lane;
+  const int local = wave * 64 * kItems + lane;
 
-  unsigned long long key[kSortItems];
-  unsigned val[kSortItems];
-  int dig[kSortItems], rank[kSortItems];
+  unsigned long long key[kItems];
+  unsigned val[kItems];
+  int dig[kItems], rank[kItems];
   {
-    const int g0 = (int)blockIdx.x * kSortTile + local;
+    const int g0 = (int)blockIdx.x * kTile + local;
 #pragma unroll
-    for (int j = 0; j < kSortItems; ++j) {
+    for (int j = 0; j < kItems; ++j) {
       const int g = g0 + j * 64;
       key[j] = g < n ? src_k[g] : 0ull;
       val[j] = g < n ? src_v[g] : 0u;
@@ -810,9 +816,9 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   if (kK == 0 && nact == 0) {
     // every key equal: the order is the identity; this sort tile's scan
     // tiles get their level-1 totals here
-    static_assert(kSortTile % kScanTile == 0, "whole scan tiles per sort tile");
-    for (int q = 0; q < kSortTile / kScanTile; ++q) {
-      const int p0 = (int)blockIdx.x * kSortTile + q * kScanTile;
+    static_assert(kTile % kScanTile == 0, "whole scan tiles per sort tile");
+    for (int q = 0; q < kTile / kScanTile; ++q) {
+      const int p0 = (int)blockIdx.x * kTile + q * kScanTile;
       if (p0 >= n) break;
       unsigned c[kL1] = {0, 0, 0, 0, 0};
       for (int p = p0 + t; p < min(n, p0 + kScanTile); p += kSortBlock) {
@@ -844,19 +850,19 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
 #pragma unroll
   for (int d = 0; d < kMaxPasses; ++d) gcount = d == digit ? hv[d] : gcount;
   const int tile = (int)blockIdx.x;
-  const int tile_base = tile * kSortTile;
+  const int tile_base = tile * kTile;
   const int shift = P.w * digit;
   const unsigned dmask = bins - 1;
   bool broken = false;
 #pragma unroll
-  for (int j = 0; j < kSortItems; ++j)
+  for (int j = 0; j < kItems; ++j)
     dig[j] = (tile_base + local + j * 64 < n) ? (int)((key[j] >> shift) & dmask) : -1;
   // the last pass carries each request's scan record along; the loads are
   // unconditional (index 0 when not needed) so that nothing waits for them
   // before the tile is ranked
-  int rx[kSortItems], ry[kSortItems], rz[kSortItems], rv[kSortItems];
+  int rx[kItems], ry[kItems], rz[kItems], rv[kItems];
 #pragma unroll
-  for (int j = 0; j < kSortItems; ++j) {
+  for (int j = 0; j < kItems; ++j) {
     const bool want = last && dig[j] >= 0;
     broken |= want && val[j] >= (unsigned)n;
     const unsigned gi = (want && val[j] < (unsigned)n) ? val[j] : 0u;
@@ -868,7 +874,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   }
   // rank within the wave, item by item (local order: wave, item, lane)
 #pragma unroll
-  for (int j = 0; j < kSortItems; ++j) {
+  for (int j = 0; j < kItems; ++j) {
     const bool v = dig[j] >= 0;
     uint64_t peers = __ballot(v);
 #pragma unroll
@@ -927,11 +933,11 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   __syncthreads();
   // reorder the tile in LDS by digit
 #pragma unroll
-  for (int j = 0; j < kSortItems; ++j) {
+  for (int j = 0; j < kItems; ++j) {
     const bool v = dig[j] >= 0;
     const int d = v ? dig[j] : 0;
     const int pos = s_start[d] + (int)s_wcnt[wave][d] + rank[j];
-    const bool ok = v && (unsigned)pos < (unsigned)kSortTile;
+    const bool ok = v && (unsigned)pos < (unsigned)kTile;
     broken |= v && !ok;
     if (ok) {
       s_keys[pos] = key[j];
@@ -940,9 +946,9 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     if (ok && last) s_rec[pos] = make_int4(rx[j], ry[j], rz[j], rv[j]);
   }
   __syncthreads();
-  const int count = min(kSortTile, n - tile_base);
-  static_assert(kSortTile % kSortBlock == 0, "every lane runs every iteration (wave sums below)");
-  for (int s = t; s < kSortTile; s += kSortBlock) {
+  const int count = min(kTile, n - tile_base);
+  static_assert(kTile % kSortBlock == 0, "every lane runs every iteration (wave sums below)");
+  for (int s = t; s < kTile; s += kSortBlock) {
     int o = -1;
     unsigned long long k = 0;
     if (s < count) {
@@ -1137,7 +1143,8 @@ __device__ __forceinline__ void request_rows(int m0, int v_total, int nv,
 // common case: the totals, running-prefill records, restore list and free
 // list together (each thread's share requested before any is stored), then
 // the victims' rows, up to kRowBatch per thread at once.
-__device__ __forceinline__ void finish_step(const Ctl *ctl, int *info, int n, int n_free, int n_tiles, int n_rp,
+__device__ __forceinline__ void finish_step(const Ctl *ctl, int *info, int n, int n_free,
+                                            int n_tiles, int n_rp,
                             const TileTot *__restrict__ tiles, const int *__restrict__ free_slots,
                             const RpInfo *__restrict__ rp, const RestoreEnt *__restrict__ rl,
                             const int *__restrict__ slots, const Outs &o, FinishLds &L) {
@@ -1518,7 +1525,8 @@ __device__ __forceinline__ void wave_look_back(const unsigned long long *status,
 }
 
 template <bool kChained>
-__device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl, int *info,
+__device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConsts &K, Ctl *ctl,
+                                               int *info,
                                const int (&idx)[kScanItems], const int4 (&r4)[kScanItems],
                                bool broken, const Outs &o,
                                RpInfo *__restrict__ rp_list,
@@ -1556,7 +1564,8 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
 #pragma unroll
       for (int k = 0; k < kL2; ++k) agg = k == t ? t2[k] : agg;
       unsigned long long *st = l2_status + (size_t)tile * kL2Stride + t;
-      if (t < kL2) publish<unsigned long long>(st, agg, tile == 0 ? kFlagInclusive : kFlagAggregate);
+      if (t < kL2)
+        publish<unsigned long long>(st, agg, tile == 0 ? kFlagInclusive : kFlagAggregate);
       unsigned long long before[kL2] = {0, 0, 0, 0, 0, 0, 0};
       if (tile > 0) {
         bool timed_out = false;
@@ -1899,7 +1908,8 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
         ld[u] = slots[L.v_row0[v] + (m - L.v_start[v])];
       } else {  // restore move
         const long long m = i - lim - v_total;
-        const int k = last_at_or_below<kRestoreSteps>(nr, m, [&](int q) { return L.rl[q].stage_off; });
+        const int k =
+            last_at_or_below<kRestoreSteps>(nr, m, [&](int q) { return L.rl[q].stage_off; });
         const RestoreEnt re = L.rl[k];
         const long long s = (long long)re.alloc_off + (m - re.stage_off);
         kind[u] = 2;
@@ -1910,7 +1920,8 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
             ld[u] = free_slots[s];
           } else {
             const int mv = (int)(s - n_free);
-            const int v = last_at_or_below<kFinVictimSteps>(nv, mv, [&](int q) { return L.v_start[q]; });
+            const int v =
+                last_at_or_below<kFinVictimSteps>(nv, mv, [&](int q) { return L.v_start[q]; });
             ld[u] = slots[L.v_row0[v] + (mv - L.v_start[v])];
           }
         }
@@ -1952,7 +1963,8 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
             int hz = -1;  // a free slot is read by no pack move
             if (s >= n_free) {
               const int mv2 = (int)(s - n_free);
-              const int v = last_at_or_below<kFinVictimSteps>(nv, mv2, [&](int q) { return L.v_start[q]; });
+              const int v = last_at_or_below<kFinVictimSteps>(
+                  nv, mv2, [&](int q) { return L.v_start[q]; });
               const long long pb = L.v_pbase[v];
               const long long j = pb >= 0 ? pb + (mv2 - L.v_start[v]) : -1;
               hz = (j >= 0 && j < o.pack_cap) ? (int)j : -1;
@@ -2544,7 +2556,7 @@ size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 Layout make_layout(int32_t n) {
   Layout L;
   const size_t np = n > 0 ? (size_t)n : 1;
-  L.sort_tiles = (int)((np + kSortTile - 1) / kSortTile);
+  L.sort_tiles = (int)((np + kSortTileSmall - 1) / kSortTileSmall);  // the most tiles a sort uses
   L.scan_tiles = (int)((np + kScanTile - 1) / kScanTile);
   L.eval_grid = (int)((np + kBlock * kEvalItems - 1) / (kBlock * kEvalItems));
   size_t off = 0;
@@ -2634,9 +2646,11 @@ int sort_passes(const cascade_params_t *p) {
 typedef void (*RadixFn)(int, int, Ctl *, int *, unsigned long long *, unsigned long long *,
                         unsigned *, unsigned *, unsigned *, const int4 *, Sorted, unsigned *);
 static_assert(kMaxPasses == 8, "one radix kernel per pass");
-const RadixFn kRadixKernels[kMaxPasses] = {
-    radix_pass_kernel<0>, radix_pass_kernel<1>, radix_pass_kernel<2>, radix_pass_kernel<3>,
-    radix_pass_kernel<4>, radix_pass_kernel<5>, radix_pass_kernel<6>, radix_pass_kernel<7>};
+template <int kItems>
+constexpr RadixFn kRadixPasses[kMaxPasses] = {
+    radix_pass_kernel<0, kItems>, radix_pass_kernel<1, kItems>, radix_pass_kernel<2, kItems>,
+    radix_pass_kernel<3, kItems>, radix_pass_kernel<4, kItems>, radix_pass_kernel<5, kItems>,
+    radix_pass_kernel<6, kItems>, radix_pass_kernel<7, kItems>};
 
 }  // namespace
 }  // namespace cascade
@@ -2770,7 +2784,12 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   // cleared by eval
   const int passes = sort_passes(p);
   const size_t clear_off = L.ctl + offsetof(Ctl, hist);
-  const size_t clear_end = L.sort_status + (size_t)passes * L.sort_tiles * kMaxBins * 4;
+  // queues up to kSmallTileMax sort 1024-key tiles: each pass's per-workgroup
+  // work halves while the look-back stays within a window or two
+  const bool small_tiles = n <= kSmallTileMax;
+  const int sort_tiles = small_tiles ? (n + kSortTileSmall - 1) / kSortTileSmall
+                                     : (n + kSortTile - 1) / kSortTile;
+  const size_t clear_end = L.sort_status + (size_t)passes * sort_tiles * kMaxBins * 4;
   const size_t clear_vec = (clear_end - clear_off) / 16;
   uint4 *clear = reinterpret_cast<uint4 *>(ws + clear_off);
   static_assert(offsetof(Ctl, hist) % 16 == 0, "16-byte clears");
@@ -2780,12 +2799,14 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
                      out->budget_ns, out->queue_tier_out, keys_a, rec);
   const int prep_grid = (n + kBlock * kPrepItems - 1) / (kBlock * kPrepItems);
   hipLaunchKernelGGL(prep_kernel, dim3(prep_grid), dim3(kBlock), 0, s, n, ts->num_blocks,
-                     L.eval_grid, passes, partials, bt->row_offsets, bt->slots, ctl, out->info, keys_a,
-                     vals_a);
+                     L.eval_grid, passes, partials, bt->row_offsets, bt->slots, ctl, out->info,
+                     keys_a, vals_a);
   for (int pass = 0; pass < passes; ++pass)
-    hipLaunchKernelGGL(kRadixKernels[pass], dim3(L.sort_tiles), dim3(kSortBlock), 0, s, n,
+    hipLaunchKernelGGL(small_tiles ? kRadixPasses<kSortItems / 2>[pass]
+                                   : kRadixPasses<kSortItems>[pass],
+                       dim3(sort_tiles), dim3(kSortBlock), 0, s, n,
                        passes, ctl, out->info, keys_a, keys_b, vals_a, vals_b,
-                       sort_status + (size_t)pass * L.sort_tiles * kMaxBins, rec, srt,
+                       sort_status + (size_t)pass * sort_tiles * kMaxBins, rec, srt,
                        l1_tot);
   hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles + kFinishGrid), dim3(kBlock), 0, s, n,
                      passes, L.scan_tiles, c, ctl, out->info, srt, rec, bt->slots,
