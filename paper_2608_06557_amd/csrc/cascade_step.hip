@@ -47,10 +47,13 @@ constexpr int kSortBlock = 512;  // radix workgroups: 8 waves, one tile of 1024 
 constexpr int kSortWaves = kSortBlock / 64;
 constexpr int kSortItems = 4;
 constexpr int kSortTile = kSortBlock * kSortItems;
-// Queues up to kSmallTileMax requests sort 1024-key tiles (half the work per
-// workgroup; at most 64 tiles, so the look-back stays short); longer ones
-// 2048-key tiles (more tiles would lengthen the look-back more than they save).
+// Queues up to kTinyTileMax requests sort 512-key tiles, up to kSmallTileMax
+// 1024-key tiles (less ranking, reorder and write work per workgroup; at
+// most 32 or 64 tiles, so the look-back stays short); longer ones 2048-key
+// tiles (more tiles would lengthen the look-back more than they save).
+constexpr int kSortTileTiny = kSortTile / 4;
 constexpr int kSortTileSmall = kSortTile / 2;
+constexpr int kTinyTileMax = 16384;
 constexpr int kSmallTileMax = 65536;
 constexpr int kSortWin = 32;     // predecessors read per look-back round trip (radix)
 constexpr int kScanItems = 4;
@@ -814,14 +817,16 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     return;
   }
   if (kK == 0 && nact == 0) {
-    // every key equal: the order is the identity; this sort tile's scan
-    // tiles get their level-1 totals here
-    static_assert(kTile % kScanTile == 0, "whole scan tiles per sort tile");
-    for (int q = 0; q < kTile / kScanTile; ++q) {
-      const int p0 = (int)blockIdx.x * kTile + q * kScanTile;
+    // every key equal: the order is the identity; this sort tile adds its
+    // positions to their scan tiles' level-1 totals (a scan tile may span
+    // several sort tiles)
+    constexpr int kSub = kTile < kScanTile ? kTile : kScanTile;
+    static_assert(kTile % kSub == 0 && kScanTile % kSub == 0, "sub-ranges inside one scan tile");
+    for (int q = 0; q < kTile / kSub; ++q) {
+      const int p0 = (int)blockIdx.x * kTile + q * kSub;
       if (p0 >= n) break;
       unsigned c[kL1] = {0, 0, 0, 0, 0};
-      for (int p = p0 + t; p < min(n, p0 + kScanTile); p += kSortBlock) {
+      for (int p = p0 + t; p < min(n, p0 + kSub); p += kSortBlock) {
         const int4 r = rec[p];
         const bool rp = rec_state(r.w) == CASCADE_RUNNING_PREFILL;
         const unsigned h = rp ? (unsigned)rec_held(r.w) : 0u;
@@ -834,7 +839,8 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
       block_sum<kL1, unsigned, kSortWaves>(c, s_sum);
       if (t == 0) {
 #pragma unroll
-        for (int k = 0; k < kL1; ++k) l1_tot[(size_t)(p0 / kScanTile) * kL1 + k] = c[k];
+        for (int k = 0; k < kL1; ++k)
+          if (c[k]) atomicAdd(l1_tot + (size_t)(p0 / kScanTile) * kL1 + k, c[k]);
       }
     }
     return;
@@ -2556,7 +2562,7 @@ size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 Layout make_layout(int32_t n) {
   Layout L;
   const size_t np = n > 0 ? (size_t)n : 1;
-  L.sort_tiles = (int)((np + kSortTileSmall - 1) / kSortTileSmall);  // the most tiles a sort uses
+  L.sort_tiles = (int)((np + kSortTileTiny - 1) / kSortTileTiny);  // the most tiles a sort uses
   L.scan_tiles = (int)((np + kScanTile - 1) / kScanTile);
   L.eval_grid = (int)((np + kBlock * kEvalItems - 1) / (kBlock * kEvalItems));
   size_t off = 0;
@@ -2784,11 +2790,9 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   // cleared by eval
   const int passes = sort_passes(p);
   const size_t clear_off = L.ctl + offsetof(Ctl, hist);
-  // queues up to kSmallTileMax sort 1024-key tiles: each pass's per-workgroup
-  // work halves while the look-back stays within a window or two
-  const bool small_tiles = n <= kSmallTileMax;
-  const int sort_tiles = small_tiles ? (n + kSortTileSmall - 1) / kSortTileSmall
-                                     : (n + kSortTile - 1) / kSortTile;
+  const int tile_keys =
+      n <= kTinyTileMax ? kSortTileTiny : (n <= kSmallTileMax ? kSortTileSmall : kSortTile);
+  const int sort_tiles = (n + tile_keys - 1) / tile_keys;
   const size_t clear_end = L.sort_status + (size_t)passes * sort_tiles * kMaxBins * 4;
   const size_t clear_vec = (clear_end - clear_off) / 16;
   uint4 *clear = reinterpret_cast<uint4 *>(ws + clear_off);
@@ -2802,8 +2806,9 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
                      L.eval_grid, passes, partials, bt->row_offsets, bt->slots, ctl, out->info,
                      keys_a, vals_a);
   for (int pass = 0; pass < passes; ++pass)
-    hipLaunchKernelGGL(small_tiles ? kRadixPasses<kSortItems / 2>[pass]
-                                   : kRadixPasses<kSortItems>[pass],
+    hipLaunchKernelGGL(tile_keys == kSortTileTiny    ? kRadixPasses<kSortItems / 4>[pass]
+                       : tile_keys == kSortTileSmall ? kRadixPasses<kSortItems / 2>[pass]
+                                                     : kRadixPasses<kSortItems>[pass],
                        dim3(sort_tiles), dim3(kSortBlock), 0, s, n,
                        passes, ctl, out->info, keys_a, keys_b, vals_a, vals_b,
                        sort_status + (size_t)pass * sort_tiles * kMaxBins, rec, srt,
