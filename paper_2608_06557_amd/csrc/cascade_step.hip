@@ -58,7 +58,8 @@ constexpr int kSmallTileMax = 65536;
 constexpr int kSortWin = 32;     // predecessors read per look-back round trip (radix)
 constexpr int kScanItems = 4;
 constexpr int kScanTile = kBlock * kScanItems;
-constexpr int kPrepItems = 8;
+constexpr int kPrepItems = 8;       // keys per prep thread (2 up to kTinyPrepMax)
+constexpr int kTinyPrepMax = 16384;
 constexpr int kEvalItems = 1;
 static_assert(kBlock * kEvalItems <= 2048, "an eval workgroup's sums fit 32 bits");
 constexpr int kMaxW = 9;         // widest digit of the multi-launch sort
@@ -485,6 +486,7 @@ __device__ __forceinline__ DigitPlan digit_plan(const Ctl *ctl, int passes) {
 // bucket).  The keys are requested before the totals they are compressed
 // with.  Also checks the block-table slots, whose extent is only trustworthy
 // after eval.
+template <int kItems>
 __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int n_partials,
                                                       int passes,
                                                       const Partial *__restrict__ partials,
@@ -496,10 +498,10 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
   __shared__ unsigned s_hist[kMaxPasses * kMaxBins];
   __shared__ unsigned long long s_red[kWaves * 9];
   const int t = threadIdx.x, lane = lane_id(), wave = wave_id();
-  const int base = blockIdx.x * kBlock * kPrepItems;
-  unsigned long long kv[kPrepItems];
+  const int base = blockIdx.x * kBlock * kItems;
+  unsigned long long kv[kItems];
 #pragma unroll
-  for (int j = 0; j < kPrepItems; ++j) {
+  for (int j = 0; j < kItems; ++j) {
     const int idx = base + j * kBlock + t;
     kv[j] = idx < n ? keys[idx] : 0ull;
   }
@@ -569,7 +571,7 @@ __global__ __launch_bounds__(kBlock) void prep_kernel(int n, int num_blocks, int
   __syncthreads();
   const unsigned long long span = mx - mn + 1;
 #pragma unroll
-  for (int j = 0; j < kPrepItems; ++j) {
+  for (int j = 0; j < kItems; ++j) {
     const int idx = base + j * kBlock + t;
     const bool in = idx < n;
     const unsigned long long k0 = kv[j];
@@ -2801,10 +2803,13 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
   hipLaunchKernelGGL(eval_kernel, dim3(L.eval_grid), dim3(kBlock), 0, s, *rq, bt->row_offsets,
                      ts->free_slots, c, n, ctl, clear, clear_vec, out->info, partials,
                      out->budget_ns, out->queue_tier_out, keys_a, rec);
-  const int prep_grid = (n + kBlock * kPrepItems - 1) / (kBlock * kPrepItems);
-  hipLaunchKernelGGL(prep_kernel, dim3(prep_grid), dim3(kBlock), 0, s, n, ts->num_blocks,
-                     L.eval_grid, passes, partials, bt->row_offsets, bt->slots, ctl, out->info,
-                     keys_a, vals_a);
+  // a short queue spreads prep over more workgroups (its block-table checks
+  // and histograms are per workgroup); a long one keeps the global adds few
+  const int prep_items = n <= kTinyPrepMax ? 2 : kPrepItems;
+  const int prep_grid = (n + kBlock * prep_items - 1) / (kBlock * prep_items);
+  hipLaunchKernelGGL(prep_items == 2 ? prep_kernel<2> : prep_kernel<kPrepItems>, dim3(prep_grid),
+                     dim3(kBlock), 0, s, n, ts->num_blocks, L.eval_grid, passes, partials,
+                     bt->row_offsets, bt->slots, ctl, out->info, keys_a, vals_a);
   for (int pass = 0; pass < passes; ++pass)
     hipLaunchKernelGGL(tile_keys == kSortTileTiny    ? kRadixPasses<kSortItems / 4>[pass]
                        : tile_keys == kSortTileSmall ? kRadixPasses<kSortItems / 2>[pass]
