@@ -12,6 +12,7 @@ allocation, preemption of the largest-budget prefill holder).
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes as C
 import os
 import subprocess
@@ -87,41 +88,58 @@ class Pool(C.Structure):
 _lib = None
 
 
+def _bind(L):
+    """Declare the argument and result types of every oracle function."""
+    L.cref_compute_ps.restype = C.c_int64
+    L.cref_compute_ps.argtypes = [C.POINTER(Params), C.c_int64, C.c_int64, C.c_int64]
+    L.cref_restore_time_ns.restype = C.c_int64
+    L.cref_restore_time_ns.argtypes = [C.POINTER(Params), C.c_int32, C.c_int64]
+    L.cref_check_params.restype = C.c_int32
+    L.cref_check_params.argtypes = [C.POINTER(Params), C.c_int32, C.c_int32]
+    L.cref_eval.restype = None
+    L.cref_eval.argtypes = [C.POINTER(Params), C.c_uint8, C.c_uint8, C.c_uint8, C.c_uint8,
+                            C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                            C.POINTER(EvalOut)]
+    L.cref_step.restype = C.c_int32
+    L.cref_step.argtypes = [C.c_int32] + [C.c_void_p] * 12 + [C.c_int32, C.c_void_p,
+                                                               C.POINTER(Params),
+                                                               C.POINTER(Outputs)]
+    L.cref_pack.restype = None
+    L.cref_pack.argtypes = [C.POINTER(Pool), C.c_void_p, C.c_void_p, C.c_int32]
+    L.cref_unpack.restype = None
+    L.cref_unpack.argtypes = [C.POINTER(Pool), C.c_void_p, C.c_void_p, C.c_int32]
+    L.cref_prefix_probe.restype = C.c_int32
+    L.cref_prefix_probe.argtypes = [C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
+                                    C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
+                                    C.c_void_p, C.c_void_p]
+    L.cref_tier_reclaim.restype = C.c_int32
+    L.cref_tier_reclaim.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
+                                    C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
+                                    C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                    C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
+    return L
+
+
 def lib():
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             build()
-        L = C.CDLL(LIB_PATH)
-        L.cref_compute_ps.restype = C.c_int64
-        L.cref_compute_ps.argtypes = [C.POINTER(Params), C.c_int64, C.c_int64, C.c_int64]
-        L.cref_restore_time_ns.restype = C.c_int64
-        L.cref_restore_time_ns.argtypes = [C.POINTER(Params), C.c_int32, C.c_int64]
-        L.cref_check_params.restype = C.c_int32
-        L.cref_check_params.argtypes = [C.POINTER(Params), C.c_int32, C.c_int32]
-        L.cref_eval.restype = None
-        L.cref_eval.argtypes = [C.POINTER(Params), C.c_uint8, C.c_uint8, C.c_uint8, C.c_uint8,
-                                C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
-                                C.POINTER(EvalOut)]
-        L.cref_step.restype = C.c_int32
-        L.cref_step.argtypes = [C.c_int32] + [C.c_void_p] * 12 + [C.c_int32, C.c_void_p,
-                                                                   C.POINTER(Params),
-                                                                   C.POINTER(Outputs)]
-        L.cref_pack.restype = None
-        L.cref_pack.argtypes = [C.POINTER(Pool), C.c_void_p, C.c_void_p, C.c_int32]
-        L.cref_unpack.restype = None
-        L.cref_unpack.argtypes = [C.POINTER(Pool), C.c_void_p, C.c_void_p, C.c_int32]
-        L.cref_prefix_probe.restype = C.c_int32
-        L.cref_prefix_probe.argtypes = [C.c_int32, C.c_void_p, C.c_void_p, C.c_int32,
-                                        C.c_void_p, C.c_void_p, C.c_void_p, C.c_int32,
-                                        C.c_void_p, C.c_void_p]
-        L.cref_tier_reclaim.restype = C.c_int32
-        L.cref_tier_reclaim.argtypes = [C.c_int32, C.c_int32, C.c_void_p, C.c_void_p,
-                                        C.c_void_p, C.c_int32, C.c_int32, C.c_void_p,
-                                        C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
-                                        C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
-        _lib = L
+        _lib = _bind(C.CDLL(LIB_PATH))
     return _lib
+
+
+@contextlib.contextmanager
+def library(path: str):
+    """Run the oracle functions of this module on another build of the
+    oracle (the tests' planted-mistake copies) inside the block."""
+    global _lib
+    saved = _lib
+    _lib = _bind(C.CDLL(path))
+    try:
+        yield
+    finally:
+        _lib = saved
 
 
 PARAM_KEYS = ["t_now_ns", "num_classes", "block_tokens", "chunk_tokens", "load_decodes",

@@ -36,6 +36,27 @@ def worked_example() -> tuple[dict, dict]:
     return w, g
 
 
+def golden_workload(name: str) -> tuple[dict, dict]:
+    """A hand-derived example whose block-table rows and free list are
+    listed explicitly ("row_slots", "free_slots")."""
+    g = load_golden(name)
+    rq = g["requests"]
+    w = {k: np.array(rq[k]) for k in ["id", "slo_class", "state", "queue_tier", "prefix_tier",
+                                       "arrival_ns", "n_in", "n_out_pred", "n_prefix",
+                                       "n_progress"]}
+    w["id"] = w["id"].astype(np.uint64)
+    rows = rq["row_slots"]
+    ro = np.zeros(len(rows) + 1, np.int32)
+    ro[1:] = np.cumsum([len(r) for r in rows])
+    w["row_offsets"] = ro
+    w["slots"] = np.array([s for r in rows for s in r], np.int32)
+    w["free_slots"] = np.array(g["free_slots"], np.int32)
+    if "prefix_group" in rq:
+        w["prefix_group"] = np.array(rq["prefix_group"], np.int32)
+    w["params"] = g["params"]
+    return w, g
+
+
 def base_params(**over) -> dict:
     """Small-number parameters under which every branch of the step is
     common: budgets of tens of microseconds, restores that are sometimes

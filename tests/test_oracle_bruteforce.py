@@ -183,13 +183,44 @@ def _check_against_definitions(w):
                 best_set = s
         assert best_set is not None      # covering is always possible
         victims = set(best_set)
+    spilled = set()
     for i in range(n):
         a = res["action"][i]
         if i in victims:
             spill = ref.restore_time_ns(p, ref.KV_DRAM, int(row[i])) <= ev[i]["budget_rem_ns"]
             assert a == (ref.ACT_PREEMPT_OFFLOAD if spill else ref.ACT_PREEMPT_DROP)
+            if spill:
+                spilled.add(i)
+            continue
+        # Section 4.4: KV already in HBM (a running request's rows, a shared
+        # HBM prefix) is kept whether or not the request is in the batch; a
+        # deeper prefix with blocks under the link cap is restored when the
+        # request is in the batch (HBM is allocated at the final hop) and only
+        # prefetched otherwise; anything else is recomputed
+        if st[i] != helpers.QUEUED or w["prefix_tier"][i] == helpers.KV_HBM:
+            assert a == ref.ACT_RETAIN, (i, a)
+        elif got[i] > 0:
+            assert a == (ref.ACT_RESTORE if i in admitted else ref.ACT_PREFETCH), (i, a)
         else:
-            assert a not in (ref.ACT_PREEMPT_OFFLOAD, ref.ACT_PREEMPT_DROP)
+            assert a == ref.ACT_RECOMPUTE, (i, a)
+
+    # slot list: the free list, then every victim's row, victims in the order
+    # they were preempted (from the back), each row in row order; a spill
+    # moves each block of a spilled victim, in that same order
+    rows = [list(w["slots"][w["row_offsets"][i]:w["row_offsets"][i + 1]]) for i in range(n)]
+    by_back = [i for i in reversed(order) if i in victims]
+    assert list(res["slot_list"]) == list(w["free_slots"]) + [s for i in by_back for s in rows[i]]
+    want_pack = [(i, b, s) for i in by_back if i in spilled for b, s in enumerate(rows[i])]
+    assert [(int(m["req"]), int(m["blk"]), int(m["pool_slot"])) for m in res["pack_moves"]] \
+        == want_pack
+    assert list(res["pack_moves"]["staging_slot"]) == list(range(len(want_pack)))
+    # restores: the first restore_blocks blocks of each admitted restoring
+    # request's allocation, in admitted order
+    sl = list(res["slot_list"])
+    want_unpack = [(i, b, sl[res["alloc_begin"][i] + b]) for i in admitted
+                   for b in range(got[i]) if res["action"][i] == ref.ACT_RESTORE]
+    assert [(int(m["req"]), int(m["blk"]), int(m["pool_slot"])) for m in res["unpack_moves"]] \
+        == want_unpack
     return res
 
 

@@ -54,6 +54,37 @@ def test_worked_example_step():
     assert list(pm["staging_slot"]) == list(range(32)) and list(pm["blk"]) == list(range(32))
 
 
+def test_second_example_per_request_values():
+    w, g = helpers.golden_workload("worked_example_2.json")
+    exp = g["expected_eval"]
+    for i in range(len(w["id"])):
+        e = _eval_req(w["params"], w, i)
+        for k in EVAL_KEYS:
+            assert e[k] == exp[k][i], (i, k, e[k], exp[k][i])
+
+
+def _moves(a):
+    return [[int(m["req"]), int(m["blk"]), int(m["pool_slot"]), int(m["staging_slot"])]
+            for m in a]
+
+
+def test_second_example_step():
+    """PREFETCH of a capped restore outside the batch, RETAIN of HBM-prefix
+    requests inside and outside the batch, three victims taken from the back
+    of the order (Tier-2 first) with their spill moves in that order."""
+    w, g = helpers.golden_workload("worked_example_2.json")
+    r = ref.step(w)
+    exp = g["expected_step"]
+    assert r["rc"] == ref.OK
+    for k in ["order", "restore_blocks", "tokens_granted", "action", "alloc_begin",
+              "alloc_count", "admitted", "slot_list", "unpack_hazard", "pack_hazard"]:
+        assert [int(x) for x in r[k]] == exp[k], (k, list(r[k]), exp[k])
+    assert _moves(r["unpack_moves"]) == exp["unpack_moves"]
+    assert _moves(r["pack_moves"]) == exp["pack_moves"]
+    assert r["n_slot_list"] == len(exp["slot_list"])
+    assert r["n_unpack"] == len(exp["unpack_moves"]) and r["n_pack"] == len(exp["pack_moves"])
+
+
 # ---------------------------------------------------------------- cost model
 
 def _zero_cost(**kw):
