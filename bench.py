@@ -29,15 +29,59 @@ METRIC = ("scheduling-step latency (µs) & requests/s at N=65536; "
           "KV pack/unpack GB/s vs HBM peak")
 HBM_PEAK_GBPS = 8000.0
 WORKLOADS = {
-    0: "256 chat requests, 3 SLO classes, 8B-class KV (32 layers), 4096-block pool",
-    1: "8192 chat requests, 5 SLO classes, 65536-block (128 GiB) pool, token cap 16384",
-    2: ("65536 requests, 80% chat / 20% agentic, 8B-class KV (32 layers x 8 heads x "
-        "128 x bf16, 16-token blocks), 200 GB pool, token cap 16384, ~2 GB packed and unpacked"),
-    3: ("65536 requests, reasoning-heavy, 30% sharing 512 prefixes of 1k-32k tokens, high load, "
-        "exact budget ties, 200 GB pool"),
-    4: ("262144 requests, 70B-class KV (80 layers), 250 GB pool, token cap 32768, "
+    0: ("256 chat requests, 3 SLO classes (2/10/60 s), waits U[0, SLO], 8B-class KV "
+        "(32 layers), 4096-block pool, token cap 8192"),
+    1: ("8192 chat requests, 5 SLO classes (2/10/60/120/300 s), waits U[0, SLO], 8B-class KV, "
+        "65536-block (128 GiB) pool, token cap 16384, restore cap 512 blocks"),
+    2: ("65536 requests, 80% chat / 20% agentic, 5 SLO classes (1/2/10/30/60 s, bound to the "
+        "application), waits U[0, SLO/2], 8B-class KV (32 layers x 8 heads x 128 x bf16, "
+        "16-token blocks), 200 GB pool, token cap 16384, ~2 GB packed and unpacked"),
+    3: ("65536 requests, 50% reasoning / 25% chat / 25% agentic, 30% in families of 4 "
+        "parallel reasoning samples sharing one of 512 prefixes of 1k-32k tokens, high load "
+        "(127 co-scheduled decodes), waits of SLO - (20 ms + prompt at 10k tok/s) +- 20 ms, "
+        "exact budget ties, 200 GB pool, token cap 16384"),
+    4: ("262144 requests, 80% chat / 20% agentic, 5 SLO classes (2/5/10/30/60 s), waits "
+        "U[0, SLO/2], 70B-class KV (80 layers), 250 GB pool, token cap 32768, "
         "~8 GB packed and unpacked"),
 }
+
+# Bytes a step must move through HBM per request: its input fields (id 8,
+# class / state / queue tier / prefix tier 1 each, arrival 8, four 4-byte
+# lengths, its block-table row offset 4) and its outputs (budget 8, action
+# 1, tier 1, tokens granted / restore blocks / order position / allocation
+# begin and count 4 each).  Block-table slots, free slots and emitted moves
+# are counted per entry on top.
+STEP_IN_BYTES_PER_REQUEST = 8 + 4 * 1 + 8 + 4 * 4 + 4
+STEP_OUT_BYTES_PER_REQUEST = 8 + 1 + 1 + 5 * 4
+
+
+def step_compulsory_bytes(w, res):
+    """HBM bytes one scheduling step (parts 1-3) cannot avoid: every
+    request's fields in and outputs out, every block-table and free-list
+    slot read once (range checks, victims' rows), the slot list and both
+    move lists (16-byte records) written once."""
+    n = len(w["id"])
+    return (n * (STEP_IN_BYTES_PER_REQUEST + STEP_OUT_BYTES_PER_REQUEST)
+            + 4 * int(w["row_offsets"][-1]) + 4 * len(w["free_slots"])
+            + 4 * int(res["n_slot_list"]) + 16 * int(res["n_unpack"] + res["n_pack"])
+            + 4 * int(res["n_admitted"]))
+
+
+def host_cpu():
+    """This host's CPU as the oracle baseline sees it."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"model": model, "nproc": os.cpu_count(), "usable_cpus": usable}
 
 
 def measured_traffic(cfg, layout, kernel, chunk_bytes):
@@ -151,6 +195,38 @@ def measure_reclaim(cfg, stream, reps=20):
             "slots_scanned_per_s": slots / (us * 1e-6)}, w
 
 
+def measure_step_only(cfg, stream, reps=100, warmup=10):
+    """Parts 1-3 alone (cascade_step: budgets, actions, order, admission,
+    preemption, move lists) on another workload, inputs resident in HBM:
+    HIP events on the launch stream, median and p90.  No KV pool is needed."""
+    import torch
+    import paper_2608_06557_amd.synth as synth
+    from paper_2608_06557_amd import device
+    w = synth.make_workload(cfg)
+    nb = w["params"]["num_blocks"]
+    d = device.DeviceStep(w, slot_cap=nb, unpack_cap=nb, pack_cap=nb)
+    for _ in range(warmup):
+        assert d.run(stream) == 0
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * reps)]
+    for k in range(reps):
+        ev[2 * k].record(stream)
+        assert d.run(stream) == 0
+        ev[2 * k + 1].record(stream)
+    torch.cuda.synchronize()
+    t = np.array([ev[2 * k].elapsed_time(ev[2 * k + 1]) for k in range(reps)]) * 1e3
+    res = d.fetch()
+    assert res["status"] == 0
+    n = len(w["id"])
+    p50 = float(np.median(t))
+    cb = step_compulsory_bytes(w, res)
+    progress(f"step alone at {n} requests measured")
+    return {"workload": WORKLOADS[cfg], "requests": n, "runs": reps,
+            "sched_step_us_p50": p50, "sched_step_us_p90": float(np.percentile(t, 90)),
+            "sched_req_per_s": n / (p50 * 1e-6), "compulsory_bytes": cb,
+            "roofline_frac": cb / (p50 * 1e-6) / 1e9 / HBM_PEAK_GBPS}
+
+
 def measure_host_tier(pl, d, st_in, st_out, n_unpack, n_pack, block_bytes, stream,
                       batch=64, reps=3):
     """The DRAM tier's side of the step's restores and spills: pinned host
@@ -177,8 +253,9 @@ def measure_host_tier(pl, d, st_in, st_out, n_unpack, n_pack, block_bytes, strea
         offs = rng.permutation(n).astype(np.int64) * block_bytes
 
         def run(bm):
+            # the entry points order their copies after earlier work on the
+            # compute stream themselves
             e0.record(stream)
-            copy_s.wait_event(e0)
             rc = fn(pl, stage.data_ptr(), n, host.data_ptr(), offs, moves, n_ptr, n, bm,
                     st.data_ptr(), copy_s.cuda_stream, stream.cuda_stream, handles)
             assert rc == 0
@@ -239,6 +316,8 @@ def parse():
                     help="skip the per-tier LRU reclamation chain measurement")
     ap.add_argument("--no-host-tier", action="store_true",
                     help="skip the DRAM-tier (pinned host) restore/spill measurement")
+    ap.add_argument("--no-scale-step", action="store_true",
+                    help="skip timing the step alone on the 262144-request queue")
     ap.add_argument("--calib-copy-gb", type=float, default=0.0,
                     help="also run a plain torch copy of this size (counter calibration)")
     return ap.parse_args()
@@ -298,6 +377,7 @@ def cpu_baseline(w, res, geom, block_bytes, budget_s, tier_w=None):
         extra["tier_reclaim_chain_ms"] = (time.perf_counter() - t0) * 1e3
     return {**extra,
         "value": n / total, "unit": "req/s", "cores": 1, "kind": "oracle",
+        "host": host_cpu(),
         "step_ms": t_step * 1e3, "copy_ms_scaled": t_copy * 1e3,
         "sample": (f"full {n}-request step x{reps}; KV copies: {k} of the step's "
                    f"{len(pm) + len(um)} block moves x{creps} through the oracle memcpy, "
@@ -450,11 +530,15 @@ def main():
         dtod = {"bytes": nb_copy, "GBps": gbps(2.0 * nb_copy, us)}
         del a, b
     progress("cold-cache steps and device copy done")
+    scale = (None if args.no_scale_step or cfg == 4
+             else measure_step_only(4, stream))
     probe = None if args.no_prefix_probe else measure_prefix_probe(cfg, stream)
     reclaim, tier_w = (None, None) if args.no_reclaim else measure_reclaim(cfg, stream)
     host_tier = None if args.no_host_tier else measure_host_tier(
         pl, d, st_in, st_out, n_unpack, n_pack, block_bytes, stream)
     kernel = "kvmove_kernel" if fused else "kvcopy_kernel"
+    step_bytes = step_compulsory_bytes(w, res)
+    step_achieved = gbps(step_bytes, float(np.median(t_step)))
     copies = {"mode": args.copy, "pack_blocks": n_pack, "unpack_blocks": n_unpack,
               "paired_blocks": int((res["unpack_hazard"] >= 0).sum()),
               "copy_us_p50": float(np.median(t_c1 + t_c2)),
@@ -483,6 +567,11 @@ def main():
         "sched_step_us_p90": float(np.percentile(t_step, 90)),
         "sched_step_us_cold_p50": float(np.median(cold)),
         "sched_req_per_s": n / (float(np.median(t_step)) * 1e-6),
+        "roofline_step": {
+            "bound": "hbm", "what": "cascade_step (parts 1-3), compulsory bytes / p50",
+            "bytes_per_request": STEP_IN_BYTES_PER_REQUEST + STEP_OUT_BYTES_PER_REQUEST,
+            "bytes": step_bytes, "achieved": step_achieved, "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s", "frac": step_achieved / HBM_PEAK_GBPS},
         "kv_copy": copies,
         "step_total_us_p50": float(np.median(t_all)),
         "roofline": {"bound": "hbm", "kernel": kernel + (" (one launch: pack and unpack)" if fused
@@ -494,6 +583,8 @@ def main():
                      "bytes_per_launch": (bytes_pack + bytes_unpack) / launches,
                      "us_per_launch": copy_us / launches},
     }
+    if scale:
+        out["step_262144"] = scale
     if probe:
         out["prefix_probe"] = probe
     if reclaim:

@@ -272,17 +272,21 @@ int cascade_pack_unpack(const cascade_kv_pool_t *pool, void *pack_staging,
    host_offsets[m] of it (host array of n_moves entries, 2*num_layers*
    chunk_bytes bytes per block, in the staging order of one block), and the
    moves must use staging slot m for move m, as cascade_step's lists do.
-   cascade_restore_from_host copies each batch of batch_moves blocks host ->
-   staging on copy_stream, records events[k % n_events] there, makes
-   compute_stream wait on it and unpacks the batch on compute_stream, so the
-   host link of batch k+1 overlaps the unpack of batch k.
-   cascade_spill_to_host packs each batch on compute_stream, then copies it
-   staging -> host on copy_stream after an event.  n_moves is the host-known
-   move count (e.g. info[CASCADE_INFO_N_UNPACK] read back); n_moves_dev the
-   step's device count.  streams and events (hipEvent_t) are the caller's;
-   any work before the call on compute_stream (the step) is ordered before
-   the copies, and the caller synchronises copy_stream (spill) or
-   compute_stream (restore) before using the results.  Returns CASCADE_EINVAL
+   cascade_restore_from_host first makes copy_stream wait for the work
+   enqueued so far on compute_stream (an event recorded there), then copies
+   each batch of batch_moves blocks host -> staging on copy_stream, records
+   events[k % n_events] there, makes compute_stream wait on it and unpacks
+   the batch on compute_stream, so the host link of batch k+1 overlaps the
+   unpack of batch k.  cascade_spill_to_host packs each batch on
+   compute_stream, then copies it staging -> host on copy_stream after an
+   event.  n_moves is the host-known move count (e.g.
+   info[CASCADE_INFO_N_UNPACK] read back) and sets the host-link copies;
+   n_moves_dev is the step's device count, and moves at or past it are
+   neither unpacked nor packed.  streams and events (hipEvent_t) are the
+   caller's; any work before the call on compute_stream (the step) is
+   ordered before the copies of both directions, and the caller
+   synchronises copy_stream (spill) or compute_stream (restore) before using
+   the results.  Returns CASCADE_EINVAL
    for NULL pointers or bad sizes, CASCADE_ENOSPC when n_moves exceeds
    staging_slots, CASCADE_EHIP when a copy or launch fails. */
 int cascade_restore_from_host(const cascade_kv_pool_t *pool, void *staging,

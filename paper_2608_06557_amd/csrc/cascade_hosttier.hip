@@ -18,6 +18,7 @@
 #include <algorithm>
 
 #include "cascade.h"
+#include "copy_range.h"
 
 namespace {
 
@@ -68,6 +69,15 @@ extern "C" int cascade_restore_from_host(const cascade_kv_pool_t *pool, void *st
   const int64_t block = 2 * (int64_t)pool->num_layers * pool->chunk_bytes;
   hipStream_t cs = static_cast<hipStream_t>(copy_stream);
   hipStream_t ks = static_cast<hipStream_t>(compute_stream);
+  if (n_moves == 0) return CASCADE_OK;
+  // the host-to-staging copies start after everything enqueued so far on
+  // the compute stream (the step that wrote the move list, earlier use of
+  // the staging buffer)
+  {
+    hipEvent_t ev = static_cast<hipEvent_t>(events[0]);
+    if (hipEventRecord(ev, ks) != hipSuccess || hipStreamWaitEvent(cs, ev, 0) != hipSuccess)
+      return CASCADE_EHIP;
+  }
   for (int32_t k = 0, m0 = 0; m0 < n_moves; ++k, m0 += batch_moves) {
     const int32_t m1 = std::min(n_moves, m0 + batch_moves);
     hipEvent_t ev = static_cast<hipEvent_t>(events[k % n_events]);
@@ -75,9 +85,9 @@ extern "C" int cascade_restore_from_host(const cascade_kv_pool_t *pool, void *st
                   host_offsets, block, m0, m1, true, cs) != hipSuccess ||
         hipEventRecord(ev, cs) != hipSuccess || hipStreamWaitEvent(ks, ev, 0) != hipSuccess)
       return CASCADE_EHIP;
-    // the device count is the step's whole list; max_moves cuts this batch
-    const int rc = cascade_unpack(pool, staging, staging_slots, moves_dev + m0, n_moves_dev,
-                                  m1 - m0, status_dev, ks);
+    // moves [m0, m1) of the list, as far as the device count reaches
+    const int rc = cascade::copy_range(false, pool, staging, staging_slots, moves_dev,
+                                       n_moves_dev, m0, m1 - m0, status_dev, ks);
     if (rc != CASCADE_OK) return rc;
   }
   return CASCADE_OK;
@@ -100,8 +110,8 @@ extern "C" int cascade_spill_to_host(const cascade_kv_pool_t *pool, void *stagin
   for (int32_t k = 0, m0 = 0; m0 < n_moves; ++k, m0 += batch_moves) {
     const int32_t m1 = std::min(n_moves, m0 + batch_moves);
     hipEvent_t ev = static_cast<hipEvent_t>(events[k % n_events]);
-    const int rc = cascade_pack(pool, staging, staging_slots, moves_dev + m0, n_moves_dev,
-                                m1 - m0, status_dev, ks);
+    const int rc = cascade::copy_range(true, pool, staging, staging_slots, moves_dev,
+                                       n_moves_dev, m0, m1 - m0, status_dev, ks);
     if (rc != CASCADE_OK) return rc;
     if (hipEventRecord(ev, ks) != hipSuccess || hipStreamWaitEvent(cs, ev, 0) != hipSuccess ||
         dma_range(static_cast<char *>(staging), static_cast<char *>(host_blocks), host_offsets,

@@ -24,6 +24,7 @@
 #include <algorithm>
 
 #include "cascade.h"
+#include "copy_range.h"
 
 namespace {
 
@@ -212,8 +213,9 @@ __global__ __launch_bounds__(kBlock) void kvcopy_kernel(cascade_kv_pool_t pool, 
                                                         char *staging, int staging_slots,
                                                         const cascade_move_t *__restrict__ moves,
                                                         const int *__restrict__ n_dev,
-                                                        int max_moves, int *status) {
-  const int nm = min(*n_dev, max_moves);
+                                                        int first, int max_moves, int *status) {
+  // moves points at entry `first` of a list of *n_dev entries
+  const int nm = min(*n_dev - first, max_moves);
   if (nm <= 0) return;
   const long long total = (long long)nm * un.per_move;
   const int vecs = (int)(pool.chunk_bytes >> 4);
@@ -341,9 +343,9 @@ int grid_for(const Units &u, long long moves) {
 
 template <bool kToStaging>
 int launch(const cascade_kv_pool_t *pool, const void *staging, int32_t staging_slots,
-           const cascade_move_t *moves, const int32_t *n_dev, int32_t max_moves,
+           const cascade_move_t *moves, const int32_t *n_dev, int32_t first, int32_t max_moves,
            int32_t *status, void *stream) {
-  if (!pool_ok(pool) || !list_ok(staging, staging_slots, moves, n_dev, max_moves))
+  if (!pool_ok(pool) || !list_ok(staging, staging_slots, moves, n_dev, max_moves) || first < 0)
     return CASCADE_EINVAL;
   if (max_moves == 0) return CASCADE_OK;
   const Units u = units_for(pool);
@@ -353,26 +355,36 @@ int launch(const cascade_kv_pool_t *pool, const void *staging, int32_t staging_s
                             : kvcopy_kernel<kToStaging, 2>;
   hipLaunchKernelGGL(kernel, dim3(grid_for(u, max_moves)), dim3(kBlock), 0,
                      static_cast<hipStream_t>(stream), *pool, u,
-                     const_cast<char *>(static_cast<const char *>(staging)), staging_slots, moves,
-                     n_dev, max_moves, status);
+                     const_cast<char *>(static_cast<const char *>(staging)), staging_slots,
+                     moves + first, n_dev, first, max_moves, status);
   return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
 }
 
 }  // namespace
 
+int cascade::copy_range(bool to_staging, const cascade_kv_pool_t *pool, const void *staging,
+                        int32_t staging_slots, const cascade_move_t *moves,
+                        const int32_t *n_moves_dev, int32_t first, int32_t max_moves,
+                        int32_t *status_dev, void *stream) {
+  return to_staging ? launch<true>(pool, staging, staging_slots, moves, n_moves_dev, first,
+                                   max_moves, status_dev, stream)
+                    : launch<false>(pool, staging, staging_slots, moves, n_moves_dev, first,
+                                    max_moves, status_dev, stream);
+}
+
 extern "C" int cascade_pack(const cascade_kv_pool_t *pool, void *staging, int32_t staging_slots,
                             const cascade_move_t *moves, const int32_t *n_moves_dev,
                             int32_t max_moves, int32_t *status_dev, void *stream) {
-  return launch<true>(pool, staging, staging_slots, moves, n_moves_dev, max_moves, status_dev,
-                      stream);
+  return launch<true>(pool, staging, staging_slots, moves, n_moves_dev, 0, max_moves,
+                      status_dev, stream);
 }
 
 extern "C" int cascade_unpack(const cascade_kv_pool_t *pool, const void *staging,
                               int32_t staging_slots, const cascade_move_t *moves,
                               const int32_t *n_moves_dev, int32_t max_moves, int32_t *status_dev,
                               void *stream) {
-  return launch<false>(pool, staging, staging_slots, moves, n_moves_dev, max_moves, status_dev,
-                       stream);
+  return launch<false>(pool, staging, staging_slots, moves, n_moves_dev, 0, max_moves,
+                       status_dev, stream);
 }
 
 extern "C" int cascade_pack_unpack(const cascade_kv_pool_t *pool, void *pack_staging,

@@ -293,6 +293,7 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
   }
   __syncthreads();
   if (!s_last) return;
+  acquire_agent();
 
   // the last workgroup: totals, incoming check, plan
   int tot[3] = {0, 0, 0};
@@ -397,6 +398,7 @@ __global__ __launch_bounds__(kBlock) void rc_pass_kernel(RcArgs a) {
   if (threadIdx.x == 0) s_last = last_workgroup(a.w.tickets);
   __syncthreads();
   if (!s_last) return;
+  acquire_agent();
 
   // the last workgroup: the digit in which the sought rank falls
   const int rank = P->rank;
@@ -510,6 +512,7 @@ __global__ __launch_bounds__(kBlock) void rc_tiles_kernel(RcArgs a) {
   }
   __syncthreads();
   if (!s_last) return;
+  acquire_agent();
   Slots8 v;
 
   // the last workgroup.  1: the tile holding the take-th slot equal to T

@@ -2122,6 +2122,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     }
     __syncthreads();
     if (s_bad) return;
+    acquire_agent();  // the tiles' hand-over stores precede every read below
     finish_grid(tile - n_tiles, (int)gridDim.x - n_tiles, n, c.n_free, n_tiles, ctl, info,
                 tile_tot, free_slots, rp_list, restore_list, slots, o, s_fin);
     return;

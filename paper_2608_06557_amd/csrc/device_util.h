@@ -191,8 +191,20 @@ constexpr int kTicketStride = 32;  // one counter per 128-byte line
 // Wait until this thread's memory operations have completed.
 __device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0f70); }  // vmcnt(0)
 
+// Acquire side of a hand-over: called by every thread of a workgroup once it
+// has seen (directly, or through a workgroup barrier after one thread did)
+// the ticket or counter that says every producer's stores are complete.  An
+// agent-scope acquire fence: later loads are neither moved above it by the
+// compiler nor served from this CU's stale L1 lines (one cache invalidate;
+// it writes nothing back).
+__device__ __forceinline__ void acquire_agent() {
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
 // Called by one thread per workgroup once its results are stored: true for
-// the last workgroup of the grid to arrive.  Two levels of counters (16
+// the last workgroup of the grid to arrive (with an acquire fence in the
+// calling thread; the others call acquire_agent() after the barrier that
+// shares the answer).  Two levels of counters (16
 // groups, then one) keep the atomics on any one address to a few dozen,
 // where a single counter would serialize one per workgroup.  Counters are
 // reset by the workgroup that completes them, so every launch finds them at
@@ -207,6 +219,7 @@ __device__ __forceinline__ bool last_workgroup(unsigned *tk) {
   unsigned *top = tk + kTicketGroups * kTicketStride;
   if (atomicAdd(top, 1u) != groups - 1) return false;
   store_agent(top, 0u);
+  acquire_agent();
   return true;
 }
 

@@ -72,7 +72,10 @@ CONFIGS = {
     0: dict(n=256, model="8b", slo_s=[2, 10, 60], mix={"chat": 1.0},
             tiers=(0.50, 0.30, 0.00, 0.20), load_decodes=64, pool=4096,
             token_cap=8192, max_move=2 ** 31 - 1, elapsed_frac=1.0),
-    1: dict(n=8192, model="8b", slo_s=[1, 2, 10, 30, 60], mix={"chat": 1.0},
+    # config 0's three targets plus two looser ones: with waits uniform over
+    # the target, the least-budget head of a queue this long still has
+    # budget to restore and spill
+    1: dict(n=8192, model="8b", slo_s=[2, 10, 60, 120, 300], mix={"chat": 1.0},
             tiers=(0.35, 0.40, 0.10, 0.15), load_decodes=64, pool=65536,
             token_cap=16384, max_move=512, elapsed_frac=1.0),
     2: dict(n=65536, model="8b", slo_s=[1, 2, 10, 30, 60], mix={"chat": 0.8, "agentic": 0.2},
@@ -83,7 +86,9 @@ CONFIGS = {
             mix={"reasoning": 0.5, "chat": 0.25, "agentic": 0.25},
             classes={"chat": [0, 1, 2], "agentic": [2, 3, 4], "reasoning": [3, 4]},
             tiers=(0.35, 0.40, 0.10, 0.15), load_decodes=MAX_BATCH - 1, pool=95367,
-            token_cap=16384, max_move=954, elapsed_frac=None, shared_prefix=True),
+            token_cap=16384, max_move=954, elapsed_frac=None, shared_prefix=True,
+            family_kind="reasoning", nominal_all_tokens=True, nominal_fixed_ms=20,
+            nominal_tok_s=10_000, eps_ms=[-20, -10, 0, 10, 20]),
     # 70B-class targets are looser, as Table 3's grow with model size
     4: dict(n=262144, model="70b", slo_s=[2, 5, 10, 30, 60], mix={"chat": 0.8, "agentic": 0.2},
             classes={"chat": [0, 1, 2], "agentic": [4]},
@@ -192,14 +197,24 @@ def make_workload(cfg: int, seed: int | None = None, n: int | None = None) -> di
 
     if c.get("shared_prefix"):
         # 30% of requests extend one of 512 shared prefixes of 1k..32k tokens;
-        # they come in families of 4 parallel samples with the same suffix
-        # length, class and arrival time (exact ties in every field).
+        # they come in families of 4 parallel samples of one reasoning prompt
+        # with the same suffix length, class and arrival time (exact ties in
+        # every field).
         nfam_req = int(0.3 * n) // 4 * 4
         fam_ids = rng.permutation(n)[:nfam_req].reshape(-1, 4)
         pre_len = bt * (rng.integers(1024, 32769, 512) // bt)
         pre_tier = rng.choice(4, size=512, p=list(c["tiers"]))
         which = rng.integers(0, 512, fam_ids.shape[0])
         lead = fam_ids[:, 0]
+        fam_kind = c.get("family_kind")
+        if fam_kind is not None:
+            # parallel samples of one prompt: the family takes that kind's
+            # length law for its own suffix and one of that kind's classes
+            kj = names.index(fam_kind)
+            kind[lead] = kj
+            n_in[lead] = _lognormal(rng, LENGTHS[fam_kind]["n_in"], len(lead))
+            n_out[lead] = _lognormal(rng, LENGTHS[fam_kind]["n_out"], len(lead))
+            slo_class[lead] = rng.choice(np.array(c["classes"][fam_kind]), len(lead))
         for col in range(4):
             members = fam_ids[:, col]
             n_in[members] = pre_len[which] + n_in[lead]
@@ -210,12 +225,16 @@ def make_workload(cfg: int, seed: int | None = None, n: int | None = None) -> di
             n_prefix[members] = pre_len[which]
         n_in = np.minimum(n_in, 131072)
         n_prefix = np.minimum(n_prefix, bt * ((n_in - 1) // bt))
-        # High load: every request has already waited about its SLO minus the
-        # time its uncached tokens take at a nominal 25k tokens/s, give or take
-        # up to 20 ms (a queueing-delay model, not the scheduler's estimator).
-        uncached = np.where(tier == KV_NONE, n_in, n_in - n_prefix)
-        nominal = (uncached * SEC) // 25_000
-        eps = rng.choice(np.array([-20, -10, 0, 10, 20], np.int64) * 10 ** 6, n)
+        # High load: every request has already waited about its SLO minus a
+        # nominal service time (a fixed 20 ms plus its prompt at 10k tokens/s),
+        # give or take up to 20 ms: a queueing-delay model, not the
+        # scheduler's estimator.  Budgets end up small against the targets
+        # (median about 0.5 s), a few of them already negative.
+        uncached = np.where((tier == KV_NONE) | c.get("nominal_all_tokens", False),
+                            n_in, n_in - n_prefix)
+        nominal = (c.get("nominal_fixed_ms", 0) * 10 ** 6
+                   + (uncached * SEC) // c.get("nominal_tok_s", 25_000))
+        eps = rng.choice(np.array(c.get("eps_ms", [-20, -10, 0, 10, 20]), np.int64) * 10 ** 6, n)
         elapsed = slo_ns[slo_class] - nominal - eps
         fam_lead_elapsed = elapsed[lead]
         for col in range(4):

@@ -119,6 +119,47 @@ def _chunk_words(geom, slot, l, kv):
     return np.arange(off // 4, (off + geom["chunk_bytes"]) // 4, dtype=np.int64)
 
 
+def _block_words(geom, slot):
+    """Word indices (4-byte words of the pool) of every (layer, K/V) chunk of
+    pool slot `slot`, in the chunk order of one staging slot."""
+    import torch
+    L, cw = geom["num_layers"], geom["chunk_bytes"] // 4
+    base = torch.tensor([(l * geom["layer_stride"] + kv * geom["kv_stride"]
+                          + slot * geom["slot_stride"]) // 4
+                         for l in range(L) for kv in range(2)], dtype=torch.int64,
+                        device="cuda")
+    return (base[:, None] + torch.arange(cw, device="cuda")[None, :]).reshape(-1)
+
+
+def _u32(t):
+    import torch
+    return t.view(torch.int32).to(torch.int64) & 0xFFFFFFFF
+
+
+def _check_packed_block(st_out, geom, staging_slot, pool_slot, seed):
+    """Staging slot `staging_slot` holds all 2L chunks of pool slot
+    `pool_slot` as filled with pattern `seed` (checked on the GPU)."""
+    import paper_2608_06557_amd.synth as synth
+    blk = 2 * geom["num_layers"] * geom["chunk_bytes"]
+    got = _u32(st_out[staging_slot * blk:(staging_slot + 1) * blk])
+    exp = synth.hash32_torch(_block_words(geom, pool_slot), seed)
+    bad = (got != exp).nonzero()
+    assert bad.numel() == 0, (staging_slot, pool_slot, int(bad[0]) if bad.numel() else None)
+
+
+def _check_unpacked_block(pool, geom, pool_slot, staging_slot, seed):
+    """Every chunk of pool slot `pool_slot` holds staging slot `staging_slot`
+    as filled with pattern `seed`."""
+    import torch
+    import paper_2608_06557_amd.synth as synth
+    blk4 = 2 * geom["num_layers"] * geom["chunk_bytes"] // 4
+    got = pool.view(torch.int32)[_block_words(geom, pool_slot)].to(torch.int64) & 0xFFFFFFFF
+    exp = synth.hash32_torch(torch.arange(staging_slot * blk4, (staging_slot + 1) * blk4,
+                                          device="cuda"), seed)
+    bad = (got != exp).nonzero()
+    assert bad.numel() == 0, (pool_slot, staging_slot, int(bad[0]) if bad.numel() else None)
+
+
 def test_65536_request_step_moves_full_size(dev):
     """Config 2 at full size: 200 GB pool, the step's own move lists, pack
     then unpack as the benchmark runs them; sampled chunks checked."""
@@ -154,24 +195,13 @@ def test_65536_request_step_moves_full_size(dev):
     assert int(status.item()) == 0
     rng = np.random.default_rng(5)
     L = geom["num_layers"]
-    cw = geom["chunk_bytes"] // 4
     pm, um = res["pack_moves"], res["unpack_moves"]
     unpacked = set(um["pool_slot"].tolist())
-    for k in rng.choice(npk, 24, replace=False):
-        m = pm[k]
-        for l, kv in [(0, 0), (L - 1, 1), (int(rng.integers(L)), int(rng.integers(2)))]:
-            soff = ((int(m["staging_slot"]) * L + l) * 2 + kv) * cw
-            got = st_out[4 * soff:4 * (soff + cw)].view(torch.int32).cpu().numpy()
-            exp = synth.hash32_np(_chunk_words(geom, int(m["pool_slot"]), l, kv), 1)
-            assert np.array_equal(got.view(np.uint32), exp)
-    for k in rng.choice(nup, 24, replace=False):
-        m = um[k]
-        for l, kv in [(0, 1), (L - 1, 0), (int(rng.integers(L)), int(rng.integers(2)))]:
-            words = _chunk_words(geom, int(m["pool_slot"]), l, kv)
-            got = pool[4 * words[0]:4 * (words[-1] + 1)].view(torch.int32).cpu().numpy()
-            soff = ((int(m["staging_slot"]) * L + l) * 2 + kv) * cw
-            exp = synth.hash32_np(np.arange(soff, soff + cw, dtype=np.int64), 2)
-            assert np.array_equal(got.view(np.uint32), exp)
+    # every (layer, K/V) chunk of each sampled block
+    for k in rng.choice(npk, 48, replace=False):
+        _check_packed_block(st_out, geom, int(pm[k]["staging_slot"]), int(pm[k]["pool_slot"]), 1)
+    for k in rng.choice(nup, 48, replace=False):
+        _check_unpacked_block(pool, geom, int(um[k]["pool_slot"]), int(um[k]["staging_slot"]), 2)
     # slots nobody wrote keep their bytes
     for slot in rng.choice(geom["num_blocks"], 64, replace=False):
         if int(slot) in unpacked:
@@ -302,7 +332,7 @@ def test_fused_bad_moves_skipped(dev):
     assert np.array_equal(pool.cpu().numpy(), exp_pool)
 
 
-@pytest.mark.parametrize("cfg", [2, 4])
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
 def test_fused_step_moves_full_size(dev, cfg):
     """The step's own lists at full size (200 GB / 250 GB pools), hazards
     included: every spilled block that a restore overwrites is checked to
@@ -317,7 +347,8 @@ def test_fused_step_moves_full_size(dev, cfg):
     assert res["status"] == 0
     npk, nup = res["n_pack"], res["n_unpack"]
     paired = np.flatnonzero(res["pack_hazard"] >= 0)
-    assert len(paired) > 100
+    assert npk > 50 and nup > 50
+    assert len(paired) > (50 if cfg != 1 else -1)
     print(f"config {cfg}: pool {geom['pool_bytes'] / 1e9:.1f} GB, pack {npk}, unpack {nup}, "
           f"paired {len(paired)}", flush=True)
     pool = torch.empty(geom["pool_bytes"], dtype=torch.uint8, device="cuda")
@@ -337,26 +368,14 @@ def test_fused_step_moves_full_size(dev, cfg):
     torch.cuda.synchronize()
     assert int(status.item()) == 0
     rng = np.random.default_rng(11)
-    L = geom["num_layers"]
-    cw = geom["chunk_bytes"] // 4
     pm, um = res["pack_moves"], res["unpack_moves"]
-    sample_p = np.unique(np.concatenate([paired, rng.choice(npk, 24, replace=False)]))
+    # every paired block and a sample of the rest, each with all its chunks
+    sample_p = np.unique(np.concatenate([paired, rng.choice(npk, 32, replace=False)]))
     for k in sample_p:
-        m = pm[k]
-        for l, kv in [(0, 0), (L - 1, 1), (int(rng.integers(L)), int(rng.integers(2)))]:
-            soff = ((int(m["staging_slot"]) * L + l) * 2 + kv) * cw
-            got = st_out[4 * soff:4 * (soff + cw)].view(torch.int32).cpu().numpy()
-            exp = synth.hash32_np(_chunk_words(geom, int(m["pool_slot"]), l, kv), 1)
-            assert np.array_equal(got.view(np.uint32), exp), (cfg, int(k), l, kv)
+        _check_packed_block(st_out, geom, int(pm[k]["staging_slot"]), int(pm[k]["pool_slot"]), 1)
     sample_u = np.unique(np.concatenate([res["pack_hazard"][paired],
-                                         rng.choice(nup, 24, replace=False)]))
+                                         rng.choice(nup, 32, replace=False)]))
     for k in sample_u:
-        m = um[k]
-        for l, kv in [(0, 1), (L - 1, 0), (int(rng.integers(L)), int(rng.integers(2)))]:
-            words = _chunk_words(geom, int(m["pool_slot"]), l, kv)
-            got = pool[4 * words[0]:4 * (words[-1] + 1)].view(torch.int32).cpu().numpy()
-            soff = ((int(m["staging_slot"]) * L + l) * 2 + kv) * cw
-            exp = synth.hash32_np(np.arange(soff, soff + cw, dtype=np.int64), 2)
-            assert np.array_equal(got.view(np.uint32), exp), (cfg, int(k), l, kv)
+        _check_unpacked_block(pool, geom, int(um[k]["pool_slot"]), int(um[k]["staging_slot"]), 2)
     del pool, st_in, st_out
     torch.cuda.empty_cache()

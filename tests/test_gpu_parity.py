@@ -225,6 +225,19 @@ def test_worked_example(dev):
     assert list(g["order"]) == gold["expected_step"]["order"]
 
 
+def test_second_worked_example(dev):
+    """PREFETCH, HBM-prefix RETAIN inside and outside the batch, three
+    victims spilled and dropped from the back of the order."""
+    w, gold = helpers.golden_workload("worked_example_2.json")
+    g, o = run_both(dev, w)
+    assert_same(g, o, "second worked example")
+    exp = gold["expected_step"]
+    for k in ["order", "action", "restore_blocks", "tokens_granted"]:
+        assert [int(x) for x in g[k]] == exp[k], k
+    assert [list(map(int, m)) for m in g["pack_moves"].view(np.int32).reshape(-1, 4)] \
+        == exp["pack_moves"]
+
+
 def test_scarce_resources(dev):
     rng = np.random.default_rng(99)
     for t in range(150):
