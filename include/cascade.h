@@ -222,6 +222,25 @@ int cascade_step(const cascade_requests_t *requests, const cascade_block_table_t
                  const cascade_outputs_t *out, void *workspace, size_t workspace_bytes,
                  void *stream);
 
+/* cascade_step for callers that cannot allocate device memory: code under
+   HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+   The same step, on the same kernels, with the same results; the workspace
+   is a fixed array inside the library instead of an argument, one per GPU,
+   sized for CASCADE_NOALLOC_MAX_REQUESTS requests (about 45 MB) and held
+   until the process ends.  The call allocates nothing.  Its first call on a
+   device looks up that device's array (the calling thread's current
+   device, which must be the stream's), so make that first call outside
+   graph capture.  Every call on one GPU shares that GPU's array: calls that
+   overlap in time on one GPU (streams not ordered against each other, or
+   host threads) race and give undefined results.  Returns CASCADE_ENOSPC
+   when requests->n exceeds CASCADE_NOALLOC_MAX_REQUESTS (nothing is
+   enqueued), CASCADE_EHIP when the array cannot be located, and otherwise
+   what cascade_step returns. */
+#define CASCADE_NOALLOC_MAX_REQUESTS 262144
+int cascade_step_noalloc(const cascade_requests_t *requests, const cascade_block_table_t *table,
+                         const cascade_tier_state_t *tier, const cascade_params_t *params,
+                         const cascade_outputs_t *out, void *stream);
+
 /* KV block gather (Section 4.4 preemption spill): for each of the first
    min(*n_moves_dev, max_moves) moves, copy every (layer, K/V) chunk of HBM
    pool slot moves[m].pool_slot to staging slot moves[m].staging_slot of a

@@ -22,7 +22,8 @@ ACT_PREEMPT_OFFLOAD, ACT_PREEMPT_DROP = 5, 6
 INFO_STATUS, INFO_N_ADMITTED, INFO_N_SLOT_LIST, INFO_N_UNPACK, INFO_N_PACK = 0, 1, 2, 3, 4
 INFO_LEN = 8
 
-EXPORTED = ["cascade_step_workspace_bytes", "cascade_step", "cascade_pack", "cascade_unpack",
+EXPORTED = ["cascade_step_workspace_bytes", "cascade_step", "cascade_step_noalloc",
+            "cascade_pack", "cascade_unpack",
             "cascade_pack_unpack", "cascade_prefix_index_bytes", "cascade_prefix_index_clear",
             "cascade_prefix_index_insert", "cascade_prefix_probe", "cascade_restore_from_host",
             "cascade_spill_to_host", "cascade_reclaim_workspace_bytes", "cascade_tier_reclaim",
@@ -108,6 +109,10 @@ def load() -> C.CDLL:
         L.cascade_step.argtypes = [C.POINTER(Requests), C.POINTER(BlockTable),
                                    C.POINTER(TierState), C.POINTER(Params), C.POINTER(Outputs),
                                    C.c_void_p, C.c_size_t, C.c_void_p]
+        L.cascade_step_noalloc.restype = C.c_int
+        L.cascade_step_noalloc.argtypes = [C.POINTER(Requests), C.POINTER(BlockTable),
+                                           C.POINTER(TierState), C.POINTER(Params),
+                                           C.POINTER(Outputs), C.c_void_p]
         for name in ("cascade_pack", "cascade_unpack"):
             f = getattr(L, name)
             f.restype = C.c_int
@@ -160,6 +165,16 @@ def cascade_step(requests: Requests, table: BlockTable, tier: TierState, params:
     return int(load().cascade_step(C.byref(requests), C.byref(table), C.byref(tier),
                                    C.byref(params), C.byref(outputs), C.c_void_p(workspace),
                                    workspace_bytes, C.c_void_p(stream)))
+
+
+NOALLOC_MAX_REQUESTS = 262144
+
+
+def cascade_step_noalloc(requests: Requests, table: BlockTable, tier: TierState, params: Params,
+                         outputs: Outputs, stream: int) -> int:
+    return int(load().cascade_step_noalloc(C.byref(requests), C.byref(table), C.byref(tier),
+                                           C.byref(params), C.byref(outputs),
+                                           C.c_void_p(stream)))
 
 
 def cascade_pack(pool: KvPool, staging: int, staging_slots: int, moves: int, n_moves_dev: int,

@@ -36,6 +36,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "cascade.h"
 #include "device_util.h"
@@ -2555,14 +2556,15 @@ __global__ __launch_bounds__(kBlock) void empty_step_kernel(int n_free, int num_
 // ---------------------------------------------------------------- host
 
 struct Layout {
-  size_t ctl, scan1, scan2, sort_status, partials, keys_a, keys_b, vals_a, vals_b, rec,
-      s_order, s_rec, rp_list, restore, tile_tot, total;
-  int sort_tiles, scan_tiles, eval_grid;
+  size_t ctl = 0, scan1 = 0, scan2 = 0, sort_status = 0, partials = 0, keys_a = 0, keys_b = 0,
+         vals_a = 0, vals_b = 0, rec = 0, s_order = 0, s_rec = 0, rp_list = 0, restore = 0,
+         tile_tot = 0, total = 0;
+  int sort_tiles = 0, scan_tiles = 0, eval_grid = 0;
 };
 
-size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
+constexpr size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 
-Layout make_layout(int32_t n) {
+constexpr Layout make_layout(int32_t n) {
   Layout L;
   const size_t np = n > 0 ? (size_t)n : 1;
   L.sort_tiles = (int)((np + kSortTileTiny - 1) / kSortTileTiny);  // the most tiles a sort uses
@@ -2683,10 +2685,14 @@ extern "C" const char *cascade_strerror(int code) {
   }
 }
 
-extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_table_t *bt,
-                            const cascade_tier_state_t *ts, const cascade_params_t *p,
-                            const cascade_outputs_t *out, void *workspace,
-                            size_t workspace_bytes, void *stream) {
+namespace {
+
+// The whole step on a caller's workspace (cascade_step) or on this device's
+// fixed array (cascade_step_noalloc).
+int step_impl(const cascade_requests_t *rq, const cascade_block_table_t *bt,
+              const cascade_tier_state_t *ts, const cascade_params_t *p,
+              const cascade_outputs_t *out, void *workspace, size_t workspace_bytes,
+              void *stream) {
   if (!rq || !bt || !ts || !p || !out || !workspace) return CASCADE_EINVAL;
   const int n = rq->n;
   if (!params_ok(p, n, ts)) return CASCADE_EINVAL;
@@ -2824,4 +2830,56 @@ extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_ta
                      ts->free_slots, o, rp_list, rlist, tile_tot, l1_tot, l2_status);
   if (hipGetLastError() != hipSuccess) return CASCADE_EHIP;
   return CASCADE_OK;
+}
+
+}  // namespace
+
+extern "C" int cascade_step(const cascade_requests_t *rq, const cascade_block_table_t *bt,
+                            const cascade_tier_state_t *ts, const cascade_params_t *p,
+                            const cascade_outputs_t *out, void *workspace,
+                            size_t workspace_bytes, void *stream) {
+  return step_impl(rq, bt, ts, p, out, workspace, workspace_bytes, stream);
+}
+
+// ------------------------------------------------ step without a workspace
+
+// The workspace of cascade_step_noalloc: one fixed array per GPU, sized for
+// CASCADE_NOALLOC_MAX_REQUESTS requests and held until the process ends.
+// Its name is a host-side stand-in, not a device address: host code only
+// ever passes the address hipGetSymbolAddress returns for the current device.
+static constexpr size_t kScratchBytes = make_layout(CASCADE_NOALLOC_MAX_REQUESTS).total;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_addr[kScratchDevices];  // device address of `scratch`, per GPU
+
+// This GPU's copy of `scratch`: looked up once per device, with that device
+// current (every GPU holds the array at its own address).
+int scratch_of_current_device(void **addr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return CASCADE_EHIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[dev] == nullptr) {
+    void *a = nullptr;
+    if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) != hipSuccess || a == nullptr)
+      return CASCADE_EHIP;
+    g_scratch_addr[dev] = a;
+  }
+  *addr = g_scratch_addr[dev];
+  return CASCADE_OK;
+}
+}  // namespace
+
+extern "C" int cascade_step_noalloc(const cascade_requests_t *rq,
+                                    const cascade_block_table_t *bt,
+                                    const cascade_tier_state_t *ts, const cascade_params_t *p,
+                                    const cascade_outputs_t *out, void *stream) {
+  if (!rq) return CASCADE_EINVAL;
+  if (rq->n > CASCADE_NOALLOC_MAX_REQUESTS) return CASCADE_ENOSPC;
+  void *ws = nullptr;
+  const int rc = scratch_of_current_device(&ws);
+  if (rc != CASCADE_OK) return rc;
+  return step_impl(rq, bt, ts, p, out, ws, kScratchBytes, stream);
 }

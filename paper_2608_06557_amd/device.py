@@ -92,6 +92,11 @@ class DeviceStep:
         return cx.cascade_step(self.c_req, self.c_table, self.c_tier, self.params, self.c_out,
                                self.ws_ptr, self.ws_bytes, stream_handle(stream))
 
+    def run_noalloc(self, stream=None) -> int:
+        """The same step through cascade_step_noalloc (no workspace)."""
+        return cx.cascade_step_noalloc(self.c_req, self.c_table, self.c_tier, self.params,
+                                       self.c_out, stream_handle(stream))
+
     def n_unpack_ptr(self) -> int:
         return self.info.data_ptr() + 4 * cx.INFO_N_UNPACK
 
