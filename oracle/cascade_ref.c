@@ -35,6 +35,11 @@
  *      (no HBM this step: HBM is allocated only at the final hop).
  *  R16 The link-bandwidth constraint of eq:opt_goal_compact is a per-step
  *      cap U on restore+prefetch blocks, taken in priority order.
+ *  R36 Shared prefixes (optional prefix_group input): within a priority
+ *      group, the first deep member of a prefix group with a positive want
+ *      restores; later members of the same group and tier reference its
+ *      restored blocks (as many as their own prefix has) instead of
+ *      restoring again.  See cascade_ref.h.
  */
 #include "cascade_ref.h"
 
@@ -226,9 +231,12 @@ int32_t cref_step(int32_t n, const uint64_t *id, const uint8_t *cls, const uint8
                   const uint8_t *qt, const uint8_t *pt, const int64_t *arr,
                   const int32_t *nin, const int32_t *nout, const int32_t *npre,
                   const int32_t *nprog, const int32_t *ro, const int32_t *slots,
-                  int32_t n_free, const int32_t *free_slots,
+                  int32_t n_free, const int32_t *free_slots, const int32_t *pg,
                   const cref_params *p, cref_outputs *out) {
   if (cref_check_params(p, n, n_free) != CREF_OK) return CREF_EINVAL;
+  if (pg)
+    for (int32_t i = 0; i < n; i++)
+      if (pg[i] < -1 || pg[i] >= n) return CREF_EINVAL;
   if (out->slot_list_capacity < 0 || out->unpack_capacity < 0 || out->pack_capacity < 0)
     return CREF_EINVAL;
   for (int32_t i = 0; i < n; i++)
@@ -248,6 +256,13 @@ int32_t cref_step(int32_t n, const uint64_t *id, const uint8_t *cls, const uint8
   int64_t *nb = (int64_t *)calloc(n ? n : 1, sizeof(int64_t));
   uint8_t *adm = (uint8_t *)calloc(n ? n : 1, 1);
   uint8_t *victim = (uint8_t *)calloc(n ? n : 1, 1);
+  /* shared prefixes (R36): the leader of each (prefix group, priority
+     group), and for every follower its leader and shared blocks */
+  int32_t *leader_of = (int32_t *)malloc(sizeof(int32_t) * 2 * (size_t)(n ? n : 1));
+  int32_t *follows = (int32_t *)malloc(sizeof(int32_t) * (size_t)(n ? n : 1));
+  int32_t *shared = (int32_t *)calloc(n ? n : 1, sizeof(int32_t));
+  for (int32_t k = 0; k < 2 * n; k++) leader_of[k] = -1;
+  for (int32_t i = 0; i < n; i++) follows[i] = -1;
 
   /* Phase 1 and the budget update (eq:est_latency .. eq:rem_budget_eq). */
   for (int32_t i = 0; i < n; i++) {
@@ -266,13 +281,26 @@ int32_t cref_step(int32_t n, const uint64_t *id, const uint8_t *cls, const uint8
   }
 
   /* Algorithm 1, Phase 2, walked in priority order. */
-  /* (a) Restore / prefetch volume, capped per step at U blocks (R16). */
+  /* (a) Restore / prefetch volume, capped per step at U blocks (R16).  A
+         follower of a shared prefix restores nothing itself (R36). */
   int64_t move_left = p->max_move_blocks;
   for (int32_t q = 0; q < n; q++) {
     int32_t i = pq[q].idx;
+    int deep = pg && pg[i] >= 0 && st[i] == CREF_QUEUED &&
+               (pt[i] == CREF_KV_DRAM || pt[i] == CREF_KV_NVME);
+    int32_t slot = deep ? 2 * pg[i] + (ev[i].group == 2 ? 1 : 0) : -1;
+    if (deep && leader_of[slot] >= 0) {
+      int32_t lead = leader_of[slot];
+      int32_t pb = npre[i] / p->block_tokens;
+      follows[i] = lead;
+      shared[i] = r[lead] < pb ? r[lead] : pb;
+      r[i] = 0;
+      continue;
+    }
     int64_t take = min64(ev[i].want_blocks, move_left);
     r[i] = (int32_t)take;
     move_left -= take;
+    if (deep && ev[i].want_blocks > 0) leader_of[slot] = i;
   }
   /* (b) Chunked-prefill token grants under the cap, with the Tier-2
          reserve (R9).  need = tokens still to compute this step. */
@@ -286,6 +314,7 @@ int32_t cref_step(int32_t n, const uint64_t *id, const uint8_t *cls, const uint8
     if (st[i] == CREF_DECODE) need = 1;
     else if (st[i] == CREF_RUNNING_PREFILL) need = nin[i] - nprog[i];
     else if (pt[i] == CREF_KV_HBM) need = nin[i] - npre[i];
+    else if (follows[i] >= 0) need = nin[i] - bt * shared[i];
     else need = nin[i] - bt * r[i];
     int64_t gi = min64(need, left);
     g[i] = gi;
@@ -305,7 +334,10 @@ int32_t cref_step(int32_t n, const uint64_t *id, const uint8_t *cls, const uint8
     int32_t i = pq[q].idx;
     if (g[i] <= 0) continue;
     int64_t held = ro[i + 1] - ro[i];
-    if (st[i] == CREF_QUEUED) {
+    if (st[i] == CREF_QUEUED && follows[i] >= 0) {
+      /* the shared blocks are referenced, not allocated */
+      nb[i] = ceil_div(bt * shared[i] + g[i], bt) - shared[i];
+    } else if (st[i] == CREF_QUEUED) {
       int64_t reuse = (pt[i] == CREF_KV_HBM) ? npre[i] : bt * r[i];
       nb[i] = ceil_div(reuse + g[i], bt) - (pt[i] == CREF_KV_HBM ? npre[i] / bt : 0);
     } else if (st[i] == CREF_RUNNING_PREFILL) {
@@ -343,13 +375,17 @@ int32_t cref_step(int32_t n, const uint64_t *id, const uint8_t *cls, const uint8
               ? CREF_ACT_PREEMPT_OFFLOAD : CREF_ACT_PREEMPT_DROP;     /* R13 */
     } else if (st[i] != CREF_QUEUED || pt[i] == CREF_KV_HBM) {
       a = CREF_ACT_RETAIN;
+    } else if (follows[i] >= 0) {
+      a = shared[i] > 0 ? CREF_ACT_SHARE : CREF_ACT_RECOMPUTE;   /* R36 */
     } else if (pt[i] == CREF_KV_NONE || r[i] == 0) {
       a = CREF_ACT_RECOMPUTE;
     } else {
       a = adm[i] ? CREF_ACT_RESTORE : CREF_ACT_PREFETCH;              /* R15 */
     }
     out->action[i] = (uint8_t)a;
-    out->restore_blocks[i] = r[i];
+    out->restore_blocks[i] = follows[i] >= 0 ? shared[i] : r[i];
+    if (out->share_leader)
+      out->share_leader[i] = (follows[i] >= 0 && shared[i] > 0) ? follows[i] : -1;
     out->tokens_granted[i] = adm[i] ? (int32_t)g[i] : 0;
     out->alloc_begin[i] = -1;
     out->alloc_count[i] = 0;
@@ -424,6 +460,7 @@ int32_t cref_step(int32_t n, const uint64_t *id, const uint8_t *cls, const uint8
   }
 
   free(ev); free(pq); free(r); free(g); free(nb); free(adm); free(victim);
+  free(leader_of); free(follows); free(shared);
   return status;
 }
 

@@ -46,6 +46,7 @@
 #define CREF_ACT_RECOMPUTE 4
 #define CREF_ACT_PREEMPT_OFFLOAD 5
 #define CREF_ACT_PREEMPT_DROP 6
+#define CREF_ACT_SHARE 7          /* references a prefix another request restores */
 
 typedef struct {
   int64_t t_now_ns;
@@ -87,6 +88,10 @@ typedef struct {
      the slot that pack move j reads, -1 where there is none. */
   int32_t *unpack_hazard;
   int32_t *pack_hazard;
+  /* Shared-prefix restores (only with a prefix_group input; may be NULL):
+     for a request that shares another request's restore (action SHARE),
+     that request's index, else -1. */
+  int32_t *share_leader;
 } cref_outputs;
 
 /* Intermediate values of the per-request evaluation, exposed for pinning. */
@@ -108,12 +113,27 @@ void cref_eval(const cref_params *p, uint8_t slo_class, uint8_t state, uint8_t q
                uint8_t prefix_tier, int64_t arrival_ns, int32_t n_in, int32_t n_out_pred,
                int32_t n_prefix, int32_t n_progress, cref_eval_out *o);
 
+/* One step.  prefix_group (NULL = none) turns on shared-prefix restores
+   within the step (Section 4.4 prefix hit detection; the paper leaves
+   within-step sharing open, the reading is this oracle's): requests with
+   the same group id g >= 0 share the leading blocks of their matched
+   prefixes.  It matters for queued requests whose prefix is in DRAM or NVMe
+   ("deep members").  Within each priority group (Tier-1 with decodes,
+   Tier-2) the first deep member in priority order with a positive restore
+   want is the group's leader: it restores under the link cap as any
+   request does.  Every later deep member of the same group and tier is a
+   follower: it takes nothing from the link cap and references the first
+   min(leader's restore blocks, its own prefix blocks) blocks of the
+   leader's restore, like an HBM prefix (need and new blocks shrink
+   accordingly); action SHARE, restore_blocks = those blocks, share_leader
+   = the leader (RECOMPUTE and -1 when that is 0 blocks).  Group ids must
+   lie in [-1, n). */
 int32_t cref_step(int32_t n, const uint64_t *id, const uint8_t *slo_class, const uint8_t *state,
                   const uint8_t *queue_tier, const uint8_t *prefix_tier,
                   const int64_t *arrival_ns, const int32_t *n_in, const int32_t *n_out_pred,
                   const int32_t *n_prefix, const int32_t *n_progress,
                   const int32_t *row_offsets, const int32_t *slots,
-                  int32_t n_free, const int32_t *free_slots,
+                  int32_t n_free, const int32_t *free_slots, const int32_t *prefix_group,
                   const cref_params *p, cref_outputs *out);
 
 /* Paged-KV block copies, one chunk_bytes memcpy per (move, layer, K/V). */

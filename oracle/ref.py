@@ -28,7 +28,7 @@ QUEUED, RUNNING_PREFILL, DECODE = 0, 1, 2
 QT_NEW, QT_TIER1, QT_TIER2 = 0, 1, 2
 KV_HBM, KV_DRAM, KV_NVME, KV_NONE = 0, 1, 2, 3
 ACT_RETAIN, ACT_RESTORE, ACT_PREFETCH, ACT_RECOMPUTE = 1, 2, 3, 4
-ACT_PREEMPT_OFFLOAD, ACT_PREEMPT_DROP = 5, 6
+ACT_PREEMPT_OFFLOAD, ACT_PREEMPT_DROP, ACT_SHARE = 5, 6, 7
 
 
 def build(force: bool = True) -> str:
@@ -70,6 +70,7 @@ class Outputs(C.Structure):
         ("unpack_moves", C.c_void_p), ("unpack_capacity", C.c_int32), ("n_unpack", C.c_int32),
         ("pack_moves", C.c_void_p), ("pack_capacity", C.c_int32), ("n_pack", C.c_int32),
         ("unpack_hazard", C.c_void_p), ("pack_hazard", C.c_void_p),
+        ("share_leader", C.c_void_p),
     ]
 
 
@@ -101,7 +102,7 @@ def _bind(L):
                             C.c_int64, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                             C.POINTER(EvalOut)]
     L.cref_step.restype = C.c_int32
-    L.cref_step.argtypes = [C.c_int32] + [C.c_void_p] * 12 + [C.c_int32, C.c_void_p,
+    L.cref_step.argtypes = [C.c_int32] + [C.c_void_p] * 12 + [C.c_int32, C.c_void_p, C.c_void_p,
                                                                C.POINTER(Params),
                                                                C.POINTER(Outputs)]
     L.cref_pack.restype = None
@@ -194,7 +195,8 @@ def _ptr(a: np.ndarray):
 
 def step(w: dict, slot_cap: int | None = None, unpack_cap: int | None = None,
          pack_cap: int | None = None) -> dict:
-    """Run the oracle step on a workload dict (numpy arrays + params).
+    """Run the oracle step on a workload dict (numpy arrays + params; an
+    optional "prefix_group" array turns on shared-prefix restores).
 
     Returns every output array, the counts and the return code."""
     n = int(len(w["id"]))
@@ -234,8 +236,16 @@ def step(w: dict, slot_cap: int | None = None, unpack_cap: int | None = None,
     out.unpack_moves, out.unpack_capacity = _ptr(um), unpack_cap
     out.pack_moves, out.pack_capacity = _ptr(pm), pack_cap
     out.unpack_hazard, out.pack_hazard = _ptr(uh), _ptr(ph)
+    pg = None
+    if w.get("prefix_group") is not None:
+        pg = np.ascontiguousarray(w["prefix_group"], dtype=np.int32)
+        if pg.size == 0:
+            pg = np.zeros(1, np.int32)
+        o["share_leader"] = np.full(nn, -7, np.int32)
+        out.share_leader = _ptr(o["share_leader"])
     args = [_ptr(req[k]) for k, _ in REQ_FIELDS] + [_ptr(ro), _ptr(slots)]
-    rc = lib().cref_step(n, *args, n_free, _ptr(free), C.byref(make_params(p)), C.byref(out))
+    rc = lib().cref_step(n, *args, n_free, _ptr(free), None if pg is None else _ptr(pg),
+                         C.byref(make_params(p)), C.byref(out))
     res = {k: v[:n] for k, v in o.items()}
     res["rc"] = rc
     res["n_admitted"] = out.n_admitted

@@ -77,13 +77,38 @@ def test_all_equal_keys_give_identity_order():
     assert r["rc"] == ref.OK and list(r["order"]) == list(range(8))
 
 
-def _blocks_needed(w, i, g, r):
+def _sharing(w, ev, order):
+    """Leaders and followers of shared prefixes, by walking the order: in
+    each (prefix group, priority group) the first queued DRAM/NVMe member
+    with a positive want leads; every later such member follows it."""
+    pg = w.get("prefix_group")
+    follows = {}
+    if pg is None:
+        return follows
+    leader = {}
+    for i in order:
+        deep = (int(pg[i]) >= 0 and w["state"][i] == helpers.QUEUED
+                and w["prefix_tier"][i] in (helpers.KV_DRAM, helpers.KV_NVME))
+        if not deep:
+            continue
+        key = (int(pg[i]), ev[i]["group"])
+        if key in leader:
+            follows[i] = leader[key]
+        elif ev[i]["want_blocks"] > 0:
+            leader[key] = i
+    return follows
+
+
+def _blocks_needed(w, i, g, r, shared=None):
     """New HBM blocks so request i holds its reused/restored prefix and g new
     tokens (the tokens it will have after this step, minus what is already in
-    HBM for it: its own row, or a shared HBM prefix)."""
+    HBM for it: its own row, a shared HBM prefix, or blocks another request
+    restores for it)."""
     bt = w["params"]["block_tokens"]
     st, pt = int(w["state"][i]), int(w["prefix_tier"][i])
     row = int(w["row_offsets"][i + 1] - w["row_offsets"][i])
+    if shared is not None:
+        return math.ceil((bt * shared + g) / bt) - shared
     if st == helpers.DECODE:
         tokens_after = int(w["n_in"][i]) + int(w["n_progress"][i]) + 1
         return math.ceil(tokens_after / bt) - row
@@ -107,14 +132,22 @@ def _check_against_definitions(w):
     row = np.diff(w["row_offsets"]).astype(int)
 
     # restore / prefetch blocks: one block at a time to the first request in
-    # priority order that still wants one, until U blocks are out
+    # priority order that still wants one, until U blocks are out; followers
+    # of a shared prefix want none themselves and take min(leader's blocks,
+    # own prefix blocks) of the leader's restore
+    follows = _sharing(w, ev, order)
     got = [0] * n
     for _ in range(min(p["max_move_blocks"], 10 ** 6)):
-        nxt = next((i for i in order if got[i] < ev[i]["want_blocks"]), None)
+        nxt = next((i for i in order if i not in follows and got[i] < ev[i]["want_blocks"]),
+                   None)
         if nxt is None:
             break
         got[nxt] += 1
-    assert list(res["restore_blocks"]) == got
+    share = {i: min(got[l], int(w["n_prefix"][i]) // bt) for i, l in follows.items()}
+    assert list(res["restore_blocks"]) == [share.get(i, got[i]) for i in range(n)]
+    if "prefix_group" in w:
+        assert list(res["share_leader"]) == [follows[i] if share.get(i, 0) > 0 else -1
+                                            for i in range(n)]
 
     # tokens: one at a time; decodes and Tier-1 share cap - reserve (the
     # reserve exists only if Tier-2 is non-empty), Tier-2 gets what is left
@@ -125,6 +158,8 @@ def _check_against_definitions(w):
             return int(w["n_in"][i] - w["n_progress"][i])
         if w["prefix_tier"][i] == helpers.KV_HBM:
             return int(w["n_in"][i] - w["n_prefix"][i])
+        if i in share:
+            return int(w["n_in"][i]) - bt * share[i]
         return int(w["n_in"][i]) - bt * got[i]
     has2 = any(e["group"] == 2 for e in ev)
     reserve = (p["token_cap"] * p["tier2_reserve_q16"]) // 65536 if has2 else 0
@@ -152,8 +187,8 @@ def _check_against_definitions(w):
     granted = [i for i in order if g[i] > 0]
     held_total = int(sum(row[i] for i in range(n) if st[i] == helpers.RUNNING_PREFILL))
     avail = len(w["free_slots"]) + held_total
-    cost = {i: _blocks_needed(w, i, g[i], got[i]) +
-            (row[i] if st[i] == helpers.RUNNING_PREFILL else 0) for i in granted}
+    nbk = lambda i: _blocks_needed(w, i, g[i], got[i], share.get(i))
+    cost = {i: nbk(i) + (row[i] if st[i] == helpers.RUNNING_PREFILL else 0) for i in granted}
     best = 0
     for j in range(len(granted) + 1):
         if sum(cost[i] for i in granted[:j]) <= avail:
@@ -163,11 +198,11 @@ def _check_against_definitions(w):
     for i in range(n):
         assert res["tokens_granted"][i] == (g[i] if i in admitted else 0)
         if i in admitted:
-            assert res["alloc_count"][i] == _blocks_needed(w, i, g[i], got[i])
+            assert res["alloc_count"][i] == nbk(i)
 
     # victims: smallest set of non-admitted prefill holders, taken from the
     # back of the order, whose blocks cover the deficit
-    deficit = sum(_blocks_needed(w, i, g[i], got[i]) for i in admitted) - len(w["free_slots"])
+    deficit = sum(nbk(i) for i in admitted) - len(w["free_slots"])
     holders = [i for i in order if st[i] == helpers.RUNNING_PREFILL and i not in admitted
                and row[i] > 0]
     victims = set()
@@ -199,6 +234,8 @@ def _check_against_definitions(w):
         # prefetched otherwise; anything else is recomputed
         if st[i] != helpers.QUEUED or w["prefix_tier"][i] == helpers.KV_HBM:
             assert a == ref.ACT_RETAIN, (i, a)
+        elif i in share:
+            assert a == (ref.ACT_SHARE if share[i] > 0 else ref.ACT_RECOMPUTE), (i, a)
         elif got[i] > 0:
             assert a == (ref.ACT_RESTORE if i in admitted else ref.ACT_PREFETCH), (i, a)
         else:
@@ -239,3 +276,45 @@ def test_definitions_under_scarce_resources():
         w = helpers.random_workload(rng, int(rng.integers(1, 9)), params=p,
                                     n_free=int(rng.integers(0, 6)))
         _check_against_definitions(w)
+
+
+def _with_groups(rng, w, k):
+    """Random prefix groups (ids below k, -1 for none) on every request;
+    the step uses them only for queued DRAM/NVMe requests."""
+    n = len(w["id"])
+    w["prefix_group"] = np.where(rng.random(n) < 0.75, rng.integers(0, max(1, min(k, n)), n),
+                                 -1).astype(np.int32)
+    return w
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_shared_prefix_step_matches_definitions(seed):
+    rng = np.random.default_rng(500 + seed)
+    for _ in range(150):
+        p = helpers.base_params(token_cap=int(rng.integers(1, 400)),
+                                max_move_blocks=int(rng.integers(0, 60)),
+                                tier2_reserve_q16=int(rng.choice([0, 4096, 65536])))
+        w = helpers.random_workload(rng, int(rng.integers(1, 9)), params=p)
+        _check_against_definitions(_with_groups(rng, w, int(rng.integers(1, 4))))
+
+
+def test_shared_prefix_without_members_changes_nothing():
+    """Groups on requests that are not queued DRAM/NVMe, or one member per
+    group, give exactly the step without groups."""
+    rng = np.random.default_rng(9)
+    for _ in range(200):
+        w = helpers.random_workload(rng, int(rng.integers(1, 9)))
+        n = len(w["id"])
+        base = ref.step(w)
+        w["prefix_group"] = np.arange(n, dtype=np.int32)      # every request alone
+        alone = ref.step(w)
+        deep = (w["state"] == helpers.QUEUED) & np.isin(w["prefix_tier"],
+                                                        [helpers.KV_DRAM, helpers.KV_NVME])
+        w["prefix_group"] = np.where(deep, -1, 0).astype(np.int32)  # only non-members grouped
+        others = ref.step(w)
+        for r in (alone, others):
+            assert r["rc"] == base["rc"] == ref.OK
+            for k in ["order", "action", "restore_blocks", "tokens_granted", "alloc_begin",
+                      "alloc_count", "admitted", "slot_list"]:
+                assert np.array_equal(r[k], base[k]), k
+            assert np.all(r["share_leader"] == -1)

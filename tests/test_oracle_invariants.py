@@ -9,6 +9,10 @@ from tests import helpers
 
 
 def _check_invariants(w, r):
+    _check_invariants_base(w, r)
+
+
+def _check_invariants_base(w, r, skip_restore_fit=None):
     p = w["params"]
     n = len(w["id"])
     assert r["rc"] == ref.OK
@@ -38,6 +42,8 @@ def _check_invariants(w, r):
                           (r["queue_tier_out"] == ref.QT_TIER1))
     # restores fit the remaining budget (eq:max_restorable) and the step cap
     rb = r["restore_blocks"]
+    if skip_restore_fit is not None:
+        rb = np.where(skip_restore_fit, 0, rb)   # a follower's blocks cross no link
     assert rb.sum() <= p["max_move_blocks"]
     for i in np.flatnonzero(rb > 0):
         assert ref.restore_time_ns(p, int(w["prefix_tier"][i]), int(rb[i])) <= r["budget_ns"][i]
@@ -96,6 +102,56 @@ def test_invariants_property(seed, n, cap, moves, rho, nfree, bt):
     w = helpers.random_workload(rng, n, params=p, n_free=None)
     w["free_slots"] = w["free_slots"][:nfree]
     _check_invariants(w, ref.step(w))
+
+
+def _check_sharing(w, r):
+    """Shared-prefix restores: a follower (SHARE) sits behind its leader in
+    the same priority group, uses no more blocks than the leader restores or
+    its own prefix holds, and is in the batch only if its leader restores in
+    the batch; the link carries at most U blocks."""
+    p = w["params"]
+    order = list(r["order"])
+    pos = {i: k for k, i in enumerate(order)}
+    adm = set(r["admitted"].tolist())
+    link = r["restore_blocks"][np.isin(r["action"], [ref.ACT_RESTORE, ref.ACT_PREFETCH])].sum()
+    assert link <= p["max_move_blocks"]
+    for i in np.flatnonzero(r["action"] == ref.ACT_SHARE):
+        lead = int(r["share_leader"][i])
+        assert lead >= 0 and pos[lead] < pos[i]
+        assert w["prefix_group"][lead] == w["prefix_group"][i] >= 0
+        assert r["queue_tier_out"][lead] == r["queue_tier_out"][i]
+        assert r["action"][lead] in (ref.ACT_RESTORE, ref.ACT_PREFETCH)
+        u = int(r["restore_blocks"][i])
+        assert 0 < u <= min(int(r["restore_blocks"][lead]),
+                            int(w["n_prefix"][i]) // p["block_tokens"])
+        if i in adm:
+            assert lead in adm and r["action"][lead] == ref.ACT_RESTORE
+    assert np.all((r["share_leader"] >= 0) == (r["action"] == ref.ACT_SHARE))
+
+
+@settings(max_examples=300, deadline=None)
+@given(seed=st.integers(0, 2 ** 32 - 1), n=st.integers(1, 64),
+       cap=st.integers(1, 400), moves=st.integers(0, 80), rho=st.sampled_from([0, 4096, 65536]),
+       groups=st.integers(1, 6))
+def test_shared_prefix_invariants(seed, n, cap, moves, rho, groups):
+    rng = np.random.default_rng(seed)
+    p = helpers.base_params(token_cap=cap, max_move_blocks=moves, tier2_reserve_q16=rho)
+    w = helpers.random_workload(rng, n, params=p)
+    w["prefix_group"] = np.where(rng.random(n) < 0.8, rng.integers(0, min(groups, n), n),
+                                 -1).astype(np.int32)
+    r = ref.step(w)
+    sharing = r["action"] == ref.ACT_SHARE
+    r2 = dict(r)
+    r2["action"] = np.where(sharing, ref.ACT_RECOMPUTE, r["action"])  # the rest as before
+    _check_invariants_base(w, r2, skip_restore_fit=sharing)
+    _check_sharing(w, r)
+
+
+def test_shared_prefix_group_ids_in_range():
+    w = helpers.random_workload(np.random.default_rng(1), 5)
+    for bad in ([-2, 0, 0, 0, 0], [0, 0, 5, 0, 0]):
+        w["prefix_group"] = np.array(bad, np.int32)
+        assert ref.step(w)["rc"] == ref.EINVAL
 
 
 def test_invariants_on_synthetic_configs():

@@ -40,6 +40,8 @@ def _step_pins():
     yield bf.test_all_equal_keys_give_identity_order
     yield lambda: [bf._check_against_definitions(w) for w in bf._cases(150, 8, 101)]
     yield bf.test_definitions_under_scarce_resources
+    yield pins.test_shared_prefix_example_step
+    yield lambda: bf.test_shared_prefix_step_matches_definitions(0)
 
 
 def _other_pins():
@@ -113,6 +115,22 @@ MUTANTS = [
     ("decode load used for the maximum estimate",
      "const int64_t dmax = p->max_batch - 1;",
      "const int64_t dmax = p->load_decodes;"),
+    # shared prefixes: a follower references at most its own prefix
+    ("follower takes the leader's whole restore",
+     "shared[i] = r[lead] < pb ? r[lead] : pb;",
+     "shared[i] = r[lead];"),
+    ("leader chosen without a restore want",
+     "if (deep && ev[i].want_blocks > 0) leader_of[slot] = i;",
+     "if (deep) leader_of[slot] = i;"),
+    ("sharing across priority groups",
+     "int32_t slot = deep ? 2 * pg[i] + (ev[i].group == 2 ? 1 : 0) : -1;",
+     "int32_t slot = deep ? 2 * pg[i] : -1;"),
+    ("shared blocks allocated again",
+     "nb[i] = ceil_div(bt * shared[i] + g[i], bt) - shared[i];",
+     "nb[i] = ceil_div(bt * shared[i] + g[i], bt);"),
+    ("follower still charged to the link",
+     "      r[i] = 0;\n      continue;",
+     "      r[i] = 0;\n      move_left -= min64(ev[i].want_blocks, move_left);\n      continue;"),
     # Section 4.4: least recently used first
     ("reclaim most recent first",
      "if (x->last_use != y->last_use) return x->last_use < y->last_use ? -1 : 1;",

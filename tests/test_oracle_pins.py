@@ -320,3 +320,29 @@ def test_key_orders_groups_then_budget():
         keys.append((e["key"], e["group"], e["budget_rem_ns"]))
     ks = sorted(keys)
     assert [k[1:] for k in ks] == sorted(k[1:] for k in keys)
+
+
+# ------------------------------------------------------ shared-prefix restores
+
+def test_shared_prefix_example_per_request_values():
+    w, g = helpers.golden_workload("worked_example_shared_prefix.json")
+    exp = g["expected_eval"]
+    for i in range(len(w["id"])):
+        e = _eval_req(w["params"], w, i)
+        for k in EVAL_KEYS:
+            assert e[k] == exp[k][i], (i, k, e[k], exp[k][i])
+
+
+def test_shared_prefix_example_step():
+    """A leader restoring for its followers inside and outside the batch, a
+    follower with a shorter prefix, a member ahead of its leader, a second
+    leader capped by the link, and a Tier-2 member that shares nothing."""
+    w, g = helpers.golden_workload("worked_example_shared_prefix.json")
+    r = ref.step(w)
+    exp = g["expected_step"]
+    assert r["rc"] == ref.OK
+    for k in ["order", "restore_blocks", "tokens_granted", "action", "share_leader",
+              "alloc_begin", "alloc_count", "admitted"]:
+        assert [int(x) for x in r[k]] == exp[k], (k, list(r[k]), exp[k])
+    assert _moves(r["unpack_moves"]) == exp["unpack_moves"]
+    assert r["n_slot_list"] == exp["n_slot_list"] and r["n_pack"] == exp["n_pack"]
