@@ -69,6 +69,8 @@ extern "C" {
 #define CASCADE_ACT_RECOMPUTE 4       /* recompute the prefix on the GPU */
 #define CASCADE_ACT_PREEMPT_OFFLOAD 5 /* preempted, blocks spilled to DRAM */
 #define CASCADE_ACT_PREEMPT_DROP 6    /* preempted, blocks dropped */
+#define CASCADE_ACT_SHARE 7           /* references the prefix blocks another request
+                                         of its prefix group restores this step */
 
 /* Indices into the device info array of cascade_outputs_t. */
 #define CASCADE_INFO_STATUS 0
@@ -91,13 +93,29 @@ extern "C" {
      n_prefix    matched prefix tokens, multiple of block_tokens, <= n_in - 1;
                  for a queued request 0 exactly when prefix_tier is NONE
      n_progress  QUEUED: 0; RUNNING_PREFILL: prompt tokens computed
-                 (1 .. n_in-1); DECODE: tokens generated (0 .. 2^17) */
+                 (1 .. n_in-1); DECODE: tokens generated (0 .. 2^17)
+     prefix_group optional (NULL = none): -1, or an id in [0, n) shared by
+                 requests whose matched prefixes begin with the same blocks
+                 (e.g. one shared system prompt or document).  Within a step,
+                 a prefix in DRAM or NVMe is then restored once per group and
+                 priority group (Section 4.4 prefix hit detection; the
+                 paper leaves within-step sharing open): the first queued
+                 DRAM/NVMe member in priority order with a positive restore
+                 want restores it as usual, and every later such member of
+                 the same group and priority group (decodes with Tier-1, or
+                 Tier-2) takes nothing from the link cap and references the
+                 first min(leader's restore blocks, own prefix blocks) blocks
+                 of that restore like an HBM prefix: action
+                 CASCADE_ACT_SHARE, restore_blocks = those blocks,
+                 share_leader = the leader (a plain RECOMPUTE when that is 0
+                 blocks).  Other requests ignore their group. */
 typedef struct {
   int32_t n; /* 0 .. 2^20 */
   const uint64_t *id;
   const uint8_t *slo_class, *state, *queue_tier, *prefix_tier;
   const int64_t *arrival_ns;
   const int32_t *n_in, *n_out_pred, *n_prefix, *n_progress;
+  const int32_t *prefix_group;
 } cascade_requests_t;
 
 /* Paged KV block table (CSR): request i holds HBM pool slots
@@ -157,7 +175,8 @@ typedef struct { int32_t req, blk, pool_slot, staging_slot; } cascade_move_t;
      tokens_granted  prompt / decode tokens scheduled this step (0 if not
                      admitted)
      restore_blocks  prefix blocks restored (RESTORE) or prefetched
-                     (PREFETCH), 0 otherwise
+                     (PREFETCH), or taken from another request's restore
+                     (SHARE), 0 otherwise
      order           request index at each priority position
      alloc_begin     first slot_list index of the request's new HBM blocks,
                      -1 if not admitted; its first restore_blocks entries
@@ -179,7 +198,14 @@ typedef struct { int32_t req, blk, pool_slot, staging_slot; } cascade_move_t;
                      meaningful when the step ends with status CASCADE_OK.
      info            device int32[CASCADE_INFO_LEN]: status and counts.  The
                      counts are the required sizes even when a list did not
-                     fit its capacity (status CASCADE_ENOSPC). */
+                     fit its capacity (status CASCADE_ENOSPC).
+     share_leader    with a prefix_group input (required then, else not
+                     written): the request whose restore a SHARE request
+                     references, -1 for every other request.  The shared
+                     blocks are the first restore_blocks entries of the
+                     leader's allocation (alloc_begin) when both are in the
+                     batch; a SHARE request outside the batch waits on its
+                     leader's prefetch. */
 typedef struct {
   int64_t *budget_ns;
   uint8_t *action, *queue_tier_out;
@@ -189,6 +215,7 @@ typedef struct {
   int32_t slot_list_capacity, unpack_capacity, pack_capacity;
   int32_t *info;
   int32_t *unpack_hazard, *pack_hazard;
+  int32_t *share_leader;
 } cascade_outputs_t;
 
 /* Paged KV pool: chunk (slot, layer l, kv in {0: K, 1: V}) of chunk_bytes
@@ -211,8 +238,9 @@ size_t cascade_step_workspace_bytes(int32_t n);
 /* One scheduling step (Algorithm 1, Phase 2 over the whole queue, with the
    estimator and budget engine of Section 4.2 and the preemption of Section
    4.4).  Returns CASCADE_OK once enqueued, CASCADE_EINVAL for NULL pointers
-   (or exactly one hazard array), parameters out of domain or negative
-   capacities, CASCADE_ENOSPC when
+   (or exactly one hazard array, or a prefix_group input without a
+   share_leader output), parameters out of domain or negative capacities,
+   CASCADE_ENOSPC when
    workspace_bytes < cascade_step_workspace_bytes(n), CASCADE_EHIP when a
    launch fails.  Request data, block-table and free-list errors set
    info[STATUS] = CASCADE_EINVAL; lists longer than their capacity set

@@ -18,7 +18,7 @@ QUEUED, RUNNING_PREFILL, DECODE = 0, 1, 2
 QT_NEW, QT_TIER1, QT_TIER2 = 0, 1, 2
 KV_HBM, KV_DRAM, KV_NVME, KV_NONE = 0, 1, 2, 3
 ACT_RETAIN, ACT_RESTORE, ACT_PREFETCH, ACT_RECOMPUTE = 1, 2, 3, 4
-ACT_PREEMPT_OFFLOAD, ACT_PREEMPT_DROP = 5, 6
+ACT_PREEMPT_OFFLOAD, ACT_PREEMPT_DROP, ACT_SHARE = 5, 6, 7
 INFO_STATUS, INFO_N_ADMITTED, INFO_N_SLOT_LIST, INFO_N_UNPACK, INFO_N_PACK = 0, 1, 2, 3, 4
 INFO_LEN = 8
 
@@ -45,7 +45,8 @@ class Requests(C.Structure):
     _fields_ = [("n", C.c_int32), ("id", C.c_void_p), ("slo_class", C.c_void_p),
                 ("state", C.c_void_p), ("queue_tier", C.c_void_p), ("prefix_tier", C.c_void_p),
                 ("arrival_ns", C.c_void_p), ("n_in", C.c_void_p), ("n_out_pred", C.c_void_p),
-                ("n_prefix", C.c_void_p), ("n_progress", C.c_void_p)]
+                ("n_prefix", C.c_void_p), ("n_progress", C.c_void_p),
+                ("prefix_group", C.c_void_p)]
 
 
 class BlockTable(C.Structure):
@@ -83,6 +84,7 @@ class Outputs(C.Structure):
         ("slot_list_capacity", C.c_int32), ("unpack_capacity", C.c_int32),
         ("pack_capacity", C.c_int32), ("info", C.c_void_p),
         ("unpack_hazard", C.c_void_p), ("pack_hazard", C.c_void_p),
+        ("share_leader", C.c_void_p),
     ]
 
 

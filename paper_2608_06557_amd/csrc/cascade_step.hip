@@ -77,13 +77,21 @@ constexpr int kL2Stride = 16;    // level-2 look-back words: one 128-byte line p
 //     entry of its block-table row instead
 //   y base_need, z reuse_tokens (HBM prefix or progress)
 //   w bits 0..19 held blocks, 20..21 state, 22..23 prefix tier,
-//     24..25 group, 26 spill-fits-budget, 27 decode needs a new block
+//     24..25 group, 26 spill-fits-budget, 27 decode needs a new block,
+//     28 a queued DRAM/NVMe member of a prefix group (then z is the group and
+//     bits 0..19 its prefix blocks), 29 a follower of that group's leader
+//     (rewritten by share_kernel: x the leader's request index, y the need
+//     net of the shared blocks, z the shared tokens, prefix tier HBM, so
+//     the scan references the shared blocks as it does an HBM prefix)
 __device__ __forceinline__ int rec_held(int w) { return w & 0xFFFFF; }
 __device__ __forceinline__ int rec_state(int w) { return (w >> 20) & 3; }
+__device__ __forceinline__ int rec_member(int w) { return (w >> 28) & 1; }
+__device__ __forceinline__ int rec_follow(int w) { return (w >> 29) & 1; }
 __device__ __forceinline__ int rec_want(const int4 &r) {
-  return rec_state(r.w) == CASCADE_RUNNING_PREFILL ? 0 : r.x;
+  return (rec_state(r.w) == CASCADE_RUNNING_PREFILL || rec_follow(r.w)) ? 0 : r.x;
 }
 __device__ __forceinline__ int rec_tier(int w) { return (w >> 22) & 3; }
+__device__ __forceinline__ int rec_grp(int w) { return (w >> 24) & 3; }
 __device__ __forceinline__ int rec_offl(int w) { return (w >> 26) & 1; }
 __device__ __forceinline__ int rec_decnb(int w) { return (w >> 27) & 1; }
 
@@ -114,6 +122,7 @@ constexpr int kRestoreCap = 1024; // restore-list entries staged in LDS for the 
 struct Ctl {
   unsigned long long bmin, bmax;  // totals, written by prep's workgroup 0
   long long held_rp, need1, want1;
+  long long want1_sub, need1_sub; // followers' wants and shared tokens in groups 0-1
   unsigned cnt[4];
   unsigned nact;                  // data-moving radix passes, from the sort plan
   int n_rp;                       // running prefills in the queue (last scan tile)
@@ -143,6 +152,7 @@ struct Consts {                   // parameters the kernels use, flattened
 
 struct Outs {                     // output pointers the scan writes
   int *order, *granted, *restore, *alloc_begin, *alloc_count, *admitted, *slot_list;
+  int *share_leader;                 // null without prefix groups
   uint8_t *action;
   cascade_move_t *unpack, *pack;
   int *unpack_hazard, *pack_hazard;  // may be null
@@ -213,7 +223,7 @@ struct ReqEval {
 
 __device__ __forceinline__ ReqEval eval_request(const cascade_requests_t &rq,
                                                 const int *__restrict__ ro, const Consts &c,
-                                                const long long *s_slo, int i) {
+                                                const long long *s_slo, int i, int n) {
   ReqEval r;
   r.bad = false;
   const unsigned cls = rq.slo_class[i], st = rq.state[i], qt = rq.queue_tier[i],
@@ -343,15 +353,25 @@ __device__ __forceinline__ ReqEval eval_request(const cascade_requests_t &rq,
   const bool hbm_prefix = st_s == CASCADE_QUEUED && pt_s == CASCADE_KV_HBM;
   const long long reuse_tok =
       (st_s == CASCADE_RUNNING_PREFILL) ? prog : (hbm_prefix ? n_pre : 0);
+  // prefix group: ids in [-1, n); a queued DRAM/NVMe request in a group is
+  // a member (its group in z, its prefix blocks in the held bits, which a
+  // queued request does not use)
+  int gid = -1;
+  if (rq.prefix_group) {
+    const int g = rq.prefix_group[i];
+    if (g < -1 || g >= n) r.bad = true;
+    else gid = g;
+  }
+  const bool member = gid >= 0 && st_s == CASCADE_QUEUED && deep;
 
   r.brem = brem;
   r.tnew = tnew;
   r.grp = grp;
   r.biased = biased;
   r.rec = make_int4(st_s == CASCADE_RUNNING_PREFILL ? r0 : (int)want, (int)base_need,
-                    (int)reuse_tok,
-                    (int)held | ((int)st_s << 20) | ((int)pt_s << 22) | (grp << 24) |
-                        (offl << 26) | (decnb << 27));
+                    member ? gid : (int)reuse_tok,
+                    (member ? (int)pb : (int)held) | ((int)st_s << 20) | ((int)pt_s << 22) |
+                        (grp << 24) | (offl << 26) | (decnb << 27) | ((int)member << 28));
   r.held = st_s == CASCADE_RUNNING_PREFILL ? held : 0;
   r.need1 = grp <= 1 ? base_need : 0;
   r.want1 = grp <= 1 ? want : 0;
@@ -360,7 +380,8 @@ __device__ __forceinline__ ReqEval eval_request(const cascade_requests_t &rq,
 
 __global__ __launch_bounds__(kBlock) void eval_kernel(
     cascade_requests_t rq, const int *__restrict__ ro, const int *__restrict__ free_slots,
-    Consts c, int n, Ctl *ctl, uint4 *clear, size_t clear_vec, int *info,
+    Consts c, int n, Ctl *ctl, uint4 *clear, size_t clear_vec, uint4 *clear2,
+    size_t clear2_vec, int *info,
     Partial *__restrict__ partials, int64_t *__restrict__ budget_out,
     uint8_t *__restrict__ tier_out, unsigned long long *__restrict__ keys,
     int4 *__restrict__ rec) {
@@ -374,6 +395,8 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
   // this step's histograms and look-back status words start at zero; the
   // first workgroup resets the control block's header and the info words
   for (size_t j = gt; j < clear_vec; j += gs) clear[j] = make_uint4(0, 0, 0, 0);
+  // the shared-prefix tables (leader positions, published leader restores)
+  for (size_t j = gt; j < clear2_vec; j += gs) clear2[j] = make_uint4(0, 0, 0, 0);
   if (blockIdx.x == 0) {
     const int t = threadIdx.x;
     constexpr int kKstarWord = offsetof(Ctl, kstar) / 4;
@@ -397,7 +420,7 @@ __global__ __launch_bounds__(kBlock) void eval_kernel(
   for (int it = 0; it < kEvalItems; ++it) {
     const int i = (int)(blockIdx.x * kBlock * kEvalItems + it * kBlock + threadIdx.x);
     if (i >= n) continue;
-    const ReqEval r = eval_request(rq, ro, c, s_slo, i);
+    const ReqEval r = eval_request(rq, ro, c, s_slo, i, n);
     bad |= r.bad;
     bmin = r.biased < bmin ? r.biased : bmin;
     bmax = r.biased > bmax ? r.biased : bmax;
@@ -1347,6 +1370,7 @@ struct TileOut {
   int granted[kScanItems], restore[kScanItems], alloc_begin[kScanItems], alloc_count[kScanItems];
   int admitted_at[kScanItems];  // index in the admitted list, -1: not admitted
   int action[kScanItems];       // -1: a running prefill (stored before the hand-over)
+  int share[kScanItems];        // share_leader output
   int p0;
 };
 
@@ -1362,6 +1386,7 @@ __device__ __forceinline__ void write_tile_outputs(const TileOut &out, const Out
     o.alloc_count[i] = out.alloc_count[j];
     if (out.action[j] >= 0) o.action[i] = (uint8_t)out.action[j];
     if (out.admitted_at[j] >= 0) o.admitted[out.admitted_at[j]] = i;
+    if (o.share_leader) o.share_leader[i] = out.share[j];
   }
 }
 
@@ -1377,7 +1402,8 @@ __device__ __forceinline__ ScanConsts scan_consts(const Consts &c, const Ctl *ct
   const bool has2 = ctl->cnt[2] != 0;
   k.cap = c.token_cap;
   k.cap1 = k.cap - (has2 ? ((k.cap * c.rho_q16) >> 16) : 0);
-  k.p_e1 = ctl->need1 - k.bt * lmin(ctl->want1, k.U);  // tokens before Tier-2
+  // tokens before Tier-2 (followers want nothing and need less)
+  k.p_e1 = (ctl->need1 - ctl->need1_sub) - k.bt * lmin(ctl->want1 - ctl->want1_sub, k.U);
   k.g1 = lmin(k.p_e1, k.cap1);                          // granted to decode+Tier-1
   k.fh = (long long)c.n_free + ctl->held_rp;            // F + H
   return k;
@@ -1619,14 +1645,19 @@ __device__ __forceinline__ long long scan_tile(int tile, int jn, const ScanConst
       store_agent(&ctl->kz, Z);
       store_agent(&ctl->kzp, zp_inc[j] - (rec_offl(w) ? hh[j] : 0));
     }
+    const bool follow = st == CASCADE_QUEUED && rec_follow(w);
+    const int shared = follow ? (int)((unsigned)r4[j].z / (unsigned)K.bt) : 0;
     out.granted[j] = adm ? (int)g[j] : 0;
-    out.restore[j] = (int)r[j];
+    out.restore[j] = follow ? shared : (int)r[j];
+    out.share[j] = (follow && shared > 0) ? r4[j].x : -1;
     out.alloc_begin[j] = adm ? (int)NB : -1;
     out.alloc_count[j] = adm ? (int)nb[j] : 0;
     out.admitted_at[j] = adm ? (int)AC : -1;
     int act;
     if (st != CASCADE_QUEUED) {
       act = CASCADE_ACT_RETAIN;  // a preempted running prefill is rewritten later
+    } else if (follow) {
+      act = shared > 0 ? CASCADE_ACT_SHARE : CASCADE_ACT_RECOMPUTE;
     } else {
       const int tier = rec_tier(w);
       if (tier == CASCADE_KV_HBM) act = CASCADE_ACT_RETAIN;
@@ -1992,7 +2023,8 @@ __device__ __forceinline__ void finish_grid(int g, int G, int n, int n_free, int
 // them, so nothing is polled.  The step's status word rides along in the
 // same reduction: the return value says whether an earlier kernel reported
 // a failure, the same in every thread.
-__device__ __forceinline__ bool earlier_totals(const unsigned *__restrict__ l1, int tile,
+__device__ __forceinline__ bool earlier_totals(const unsigned *__restrict__ l1,
+                                               const unsigned *__restrict__ adj, int tile,
                                                int n_tiles, const int *info,
                                                long long (&pre1)[kL1], long long &rp_total,
                                                long long *s_red) {
@@ -2011,11 +2043,25 @@ __device__ __forceinline__ bool earlier_totals(const unsigned *__restrict__ l1, 
 #pragma unroll
       for (int k = 0; k < kL1; ++k) w1[u][k] = l1[(size_t)jc * kL1 + k];
     }
+    // shared prefixes: the followers' wants and shared tokens, taken off
+    // the earlier tiles' want and need totals
+    unsigned a1[kPer][2] = {{0, 0}, {0, 0}};
+    if (adj) {
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int j = b0 + u * kBlock + (int)threadIdx.x;
+        const int jc = j < n_tiles ? j : 0;
+        a1[u][0] = adj[(size_t)jc * 2];
+        a1[u][1] = adj[(size_t)jc * 2 + 1];
+      }
+    }
 #pragma unroll
     for (int u = 0; u < kPer; ++u) {
       const int j = b0 + u * kBlock + (int)threadIdx.x;
 #pragma unroll
       for (int k = 0; k < kL1; ++k) v[k] += j < tile ? (long long)w1[u][k] : 0ll;
+      v[0] -= j < tile ? (long long)a1[u][0] : 0ll;
+      v[1] -= j < tile ? (long long)a1[u][1] : 0ll;
       v[kL1] += j < n_tiles ? (long long)w1[u][4] : 0ll;
     }
   }
@@ -2074,6 +2120,188 @@ __device__ __forceinline__ void load_sorted(int n, const Sorted &srt, unsigned (
   }
 }
 
+// ------------------------------------------------------ shared prefixes
+
+// Shared-prefix restores within a step (Section 4.4 prefix hit detection;
+// the paper leaves within-step sharing open, reading: within a priority
+// group, the first queued DRAM/NVMe member of a prefix group with a restore
+// want leads and restores under the link cap; every later such member of
+// the group follows and references min(leader's restore, own prefix) blocks
+// of it, taking nothing from the cap).  Three launches between the sort and
+// the scan, each over the scan tiles' positions: the leaders' positions
+// (share_lead_kernel), the followers' wants taken off each tile's level-1
+// want total (share_drop_kernel), then the leaders' restores and the
+// followers' rewritten records (share_kernel).  The table of leaders holds
+// n - position (0: none yet), so the maximum is the first position.
+
+// The request index and scan record at position p: the sorted buffers, or
+// the identity order when no radix pass moved data.
+__device__ __forceinline__ void position_rec(int p, int nact, const Sorted &srt,
+                                             const int4 *__restrict__ rec, int &ix, int4 &r) {
+  if (nact == 0) {
+    ix = p;
+    r = rec[p];
+  } else {
+    ix = (int)srt.order[p];
+    r = srt.rec[p];
+  }
+}
+// Slot of a member's (prefix group, priority group) in the leader tables.
+__device__ __forceinline__ int share_slot(const int4 &r) {
+  return 2 * r.z + (rec_grp(r.w) == 2 ? 1 : 0);
+}
+
+__global__ __launch_bounds__(kBlock) void share_lead_kernel(int n, const Ctl *ctl,
+                                                            const int *info, Sorted srt,
+                                                            const int4 *__restrict__ rec,
+                                                            unsigned *lead) {
+  if (bad_status(load_agent(info))) return;
+  const int nact = (int)ctl->nact;
+  const int p0 = (int)blockIdx.x * kScanTile + (int)threadIdx.x * kScanItems;
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    const int p = p0 + j;
+    if (p >= n) break;
+    int ix;
+    int4 r;
+    position_rec(p, nact, srt, rec, ix, r);
+    if (rec_member(r.w) && r.x > 0 && (unsigned)r.z < (unsigned)n)
+      atomicMax(lead + share_slot(r), (unsigned)(n - p));
+  }
+}
+
+// Is position p's member a follower (behind its group's leader)?
+__device__ __forceinline__ bool share_follows(const int4 &r, int p, int n,
+                                              const unsigned *lead, unsigned *enc_out) {
+  if (!rec_member(r.w) || (unsigned)r.z >= (unsigned)n) return false;
+  const unsigned enc = lead[share_slot(r)];
+  *enc_out = enc;
+  return enc != 0 && p > n - (int)enc;
+}
+
+__global__ __launch_bounds__(kBlock) void share_drop_kernel(int n, Ctl *ctl, const int *info,
+                                                            Sorted srt,
+                                                            const int4 *__restrict__ rec,
+                                                            const unsigned *__restrict__ lead,
+                                                            unsigned *adj) {
+  __shared__ long long s_red[kWaves * 2];
+  if (bad_status(load_agent(info))) return;
+  const int nact = (int)ctl->nact;
+  const int tile = (int)blockIdx.x;
+  const int p0 = tile * kScanTile + (int)threadIdx.x * kScanItems;
+  long long v[2] = {0, 0};  // the tile's followers' wants, those in groups 0-1
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    const int p = p0 + j;
+    if (p >= n) break;
+    int ix;
+    int4 r;
+    position_rec(p, nact, srt, rec, ix, r);
+    unsigned enc = 0;
+    if (share_follows(r, p, n, lead, &enc)) {
+      v[0] += r.x;
+      v[1] += rec_grp(r.w) <= 1 ? r.x : 0;
+    }
+  }
+  block_sum<2>(v, s_red);
+  if (threadIdx.x == 0) {
+    adj[(size_t)tile * 2] = (unsigned)v[0];   // below 2^31: 1024 wants below 2^18
+    if (v[1]) atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->want1_sub),
+                        (unsigned long long)v[1]);
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void share_kernel(int n, int n_tiles, int bt, int max_move,
+                                                       Ctl *ctl, int *info, Sorted srt,
+                                                       int4 *__restrict__ rec,
+                                                       const unsigned *__restrict__ l1_tot,
+                                                       const unsigned *__restrict__ lead,
+                                                       unsigned *rl, unsigned *adj) {
+  __shared__ long long s_red[kWaves * 3];
+  __shared__ unsigned s_scan[kWaves];
+  if (bad_status(load_agent(info))) return;
+  const int nact = (int)ctl->nact;
+  const int tile = (int)blockIdx.x;
+  const int p0 = tile * kScanTile + (int)threadIdx.x * kScanItems;
+  int ix[kScanItems];
+  int4 r4[kScanItems];
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    ix[j] = -1;
+    r4[j] = make_int4(0, 0, 0, 0);
+    if (p0 + j < n) position_rec(p0 + j, nact, srt, rec, ix[j], r4[j]);
+  }
+  // the link-cap prefix before this tile: the earlier tiles' want totals
+  // without their followers' wants
+  long long pre[1] = {0};
+  for (int k = (int)threadIdx.x; k < tile; k += kBlock)
+    pre[0] += (long long)l1_tot[(size_t)k * kL1] - (long long)adj[(size_t)k * 2];
+  block_sum<1>(pre, s_red);
+  // this tile's wants in position order (a follower wants nothing)
+  unsigned enc[kScanItems];
+  bool fol[kScanItems];
+  unsigned wsum[1] = {0}, wtot[1];
+  int wj[kScanItems];
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    enc[j] = 0;
+    fol[j] = ix[j] >= 0 && share_follows(r4[j], p0 + j, n, lead, &enc[j]);
+    wj[j] = (ix[j] >= 0 && !fol[j]) ? rec_want(r4[j]) : 0;
+    wsum[0] += (unsigned)wj[j];
+  }
+  block_exclusive_scan<1>(wsum, wtot, s_scan);
+  // leaders publish their restore blocks (eq:max_restorable under the cap)
+  long long wx = pre[0] + wsum[0];
+  const long long U = max_move;
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    const long long rj = lmin(wx + wj[j], U) - lmin(wx, U);
+    wx += wj[j];
+    if (ix[j] >= 0 && rec_member(r4[j].w) && enc[j] != 0 && p0 + j == n - (int)enc[j])
+      store_agent(rl + share_slot(r4[j]), 0x80000000u | (unsigned)rj);
+  }
+  __syncthreads();
+  // followers: wait for their leader's restore (a leader sits at a lower
+  // position, in this tile or an earlier one, which publishes before it
+  // waits on anything), then reference min(its blocks, own prefix blocks)
+  long long dn[3] = {0, 0, 0};  // shared tokens: all, groups 0-1, timeouts
+#pragma unroll
+  for (int j = 0; j < kScanItems; ++j) {
+    if (!fol[j]) continue;
+    const int4 r = r4[j];
+    unsigned v = load_agent(rl + share_slot(r));
+    unsigned spins = 0;
+    while ((v >> 31) == 0) {
+      if (++spins > kSpinLimit) break;
+      __builtin_amdgcn_s_sleep(1);
+      v = load_agent(rl + share_slot(r));
+    }
+    if ((v >> 31) == 0) {
+      dn[2] += 1;
+      continue;
+    }
+    const int pl = n - (int)enc[j];
+    const int lead_req = nact == 0 ? pl : (int)srt.order[pl];
+    const int u = min((int)(v & 0x7FFFFFFFu), rec_held(r.w));
+    int4 nr;
+    nr.x = u > 0 ? lead_req : -1;
+    nr.y = r.y - bt * u;
+    nr.z = bt * u;
+    nr.w = (r.w & ~(3 << 22)) | (CASCADE_KV_HBM << 22) | (1 << 29);
+    if (nact == 0) rec[p0 + j] = nr;
+    else srt.rec[p0 + j] = nr;
+    dn[0] += (long long)bt * u;
+    dn[1] += rec_grp(r.w) <= 1 ? (long long)bt * u : 0;
+  }
+  block_sum<3>(dn, s_red);
+  if (threadIdx.x == 0) {
+    adj[(size_t)tile * 2 + 1] = (unsigned)dn[0];  // below 2^31: 1024 needs below 2^18
+    if (dn[1]) atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->need1_sub),
+                         (unsigned long long)dn[1]);
+    if (dn[2]) set_status(info, CASCADE_ETIMEOUT);
+  }
+}
+
 // Algorithm 1's Phase 2 loop in priority order as prefix sums.
 // Level 1 (independent of earlier decisions): restore want, base token need,
 // blocks held by running prefills (all / spill-fits).  They give the restore
@@ -2092,7 +2320,8 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
     const int4 *__restrict__ rec, const int *__restrict__ slots,
     const int *__restrict__ free_slots, Outs o, RpInfo *__restrict__ rp_list,
     RestoreEnt *__restrict__ restore_list, TileTot *__restrict__ tile_tot,
-    const unsigned *__restrict__ l1_tot, unsigned long long *l2_status) {
+    const unsigned *__restrict__ l1_tot, const unsigned *__restrict__ share_adj,
+    unsigned long long *l2_status) {
   __shared__ ScanLds s_lds;
   __shared__ FinishAnyLds s_fin;
   __shared__ int s_bad;
@@ -2133,7 +2362,7 @@ __global__ __launch_bounds__(kBlock) void scan_kernel(
   load_sorted(n, srt, so, sr);
   const int nact = (int)ctl->nact;
   long long pre1[kL1], rp_total;
-  if (earlier_totals(l1_tot, tile, n_tiles, info, pre1, rp_total, s_lds.red)) {
+  if (earlier_totals(l1_tot, share_adj, tile, n_tiles, info, pre1, rp_total, s_lds.red)) {
     // a failed step: the look-back words say "nothing before me", so no later
     // tile waits, and the tile is counted, so the finishing workgroups stop
     if (t < kL2) publish<unsigned long long>(l2_status + (size_t)tile * kL2Stride + t, 0ull,
@@ -2306,7 +2535,7 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
   for (int j = 0; j < kSmallItems; ++j) {
     const int i = j * kBlock + t;
     if (i >= n) continue;
-    const ReqEval r = eval_request(rq, ro, c, s_slo, i);
+    const ReqEval r = eval_request(rq, ro, c, s_slo, i, n);
     bad |= r.bad;
     v[7] = r.biased < v[7] ? r.biased : v[7];
     v[8] = r.biased > v[8] ? r.biased : v[8];
@@ -2519,6 +2748,73 @@ __global__ __launch_bounds__(kBlock) void step_small_kernel(
     idx[j] = (j < jn && p < n) ? (moved ? (int)U.sort.val[p] : p) : -1;
     r4[j] = idx[j] >= 0 ? U.sort.rec[idx[j]] : make_int4(0, 0, 0, 0);
   }
+  if (rq.prefix_group) {
+    // shared prefixes, the three stages of the multi-launch path in one
+    // workgroup; the finished sort's keys and records (every position's
+    // record is in registers now) hold the two tables
+    __syncthreads();
+    unsigned *lead = reinterpret_cast<unsigned *>(U.sort.key);
+    unsigned *rl = reinterpret_cast<unsigned *>(U.sort.rec);
+    static_assert(sizeof(U.sort.key) >= 2 * kSmallMax * sizeof(unsigned) &&
+                      sizeof(U.sort.rec) >= 2 * kSmallMax * sizeof(unsigned),
+                  "two table entries per request");
+    for (int k = t; k < 2 * n; k += kBlock) {
+      lead[k] = 0;
+      rl[k] = 0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+      const int p = t * jn + j;
+      if (idx[j] >= 0 && rec_member(r4[j].w) && r4[j].x > 0 && (unsigned)r4[j].z < (unsigned)n)
+        atomicMax(lead + share_slot(r4[j]), (unsigned)(n - p));
+    }
+    __syncthreads();
+    unsigned enc[kScanItems];
+    bool fol[kScanItems];
+    int wj[kScanItems];
+    unsigned ws[1] = {0}, wt[1];
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+      enc[j] = 0;
+      fol[j] = idx[j] >= 0 && share_follows(r4[j], t * jn + j, n, lead, &enc[j]);
+      wj[j] = (idx[j] >= 0 && !fol[j]) ? rec_want(r4[j]) : 0;
+      ws[0] += (unsigned)wj[j];
+    }
+    block_exclusive_scan<1>(ws, wt, reinterpret_cast<unsigned *>(s_scan1));
+    long long wx = ws[0];
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+      const long long rj = lmin(wx + wj[j], (long long)c.max_move) - lmin(wx, (long long)c.max_move);
+      wx += wj[j];
+      if (idx[j] >= 0 && rec_member(r4[j].w) && enc[j] != 0 && t * jn + j == n - (int)enc[j])
+        rl[share_slot(r4[j])] = 0x80000000u | (unsigned)rj;
+    }
+    __syncthreads();
+    long long dv[2] = {0, 0};  // groups 0-1: the followers' wants and shared tokens
+#pragma unroll
+    for (int j = 0; j < kScanItems; ++j) {
+      if (!fol[j]) continue;
+      const int4 r = r4[j];
+      const unsigned v = rl[share_slot(r)];
+      const int pl = n - (int)enc[j];
+      const int u = min((int)(v & 0x7FFFFFFFu), rec_held(r.w));
+      if (rec_grp(r.w) <= 1) {
+        dv[0] += r.x;
+        dv[1] += (long long)c.bt * u;
+      }
+      r4[j].x = u > 0 ? (moved ? (int)U.sort.val[pl] : pl) : -1;
+      r4[j].y = r.y - c.bt * u;
+      r4[j].z = c.bt * u;
+      r4[j].w = (r.w & ~(3 << 22)) | (CASCADE_KV_HBM << 22) | (1 << 29);
+    }
+    block_sum<2>(dv, reinterpret_cast<long long *>(s_red));
+    if (t == 0) {
+      ctl->want1 -= dv[0];
+      ctl->need1 -= dv[1];
+    }
+    __syncthreads();
+  }
   const ScanConsts K = scan_consts(c, ctl);
   TileOut out;
   const long long zero1[kL1] = {0, 0, 0, 0, 0};
@@ -2558,7 +2854,7 @@ __global__ __launch_bounds__(kBlock) void empty_step_kernel(int n_free, int num_
 struct Layout {
   size_t ctl = 0, scan1 = 0, scan2 = 0, sort_status = 0, partials = 0, keys_a = 0, keys_b = 0,
          vals_a = 0, vals_b = 0, rec = 0, s_order = 0, s_rec = 0, rp_list = 0, restore = 0,
-         tile_tot = 0, total = 0;
+         tile_tot = 0, share_lead = 0, share_rl = 0, share_adj = 0, total = 0;
   int sort_tiles = 0, scan_tiles = 0, eval_grid = 0;
 };
 
@@ -2589,6 +2885,12 @@ constexpr Layout make_layout(int32_t n) {
   L.rp_list = take(np * sizeof(RpInfo));
   L.restore = take(np * sizeof(RestoreEnt));
   L.tile_tot = take((size_t)L.scan_tiles * sizeof(TileTot));
+  // shared prefixes: leader positions and published leader restores per
+  // (group, priority group), contiguous for eval's clear; per scan tile the
+  // followers' wants and shared tokens
+  L.share_lead = take(np * 2 * 4);
+  L.share_rl = take(np * 2 * 4);
+  L.share_adj = take((size_t)L.scan_tiles * 2 * 4);
   L.total = off;
   return L;
 }
@@ -2712,6 +3014,7 @@ int step_impl(const cascade_requests_t *rq, const cascade_block_table_t *bt,
       (out->pack_capacity > 0 && !out->pack_moves))
     return CASCADE_EINVAL;
   if ((out->unpack_hazard == nullptr) != (out->pack_hazard == nullptr)) return CASCADE_EINVAL;
+  if (n > 0 && rq->prefix_group && !out->share_leader) return CASCADE_EINVAL;
   if (((uintptr_t)workspace & 255) != 0) return CASCADE_EINVAL;
   const Layout L = make_layout(n);
   if (workspace_bytes < L.total) return CASCADE_ENOSPC;
@@ -2754,6 +3057,7 @@ int step_impl(const cascade_requests_t *rq, const cascade_block_table_t *bt,
   o.pack = out->pack_moves;
   o.unpack_hazard = out->unpack_hazard;
   o.pack_hazard = out->pack_hazard;
+  o.share_leader = rq->prefix_group ? out->share_leader : nullptr;
   o.sl_cap = out->slot_list_capacity;
   o.unpack_cap = out->unpack_capacity;
   o.pack_cap = out->pack_capacity;
@@ -2806,10 +3110,17 @@ int step_impl(const cascade_requests_t *rq, const cascade_block_table_t *bt,
   const size_t clear_vec = (clear_end - clear_off) / 16;
   uint4 *clear = reinterpret_cast<uint4 *>(ws + clear_off);
   static_assert(offsetof(Ctl, hist) % 16 == 0, "16-byte clears");
+  const bool share = rq->prefix_group != nullptr;
+  auto *share_lead = reinterpret_cast<unsigned *>(ws + L.share_lead);
+  auto *share_rl = reinterpret_cast<unsigned *>(ws + L.share_rl);
+  auto *share_adj = reinterpret_cast<unsigned *>(ws + L.share_adj);
+  // both share tables (2n words each), one 16-byte clear region
+  const size_t clear2_vec = share ? (L.share_adj - L.share_lead) / 16 : 0;
 
   hipLaunchKernelGGL(eval_kernel, dim3(L.eval_grid), dim3(kBlock), 0, s, *rq, bt->row_offsets,
-                     ts->free_slots, c, n, ctl, clear, clear_vec, out->info, partials,
-                     out->budget_ns, out->queue_tier_out, keys_a, rec);
+                     ts->free_slots, c, n, ctl, clear, clear_vec,
+                     reinterpret_cast<uint4 *>(ws + L.share_lead), clear2_vec, out->info,
+                     partials, out->budget_ns, out->queue_tier_out, keys_a, rec);
   // a short queue spreads prep over more workgroups (its block-table checks
   // and histograms are per workgroup); a long one keeps the global adds few
   const int prep_items = n <= kTinyPrepMax ? 2 : kPrepItems;
@@ -2825,9 +3136,19 @@ int step_impl(const cascade_requests_t *rq, const cascade_block_table_t *bt,
                        passes, ctl, out->info, keys_a, keys_b, vals_a, vals_b,
                        sort_status + (size_t)pass * sort_tiles * kMaxBins, rec, srt,
                        l1_tot);
+  if (share) {
+    hipLaunchKernelGGL(share_lead_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, ctl,
+                       out->info, srt, rec, share_lead);
+    hipLaunchKernelGGL(share_drop_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, ctl,
+                       out->info, srt, rec, share_lead, share_adj);
+    hipLaunchKernelGGL(share_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, L.scan_tiles,
+                       c.bt, c.max_move, ctl, out->info, srt, rec, l1_tot, share_lead, share_rl,
+                       share_adj);
+  }
   hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles + kFinishGrid), dim3(kBlock), 0, s, n,
                      passes, L.scan_tiles, c, ctl, out->info, srt, rec, bt->slots,
-                     ts->free_slots, o, rp_list, rlist, tile_tot, l1_tot, l2_status);
+                     ts->free_slots, o, rp_list, rlist, tile_tot, l1_tot,
+                     share ? share_adj : nullptr, l2_status);
   if (hipGetLastError() != hipSuccess) return CASCADE_EHIP;
   return CASCADE_OK;
 }

@@ -55,6 +55,9 @@ class DeviceStep:
         self.slots = to_device(np.asarray(w["slots"]), self.device, np.int32)
         self.free = to_device(np.asarray(w["free_slots"]), self.device, np.int32)
         self.n_free = int(len(w["free_slots"]))
+        # shared-prefix restores: a prefix_group array in the workload
+        self.pg = (to_device(np.asarray(w["prefix_group"]), self.device, np.int32)
+                   if w.get("prefix_group") is not None else None)
         nb = self.num_blocks
         self.caps = (nb if slot_cap is None else slot_cap, nb if unpack_cap is None else unpack_cap,
                      nb if pack_cap is None else pack_cap)
@@ -71,11 +74,14 @@ class DeviceStep:
         self.unpack_hazard = z(self.caps[1], torch.int32)
         self.pack_hazard = z(self.caps[2], torch.int32)
         self.info = z(cx.INFO_LEN, torch.int32)
+        if self.pg is not None:
+            self.out["share_leader"] = z(nn, torch.int32)
         self.ws_bytes = cx.cascade_step_workspace_bytes(n)
         self.ws = torch.empty(self.ws_bytes + 256, dtype=torch.uint8, device=self.device)
         self.ws_ptr = (self.ws.data_ptr() + 255) & ~255
 
-        self.c_req = cx.Requests(n, *[self.inp[k].data_ptr() for k, _ in REQ_FIELDS])
+        self.c_req = cx.Requests(n, *[self.inp[k].data_ptr() for k, _ in REQ_FIELDS],
+                                 self.pg.data_ptr() if self.pg is not None else None)
         self.c_table = cx.BlockTable(self.ro.data_ptr(), self.slots.data_ptr())
         self.c_tier = cx.TierState(self.num_blocks, self.n_free, self.free.data_ptr())
         o = self.out
@@ -85,7 +91,8 @@ class DeviceStep:
             o["alloc_begin"].data_ptr(), o["alloc_count"].data_ptr(), o["admitted"].data_ptr(),
             self.slot_list.data_ptr(), self.unpack_moves.data_ptr(), self.pack_moves.data_ptr(),
             self.caps[0], self.caps[1], self.caps[2], self.info.data_ptr(),
-            self.unpack_hazard.data_ptr(), self.pack_hazard.data_ptr())
+            self.unpack_hazard.data_ptr(), self.pack_hazard.data_ptr(),
+            o["share_leader"].data_ptr() if self.pg is not None else None)
 
     def run(self, stream=None) -> int:
         """Enqueue one step; returns the host-side return code."""

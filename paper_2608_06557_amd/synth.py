@@ -144,11 +144,15 @@ def kv_geometry(model: str, num_blocks: int, layout: str = "layer_major",
     return g
 
 
-def make_workload(cfg: int, seed: int | None = None, n: int | None = None) -> dict:
+def make_workload(cfg: int, seed: int | None = None, n: int | None = None,
+                  prefix_groups: bool = False) -> dict:
     """Draw one synthetic scheduling-step input.
 
     Returns a dict of numpy arrays (request SoA, block table, free list) plus
-    ``params`` (integers), ``geometry`` and ``config``."""
+    ``params`` (integers), ``geometry`` and ``config``.  With
+    ``prefix_groups`` (workloads with shared prefixes), also a
+    ``prefix_group`` array: the shared prefix each request extends, -1 for
+    the others."""
     c = dict(CONFIGS[cfg])
     if n is not None:
         c["n"] = n
@@ -194,6 +198,7 @@ def make_workload(cfg: int, seed: int | None = None, n: int | None = None) -> di
     n_prefix = bt * np.floor(frac * n_in / bt).astype(np.int64)
     n_prefix = np.minimum(n_prefix, bt * ((n_in - 1) // bt))
     arrival_jitter = None
+    group = np.full(n, -1, np.int64)
 
     if c.get("shared_prefix"):
         # 30% of requests extend one of 512 shared prefixes of 1k..32k tokens;
@@ -217,6 +222,7 @@ def make_workload(cfg: int, seed: int | None = None, n: int | None = None) -> di
             slo_class[lead] = rng.choice(np.array(c["classes"][fam_kind]), len(lead))
         for col in range(4):
             members = fam_ids[:, col]
+            group[members] = which
             n_in[members] = pre_len[which] + n_in[lead]
             n_out[members] = n_out[lead]
             slo_class[members] = slo_class[lead]
@@ -286,8 +292,9 @@ def make_workload(cfg: int, seed: int | None = None, n: int | None = None) -> di
 
     ids = np.cumsum(rng.integers(1, 4, n)).astype(np.uint64) + np.uint64(10 ** 6)
     params = make_params(c)
+    extra = {"prefix_group": group.astype(np.int32)} if prefix_groups else {}
     return dict(
-        id=ids, slo_class=slo_class.astype(np.uint8), state=state.astype(np.uint8),
+        **extra, id=ids, slo_class=slo_class.astype(np.uint8), state=state.astype(np.uint8),
         queue_tier=queue_tier.astype(np.uint8), prefix_tier=tier.astype(np.uint8),
         arrival_ns=arrival.astype(np.int64), n_in=n_in.astype(np.int32),
         n_out_pred=n_out.astype(np.int32), n_prefix=n_prefix.astype(np.int32),
