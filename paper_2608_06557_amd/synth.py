@@ -304,6 +304,27 @@ def make_workload(cfg: int, seed: int | None = None, n: int | None = None,
     )
 
 
+# ------------------------------------------------------ save and replay
+
+def save_workload(w: dict, path: str) -> None:
+    """One step's inputs (request arrays, block table, free list, optional
+    prefix groups, parameters) to an .npz file (no pickled objects)."""
+    import json
+    arrays = {k: np.asarray(v) for k, v in w.items()
+              if isinstance(v, np.ndarray) and k not in ("queued",)}
+    arrays["params_json"] = np.frombuffer(json.dumps(w["params"]).encode(), np.uint8)
+    np.savez_compressed(path, **arrays)
+
+
+def load_workload(path: str) -> dict:
+    """The inverse of save_workload (loads with allow_pickle=False)."""
+    import json
+    with np.load(path, allow_pickle=False) as z:
+        w = {k: z[k] for k in z.files if k != "params_json"}
+        w["params"] = json.loads(bytes(z["params_json"]).decode())
+    return w
+
+
 # ------------------------------------------------------------ KV payload
 
 def hash32_np(word_index: np.ndarray, seed: int) -> np.ndarray:

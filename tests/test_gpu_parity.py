@@ -26,7 +26,13 @@ def dev():
     return device
 
 
+# the workload of the running test, saved to .npz if the test fails (see
+# conftest.py; replay with `python -m tests.replay_step FILE`)
+LAST_WORKLOAD = {}
+
+
 def run_both(dev, w, caps=(None, None, None)):
+    LAST_WORKLOAD["w"] = w
     d = dev.DeviceStep(w, slot_cap=caps[0], unpack_cap=caps[1], pack_cap=caps[2])
     rc = d.run()
     assert rc == 0, rc
@@ -342,3 +348,56 @@ def test_repeatable(dev):
         outs.append(d.fetch())
     for k in ARRAYS + ["admitted", "slot_list"]:
         assert np.array_equal(outs[0][k], outs[1][k]) and np.array_equal(outs[0][k], outs[2][k])
+
+
+# ------------------------------------------------------ domain corners
+
+CORNERS = {
+    # every cost at its bound: c_iter + B_max * c_dec = 2^36, c_tok = 2^28,
+    # c_attn = 2^16, gamma = 16, one-token blocks, links at 2^40 / 2^32 per
+    # block, targets of 2^50 ns, a clock just under 2^62, the largest caps
+    "max": dict(c_iter_ps=(1 << 36) - 4096 * (1 << 23), c_decode_ps=1 << 23, max_batch=4096,
+                load_decodes=4095, c_token_ps=1 << 28, c_attn_ps=1 << 16, gamma_q16=1 << 20,
+                block_tokens=1, chunk_tokens=16, link_delta_ns=[1 << 40, 1 << 40],
+                link_blk_ns=[1 << 32, 1 << 32], slo_ns=[1 << 50] * 16, num_classes=16,
+                t_now_ns=(1 << 62) - 1, token_cap=1 << 24, tier2_reserve_q16=65536,
+                max_move_blocks=2 ** 31 - 1),
+    # every cost and cap at its floor, a clock at zero, 65536-token blocks
+    "min": dict(c_iter_ps=0, c_decode_ps=0, c_token_ps=0, c_attn_ps=0, gamma_q16=65536,
+                max_batch=1, load_decodes=0, block_tokens=1 << 16, chunk_tokens=1 << 20,
+                link_delta_ns=[0, 0], link_blk_ns=[1, 1], slo_ns=[0] * 16, num_classes=1,
+                t_now_ns=0, token_cap=1, tier2_reserve_q16=0, max_move_blocks=0),
+    # the cost bound reached at batch 128 with 16-token blocks, full guardband
+    "mid": dict(c_iter_ps=(1 << 36) - 128 * (1 << 28), c_decode_ps=1 << 28, max_batch=128,
+                load_decodes=64, c_token_ps=1 << 28, c_attn_ps=1 << 16, gamma_q16=1 << 20,
+                block_tokens=16, chunk_tokens=512, slo_ns=[1 << 50, 1 << 40, 1 << 30] + [0] * 13,
+                num_classes=3, t_now_ns=(1 << 62) - 1, token_cap=1 << 20,
+                tier2_reserve_q16=4096, max_move_blocks=100000),
+}
+
+
+@pytest.mark.parametrize("corner", sorted(CORNERS))
+@pytest.mark.parametrize("n,max_in", [(300, 1 << 17), (3000, 1 << 12)])
+def test_parameter_domain_corners(dev, corner, n, max_in):
+    """Parameters at the edges of the domain (the gamma product needs more
+    than 64 bits before its shift at the "max" corner), prompts up to 2^17
+    tokens, and a fifth of the queue arriving at time zero (budgets clamped
+    in the key); the one-workgroup and the multi-launch path."""
+    rng = np.random.default_rng(n + len(corner))
+    p = helpers.base_params(**CORNERS[corner])
+    w = helpers.random_workload(rng, n, params=p, max_in=max_in)
+    old = rng.random(n) < 0.2
+    w["arrival_ns"] = np.where(old, 0, w["arrival_ns"]).astype(np.int64)
+    print(f"corner {corner} n={n} max_in={max_in} pool={w['params']['num_blocks']}", flush=True)
+    g, o = run_both(dev, w)
+    assert o["rc"] == ref.OK
+    assert_same(g, o, f"corner {corner} n={n}")
+
+
+def test_largest_queue(dev):
+    """2^20 requests, the most a step takes."""
+    import paper_2608_06557_amd.synth as synth
+    w = synth.make_workload(2, seed=2024, n=1 << 20)
+    print(f"n={len(w['id'])}", flush=True)
+    g, o = run_both(dev, w)
+    assert_same(g, o, "n=2^20")

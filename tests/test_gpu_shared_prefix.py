@@ -23,7 +23,11 @@ def dev():
     return device
 
 
+LAST_WORKLOAD = {}
+
+
 def run_both(dev, w):
+    LAST_WORKLOAD["w"] = w
     nb = int(w["params"]["num_blocks"])
     d = dev.DeviceStep(w, slot_cap=nb, unpack_cap=nb, pack_cap=nb)
     assert d.run() == 0
