@@ -946,24 +946,11 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
   // tile-local starts and global bucket bases, in digit order
   int v2[2] = {(int)tcount, dt ? (int)gcount : 0}, tot2[2];
   block_exclusive_scan<2, int, kSortWaves>(v2, tot2, s_scan);
-  // the earlier tiles' counts, kSortWin predecessors per round trip; with
-  // 8-bit digits and more tiles than one window reaches, two threads share
-  // a bin and read two windows
-  bool timed_out = false;
-  unsigned pre = 0;
-  if (bins * 2 <= kSortBlock && (int)gridDim.x > kSortWin + 1) {
-    pre = paired_look_back(status, tile, bins, s_px, s_pc, s_pn, &timed_out);
-  } else if (dt && tile > 0) {
-    pre = look_back<unsigned, kSortWin>(status, kMaxBins, tile, t, &timed_out);
-  }
-  if (dt) {
-    if (tile > 0) publish<unsigned>(st + t, pre + tcount, kFlagInclusive);
-    s_start[t] = v2[0];
-    s_off[t] = v2[1] + (int)pre - v2[0];
-  }
-  if (timed_out) set_status(info, CASCADE_ETIMEOUT);
+  if (dt) s_start[t] = v2[0];
   __syncthreads();
-  // reorder the tile in LDS by digit
+  // reorder the tile in LDS by digit: this needs only the tile-local
+  // starts, so it runs before the look-back, whose first read then finds
+  // more of the other tiles' counts already published
 #pragma unroll
   for (int j = 0; j < kItems; ++j) {
     const bool v = dig[j] >= 0;
@@ -977,6 +964,21 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     }
     if (ok && last) s_rec[pos] = make_int4(rx[j], ry[j], rz[j], rv[j]);
   }
+  // the earlier tiles' counts, kSortWin predecessors per round trip; with
+  // 8-bit digits and more tiles than one window reaches, two threads share
+  // a bin and read two windows
+  bool timed_out = false;
+  unsigned pre = 0;
+  if (bins * 2 <= kSortBlock && (int)gridDim.x > kSortWin + 1) {
+    pre = paired_look_back(status, tile, bins, s_px, s_pc, s_pn, &timed_out);
+  } else if (dt && tile > 0) {
+    pre = look_back<unsigned, kSortWin>(status, kMaxBins, tile, t, &timed_out);
+  }
+  if (dt) {
+    if (tile > 0) publish<unsigned>(st + t, pre + tcount, kFlagInclusive);
+    s_off[t] = v2[1] + (int)pre - v2[0];
+  }
+  if (timed_out) set_status(info, CASCADE_ETIMEOUT);
   __syncthreads();
   const int count = min(kTile, n - tile_base);
   static_assert(kTile % kSortBlock == 0, "every lane runs every iteration (wave sums below)");
