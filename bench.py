@@ -163,12 +163,16 @@ def measure_reclaim(cfg, stream, reps=20):
     keep = ([b.clone() for b in d.bh], [x.clone() for x in d.lu], d.index.clone())
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
     per, tot = [[], [], []], []
-    for r in range(reps + 2):
+
+    def restore():
         for t in range(3):
             d.bh[t].copy_(keep[0][t])
             d.lu[t].copy_(keep[1][t])
         d.index.copy_(keep[2])
         d.status.zero_()
+
+    for r in range(reps + 2):
+        restore()
         ev[0].record(stream)
         for t in range(3):
             assert d.call(t, stream) == 0
@@ -180,6 +184,28 @@ def measure_reclaim(cfg, stream, reps=20):
             tot.append(ev[0].elapsed_time(ev[3]) * 1e3)
     g = d.fetch()
     assert g["status"] == 0
+    # the same chain replayed from a graph: the host enqueues nothing between
+    # the tiers; the replay's results must equal the eager chain's
+    graph = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    restore()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=cs):
+        assert d.run(cs) == 0
+    gtot = []
+    for r in range(reps + 2):
+        restore()
+        ev[0].record(stream)
+        graph.replay()
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        if r >= 2:
+            gtot.append(ev[0].elapsed_time(ev[3]) * 1e3)
+    gg = d.fetch()
+    assert gg["status"] == 0
+    for t in range(3):
+        for k in ["freed", "placed", "block_hash", "last_use_ns"]:
+            assert np.array_equal(gg["tiers"][t][k], g["tiers"][t][k]), (t, k)
     n_rec = [len(g["tiers"][t]["freed"]) + len(g["tiers"][t]["placed"]) for t in range(3)]
     slots = int(sum(w["sizes"]))
     us = float(np.median(tot))
@@ -192,6 +218,7 @@ def measure_reclaim(cfg, stream, reps=20):
             "reclaimed": n_rec, "demoted": [g["tiers"][t]["n_outgoing"] for t in range(2)],
             "index_keys": int(len(w["index_keys"])),
             "tier_us_p50": [float(np.median(x)) for x in per], "chain_us_p50": us,
+            "chain_graph_us_p50": float(np.median(gtot)),
             "slots_scanned_per_s": slots / (us * 1e-6)}, w
 
 

@@ -423,9 +423,12 @@ int cascade_prefix_probe(const void *index, int32_t capacity, int32_t n,
    freed        device int32[need]; placed device int32[max_incoming].
    index        the prefix index (NULL = none) and its capacity.
    workspace    device memory of cascade_reclaim_workspace_bytes(n_slots)
-                bytes, 256-byte aligned, zero-filled once before its first
-                use; every call leaves it that way.  One call at a time per
-                workspace.
+                bytes (about 12 bytes per slot: the call lists the slots it
+                may reclaim), 256-byte aligned, zero-filled once before its
+                first use; every call leaves its counters and histograms at
+                zero again (the rest is rewritten before it is read).  A
+                workspace sized for n slots serves every table of at most n
+                slots.  One call at a time per workspace.
    status_dev   device int32, cleared by the caller before the first call of
                 a chain.  A call that finds it nonzero does nothing.  A call
                 sets CASCADE_EINVAL for a negative last use, an incoming

@@ -6,31 +6,42 @@
 // One call reclaims `total` = need + n_incoming free slots of one tier.  The
 // reclaimed set is the `total` smallest free slots under the key
 //   empty slot -> 0,   cached block -> 1 + (last_use - min cached last_use),
-// ties by slot.  Selection is a most-significant-digit radix select over the
-// key (an 8-bit digit, then 12-bit digits), so it never sorts the table.  The
-// table is read in tiles of 2048 slots, 8 consecutive slots per thread with
-// 16-byte loads:
+// ties by slot.  The table is read in tiles of 2048 slots, 8 consecutive
+// slots per thread with 16-byte loads, three times per call:
 //
-//   rc_count_kernel  per-workgroup counts of empty / cached free slots and
-//                    the cached last-use range; the last workgroup checks the
-//                    call, sizes the key and writes the plan
-//   rc_pass_kernel   one digit: LDS histogram of the keys that match the
-//                    threshold's digits found so far, merged with atomics;
-//                    the last workgroup finds the digit holding the rank
-//   rc_tiles_kernel  per tile: slots below the threshold key T, slots equal
-//                    to T, and how many of each are demoted (the index read
-//                    once); the last workgroup locates the last slot equal to
-//                    T that is taken (they are taken in slot order), then
-//                    turns the counts into each tile's output offsets
-//   rc_write_kernel  tiles holding reclaimed slots write them, and their
-//                    demoted blocks, at those offsets; the others exit
-//   rc_update_kernel index bit updates (clear this tier, set the next for
-//                    demoted blocks) and the slot-table writes
+//   rc_count_kernel    per-workgroup counts of empty / cached free slots and
+//                      the cached last-use range; the last workgroup checks
+//                      the call, sizes the key and writes the plan
+//   rc_hist_kernel     (cached blocks needed) a histogram of the key's top
+//                      digit, 8 bits; the last workgroup finds the bucket
+//                      holding the threshold and the rank sought inside it
+//   rc_compact_kernel  per tile, in slot order: the slots certainly reclaimed
+//                      (empty ones, keys below the bucket) and the candidates
+//                      (keys inside it; with empty slots alone enough, the
+//                      empty slots), each with its key and whether it is
+//                      demoted (the index read once, before any update), in
+//                      one chunk of a list reserved with one atomic add; a
+//                      histogram of the candidates' next 12-bit digit
+//
+// Then, over the list only:
+//
+//   rc_select_kernel   every workgroup takes the next digit of the threshold
+//                      key T from that histogram and a share of the list:
+//                      candidates below that digit go to their tile's
+//                      counters, those on it are staged; the last workgroup
+//                      finds T's remaining digits among the staged ones, the
+//                      last taken slot with key T (ties are taken in slot
+//                      order, so by tile, then by position in the tile's
+//                      chunk), and every tile's output offsets
+//   rc_write_kernel    a workgroup per tile with reclaimed slots: their
+//                      positions in slot order, the freed / placed / outgoing
+//                      entries, the index bit updates (clear this tier, set
+//                      the next for demoted blocks) and the slot-table writes
 //
 // The plan lives in the caller's workspace; every kernel after the first reads
 // it and returns at once when the call failed or has nothing left to do, so
-// the host launches a fixed sequence and never waits.  The last workgroup of
-// each kernel resets the counter it used, which leaves the workspace zeroed.
+// the host launches a fixed sequence and never waits.  Counters and
+// histograms are reset by the workgroup that last uses them.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <stdint.h>
@@ -46,12 +57,28 @@ namespace {
 
 constexpr int kRcItems = 8;                  // slots per thread in slot-order kernels
 constexpr int kRcTile = kBlock * kRcItems;   // 2048 slots per tile
-constexpr int kRcGridCount = 1024;           // workgroups of the count and tile kernels
-constexpr int kRcGridPass = 512;             // workgroups of a radix pass (fewer bin merges)
-constexpr int kDigit0 = 8, kDigitN = 12;     // first digit, later digits
+constexpr int kRcGridCount = 512;            // workgroups of the count kernel
+constexpr int kRcGridCompact = 1024;         // workgroups of the compaction kernel
+constexpr int kRcGridHist = 512;             // workgroups of the histogram (fewer bin merges)
+constexpr int kDigit0 = 8, kDigitN = 12;     // top digit, later digits
 constexpr int kRcBins = 1 << kDigitN;
-constexpr int kRcPasses = 1 + (64 - kDigit0 + kDigitN - 1) / kDigitN;  // 6 covers 64 bits
-constexpr int kBinsPerThread = kRcBins / kBlock;                        // 16
+constexpr int kHistCopies = 8;               // copies of the top-digit histogram (fewer
+                                             // atomics per address), workgroup b adds to b % 8
+constexpr int kSelGrid = 64;                 // workgroups of the select kernel
+constexpr int kStageCap = 65536;             // candidates on the threshold's first digits kept
+constexpr int kStageLds = 2048;              // of them, read into the last workgroup's LDS
+constexpr int kTieLds = 256;                 // staged ones up to which the tie is found in LDS
+constexpr int kTilesLds = 2048;              // tiles whose counts the last workgroup keeps in LDS
+constexpr int kModeCached = 0, kModeEmpty = 1;
+// The list is reserved in kListGroups regions, tile t in region t % kListGroups
+// with its own counter, so no counter takes more than a few hundred adds;
+// a region holds every slot of its tiles.
+constexpr int kListGroups = 16;
+constexpr int kCountStride = 32;  // one counter per 128-byte line
+// list entry: slot in bits 0..29, certainly reclaimed in bit 30, demoted in bit 31
+constexpr unsigned kEntSlot = (1u << 30) - 1u, kEntSure = 1u << 30, kEntDem = 1u << 31;
+constexpr unsigned kNoPos = ~0u;  // a block absent from the index (or no index, or no block)
+constexpr unsigned kFindPos = ~1u;  // not looked up yet (tier 2, where nothing is demoted)
 
 struct RcPartial {
   int n_empty, n_cached, bad, pad;
@@ -62,40 +89,63 @@ struct alignas(256) RcPlan {
   int ok;         // 1: the call proceeds (checked, room enough)
   int total;      // need + n_in
   int n_in;
+  int mode;       // kModeCached: cached blocks are reclaimed; kModeEmpty: empty slots only
   int width;      // bits of the key
-  int shift;      // low bit of the digit the next pass examines
-  int dbits;      // width of that digit
-  int done;       // threshold key found
-  int rank;       // 0-based rank still sought among keys matching `prefix`
-  int take;       // slots with the threshold key taken, in slot order
-  int find_tie;   // 1: only some slots equal to T are taken
-  int tie_slot;   // last slot with the threshold key taken (-1: none; INT_MAX: all)
-  int pad0;
+  int shift;      // low bit of the top digit
+  int dbits;      // width of the top digit
+  int rank;       // 0-based rank sought: among cached keys, then inside the bucket
+                  // (kModeEmpty: among empty slots)
+  int bucket;     // the top digit of the threshold key
+  int tie_slot;   // last reclaimed slot with the threshold key (-1: none)
+  int pad[2];
   unsigned long long lu_min;
-  unsigned long long prefix;  // the threshold's digits found so far, in place; T when done
+  unsigned long long thresh;  // the threshold key T
 };
 
 struct RcWork {
   RcPlan *plan;
   unsigned *tickets;      // [(kTicketGroups + 1) * kTicketStride]
   RcPartial *partial;     // [kRcGridCount]
-  unsigned *hist;         // [kRcBins]
-  int4 *tile;             // [tiles] counts, then output offsets
+  unsigned *hist;         // [kHistCopies][1 << kDigit0] top digit
+  unsigned *sub;          // [kRcBins] candidates' next digit
+  unsigned *count;        // [kListGroups * kCountStride] entries reserved per region
+  unsigned *stage_n;      // candidates staged by the select kernel
+  unsigned long long *stage_key;  // [kStageCap]
+  unsigned *stage_ent;            // [kStageCap]
+  int4 *rec;              // [tiles] the tile's chunk: start, sure, candidates, sure demoted
+  int4 *off;              // [tiles] counts, then output offsets
+  unsigned long long *key;  // [n_slots] list: keys
+  unsigned *ent;            // [n_slots] list: slot and flags
+  unsigned *pos;            // [n_slots] list: the block's index slot (kNoPos: none)
 };
 
 constexpr size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 __host__ __device__ inline int tiles_of(long long n) { return (int)((n + kRcTile - 1) / kRcTile); }
+// entries of one list region: every slot of ceil(tiles / kListGroups) tiles
+__host__ __device__ inline long long region_cap(long long n) {
+  const long long tiles = tiles_of(n) > 0 ? tiles_of(n) : 1;
+  return (tiles + kListGroups - 1) / kListGroups * kRcTile;
+}
 
+// The counters and histograms come first, at offsets that do not depend on
+// the table size, so one workspace serves tables of any size up to its own.
 size_t workspace_bytes_for(int32_t n) {
   const size_t tiles = (size_t)std::max(1, tiles_of(n));
+  const size_t slots = (size_t)(kListGroups * region_cap(n));
   return align256(sizeof(RcPlan)) + align256(sizeof(unsigned) * (kTicketGroups + 1) * kTicketStride) +
          align256(sizeof(RcPartial) * kRcGridCount) +
-         align256(sizeof(unsigned) * kRcBins) + align256(sizeof(int4) * tiles);
+         align256(sizeof(unsigned) * kHistCopies * (1 << kDigit0)) +
+         align256(sizeof(unsigned) * kRcBins) +
+         align256(sizeof(unsigned) * kListGroups * kCountStride) + align256(sizeof(unsigned)) +
+         align256(sizeof(unsigned long long) * kStageCap) + align256(sizeof(unsigned) * kStageCap) +
+         2 * align256(sizeof(int4) * tiles) + align256(sizeof(unsigned long long) * slots) +
+         2 * align256(sizeof(unsigned) * slots);
 }
 
 RcWork carve(void *ws, int32_t n) {
   char *p = static_cast<char *>(ws);
   const size_t tiles = (size_t)std::max(1, tiles_of(n));
+  const size_t slots = (size_t)(kListGroups * region_cap(n));
   RcWork w;
   w.plan = reinterpret_cast<RcPlan *>(p);
   p += align256(sizeof(RcPlan));
@@ -104,9 +154,26 @@ RcWork carve(void *ws, int32_t n) {
   w.partial = reinterpret_cast<RcPartial *>(p);
   p += align256(sizeof(RcPartial) * kRcGridCount);
   w.hist = reinterpret_cast<unsigned *>(p);
+  p += align256(sizeof(unsigned) * kHistCopies * (1 << kDigit0));
+  w.sub = reinterpret_cast<unsigned *>(p);
   p += align256(sizeof(unsigned) * kRcBins);
-  w.tile = reinterpret_cast<int4 *>(p);
-  (void)tiles;
+  w.count = reinterpret_cast<unsigned *>(p);
+  p += align256(sizeof(unsigned) * kListGroups * kCountStride);
+  w.stage_n = reinterpret_cast<unsigned *>(p);
+  p += align256(sizeof(unsigned));
+  w.stage_key = reinterpret_cast<unsigned long long *>(p);
+  p += align256(sizeof(unsigned long long) * kStageCap);
+  w.stage_ent = reinterpret_cast<unsigned *>(p);
+  p += align256(sizeof(unsigned) * kStageCap);
+  w.rec = reinterpret_cast<int4 *>(p);
+  p += align256(sizeof(int4) * tiles);
+  w.off = reinterpret_cast<int4 *>(p);
+  p += align256(sizeof(int4) * tiles);
+  w.key = reinterpret_cast<unsigned long long *>(p);
+  p += align256(sizeof(unsigned long long) * slots);
+  w.ent = reinterpret_cast<unsigned *>(p);
+  p += align256(sizeof(unsigned) * slots);
+  w.pos = reinterpret_cast<unsigned *>(p);
   return w;
 }
 
@@ -224,19 +291,22 @@ __device__ __forceinline__ int block_slot_rank(const bool (&f)[kRcItems], int (&
   return total;
 }
 
-__device__ __forceinline__ bool status_bad(const int *status) {
-  return load_agent(status) != CASCADE_OK;
-}
 
 // Calls f(tile, slots) for this workgroup's tiles (grid-stride), loading the
 // next tile before working on the current one.
+// The workgroup's first tile (nothing is read past the table), loaded
+// before the kernel reads anything else, so the table loads do not wait for it.
+__device__ __forceinline__ Slots8 load_first(const RcArgs &a) {
+  Slots8 v;
+  load8(a, slot_base(blockIdx.x), v);
+  return v;
+}
 template <typename F>
-__device__ __forceinline__ void for_tiles(const RcArgs &a, F &&f) {
+__device__ __forceinline__ void for_tiles(const RcArgs &a, const Slots8 &first, F &&f) {
   const int tiles = max(1, tiles_of(a.n));
   int t = blockIdx.x;
   if (t >= tiles) return;
-  Slots8 cur, nxt;
-  load8(a, slot_base(t), cur);
+  Slots8 cur = first, nxt;
   for (;;) {
     const int tn = t + (int)gridDim.x;
     if (tn < tiles) load8(a, slot_base(tn), nxt);
@@ -246,6 +316,10 @@ __device__ __forceinline__ void for_tiles(const RcArgs &a, F &&f) {
     t = tn;
   }
 }
+template <typename F>
+__device__ __forceinline__ void for_tiles(const RcArgs &a, F &&f) {
+  for_tiles(a, load_first(a), f);
+}
 
 // ------------------------------------------------------------- count kernel
 
@@ -254,8 +328,9 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
   __shared__ unsigned long long s_mm[kWaves * 2];
   __shared__ bool s_last;
   __shared__ int s_err;
-  int cnt[3] = {0, 0, 0};  // empty free, cached free, negative last use
+  int cnt[3] = {0, 0, 0};  // empty free, cached free, bad data (negative last use, hash 0 in)
   unsigned long long mn = ~0ull, mx = 0ull;
+  const int n_in_all = a.n_in_dev ? load_agent(a.n_in_dev) : 0;
   for_tiles(a, [&](int, const Slots8 &v) {  // past the table: held, stamp 0
 #pragma unroll
     for (int j = 0; j < kRcItems; ++j) {
@@ -269,6 +344,11 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
       }
     }
   });
+  // this workgroup's share of the incoming blocks: none may have hash 0
+  if (n_in_all >= 0 && n_in_all <= a.max_in)
+    for (int j = (int)(blockIdx.x * kBlock + threadIdx.x); j < n_in_all;
+         j += (int)(gridDim.x * kBlock))
+      cnt[2] |= a.incoming[j].hash == 0ull;
   block_sum<3, int>(cnt, s_red);
   mn = wave_min(mn);
   mx = wave_max(mx);
@@ -295,16 +375,22 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
   if (!s_last) return;
   acquire_agent();
 
-  // the last workgroup: totals, incoming check, plan
+  // the last workgroup: totals and plan
+  const int status_was = load_agent(a.status);  // requested with the partials
   int tot[3] = {0, 0, 0};
   unsigned long long tmn = ~0ull, tmx = 0ull;
-  for (int g = threadIdx.x; g < (int)gridDim.x; g += kBlock) {
-    const RcPartial *p = a.w.partial + g;
-    tot[0] += load_agent(&p->n_empty);
-    tot[1] += load_agent(&p->n_cached);
-    tot[2] |= load_agent(&p->bad);
-    tmn = min(tmn, load_agent(&p->lu_min));
-    tmx = max(tmx, load_agent(&p->lu_max));
+  static_assert(kRcGridCount % kBlock == 0, "whole rounds of partials");
+#pragma unroll
+  for (int r = 0; r < kRcGridCount / kBlock; ++r) {  // all loads in flight at once
+    const int g = r * kBlock + (int)threadIdx.x;
+    if (g < (int)gridDim.x) {
+      const RcPartial *p = a.w.partial + g;
+      tot[0] += load_agent(&p->n_empty);
+      tot[1] += load_agent(&p->n_cached);
+      tot[2] |= load_agent(&p->bad);
+      tmn = min(tmn, load_agent(&p->lu_min));
+      tmx = max(tmx, load_agent(&p->lu_max));
+    }
   }
   block_sum<3, int>(tot, s_red);
   tmn = wave_min(tmn);
@@ -314,17 +400,13 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
     s_mm[wave_id() * 2 + 1] = tmx;
   }
   if (threadIdx.x == 0) {
-    const int n_in = a.n_in_dev ? load_agent(a.n_in_dev) : 0;
-    s_err = status_bad(a.status) ? 1 : 0;  // an earlier call of the chain failed
+    const int n_in = n_in_all;
+    s_err = status_was != CASCADE_OK ? 1 : 0;  // an earlier call of the chain failed
     if (!s_err && (tot[2] || n_in < 0 || n_in > a.max_in)) s_err = CASCADE_EINVAL;
     s_red[0] = n_in;
   }
   __syncthreads();
   const int n_in = s_red[0];
-  int zero_hash = 0;
-  if (s_err == 0)
-    for (int j = threadIdx.x; j < n_in; j += kBlock) zero_hash |= a.incoming[j].hash == 0ull;
-  zero_hash = __syncthreads_or(zero_hash);
   if (threadIdx.x == 0) {
     for (int w = 1; w < kWaves; ++w) {
       tmn = min(tmn, s_mm[w * 2]);
@@ -332,7 +414,6 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
     }
     RcPlan *P = a.w.plan;
     int err = s_err;
-    if (err == 0 && zero_hash) err = CASCADE_EINVAL;
     const long long total = (long long)a.need + n_in;
     if (err == 0 && total > (long long)tot[0] + tot[1]) err = CASCADE_ENOSPC;
     if (err < 0) store_agent(a.status, err);
@@ -340,22 +421,19 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
     P->total = (int)total;
     P->n_in = n_in;
     P->lu_min = tmn;
-    P->prefix = 0ull;
+    P->thresh = 0ull;
     P->tie_slot = -1;
-    P->find_tie = 0;
+    P->bucket = 0;
     if (total <= tot[0]) {
-      // empty slots suffice: the threshold is key 0, taken in slot order
-      P->width = 0;
-      P->done = 1;
-      P->rank = 0;
-      P->take = (int)total;
-      P->find_tie = total > 0 && total < tot[0];
-      P->tie_slot = total == 0 ? -1 : (total == tot[0] ? INT_MAX : -1);
+      // empty slots suffice: the first `total` of them in slot order
+      P->mode = kModeEmpty;
+      P->width = P->shift = P->dbits = 0;
+      P->rank = (int)total - 1;
     } else {
       // every empty slot plus the (total - n_empty) least recent cached ones
       const int width = bit_width64(1ull + (tmx - tmn));
+      P->mode = kModeCached;
       P->width = width;
-      P->done = 0;
       P->dbits = min(width, kDigit0);
       P->shift = width - P->dbits;
       P->rank = (int)(total - tot[0] - 1);
@@ -363,329 +441,651 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
   }
 }
 
-// ----------------------------------------------------- radix select passes
+// ------------------------------------------------------------ top digit
 
-__global__ __launch_bounds__(kBlock) void rc_pass_kernel(RcArgs a) {
-  __shared__ unsigned s_hist[kRcBins];
+// Histogram of the top digit of every cached free slot's key (kModeCached
+// only); the last workgroup finds the bucket holding the sought rank.
+__global__ __launch_bounds__(kBlock) void rc_hist_kernel(RcArgs a) {
+  constexpr int kBins0 = 1 << kDigit0;
+  static_assert(kBins0 == kBlock, "one bin per thread");
+  __shared__ unsigned s_hist[kBins0];
   __shared__ int s_scan[kWaves];
   __shared__ bool s_last;
   __shared__ int s_found[2];
+  const Slots8 first = load_first(a);
   const RcPlan *P = a.w.plan;
-  if (!P->ok || P->done) return;  // uniform: the plan is the previous kernel's
-  const int shift = P->shift, dbits = P->dbits;
+  if (!P->ok || P->mode != kModeCached) return;  // uniform: the plan is the previous kernel's
+  const int t = threadIdx.x, shift = P->shift;
   const unsigned long long lu_min = P->lu_min;
-  const unsigned long long hi = shr64(P->prefix, shift + dbits);
-  const unsigned dmask = (1u << dbits) - 1u;
-  const int nbins = 1 << dbits;
-  for (int b = threadIdx.x; b < nbins; b += kBlock) s_hist[b] = 0u;
+  s_hist[t] = 0u;
   __syncthreads();
-  for_tiles(a, [&](int, const Slots8 &v) {
+  for_tiles(a, first, [&](int, const Slots8 &v) {
 #pragma unroll
     for (int j = 0; j < kRcItems; ++j) {
       if (v.held[j] || v.h[j] == 0ull) continue;  // only cached free slots have keys above 0
-      const unsigned long long k = rc_key(v.h[j], v.lu[j], lu_min);
-      if (shr64(k, shift + dbits) == hi)
-        atomicAdd(&s_hist[(unsigned)(k >> shift) & dmask], 1u);
+      // below 2^dbits: the count kernel saw every stamp in [lu_min, lu_max]
+      const unsigned b = (unsigned)shr64(rc_key(v.h[j], v.lu[j], lu_min), shift);
+      atomicAdd(&s_hist[b & (kBins0 - 1)], 1u);
     }
   });
   __syncthreads();
-  for (int b = threadIdx.x; b < nbins; b += kBlock) {
-    const unsigned v = s_hist[b];
-    if (v) atomicAdd(&a.w.hist[b], v);
+  {
+    const unsigned v = s_hist[t];
+    if (v) atomicAdd(a.w.hist + (blockIdx.x % kHistCopies) * kBins0 + t, v);
   }
   wait_stores();
   __syncthreads();
-  if (threadIdx.x == 0) s_last = last_workgroup(a.w.tickets);
+  if (t == 0) s_last = last_workgroup(a.w.tickets);
   __syncthreads();
   if (!s_last) return;
   acquire_agent();
 
-  // the last workgroup: the digit in which the sought rank falls
+  // the last workgroup: the bucket in which the sought rank falls
   const int rank = P->rank;
-  if (threadIdx.x == 0) s_found[0] = -1;
-  unsigned v[kBinsPerThread];
-  int sum = 0;
-  const int b0 = threadIdx.x * kBinsPerThread;
-#pragma unroll
-  for (int j = 0; j < kBinsPerThread; ++j) {
-    const int b = b0 + j;
-    v[j] = b < nbins ? load_agent(a.w.hist + b) : 0u;
-    sum += (int)v[j];
+  unsigned v = 0;
+  for (int c = 0; c < kHistCopies; ++c) {
+    v += load_agent(a.w.hist + c * kBins0 + t);
+    store_agent(a.w.hist + c * kBins0 + t, 0u);  // cleared for the next call
   }
-#pragma unroll
-  for (int j = 0; j < kBinsPerThread; ++j)  // clear for the next pass
-    if (b0 + j < nbins) store_agent(a.w.hist + b0 + j, 0u);
-  int excl[1] = {sum}, tot[1];
-  block_exclusive_scan<1, int>(excl, tot, s_scan);
-  if (rank >= excl[0] && rank < excl[0] + sum) {
-    int r = rank - excl[0];
-#pragma unroll
-    for (int j = 0; j < kBinsPerThread; ++j) {
-      if (r >= 0 && r < (int)v[j]) {
-        s_found[0] = b0 + j;
-        s_found[1] = r;
-        s_hist[0] = v[j];  // keys equal on every digit so far
-        r = -1;
-      } else if (r >= 0) {
-        r -= (int)v[j];
-      }
-    }
+  if (t == 0) s_found[0] = -1;
+  int ex[1] = {(int)v}, tot[1];
+  block_exclusive_scan<1, int>(ex, tot, s_scan);
+  if (rank >= ex[0] && rank < ex[0] + (int)v) {
+    s_found[0] = t;
+    s_found[1] = rank - ex[0];
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (t == 0) {
     RcPlan *W = a.w.plan;
     if (s_found[0] < 0) {  // the counts disagree with the plan: stop the call
       store_agent(a.status, (int)CASCADE_EINTERNAL);
       W->ok = 0;
       return;
     }
-    W->prefix = P->prefix | ((unsigned long long)s_found[0] << shift);
+    W->bucket = s_found[0];
     W->rank = s_found[1];
-    if (shift == 0) {
-      // the threshold is known; take = rank + 1 of the slots holding it
-      const int ties = (int)s_hist[0];
-      W->done = 1;
-      W->take = s_found[1] + 1;
-      W->find_tie = W->take < ties;
-      W->tie_slot = W->take < ties ? -1 : INT_MAX;
-    } else {
-      const int d = min(shift, kDigitN);
-      W->dbits = d;
-      W->shift = shift - d;
-    }
   }
 }
 
-// ------------------------------------------------------ per-tile counts
+// ------------------------------------------------------------ compaction
 
-__device__ __forceinline__ bool demotable(const RcArgs &a, unsigned long long h) {
-  if (a.tier >= 2 || h == 0ull) return false;
-  if (!a.index) return true;
-  const IndexSlot *e = index_find(a.index, a.index_mask, h);
+// Whether reclaiming block h from tier 0 or 1 demotes it (no deeper tier
+// holds it in the index), and its index slot for the later bit updates.
+__device__ __forceinline__ bool demotable(const RcArgs &a, unsigned long long h, unsigned &pos) {
+  pos = kNoPos;
+  if (h == 0ull) return false;
+  const IndexSlot *e = a.index ? index_find(a.index, a.index_mask, h) : nullptr;
+  if (e) pos = (unsigned)(e - a.index);
   return e == nullptr || (e->tiers & ~((2u << a.tier) - 1u)) == 0u;  // no deeper tier
 }
 
-// a tile's four counts, written by another workgroup as two atomic words
-__device__ __forceinline__ int4 load_rec(const unsigned long long *rec64, int t) {
-  const unsigned long long u = load_agent(rec64 + 2 * t), w = load_agent(rec64 + 2 * t + 1);
-  return make_int4((int)(unsigned)u, (int)(unsigned)(u >> 32), (int)(unsigned)w,
-                   (int)(unsigned)(w >> 32));
-}
-
-// Per tile: slots below T, slots equal to T, and the demoted ones among
-// each.  The last workgroup finds the last slot equal to T that is taken
-// (the take-th in slot order), then writes every tile's output offsets and
-// counts: tile[t] = (reclaimed before t, demoted before t, reclaimed in t,
-// demoted in t).
-__global__ __launch_bounds__(kBlock) void rc_tiles_kernel(RcArgs a) {
-  __shared__ int s_red[kWaves * 4];
-  __shared__ bool s_last;
-  __shared__ int s_hit[2];
+// Per tile, in slot order: the slots certainly reclaimed and the candidates,
+// as one chunk of the list (start, certain count, candidate count, certain
+// demoted count in rec[tile]); the candidates' next digit is histogrammed.
+// Demotion is decided here, on the index as it was when the call began.
+__global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
+  __shared__ unsigned s_sub[kRcBins];
+  __shared__ int s_rank[kWaves];
+  __shared__ int s_red[kWaves * 2];
+  __shared__ int s_start;
+  const Slots8 first = load_first(a);
   const RcPlan *P = a.w.plan;
   if (!P->ok) return;
-  const int tiles = max(1, tiles_of(a.n));
-  const unsigned long long T = P->prefix, lu_min = P->lu_min;
-  unsigned long long *rec64 = reinterpret_cast<unsigned long long *>(a.w.tile);
-  for_tiles(a, [&](int tile, const Slots8 &v) {
-    int c[4] = {0, 0, 0, 0};
+  const int t = threadIdx.x;
+  const bool cached = P->mode == kModeCached;
+  const int shift = P->shift;
+  const unsigned long long lu_min = P->lu_min, bucket = (unsigned long long)P->bucket;
+  const int d2 = cached ? min(shift, kDigitN) : 0, s2 = shift - d2;
+  const unsigned m2 = (1u << d2) - 1u;
+  if (d2 > 0)
+    for (int b = t; b < (1 << d2); b += kBlock) s_sub[b] = 0u;
+  __syncthreads();
+  for_tiles(a, first, [&](int tile, const Slots8 &v) {
+    bool f[kRcItems], sure[kRcItems];
+    unsigned long long k[kRcItems];
 #pragma unroll
     for (int j = 0; j < kRcItems; ++j) {
-      const unsigned long long k = rc_key(v.h[j], v.lu[j], lu_min);
-      const bool below = !v.held[j] && k < T, equal = !v.held[j] && k == T;
-      const bool dem = (below || equal) && demotable(a, v.h[j]);
-      c[0] += below;
-      c[1] += equal;
-      c[2] += below && dem;
-      c[3] += equal && dem;
+      const bool fr = !v.held[j], empty = fr && v.h[j] == 0ull, full = fr && v.h[j] != 0ull;
+      k[j] = full ? rc_key(v.h[j], v.lu[j], lu_min) : 0ull;
+      if (cached) {
+        const unsigned long long top = shr64(k[j], shift);
+        sure[j] = empty || (full && top < bucket);
+        f[j] = sure[j] || (full && top == bucket);
+      } else {
+        sure[j] = false;
+        f[j] = empty;
+      }
     }
-    block_sum<4, int>(c, s_red);
-    if (threadIdx.x == 0) {  // (x, y) and (z, w) of the tile's int4, as two atomic words
-      store_agent(rec64 + 2 * tile, (unsigned long long)(unsigned)c[0] |
-                                        ((unsigned long long)(unsigned)c[1] << 32));
-      store_agent(rec64 + 2 * tile + 1, (unsigned long long)(unsigned)c[2] |
-                                            ((unsigned long long)(unsigned)c[3] << 32));
+    // the index lookups first: their latency overlaps the workgroup scans
+    // (tier 2 demotes nothing: its reclaimed blocks are looked up when written)
+    bool dem[kRcItems];
+    unsigned ip[kRcItems];
+#pragma unroll
+    for (int j = 0; j < kRcItems; ++j) {
+      ip[j] = (a.tier >= 2 && v.h[j] != 0ull && a.index) ? kFindPos : kNoPos;
+      dem[j] = f[j] && a.tier < 2 && demotable(a, v.h[j], ip[j]);  // false when empty
+    }
+    int rk[kRcItems];
+    const int cnt = block_slot_rank(f, rk, s_rank);
+    // the chunk is reserved at once; its start is used only after the sums
+    const int g = tile % kListGroups;
+    const int start0 = (t == 0 && cnt)
+                           ? (int)(g * region_cap(a.n)) +
+                                 (int)atomicAdd(a.w.count + g * kCountStride, (unsigned)cnt)
+                           : 0;
+    int c2[2] = {0, 0};
+#pragma unroll
+    for (int j = 0; j < kRcItems; ++j) {
+      c2[0] += sure[j];
+      c2[1] += sure[j] && dem[j];
+    }
+    block_sum<2, int>(c2, s_red);
+    if (t == 0) {
+      s_start = start0;
+      a.w.rec[tile] = make_int4(start0, c2[0], cnt - c2[0], c2[1]);
+      a.w.off[tile] = make_int4(0, 0, 0, 0);  // the select kernel's counters
+    }
+    __syncthreads();
+    const int start = s_start, base = slot_base(tile);
+#pragma unroll
+    for (int j = 0; j < kRcItems; ++j) {
+      const int i = start + rk[j];
+      if (!f[j] || (long long)(unsigned)i >= kListGroups * region_cap(a.n)) continue;
+      a.w.key[i] = k[j];
+      a.w.ent[i] = (unsigned)item_slot(base, j) | (sure[j] ? kEntSure : 0u) |
+                   (dem[j] ? kEntDem : 0u);
+      a.w.pos[i] = ip[j];
+      if (d2 > 0 && !sure[j]) atomicAdd(&s_sub[(unsigned)(k[j] >> s2) & m2], 1u);
     }
   });
-  if (threadIdx.x == 0) {
-    wait_stores();
-    s_last = last_workgroup(a.w.tickets);
+  if (d2 > 0) {
+    __syncthreads();
+    for (int b = t; b < (1 << d2); b += kBlock) {
+      const unsigned v = s_sub[b];
+      if (v) atomicAdd(a.w.sub + b, v);
+    }
   }
+}
+
+// ------------------------------------------------------------ selection
+
+// The bin of a kRcBins-bin histogram (kSelBins consecutive bins per thread
+// of a kBlock-thread workgroup) holding the 0-based rank r: the bin, the
+// rank inside it and its count; bin -1 when no bin holds it.
+constexpr int kSelBins = kRcBins / kBlock;
+struct Hit {
+  int bin, rank, count;
+};
+__device__ __forceinline__ Hit find_rank(const unsigned (&v)[kSelBins], int r, int *s_scan,
+                                         int *s_found) {
+  int sum = 0;
+#pragma unroll
+  for (int j = 0; j < kSelBins; ++j) sum += (int)v[j];
+  if (threadIdx.x == 0) s_found[0] = -1;
+  int ex[1] = {sum}, tot[1];
+  block_exclusive_scan<1, int>(ex, tot, s_scan);
+  if (r >= ex[0] && r < ex[0] + sum) {
+    int q = r - ex[0];
+#pragma unroll
+    for (int j = 0; j < kSelBins; ++j) {
+      if (q >= 0 && q < (int)v[j]) {
+        s_found[0] = (int)threadIdx.x * kSelBins + j;
+        s_found[1] = q;
+        s_found[2] = (int)v[j];
+        q = -1;
+      } else if (q >= 0) {
+        q -= (int)v[j];
+      }
+    }
+  }
+  __syncthreads();
+  const Hit h = {s_found[0], s_found[1], s_found[2]};
+  __syncthreads();
+  return h;
+}
+
+// The list regions walked as one flat index: entry f of region g sits at
+// g * cap + (f - pre[g]), pre the regions' exclusive prefix.
+struct ListMap {
+  int pre[kListGroups + 1];
+  int cap;
+  __device__ __forceinline__ int at(int f) const {
+    int g = 0, start = 0;  // constant indices only: pre stays in registers
+#pragma unroll
+    for (int q = 1; q < kListGroups; ++q) {
+      const bool ge = f >= pre[q];
+      g = ge ? q : g;
+      start = ge ? pre[q] : start;
+    }
+    return g * cap + (f - start);
+  }
+  __device__ __forceinline__ int size() const { return pre[kListGroups]; }
+};
+
+// Calls f(e, k) for the entries a thread owns among n (flat index fi =
+// first + j * stride): e = ent[at(fi)], k = key[at(fi)], kSelBatch entries
+// per round, all loaded before any is used, so a pass costs a few memory
+// round trips rather than one per entry.  Certainly reclaimed entries are
+// skipped.
+constexpr int kSelBatch = 8;
+template <typename At, typename F>
+__device__ __forceinline__ void for_entries(const unsigned *__restrict__ ent,
+                                            const unsigned long long *__restrict__ key, int n,
+                                            int first, int stride, At &&at, F &&f) {
+  for (int r0 = first; r0 < n; r0 += stride * kSelBatch) {
+    unsigned e[kSelBatch];
+    unsigned long long k[kSelBatch];
+#pragma unroll
+    for (int j = 0; j < kSelBatch; ++j) {
+      const int fi = r0 + j * stride;
+      const int i = fi < n ? at(fi) : 0;
+      e[j] = fi < n ? ent[i] : kEntSure;  // past the end: skipped
+      k[j] = fi < n ? key[i] : 0ull;
+    }
+#pragma unroll
+    for (int j = 0; j < kSelBatch; ++j)
+      if (!(e[j] & kEntSure)) f(e[j], k[j]);
+  }
+}
+
+// Adds one candidate to its tile's counters in off[]: (below T, equal to T,
+// demoted below, demoted equal).
+__device__ __forceinline__ void count_in_tile(int4 *off, unsigned e, bool below) {
+  int *c = &off[(e & kEntSlot) / kRcTile].x;
+  atomicAdd(c + (below ? 0 : 1), 1);
+  if (e & kEntDem) atomicAdd(c + (below ? 2 : 3), 1);
+}
+
+// The threshold key T, the last taken slot with key T and every tile's
+// output offsets.  Every workgroup: the next digit d2 of T from the
+// compaction's histogram, then a share of the list: candidates whose digit
+// is below d2 are below T and go straight to their tile's counters, those
+// on d2 are staged (when every bit of T is already known, each candidate is
+// counted against T instead).  The last workgroup: T's remaining digits
+// over the staged candidates, their counts, the tile holding the take-th
+// key T in tile (slot) order, that key's slot, and
+//   off[t] = (reclaimed before t, demoted before t, reclaimed in t, demoted in t).
+// A threshold prefix shared by more than kStageCap candidates is resolved
+// from the whole list instead of the stage.
+__global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
+  __shared__ unsigned s_hist[kRcBins];
+  __shared__ int s_scan[kWaves * 2];
+  __shared__ int s_found[3];
+  __shared__ int s_pre[kListGroups + 1];
+  __shared__ bool s_last;
+  __shared__ unsigned long long s_skey[kStageLds];
+  __shared__ unsigned s_sent[kStageLds];
+  __shared__ int4 s_q[kTilesLds];
+  RcPlan *P = a.w.plan;
+  if (!P->ok) return;
+  const int t = threadIdx.x;
+  const int tiles = max(1, tiles_of(a.n));
+  // the compaction's histogram of the next digit, requested with the counts
+  // (bins past 2^d2 were never added to)
+  unsigned v2[kSelBins];
+  {
+    const uint4 *sub = reinterpret_cast<const uint4 *>(a.w.sub) + t * (kSelBins / 4);
+#pragma unroll
+    for (int q = 0; q < kSelBins / 4; ++q) {
+      const uint4 u = sub[q];
+      v2[4 * q] = u.x;
+      v2[4 * q + 1] = u.y;
+      v2[4 * q + 2] = u.z;
+      v2[4 * q + 3] = u.w;
+    }
+  }
+  if (t < 64) {  // the regions' entry counts and their prefix
+    const int c = t < kListGroups ? (int)a.w.count[t * kCountStride] : 0;
+    const int inc = (int)wave_inclusive_sum((unsigned)c);
+    if (t < kListGroups) s_pre[t + 1] = inc;
+    if (t == 0) s_pre[0] = 0;
+  }
+  __syncthreads();
+  ListMap lst;
+#pragma unroll
+  for (int g = 0; g <= kListGroups; ++g) lst.pre[g] = s_pre[g];
+  lst.cap = (int)region_cap(a.n);
+  auto at_list = [lst](int fi) { return lst.at(fi); };
+  const unsigned long long *key = a.w.key;
+  const unsigned *ent = a.w.ent;
+
+  const bool cached = P->mode == kModeCached;
+  const int shift0 = P->shift;
+  const bool has_sub = cached && shift0 > 0;
+  unsigned long long T = cached ? (unsigned long long)P->bucket << shift0 : 0ull;
+  int rank = P->rank;  // kModeEmpty: total - 1 among the empty slots
+  int shift = has_sub ? shift0 : 0, matching = 0, d2 = 0, s2 = 0;
+  unsigned b2 = 0;
+  bool fail = false;
+  if (has_sub) {
+    d2 = min(shift0, kDigitN);
+    s2 = shift0 - d2;
+    const Hit h = find_rank(v2, rank, s_scan, s_found);
+    if (h.bin < 0) {
+      fail = true;
+    } else {
+      b2 = (unsigned)h.bin;
+      T |= (unsigned long long)b2 << s2;
+      rank = h.rank;
+      matching = h.count;
+      shift = s2;
+    }
+  }
+  const bool staging = has_sub && matching <= kStageCap;
+  if (cached && !fail) {
+    const unsigned m2 = (1u << d2) - 1u;
+    for_entries(ent, key, lst.size(), (int)(blockIdx.x * kBlock) + t, (int)(gridDim.x * kBlock),
+                at_list, [&](unsigned e, unsigned long long k) {
+      if (!has_sub) {  // every bit of T known
+        if (k <= T) count_in_tile(a.w.off, e, k < T);
+        return;
+      }
+      const unsigned dg = (unsigned)(k >> s2) & m2;
+      if (dg < b2) {
+        count_in_tile(a.w.off, e, true);
+      } else if (dg == b2 && staging) {
+        const unsigned p = atomicAdd(a.w.stage_n, 1u);
+        if (p < (unsigned)kStageCap) {
+          a.w.stage_key[p] = k;
+          a.w.stage_ent[p] = e;
+        }
+      }
+    });
+  }
+  wait_stores();
+  __syncthreads();
+  if (t == 0) s_last = last_workgroup(a.w.tickets);
   __syncthreads();
   if (!s_last) return;
   acquire_agent();
-  Slots8 v;
 
-  // the last workgroup.  1: the tile holding the take-th slot equal to T
-  const int take = P->take;
-  const int per = (tiles + kBlock - 1) / kBlock;
-  const int t0 = min(tiles, (int)threadIdx.x * per), t1 = min(tiles, t0 + per);
-  int cut = take == 0 ? -1 : tiles;  // tiles before `cut` give all their slots equal to T
-  int r_cut = 0, dem_cut = 0, tie_slot = take == 0 ? -1 : INT_MAX;
-  if (threadIdx.x == 0) s_hit[0] = -1;
-  if (P->find_tie) {
-    int sum = 0;
-    for (int t = t0; t < t1; ++t) sum += (int)(load_agent(rec64 + 2 * t) >> 32);
-    int ex[1] = {sum}, tot[1];
-    block_exclusive_scan<1, int>(ex, tot, s_red);
-    if (take > ex[0] && take <= ex[0] + sum) {
-      int before = ex[0];
-      for (int t = t0; t < t1; ++t) {
-        const int ct = (int)(load_agent(rec64 + 2 * t) >> 32);
-        if (take <= before + ct) {
-          s_hit[0] = t;
-          s_hit[1] = take - before;  // 1-based rank inside tile t
-          break;
-        }
-        before += ct;
+  // ---- the last workgroup
+  if (has_sub)
+    for (int b = t; b < kRcBins; b += kBlock) a.w.sub[b] = 0u;  // free for the next call
+  const int n_staged = (int)load_agent(a.w.stage_n);
+  if (staging && n_staged != matching) fail = true;
+  // the candidates on T's first digits: the stage (in LDS when it fits),
+  // or the whole list filtered by those digits
+  const unsigned long long *skey = a.w.stage_key;
+  const unsigned *sent = a.w.stage_ent;
+  const bool in_lds = staging && !fail && n_staged <= kStageLds;
+  if (in_lds) {
+    static_assert(kStageLds % kBlock == 0, "whole rounds");
+#pragma unroll
+    for (int j = 0; j < kStageLds / kBlock; ++j) {  // all loads in flight at once
+      const int i = j * kBlock + t;
+      if (i < n_staged) {
+        s_skey[i] = skey[i];
+        s_sent[i] = sent[i];
       }
     }
     __syncthreads();
-    if (s_hit[0] < 0) {  // the counts disagree with the plan: stop the call
-      if (threadIdx.x == 0) {
-        store_agent(a.status, (int)CASCADE_EINTERNAL);
-        a.w.plan->ok = 0;
-      }
-      return;
+  }
+  auto at_stage = [](int fi) { return fi; };
+  auto for_matching = [&](auto &&f) {
+    if (in_lds) {
+      for (int i = t; i < n_staged; i += kBlock) f(s_sent[i], s_skey[i]);
+    } else if (staging) {
+      for_entries(sent, skey, n_staged, t, kBlock, at_stage, f);
+    } else {
+      const unsigned long long hi = shr64(T, s2);
+      for_entries(ent, key, lst.size(), t, kBlock, at_list,
+                  [&](unsigned e, unsigned long long k) {
+                    if (shr64(k, s2) == hi) f(e, k);
+                  });
     }
-    cut = s_hit[0];
-    r_cut = s_hit[1];
-    // inside the cut tile: the slot of the r_cut-th equal key, and how many
-    // of the first r_cut are demoted
-    const int base = slot_base(cut);
-    load8(a, base, v);
-    bool eq[kRcItems];
-    int rk[kRcItems];
-#pragma unroll
-    for (int j = 0; j < kRcItems; ++j) eq[j] = !v.held[j] && rc_key(v.h[j], v.lu[j], lu_min) == T;
-    block_slot_rank(eq, rk, s_red);
-    int d[1] = {0};
-#pragma unroll
-    for (int j = 0; j < kRcItems; ++j) {
-      if (eq[j] && rk[j] < r_cut) {
-        d[0] += demotable(a, v.h[j]);
-        if (rk[j] == r_cut - 1) s_hit[0] = item_slot(base, j);
+  };
+  // 1. T's remaining digits: few staged candidates are ranked directly
+  //    (keys below and keys at most each one), more take a digit per pass
+  if (!fail && has_sub && shift > 0 && in_lds && n_staged <= kTieLds) {
+    if (t == 0) s_found[0] = -1;
+    __syncthreads();
+    for (int i = t; i < n_staged; i += kBlock) {
+      const unsigned long long ki = s_skey[i];
+      int lt = 0, le = 0;
+      for (int j = 0; j < n_staged; ++j) {
+        const unsigned long long kj = s_skey[j];
+        lt += kj < ki ? 1 : 0;
+        le += kj <= ki ? 1 : 0;
+      }
+      if (rank >= lt && rank < le) {  // every writer holds the same key and rank
+        s_found[0] = i;
+        s_found[1] = rank - lt;
       }
     }
-    block_sum<1, int>(d, s_red);
-    tie_slot = s_hit[0];
-    dem_cut = d[0];
+    __syncthreads();
+    if (s_found[0] < 0) {
+      fail = true;
+    } else {
+      T = s_skey[s_found[0]];
+      rank = s_found[1];
+      shift = 0;
+    }
+    __syncthreads();
   }
-  // 2: offsets, in tile order
-  int sums[2] = {0, 0};
-  for (int t = t0; t < t1; ++t) {
-    const int4 q = load_rec(rec64, t);
-    sums[0] += q.x + (t < cut ? q.y : (t == cut ? r_cut : 0));
-    sums[1] += q.z + (t < cut ? q.w : (t == cut ? dem_cut : 0));
+  while (!fail && has_sub && shift > 0) {
+    const int d = min(shift, kDigitN), s = shift - d;
+    const unsigned m = (1u << d) - 1u;
+    for (int b = t; b < kRcBins; b += kBlock) s_hist[b] = 0u;
+    __syncthreads();
+    const unsigned long long hi = shr64(T, shift);
+    for_matching([&](unsigned, unsigned long long k) {
+      if (shr64(k, shift) == hi) atomicAdd(&s_hist[(unsigned)(k >> s) & m], 1u);
+    });
+    __syncthreads();
+    unsigned v[kSelBins];
+#pragma unroll
+    for (int j = 0; j < kSelBins; ++j) v[j] = s_hist[t * kSelBins + j];
+    const Hit h = find_rank(v, rank, s_scan, s_found);
+    if (h.bin < 0) {
+      fail = true;
+      break;
+    }
+    T |= (unsigned long long)h.bin << s;
+    rank = h.rank;
+    shift = s;
   }
-  int tot[2];
-  block_exclusive_scan<2, int>(sums, tot, s_red);
-  int off_sel = sums[0], off_dem = sums[1];
-  for (int t = t0; t < t1; ++t) {
-    const int4 q = load_rec(rec64, t);
-    const int ns = q.x + (t < cut ? q.y : (t == cut ? r_cut : 0));
-    const int nd = q.z + (t < cut ? q.w : (t == cut ? dem_cut : 0));
-    a.w.tile[t] = make_int4(off_sel, off_dem, ns, nd);
-    off_sel += ns;
-    off_dem += nd;
+  // 2. the candidates on T's first digits, counted against T
+  if (!fail && has_sub) {
+    for_matching([&](unsigned e, unsigned long long k) {
+      if (k <= T) count_in_tile(a.w.off, e, k < T);
+    });
+    wait_stores();
   }
-  if (threadIdx.x == 0) {
-    RcPlan *W = a.w.plan;
-    W->tie_slot = tie_slot;
-    if (tot[0] != P->total || tot[1] > a.max_out) {  // must reclaim exactly total
+  __syncthreads();
+  acquire_agent();  // the counters are read back from memory
+
+  // 3. per tile: the certain ones join the counts; the tile holding the
+  //    take-th key T in slot order
+  const int take = rank + 1;
+  int carry = 0;
+  if (t == 0) s_found[0] = -1;
+  for (int c0 = 0; c0 < tiles; c0 += kBlock) {
+    const int tile = c0 + t;
+    int4 q = make_int4(0, 0, 0, 0);
+    if (tile < tiles) {
+      const int4 r = a.w.rec[tile];
+      q = a.w.off[tile];
+      q.x += r.y;  // certainly reclaimed: below T
+      q.z += r.w;
+      if (!cached) q.y += r.z;  // empty slots only: every candidate is key 0 = T, none demoted
+      if (tiles <= kTilesLds) s_q[tile] = q;
+      else a.w.off[tile] = q;
+    }
+    int ex[1] = {q.y}, tot[1];
+    block_exclusive_scan<1, int>(ex, tot, s_scan);
+    if (take > carry + ex[0] && take <= carry + ex[0] + q.y) {
+      s_found[0] = tile;
+      s_found[1] = take - carry - ex[0];  // keys T taken in that tile
+    }
+    carry += tot[0];
+  }
+  __syncthreads();
+  const int cut = s_found[0], r_cut = take > 0 ? s_found[1] : 0;
+  if (take > 0 && cut < 0) fail = true;
+
+  // 4. inside the cut tile: the slot of its r_cut-th key T, and how many of
+  //    its first r_cut keys T are demoted (wave 0, 64 entries per round)
+  int tie_slot = -1, dem_cut = 0;
+  __syncthreads();
+  if (t == 0) s_found[2] = -1;
+  __syncthreads();
+  if (!fail && cut >= 0 && in_lds && n_staged <= kTieLds) {
+    // every candidate equal to T is staged: rank the cut tile's by slot
+    if (t == 0) s_found[1] = 0;
+    __syncthreads();
+    for (int i = t; i < n_staged; i += kBlock) {
+      const int slot = (int)(s_sent[i] & kEntSlot);
+      if (s_skey[i] != T || slot / kRcTile != cut) continue;
+      int before = 0;
+      for (int j = 0; j < n_staged; ++j) {
+        const int sj = (int)(s_sent[j] & kEntSlot);
+        before += (s_skey[j] == T && sj / kRcTile == cut && sj < slot) ? 1 : 0;
+      }
+      if (before < r_cut && (s_sent[i] & kEntDem)) atomicAdd(&s_found[1], 1);
+      if (before == r_cut - 1) s_found[2] = slot;
+    }
+    __syncthreads();
+    tie_slot = s_found[2];
+    dem_cut = s_found[1];
+    if (tie_slot < 0) fail = true;
+  } else if (!fail && cut >= 0) {
+    if (t < 64) {
+      const int4 r = a.w.rec[cut];
+      const int end = r.x + r.y + r.z;
+      int seen = 0, dsum = 0;
+      for (int i0 = r.x; i0 < end && seen < r_cut; i0 += 64) {
+        const int i = i0 + t;
+        unsigned e = 0u;
+        bool eq = false;
+        if (i < end) {
+          e = ent[i];
+          eq = !(e & kEntSure) && key[i] == T;
+        }
+        const uint64_t mk = __ballot(eq);
+        const int before = seen + rank_in_mask(mk);
+        const bool taken = eq && before < r_cut;
+        dsum += (int)wave_sum((unsigned)(taken && (e & kEntDem) ? 1 : 0));
+        if (taken && before == r_cut - 1) s_found[2] = (int)(e & kEntSlot);
+        seen += __builtin_popcountll(mk);
+      }
+      if (t == 0) s_found[1] = dsum;
+    }
+    __syncthreads();
+    tie_slot = s_found[2];
+    dem_cut = s_found[1];
+    if (tie_slot < 0) fail = true;
+  }
+
+  // 5. output offsets, in tile order
+  int carry_s = 0, carry_d = 0;
+  for (int c0 = 0; c0 < tiles; c0 += kBlock) {
+    const int tile = c0 + t;
+    int v[2] = {0, 0};
+    if (tile < tiles) {
+      const int4 q = tiles <= kTilesLds ? s_q[tile] : a.w.off[tile];
+      v[0] = q.x + (tile < cut ? q.y : (tile == cut ? r_cut : 0));
+      v[1] = q.z + (tile < cut ? q.w : (tile == cut ? dem_cut : 0));
+    }
+    int ex[2] = {v[0], v[1]}, tot[2];
+    block_exclusive_scan<2, int>(ex, tot, s_scan);
+    if (tile < tiles) a.w.off[tile] = make_int4(carry_s + ex[0], carry_d + ex[1], v[0], v[1]);
+    carry_s += tot[0];
+    carry_d += tot[1];
+  }
+  if (t == 0) {
+    if (fail || carry_s != P->total || carry_d > a.max_out) {  // must reclaim exactly total
       store_agent(a.status, (int)CASCADE_EINTERNAL);
-      W->ok = 0;
-    } else if (a.n_out_dev) {
-      store_agent(a.n_out_dev, tot[1]);
+      P->ok = 0;
+    } else {
+      P->thresh = T;
+      P->tie_slot = tie_slot;
+      if (a.n_out_dev) store_agent(a.n_out_dev, carry_d);
     }
+    for (int g = 0; g < kListGroups; ++g) a.w.count[g * kCountStride] = 0u;  // free again
+    *a.w.stage_n = 0u;
   }
 }
 
 // ---------------------------------------------------------------- writes
 
-// Tiles holding reclaimed slots write them (ascending: freed, then placed)
-// and their demoted blocks at the offsets the counts gave.
+// A workgroup per tile with reclaimed slots: their positions in slot order
+// (flags staged in LDS from the tile's chunk), then for position p of the
+// reclaimed list: freed[p] or placed[p - need], the demoted block into
+// outgoing, the index bits (the old block leaves this tier, a demoted one
+// joins the next) and the slot's new contents.
 __global__ __launch_bounds__(kBlock) void rc_write_kernel(RcArgs a) {
-  __shared__ int s_red[kWaves];
+  __shared__ unsigned s_flagw[kRcTile / 4];
+  __shared__ unsigned s_ipos[kRcTile];
+  __shared__ int s_rank[kWaves];
   const RcPlan *P = a.w.plan;
   if (!P->ok) return;
-  const int4 rec = a.w.tile[blockIdx.x];
-  if (rec.z == 0) return;  // nothing reclaimed here (so nothing demoted either)
-  const unsigned long long T = P->prefix, lu_min = P->lu_min;
+  const int tile = blockIdx.x, t = threadIdx.x;
+  const int4 o = a.w.off[tile], r = a.w.rec[tile];  // requested together
+  if (o.z == 0) return;  // nothing reclaimed here (so nothing demoted either)
+  const unsigned long long T = P->thresh;
   const int tie_slot = P->tie_slot, need = a.need, total = P->total;
-  const int base = slot_base(blockIdx.x);
-  Slots8 v;
-  load8(a, base, v);
+  const int tile0 = tile * kRcTile;
+  unsigned char *s_flag = reinterpret_cast<unsigned char *>(s_flagw);
+  for (int i = t; i < kRcTile / 4; i += kBlock) s_flagw[i] = 0u;
+  __syncthreads();
+  for (int i = r.x + t; i < r.x + r.y + r.z; i += kBlock) {
+    const unsigned e = a.w.ent[i];
+    const int slot = (int)(e & kEntSlot);
+    const unsigned long long k = a.w.key[i];
+    const bool sel = (e & kEntSure) || k < T || (k == T && slot <= tie_slot);
+    const int loc = slot - tile0;
+    if (sel && (unsigned)loc < (unsigned)kRcTile) {
+      s_flag[loc] = (unsigned char)(1u | ((e & kEntDem) ? 2u : 0u));
+      s_ipos[loc] = a.w.pos[i];
+    }
+  }
+  __syncthreads();
+  const int base = slot_base(tile);
   bool sel[kRcItems], dem[kRcItems];
 #pragma unroll
   for (int j = 0; j < kRcItems; ++j) {
-    const unsigned long long k = rc_key(v.h[j], v.lu[j], lu_min);
-    sel[j] = !v.held[j] && (k < T || (k == T && item_slot(base, j) <= tie_slot));
-    dem[j] = sel[j] && demotable(a, v.h[j]);
+    const unsigned f = s_flag[item_slot(base, j) - tile0];
+    sel[j] = (f & 1u) != 0u;
+    dem[j] = (f & 2u) != 0u;
   }
   int rs[kRcItems], rd[kRcItems];
-  const int n_sel = block_slot_rank(sel, rs, s_red);
-  const int n_dem = block_slot_rank(dem, rd, s_red);
-  bool bad = n_sel != rec.z || n_dem != rec.w;
+  const int n_sel = block_slot_rank(sel, rs, s_rank);
+  const int n_dem = block_slot_rank(dem, rd, s_rank);
+  if (n_sel != o.z || n_dem != o.w || o.x + n_sel > total || o.y + n_dem > a.max_out) {
+    if (t == 0) store_agent(a.status, (int)CASCADE_EINTERNAL);
+    return;  // the counts disagree: this tile writes nothing
+  }
 #pragma unroll
   for (int j = 0; j < kRcItems; ++j) {
+    if (!sel[j]) continue;
     const int slot = item_slot(base, j);
-    if (sel[j]) {
-      const int p = rec.x + rs[j];
-      if (p < need) a.freed[p] = slot;
-      else if (p < total) a.placed[p - need] = slot;
-      else bad = true;
-    }
+    const int p = o.x + rs[j];
+    const unsigned long long old = a.hash[slot];
+    const long long old_lu = a.lu[slot];
+    const unsigned ipos = s_ipos[item_slot(base, j) - tile0];  // found by the compaction
+    IndexSlot *e = nullptr;
+    if (ipos == kFindPos) e = index_find(a.index, a.index_mask, old);
+    else if (ipos != kNoPos && a.index) e = a.index + ipos;
     if (dem[j]) {
-      const int q = rec.y + rd[j];
-      if (q < a.max_out) {
-        cascade_demotion_t d;
-        d.hash = v.h[j];
-        d.last_use_ns = v.lu[j];
-        d.src_slot = slot;
-        d.pad = 0;
-        a.outgoing[q] = d;
-      } else {
-        bad = true;
-      }
+      cascade_demotion_t d;
+      d.hash = old;
+      d.last_use_ns = old_lu;
+      d.src_slot = slot;
+      d.pad = 0;
+      a.outgoing[o.y + rd[j]] = d;
+      if (e) atomicOr(&e->tiers, 1u << (a.tier + 1));
     }
-  }
-  if (bad) store_agent(a.status, (int)CASCADE_EINTERNAL);
-}
-
-// ---------------------------------------------------------------- updates
-
-// Position p of the reclaimed list: the old block leaves this tier in the
-// index and the slot takes its new contents; position p of the outgoing list:
-// the demoted block joins the next tier in the index.
-__global__ __launch_bounds__(kBlock) void rc_update_kernel(RcArgs a) {
-  const RcPlan *P = a.w.plan;
-  if (!P->ok || status_bad(a.status)) return;
-  const int p = blockIdx.x * kBlock + threadIdx.x;
-  const int total = P->total, need = a.need;
-  unsigned long long *hash = a.hash;
-  long long *lu = a.lu;
-  if (p < total) {
-    const int s = p < need ? a.freed[p] : a.placed[p - need];
-    if ((unsigned)s >= (unsigned)a.n) return;  // only after a failed check, reported already
-    const unsigned long long old = hash[s];
-    if (old != 0ull && a.index) {
-      IndexSlot *e = index_find(a.index, a.index_mask, old);
-      if (e) atomicAnd(&e->tiers, ~(1u << a.tier));
-    }
+    if (e) atomicAnd(&e->tiers, ~(1u << a.tier));
     if (p < need) {
-      hash[s] = 0ull;
-      lu[s] = 0ll;
+      a.freed[p] = slot;
+      a.hash[slot] = 0ull;
+      a.lu[slot] = 0ll;
     } else {
       const cascade_demotion_t in = a.incoming[p - need];
-      hash[s] = in.hash;
-      lu[s] = in.last_use_ns;
-    }
-  }
-  if (a.tier < 2 && a.index) {
-    const int n_out = *a.n_out_dev;
-    if (p < n_out) {
-      IndexSlot *e = index_find(a.index, a.index_mask, a.outgoing[p].hash);
-      if (e) atomicOr(&e->tiers, 1u << (a.tier + 1));
+      a.placed[p - need] = slot;
+      a.hash[slot] = in.hash;
+      a.lu[slot] = in.last_use_ns;
     }
   }
 }
@@ -754,17 +1154,12 @@ extern "C" int cascade_tier_reclaim(int32_t tier, const cascade_tier_table_t *ta
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int tiles = std::max(1, tiles_of(n));
-  const int total_cap = (int)std::min<long long>((long long)need + max_incoming, n);
   hipLaunchKernelGGL(rc_count_kernel, dim3(std::min(tiles, kRcGridCount)), dim3(kBlock), 0, s,
                      a);
-  for (int p = 0; p < kRcPasses; ++p)
-    hipLaunchKernelGGL(rc_pass_kernel, dim3(std::min(tiles, kRcGridPass)), dim3(kBlock), 0, s,
-                       a);
-  hipLaunchKernelGGL(rc_tiles_kernel, dim3(std::min(tiles, kRcGridCount)), dim3(kBlock), 0, s,
+  hipLaunchKernelGGL(rc_hist_kernel, dim3(std::min(tiles, kRcGridHist)), dim3(kBlock), 0, s, a);
+  hipLaunchKernelGGL(rc_compact_kernel, dim3(std::min(tiles, kRcGridCompact)), dim3(kBlock), 0, s,
                      a);
+  hipLaunchKernelGGL(rc_select_kernel, dim3(kSelGrid), dim3(kBlock), 0, s, a);
   hipLaunchKernelGGL(rc_write_kernel, dim3(tiles), dim3(kBlock), 0, s, a);
-  if (total_cap > 0)
-    hipLaunchKernelGGL(rc_update_kernel, dim3((total_cap + kBlock - 1) / kBlock), dim3(kBlock),
-                       0, s, a);
   return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
 }

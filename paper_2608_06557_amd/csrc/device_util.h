@@ -204,18 +204,24 @@ __device__ __forceinline__ void acquire_agent() {
 // Called by one thread per workgroup once its results are stored: true for
 // the last workgroup of the grid to arrive (with an acquire fence in the
 // calling thread; the others call acquire_agent() after the barrier that
-// shares the answer).  Two levels of counters (16
-// groups, then one) keep the atomics on any one address to a few dozen,
-// where a single counter would serialize one per workgroup.  Counters are
-// reset by the workgroup that completes them, so every launch finds them at
-// zero.  `tk` holds (kTicketGroups + 1) * kTicketStride words.
+// shares the answer).  Above kTicketFlat workgroups, two levels of counters
+// (16 groups, then one) keep the atomics on any one address to a few dozen,
+// where a single counter would serialize one per workgroup; up to it, one
+// counter and one round trip.  Counters are reset by the workgroup that
+// completes them, so every launch finds them at zero.  `tk` holds
+// (kTicketGroups + 1) * kTicketStride words.
+constexpr unsigned kTicketFlat = 64;
 __device__ __forceinline__ bool last_workgroup(unsigned *tk) {
-  const unsigned G = gridDim.x, groups = min(G, (unsigned)kTicketGroups);
+  const unsigned G = gridDim.x, groups = G <= kTicketFlat ? 1u : min(G, (unsigned)kTicketGroups);
   const unsigned g = blockIdx.x % groups;
   const unsigned size = (G - g + groups - 1) / groups;
   unsigned *c = tk + g * kTicketStride;
   if (atomicAdd(c, 1u) != size - 1) return false;
   store_agent(c, 0u);
+  if (groups == 1u) {
+    acquire_agent();
+    return true;
+  }
   unsigned *top = tk + kTicketGroups * kTicketStride;
   if (atomicAdd(top, 1u) != groups - 1) return false;
   store_agent(top, 0u);
