@@ -334,6 +334,9 @@ def parse():
                          "16384 = FP8 KV")
     ap.add_argument("--copy", default="fused", choices=["fused", "separate"],
                     help="one cascade_pack_unpack launch, or cascade_pack then cascade_unpack")
+    ap.add_argument("--prefix-groups", action="store_true",
+                    help="pass each request's shared-prefix family (config 3) as prefix_group, "
+                         "so restores of a shared prefix are shared within the step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time spent on the oracle baseline")
@@ -427,7 +430,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cfg = args.config
-    w = synth.make_workload(cfg)
+    w = synth.make_workload(cfg, prefix_groups=args.prefix_groups)
     c = synth.CONFIGS[cfg]
     geom = (synth.kv_geometry(c["model"], c["pool"], args.layout, args.chunk_bytes)
             if args.chunk_bytes else synth.kv_geometry(c["model"], c["pool"], args.layout))
@@ -585,7 +588,10 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int64",
         "data": "synthetic",
-        "config": {"workload": WORKLOADS[cfg], "requests": n,
+        "config": {"workload": WORKLOADS[cfg] + (", shared-prefix restores shared within "
+                                                 "the step (prefix_group)"
+                                                 if args.prefix_groups else ""),
+                   "requests": n,
                    "kv_layout": args.layout, "pool_blocks": nb,
                    "chunk_bytes": geom["chunk_bytes"],
                    "block_bytes": block_bytes, "token_cap": c["token_cap"],
