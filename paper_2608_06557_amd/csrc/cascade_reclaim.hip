@@ -900,17 +900,16 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
   const int take = rank + 1;
   int carry = 0;
   if (t == 0) s_found[0] = -1;
-  for (int c0 = 0; c0 < tiles; c0 += kBlock) {
-    const int tile = c0 + t;
-    int4 q = make_int4(0, 0, 0, 0);
+  // one chunk of kBlock tiles, in tile order (called by every thread)
+  auto tile_chunk = [&](int tile, int4 q, const int4 &r) {
     if (tile < tiles) {
-      const int4 r = a.w.rec[tile];
-      q = a.w.off[tile];
       q.x += r.y;  // certainly reclaimed: below T
       q.z += r.w;
       if (!cached) q.y += r.z;  // empty slots only: every candidate is key 0 = T, none demoted
       if (tiles <= kTilesLds) s_q[tile] = q;
       else a.w.off[tile] = q;
+    } else {
+      q = make_int4(0, 0, 0, 0);
     }
     int ex[1] = {q.y}, tot[1];
     block_exclusive_scan<1, int>(ex, tot, s_scan);
@@ -919,6 +918,26 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
       s_found[1] = take - carry - ex[0];  // keys T taken in that tile
     }
     carry += tot[0];
+  };
+  if (tiles <= kTilesLds) {
+    // every chunk's records requested at once
+    constexpr int kChunks = kTilesLds / kBlock;
+    int4 qa[kChunks], ra[kChunks];
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const int tile = c * kBlock + t;
+      qa[c] = tile < tiles ? a.w.off[tile] : make_int4(0, 0, 0, 0);
+      ra[c] = tile < tiles ? a.w.rec[tile] : make_int4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c)
+      if (c * kBlock < tiles) tile_chunk(c * kBlock + t, qa[c], ra[c]);
+  } else {
+    for (int c0 = 0; c0 < tiles; c0 += kBlock) {
+      const int tile = c0 + t;
+      const int4 r = tile < tiles ? a.w.rec[tile] : make_int4(0, 0, 0, 0);
+      tile_chunk(tile, tile < tiles ? a.w.off[tile] : make_int4(0, 0, 0, 0), r);
+    }
   }
   __syncthreads();
   const int cut = s_found[0], r_cut = take > 0 ? s_found[1] : 0;
