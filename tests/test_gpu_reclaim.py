@@ -144,6 +144,31 @@ def test_heavy_ties_and_extreme_stamps(dev):
         assert_chain_same(w, g, rc, outs, masks, stamps)
 
 
+def test_threshold_prefix_shared_by_more_than_the_stage(dev):
+    # NVMe: 80 % of the slots share one stamp, the oldest, and the rest lie
+    # far above it, so the threshold's key and its first 20 bits are shared by
+    # about 240 000 candidates: more than the select kernel stages, so it
+    # resolves them from the whole list
+    rng = np.random.default_rng(71)
+    w = small(71, (3000, 4000, 300_000), (600, 300, 5000), empty=(0.05, 0.05, 0.0))
+    t = w["tables"][2]
+    n = len(t["block_hash"])
+    t["last_use_ns"] = np.where(rng.random(n) < 0.8, 1_000_000,
+                                rng.integers(2_000_000, 2 ** 40, n)).astype(np.int64)
+    g, rc, outs, masks, _ = run_both(dev, w)
+    assert rc == 0
+    assert_chain_same(w, g, rc, outs, masks, "shared threshold prefix")
+
+
+def test_more_tiles_than_the_select_kernel_keeps_in_lds(dev):
+    # 2100 tiles of 2048 slots (above 2048): the select kernel keeps its
+    # per-tile counts in memory instead of LDS
+    w = small(73, (3000, 4000, 4_300_000), (600, 300, 3000), empty=(0.05, 0.05, 0.0))
+    g, rc, outs, masks, _ = run_both(dev, w)
+    assert rc == 0
+    assert_chain_same(w, g, rc, outs, masks, "2100 tiles")
+
+
 def test_every_free_slot_reclaimed(dev):
     w = small(21, (3000, 5000, 5000), (0, 0, 0))
     free0 = int((w["tables"][0]["held"] == 0).sum())
