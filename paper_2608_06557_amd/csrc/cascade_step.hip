@@ -94,6 +94,17 @@ __device__ __forceinline__ int rec_tier(int w) { return (w >> 22) & 3; }
 __device__ __forceinline__ int rec_grp(int w) { return (w >> 24) & 3; }
 __device__ __forceinline__ int rec_offl(int w) { return (w >> 26) & 1; }
 __device__ __forceinline__ int rec_decnb(int w) { return (w >> 27) & 1; }
+// Slot of a member's (prefix group, priority group) in the shared-prefix
+// leader tables.
+__device__ __forceinline__ int share_slot(const int4 &r) {
+  return 2 * r.z + (rec_grp(r.w) == 2 ? 1 : 0);
+}
+// A member with a restore want marks its group's leader table with its
+// position p: the table keeps the largest n - p, so the first such position.
+__device__ __forceinline__ void share_mark(unsigned *lead, const int4 &r, int p, int n) {
+  if (lead && rec_member(r.w) && r.x > 0 && (unsigned)r.z < (unsigned)n)
+    atomicMax(lead + share_slot(r), (unsigned)(n - p));
+}
 
 // Totals of one eval workgroup (64 bytes).
 struct Partial {
@@ -764,7 +775,8 @@ __device__ __forceinline__ unsigned paired_look_back(const unsigned *status, int
 // decoupled look-back; keys are reordered in LDS and written out in runs of
 // equal digits.  The last pass writes the sorted order with each request's
 // scan record (gathered while the tile is ranked) instead of
-// the keys, and adds every scan tile's level-1 totals.  The k-th pass reads
+// the keys, adds every scan tile's level-1 totals and, with shared prefixes,
+// marks each prefix group's leader position.  The k-th pass reads
 // buffer k & 1, so the tile's keys are requested at once, in parallel with
 // the plan.  Workgroup b sorts tile b: workgroups are dispatched in index
 // order (on each XCD), so every tile a look-back waits on belongs to a
@@ -774,7 +786,8 @@ template <int kK, int kItems>
 __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
     int n, int passes, Ctl *ctl, int *info, unsigned long long *keys_a,
     unsigned long long *keys_b, unsigned *vals_a, unsigned *vals_b, unsigned *status,
-    const int4 *__restrict__ rec, Sorted srt, unsigned *__restrict__ l1_tot) {
+    const int4 *__restrict__ rec, Sorted srt, unsigned *__restrict__ l1_tot,
+    unsigned *share_lead) {
   constexpr int kTile = kSortBlock * kItems;  // keys per tile
   __shared__ unsigned long long s_keys[kTile];
   __shared__ unsigned s_vals[kTile];
@@ -854,6 +867,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
       unsigned c[kL1] = {0, 0, 0, 0, 0};
       for (int p = p0 + t; p < min(n, p0 + kSub); p += kSortBlock) {
         const int4 r = rec[p];
+        share_mark(share_lead, r, p, n);
         const bool rp = rec_state(r.w) == CASCADE_RUNNING_PREFILL;
         const unsigned h = rp ? (unsigned)rec_held(r.w) : 0u;
         c[0] += (unsigned)rec_want(r);
@@ -999,6 +1013,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_pass_kernel(
         r = s_rec[s];
         srt.order[o] = s_vals[s];
         srt.rec[o] = r;
+        share_mark(share_lead, r, o, n);
       }
       l1_contrib(s_l1, o >= 0 ? o / kScanTile : -1, r);
     } else if (o >= 0) {
@@ -2129,13 +2144,12 @@ __device__ __forceinline__ void load_sorted(int n, const Sorted &srt, unsigned (
 // group, the first queued DRAM/NVMe member of a prefix group with a restore
 // want leads and restores under the link cap; every later such member of
 // the group follows and references min(leader's restore, own prefix) blocks
-// of it, taking nothing from the cap).  Three launches between the sort and
-// the scan, each over the scan tiles' positions: the leaders' positions
-// (share_lead_kernel), the followers' wants taken off each tile's level-1
-// want total (share_drop_kernel), then the leaders' restores and the
-// followers' rewritten records (share_kernel).  The table of leaders holds
-// n - position (0: none yet), so the maximum is the first position.
-
+// of it, taking nothing from the cap).  The last radix pass marks each
+// group's leader position as it writes the order (share_mark: the table
+// holds n - position, 0 for none, so the maximum is the first position);
+// then one launch over the scan tiles (share_kernel) takes the followers'
+// wants off the link cap, lets the leaders restore and rewrites the
+// followers' records.
 // The request index and scan record at position p: the sorted buffers, or
 // the identity order when no radix pass moved data.
 __device__ __forceinline__ void position_rec(int p, int nact, const Sorted &srt,
@@ -2148,29 +2162,6 @@ __device__ __forceinline__ void position_rec(int p, int nact, const Sorted &srt,
     r = srt.rec[p];
   }
 }
-// Slot of a member's (prefix group, priority group) in the leader tables.
-__device__ __forceinline__ int share_slot(const int4 &r) {
-  return 2 * r.z + (rec_grp(r.w) == 2 ? 1 : 0);
-}
-
-__global__ __launch_bounds__(kBlock) void share_lead_kernel(int n, const Ctl *ctl,
-                                                            const int *info, Sorted srt,
-                                                            const int4 *__restrict__ rec,
-                                                            unsigned *lead) {
-  if (bad_status(load_agent(info))) return;
-  const int nact = (int)ctl->nact;
-  const int p0 = (int)blockIdx.x * kScanTile + (int)threadIdx.x * kScanItems;
-#pragma unroll
-  for (int j = 0; j < kScanItems; ++j) {
-    const int p = p0 + j;
-    if (p >= n) break;
-    int ix;
-    int4 r;
-    position_rec(p, nact, srt, rec, ix, r);
-    if (rec_member(r.w) && r.x > 0 && (unsigned)r.z < (unsigned)n)
-      atomicMax(lead + share_slot(r), (unsigned)(n - p));
-  }
-}
 
 // Is position p's member a follower (behind its group's leader)?
 __device__ __forceinline__ bool share_follows(const int4 &r, int p, int n,
@@ -2181,49 +2172,28 @@ __device__ __forceinline__ bool share_follows(const int4 &r, int p, int n,
   return enc != 0 && p > n - (int)enc;
 }
 
-__global__ __launch_bounds__(kBlock) void share_drop_kernel(int n, Ctl *ctl, const int *info,
-                                                            Sorted srt,
-                                                            const int4 *__restrict__ rec,
-                                                            const unsigned *__restrict__ lead,
-                                                            unsigned *adj) {
-  __shared__ long long s_red[kWaves * 2];
-  if (bad_status(load_agent(info))) return;
-  const int nact = (int)ctl->nact;
-  const int tile = (int)blockIdx.x;
-  const int p0 = tile * kScanTile + (int)threadIdx.x * kScanItems;
-  long long v[2] = {0, 0};  // the tile's followers' wants, those in groups 0-1
-#pragma unroll
-  for (int j = 0; j < kScanItems; ++j) {
-    const int p = p0 + j;
-    if (p >= n) break;
-    int ix;
-    int4 r;
-    position_rec(p, nact, srt, rec, ix, r);
-    unsigned enc = 0;
-    if (share_follows(r, p, n, lead, &enc)) {
-      v[0] += r.x;
-      v[1] += rec_grp(r.w) <= 1 ? r.x : 0;
-    }
-  }
-  block_sum<2>(v, s_red);
-  if (threadIdx.x == 0) {
-    adj[(size_t)tile * 2] = (unsigned)v[0];   // below 2^31: 1024 wants below 2^18
-    if (v[1]) atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->want1_sub),
-                        (unsigned long long)v[1]);
-  }
-}
-
+// One workgroup per scan tile.  The tile's followers' wants are published at
+// once (pub[tile] = wants << 1 | 1, and adj[2 tile] for the scan); the link-cap
+// prefix before the tile is the earlier tiles' level-1 want totals less
+// their published followers' wants (a look-back over lower tiles only, which
+// publish before they wait on anything).  Then the tile's leaders publish
+// their restore blocks, and its followers wait for their leader's.
 __global__ __launch_bounds__(kBlock) void share_kernel(int n, int n_tiles, int bt, int max_move,
                                                        Ctl *ctl, int *info, Sorted srt,
                                                        int4 *__restrict__ rec,
                                                        const unsigned *__restrict__ l1_tot,
                                                        const unsigned *__restrict__ lead,
-                                                       unsigned *rl, unsigned *adj) {
+                                                       unsigned *rl, unsigned *adj,
+                                                       unsigned *pub) {
   __shared__ long long s_red[kWaves * 3];
   __shared__ unsigned s_scan[kWaves];
-  if (bad_status(load_agent(info))) return;
-  const int nact = (int)ctl->nact;
   const int tile = (int)blockIdx.x;
+  if (bad_status(load_agent(info))) {
+    // a failed step: publish "no followers", so no later tile waits on this one
+    if (threadIdx.x == 0) store_agent(pub + tile, 1u);
+    return;
+  }
+  const int nact = (int)ctl->nact;
   const int p0 = tile * kScanTile + (int)threadIdx.x * kScanItems;
   int ix[kScanItems];
   int4 r4[kScanItems];
@@ -2233,24 +2203,48 @@ __global__ __launch_bounds__(kBlock) void share_kernel(int n, int n_tiles, int b
     r4[j] = make_int4(0, 0, 0, 0);
     if (p0 + j < n) position_rec(p0 + j, nact, srt, rec, ix[j], r4[j]);
   }
-  // the link-cap prefix before this tile: the earlier tiles' want totals
-  // without their followers' wants
-  long long pre[1] = {0};
-  for (int k = (int)threadIdx.x; k < tile; k += kBlock)
-    pre[0] += (long long)l1_tot[(size_t)k * kL1] - (long long)adj[(size_t)k * 2];
-  block_sum<1>(pre, s_red);
-  // this tile's wants in position order (a follower wants nothing)
+  // this tile's wants in position order (a follower wants nothing), and its
+  // followers' wants, published at once
   unsigned enc[kScanItems];
   bool fol[kScanItems];
   unsigned wsum[1] = {0}, wtot[1];
   int wj[kScanItems];
+  long long fw[2] = {0, 0};  // the followers' wants, those in groups 0-1
 #pragma unroll
   for (int j = 0; j < kScanItems; ++j) {
     enc[j] = 0;
     fol[j] = ix[j] >= 0 && share_follows(r4[j], p0 + j, n, lead, &enc[j]);
     wj[j] = (ix[j] >= 0 && !fol[j]) ? rec_want(r4[j]) : 0;
     wsum[0] += (unsigned)wj[j];
+    if (fol[j]) {
+      fw[0] += r4[j].x;
+      fw[1] += rec_grp(r4[j].w) <= 1 ? r4[j].x : 0;
+    }
   }
+  block_sum<2>(fw, s_red);
+  if (threadIdx.x == 0) {
+    // below 2^31: 1024 wants below 2^18
+    store_agent(pub + tile, ((unsigned)fw[0] << 1) | 1u);
+    adj[(size_t)tile * 2] = (unsigned)fw[0];
+    if (fw[1]) atomicAdd(reinterpret_cast<unsigned long long *>(&ctl->want1_sub),
+                         (unsigned long long)fw[1]);
+  }
+  // the link-cap prefix before this tile: the earlier tiles' want totals
+  // without their followers' wants
+  long long pre[2] = {0, 0};  // the prefix, timeouts
+  for (int k = (int)threadIdx.x; k < tile; k += kBlock) {
+    unsigned v = load_agent(pub + k);
+    unsigned spins = 0;
+    while ((v & 1u) == 0u) {
+      if (++spins > kSpinLimit) break;
+      __builtin_amdgcn_s_sleep(1);
+      v = load_agent(pub + k);
+    }
+    if ((v & 1u) == 0u) pre[1] += 1;
+    pre[0] += (long long)l1_tot[(size_t)k * kL1] - (long long)(v >> 1);
+  }
+  block_sum<2>(pre, s_red);
+  if (pre[1] && threadIdx.x == 0) set_status(info, CASCADE_ETIMEOUT);
   block_exclusive_scan<1>(wsum, wtot, s_scan);
   // leaders publish their restore blocks (eq:max_restorable under the cap)
   long long wx = pre[0] + wsum[0];
@@ -2856,7 +2850,7 @@ __global__ __launch_bounds__(kBlock) void empty_step_kernel(int n_free, int num_
 struct Layout {
   size_t ctl = 0, scan1 = 0, scan2 = 0, sort_status = 0, partials = 0, keys_a = 0, keys_b = 0,
          vals_a = 0, vals_b = 0, rec = 0, s_order = 0, s_rec = 0, rp_list = 0, restore = 0,
-         tile_tot = 0, share_lead = 0, share_rl = 0, share_adj = 0, total = 0;
+         tile_tot = 0, share_lead = 0, share_rl = 0, share_pub = 0, share_adj = 0, total = 0;
   int sort_tiles = 0, scan_tiles = 0, eval_grid = 0;
 };
 
@@ -2888,10 +2882,12 @@ constexpr Layout make_layout(int32_t n) {
   L.restore = take(np * sizeof(RestoreEnt));
   L.tile_tot = take((size_t)L.scan_tiles * sizeof(TileTot));
   // shared prefixes: leader positions and published leader restores per
-  // (group, priority group), contiguous for eval's clear; per scan tile the
-  // followers' wants and shared tokens
+  // (group, priority group) and the tiles' published followers' wants,
+  // contiguous for eval's clear; per scan tile the followers' wants and
+  // shared tokens for the scan
   L.share_lead = take(np * 2 * 4);
   L.share_rl = take(np * 2 * 4);
+  L.share_pub = take((size_t)L.scan_tiles * 4);
   L.share_adj = take((size_t)L.scan_tiles * 2 * 4);
   L.total = off;
   return L;
@@ -2959,7 +2955,8 @@ int sort_passes(const cascade_params_t *p) {
 }
 
 typedef void (*RadixFn)(int, int, Ctl *, int *, unsigned long long *, unsigned long long *,
-                        unsigned *, unsigned *, unsigned *, const int4 *, Sorted, unsigned *);
+                        unsigned *, unsigned *, unsigned *, const int4 *, Sorted, unsigned *,
+                        unsigned *);
 static_assert(kMaxPasses == 8, "one radix kernel per pass");
 template <int kItems>
 constexpr RadixFn kRadixPasses[kMaxPasses] = {
@@ -3116,7 +3113,9 @@ int step_impl(const cascade_requests_t *rq, const cascade_block_table_t *bt,
   auto *share_lead = reinterpret_cast<unsigned *>(ws + L.share_lead);
   auto *share_rl = reinterpret_cast<unsigned *>(ws + L.share_rl);
   auto *share_adj = reinterpret_cast<unsigned *>(ws + L.share_adj);
-  // both share tables (2n words each), one 16-byte clear region
+  auto *share_pub = reinterpret_cast<unsigned *>(ws + L.share_pub);
+  // both share tables (2n words each) and the published wants, one 16-byte
+  // clear region
   const size_t clear2_vec = share ? (L.share_adj - L.share_lead) / 16 : 0;
 
   hipLaunchKernelGGL(eval_kernel, dim3(L.eval_grid), dim3(kBlock), 0, s, *rq, bt->row_offsets,
@@ -3137,16 +3136,11 @@ int step_impl(const cascade_requests_t *rq, const cascade_block_table_t *bt,
                        dim3(sort_tiles), dim3(kSortBlock), 0, s, n,
                        passes, ctl, out->info, keys_a, keys_b, vals_a, vals_b,
                        sort_status + (size_t)pass * sort_tiles * kMaxBins, rec, srt,
-                       l1_tot);
-  if (share) {
-    hipLaunchKernelGGL(share_lead_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, ctl,
-                       out->info, srt, rec, share_lead);
-    hipLaunchKernelGGL(share_drop_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, ctl,
-                       out->info, srt, rec, share_lead, share_adj);
+                       l1_tot, share ? share_lead : nullptr);
+  if (share)
     hipLaunchKernelGGL(share_kernel, dim3(L.scan_tiles), dim3(kBlock), 0, s, n, L.scan_tiles,
                        c.bt, c.max_move, ctl, out->info, srt, rec, l1_tot, share_lead, share_rl,
-                       share_adj);
-  }
+                       share_adj, share_pub);
   hipLaunchKernelGGL(scan_kernel, dim3(L.scan_tiles + kFinishGrid), dim3(kBlock), 0, s, n,
                      passes, L.scan_tiles, c, ctl, out->info, srt, rec, bt->slots,
                      ts->free_slots, o, rp_list, rlist, tile_tot, l1_tot,
