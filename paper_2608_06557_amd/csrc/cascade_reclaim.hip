@@ -10,18 +10,21 @@
 // slots per thread with 16-byte loads, three times per call:
 //
 //   rc_count_kernel    per-workgroup counts of empty / cached free slots and
-//                      the cached last-use range; the last workgroup checks
-//                      the call, sizes the key and writes the plan
+//                      the cached last-use range, and a share of the incoming
+//                      blocks' hashes checked; the last workgroup checks the
+//                      call, sizes the key and writes the plan
 //   rc_hist_kernel     (cached blocks needed) a histogram of the key's top
 //                      digit, 8 bits; the last workgroup finds the bucket
 //                      holding the threshold and the rank sought inside it
 //   rc_compact_kernel  per tile, in slot order: the slots certainly reclaimed
 //                      (empty ones, keys below the bucket) and the candidates
 //                      (keys inside it; with empty slots alone enough, the
-//                      empty slots), each with its key and whether it is
-//                      demoted (the index read once, before any update), in
-//                      one chunk of a list reserved with one atomic add; a
-//                      histogram of the candidates' next 12-bit digit
+//                      empty slots), each with its key and, on tiers 0 and 1,
+//                      its index slot and whether it is demoted (the index as
+//                      it was when the call began), in one chunk of a list
+//                      reserved with one atomic add on one of 16 region
+//                      counters; a histogram of the candidates' next 12-bit
+//                      digit
 //
 // Then, over the list only:
 //
@@ -36,7 +39,9 @@
 //   rc_write_kernel    a workgroup per tile with reclaimed slots: their
 //                      positions in slot order, the freed / placed / outgoing
 //                      entries, the index bit updates (clear this tier, set
-//                      the next for demoted blocks) and the slot-table writes
+//                      the next for demoted blocks) at the index slots the
+//                      compaction found (tier 2 looks them up here) and the
+//                      slot-table writes
 //
 // The plan lives in the caller's workspace; every kernel after the first reads
 // it and returns at once when the call failed or has nothing left to do, so
@@ -292,8 +297,6 @@ __device__ __forceinline__ int block_slot_rank(const bool (&f)[kRcItems], int (&
 }
 
 
-// Calls f(tile, slots) for this workgroup's tiles (grid-stride), loading the
-// next tile before working on the current one.
 // The workgroup's first tile (nothing is read past the table), loaded
 // before the kernel reads anything else, so the table loads do not wait for it.
 __device__ __forceinline__ Slots8 load_first(const RcArgs &a) {
@@ -301,6 +304,9 @@ __device__ __forceinline__ Slots8 load_first(const RcArgs &a) {
   load8(a, slot_base(blockIdx.x), v);
   return v;
 }
+// Calls f(tile, slots) for this workgroup's tiles (grid-stride), loading the
+// next tile before working on the current one; `first` is the first tile's
+// slots.
 template <typename F>
 __device__ __forceinline__ void for_tiles(const RcArgs &a, const Slots8 &first, F &&f) {
   const int tiles = max(1, tiles_of(a.n));
