@@ -11,12 +11,14 @@
 //
 //   rc_count_kernel    per-workgroup counts of empty / cached free slots and
 //                      the cached last-use range, and a share of the incoming
-//                      blocks' hashes checked; the last workgroup checks the
-//                      call, sizes the key and writes the plan
-//   rc_hist_kernel     (cached blocks needed) a histogram of the key's top
-//                      digit, 8 bits; the last workgroup finds the bucket
-//                      holding the threshold and the rank sought inside it
-//   rc_compact_kernel  per tile, in slot order: the slots certainly reclaimed
+//                      blocks' hashes checked
+//   rc_hist_kernel     every workgroup derives the plan from those counts
+//                      (the checks, the key's size; workgroup 0 stores it),
+//                      then, when cached blocks are needed, adds its tiles to
+//                      a histogram of the key's top digit, 8 bits
+//   rc_compact_kernel  every workgroup finds the bucket holding the threshold
+//                      in that histogram, then per tile, in slot order: the
+//                      slots certainly reclaimed
 //                      (empty ones, keys below the bucket) and the candidates
 //                      (keys inside it; with empty slots alone enough, the
 //                      empty slots), each with its key and, on tiers 0 and 1,
@@ -43,10 +45,13 @@
 //                      compaction found (tier 2 looks them up here) and the
 //                      slot-table writes
 //
-// The plan lives in the caller's workspace; every kernel after the first reads
-// it and returns at once when the call failed or has nothing left to do, so
-// the host launches a fixed sequence and never waits.  Counters and
-// histograms are reset by the workgroup that last uses them.
+// Values the next kernel needs are handed over by the kernel boundary, not
+// by a last workgroup: each kernel recomputes what it needs from the
+// previous one's output (the plan from the counts, the bucket from the
+// histogram).  The plan lives in the caller's workspace; every kernel after
+// the histogram reads it and returns at once when the call failed or has
+// nothing left to do, so the host launches a fixed sequence and never waits.
+// Counters and histograms are reset by the kernel after their last reader.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <stdint.h>
@@ -98,11 +103,11 @@ struct alignas(256) RcPlan {
   int width;      // bits of the key
   int shift;      // low bit of the top digit
   int dbits;      // width of the top digit
-  int rank;       // 0-based rank sought: among cached keys, then inside the bucket
-                  // (kModeEmpty: among empty slots)
+  int rank;       // 0-based rank sought among cached keys (kModeEmpty: among empty slots)
   int bucket;     // the top digit of the threshold key
+  int brank;      // the rank sought inside the bucket
   int tie_slot;   // last reclaimed slot with the threshold key (-1: none)
-  int pad[2];
+  int pad;
   unsigned long long lu_min;
   unsigned long long thresh;  // the threshold key T
 };
@@ -332,8 +337,6 @@ __device__ __forceinline__ void for_tiles(const RcArgs &a, F &&f) {
 __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
   __shared__ int s_red[kWaves * 3];
   __shared__ unsigned long long s_mm[kWaves * 2];
-  __shared__ bool s_last;
-  __shared__ int s_err;
   int cnt[3] = {0, 0, 0};  // empty free, cached free, bad data (negative last use, hash 0 in)
   unsigned long long mn = ~0ull, mx = 0ull;
   const int n_in_all = a.n_in_dev ? load_agent(a.n_in_dev) : 0;
@@ -363,39 +366,46 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
     s_mm[wave_id() * 2 + 1] = mx;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (threadIdx.x == 0) {  // read by the next kernel
     for (int w = 1; w < kWaves; ++w) {
       mn = min(mn, s_mm[w * 2]);
       mx = max(mx, s_mm[w * 2 + 1]);
     }
     RcPartial *p = a.w.partial + blockIdx.x;
-    store_agent(&p->n_empty, cnt[0]);
-    store_agent(&p->n_cached, cnt[1]);
-    store_agent(&p->bad, cnt[2]);
-    store_agent(&p->lu_min, mn);
-    store_agent(&p->lu_max, mx);
-    wait_stores();
-    s_last = last_workgroup(a.w.tickets);
+    p->n_empty = cnt[0];
+    p->n_cached = cnt[1];
+    p->bad = cnt[2];
+    p->lu_min = mn;
+    p->lu_max = mx;
   }
-  __syncthreads();
-  if (!s_last) return;
-  acquire_agent();
+}
 
-  // the last workgroup: totals and plan
-  const int status_was = load_agent(a.status);  // requested with the partials
+// The call's plan from the count kernel's partials, computed alike by every
+// workgroup that needs it: the checks (an earlier failure in the chain, bad
+// data, room), then which slots are reclaimed and the key's size.
+struct PlanCalc {
+  int err;   // 0, 1 (an earlier call failed) or a negative code
+  int total, n_in, mode, width, shift, dbits, rank;
+  unsigned long long lu_min;
+};
+__device__ __forceinline__ PlanCalc plan_of(const RcArgs &a, int *s_red,
+                                            unsigned long long *s_mm) {
+  const int g_count = min(max(1, tiles_of(a.n)), kRcGridCount);
+  const int status_was = load_agent(a.status);
+  const int n_in = a.n_in_dev ? load_agent(a.n_in_dev) : 0;
   int tot[3] = {0, 0, 0};
   unsigned long long tmn = ~0ull, tmx = 0ull;
   static_assert(kRcGridCount % kBlock == 0, "whole rounds of partials");
 #pragma unroll
   for (int r = 0; r < kRcGridCount / kBlock; ++r) {  // all loads in flight at once
     const int g = r * kBlock + (int)threadIdx.x;
-    if (g < (int)gridDim.x) {
+    if (g < g_count) {
       const RcPartial *p = a.w.partial + g;
-      tot[0] += load_agent(&p->n_empty);
-      tot[1] += load_agent(&p->n_cached);
-      tot[2] |= load_agent(&p->bad);
-      tmn = min(tmn, load_agent(&p->lu_min));
-      tmx = max(tmx, load_agent(&p->lu_max));
+      tot[0] += p->n_empty;
+      tot[1] += p->n_cached;
+      tot[2] |= p->bad;
+      tmn = min(tmn, p->lu_min);
+      tmx = max(tmx, p->lu_max);
     }
   }
   block_sum<3, int>(tot, s_red);
@@ -405,112 +415,85 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
     s_mm[wave_id() * 2] = tmn;
     s_mm[wave_id() * 2 + 1] = tmx;
   }
-  if (threadIdx.x == 0) {
-    const int n_in = n_in_all;
-    s_err = status_was != CASCADE_OK ? 1 : 0;  // an earlier call of the chain failed
-    if (!s_err && (tot[2] || n_in < 0 || n_in > a.max_in)) s_err = CASCADE_EINVAL;
-    s_red[0] = n_in;
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    tmn = min(tmn, s_mm[w * 2]);
+    tmx = max(tmx, s_mm[w * 2 + 1]);
   }
   __syncthreads();
-  const int n_in = s_red[0];
-  if (threadIdx.x == 0) {
-    for (int w = 1; w < kWaves; ++w) {
-      tmn = min(tmn, s_mm[w * 2]);
-      tmx = max(tmx, s_mm[w * 2 + 1]);
-    }
-    RcPlan *P = a.w.plan;
-    int err = s_err;
-    const long long total = (long long)a.need + n_in;
-    if (err == 0 && total > (long long)tot[0] + tot[1]) err = CASCADE_ENOSPC;
-    if (err < 0) store_agent(a.status, err);
-    P->ok = err == 0;
-    P->total = (int)total;
-    P->n_in = n_in;
-    P->lu_min = tmn;
-    P->thresh = 0ull;
-    P->tie_slot = -1;
-    P->bucket = 0;
-    if (total <= tot[0]) {
-      // empty slots suffice: the first `total` of them in slot order
-      P->mode = kModeEmpty;
-      P->width = P->shift = P->dbits = 0;
-      P->rank = (int)total - 1;
-    } else {
-      // every empty slot plus the (total - n_empty) least recent cached ones
-      const int width = bit_width64(1ull + (tmx - tmn));
-      P->mode = kModeCached;
-      P->width = width;
-      P->dbits = min(width, kDigit0);
-      P->shift = width - P->dbits;
-      P->rank = (int)(total - tot[0] - 1);
-    }
+  PlanCalc c;
+  c.err = status_was != CASCADE_OK ? 1 : 0;
+  if (c.err == 0 && (tot[2] || n_in < 0 || n_in > a.max_in)) c.err = CASCADE_EINVAL;
+  const long long total = (long long)a.need + n_in;
+  if (c.err == 0 && total > (long long)tot[0] + tot[1]) c.err = CASCADE_ENOSPC;
+  c.total = (int)total;
+  c.n_in = n_in;
+  c.lu_min = tmn;
+  if (total <= tot[0]) {
+    // empty slots suffice: the first `total` of them in slot order
+    c.mode = kModeEmpty;
+    c.width = c.shift = c.dbits = 0;
+    c.rank = (int)total - 1;
+  } else {
+    // every empty slot plus the (total - n_empty) least recent cached ones
+    c.mode = kModeCached;
+    c.width = bit_width64(1ull + (tmx - tmn));
+    c.dbits = min(c.width, kDigit0);
+    c.shift = c.width - c.dbits;
+    c.rank = (int)(total - tot[0] - 1);
   }
+  return c;
 }
 
 // ------------------------------------------------------------ top digit
 
-// Histogram of the top digit of every cached free slot's key (kModeCached
-// only); the last workgroup finds the bucket holding the sought rank.
+// Every workgroup derives the plan from the count kernel's partials
+// (workgroup 0 stores it for the later kernels and reports a failed check),
+// then, when cached blocks are reclaimed, adds its tiles to the histogram of
+// the key's top digit (8 copies, workgroup b adds to copy b % 8).
 __global__ __launch_bounds__(kBlock) void rc_hist_kernel(RcArgs a) {
   constexpr int kBins0 = 1 << kDigit0;
   static_assert(kBins0 == kBlock, "one bin per thread");
   __shared__ unsigned s_hist[kBins0];
-  __shared__ int s_scan[kWaves];
-  __shared__ bool s_last;
-  __shared__ int s_found[2];
+  __shared__ int s_red[kWaves * 3];
+  __shared__ unsigned long long s_mm[kWaves * 2];
   const Slots8 first = load_first(a);
-  const RcPlan *P = a.w.plan;
-  if (!P->ok || P->mode != kModeCached) return;  // uniform: the plan is the previous kernel's
-  const int t = threadIdx.x, shift = P->shift;
-  const unsigned long long lu_min = P->lu_min;
+  const PlanCalc c = plan_of(a, s_red, s_mm);
+  const int t = threadIdx.x;
+  if (blockIdx.x == 0 && t == 0) {
+    if (c.err < 0) store_agent(a.status, c.err);
+    RcPlan *P = a.w.plan;
+    P->ok = c.err == 0;
+    P->total = c.total;
+    P->n_in = c.n_in;
+    P->mode = c.mode;
+    P->width = c.width;
+    P->shift = c.shift;
+    P->dbits = c.dbits;
+    P->rank = c.rank;
+    P->bucket = 0;
+    P->tie_slot = -1;
+    P->lu_min = c.lu_min;
+    P->thresh = 0ull;
+  }
+  if (c.err != 0 || c.mode != kModeCached) return;  // uniform: every workgroup computes c alike
+  const int shift = c.shift;
+  const unsigned long long lu_min = c.lu_min;
   s_hist[t] = 0u;
   __syncthreads();
   for_tiles(a, first, [&](int, const Slots8 &v) {
 #pragma unroll
     for (int j = 0; j < kRcItems; ++j) {
       if (v.held[j] || v.h[j] == 0ull) continue;  // only cached free slots have keys above 0
-      // below 2^dbits: the count kernel saw every stamp in [lu_min, lu_max]
+      // below 2^dbits: every stamp lies in [lu_min, lu_max]
       const unsigned b = (unsigned)shr64(rc_key(v.h[j], v.lu[j], lu_min), shift);
       atomicAdd(&s_hist[b & (kBins0 - 1)], 1u);
     }
   });
   __syncthreads();
-  {
-    const unsigned v = s_hist[t];
-    if (v) atomicAdd(a.w.hist + (blockIdx.x % kHistCopies) * kBins0 + t, v);
-  }
-  wait_stores();
-  __syncthreads();
-  if (t == 0) s_last = last_workgroup(a.w.tickets);
-  __syncthreads();
-  if (!s_last) return;
-  acquire_agent();
-
-  // the last workgroup: the bucket in which the sought rank falls
-  const int rank = P->rank;
-  unsigned v = 0;
-  for (int c = 0; c < kHistCopies; ++c) {
-    v += load_agent(a.w.hist + c * kBins0 + t);
-    store_agent(a.w.hist + c * kBins0 + t, 0u);  // cleared for the next call
-  }
-  if (t == 0) s_found[0] = -1;
-  int ex[1] = {(int)v}, tot[1];
-  block_exclusive_scan<1, int>(ex, tot, s_scan);
-  if (rank >= ex[0] && rank < ex[0] + (int)v) {
-    s_found[0] = t;
-    s_found[1] = rank - ex[0];
-  }
-  __syncthreads();
-  if (t == 0) {
-    RcPlan *W = a.w.plan;
-    if (s_found[0] < 0) {  // the counts disagree with the plan: stop the call
-      store_agent(a.status, (int)CASCADE_EINTERNAL);
-      W->ok = 0;
-      return;
-    }
-    W->bucket = s_found[0];
-    W->rank = s_found[1];
-  }
+  const unsigned v = s_hist[t];
+  if (v) atomicAdd(a.w.hist + (blockIdx.x % kHistCopies) * kBins0 + t, v);
 }
 
 // ------------------------------------------------------------ compaction
@@ -534,13 +517,45 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
   __shared__ int s_rank[kWaves];
   __shared__ int s_red[kWaves * 2];
   __shared__ int s_start;
+  __shared__ int s_found[2];
   const Slots8 first = load_first(a);
-  const RcPlan *P = a.w.plan;
+  RcPlan *P = a.w.plan;
   if (!P->ok) return;
   const int t = threadIdx.x;
   const bool cached = P->mode == kModeCached;
   const int shift = P->shift;
-  const unsigned long long lu_min = P->lu_min, bucket = (unsigned long long)P->bucket;
+  const unsigned long long lu_min = P->lu_min;
+  unsigned long long bucket = 0;
+  if (cached) {
+    // the bucket holding the sought rank, from the histogram's copies
+    // (every workgroup alike; workgroup 0 stores it for the select kernel)
+    constexpr int kBins0 = 1 << kDigit0;
+    static_assert(kBins0 == kBlock, "one bin per thread");
+    unsigned v = 0;
+#pragma unroll
+    for (int c = 0; c < kHistCopies; ++c) v += load_agent(a.w.hist + c * kBins0 + t);
+    const int rank = P->rank;
+    if (t == 0) s_found[0] = -1;
+    int ex[1] = {(int)v}, tot[1];
+    block_exclusive_scan<1, int>(ex, tot, s_red);
+    if (rank >= ex[0] && rank < ex[0] + (int)v) {
+      s_found[0] = t;
+      s_found[1] = rank - ex[0];
+    }
+    __syncthreads();
+    if (s_found[0] < 0) {  // the counts disagree with the plan: stop the call
+      if (blockIdx.x == 0 && t == 0) {
+        store_agent(a.status, (int)CASCADE_EINTERNAL);
+        P->ok = 0;
+      }
+      return;
+    }
+    bucket = (unsigned long long)s_found[0];
+    if (blockIdx.x == 0 && t == 0) {  // P->rank stays: the other workgroups read it
+      P->bucket = s_found[0];
+      P->brank = s_found[1];
+    }
+  }
   const int d2 = cached ? min(shift, kDigitN) : 0, s2 = shift - d2;
   const unsigned m2 = (1u << d2) - 1u;
   if (d2 > 0)
@@ -589,7 +604,10 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
     if (t == 0) {
       s_start = start0;
       a.w.rec[tile] = make_int4(start0, c2[0], cnt - c2[0], c2[1]);
-      a.w.off[tile] = make_int4(0, 0, 0, 0);  // the select kernel's counters
+      // the select kernel's counters (added to with atomics)
+      unsigned long long *o64 = reinterpret_cast<unsigned long long *>(a.w.off + tile);
+      store_agent(o64, 0ull);
+      store_agent(o64 + 1, 0ull);
     }
     __syncthreads();
     const int start = s_start, base = slot_base(tile);
@@ -674,7 +692,7 @@ struct ListMap {
 // round trips rather than one per entry.  Certainly reclaimed entries are
 // skipped.
 constexpr int kSelBatch = 8;
-template <typename At, typename F>
+template <bool kAgent = false, typename At, typename F>
 __device__ __forceinline__ void for_entries(const unsigned *__restrict__ ent,
                                             const unsigned long long *__restrict__ key, int n,
                                             int first, int stride, At &&at, F &&f) {
@@ -685,13 +703,23 @@ __device__ __forceinline__ void for_entries(const unsigned *__restrict__ ent,
     for (int j = 0; j < kSelBatch; ++j) {
       const int fi = r0 + j * stride;
       const int i = fi < n ? at(fi) : 0;
-      e[j] = fi < n ? ent[i] : kEntSure;  // past the end: skipped
-      k[j] = fi < n ? key[i] : 0ull;
+      // (kAgent: written by other workgroups of this launch)
+      e[j] = fi < n ? (kAgent ? load_agent(ent + i) : ent[i]) : kEntSure;  // past the end: skipped
+      k[j] = fi < n ? (kAgent ? load_agent(key + i) : key[i]) : 0ull;
     }
 #pragma unroll
     for (int j = 0; j < kSelBatch; ++j)
       if (!(e[j] & kEntSure)) f(e[j], k[j]);
   }
+}
+
+// A tile's four counters in off[], read as two agent-scope words (other
+// workgroups add to them with atomics).
+__device__ __forceinline__ int4 load_counts(const int4 *off, int tile) {
+  const unsigned long long *o64 = reinterpret_cast<const unsigned long long *>(off + tile);
+  const unsigned long long u = load_agent(o64), w = load_agent(o64 + 1);
+  return make_int4((int)(unsigned)u, (int)(unsigned)(u >> 32), (int)(unsigned)w,
+                   (int)(unsigned)(w >> 32));
 }
 
 // Adds one candidate to its tile's counters in off[]: (below T, equal to T,
@@ -723,25 +751,19 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
   __shared__ unsigned s_sent[kStageLds];
   __shared__ int4 s_q[kTilesLds];
   RcPlan *P = a.w.plan;
-  if (!P->ok) return;
   const int t = threadIdx.x;
+  if (blockIdx.x == 0) {  // the top-digit histogram is free again (the compaction read it)
+    for (int i = t; i < kHistCopies * (1 << kDigit0); i += kBlock) store_agent(a.w.hist + i, 0u);
+  }
+  if (!P->ok) return;
   const int tiles = max(1, tiles_of(a.n));
   // the compaction's histogram of the next digit, requested with the counts
   // (bins past 2^d2 were never added to)
   unsigned v2[kSelBins];
-  {
-    const uint4 *sub = reinterpret_cast<const uint4 *>(a.w.sub) + t * (kSelBins / 4);
 #pragma unroll
-    for (int q = 0; q < kSelBins / 4; ++q) {
-      const uint4 u = sub[q];
-      v2[4 * q] = u.x;
-      v2[4 * q + 1] = u.y;
-      v2[4 * q + 2] = u.z;
-      v2[4 * q + 3] = u.w;
-    }
-  }
+  for (int j = 0; j < kSelBins; ++j) v2[j] = load_agent(a.w.sub + t * kSelBins + j);
   if (t < 64) {  // the regions' entry counts and their prefix
-    const int c = t < kListGroups ? (int)a.w.count[t * kCountStride] : 0;
+    const int c = t < kListGroups ? (int)load_agent(a.w.count + t * kCountStride) : 0;
     const int inc = (int)wave_inclusive_sum((unsigned)c);
     if (t < kListGroups) s_pre[t + 1] = inc;
     if (t == 0) s_pre[0] = 0;
@@ -759,7 +781,7 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
   const int shift0 = P->shift;
   const bool has_sub = cached && shift0 > 0;
   unsigned long long T = cached ? (unsigned long long)P->bucket << shift0 : 0ull;
-  int rank = P->rank;  // kModeEmpty: total - 1 among the empty slots
+  int rank = cached ? P->brank : P->rank;  // kModeEmpty: total - 1 among the empty slots
   int shift = has_sub ? shift0 : 0, matching = 0, d2 = 0, s2 = 0;
   unsigned b2 = 0;
   bool fail = false;
@@ -791,9 +813,9 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
         count_in_tile(a.w.off, e, true);
       } else if (dg == b2 && staging) {
         const unsigned p = atomicAdd(a.w.stage_n, 1u);
-        if (p < (unsigned)kStageCap) {
-          a.w.stage_key[p] = k;
-          a.w.stage_ent[p] = e;
+        if (p < (unsigned)kStageCap) {  // read by the last workgroup: agent scope
+          store_agent(a.w.stage_key + p, k);
+          store_agent(a.w.stage_ent + p, e);
         }
       }
     });
@@ -807,7 +829,7 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
 
   // ---- the last workgroup
   if (has_sub)
-    for (int b = t; b < kRcBins; b += kBlock) a.w.sub[b] = 0u;  // free for the next call
+    for (int b = t; b < kRcBins; b += kBlock) store_agent(a.w.sub + b, 0u);  // free again
   const int n_staged = (int)load_agent(a.w.stage_n);
   if (staging && n_staged != matching) fail = true;
   // the candidates on T's first digits: the stage (in LDS when it fits),
@@ -821,8 +843,8 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
     for (int j = 0; j < kStageLds / kBlock; ++j) {  // all loads in flight at once
       const int i = j * kBlock + t;
       if (i < n_staged) {
-        s_skey[i] = skey[i];
-        s_sent[i] = sent[i];
+        s_skey[i] = load_agent(skey + i);
+        s_sent[i] = load_agent(sent + i);
       }
     }
     __syncthreads();
@@ -832,7 +854,7 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
     if (in_lds) {
       for (int i = t; i < n_staged; i += kBlock) f(s_sent[i], s_skey[i]);
     } else if (staging) {
-      for_entries(sent, skey, n_staged, t, kBlock, at_stage, f);
+      for_entries<true>(sent, skey, n_staged, t, kBlock, at_stage, f);
     } else {
       const unsigned long long hi = shr64(T, s2);
       for_entries(ent, key, lst.size(), t, kBlock, at_list,
@@ -932,7 +954,7 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
 #pragma unroll
     for (int c = 0; c < kChunks; ++c) {
       const int tile = c * kBlock + t;
-      qa[c] = tile < tiles ? a.w.off[tile] : make_int4(0, 0, 0, 0);
+      qa[c] = tile < tiles ? load_counts(a.w.off, tile) : make_int4(0, 0, 0, 0);
       ra[c] = tile < tiles ? a.w.rec[tile] : make_int4(0, 0, 0, 0);
     }
 #pragma unroll
@@ -942,7 +964,7 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
     for (int c0 = 0; c0 < tiles; c0 += kBlock) {
       const int tile = c0 + t;
       const int4 r = tile < tiles ? a.w.rec[tile] : make_int4(0, 0, 0, 0);
-      tile_chunk(tile, tile < tiles ? a.w.off[tile] : make_int4(0, 0, 0, 0), r);
+      tile_chunk(tile, tile < tiles ? load_counts(a.w.off, tile) : make_int4(0, 0, 0, 0), r);
     }
   }
   __syncthreads();
@@ -1008,7 +1030,7 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
     const int tile = c0 + t;
     int v[2] = {0, 0};
     if (tile < tiles) {
-      const int4 q = tiles <= kTilesLds ? s_q[tile] : a.w.off[tile];
+      const int4 q = tiles <= kTilesLds ? s_q[tile] : load_counts(a.w.off, tile);
       v[0] = q.x + (tile < cut ? q.y : (tile == cut ? r_cut : 0));
       v[1] = q.z + (tile < cut ? q.w : (tile == cut ? dem_cut : 0));
     }
@@ -1027,8 +1049,8 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
       P->tie_slot = tie_slot;
       if (a.n_out_dev) store_agent(a.n_out_dev, carry_d);
     }
-    for (int g = 0; g < kListGroups; ++g) a.w.count[g * kCountStride] = 0u;  // free again
-    *a.w.stage_n = 0u;
+    for (int g = 0; g < kListGroups; ++g) store_agent(a.w.count + g * kCountStride, 0u);
+    store_agent(a.w.stage_n, 0u);  // both free again
   }
 }
 
