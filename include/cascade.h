@@ -423,7 +423,7 @@ int cascade_prefix_probe(const void *index, int32_t capacity, int32_t n,
    freed        device int32[need]; placed device int32[max_incoming].
    index        the prefix index (NULL = none) and its capacity.
    workspace    device memory of cascade_reclaim_workspace_bytes(n_slots)
-                bytes (about 12 bytes per slot: the call lists the slots it
+                bytes (about 24 bytes per slot: the call lists the slots it
                 may reclaim), 256-byte aligned, zero-filled once before its
                 first use; every call leaves its counters and histograms at
                 zero again (the rest is rewritten before it is read).  A

@@ -21,9 +21,10 @@
 //                      slots certainly reclaimed
 //                      (empty ones, keys below the bucket) and the candidates
 //                      (keys inside it; with empty slots alone enough, the
-//                      empty slots), each with its key and, on tiers 0 and 1,
-//                      its index slot and whether it is demoted (the index as
-//                      it was when the call began), in one chunk of a list
+//                      empty slots), each with its key, its block and, on
+//                      tiers 0 and 1, its index slot and whether it is
+//                      demoted (the index as it was when the call began), in
+//                      one chunk of a list
 //                      reserved with one atomic add on one of 16 region
 //                      counters; a histogram of the candidates' next 12-bit
 //                      digit
@@ -127,6 +128,7 @@ struct RcWork {
   unsigned long long *key;  // [n_slots] list: keys
   unsigned *ent;            // [n_slots] list: slot and flags
   unsigned *pos;            // [n_slots] list: the block's index slot (kNoPos: none)
+  unsigned long long *hash;  // [n_slots] list: the slot's block (0: empty)
 };
 
 constexpr size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -148,7 +150,7 @@ size_t workspace_bytes_for(int32_t n) {
          align256(sizeof(unsigned) * kRcBins) +
          align256(sizeof(unsigned) * kListGroups * kCountStride) + align256(sizeof(unsigned)) +
          align256(sizeof(unsigned long long) * kStageCap) + align256(sizeof(unsigned) * kStageCap) +
-         2 * align256(sizeof(int4) * tiles) + align256(sizeof(unsigned long long) * slots) +
+         2 * align256(sizeof(int4) * tiles) + 2 * align256(sizeof(unsigned long long) * slots) +
          2 * align256(sizeof(unsigned) * slots);
 }
 
@@ -184,6 +186,8 @@ RcWork carve(void *ws, int32_t n) {
   w.ent = reinterpret_cast<unsigned *>(p);
   p += align256(sizeof(unsigned) * slots);
   w.pos = reinterpret_cast<unsigned *>(p);
+  p += align256(sizeof(unsigned) * slots);
+  w.hash = reinterpret_cast<unsigned long long *>(p);
   return w;
 }
 
@@ -498,14 +502,66 @@ __global__ __launch_bounds__(kBlock) void rc_hist_kernel(RcArgs a) {
 
 // ------------------------------------------------------------ compaction
 
-// Whether reclaiming block h from tier 0 or 1 demotes it (no deeper tier
-// holds it in the index), and its index slot for the later bit updates.
-__device__ __forceinline__ bool demotable(const RcArgs &a, unsigned long long h, unsigned &pos) {
-  pos = kNoPos;
-  if (h == 0ull) return false;
-  const IndexSlot *e = a.index ? index_find(a.index, a.index_mask, h) : nullptr;
-  if (e) pos = (unsigned)(e - a.index);
-  return e == nullptr || (e->tiers & ~((2u << a.tier) - 1u)) == 0u;  // no deeper tier
+// For the tile's listed blocks of tiers 0 and 1 (want[j]): whether
+// reclaiming them demotes them (no deeper tier holds the block in the index)
+// and their index slots for the later bit updates.  The blocks are gathered
+// in LDS and spread over the workgroup, kLookBatch lookups per thread in
+// flight, so up to kLookBatch * kBlock lookups of a tile cost one memory
+// round trip whichever threads hold them.  (Two per thread would take the
+// kernel past 128 VGPRs, below four waves per SIMD, which the full-table
+// read of the deepest tier needs.)  `look` holds kRcTile hashes, each
+// replaced by its result, and is free again on return.
+constexpr int kLookBatch = 1;
+__device__ __forceinline__ void demotions(const RcArgs &a, const unsigned long long (&h)[kRcItems],
+                                          const bool (&want)[kRcItems], bool (&dem)[kRcItems],
+                                          unsigned (&ip)[kRcItems], unsigned long long *look,
+                                          int *s_rank) {
+#pragma unroll
+  for (int j = 0; j < kRcItems; ++j) {
+    dem[j] = false;
+    ip[j] = kNoPos;
+  }
+  if (a.tier >= 2) return;  // nothing is demoted from the deepest tier
+  int wr[kRcItems];
+  const int n_want = block_slot_rank(want, wr, s_rank);
+  if (n_want == 0) return;  // uniform
+#pragma unroll
+  for (int j = 0; j < kRcItems; ++j)
+    if (want[j]) look[wr[j]] = h[j];
+  __syncthreads();
+  const unsigned deeper = ~((2u << a.tier) - 1u);
+  for (int i0 = (int)threadIdx.x; i0 < n_want; i0 += kLookBatch * kBlock) {
+    unsigned long long hh[kLookBatch];
+    bool w[kLookBatch];
+#pragma unroll
+    for (int q = 0; q < kLookBatch; ++q) {
+      const int i = i0 + q * kBlock;
+      w[q] = i < n_want && a.index;
+      hh[q] = i < n_want ? look[i] : 0ull;
+    }
+    int pos[kLookBatch];
+    unsigned tiers[kLookBatch];
+    index_find_n(a.index, a.index_mask, hh, w, pos, tiers);
+#pragma unroll
+    for (int q = 0; q < kLookBatch; ++q) {
+      const int i = i0 + q * kBlock;
+      // slot (below 2^30) | demoted in bit 31; kNoPos's slot bits: absent
+      // (each entry is read and rewritten by the same thread)
+      if (i < n_want)
+        look[i] = (pos[q] >= 0 ? (unsigned)pos[q] : (kNoPos >> 1)) |
+                  ((pos[q] < 0 || (tiers[q] & deeper) == 0u) ? 0x80000000u : 0u);
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < kRcItems; ++j) {
+    if (!want[j]) continue;
+    const unsigned v = (unsigned)look[wr[j]];
+    const unsigned sl = v & 0x7fffffffu;
+    ip[j] = sl == (kNoPos >> 1) ? kNoPos : sl;
+    dem[j] = (v >> 31) != 0u;
+  }
+  __syncthreads();
 }
 
 // Per tile, in slot order: the slots certainly reclaimed and the candidates,
@@ -514,27 +570,31 @@ __device__ __forceinline__ bool demotable(const RcArgs &a, unsigned long long h,
 // Demotion is decided here, on the index as it was when the call began.
 __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
   __shared__ unsigned s_sub[kRcBins];
+  __shared__ unsigned long long s_look[kRcTile];
   __shared__ int s_rank[kWaves];
   __shared__ int s_red[kWaves * 2];
   __shared__ int s_start;
   __shared__ int s_found[2];
   const Slots8 first = load_first(a);
-  RcPlan *P = a.w.plan;
-  if (!P->ok) return;
   const int t = threadIdx.x;
-  const bool cached = P->mode == kModeCached;
-  const int shift = P->shift;
+  // the top digit's histogram, requested with the plan (used when cached)
+  constexpr int kBins0 = 1 << kDigit0;
+  static_assert(kBins0 == kBlock, "one bin per thread");
+  unsigned hv[kHistCopies];
+#pragma unroll
+  for (int c = 0; c < kHistCopies; ++c) hv[c] = load_agent(a.w.hist + c * kBins0 + t);
+  RcPlan *P = a.w.plan;
+  const int ok = P->ok, mode = P->mode, shift = P->shift, rank = P->rank;
   const unsigned long long lu_min = P->lu_min;
+  if (!ok) return;
+  const bool cached = mode == kModeCached;
   unsigned long long bucket = 0;
   if (cached) {
     // the bucket holding the sought rank, from the histogram's copies
     // (every workgroup alike; workgroup 0 stores it for the select kernel)
-    constexpr int kBins0 = 1 << kDigit0;
-    static_assert(kBins0 == kBlock, "one bin per thread");
     unsigned v = 0;
 #pragma unroll
-    for (int c = 0; c < kHistCopies; ++c) v += load_agent(a.w.hist + c * kBins0 + t);
-    const int rank = P->rank;
+    for (int c = 0; c < kHistCopies; ++c) v += hv[c];
     if (t == 0) s_found[0] = -1;
     int ex[1] = {(int)v}, tot[1];
     block_exclusive_scan<1, int>(ex, tot, s_red);
@@ -579,12 +639,14 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
     }
     // the index lookups first: their latency overlaps the workgroup scans
     // (tier 2 demotes nothing: its reclaimed blocks are looked up when written)
-    bool dem[kRcItems];
+    bool dem[kRcItems], want[kRcItems];
     unsigned ip[kRcItems];
 #pragma unroll
-    for (int j = 0; j < kRcItems; ++j) {
-      ip[j] = (a.tier >= 2 && v.h[j] != 0ull && a.index) ? kFindPos : kNoPos;
-      dem[j] = f[j] && a.tier < 2 && demotable(a, v.h[j], ip[j]);  // false when empty
+    for (int j = 0; j < kRcItems; ++j) want[j] = f[j] && a.tier < 2 && v.h[j] != 0ull;
+    demotions(a, v.h, want, dem, ip, s_look, s_rank);  // (empty slots: none)
+    if (a.tier >= 2) {
+#pragma unroll
+      for (int j = 0; j < kRcItems; ++j) ip[j] = (v.h[j] != 0ull && a.index) ? kFindPos : kNoPos;
     }
     int rk[kRcItems];
     const int cnt = block_slot_rank(f, rk, s_rank);
@@ -619,6 +681,7 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
       a.w.ent[i] = (unsigned)item_slot(base, j) | (sure[j] ? kEntSure : 0u) |
                    (dem[j] ? kEntDem : 0u);
       a.w.pos[i] = ip[j];
+      a.w.hash[i] = v.h[j];
       if (d2 > 0 && !sure[j]) atomicAdd(&s_sub[(unsigned)(k[j] >> s2) & m2], 1u);
     }
   });
@@ -752,18 +815,21 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
   __shared__ int4 s_q[kTilesLds];
   RcPlan *P = a.w.plan;
   const int t = threadIdx.x;
-  if (blockIdx.x == 0) {  // the top-digit histogram is free again (the compaction read it)
-    for (int i = t; i < kHistCopies * (1 << kDigit0); i += kBlock) store_agent(a.w.hist + i, 0u);
-  }
-  if (!P->ok) return;
-  const int tiles = max(1, tiles_of(a.n));
-  // the compaction's histogram of the next digit, requested with the counts
-  // (bins past 2^d2 were never added to)
+  // the compaction's histogram of the next digit (bins past 2^d2 were never
+  // added to) and the regions' entry counts, requested with the plan
   unsigned v2[kSelBins];
 #pragma unroll
   for (int j = 0; j < kSelBins; ++j) v2[j] = load_agent(a.w.sub + t * kSelBins + j);
+  const int c_reg = t < kListGroups ? (int)load_agent(a.w.count + t * kCountStride) : 0;
+  const int ok = P->ok, mode = P->mode, shift0 = P->shift, bucket = P->bucket, brank = P->brank,
+            prank = P->rank;
+  if (blockIdx.x == 0) {  // the top-digit histogram is free again (the compaction read it)
+    for (int i = t; i < kHistCopies * (1 << kDigit0); i += kBlock) store_agent(a.w.hist + i, 0u);
+  }
+  if (!ok) return;
+  const int tiles = max(1, tiles_of(a.n));
   if (t < 64) {  // the regions' entry counts and their prefix
-    const int c = t < kListGroups ? (int)load_agent(a.w.count + t * kCountStride) : 0;
+    const int c = c_reg;
     const int inc = (int)wave_inclusive_sum((unsigned)c);
     if (t < kListGroups) s_pre[t + 1] = inc;
     if (t == 0) s_pre[0] = 0;
@@ -777,11 +843,10 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
   const unsigned long long *key = a.w.key;
   const unsigned *ent = a.w.ent;
 
-  const bool cached = P->mode == kModeCached;
-  const int shift0 = P->shift;
+  const bool cached = mode == kModeCached;
   const bool has_sub = cached && shift0 > 0;
-  unsigned long long T = cached ? (unsigned long long)P->bucket << shift0 : 0ull;
-  int rank = cached ? P->brank : P->rank;  // kModeEmpty: total - 1 among the empty slots
+  unsigned long long T = cached ? (unsigned long long)bucket << shift0 : 0ull;
+  int rank = cached ? brank : prank;  // kModeEmpty: total - 1 among the empty slots
   int shift = has_sub ? shift0 : 0, matching = 0, d2 = 0, s2 = 0;
   unsigned b2 = 0;
   bool fail = false;
@@ -1056,85 +1121,81 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
 
 // ---------------------------------------------------------------- writes
 
-// A workgroup per tile with reclaimed slots: their positions in slot order
-// (flags staged in LDS from the tile's chunk), then for position p of the
-// reclaimed list: freed[p] or placed[p - need], the demoted block into
-// outgoing, the index bits (the old block leaves this tier, a demoted one
-// joins the next) and the slot's new contents.
+// A workgroup per tile with reclaimed slots.  The tile's chunk of the list
+// is in slot order, so a reclaimed entry's position p in the reclaimed list
+// is the tile's offset plus the reclaimed entries before it in the chunk
+// (the demoted ones likewise).  For position p: freed[p] or
+// placed[p - need], the demoted block into outgoing, the index bits (the old
+// block leaves this tier, a demoted one joins the next) and the slot's new
+// contents.  The old block comes from the list and its stamp from its key,
+// so the table is not read again.
 __global__ __launch_bounds__(kBlock) void rc_write_kernel(RcArgs a) {
-  __shared__ unsigned s_flagw[kRcTile / 4];
-  __shared__ unsigned s_ipos[kRcTile];
-  __shared__ int s_rank[kWaves];
+  __shared__ int s_scan[kWaves * 2];
   const RcPlan *P = a.w.plan;
-  if (!P->ok) return;
   const int tile = blockIdx.x, t = threadIdx.x;
-  const int4 o = a.w.off[tile], r = a.w.rec[tile];  // requested together
-  if (o.z == 0) return;  // nothing reclaimed here (so nothing demoted either)
-  const unsigned long long T = P->thresh;
-  const int tie_slot = P->tie_slot, need = a.need, total = P->total;
-  const int tile0 = tile * kRcTile;
-  unsigned char *s_flag = reinterpret_cast<unsigned char *>(s_flagw);
-  for (int i = t; i < kRcTile / 4; i += kBlock) s_flagw[i] = 0u;
-  __syncthreads();
-  for (int i = r.x + t; i < r.x + r.y + r.z; i += kBlock) {
-    const unsigned e = a.w.ent[i];
+  const int4 o = a.w.off[tile], r = a.w.rec[tile];  // requested with the plan
+  const int ok = P->ok, tie_slot = P->tie_slot, total = P->total, need = a.need;
+  const unsigned long long T = P->thresh, lu_min = P->lu_min;
+  if (!ok || o.z == 0) return;  // nothing reclaimed here (so nothing demoted either)
+  const int len = min(r.y + r.z, kRcTile);  // a chunk holds at most its tile's slots
+  // a row of kBlock entries at a time (one row in the usual case)
+  int n_sel = 0, n_dem = 0;  // before this row
+  for (int c0 = 0; c0 < len; c0 += kBlock) {  // uniform
+    const int c = c0 + t, i = r.x + c;
+    const bool in = c < len;
+    const unsigned e = in ? a.w.ent[i] : 0u;
+    const unsigned long long k = in ? a.w.key[i] : 0ull, h = in ? a.w.hash[i] : 0ull;
+    const unsigned ipos = in ? a.w.pos[i] : kNoPos;
     const int slot = (int)(e & kEntSlot);
-    const unsigned long long k = a.w.key[i];
-    const bool sel = (e & kEntSure) || k < T || (k == T && slot <= tie_slot);
-    const int loc = slot - tile0;
-    if (sel && (unsigned)loc < (unsigned)kRcTile) {
-      s_flag[loc] = (unsigned char)(1u | ((e & kEntDem) ? 2u : 0u));
-      s_ipos[loc] = a.w.pos[i];
+    const bool sel = in && (unsigned)slot < (unsigned)a.n &&
+                     ((e & kEntSure) || k < T || (k == T && slot <= tie_slot));
+    const bool dem = sel && (e & kEntDem);
+    // tier 2 looks its reclaimed blocks up here
+    const unsigned long long hq[1] = {h};
+    const bool lq[1] = {sel && ipos == kFindPos && a.index};
+    int fpos[1];
+    unsigned ftiers[1];
+    index_find_n(a.index, a.index_mask, hq, lq, fpos, ftiers);
+    int ex[2] = {(int)sel, (int)dem}, tot[2];
+    block_exclusive_scan<2, int>(ex, tot, s_scan);
+    const int p = o.x + n_sel + ex[0], q = o.y + n_dem + ex[1];
+    n_sel += tot[0];
+    n_dem += tot[1];
+    // positions past the tile's counts are never written (the counts disagree)
+    if (!sel || p - o.x >= o.z || p >= total || (dem && (q - o.y >= o.w || q >= a.max_out)))
+      continue;
+    const bool place = p >= need;
+    unsigned long long in_h = 0ull;
+    long long in_lu = 0ll;
+    if (place) {
+      in_h = a.incoming[p - need].hash;
+      in_lu = a.incoming[p - need].last_use_ns;
     }
-  }
-  __syncthreads();
-  const int base = slot_base(tile);
-  bool sel[kRcItems], dem[kRcItems];
-#pragma unroll
-  for (int j = 0; j < kRcItems; ++j) {
-    const unsigned f = s_flag[item_slot(base, j) - tile0];
-    sel[j] = (f & 1u) != 0u;
-    dem[j] = (f & 2u) != 0u;
-  }
-  int rs[kRcItems], rd[kRcItems];
-  const int n_sel = block_slot_rank(sel, rs, s_rank);
-  const int n_dem = block_slot_rank(dem, rd, s_rank);
-  if (n_sel != o.z || n_dem != o.w || o.x + n_sel > total || o.y + n_dem > a.max_out) {
-    if (t == 0) store_agent(a.status, (int)CASCADE_EINTERNAL);
-    return;  // the counts disagree: this tile writes nothing
-  }
-#pragma unroll
-  for (int j = 0; j < kRcItems; ++j) {
-    if (!sel[j]) continue;
-    const int slot = item_slot(base, j);
-    const int p = o.x + rs[j];
-    const unsigned long long old = a.hash[slot];
-    const long long old_lu = a.lu[slot];
-    const unsigned ipos = s_ipos[item_slot(base, j) - tile0];  // found by the compaction
-    IndexSlot *e = nullptr;
-    if (ipos == kFindPos) e = index_find(a.index, a.index_mask, old);
-    else if (ipos != kNoPos && a.index) e = a.index + ipos;
-    if (dem[j]) {
+    IndexSlot *ix = nullptr;
+    if (ipos == kFindPos) ix = fpos[0] >= 0 ? a.index + fpos[0] : nullptr;
+    else if (ipos != kNoPos && a.index) ix = a.index + ipos;  // found by the compaction
+    if (dem) {  // a cached block: key = 1 + last use - lu_min
       cascade_demotion_t d;
-      d.hash = old;
-      d.last_use_ns = old_lu;
+      d.hash = h;
+      d.last_use_ns = (long long)(k - 1ull + lu_min);
       d.src_slot = slot;
       d.pad = 0;
-      a.outgoing[o.y + rd[j]] = d;
-      if (e) atomicOr(&e->tiers, 1u << (a.tier + 1));
+      a.outgoing[q] = d;
+      if (ix) atomicOr(&ix->tiers, 1u << (a.tier + 1));
     }
-    if (e) atomicAnd(&e->tiers, ~(1u << a.tier));
-    if (p < need) {
+    if (ix) atomicAnd(&ix->tiers, ~(1u << a.tier));
+    if (!place) {
       a.freed[p] = slot;
       a.hash[slot] = 0ull;
       a.lu[slot] = 0ll;
     } else {
-      const cascade_demotion_t in = a.incoming[p - need];
       a.placed[p - need] = slot;
-      a.hash[slot] = in.hash;
-      a.lu[slot] = in.last_use_ns;
+      a.hash[slot] = in_h;
+      a.lu[slot] = in_lu;
     }
   }
+  if (t == 0 && (n_sel != o.z || n_dem != o.w))
+    store_agent(a.status, (int)CASCADE_EINTERNAL);  // the counts disagree
 }
 
 bool index_capacity_ok(int32_t capacity) {

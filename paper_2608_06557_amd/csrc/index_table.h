@@ -32,17 +32,64 @@ __device__ __forceinline__ unsigned long long fmix64(unsigned long long k) {
   return k;
 }
 
-// The slot holding key h, or nullptr when h is not in the table.  Keys are
-// never removed, so the first empty slot on the probe sequence ends it.
-__device__ __forceinline__ IndexSlot *index_find(IndexSlot *slots, unsigned mask,
-                                                 unsigned long long h) {
-  unsigned s = (unsigned)fmix64(h) & mask;
-  for (unsigned p = 0; p <= mask; ++p, s = (s + 1) & mask) {
-    const unsigned long long k = slots[s].key;
-    if (k == h) return &slots[s];
-    if (k == 0ull) return nullptr;
+// N lookups at once, for the keys h[j] with want[j].  Every home slot is
+// requested whole (key and tiers in one 16-byte load) before any is
+// examined, so the N lookups share one memory round trip instead of taking
+// one or two each in turn; a key that sits past its home slot continues
+// probing alone.  Keys are never removed, so the first empty slot on a
+// probe sequence ends it.  pos[j] is the key's slot (-1: absent or not
+// wanted) and tiers[j] that slot's tier set.
+template <int N>
+__device__ __forceinline__ void index_find_n(const IndexSlot *slots, unsigned mask,
+                                             const unsigned long long (&h)[N],
+                                             const bool (&want)[N], int (&pos)[N],
+                                             unsigned (&tiers)[N]) {
+  static_assert(N <= 32, "one bit per lookup");
+  unsigned s[N];
+  uint4 v[N];
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    s[j] = (unsigned)fmix64(h[j]) & mask;
+    v[j] = want[j] ? *reinterpret_cast<const uint4 *>(slots + s[j]) : make_uint4(0u, 0u, 0u, 0u);
   }
-  return nullptr;
+  unsigned pending = 0u;  // lookups whose home slot holds another key
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    const unsigned long long k = (unsigned long long)v[j].x | ((unsigned long long)v[j].y << 32);
+    const bool hit = want[j] && k == h[j];
+    pos[j] = hit ? (int)s[j] : -1;
+    tiers[j] = hit ? v[j].z : 0u;
+    if (want[j] && !hit && k != 0ull) pending |= 1u << j;
+  }
+  while (pending) {  // rare: one lookup at a time (items picked by constant index)
+    const int j = __builtin_ctz(pending);
+    pending &= pending - 1u;
+    unsigned long long hj = 0ull;
+    unsigned sj = 0u;
+#pragma unroll
+    for (int q = 0; q < N; ++q) {
+      hj = q == j ? h[q] : hj;
+      sj = q == j ? s[q] : sj;
+    }
+    int pj = -1;
+    unsigned tj = 0u;
+    for (unsigned p = 1; p <= mask; ++p) {  // mask + 1 slots in all
+      sj = (sj + 1u) & mask;
+      const uint4 w = *reinterpret_cast<const uint4 *>(slots + sj);
+      const unsigned long long k = (unsigned long long)w.x | ((unsigned long long)w.y << 32);
+      if (k == hj) {
+        pj = (int)sj;
+        tj = w.z;
+        break;
+      }
+      if (k == 0ull) break;
+    }
+#pragma unroll
+    for (int q = 0; q < N; ++q) {
+      pos[q] = q == j ? pj : pos[q];
+      tiers[q] = q == j ? tj : tiers[q];
+    }
+  }
 }
 
 }  // namespace cascade
