@@ -115,6 +115,24 @@ def test_small_chains(dev, case, seed):
     assert_chain_same(w, g, rc, outs, masks, f"case {case} seed {seed}")
 
 
+def test_nearly_full_index(dev):
+    # an index at load 0.9: many blocks sit past their home slot, so the
+    # compaction's gathered lookups (tiers 0 and 1) and the write kernel's
+    # (tier 2) continue probing one lookup at a time
+    w = small(41, (3500, 6000, 8200), (1000, 500, 100))
+    keys = len(w["index_keys"])
+    cap = 1 << int(np.ceil(np.log2(keys + 1)))
+    assert keys / cap > 0.85, keys / cap
+    d = dev.DeviceTiers(w["tables"], w["needs"], w["index_keys"], w["index_masks"],
+                        capacity=cap)
+    assert d.run() == 0
+    g = d.fetch()
+    rc, outs, masks = oracle_chain(w)
+    assert rc == 0
+    assert_chain_same(w, g, rc, outs, masks, "index at load 0.9")
+    assert outs[0]["n_outgoing"] > 0 and outs[1]["n_outgoing"] > 0
+
+
 def test_empty_slots_alone_suffice_and_ties_split(dev):
     # plenty of empty slots: the threshold is the empty key, cut mid-way in
     # slot order; DRAM then takes exactly its empties
