@@ -206,6 +206,24 @@ def measure_reclaim(cfg, stream, reps=20):
     for t in range(3):
         for k in ["freed", "placed", "block_hash", "last_use_ns"]:
             assert np.array_equal(gg["tiers"][t][k], g["tiers"][t][k]), (t, k)
+    # the same chain as one cascade_tier_reclaim_chain call (the three tables'
+    # count and histogram passes launched together); results equal the
+    # per-tier calls'
+    d.chain_args()
+    ctot = []
+    for r in range(reps + 2):
+        restore()
+        ev[0].record(stream)
+        assert d.run_chain(stream) == 0
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        if r >= 2:
+            ctot.append(ev[0].elapsed_time(ev[3]) * 1e3)
+    gc = d.fetch()
+    assert gc["status"] == 0
+    for t in range(3):
+        for k in ["freed", "placed", "block_hash", "last_use_ns"]:
+            assert np.array_equal(gc["tiers"][t][k], g["tiers"][t][k]), (t, k)
     n_rec = [len(g["tiers"][t]["freed"]) + len(g["tiers"][t]["placed"]) for t in range(3)]
     slots = int(sum(w["sizes"]))
     us = float(np.median(tot))
@@ -219,6 +237,7 @@ def measure_reclaim(cfg, stream, reps=20):
             "index_keys": int(len(w["index_keys"])),
             "tier_us_p50": [float(np.median(x)) for x in per], "chain_us_p50": us,
             "chain_graph_us_p50": float(np.median(gtot)),
+            "chain_call_us_p50": float(np.median(ctot)),
             "slots_scanned_per_s": slots / (us * 1e-6)}, w
 
 

@@ -462,6 +462,47 @@ int cascade_tier_reclaim(int32_t tier, const cascade_tier_table_t *table, int32_
                          int32_t *placed, void *index, int32_t index_capacity, void *workspace,
                          size_t workspace_bytes, int32_t *status_dev, void *stream);
 
+/* The whole chain HBM -> DRAM -> NVMe of per-tier LRU reclamation (Section
+   4.4, prefix hit detection) in one call: the same results, status word and
+   index updates as cascade_tier_reclaim on tiers 0, 1 and 2 in turn, each
+   tier's outgoing blocks passed as the next tier's incoming ones.  Neither
+   the counting pass nor the histogram pass of a table depends on the tier
+   above, so the call runs each of them once for all three tables, and the
+   deeper tiers' full-table reads overlap the shallower tiers' work (11
+   launches instead of 15).  The demotions it passes between tiers are its
+   own, so it does not check their hashes.
+
+   chain      per tier t: table[t], need[t], freed[t] (device int32[need[t]]);
+              outgoing[t], n_outgoing_dev[t], max_outgoing[t] for t = 0, 1
+              (max_outgoing[0] >= need[0], max_outgoing[1] >= need[1] +
+              max_outgoing[0]); placed[t] for t = 1, 2 (device
+              int32[max_outgoing[t - 1]]), placed[0] unused.  The arguments
+              of each tier follow cascade_tier_reclaim.
+   index      the prefix index (NULL = none) and its capacity.
+   workspace  device memory of cascade_tier_chain_workspace_bytes(n) bytes
+              (n = the three tables' slot counts: the three tiers' workspaces,
+              their fixed-size parts first), 256-byte aligned, zero-filled
+              once before its first use; every call leaves it ready for the
+              next.  A workspace sized for n serves every chain whose tables
+              hold at most n[t] slots.  One call at a time per workspace.
+   status_dev as for cascade_tier_reclaim, one word for the chain.
+   Returns CASCADE_EINVAL for bad host arguments (of any tier), CASCADE_EHIP
+   on a failed launch.  Asynchronous on `stream`. */
+typedef struct {
+  cascade_tier_table_t table[3];
+  int32_t need[3];
+  cascade_demotion_t *outgoing[2];
+  int32_t *n_outgoing_dev[2];
+  int32_t max_outgoing[2];
+  int32_t *freed[3];
+  int32_t *placed[3];
+} cascade_tier_chain_t;
+
+size_t cascade_tier_chain_workspace_bytes(const int32_t *n_slots);
+int cascade_tier_reclaim_chain(const cascade_tier_chain_t *chain, void *index,
+                               int32_t index_capacity, void *workspace, size_t workspace_bytes,
+                               int32_t *status_dev, void *stream);
+
 /* Short English text for a return code or status value. */
 const char *cascade_strerror(int code);
 

@@ -27,6 +27,7 @@ EXPORTED = ["cascade_step_workspace_bytes", "cascade_step", "cascade_step_noallo
             "cascade_pack_unpack", "cascade_prefix_index_bytes", "cascade_prefix_index_clear",
             "cascade_prefix_index_insert", "cascade_prefix_probe", "cascade_restore_from_host",
             "cascade_spill_to_host", "cascade_reclaim_workspace_bytes", "cascade_tier_reclaim",
+            "cascade_tier_chain_workspace_bytes", "cascade_tier_reclaim_chain",
             "cascade_strerror"]
 INDEX_SLOT_BYTES = 16
 
@@ -39,6 +40,13 @@ class TierTable(C.Structure):
 # cascade_demotion_t: hash, last use, source slot (24 bytes)
 DEMOTION_DTYPE = np.dtype([("hash", np.uint64), ("last_use_ns", np.int64),
                            ("src_slot", np.int32), ("pad", np.int32)])
+
+
+class TierChain(C.Structure):
+    _fields_ = [("table", TierTable * 3), ("need", C.c_int32 * 3),
+                ("outgoing", C.c_void_p * 2), ("n_outgoing_dev", C.c_void_p * 2),
+                ("max_outgoing", C.c_int32 * 2), ("freed", C.c_void_p * 3),
+                ("placed", C.c_void_p * 3)]
 
 
 class Requests(C.Structure):
@@ -152,6 +160,12 @@ def load() -> C.CDLL:
                                            C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p,
                                            C.c_void_p, C.c_int32, C.c_void_p, C.c_size_t,
                                            C.c_void_p, C.c_void_p]
+        L.cascade_tier_chain_workspace_bytes.restype = C.c_size_t
+        L.cascade_tier_chain_workspace_bytes.argtypes = [C.POINTER(C.c_int32)]
+        L.cascade_tier_reclaim_chain.restype = C.c_int
+        L.cascade_tier_reclaim_chain.argtypes = [C.POINTER(TierChain), C.c_void_p, C.c_int32,
+                                                 C.c_void_p, C.c_size_t, C.c_void_p,
+                                                 C.c_void_p]
         L.cascade_strerror.restype = C.c_char_p
         L.cascade_strerror.argtypes = [C.c_int]
         _lib = L
@@ -273,6 +287,20 @@ def cascade_tier_reclaim(tier: int, table: TierTable, need: int, incoming: int,
         tier, C.byref(table), need, v(incoming), v(n_incoming_dev), max_incoming, v(outgoing),
         v(n_outgoing_dev), max_outgoing, v(freed), v(placed), v(index), index_capacity,
         v(workspace), workspace_bytes, v(status_dev), v(stream)))
+
+
+def cascade_tier_chain_workspace_bytes(n_slots) -> int:
+    arr = (C.c_int32 * 3)(*[int(x) for x in n_slots])
+    return int(load().cascade_tier_chain_workspace_bytes(arr))
+
+
+def cascade_tier_reclaim_chain(chain: TierChain, index: int, index_capacity: int,
+                               workspace: int, workspace_bytes: int, status_dev: int,
+                               stream: int) -> int:
+    v = C.c_void_p
+    return int(load().cascade_tier_reclaim_chain(C.byref(chain), v(index), index_capacity,
+                                                 v(workspace), workspace_bytes, v(status_dev),
+                                                 v(stream)))
 
 
 def cascade_strerror(code: int) -> str:

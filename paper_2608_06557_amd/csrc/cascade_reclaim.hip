@@ -139,23 +139,30 @@ __host__ __device__ inline long long region_cap(long long n) {
   return (tiles + kListGroups - 1) / kListGroups * kRcTile;
 }
 
-// The counters and histograms come first, at offsets that do not depend on
-// the table size, so one workspace serves tables of any size up to its own.
-size_t workspace_bytes_for(int32_t n) {
-  const size_t tiles = (size_t)std::max(1, tiles_of(n));
-  const size_t slots = (size_t)(kListGroups * region_cap(n));
+// A workspace is a head of fixed size (the plan, counters, histograms and
+// the stage: what must be zero when a call starts, at offsets that do not
+// depend on the table) and a body sized by the table (per-tile records and
+// the list, rewritten before they are read).  One call's workspace is its
+// head then its body, so a workspace sized for n slots serves every table
+// of at most n slots; a chain keeps its three heads first.
+constexpr size_t head_bytes() {
   return align256(sizeof(RcPlan)) + align256(sizeof(unsigned) * (kTicketGroups + 1) * kTicketStride) +
          align256(sizeof(RcPartial) * kRcGridCount) +
          align256(sizeof(unsigned) * kHistCopies * (1 << kDigit0)) +
          align256(sizeof(unsigned) * kRcBins) +
          align256(sizeof(unsigned) * kListGroups * kCountStride) + align256(sizeof(unsigned)) +
-         align256(sizeof(unsigned long long) * kStageCap) + align256(sizeof(unsigned) * kStageCap) +
-         2 * align256(sizeof(int4) * tiles) + 2 * align256(sizeof(unsigned long long) * slots) +
+         align256(sizeof(unsigned long long) * kStageCap) + align256(sizeof(unsigned) * kStageCap);
+}
+size_t body_bytes(int32_t n) {
+  const size_t tiles = (size_t)std::max(1, tiles_of(n));
+  const size_t slots = (size_t)(kListGroups * region_cap(n));
+  return 2 * align256(sizeof(int4) * tiles) + 2 * align256(sizeof(unsigned long long) * slots) +
          2 * align256(sizeof(unsigned) * slots);
 }
+size_t workspace_bytes_for(int32_t n) { return head_bytes() + body_bytes(n); }
 
-RcWork carve(void *ws, int32_t n) {
-  char *p = static_cast<char *>(ws);
+RcWork carve(void *head, void *body, int32_t n) {
+  char *p = static_cast<char *>(head);
   const size_t tiles = (size_t)std::max(1, tiles_of(n));
   const size_t slots = (size_t)(kListGroups * region_cap(n));
   RcWork w;
@@ -176,7 +183,7 @@ RcWork carve(void *ws, int32_t n) {
   w.stage_key = reinterpret_cast<unsigned long long *>(p);
   p += align256(sizeof(unsigned long long) * kStageCap);
   w.stage_ent = reinterpret_cast<unsigned *>(p);
-  p += align256(sizeof(unsigned) * kStageCap);
+  p = static_cast<char *>(body);
   w.rec = reinterpret_cast<int4 *>(p);
   p += align256(sizeof(int4) * tiles);
   w.off = reinterpret_cast<int4 *>(p);
@@ -306,24 +313,32 @@ __device__ __forceinline__ int block_slot_rank(const bool (&f)[kRcItems], int (&
 }
 
 
+// A workgroup's place in the part of the grid that serves one table: its
+// index there and the part's size (the whole grid unless one launch serves
+// several tables).
+struct Part {
+  int block, count;
+};
+__device__ __forceinline__ Part whole_grid() { return {(int)blockIdx.x, (int)gridDim.x}; }
+
 // The workgroup's first tile (nothing is read past the table), loaded
 // before the kernel reads anything else, so the table loads do not wait for it.
-__device__ __forceinline__ Slots8 load_first(const RcArgs &a) {
+__device__ __forceinline__ Slots8 load_first(const RcArgs &a, Part g) {
   Slots8 v;
-  load8(a, slot_base(blockIdx.x), v);
+  load8(a, slot_base(g.block), v);
   return v;
 }
-// Calls f(tile, slots) for this workgroup's tiles (grid-stride), loading the
-// next tile before working on the current one; `first` is the first tile's
-// slots.
+// Calls f(tile, slots) for this workgroup's tiles (part-stride), loading
+// the next tile before working on the current one; `first` is the first
+// tile's slots.
 template <typename F>
-__device__ __forceinline__ void for_tiles(const RcArgs &a, const Slots8 &first, F &&f) {
+__device__ __forceinline__ void for_tiles(const RcArgs &a, Part g, const Slots8 &first, F &&f) {
   const int tiles = max(1, tiles_of(a.n));
-  int t = blockIdx.x;
+  int t = g.block;
   if (t >= tiles) return;
   Slots8 cur = first, nxt;
   for (;;) {
-    const int tn = t + (int)gridDim.x;
+    const int tn = t + g.count;
     if (tn < tiles) load8(a, slot_base(tn), nxt);
     f(t, cur);
     if (tn >= tiles) break;
@@ -331,20 +346,36 @@ __device__ __forceinline__ void for_tiles(const RcArgs &a, const Slots8 &first, 
     t = tn;
   }
 }
+
+// Up to three tables served by one launch of the count or histogram kernel:
+// table k takes workgroups [first[k], first[k + 1]) (first[n] = the grid).
+// A chain of tiers launches these two passes once for all its tables, since
+// neither depends on the tier above.
+struct RcTables {
+  RcArgs t[3];
+  int n;
+  int first[3];
+  int check_in;  // count kernel: check the incoming hashes (one call per tier)
+};
+// Calls f(table, part) for the table this workgroup serves (constant
+// indices into the launch's arguments, one branch per table).
 template <typename F>
-__device__ __forceinline__ void for_tiles(const RcArgs &a, F &&f) {
-  for_tiles(a, load_first(a), f);
+__device__ __forceinline__ void with_table(const RcTables &m, F &&f) {
+  const int b = (int)blockIdx.x, grid = (int)gridDim.x;
+  if (m.n > 2 && b >= m.first[2]) f(m.t[2], Part{b - m.first[2], grid - m.first[2]});
+  else if (m.n > 1 && b >= m.first[1])
+    f(m.t[1], Part{b - m.first[1], (m.n > 2 ? m.first[2] : grid) - m.first[1]});
+  else f(m.t[0], Part{b, m.n > 1 ? m.first[1] : grid});
 }
 
 // ------------------------------------------------------------- count kernel
 
-__global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
-  __shared__ int s_red[kWaves * 3];
-  __shared__ unsigned long long s_mm[kWaves * 2];
+__device__ __forceinline__ void count_table(const RcArgs &a, Part g, bool check_in, int *s_red,
+                                            unsigned long long *s_mm) {
   int cnt[3] = {0, 0, 0};  // empty free, cached free, bad data (negative last use, hash 0 in)
   unsigned long long mn = ~0ull, mx = 0ull;
-  const int n_in_all = a.n_in_dev ? load_agent(a.n_in_dev) : 0;
-  for_tiles(a, [&](int, const Slots8 &v) {  // past the table: held, stamp 0
+  const int n_in_all = check_in && a.n_in_dev ? load_agent(a.n_in_dev) : 0;
+  for_tiles(a, g, load_first(a, g), [&](int, const Slots8 &v) {  // past the table: held, stamp 0
 #pragma unroll
     for (int j = 0; j < kRcItems; ++j) {
       const long long lu = v.lu[j];
@@ -358,9 +389,9 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
     }
   });
   // this workgroup's share of the incoming blocks: none may have hash 0
+  // (a chain's own demotions never do, and are not checked)
   if (n_in_all >= 0 && n_in_all <= a.max_in)
-    for (int j = (int)(blockIdx.x * kBlock + threadIdx.x); j < n_in_all;
-         j += (int)(gridDim.x * kBlock))
+    for (int j = g.block * kBlock + (int)threadIdx.x; j < n_in_all; j += g.count * kBlock)
       cnt[2] |= a.incoming[j].hash == 0ull;
   block_sum<3, int>(cnt, s_red);
   mn = wave_min(mn);
@@ -370,12 +401,12 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
     s_mm[wave_id() * 2 + 1] = mx;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {  // read by the next kernel
+  if (threadIdx.x == 0) {  // read by the later kernels
     for (int w = 1; w < kWaves; ++w) {
       mn = min(mn, s_mm[w * 2]);
       mx = max(mx, s_mm[w * 2 + 1]);
     }
-    RcPartial *p = a.w.partial + blockIdx.x;
+    RcPartial *p = a.w.partial + g.block;
     p->n_empty = cnt[0];
     p->n_cached = cnt[1];
     p->bad = cnt[2];
@@ -384,19 +415,25 @@ __global__ __launch_bounds__(kBlock) void rc_count_kernel(RcArgs a) {
   }
 }
 
-// The call's plan from the count kernel's partials, computed alike by every
-// workgroup that needs it: the checks (an earlier failure in the chain, bad
-// data, room), then which slots are reclaimed and the key's size.
-struct PlanCalc {
-  int err;   // 0, 1 (an earlier call failed) or a negative code
-  int total, n_in, mode, width, shift, dbits, rank;
+// Per workgroup of a table: counts of empty and cached free slots, the
+// cached last-use range and bad data, as one partial record.
+__global__ __launch_bounds__(kBlock) void rc_count_kernel(RcTables m) {
+  __shared__ int s_red[kWaves * 3];
+  __shared__ unsigned long long s_mm[kWaves * 2];
+  with_table(m, [&](const RcArgs &a, Part g) { count_table(a, g, m.check_in != 0, s_red, s_mm); });
+}
+
+// The table's totals from the count kernel's partials, computed alike by
+// every workgroup that needs them: free slots, bad data, the cached
+// last-use range and the key's size.
+struct RangeCalc {
+  int n_empty, n_cached, bad;
+  int width, shift, dbits;
   unsigned long long lu_min;
 };
-__device__ __forceinline__ PlanCalc plan_of(const RcArgs &a, int *s_red,
-                                            unsigned long long *s_mm) {
+__device__ __forceinline__ RangeCalc range_of(const RcArgs &a, int *s_red,
+                                              unsigned long long *s_mm) {
   const int g_count = min(max(1, tiles_of(a.n)), kRcGridCount);
-  const int status_was = load_agent(a.status);
-  const int n_in = a.n_in_dev ? load_agent(a.n_in_dev) : 0;
   int tot[3] = {0, 0, 0};
   unsigned long long tmn = ~0ull, tmx = 0ull;
   static_assert(kRcGridCount % kBlock == 0, "whole rounds of partials");
@@ -426,67 +463,64 @@ __device__ __forceinline__ PlanCalc plan_of(const RcArgs &a, int *s_red,
     tmx = max(tmx, s_mm[w * 2 + 1]);
   }
   __syncthreads();
+  RangeCalc r;
+  r.n_empty = tot[0];
+  r.n_cached = tot[1];
+  r.bad = tot[2];
+  r.lu_min = tmn;
+  r.width = tot[1] > 0 ? bit_width64(1ull + (tmx - tmn)) : 0;
+  r.dbits = min(r.width, kDigit0);
+  r.shift = r.width - r.dbits;
+  return r;
+}
+
+// The call's plan: the checks (an earlier failure in the chain, bad data,
+// the incoming count, room), then which slots are reclaimed.
+struct PlanCalc {
+  int err;   // 0, 1 (an earlier call failed) or a negative code
+  int total, n_in, mode, rank;
+};
+__device__ __forceinline__ PlanCalc plan_of(const RcArgs &a, const RangeCalc &r, int status_was,
+                                            int n_in) {
   PlanCalc c;
   c.err = status_was != CASCADE_OK ? 1 : 0;
-  if (c.err == 0 && (tot[2] || n_in < 0 || n_in > a.max_in)) c.err = CASCADE_EINVAL;
+  if (c.err == 0 && (r.bad || n_in < 0 || n_in > a.max_in)) c.err = CASCADE_EINVAL;
   const long long total = (long long)a.need + n_in;
-  if (c.err == 0 && total > (long long)tot[0] + tot[1]) c.err = CASCADE_ENOSPC;
+  if (c.err == 0 && total > (long long)r.n_empty + r.n_cached) c.err = CASCADE_ENOSPC;
   c.total = (int)total;
   c.n_in = n_in;
-  c.lu_min = tmn;
-  if (total <= tot[0]) {
+  if (total <= r.n_empty) {
     // empty slots suffice: the first `total` of them in slot order
     c.mode = kModeEmpty;
-    c.width = c.shift = c.dbits = 0;
     c.rank = (int)total - 1;
   } else {
     // every empty slot plus the (total - n_empty) least recent cached ones
     c.mode = kModeCached;
-    c.width = bit_width64(1ull + (tmx - tmn));
-    c.dbits = min(c.width, kDigit0);
-    c.shift = c.width - c.dbits;
-    c.rank = (int)(total - tot[0] - 1);
+    c.rank = (int)(total - r.n_empty - 1);
   }
   return c;
 }
 
 // ------------------------------------------------------------ top digit
 
-// Every workgroup derives the plan from the count kernel's partials
-// (workgroup 0 stores it for the later kernels and reports a failed check),
-// then, when cached blocks are reclaimed, adds its tiles to the histogram of
-// the key's top digit (8 copies, workgroup b adds to copy b % 8).
-__global__ __launch_bounds__(kBlock) void rc_hist_kernel(RcArgs a) {
+// Every workgroup of a table derives the cached last-use range from the
+// count kernel's partials, then adds its tiles to the histogram of the
+// key's top digit (8 copies, workgroup b adds to copy b % 8).  The
+// histogram is built whether or not the call will need cached blocks (that
+// depends on the incoming count, known only when the tier above is done).
+__device__ __forceinline__ void hist_table(const RcArgs &a, Part g, unsigned *s_hist, int *s_red,
+                                           unsigned long long *s_mm) {
   constexpr int kBins0 = 1 << kDigit0;
   static_assert(kBins0 == kBlock, "one bin per thread");
-  __shared__ unsigned s_hist[kBins0];
-  __shared__ int s_red[kWaves * 3];
-  __shared__ unsigned long long s_mm[kWaves * 2];
-  const Slots8 first = load_first(a);
-  const PlanCalc c = plan_of(a, s_red, s_mm);
+  const Slots8 first = load_first(a, g);
+  const RangeCalc r = range_of(a, s_red, s_mm);
   const int t = threadIdx.x;
-  if (blockIdx.x == 0 && t == 0) {
-    if (c.err < 0) store_agent(a.status, c.err);
-    RcPlan *P = a.w.plan;
-    P->ok = c.err == 0;
-    P->total = c.total;
-    P->n_in = c.n_in;
-    P->mode = c.mode;
-    P->width = c.width;
-    P->shift = c.shift;
-    P->dbits = c.dbits;
-    P->rank = c.rank;
-    P->bucket = 0;
-    P->tie_slot = -1;
-    P->lu_min = c.lu_min;
-    P->thresh = 0ull;
-  }
-  if (c.err != 0 || c.mode != kModeCached) return;  // uniform: every workgroup computes c alike
-  const int shift = c.shift;
-  const unsigned long long lu_min = c.lu_min;
+  if (r.bad || r.n_cached == 0) return;  // uniform: every workgroup computes r alike
+  const int shift = r.shift;
+  const unsigned long long lu_min = r.lu_min;
   s_hist[t] = 0u;
   __syncthreads();
-  for_tiles(a, first, [&](int, const Slots8 &v) {
+  for_tiles(a, g, first, [&](int, const Slots8 &v) {
 #pragma unroll
     for (int j = 0; j < kRcItems; ++j) {
       if (v.held[j] || v.h[j] == 0ull) continue;  // only cached free slots have keys above 0
@@ -497,7 +531,14 @@ __global__ __launch_bounds__(kBlock) void rc_hist_kernel(RcArgs a) {
   });
   __syncthreads();
   const unsigned v = s_hist[t];
-  if (v) atomicAdd(a.w.hist + (blockIdx.x % kHistCopies) * kBins0 + t, v);
+  if (v) atomicAdd(a.w.hist + (g.block % kHistCopies) * kBins0 + t, v);
+}
+
+__global__ __launch_bounds__(kBlock) void rc_hist_kernel(RcTables m) {
+  __shared__ unsigned s_hist[1 << kDigit0];
+  __shared__ int s_red[kWaves * 3];
+  __shared__ unsigned long long s_mm[kWaves * 2];
+  with_table(m, [&](const RcArgs &a, Part g) { hist_table(a, g, s_hist, s_red, s_mm); });
 }
 
 // ------------------------------------------------------------ compaction
@@ -572,22 +613,47 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
   __shared__ unsigned s_sub[kRcBins];
   __shared__ unsigned long long s_look[kRcTile];
   __shared__ int s_rank[kWaves];
-  __shared__ int s_red[kWaves * 2];
+  __shared__ int s_red[kWaves * 3];
+  __shared__ unsigned long long s_mm[kWaves * 2];
   __shared__ int s_start;
   __shared__ int s_found[2];
-  const Slots8 first = load_first(a);
+  const Part g = whole_grid();
+  const Slots8 first = load_first(a, g);
   const int t = threadIdx.x;
-  // the top digit's histogram, requested with the plan (used when cached)
+  // the top digit's histogram, the status and the incoming count, requested
+  // with the partials (the histogram is used when cached blocks are needed)
   constexpr int kBins0 = 1 << kDigit0;
   static_assert(kBins0 == kBlock, "one bin per thread");
   unsigned hv[kHistCopies];
 #pragma unroll
   for (int c = 0; c < kHistCopies; ++c) hv[c] = load_agent(a.w.hist + c * kBins0 + t);
+  const int status_was = load_agent(a.status);
+  const int n_in = a.n_in_dev ? load_agent(a.n_in_dev) : 0;
+  // the call's plan, alike in every workgroup; workgroup 0 stores it for
+  // the later kernels and reports a failed check
+  const RangeCalc rg = range_of(a, s_red, s_mm);
+  const PlanCalc pc = plan_of(a, rg, status_was, n_in);
   RcPlan *P = a.w.plan;
-  const int ok = P->ok, mode = P->mode, shift = P->shift, rank = P->rank;
-  const unsigned long long lu_min = P->lu_min;
-  if (!ok) return;
-  const bool cached = mode == kModeCached;
+  if (blockIdx.x == 0 && t == 0) {
+    if (pc.err < 0) store_agent(a.status, pc.err);
+    P->ok = pc.err == 0;
+    P->total = pc.total;
+    P->n_in = pc.n_in;
+    P->mode = pc.mode;
+    P->width = rg.width;
+    P->shift = rg.shift;
+    P->dbits = rg.dbits;
+    P->rank = pc.rank;
+    P->bucket = 0;
+    P->brank = 0;
+    P->tie_slot = -1;
+    P->lu_min = rg.lu_min;
+    P->thresh = 0ull;
+  }
+  if (pc.err != 0) return;  // uniform
+  const bool cached = pc.mode == kModeCached;
+  const int shift = rg.shift, rank = pc.rank;
+  const unsigned long long lu_min = rg.lu_min;
   unsigned long long bucket = 0;
   if (cached) {
     // the bucket holding the sought rank, from the histogram's copies
@@ -611,7 +677,7 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
       return;
     }
     bucket = (unsigned long long)s_found[0];
-    if (blockIdx.x == 0 && t == 0) {  // P->rank stays: the other workgroups read it
+    if (blockIdx.x == 0 && t == 0) {
       P->bucket = s_found[0];
       P->brank = s_found[1];
     }
@@ -621,7 +687,7 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
   if (d2 > 0)
     for (int b = t; b < (1 << d2); b += kBlock) s_sub[b] = 0u;
   __syncthreads();
-  for_tiles(a, first, [&](int tile, const Slots8 &v) {
+  for_tiles(a, g, first, [&](int tile, const Slots8 &v) {
     bool f[kRcItems], sure[kRcItems];
     unsigned long long k[kRcItems];
 #pragma unroll
@@ -1212,13 +1278,15 @@ extern "C" size_t cascade_reclaim_workspace_bytes(int32_t n_slots) {
   return workspace_bytes_for(n_slots);
 }
 
-extern "C" int cascade_tier_reclaim(int32_t tier, const cascade_tier_table_t *table, int32_t need,
-                                    const cascade_demotion_t *incoming,
-                                    const int32_t *n_incoming_dev, int32_t max_incoming,
-                                    cascade_demotion_t *outgoing, int32_t *n_outgoing_dev,
-                                    int32_t max_outgoing, int32_t *freed, int32_t *placed,
-                                    void *index, int32_t index_capacity, void *workspace,
-                                    size_t workspace_bytes, int32_t *status_dev, void *stream) {
+namespace cascade {
+namespace {
+
+// One tier's host-side checks and kernel arguments (CASCADE_OK or EINVAL).
+int tier_args(int32_t tier, const cascade_tier_table_t *table, int32_t need,
+              const cascade_demotion_t *incoming, const int32_t *n_incoming_dev,
+              int32_t max_incoming, cascade_demotion_t *outgoing, int32_t *n_outgoing_dev,
+              int32_t max_outgoing, int32_t *freed, int32_t *placed, void *index,
+              int32_t index_capacity, void *head, void *body, int32_t *status_dev, RcArgs &a) {
   if (tier < 0 || tier > 2 || !table || need < 0 || max_incoming < 0 || !status_dev ||
       (long long)need + max_incoming > INT_MAX)
     return CASCADE_EINVAL;
@@ -1237,10 +1305,6 @@ extern "C" int cascade_tier_reclaim(int32_t tier, const cascade_tier_table_t *ta
   }
   if (index && (!index_capacity_ok(index_capacity) || ((uintptr_t)index & 15)))
     return CASCADE_EINVAL;
-  if (!workspace || ((uintptr_t)workspace & 255) || workspace_bytes < workspace_bytes_for(n))
-    return CASCADE_EINVAL;
-
-  RcArgs a;
   a.tier = tier;
   a.n = n;
   a.need = need;
@@ -1258,16 +1322,98 @@ extern "C" int cascade_tier_reclaim(int32_t tier, const cascade_tier_table_t *ta
   a.index = static_cast<IndexSlot *>(index);
   a.index_mask = index ? (unsigned)(index_capacity - 1) : 0u;
   a.status = status_dev;
-  a.w = carve(workspace, n);
+  a.w = carve(head, body, n);
+  return CASCADE_OK;
+}
 
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const int tiles = std::max(1, tiles_of(n));
-  hipLaunchKernelGGL(rc_count_kernel, dim3(std::min(tiles, kRcGridCount)), dim3(kBlock), 0, s,
-                     a);
-  hipLaunchKernelGGL(rc_hist_kernel, dim3(std::min(tiles, kRcGridHist)), dim3(kBlock), 0, s, a);
+int tiles_or_one(const RcArgs &a) { return std::max(1, tiles_of(a.n)); }
+
+// The compaction, selection and writes of one tier's call.
+void launch_tail(const RcArgs &a, hipStream_t s) {
+  const int tiles = tiles_or_one(a);
   hipLaunchKernelGGL(rc_compact_kernel, dim3(std::min(tiles, kRcGridCompact)), dim3(kBlock), 0, s,
                      a);
   hipLaunchKernelGGL(rc_select_kernel, dim3(kSelGrid), dim3(kBlock), 0, s, a);
   hipLaunchKernelGGL(rc_write_kernel, dim3(tiles), dim3(kBlock), 0, s, a);
+}
+
+// The count and histogram passes over m.n tables, one launch each.
+void launch_head(RcTables &m, hipStream_t s) {
+  int gc = 0, gh = 0;
+  int first_h[3] = {0, 0, 0};
+  for (int k = 0; k < m.n; ++k) {
+    m.first[k] = gc;
+    first_h[k] = gh;
+    gc += std::min(tiles_or_one(m.t[k]), kRcGridCount);
+    gh += std::min(tiles_or_one(m.t[k]), kRcGridHist);
+  }
+  hipLaunchKernelGGL(rc_count_kernel, dim3(gc), dim3(kBlock), 0, s, m);
+  for (int k = 0; k < m.n; ++k) m.first[k] = first_h[k];
+  hipLaunchKernelGGL(rc_hist_kernel, dim3(gh), dim3(kBlock), 0, s, m);
+}
+
+}  // namespace
+}  // namespace cascade
+
+extern "C" int cascade_tier_reclaim(int32_t tier, const cascade_tier_table_t *table, int32_t need,
+                                    const cascade_demotion_t *incoming,
+                                    const int32_t *n_incoming_dev, int32_t max_incoming,
+                                    cascade_demotion_t *outgoing, int32_t *n_outgoing_dev,
+                                    int32_t max_outgoing, int32_t *freed, int32_t *placed,
+                                    void *index, int32_t index_capacity, void *workspace,
+                                    size_t workspace_bytes, int32_t *status_dev, void *stream) {
+  if (!table || table->n_slots < 0 || table->n_slots > (1 << 30) || !workspace ||
+      ((uintptr_t)workspace & 255) || workspace_bytes < workspace_bytes_for(table->n_slots))
+    return CASCADE_EINVAL;
+  RcTables m{};
+  char *ws = static_cast<char *>(workspace);
+  const int rc = tier_args(tier, table, need, incoming, n_incoming_dev, max_incoming, outgoing,
+                           n_outgoing_dev, max_outgoing, freed, placed, index, index_capacity,
+                           ws, ws + head_bytes(), status_dev, m.t[0]);
+  if (rc != CASCADE_OK) return rc;
+  m.n = 1;
+  m.check_in = 1;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  launch_head(m, s);
+  launch_tail(m.t[0], s);
+  return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
+}
+
+extern "C" size_t cascade_tier_chain_workspace_bytes(const int32_t *n_slots) {
+  if (!n_slots) return 0;
+  size_t total = 0;
+  for (int t = 0; t < 3; ++t) {
+    if (n_slots[t] < 0 || n_slots[t] > (1 << 30)) return 0;
+    total += workspace_bytes_for(n_slots[t]);  // each a multiple of 256 bytes
+  }
+  return total;  // three heads, then three bodies
+}
+
+extern "C" int cascade_tier_reclaim_chain(const cascade_tier_chain_t *c, void *index,
+                                          int32_t index_capacity, void *workspace,
+                                          size_t workspace_bytes, int32_t *status_dev,
+                                          void *stream) {
+  if (!c || !workspace || ((uintptr_t)workspace & 255)) return CASCADE_EINVAL;
+  const int32_t n[3] = {c->table[0].n_slots, c->table[1].n_slots, c->table[2].n_slots};
+  const size_t need_bytes = cascade_tier_chain_workspace_bytes(n);
+  if (need_bytes == 0 || workspace_bytes < need_bytes) return CASCADE_EINVAL;
+  RcTables m{};
+  char *ws = static_cast<char *>(workspace);
+  char *body = ws + 3 * head_bytes();  // the heads at fixed offsets, whatever the tables
+  for (int t = 0; t < 3; ++t) {
+    const int rc = tier_args(
+        t, &c->table[t], c->need[t], t > 0 ? c->outgoing[t - 1] : nullptr,
+        t > 0 ? c->n_outgoing_dev[t - 1] : nullptr, t > 0 ? c->max_outgoing[t - 1] : 0,
+        t < 2 ? c->outgoing[t] : nullptr, t < 2 ? c->n_outgoing_dev[t] : nullptr,
+        t < 2 ? c->max_outgoing[t] : 0, c->freed[t], c->placed[t], index, index_capacity,
+        ws + t * head_bytes(), body, status_dev, m.t[t]);
+    if (rc != CASCADE_OK) return rc;
+    body += body_bytes(n[t]);
+  }
+  m.n = 3;
+  m.check_in = 0;  // each tier's incoming blocks are the chain's own demotions
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  launch_head(m, s);
+  for (int t = 0; t < 3; ++t) launch_tail(m.t[t], s);
   return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
 }

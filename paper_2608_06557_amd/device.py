@@ -316,6 +316,35 @@ class DeviceTiers:
                 return rc
         return 0
 
+    def chain_args(self):
+        """The chain call's arguments over the same buffers, with a workspace
+        of its own (the three per-tier workspaces back to back)."""
+        torch = _torch()
+        if getattr(self, "ws_chain", None) is None:
+            self.ws_chain_bytes = cx.cascade_tier_chain_workspace_bytes(self.n)
+            self.ws_chain = torch.zeros(self.ws_chain_bytes, dtype=torch.uint8,
+                                        device=self.device)
+            c = cx.TierChain()
+            for t in range(3):
+                c.table[t] = self.tabs[t]
+                c.need[t] = self.needs[t]
+                c.freed[t] = self.freed[t].data_ptr()
+                c.placed[t] = self.placed[t].data_ptr() if t > 0 else 0
+            for t in range(2):
+                c.outgoing[t] = self.out[t].data_ptr()
+                c.n_outgoing_dev[t] = self.n_out[t:t + 1].data_ptr()
+                c.max_outgoing[t] = self.max_out[t]
+            self.chain = c
+        return self.chain
+
+    def run_chain(self, stream=None) -> int:
+        """The whole chain in one cascade_tier_reclaim_chain call."""
+        c = self.chain_args()
+        return cx.cascade_tier_reclaim_chain(
+            c, self.index.data_ptr() if self.index is not None else 0, self.capacity,
+            self.ws_chain.data_ptr(), self.ws_chain_bytes, self.status.data_ptr(),
+            stream_handle(stream))
+
     def fetch(self) -> dict:
         torch = _torch()
         torch.cuda.synchronize(self.device)

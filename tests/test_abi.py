@@ -44,6 +44,7 @@ STRUCTS = {
     "cascade_tier_state_t": cascade.TierState, "cascade_params_t": cascade.Params,
     "cascade_move_t": cascade.Move, "cascade_outputs_t": cascade.Outputs,
     "cascade_kv_pool_t": cascade.KvPool, "cascade_tier_table_t": cascade.TierTable,
+    "cascade_tier_chain_t": cascade.TierChain,
 }
 
 
@@ -251,3 +252,47 @@ def test_reclaim_host_checks(lib):
     assert call(need=2**31 - 1, max_in=1, inc=fake, n_inc=fake, placed=fake) == E
     # NVMe demotes nothing: no outgoing room needed, but the rest still checked
     assert call(tier=2, max_out=0, out=0, n_out=0, wsb=ws_bytes - 1) == E
+
+
+def test_reclaim_chain_host_checks(lib):
+    fake = 4096  # never dereferenced: every case below fails a host-side check
+    n = [100, 200, 300]
+    wsb = cascade.cascade_tier_chain_workspace_bytes(n)
+    assert wsb == sum(cascade.cascade_reclaim_workspace_bytes(x) for x in n)
+    assert cascade.cascade_tier_chain_workspace_bytes([100, -1, 300]) == 0
+    assert cascade.cascade_tier_chain_workspace_bytes([100, 200, (1 << 30) + 1]) == 0
+
+    def chain(**kw):
+        c = cascade.TierChain()
+        for t in range(3):
+            c.table[t] = cascade.TierTable(n[t], fake, fake, fake)
+            c.need[t] = 10
+            c.freed[t] = fake
+            c.placed[t] = fake if t > 0 else 0
+        for t in range(2):
+            c.outgoing[t] = fake
+            c.n_outgoing_dev[t] = fake
+        c.max_outgoing[0] = 10
+        c.max_outgoing[1] = 20
+        for k, v in kw.items():
+            t, f, x = v
+            getattr(c, f)[t] = x
+        return c
+
+    def call(c=None, ws=fake * 2, b=wsb, status=fake):
+        return cascade.cascade_tier_reclaim_chain(c if c is not None else chain(), 0, 0, ws, b,
+                                                  status, 0)
+
+    E = cascade.EINVAL
+    assert call(b=wsb - 1) == E                     # room for three workspaces
+    assert call(ws=0) == E
+    assert call(ws=fake + 16) == E                  # not 256-byte aligned
+    assert call(status=0) == E
+    assert call(chain(a=(1, "need", -1))) == E
+    assert call(chain(a=(0, "max_outgoing", 9))) == E   # tier 0: room for its demotions
+    assert call(chain(a=(1, "max_outgoing", 19))) == E  # tier 1: need + tier 0's demotions
+    assert call(chain(a=(2, "placed", 0))) == E          # tier 2 receives tier 1's demotions
+    assert call(chain(a=(2, "freed", 0))) == E
+    bad = chain()
+    bad.table[1] = cascade.TierTable(200, fake + 8, fake, fake)  # misaligned
+    assert call(bad) == E

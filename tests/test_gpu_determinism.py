@@ -56,10 +56,12 @@ def test_step_repeats_bit_for_bit(dev, cfg):
         assert _same(outs, first), f"config {cfg}: run {k + 1} differs from the first"
 
 
-def test_tier_chain_repeats_bit_for_bit(dev):
+@pytest.mark.parametrize("one_call", [False, True], ids=["per_tier", "chain_call"])
+def test_tier_chain_repeats_bit_for_bit(dev, one_call):
     import paper_2608_06557_amd.synth as synth
     w = synth.make_tier_workload(2)
     d = dev.DeviceTiers(w["tables"], w["needs"], w["index_keys"], w["index_masks"])
+    run = d.run_chain if one_call else d.run
     keep = _snapshot(d.bh + d.lu + [d.index])
     outs = d.bh + d.lu + [d.index] + d.out + [d.n_out] + d.freed + d.placed
 
@@ -73,12 +75,13 @@ def test_tier_chain_repeats_bit_for_bit(dev):
         d.status.zero_()
 
     reset()
-    assert d.run() == 0
+    assert run() == 0
     assert int(d.status.item()) == 0
     first = _snapshot(outs)
-    print(f"tier chain {w['sizes']} x {REPS}", flush=True)
+    print(f"tier chain {w['sizes']} x {REPS} ({'one call' if one_call else 'per tier'})",
+          flush=True)
     for k in range(REPS):
         reset()
-        assert d.run() == 0
+        assert run() == 0
         assert _same(outs, first), f"tier chain: run {k + 1} differs from the first"
     assert int(d.status.item()) == 0

@@ -84,7 +84,8 @@ def test_step_and_copies_replay_like_eager(dev, cfg):
         assert torch.equal(pst, want_pst), (cfg, r)
 
 
-def test_tier_chain_replays_like_eager(dev):
+@pytest.mark.parametrize("one_call", [False, True], ids=["per_tier", "chain_call"])
+def test_tier_chain_replays_like_eager(dev, one_call):
     import torch
     w = synth.make_tier_workload(0, seed=77, sizes=(6000, 9000, 20000), needs=(1200, 500, 30),
                                  held=(0.3, 0.1, 0.05), empty=(0.01, 0.01, 0.01))
@@ -104,14 +105,16 @@ def test_tier_chain_replays_like_eager(dev):
             d.placed[t].fill_(-1)
         torch.cuda.synchronize()
 
+    run = d.run_chain if one_call else d.run
+    d.chain_args()  # the chain call's workspace, allocated outside the capture
     restore()
-    assert d.run(s) == 0
+    assert run(s) == 0
     ref = d.fetch()
     assert ref["status"] == 0
     restore()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=s):
-        assert d.run(s) == 0
+        assert run(s) == 0
     for r in range(4):
         restore()
         with torch.cuda.stream(s):

@@ -42,12 +42,34 @@ def oracle_chain(w, tiers=(0, 1, 2)):
     return rc, outs, masks
 
 
-def run_both(dev, w, index=True):
-    d = dev.DeviceTiers(w["tables"], w["needs"],
-                        w["index_keys"] if index else None,
-                        w["index_masks"] if index else None)
+def assert_same_results(g, h, label=""):
+    """Two device runs of a chain gave the same status, outputs and index."""
+    assert g["status"] == h["status"], (label, g["status"], h["status"])
+    for t in range(3):
+        a, b = g["tiers"][t], h["tiers"][t]
+        assert a["n_outgoing"] == b["n_outgoing"], (label, t)
+        for k in ["freed", "placed", "block_hash", "last_use_ns"]:
+            assert np.array_equal(a[k], b[k]), (label, t, k)
+        assert np.array_equal(a["outgoing"].view(np.uint8), b["outgoing"].view(np.uint8)), \
+            (label, t)
+    assert ("index" in g) == ("index" in h)
+    if "index" in g:
+        for x, y in zip(g["index"], h["index"]):
+            assert np.array_equal(x, y), label
+
+
+def run_both(dev, w, index=True, capacity=None):
+    """The chain as three per-tier calls and as one chain call (each on
+    tables of its own), checked equal to each other; the per-tier results,
+    the oracle's and the per-tier DeviceTiers are returned."""
+    keys = w["index_keys"] if index else None
+    masks = w["index_masks"] if index else None
+    d = dev.DeviceTiers(w["tables"], w["needs"], keys, masks, capacity=capacity)
     assert d.run() == 0
     g = d.fetch()
+    dc = dev.DeviceTiers(w["tables"], w["needs"], keys, masks, capacity=capacity)
+    assert dc.run_chain() == 0
+    assert_same_results(g, dc.fetch(), "one chain call")
     ow = dict(w)
     if not index:
         ow["index_keys"] = ow["index_masks"] = None
@@ -123,11 +145,7 @@ def test_nearly_full_index(dev):
     keys = len(w["index_keys"])
     cap = 1 << int(np.ceil(np.log2(keys + 1)))
     assert keys / cap > 0.85, keys / cap
-    d = dev.DeviceTiers(w["tables"], w["needs"], w["index_keys"], w["index_masks"],
-                        capacity=cap)
-    assert d.run() == 0
-    g = d.fetch()
-    rc, outs, masks = oracle_chain(w)
+    g, rc, outs, masks, _ = run_both(dev, w, capacity=cap)
     assert rc == 0
     assert_chain_same(w, g, rc, outs, masks, "index at load 0.9")
     assert outs[0]["n_outgoing"] > 0 and outs[1]["n_outgoing"] > 0
@@ -282,6 +300,26 @@ def test_workspace_reused_across_calls(dev):
     rc, outs, masks = oracle_chain(w2)
     assert_chain_same(w2, g2, rc, outs, masks, "second")
     torch.cuda.synchronize()
+
+
+def test_chain_workspace_reused_across_calls(dev):
+    # the same for one chain call per chain: a workspace sized for the first
+    # chain's tables serves a second chain over smaller ones
+    w1 = small(53, (9000, 12000, 15000), (2000, 900, 50))
+    d = dev.DeviceTiers(w1["tables"], w1["needs"], w1["index_keys"], w1["index_masks"])
+    assert d.run_chain() == 0
+    g1 = d.fetch()
+    rc, outs, masks = oracle_chain(w1)
+    assert_chain_same(w1, g1, rc, outs, masks, "first chain call")
+    w2 = small(54, (3000, 2500, 2100), (700, 300, 20))
+    d2 = dev.DeviceTiers(w2["tables"], w2["needs"], w2["index_keys"], w2["index_masks"])
+    d2.chain_args()
+    d2.ws_chain = d.ws_chain  # the first call's workspace, as it left it
+    d2.ws_chain_bytes = d.ws_chain_bytes
+    assert d2.run_chain() == 0
+    g2 = d2.fetch()
+    rc, outs, masks = oracle_chain(w2)
+    assert_chain_same(w2, g2, rc, outs, masks, "second chain call")
 
 
 def test_lookup_after_reclaim_reads_the_new_tiers(dev):
