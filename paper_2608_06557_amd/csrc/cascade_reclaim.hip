@@ -10,24 +10,24 @@
 // slots per thread with 16-byte loads, three times per call:
 //
 //   rc_count_kernel    per-workgroup counts of empty / cached free slots and
-//                      the cached last-use range, and a share of the incoming
-//                      blocks' hashes checked
-//   rc_hist_kernel     every workgroup derives the plan from those counts
-//                      (the checks, the key's size; workgroup 0 stores it),
-//                      then, when cached blocks are needed, adds its tiles to
-//                      a histogram of the key's top digit, 8 bits
-//   rc_compact_kernel  every workgroup finds the bucket holding the threshold
-//                      in that histogram, then per tile, in slot order: the
-//                      slots certainly reclaimed
-//                      (empty ones, keys below the bucket) and the candidates
-//                      (keys inside it; with empty slots alone enough, the
-//                      empty slots), each with its key, its block and, on
-//                      tiers 0 and 1, its index slot and whether it is
-//                      demoted (the index as it was when the call began), in
-//                      one chunk of a list
-//                      reserved with one atomic add on one of 16 region
-//                      counters; a histogram of the candidates' next 12-bit
-//                      digit
+//                      the cached last-use range, and (one call per tier) a
+//                      share of the incoming blocks' hashes checked
+//   rc_hist_kernel     every workgroup derives the cached last-use range and
+//                      the key's size from those counts, then adds its tiles
+//                      to a histogram of the key's top digit, 8 bits
+//   rc_compact_kernel  every workgroup derives the call's plan from the
+//                      counts and the incoming count (the checks, which
+//                      slots are reclaimed; workgroup 0 stores it) and finds
+//                      the bucket holding the threshold in that histogram,
+//                      then per tile, in slot order: the slots certainly
+//                      reclaimed (empty ones, keys below the bucket) and the
+//                      candidates (keys inside it; with empty slots alone
+//                      enough, the empty slots), each with its key, its block
+//                      and, on tiers 0 and 1, its index slot and whether it
+//                      is demoted (the index as it was when the call began),
+//                      in one chunk of a list reserved with one atomic add on
+//                      one of 16 region counters; a histogram of the
+//                      candidates' next 12-bit digit
 //
 // Then, over the list only:
 //
@@ -50,9 +50,15 @@
 // by a last workgroup: each kernel recomputes what it needs from the
 // previous one's output (the plan from the counts, the bucket from the
 // histogram).  The plan lives in the caller's workspace; every kernel after
-// the histogram reads it and returns at once when the call failed or has
+// the compaction reads it and returns at once when the call failed or has
 // nothing left to do, so the host launches a fixed sequence and never waits.
 // Counters and histograms are reset by the kernel after their last reader.
+//
+// Neither the count nor the histogram pass depends on the tier above (a
+// tier's table changes only in its own write kernel; the incoming count is
+// first needed by the compaction), so a chain HBM -> DRAM -> NVMe in one call
+// launches each of those two passes once for all three tables, then the
+// rest tier by tier.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <stdint.h>
