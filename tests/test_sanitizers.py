@@ -103,7 +103,8 @@ def test_library_host_code_under_asan_and_ubsan(tmp_path):
         from tests import test_zz_no_alloc as z
         for c in [t.test_workspace_size, t.test_host_checks_return_einval_without_launch,
                   t.test_copy_host_checks, t.test_fused_copy_host_checks,
-                  t.test_reclaim_workspace_size, t.test_reclaim_host_checks]:
+                  t.test_reclaim_workspace_size, t.test_reclaim_host_checks,
+                  t.test_reclaim_chain_host_checks]:
             c(lib)
         z.test_noalloc_refuses_a_queue_over_its_limit()
         for code in range(-6, 2):
