@@ -125,6 +125,10 @@ CASES = [
     ((2049, 4096, 6150), (900, 500, 0)),
     ((5000, 9000, 20011), (1500, 700, 300)),
     ((300, 301, 1999), (100, 37, 5)),
+    # a tier with no slots at all: nothing to reclaim, or no room for the
+    # demotions it receives (ENOSPC at DRAM)
+    ((0, 3000, 2000), (0, 100, 10)),
+    ((500, 0, 700), (50, 0, 0)),
 ]
 
 
