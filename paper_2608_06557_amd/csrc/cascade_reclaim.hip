@@ -615,7 +615,7 @@ __device__ __forceinline__ void demotions(const RcArgs &a, const unsigned long l
 // as one chunk of the list (start, certain count, candidate count, certain
 // demoted count in rec[tile]); the candidates' next digit is histogrammed.
 // Demotion is decided here, on the index as it was when the call began.
-__global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
+__device__ __forceinline__ void compact_table(const RcArgs &a, Part g) {
   __shared__ unsigned s_sub[kRcBins];
   __shared__ unsigned long long s_look[kRcTile];
   __shared__ int s_rank[kWaves];
@@ -623,7 +623,7 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
   __shared__ unsigned long long s_mm[kWaves * 2];
   __shared__ int s_start;
   __shared__ int s_found[2];
-  const Part g = whole_grid();
+  const bool lead = g.block == 0;  // stores the plan
   const Slots8 first = load_first(a, g);
   const int t = threadIdx.x;
   // the top digit's histogram, the status and the incoming count, requested
@@ -640,7 +640,7 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
   const RangeCalc rg = range_of(a, s_red, s_mm);
   const PlanCalc pc = plan_of(a, rg, status_was, n_in);
   RcPlan *P = a.w.plan;
-  if (blockIdx.x == 0 && t == 0) {
+  if (lead && t == 0) {
     if (pc.err < 0) store_agent(a.status, pc.err);
     P->ok = pc.err == 0;
     P->total = pc.total;
@@ -676,14 +676,14 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
     }
     __syncthreads();
     if (s_found[0] < 0) {  // the counts disagree with the plan: stop the call
-      if (blockIdx.x == 0 && t == 0) {
+      if (lead && t == 0) {
         store_agent(a.status, (int)CASCADE_EINTERNAL);
         P->ok = 0;
       }
       return;
     }
     bucket = (unsigned long long)s_found[0];
-    if (blockIdx.x == 0 && t == 0) {
+    if (lead && t == 0) {
       P->bucket = s_found[0];
       P->brank = s_found[1];
     }
@@ -764,6 +764,10 @@ __global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
       if (v) atomicAdd(a.w.sub + b, v);
     }
   }
+}
+
+__global__ __launch_bounds__(kBlock) void rc_compact_kernel(RcArgs a) {
+  compact_table(a, whole_grid());
 }
 
 // ------------------------------------------------------------ selection
@@ -895,10 +899,22 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
   const int c_reg = t < kListGroups ? (int)load_agent(a.w.count + t * kCountStride) : 0;
   const int ok = P->ok, mode = P->mode, shift0 = P->shift, bucket = P->bucket, brank = P->brank,
             prank = P->rank;
+  const int st_now = load_agent(a.status);
   if (blockIdx.x == 0) {  // the top-digit histogram is free again (the compaction read it)
     for (int i = t; i < kHistCopies * (1 << kDigit0); i += kBlock) store_agent(a.w.hist + i, 0u);
   }
-  if (!ok) return;
+  if (!ok || st_now != CASCADE_OK) {
+    // The call failed, or (in a chain call, whose compaction shares a launch
+    // with the tier above's writes) the tier above failed while this call's
+    // compaction ran: nothing is selected, the write kernel writes nothing,
+    // and what the compaction may have counted is cleared.
+    if (blockIdx.x == 0) {
+      for (int b = t; b < kRcBins; b += kBlock) store_agent(a.w.sub + b, 0u);
+      if (t < kListGroups) store_agent(a.w.count + t * kCountStride, 0u);
+      if (t == 0 && ok) P->ok = 0;
+    }
+    return;
+  }
   const int tiles = max(1, tiles_of(a.n));
   if (t < 64) {  // the regions' entry counts and their prefix
     const int c = c_reg;
@@ -1201,10 +1217,10 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
 // block leaves this tier, a demoted one joins the next) and the slot's new
 // contents.  The old block comes from the list and its stamp from its key,
 // so the table is not read again.
-__global__ __launch_bounds__(kBlock) void rc_write_kernel(RcArgs a) {
+__device__ __forceinline__ void write_tile(const RcArgs &a, int tile) {
   __shared__ int s_scan[kWaves * 2];
   const RcPlan *P = a.w.plan;
-  const int tile = blockIdx.x, t = threadIdx.x;
+  const int t = threadIdx.x;
   const int4 o = a.w.off[tile], r = a.w.rec[tile];  // requested with the plan
   const int ok = P->ok, tie_slot = P->tie_slot, total = P->total, need = a.need;
   const unsigned long long T = P->thresh, lu_min = P->lu_min;
@@ -1268,6 +1284,25 @@ __global__ __launch_bounds__(kBlock) void rc_write_kernel(RcArgs a) {
   }
   if (t == 0 && (n_sel != o.z || n_dem != o.w))
     store_agent(a.status, (int)CASCADE_EINTERNAL);  // the counts disagree
+}
+
+__global__ __launch_bounds__(kBlock) void rc_write_kernel(RcArgs a) {
+  write_tile(a, (int)blockIdx.x);
+}
+
+// In a chain call, one tier's writes and the next tier's compaction, which
+// do not depend on each other, share a launch: workgroups [0, n_write)
+// write tier w's tiles, the rest compact tier c.  The compaction needs only
+// the incoming count, which tier w's select kernel has stored, and the
+// index's bits of the tiers below c, which tier w's writes do not touch
+// (they change the bits of tiers w and w + 1 = c); it does not read the
+// incoming blocks, which tier w's writes produce.  A failure tier w's writes
+// report while the compaction runs is caught by tier c's select kernel.
+__global__ __launch_bounds__(kBlock) void rc_write_compact_kernel(RcArgs w, RcArgs c,
+                                                                  int n_write) {
+  const int b = (int)blockIdx.x;
+  if (b < n_write) write_tile(w, b);
+  else compact_table(c, Part{b - n_write, (int)gridDim.x - n_write});
 }
 
 bool index_capacity_ok(int32_t capacity) {
@@ -1420,6 +1455,20 @@ extern "C" int cascade_tier_reclaim_chain(const cascade_tier_chain_t *c, void *i
   m.check_in = 0;  // each tier's incoming blocks are the chain's own demotions
   hipStream_t s = static_cast<hipStream_t>(stream);
   launch_head(m, s);
-  for (int t = 0; t < 3; ++t) launch_tail(m.t[t], s);
+  // compact 0, select 0, [write 0 | compact 1], select 1, [write 1 | compact 2],
+  // select 2, write 2
+  hipLaunchKernelGGL(rc_compact_kernel, dim3(std::min(tiles_or_one(m.t[0]), kRcGridCompact)),
+                     dim3(kBlock), 0, s, m.t[0]);
+  for (int t = 0; t < 3; ++t) {
+    hipLaunchKernelGGL(rc_select_kernel, dim3(kSelGrid), dim3(kBlock), 0, s, m.t[t]);
+    const int n_write = tiles_or_one(m.t[t]);
+    if (t < 2) {
+      const int n_compact = std::min(tiles_or_one(m.t[t + 1]), kRcGridCompact);
+      hipLaunchKernelGGL(rc_write_compact_kernel, dim3(n_write + n_compact), dim3(kBlock), 0, s,
+                         m.t[t], m.t[t + 1], n_write);
+    } else {
+      hipLaunchKernelGGL(rc_write_kernel, dim3(n_write), dim3(kBlock), 0, s, m.t[t]);
+    }
+  }
   return hipGetLastError() == hipSuccess ? CASCADE_OK : CASCADE_EHIP;
 }

@@ -326,6 +326,30 @@ def test_chain_workspace_reused_across_calls(dev):
     assert_chain_same(w2, g2, rc, outs, masks, "second chain call")
 
 
+@pytest.mark.parametrize("one_call", [False, True], ids=["per_tier", "chain_call"])
+def test_workspace_clean_after_a_failed_chain(dev, one_call):
+    # a chain that stops at DRAM (ENOSPC) leaves its workspace as a good
+    # chain needs it: the histograms its shared passes built for the tiers it
+    # never reached are cleared too
+    bad = small(55, (3000, 400, 400), (1000, 0, 0), held=(0.1, 0.9, 0.0))
+    d = dev.DeviceTiers(bad["tables"], bad["needs"], bad["index_keys"], bad["index_masks"])
+    assert (d.run_chain() if one_call else d.run()) == 0
+    rc, _, _ = oracle_chain(bad)
+    assert rc == ref.ENOSPC and d.fetch()["status"] == ref.ENOSPC
+    good = small(56, (2500, 400, 400), (100, 20, 10))
+    d2 = dev.DeviceTiers(good["tables"], good["needs"], good["index_keys"], good["index_masks"])
+    if one_call:
+        d2.chain_args()
+        d2.ws_chain, d2.ws_chain_bytes = d.ws_chain, d.ws_chain_bytes
+    else:
+        d2.ws, d2.ws_bytes = d.ws, d.ws_bytes
+    assert (d2.run_chain() if one_call else d2.run()) == 0
+    g = d2.fetch()
+    rc, outs, masks = oracle_chain(good)
+    assert rc == 0
+    assert_chain_same(good, g, rc, outs, masks, "after a failed chain")
+
+
 def test_lookup_after_reclaim_reads_the_new_tiers(dev):
     # the prefix lookup on the updated index: a block whose every copy was
     # reclaimed is a miss; demoted blocks report their deeper tier
