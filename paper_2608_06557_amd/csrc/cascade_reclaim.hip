@@ -1291,18 +1291,19 @@ __global__ __launch_bounds__(kBlock) void rc_write_kernel(RcArgs a) {
 }
 
 // In a chain call, one tier's writes and the next tier's compaction, which
-// do not depend on each other, share a launch: workgroups [0, n_write)
-// write tier w's tiles, the rest compact tier c.  The compaction needs only
+// do not depend on each other, share a launch: workgroups [0, n_compact)
+// compact tier c (first, so the longer work starts first), the rest write
+// tier w's tiles.  The compaction needs only
 // the incoming count, which tier w's select kernel has stored, and the
 // index's bits of the tiers below c, which tier w's writes do not touch
 // (they change the bits of tiers w and w + 1 = c); it does not read the
 // incoming blocks, which tier w's writes produce.  A failure tier w's writes
 // report while the compaction runs is caught by tier c's select kernel.
 __global__ __launch_bounds__(kBlock) void rc_write_compact_kernel(RcArgs w, RcArgs c,
-                                                                  int n_write) {
+                                                                  int n_compact) {
   const int b = (int)blockIdx.x;
-  if (b < n_write) write_tile(w, b);
-  else compact_table(c, Part{b - n_write, (int)gridDim.x - n_write});
+  if (b < n_compact) compact_table(c, Part{b, n_compact});
+  else write_tile(w, b - n_compact);
 }
 
 bool index_capacity_ok(int32_t capacity) {
@@ -1465,7 +1466,7 @@ extern "C" int cascade_tier_reclaim_chain(const cascade_tier_chain_t *c, void *i
     if (t < 2) {
       const int n_compact = std::min(tiles_or_one(m.t[t + 1]), kRcGridCompact);
       hipLaunchKernelGGL(rc_write_compact_kernel, dim3(n_write + n_compact), dim3(kBlock), 0, s,
-                         m.t[t], m.t[t + 1], n_write);
+                         m.t[t], m.t[t + 1], n_compact);
     } else {
       hipLaunchKernelGGL(rc_write_kernel, dim3(n_write), dim3(kBlock), 0, s, m.t[t]);
     }
