@@ -155,6 +155,23 @@ def test_nearly_full_index(dev):
     assert outs[0]["n_outgoing"] > 0 and outs[1]["n_outgoing"] > 0
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_chains(dev, seed):
+    # seeded random chains: table sizes across tile boundaries, held and
+    # empty shares, needs (some beyond the free slots: ENOSPC at some tier),
+    # full or partial index; both call paths against the oracle
+    rng = np.random.default_rng(900 + seed)
+    sizes = tuple(int(x) for x in rng.integers(1, 9000, 3))
+    held = tuple(float(x) for x in rng.uniform(0.0, 0.6, 3))
+    empty = tuple(float(x) for x in rng.uniform(0.0, 0.3, 3))
+    needs = tuple(int(rng.integers(0, max(1, int(sz * 0.5)) + 1)) for sz in sizes)
+    w = small(900 + seed, sizes, needs, held=held, empty=empty,
+              index_frac=float(rng.choice([1.0, 0.7])))
+    print(f"random chain {seed}: sizes {sizes} needs {needs}", flush=True)
+    g, rc, outs, masks, _ = run_both(dev, w)
+    assert_chain_same(w, g, rc, outs, masks, f"random chain {seed}")
+
+
 def test_empty_slots_alone_suffice_and_ties_split(dev):
     # plenty of empty slots: the threshold is the empty key, cut mid-way in
     # slot order; DRAM then takes exactly its empties
