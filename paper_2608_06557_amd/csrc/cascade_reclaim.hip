@@ -119,7 +119,7 @@ struct alignas(256) RcPlan {
   unsigned long long thresh;  // the threshold key T
 };
 
-struct RcWork {
+struct RcWork {  // the head (zero when a call starts) through stage_ent, then the body
   RcPlan *plan;
   unsigned *tickets;      // [(kTicketGroups + 1) * kTicketStride]
   RcPartial *partial;     // [kRcGridCount]
