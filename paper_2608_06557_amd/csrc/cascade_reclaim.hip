@@ -119,7 +119,9 @@ struct alignas(256) RcPlan {
   unsigned long long thresh;  // the threshold key T
 };
 
-struct RcWork {  // the head (zero when a call starts) through stage_ent, then the body
+// The head (fixed offsets; its counters and histograms are zero when a call
+// starts) runs through stage_ent, then the body (sized by the table).
+struct RcWork {
   RcPlan *plan;
   unsigned *tickets;      // [(kTicketGroups + 1) * kTicketStride]
   RcPartial *partial;     // [kRcGridCount]
