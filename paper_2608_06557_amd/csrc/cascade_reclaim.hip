@@ -363,7 +363,8 @@ struct RcTables {
   RcArgs t[3];
   int n;
   int first[3];
-  int check_in;  // count kernel: check the incoming hashes (one call per tier)
+  int check_in;  // one call per tier: the count kernel checks the incoming hashes, and
+                 // the incoming count is final when the histogram is built
 };
 // Calls f(table, part) for the table this workgroup serves (constant
 // indices into the launch's arguments, one branch per table).
@@ -513,17 +514,26 @@ __device__ __forceinline__ PlanCalc plan_of(const RcArgs &a, const RangeCalc &r,
 
 // Every workgroup of a table derives the cached last-use range from the
 // count kernel's partials, then adds its tiles to the histogram of the
-// key's top digit (8 copies, workgroup b adds to copy b % 8).  The
-// histogram is built whether or not the call will need cached blocks (that
-// depends on the incoming count, known only when the tier above is done).
-__device__ __forceinline__ void hist_table(const RcArgs &a, Part g, unsigned *s_hist, int *s_red,
+// key's top digit (8 copies, workgroup b adds to copy b % 8).  When the
+// incoming count is already final (one call per tier) a call that will not
+// reclaim cached blocks skips it; in a chain call it is built whether or not
+// the call will need it (the incoming count is known only when the tier
+// above is done).
+__device__ __forceinline__ void hist_table(const RcArgs &a, Part g, bool plan_known,
+                                           unsigned *s_hist, int *s_red,
                                            unsigned long long *s_mm) {
   constexpr int kBins0 = 1 << kDigit0;
   static_assert(kBins0 == kBlock, "one bin per thread");
   const Slots8 first = load_first(a, g);
+  const int status_was = plan_known ? load_agent(a.status) : CASCADE_OK;
+  const int n_in = plan_known && a.n_in_dev ? load_agent(a.n_in_dev) : 0;
   const RangeCalc r = range_of(a, s_red, s_mm);
   const int t = threadIdx.x;
   if (r.bad || r.n_cached == 0) return;  // uniform: every workgroup computes r alike
+  if (plan_known) {
+    const PlanCalc pc = plan_of(a, r, status_was, n_in);
+    if (pc.err != 0 || pc.mode != kModeCached) return;  // nothing will read the histogram
+  }
   const int shift = r.shift;
   const unsigned long long lu_min = r.lu_min;
   s_hist[t] = 0u;
@@ -546,7 +556,9 @@ __global__ __launch_bounds__(kBlock) void rc_hist_kernel(RcTables m) {
   __shared__ unsigned s_hist[1 << kDigit0];
   __shared__ int s_red[kWaves * 3];
   __shared__ unsigned long long s_mm[kWaves * 2];
-  with_table(m, [&](const RcArgs &a, Part g) { hist_table(a, g, s_hist, s_red, s_mm); });
+  with_table(m, [&](const RcArgs &a, Part g) {
+    hist_table(a, g, m.check_in != 0, s_hist, s_red, s_mm);
+  });
 }
 
 // ------------------------------------------------------------ compaction
