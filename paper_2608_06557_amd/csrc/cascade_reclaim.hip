@@ -903,6 +903,7 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
   __shared__ unsigned long long s_skey[kStageLds];
   __shared__ unsigned s_sent[kStageLds];
   __shared__ int4 s_q[kTilesLds];
+  __shared__ int s_scan_w[kWaves * 2 * (kTilesLds / kBlock)];  // a scan of every chunk at once
   RcPlan *P = a.w.plan;
   const int t = threadIdx.x;
   // the compaction's histogram of the next digit (bins past 2^d2 were never
@@ -1124,9 +1125,38 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
       qa[c] = tile < tiles ? load_counts(a.w.off, tile) : make_int4(0, 0, 0, 0);
       ra[c] = tile < tiles ? a.w.rec[tile] : make_int4(0, 0, 0, 0);
     }
+    if (tiles <= kBlock) {
+      tile_chunk(t, qa[0], ra[0]);
+    } else {
+      // every chunk's keys T counted in one block scan (chunk c holds tiles
+      // c * kBlock + thread), then chunk by chunk the tile holding the take-th
+      int ys[kChunks], tot[kChunks];
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c)
-      if (c * kBlock < tiles) tile_chunk(c * kBlock + t, qa[c], ra[c]);
+      for (int c = 0; c < kChunks; ++c) {
+        const int tile = c * kBlock + t;
+        int4 q = make_int4(0, 0, 0, 0);
+        if (tile < tiles) {
+          q = qa[c];
+          q.x += ra[c].y;  // certainly reclaimed: below T
+          q.z += ra[c].w;
+          if (!cached) q.y += ra[c].z;  // empty slots only: every candidate is key 0 = T
+          s_q[tile] = q;
+        }
+        qa[c] = q;
+        ys[c] = q.y;
+      }
+      block_exclusive_scan<kChunks, int>(ys, tot, s_scan_w);
+      int base = 0;
+#pragma unroll
+      for (int c = 0; c < kChunks; ++c) {
+        const int pre = base + ys[c], y = qa[c].y;
+        if (take > pre && take <= pre + y) {
+          s_found[0] = c * kBlock + t;
+          s_found[1] = take - pre;  // keys T taken in that tile
+        }
+        base += tot[c];
+      }
+    }
   } else {
     for (int c0 = 0; c0 < tiles; c0 += kBlock) {
       const int tile = c0 + t;
@@ -1193,7 +1223,33 @@ __global__ __launch_bounds__(kBlock) void rc_select_kernel(RcArgs a) {
 
   // 5. output offsets, in tile order
   int carry_s = 0, carry_d = 0;
-  for (int c0 = 0; c0 < tiles; c0 += kBlock) {
+  if (tiles > kBlock && tiles <= kTilesLds) {  // every chunk in one block scan
+    constexpr int kChunks = kTilesLds / kBlock;
+    int v[2 * kChunks], ex[2 * kChunks], tot[2 * kChunks];
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const int tile = c * kBlock + t;
+      v[2 * c] = v[2 * c + 1] = 0;
+      if (tile < tiles) {
+        const int4 q = s_q[tile];
+        v[2 * c] = q.x + (tile < cut ? q.y : (tile == cut ? r_cut : 0));
+        v[2 * c + 1] = q.z + (tile < cut ? q.w : (tile == cut ? dem_cut : 0));
+      }
+      ex[2 * c] = v[2 * c];
+      ex[2 * c + 1] = v[2 * c + 1];
+    }
+    block_exclusive_scan<2 * kChunks, int>(ex, tot, s_scan_w);
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const int tile = c * kBlock + t;
+      if (tile < tiles)
+        a.w.off[tile] = make_int4(carry_s + ex[2 * c], carry_d + ex[2 * c + 1], v[2 * c],
+                                  v[2 * c + 1]);
+      carry_s += tot[2 * c];
+      carry_d += tot[2 * c + 1];
+    }
+  }
+  for (int c0 = 0; (tiles <= kBlock || tiles > kTilesLds) && c0 < tiles; c0 += kBlock) {
     const int tile = c0 + t;
     int v[2] = {0, 0};
     if (tile < tiles) {

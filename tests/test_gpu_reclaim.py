@@ -226,6 +226,15 @@ def test_more_tiles_than_the_select_kernel_keeps_in_lds(dev):
     assert_chain_same(w, g, rc, outs, masks, "2100 tiles")
 
 
+def test_hundreds_of_tiles_scanned_at_once(dev):
+    # 489 tiles, a ragged last one: the select kernel's last workgroup scans
+    # all chunks of 256 tiles in one block scan
+    w = small(75, (3000, 4000, 1_000_001), (600, 300, 3000), empty=(0.05, 0.05, 0.0))
+    g, rc, outs, masks, _ = run_both(dev, w)
+    assert rc == 0
+    assert_chain_same(w, g, rc, outs, masks, "489 tiles")
+
+
 def test_every_free_slot_reclaimed(dev):
     w = small(21, (3000, 5000, 5000), (0, 0, 0))
     free0 = int((w["tables"][0]["held"] == 0).sum())
