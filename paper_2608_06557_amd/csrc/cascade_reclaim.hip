@@ -704,7 +704,11 @@ __device__ __forceinline__ void compact_table(const RcArgs &a, Part g) {
   }
   const int d2 = cached ? min(shift, kDigitN) : 0, s2 = shift - d2;
   const unsigned m2 = (1u << d2) - 1u;
-  if (d2 > 0)
+  // One tile per workgroup: its few candidates add to the global histogram
+  // as they are listed, so nothing is left to flush when the kernel ends;
+  // several tiles per workgroup (the deepest tier) count in LDS first.
+  const bool sub_direct = max(1, tiles_of(a.n)) <= g.count;  // uniform
+  if (d2 > 0 && !sub_direct)
     for (int b = t; b < (1 << d2); b += kBlock) s_sub[b] = 0u;
   __syncthreads();
   for_tiles(a, g, first, [&](int tile, const Slots8 &v) {
@@ -768,10 +772,14 @@ __device__ __forceinline__ void compact_table(const RcArgs &a, Part g) {
                    (dem[j] ? kEntDem : 0u);
       a.w.pos[i] = ip[j];
       a.w.hash[i] = v.h[j];
-      if (d2 > 0 && !sure[j]) atomicAdd(&s_sub[(unsigned)(k[j] >> s2) & m2], 1u);
+      if (d2 > 0 && !sure[j]) {
+        const unsigned b = (unsigned)(k[j] >> s2) & m2;
+        if (sub_direct) atomicAdd(a.w.sub + b, 1u);
+        else atomicAdd(&s_sub[b], 1u);
+      }
     }
   });
-  if (d2 > 0) {
+  if (d2 > 0 && !sub_direct) {
     __syncthreads();
     for (int b = t; b < (1 << d2); b += kBlock) {
       const unsigned v = s_sub[b];
