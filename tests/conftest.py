@@ -19,7 +19,8 @@ def pytest_runtest_setup(item):
 
 def pytest_runtest_makereport(item, call):
     """A failing parity test leaves its step input behind as an .npz (under
-    $CASCADE_FAILED_STEPS, default gpurun_out/failed_steps) for replay."""
+    $CASCADE_FAILED_STEPS, default failed_steps/ at the repository root) for
+    replay."""
     if call.when != "call" or call.excinfo is None:
         return
     last = getattr(getattr(item, "module", None), "LAST_WORKLOAD", None)
@@ -27,7 +28,7 @@ def pytest_runtest_makereport(item, call):
         return
     import re
     import paper_2608_06557_amd.synth as synth
-    out = os.environ.get("CASCADE_FAILED_STEPS", os.path.join(ROOT, "gpurun_out", "failed_steps"))
+    out = os.environ.get("CASCADE_FAILED_STEPS", os.path.join(ROOT, "failed_steps"))
     try:
         os.makedirs(out, exist_ok=True)
         path = os.path.join(out, re.sub(r"[^\w.-]+", "_", item.nodeid) + ".npz")
