@@ -13,9 +13,9 @@
 // tiers holding the block) in device memory (index_table.h); key 0 marks an
 // empty slot.  Insert claims a slot with a 64-bit CAS and adds the tier to the
 // set with atomicOr; the block's deepest tier is the highest tier in its set.
-// The probe gives each request one wave: 64 leading blocks are looked up at
-// once, a ballot finds the first miss (a block absent, or whose set is empty),
-// and the wave stops there, so blocks past a miss cost nothing.
+// The probe gives each request one wave, which looks up its leading blocks
+// in windows that grow while every block hits; a ballot finds the first miss
+// (a block absent, or whose set is empty), and the wave stops there.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -57,6 +57,119 @@ __global__ __launch_bounds__(kBlock) void index_insert_kernel(IndexSlot *slots, 
   if (status) store_agent(status, (int)CASCADE_ENOSPC);  // every slot holds another key
 }
 
+// Lookups per lane in a probe window, at most: the window doubles from 64
+// blocks (one per lane) up to 64 * kProbeMaxK.
+constexpr int kProbeMaxK = 4;
+// Whether a lookup also requests the slot after its home slot when both lie
+// in one 128-byte line (8 slots): that read costs no extra line and decides
+// most keys that sit one past their home.
+constexpr bool kProbePair = true;
+
+// Examines slot v for key h when go: returns true when that decides the
+// lookup (key found, or an empty slot ends the probe sequence), and then sets
+// hit (the key is there and its tier set is not empty) and t (its deepest
+// tier).  Branch-free, so that the compiler keeps each slot a single load.
+__device__ __forceinline__ bool examine_slot(const uint4 &v, unsigned long long h, bool go,
+                                             bool &hit, unsigned &t) {
+  const unsigned long long k = (unsigned long long)v.x | ((unsigned long long)v.y << 32);
+  const bool match = go && k == h;
+  hit = match ? v.z != 0u : hit;
+  t = (match && v.z != 0u) ? 31u - (unsigned)__builtin_clz(v.z | 1u) : t;
+  return go && (k == h || k == 0ull);
+}
+
+// One window of a request's lookup: 64 * K leading blocks from `base`, K per
+// lane (lane l, item u: block base + 64 u + l), whose hashes h[0..K) the
+// previous window requested.  Every home slot is requested at once (and, with
+// kProbePair, the slot after it when both lie in one line), then the next
+// window's hashes, before any slot is examined; the keys past what was read
+// continue slot by slot, all together.  Every load is issued and none under a
+// branch, so that they are all in flight together: the unwanted ones read the
+// anchor, the slot that lane 0 looks up first (one line per wave, requested
+// anyway), and are ignored.  A ballot per item finds the window's first miss
+// (a block absent, or whose set is empty).  Returns true once the run has
+// ended, with matched its length; otherwise h holds the next window's hashes.
+template <int K, int KM>
+__device__ __forceinline__ bool probe_window(const uint4 *__restrict__ sl, unsigned mask,
+                                             const unsigned long long *__restrict__ hb, int lim,
+                                             int base, int lane, unsigned long long (&h)[KM],
+                                             int &matched, unsigned &deepest, bool &bad) {
+  constexpr int KN = K < KM ? 2 * K : KM;  // items per lane of the next window
+  const int win = 64 * K, nbase = base + win;
+  unsigned long long hc[K];
+  bool want[K], look[K], pair[K], hit[K];
+  unsigned s[K], t[K];
+  uint4 v[K], w[K];
+#pragma unroll
+  for (int u = 0; u < K; ++u) {
+    hc[u] = h[u];
+    want[u] = base + u * 64 + lane < lim;
+    look[u] = want[u] && hc[u] != 0ull;
+    bad = bad || (want[u] && !look[u]);  // hash 0 is reserved for empty slots: a miss
+    s[u] = (unsigned)fmix64(hc[u]) & mask;
+  }
+  const unsigned anchor = (unsigned)__builtin_amdgcn_readfirstlane((int)s[0]);
+#pragma unroll
+  for (int u = 0; u < K; ++u) {
+    v[u] = sl[look[u] ? s[u] : anchor];
+    pair[u] = kProbePair && look[u] && (s[u] & 7u) != 7u;  // s + 1 <= mask then
+    if (kProbePair) w[u] = sl[pair[u] ? s[u] + 1u : anchor];
+  }
+#pragma unroll
+  for (int u = 0; u < KN; ++u) {
+    const int j = nbase + u * 64 + lane;
+    h[u] = j < lim ? hb[j] : 0ull;
+  }
+  unsigned pend = 0u;
+#pragma unroll
+  for (int u = 0; u < K; ++u) {
+    hit[u] = false;
+    t[u] = 0u;
+    const bool d1 = examine_slot(v[u], hc[u], look[u], hit[u], t[u]);
+    const bool go2 = pair[u] && !d1;
+    const bool d2 = kProbePair && examine_slot(w[u], hc[u], go2, hit[u], t[u]);
+    s[u] = go2 ? s[u] + 1u : s[u];
+    pend |= (look[u] && !d1 && !d2) ? 1u << u : 0u;
+  }
+  for (unsigned p = 1; p <= mask && __ballot(pend != 0u) != 0; ++p) {  // mask + 1 slots
+#pragma unroll
+    for (int u = 0; u < K; ++u) {
+      const bool go = (pend >> u) & 1u;
+      s[u] = go ? (s[u] + 1u) & mask : s[u];
+      v[u] = sl[go ? s[u] : anchor];
+    }
+    unsigned left = pend;
+#pragma unroll
+    for (int u = 0; u < K; ++u)
+      left &= examine_slot(v[u], hc[u], (pend >> u) & 1u, hit[u], t[u]) ? ~(1u << u) : ~0u;
+    pend = left;
+  }
+  // a lookup still pending has visited every slot: the key is absent
+  int first = win;  // window position of the first miss
+#pragma unroll
+  for (int u = 0; u < K; ++u) {
+    const uint64_t miss = __ballot(want[u] && !hit[u]);
+    if (first == win && miss) first = u * 64 + __builtin_ctzll(miss);
+  }
+  unsigned tm = 0u;
+#pragma unroll
+  for (int u = 0; u < K; ++u)
+    tm = (want[u] && hit[u] && u * 64 + lane < first && t[u] > tm) ? t[u] : tm;
+  deepest = max(deepest, (unsigned)wave_max((unsigned long long)tm));
+  if (first < win) {
+    matched = base + first;
+    return true;
+  }
+  matched = nbase < lim ? nbase : lim;
+  return nbase >= lim;
+}
+
+// One wave per request.  Its leading blocks are looked up in windows of
+// 64 * k blocks, k doubling from 1 to kProbeMaxK while every block hits, so a
+// run of R cached blocks takes about log2 + R / (64 * kProbeMaxK) dependent
+// rounds instead of R / 64, while a short run (most of them) costs one small
+// window.  The wave stops at the first miss: blocks past it in later windows
+// cost nothing.
 __global__ __launch_bounds__(kBlock) void probe_kernel(const IndexSlot *__restrict__ slots,
                                                        unsigned mask, int n,
                                                        const int *__restrict__ offsets,
@@ -65,9 +178,12 @@ __global__ __launch_bounds__(kBlock) void probe_kernel(const IndexSlot *__restri
                                                        int *__restrict__ n_prefix_out,
                                                        uint8_t *__restrict__ tier_out,
                                                        int *status) {
+  constexpr int KM = kProbeMaxK;
+  static_assert(KM == 1 || KM == 2 || KM == 4 || KM == 8, "window sizes");
   const int i = blockIdx.x * kWaves + wave_id();
   if (i >= n) return;  // uniform over the wave
   const int lane = lane_id();
+  const uint4 *sl = reinterpret_cast<const uint4 *>(slots);
   // every read stays in [0, offsets[n]), the caller's hash array, even when
   // another request's offsets are out of order
   const int b0 = offsets[i], b1 = offsets[i + 1], total = offsets[n], nin = n_in[i];
@@ -75,36 +191,27 @@ __global__ __launch_bounds__(kBlock) void probe_kernel(const IndexSlot *__restri
   const int have = bad ? 0 : b1 - b0;
   const int cap = bad ? 0 : (nin - 1) / bt;
   const int lim = have < cap ? have : cap;
+  const unsigned long long *hb = hashes + (bad ? 0 : b0);
   int matched = 0;
   unsigned deepest = 0;
-  for (int base = 0; base < lim; base += 64) {
-    const int j = base + lane;
-    const bool active = j < lim;
-    bool hit = false;
-    unsigned t = 0;
-    if (active) {
-      const unsigned long long h = hashes[b0 + j];
-      if (h == 0) {
-        bad = true;  // reserved for empty slots: never cached
-      } else {
-        unsigned s = (unsigned)fmix64(h) & mask;
-        for (unsigned p = 0; p <= mask; ++p, s = (s + 1) & mask) {
-          const IndexSlot e = slots[s];
-          if (e.key == h) {
-            hit = e.tiers != 0u;
-            t = hit ? 31u - (unsigned)__builtin_clz(e.tiers) : 0u;
-            break;
-          }
-          if (e.key == 0ull) break;
-        }
-      }
-    }
-    const uint64_t miss = __ballot(active && !hit);
-    const int first = miss ? __builtin_ctzll(miss) : 64;
-    const unsigned run_t = (active && lane < first) ? t : 0u;
-    deepest = max(deepest, (unsigned)wave_max((unsigned long long)run_t));
-    matched = miss ? base + first : min(base + 64, lim);
-    if (miss) break;
+  unsigned long long h[KM];
+#pragma unroll
+  for (int u = 0; u < KM; ++u) h[u] = (u == 0 && lane < lim) ? hb[lane] : 0ull;
+  int base = 0, k = 1;
+  bool done = lim <= 0;
+  while (!done) {  // uniform over the wave
+    if (k == 1)
+      done = probe_window<1, KM>(sl, mask, hb, lim, base, lane, h, matched, deepest, bad);
+    else if (k == 2)
+      done = probe_window<(KM < 2 ? KM : 2), KM>(sl, mask, hb, lim, base, lane, h, matched,
+                                                  deepest, bad);
+    else if (k == 4)
+      done = probe_window<(KM < 4 ? KM : 4), KM>(sl, mask, hb, lim, base, lane, h, matched,
+                                                  deepest, bad);
+    else
+      done = probe_window<KM, KM>(sl, mask, hb, lim, base, lane, h, matched, deepest, bad);
+    base += 64 * k;
+    k = k < KM ? 2 * k : KM;
   }
   if (__ballot(bad) && lane == 0 && status) store_agent(status, (int)CASCADE_EINVAL);
   if (lane == 0) {

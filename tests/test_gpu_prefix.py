@@ -133,3 +133,51 @@ def test_empty(dev):
     assert_same(g, o, "empty index")
     g, o, _ = run_both(dev, _pw([(5, 1)], []))
     assert g["status"] == 0
+
+
+def test_runs_ending_at_window_edges(dev):
+    # A wave looks up 64, 128, 256, 256, ... blocks per window, so windows
+    # start at blocks 0, 64, 192, 448, 704, 960, ...  Request j owns a
+    # sequence whose first miss is at block m_j; the blocks past the miss are
+    # cached in the deepest tier, and only the last block before the miss
+    # reaches tier 1, so a window that let a block past the miss into the run
+    # or its tier would show.
+    edges = [0, 1, 2, 63, 64, 65, 127, 191, 192, 193, 447, 448, 449, 703, 704, 705, 959,
+             960, 1215, 1216]
+    entries, reqs = [], []
+    for j, m in enumerate(edges):
+        seq = [(j + 1) * 10_000 + b for b in range(1400)]
+        entries += [(h, 0) for h in seq[:max(m - 1, 0)]]
+        if m >= 1:
+            entries.append((seq[m - 1], 1))
+        entries += [(h, 2) for h in seq[m + 1:]]
+        reqs.append((16 * 1400 + 5, seq))
+    # runs capped by the prompt length at a window edge, with every block cached
+    for j, lim in enumerate([64, 192, 448, 704]):
+        seq = [900_000 + j * 10_000 + b for b in range(lim + 40)]
+        entries += [(h, 1) for h in seq]
+        reqs.append((16 * lim + 1, seq))
+    g, o, _ = run_both(dev, _pw(entries, reqs))
+    assert_same(g, o, "window edges")
+    assert list(g["n_prefix"][:len(edges)] // 16) == edges
+    assert list(g["n_prefix"][len(edges):] // 16) == [64, 192, 448, 704]
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_crowded_table(dev, seed):
+    # 3700 keys in 4096 slots: long probe sequences, sequences that wrap past
+    # the table's last slot, and keys one past a home slot at the end of a line
+    rng = np.random.default_rng(seed)
+    keys = np.unique(rng.integers(1, 1 << 40, 4000, dtype=np.uint64))[:3700]
+    assert len(keys) == 3700
+    tiers = rng.integers(0, 3, len(keys))
+    entries = [(int(k), int(t)) for k, t in zip(keys, tiers)]
+    absent = rng.integers(1 << 40, 1 << 41, 300, dtype=np.uint64)  # never a key
+    reqs = []
+    for _ in range(400):
+        run = int(rng.integers(0, 600))
+        seq = [int(k) for k in rng.choice(keys, run)] + [int(absent[rng.integers(0, 300)])]
+        seq += [int(k) for k in rng.choice(keys, int(rng.integers(0, 50)))]
+        reqs.append((16 * len(seq) + 1, seq))
+    g, o, _ = run_both(dev, _pw(entries, reqs), capacity=4096)
+    assert_same(g, o, f"crowded {seed}")
