@@ -219,10 +219,14 @@ __global__ __launch_bounds__(kBlock) void kvcopy_kernel(cascade_kv_pool_t pool, 
   if (nm <= 0) return;
   const long long total = (long long)nm * un.per_move;
   const int vecs = (int)(pool.chunk_bytes >> 4);
+  // each item's move is requested one item ahead, as in kvmove_kernel
+  cascade_move_t n_mv = {0, 0, 0, 0};
+  if ((long long)blockIdx.x < total) n_mv = moves[(int)(blockIdx.x / un.per_move)];
   for (long long c = blockIdx.x; c < total; c += gridDim.x) {
     const int m = (int)(c / un.per_move);
     const int r0 = (int)(c - (long long)m * un.per_move) * un.g;
-    const cascade_move_t mv = moves[m];
+    const cascade_move_t mv = n_mv;
+    if (c + gridDim.x < total) n_mv = moves[(int)((c + gridDim.x) / un.per_move)];
     if (!move_ok(mv, pool.num_slots, staging_slots)) {
       flag_bad(status);
       continue;
