@@ -181,3 +181,31 @@ def test_crowded_table(dev, seed):
         reqs.append((16 * len(seq) + 1, seq))
     g, o, _ = run_both(dev, _pw(entries, reqs), capacity=4096)
     assert_same(g, o, f"crowded {seed}")
+
+
+def test_null_status_and_a_single_long_request(dev):
+    # status_dev may be NULL: the lookup then reports nothing, also on a zero
+    # hash, and still writes every request's result.  One request in a
+    # workgroup of four waves, its run of 700 blocks over five windows.
+    import paper_2608_06557_amd.cascade as cx
+    from paper_2608_06557_amd.device import stream_handle
+    seq = [50_000 + b for b in range(900)]
+    entries = [(h, 1) for h in seq[:700]]
+    for reqs, want in [([(16 * 900 + 1, seq)], 700), ([(16 * 4 + 1, [7, 0, 8, 9])], None)]:
+        pw = _pw(entries + [(7, 2)], reqs)
+        d = dev.DevicePrefix(pw)
+        assert d.build() == 0
+        d.n_prefix.fill_(-1)
+        assert cx.cascade_prefix_probe(d.index.data_ptr(), d.capacity, d.n, d.off.data_ptr(),
+                                       d.bh.data_ptr(), d.n_in.data_ptr(), d.bt,
+                                       d.n_prefix.data_ptr(), d.tier.data_ptr(), None,
+                                       stream_handle(None)) == 0
+        g = d.fetch()
+        o = ref.prefix_probe(pw["index_hashes"], pw["index_tiers"], pw["block_offsets"],
+                             pw["block_hashes"], pw["n_in"], pw["block_tokens"])
+        assert g["status"] == 0  # the status word was left alone
+        if want is None:  # invalid input (hash 0): the result is written, its value unspecified
+            assert o["rc"] == ref.EINVAL and int(g["n_prefix"][0]) >= 0
+        else:
+            assert_same(g, o, "null status")
+            assert int(g["n_prefix"][0]) == 16 * want
